@@ -1,0 +1,21 @@
+"""Plain float64 CPU oracle of the factorized-cache decode path.
+
+TEST INFRASTRUCTURE.  It exists to check the GPU library and is never part of
+it: only the tests, ``__graft_entry__.smoke()`` and the benchmark's CPU-baseline
+leg may import it.  It shares no code with the library (no kernels, headers,
+helpers or table generators); both sides only read the same seeded synthetic
+inputs.
+
+* ``factorized``: Eq. 1 reconstruction, softmax decode attention, Eq. 3 probe
+  error and the dense residual map.
+* ``router``: Eq. 2 rank routing (multi-level reading) and residual offsets.
+
+Every function is pinned by the CPU tests (brute force in exact arithmetic,
+closed forms, reductions to library attention, invariants); none is marked
+"parity unpinned".
+"""
+from . import factorized, router
+from .factorized import (attention, decode, probe, probe_error, reconstruct,
+                         residual_map, int4_from_nibble, entry_codes, q_to_f64,
+                         default_scale)
+from .router import route, router_score, level_index, theta_from_tau

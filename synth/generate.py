@@ -1,0 +1,289 @@
+"""Seeded synthetic factorized KV caches in the library's storage layout.
+
+Every random draw comes from a PCG64DXSM stream keyed by
+(workload seed, tensor id, indices), so any slab (one sequence, layer,
+K-or-V, head) regenerates on its own and equals the same slab of a full
+generation.  The draws follow the workload's stated distributions:
+
+* shared bases: r_b x d N(0,1) rows, orthonormalised in float64, rounded to fp16;
+* per-token basis coefficients: N(0,1) rounded to fp16;
+* routed residual rank: categorical over the level table (salient spans, when
+  the workload has them, force one level for every window and head);
+* residual entries: the routed number of distinct channels drawn uniformly,
+  int4 codes uniform on [-7, 7], stored largest |code| first, then by channel;
+* per-token residual scale (gate folded in, gate = 1): U(0.01, 0.1) in fp16;
+* queries: N(0,1)/sqrt(d) rounded to the workload's query dtype.
+
+Packing variable-length residual entries needs the running position of each
+token's first entry; that is storage layout, computed here with a cumulative
+sum of the drawn ranks.  Nothing in this module evaluates the method itself
+(reconstruction, routing scores, attention or probe error).
+"""
+from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass
+
+import numpy as np
+
+from .workloads import Workload
+
+# tensor ids used to key the random streams
+_BASIS, _COEF, _RANK, _RES_CH, _RES_CODE, _RES_SCALE, _Q, _SPANS = 1, 2, 3, 4, 5, 6, 7, 8
+_PHI, _ROUTER_U, _PROBE = 10, 11, 12
+
+RES_TAIL_PAD = 512      # spare entries after the longest slab
+RES_ALIGN = 256         # res_stride is a multiple of this
+
+
+def rng_for(*key) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64DXSM(np.random.SeedSequence(list(key))))
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 to bfloat16 (nearest, ties to even); returns uint16 bits."""
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    rounded = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    return rounded.astype(np.uint16)
+
+
+def f16_bits(x: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(x, dtype=np.float64).astype(np.float16).view(np.uint16)
+
+
+@dataclass
+class CompressedCache:
+    """Host copy of one factorized cache, laid out as the C ABI expects.
+
+    Shapes (M windows, L layers held, T packed tokens over all sequences):
+      basis     fp16  [B][M][Hkv][2][r_b][d]   Z=0 keys, Z=1 values
+      coef      fp16  [L][2][Hkv][T][r_b]
+      rank_code uint8 [M][Hkv][T]
+      res_off   uint32[M][Hkv][T+1]
+      res_idx   uint8 [L][2][Hkv][res_stride]
+      res_val   uint8 [L][2][Hkv][res_stride/2]  two int4 codes per byte, low nibble first
+      res_scale fp16  [L][2][Hkv][T]
+      q_bits    uint16[L][B][Hq][d]              fp16 or bf16 bit patterns
+    """
+    workload: Workload
+    layer0: int                 # absolute index of the first layer held
+    n_layers: int               # layers held (a whole number of windows)
+    seqlens: list
+    cu_seqlens: np.ndarray      # int32 [B+1]
+    levels: tuple
+    res_stride: int
+    basis: np.ndarray
+    coef: np.ndarray
+    rank_code: np.ndarray
+    res_off: np.ndarray
+    res_idx: np.ndarray
+    res_val: np.ndarray
+    res_scale: np.ndarray
+    q_bits: np.ndarray
+    q_dtype: str
+
+    @property
+    def batch(self): return len(self.seqlens)
+    @property
+    def window(self): return self.workload.window
+    @property
+    def n_kv_heads(self): return self.workload.n_kv_heads
+    @property
+    def n_q_heads(self): return self.workload.n_q_heads
+    @property
+    def head_dim(self): return self.workload.head_dim
+    @property
+    def basis_rank(self): return self.workload.basis_rank
+    @property
+    def total_tokens(self): return int(self.cu_seqlens[-1])
+    @property
+    def n_windows(self): return self.n_layers // self.window
+
+    def nbytes_layer(self) -> int:
+        """Compressed bytes one per-layer decode reads (bases, coefficients,
+        offsets, residual scales/indices/values) plus q in and fp32 out."""
+        Hk, T, rb, d = self.n_kv_heads, self.total_tokens, self.basis_rank, self.head_dim
+        B, Hq = self.batch, self.n_q_heads
+        basis = B * Hk * 2 * rb * d * 2
+        coef = 2 * Hk * T * rb * 2
+        off = Hk * (T + 1) * 4
+        ent = 0
+        for h in range(Hk):      # average over windows of the entries per slab
+            ent += sum(int(self.res_off[m, h, -1]) for m in range(self.n_windows)) / self.n_windows
+        resid = 2 * (ent * 1 + ent / 2) + 2 * Hk * T * 2
+        qo = B * Hq * d * (2 + 4)
+        return int(basis + coef + off + resid + qo)
+
+
+def _window_codes(w: Workload, b: int, m: int, h: int, T: int) -> np.ndarray:
+    rng = rng_for(w.seed, _RANK, b, m, h)
+    codes = rng.choice(len(w.levels), size=T, p=np.asarray(w.probs, dtype=np.float64))
+    codes = codes.astype(np.uint8)
+    if w.salient_frac > 0:
+        span = w.salient_span
+        n_slots = T // span
+        n_spans = min(n_slots, int(round(w.salient_frac * T / span)))
+        srng = rng_for(w.seed, _SPANS, b)          # shared by every (window, head)
+        slots = srng.choice(n_slots, size=n_spans, replace=False)
+        for s in slots:
+            codes[s * span:(s + 1) * span] = w.salient_level
+    return codes
+
+
+def _orthonormal_rows(rng: np.random.Generator, r: int, d: int) -> np.ndarray:
+    x = rng.standard_normal((r, d))
+    q, rr = np.linalg.qr(x.T)                    # columns of q: orthonormal
+    q = q * np.sign(np.diag(rr))[None, :]        # fixed sign convention
+    return q.T                                   # r x d, orthonormal rows
+
+
+def _slab_entries(w: Workload, b: int, l: int, z: int, h: int, ranks: np.ndarray):
+    """Residual channels and codes for one (sequence, layer, Z, head) slab,
+    in token order, each token's entries largest |code| first then by channel."""
+    d = w.head_dim
+    T = ranks.shape[0]
+    n_e = int(ranks.sum())
+    chans = np.empty(n_e, dtype=np.uint8)
+    codes = np.empty(n_e, dtype=np.int8)
+    starts = np.zeros(T, dtype=np.int64)
+    np.cumsum(ranks[:-1], out=starts[1:])
+    rng_c = rng_for(w.seed, _RES_CH, b, l, z, h)
+    rng_k = rng_for(w.seed, _RES_CODE, b, l, z, h)
+    for r in sorted(set(int(x) for x in np.unique(ranks)) - {0}):
+        toks = np.nonzero(ranks == r)[0]
+        keys = rng_c.random((toks.size, d))
+        ch = np.argpartition(keys, r - 1, axis=1)[:, :r] if r < d else np.argsort(keys, axis=1)
+        k = rng_k.integers(-7, 8, size=(toks.size, r))
+        order = np.argsort((7 - np.abs(k)) * 256 + ch, axis=1, kind="stable")
+        ch = np.take_along_axis(ch, order, axis=1)
+        k = np.take_along_axis(k, order, axis=1)
+        pos = starts[toks][:, None] + np.arange(r)[None, :]
+        chans[pos] = ch
+        codes[pos] = k
+    return chans, codes
+
+
+def _pack_nibbles(codes: np.ndarray) -> np.ndarray:
+    n = codes.size
+    u = (codes.astype(np.int16) & 0xF).astype(np.uint8)
+    if n % 2:
+        u = np.concatenate([u, np.zeros(1, np.uint8)])
+    return (u[0::2] | (u[1::2] << 4)).astype(np.uint8)
+
+
+def generate(w: Workload, layers: tuple | None = None, threads: int | None = None,
+             with_q: bool = True) -> CompressedCache:
+    """Build the cache of workload ``w``.
+
+    ``layers`` = (start, stop) restricts the cache to whole depth windows
+    [start, stop); every draw keeps its absolute layer/window key, so the slice
+    equals the same layers of a full generation.
+    """
+    L0, L1 = (0, w.n_layers) if layers is None else layers
+    assert L0 % w.window == 0 and L1 % w.window == 0 and 0 <= L0 < L1 <= w.n_layers
+    nL, nM = L1 - L0, (L1 - L0) // w.window
+    m0 = L0 // w.window
+    B, Hk, Hq, d, rb = w.batch, w.n_kv_heads, w.n_q_heads, w.head_dim, w.basis_rank
+    seqlens = w.seqlens()
+    cu = np.zeros(B + 1, dtype=np.int32)
+    cu[1:] = np.cumsum(seqlens)
+    T = int(cu[-1])
+    levels = np.asarray(w.levels, dtype=np.int64)
+    threads = threads or min(16, os.cpu_count() or 1)
+    pool = ThreadPoolExecutor(threads)
+
+    # routed ranks, shared by the layers of a window and by K and V
+    rank_code = np.empty((nM, Hk, T), dtype=np.uint8)
+    def _codes(job):
+        m, h = job
+        for b in range(B):
+            rank_code[m, h, cu[b]:cu[b + 1]] = _window_codes(w, b, m0 + m, h, seqlens[b])
+    list(pool.map(_codes, [(m, h) for m in range(nM) for h in range(Hk)]))
+    res_off = np.zeros((nM, Hk, T + 1), dtype=np.uint32)
+    totals = np.zeros((nM, Hk), dtype=np.int64)
+    for m in range(nM):
+        for h in range(Hk):
+            c = np.cumsum(levels[rank_code[m, h]])
+            totals[m, h] = c[-1] if T else 0
+            assert totals[m, h] < 2**32
+            res_off[m, h, 1:] = c
+    res_stride = int(-(-(int(totals.max()) + RES_TAIL_PAD) // RES_ALIGN) * RES_ALIGN)
+
+    basis = np.empty((B, nM, Hk, 2, rb, d), dtype=np.float16)
+    def _basis(job):
+        b, m, h, z = job
+        basis[b, m, h, z] = _orthonormal_rows(rng_for(w.seed, _BASIS, b, m0 + m, h, z), rb, d).astype(np.float16)
+    list(pool.map(_basis, [(b, m, h, z) for b in range(B) for m in range(nM)
+                           for h in range(Hk) for z in range(2)]))
+
+    coef = np.empty((nL, 2, Hk, T, rb), dtype=np.float16)
+    res_scale = np.empty((nL, 2, Hk, T), dtype=np.float16)
+    res_idx = np.zeros((nL, 2, Hk, res_stride), dtype=np.uint8)
+    res_val = np.zeros((nL, 2, Hk, res_stride // 2), dtype=np.uint8)
+
+    def _slab(job):
+        li, z, h = job
+        l = L0 + li
+        m = li // w.window
+        for b in range(B):
+            t0, t1 = int(cu[b]), int(cu[b + 1])
+            n = t1 - t0
+            if n == 0:
+                continue
+            g = rng_for(w.seed, _COEF, b, l, z, h)
+            coef[li, z, h, t0:t1] = g.standard_normal((n, rb), dtype=np.float32).astype(np.float16)
+            s = rng_for(w.seed, _RES_SCALE, b, l, z, h).uniform(0.01, 0.1, size=n)
+            res_scale[li, z, h, t0:t1] = s.astype(np.float16)
+        # entries of every sequence, packed in token order
+        all_ch, all_k = [], []
+        for b in range(B):
+            t0, t1 = int(cu[b]), int(cu[b + 1])
+            ranks = levels[rank_code[m, h, t0:t1]]
+            ch, k = _slab_entries(w, b, l, z, h, ranks)
+            all_ch.append(ch)
+            all_k.append(k)
+        ch = np.concatenate(all_ch) if all_ch else np.zeros(0, np.uint8)
+        k = np.concatenate(all_k) if all_k else np.zeros(0, np.int8)
+        assert ch.size == totals[m, h]
+        res_idx[li, z, h, :ch.size] = ch
+        packed = _pack_nibbles(k)
+        res_val[li, z, h, :packed.size] = packed
+    list(pool.map(_slab, [(li, z, h) for li in range(nL) for z in range(2) for h in range(Hk)]))
+
+    q_bits = np.empty((nL, B, Hq, d), dtype=np.uint16)
+    if with_q:
+        for li in range(nL):
+            x = rng_for(w.seed, _Q, L0 + li).standard_normal((B, Hq, d)) / np.sqrt(d)
+            q_bits[li] = f16_bits(x) if w.q_dtype == "f16" else f32_to_bf16_bits(x.astype(np.float32))
+    pool.shutdown()
+    return CompressedCache(
+        workload=w, layer0=L0, n_layers=nL, seqlens=list(seqlens), cu_seqlens=cu,
+        levels=tuple(int(x) for x in w.levels), res_stride=res_stride, basis=basis,
+        coef=coef, rank_code=rank_code, res_off=res_off, res_idx=res_idx,
+        res_val=res_val, res_scale=res_scale, q_bits=q_bits, q_dtype=w.q_dtype)
+
+
+def router_inputs(w: Workload, n_windows: int, T: int, window0: int = 0):
+    """Router features phi [M][Hkv][T][4] (float32), router weights u [M][4] and
+    ascending thresholds theta [M][n_levels-1] (float32), seeded.
+
+    Features: attention mass and spike (non-negative, heavy tailed), a 0/1
+    delimiter flag and the previous probe error; thresholds are spread so every
+    level is reached."""
+    Hk = w.n_kv_heads
+    n_lev = len(w.levels)
+    phi = np.empty((n_windows, Hk, T, 4), dtype=np.float32)
+    u = np.empty((n_windows, 4), dtype=np.float32)
+    theta = np.empty((n_windows, max(n_lev - 1, 0)), dtype=np.float32)
+    for m in range(n_windows):
+        g = rng_for(w.seed, _ROUTER_U, window0 + m)
+        u[m] = g.uniform(0.25, 1.5, size=4).astype(np.float32)
+        theta[m] = np.sort(g.uniform(0.5, 4.0, size=n_lev - 1)).astype(np.float32)
+        for h in range(Hk):
+            r = rng_for(w.seed, _PHI, window0 + m, h)
+            phi[m, h, :, 0] = r.exponential(1.0, size=T)
+            phi[m, h, :, 1] = r.exponential(0.5, size=T)
+            phi[m, h, :, 2] = (r.random(T) < 0.05)
+            phi[m, h, :, 3] = r.uniform(0.0, 0.2, size=T)
+    return phi, u, theta

@@ -1,0 +1,594 @@
+"""Pins of the float64 oracle against facts that do not come from the oracle.
+
+Each ``pin_*`` function takes the oracle package (so the mutation test can hand
+it a copy with a planted mistake) and returns None on success or a string that
+says what disagreed.  The pins are:
+
+* brute force in 40-digit decimal arithmetic with scalar loops on tiny caches;
+* closed forms on hand-built caches (one-hot coefficients over permutation
+  bases, residual-only caches, a single token, a zero query);
+* reductions to library attention (torch CPU float64 scaled_dot_product_attention):
+  rank-0 residuals, an identity basis, and a full-rank residual with no basis term;
+* invariants: probabilities sum to one, token-permutation invariance, sequence
+  independence, the query-head to KV-head grouping;
+* Eq. 3 closed forms (e = 0 for an exact reference, e = |1-c|/(|c| + eps/||O||)
+  for a value reference scaled by c);
+* the router score in exact rational arithmetic rounded per operation, Eq. 2 in
+  float64 for two levels, infinite thresholds, monotonicity, and offsets by a
+  running loop;
+* the int4 nibble table in ``tests/golden/int4_nibbles.txt``.
+"""
+from __future__ import annotations
+
+import copy
+import math
+import os
+from decimal import Decimal, getcontext
+from fractions import Fraction
+
+import numpy as np
+
+from synth import generate, router_inputs, Workload
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ------------------------------------------------------------------ helpers
+def small_workload(**kw) -> Workload:
+    base = dict(name="pin", batch=2, n_layers=4, window=2, n_kv_heads=2, n_q_heads=4,
+                head_dim=16, context=7, basis_rank=4, levels=(0, 2, 4),
+                probs=(0.5, 0.3, 0.2), q_dtype="f16", seed=11, ragged=(3, 9))
+    base.update(kw)
+    return Workload(**base)
+
+
+def small_cache(**kw):
+    return generate(small_workload(**kw), threads=2)
+
+
+def _rel(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    den = max(np.linalg.norm(b), 1e-300)
+    return float(np.linalg.norm(a - b) / den)
+
+
+def _q64(o, cache, layer):
+    return o.q_to_f64(cache.q_bits[layer], cache.q_dtype)
+
+
+def _pack(codes):
+    u = [(int(c) & 0xF) for c in codes]
+    if len(u) % 2:
+        u.append(0)
+    return np.array([u[i] | (u[i + 1] << 4) for i in range(0, len(u), 2)], dtype=np.uint8)
+
+
+def set_entries(cache, layer, z, h, token, chans, codes):
+    """Overwrite the stored entries of one token (its rank must equal len(chans))."""
+    m = layer // cache.window
+    e0 = int(cache.res_off[m, h, token])
+    assert int(cache.res_off[m, h, token + 1]) - e0 == len(chans)
+    for j, (c, k) in enumerate(zip(chans, codes)):
+        e = e0 + j
+        cache.res_idx[layer, z, h, e] = c
+        byte = int(cache.res_val[layer, z, h, e // 2])
+        nib = int(k) & 0xF
+        byte = (byte & 0xF0) | nib if e % 2 == 0 else (byte & 0x0F) | (nib << 4)
+        cache.res_val[layer, z, h, e // 2] = byte
+
+
+# ------------------------------------------------------- 40-digit brute force
+def _nibble_value(byte, high):
+    n = (byte >> 4) & 0xF if high else byte & 0xF
+    return n - 16 if n & 0x8 else n
+
+
+def brute_force_decode(cache, layer, b, hq, scale):
+    """Scalar-loop Eq. 1 + softmax attention in 40-digit decimal arithmetic."""
+    getcontext().prec = 40
+    d, rb = cache.head_dim, cache.basis_rank
+    G = cache.n_q_heads // cache.n_kv_heads
+    h = hq // G
+    m = layer // cache.window
+    t0, t1 = int(cache.cu_seqlens[b]), int(cache.cu_seqlens[b + 1])
+    qd = [Decimal(float(v)) for v in _qvals(cache, layer, b, hq)]
+    rows = {}
+    for z in (0, 1):
+        basis = cache.basis[b, m, h, z]
+        rows[z] = []
+        for t in range(t0, t1):
+            x = [Decimal(0)] * d
+            for c in range(d):
+                acc = Decimal(0)
+                for i in range(rb):
+                    acc += Decimal(float(cache.coef[layer, z, h, t, i])) * Decimal(float(basis[i, c]))
+                x[c] = acc
+            e = int(cache.res_off[m, h, t])
+            while e < int(cache.res_off[m, h, t + 1]):
+                byte = int(cache.res_val[layer, z, h, e >> 1])
+                code = _nibble_value(byte, e & 1)
+                c = int(cache.res_idx[layer, z, h, e])
+                x[c] += Decimal(float(cache.res_scale[layer, z, h, t])) * Decimal(code)
+                e += 1
+            rows[z].append(x)
+    if t1 == t0:
+        return [0.0] * d
+    sc = Decimal(scale)
+    s = [sc * sum(qd[c] * k[c] for c in range(d)) for k in rows[0]]
+    mx = max(s)
+    w = [(v - mx).exp() for v in s]
+    tot = sum(w)
+    return [float(sum(w[i] * rows[1][i][c] for i in range(len(w))) / tot) for c in range(d)]
+
+
+def _qvals(cache, layer, b, hq):
+    bits = int(0)
+    out = []
+    for v in cache.q_bits[layer, b, hq]:
+        v = int(v)
+        if cache.q_dtype == "f16":
+            out.append(float(np.array([v], dtype=np.uint16).view(np.float16)[0]))
+        else:
+            out.append(float(np.array([v << 16], dtype=np.uint32).view(np.float32)[0]))
+    return out
+
+
+def pin_brute_force(o):
+    cache = small_cache(head_dim=8, basis_rank=3, context=4, ragged=(0, 4), levels=(0, 2, 4),
+                        probs=(0.3, 0.4, 0.3), batch=3, n_q_heads=4, n_kv_heads=2)
+    scale = 0.37
+    for layer in (1, 2):
+        got = o.decode(cache, layer, sm_scale=scale)
+        for b in range(cache.batch):
+            for hq in range(cache.n_q_heads):
+                ref = brute_force_decode(cache, layer, b, hq, scale)
+                if np.linalg.norm(ref) == 0:
+                    if np.abs(got[b, hq]).max() != 0:
+                        return f"empty sequence b={b} should give zeros"
+                    continue
+                if _rel(got[b, hq], ref) > 1e-13:
+                    return f"brute force mismatch layer={layer} b={b} hq={hq}: {_rel(got[b, hq], ref):.3e}"
+    return None
+
+
+# -------------------------------------------------------------- closed forms
+def _perm_basis(cache, seed):
+    """Replace every basis by one-hot rows e_{pi(i)} (a non-involutive permutation
+    per (b, m, h, z)); returns the permutations."""
+    rng = np.random.default_rng(seed)
+    B, M, Hk = cache.basis.shape[:3]
+    rb, d = cache.basis_rank, cache.head_dim
+    perms = {}
+    for b in range(B):
+        for m in range(M):
+            for h in range(Hk):
+                for z in range(2):
+                    p = rng.permutation(d)[:rb]
+                    cache.basis[b, m, h, z] = 0
+                    cache.basis[b, m, h, z, np.arange(rb), p] = 1
+                    perms[(b, m, h, z)] = p
+    return perms
+
+
+def pin_closed_forms(o):
+    # (1) zero residual rank, one-hot coefficients, permutation bases: V_hat_t is a
+    # basis row; q = 0 gives the plain mean of the selected rows.
+    c = small_cache(levels=(0,), probs=(1.0,), head_dim=16, basis_rank=5)
+    perms = _perm_basis(c, 3)
+    rng = np.random.default_rng(4)
+    layer = 3
+    m = layer // c.window
+    Hq, Hk = c.n_q_heads, c.n_kv_heads
+    G = Hq // Hk
+    c.coef[layer] = 0
+    sel = rng.integers(0, c.basis_rank, size=(2, Hk, c.total_tokens))
+    for z in range(2):
+        for h in range(Hk):
+            c.coef[layer, z, h, np.arange(c.total_tokens), sel[z, h]] = 1
+    q0 = np.zeros((c.batch, Hq, c.head_dim))
+    out = o.decode(c, layer, q=q0)
+    for b in range(c.batch):
+        t0, t1 = int(c.cu_seqlens[b]), int(c.cu_seqlens[b + 1])
+        for hq in range(Hq):
+            h = hq // G
+            exp = np.zeros(c.head_dim)
+            for t in range(t0, t1):
+                exp[perms[(b, m, h, 1)][sel[1, h, t]]] += 1.0 / (t1 - t0)
+            if np.abs(out[b, hq] - exp).max() > 1e-15:
+                return f"q=0 mean of one-hot value rows wrong at b={b} hq={hq}"
+    # (2) two tokens, keys one-hot along a basis row, query along the same output
+    # channel: scores differ by exactly ln 3, so p = (1/4, 3/4).
+    c = small_cache(levels=(0,), probs=(1.0,), head_dim=16, basis_rank=5, batch=1,
+                    ragged=None, context=2)
+    perms = _perm_basis(c, 5)
+    layer = 2
+    m = layer // c.window
+    c.coef[layer] = 0
+    for h in range(Hk):
+        c.coef[layer, 0, h, 1, 2] = 2.0                  # K_hat_1 = 2 e_{pi_K(2)}, K_hat_0 = 0
+        c.coef[layer, 1, h, 0, 0] = 1.0                  # V_hat_0 = e_{pi_V(0)}
+        c.coef[layer, 1, h, 1, 1] = -4.0                 # V_hat_1 = -4 e_{pi_V(1)}
+    q = np.zeros((1, Hq, c.head_dim))
+    for hq in range(Hq):
+        h = hq // G
+        q[0, hq, perms[(0, m, h, 0)][2]] = math.log(3.0) / 2.0
+    out = o.decode(c, layer, q=q, sm_scale=1.0)
+    for hq in range(Hq):
+        h = hq // G
+        exp = np.zeros(c.head_dim)
+        exp[perms[(0, m, h, 1)][0]] += 0.25
+        exp[perms[(0, m, h, 1)][1]] += 0.75 * -4.0
+        if np.abs(out[0, hq] - exp).max() > 1e-14:
+            return f"two-token ln3 closed form wrong at hq={hq}: {out[0, hq]} vs {exp}"
+    # (3) single token: output is that token's rebuilt value row, here a basis row
+    # plus one residual entry s*k at a chosen channel.
+    c = small_cache(levels=(2,), probs=(1.0,), head_dim=16, basis_rank=4, batch=1,
+                    ragged=None, context=1)
+    perms = _perm_basis(c, 7)
+    layer = 1
+    m = 0
+    c.coef[layer] = 0
+    for h in range(Hk):
+        c.coef[layer, 1, h, 0, 3] = 1.0
+        set_entries(c, layer, 1, h, 0, [5, 11], [-7, 3])
+        c.res_scale[layer, 1, h, 0] = np.float16(0.0625)
+    out = o.decode(c, layer)
+    for hq in range(Hq):
+        h = hq // G
+        exp = np.zeros(c.head_dim)
+        exp[perms[(0, m, h, 1)][3]] += 1.0
+        exp[5] += 0.0625 * -7
+        exp[11] += 0.0625 * 3
+        if np.abs(out[0, hq] - exp).max() > 1e-15:
+            return f"single-token output is not V_hat_0 at hq={hq}"
+    # (4) residual-only keys: A^K = 0, one K entry per token -> score s*k*q[c].
+    c = small_cache(levels=(2,), probs=(1.0,), head_dim=16, basis_rank=4, batch=1,
+                    ragged=None, context=2)
+    layer = 0
+    c.coef[layer] = 0
+    for h in range(Hk):
+        set_entries(c, layer, 0, h, 0, [1, 9], [2, 0])      # K_hat_0 = 2 s0 e_1
+        set_entries(c, layer, 0, h, 1, [4, 9], [-1, 0])     # K_hat_1 = -s1 e_4
+        c.res_scale[layer, 0, h, 0] = np.float16(0.5)
+        c.res_scale[layer, 0, h, 1] = np.float16(0.25)
+        c.coef[layer, 1, h, 0, 0] = 1.0
+        c.coef[layer, 1, h, 1, 0] = 0.0
+        set_entries(c, layer, 1, h, 0, [0, 1], [0, 0])
+        set_entries(c, layer, 1, h, 1, [0, 1], [0, 0])
+    q = np.zeros((1, Hq, c.head_dim))
+    q[0, :, 1] = 3.0
+    q[0, :, 4] = 2.0
+    out = o.decode(c, layer, q=q, sm_scale=0.5)
+    # s0 = 0.5 * (2*0.5*3) = 1.5 ; s1 = 0.5 * (-0.25*2) = -0.25
+    p0 = 1.0 / (1.0 + math.exp(-0.25 - 1.5))
+    for hq in range(Hq):
+        h = hq // G
+        vrow = c.basis[0, 0, h, 1, 0].astype(np.float64)
+        if np.abs(out[0, hq] - p0 * vrow).max() > 1e-14:
+            return f"residual-only key closed form wrong at hq={hq}"
+    return None
+
+
+# ------------------------------------------------ reductions to library attention
+def _sdpa(q, K, V, scale):
+    import torch
+    qt = torch.tensor(q, dtype=torch.float64)[None, None]
+    kt = torch.tensor(K, dtype=torch.float64)[None, None]
+    vt = torch.tensor(V, dtype=torch.float64)[None, None]
+    return torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, scale=scale)[0, 0].numpy()
+
+
+def pin_reductions(o):
+    # R0: rank-0 residuals: K = A^K B^K, V = A^V B^V built here with torch matmul
+    import torch
+    c = small_cache(levels=(0,), probs=(1.0,), head_dim=32, basis_rank=8, context=40,
+                    ragged=(20, 60), n_layers=6, window=3, n_kv_heads=3, n_q_heads=6)
+    scale = 0.2
+    for layer in (0, 4, 5):
+        out = o.decode(c, layer, sm_scale=scale)
+        m = layer // 3
+        for b in range(c.batch):
+            t0, t1 = int(c.cu_seqlens[b]), int(c.cu_seqlens[b + 1])
+            for hq in range(c.n_q_heads):
+                h = hq // 2
+                K = torch.tensor(c.coef[layer, 0, h, t0:t1].astype(np.float64)) @ \
+                    torch.tensor(c.basis[b, m, h, 0].astype(np.float64))
+                V = torch.tensor(c.coef[layer, 1, h, t0:t1].astype(np.float64)) @ \
+                    torch.tensor(c.basis[b, m, h, 1].astype(np.float64))
+                ref = _sdpa(_q64(o, c, layer)[b, hq][None], K.numpy(), V.numpy(), scale)[0]
+                if _rel(out[b, hq], ref) > 1e-12:
+                    return f"R0 mismatch layer={layer} b={b} hq={hq}"
+    # R1: identity basis (r_b = d): attention over the raw fp16 coefficient rows
+    c = small_cache(levels=(0,), probs=(1.0,), head_dim=16, basis_rank=16, context=30,
+                    ragged=None, batch=1)
+    c.basis[:] = np.eye(16, dtype=np.float16)
+    for layer in range(c.n_layers):
+        out = o.decode(c, layer)
+        for hq in range(c.n_q_heads):
+            h = hq // 2
+            ref = _sdpa(_q64(o, c, layer)[0, hq][None], c.coef[layer, 0, h].astype(np.float64),
+                        c.coef[layer, 1, h].astype(np.float64), 0.25)[0]
+            if _rel(out[0, hq], ref) > 1e-12:
+                return f"R1 mismatch layer={layer} hq={hq}"
+    # R2: full-rank residual (every channel), no basis term: attention over the
+    # dequantised dense int4 cache, built here entry by entry.
+    c = small_cache(levels=(16,), probs=(1.0,), head_dim=16, basis_rank=4, context=25,
+                    ragged=None, batch=1)
+    c.coef[:] = 0
+    for layer in range(c.n_layers):
+        out = o.decode(c, layer)
+        m = layer // c.window
+        for hq in range(c.n_q_heads):
+            h = hq // 2
+            dense = {0: np.zeros((25, 16)), 1: np.zeros((25, 16))}
+            for z in (0, 1):
+                for t in range(25):
+                    for e in range(int(c.res_off[m, h, t]), int(c.res_off[m, h, t + 1])):
+                        byte = int(c.res_val[layer, z, h, e >> 1])
+                        dense[z][t, int(c.res_idx[layer, z, h, e])] = \
+                            float(c.res_scale[layer, z, h, t]) * _nibble_value(byte, e & 1)
+            ref = _sdpa(_q64(o, c, layer)[0, hq][None], dense[0], dense[1], 0.25)[0]
+            if _rel(out[0, hq], ref) > 1e-12:
+                return f"R2 mismatch layer={layer} hq={hq}"
+    return None
+
+
+# ---------------------------------------------------------------- invariants
+def pin_invariants(o):
+    c = small_cache(head_dim=16, basis_rank=6, context=50, ragged=(30, 70),
+                    levels=(0, 2, 4, 8), probs=(0.4, 0.3, 0.2, 0.1))
+    layer = 3
+    out, probs = o.decode(c, layer, with_probs=True)
+    for key, p in probs.items():
+        if p.size and (np.abs(p.sum(axis=1) - 1).max() > 1e-12 or p.min() < 0):
+            return f"probabilities of {key} do not sum to one"
+    # token permutation within sequence 1 (with metadata and rebuilt offsets)
+    c2 = permute_tokens(c, b=1, seed=9)
+    out2 = o.decode(c2, layer)
+    if np.abs(out2 - out).max() > 1e-13 * max(1.0, np.abs(out).max()):
+        return "output changed under token permutation"
+    # another sequence's data does not leak
+    c3 = copy.deepcopy(c)
+    t0, t1 = int(c.cu_seqlens[0]), int(c.cu_seqlens[1])
+    c3.coef[:, :, :, t0:t1] = -c3.coef[:, :, :, t0:t1]
+    out3 = o.decode(c3, layer)
+    if np.abs(out3[1:] - out[1:]).max() != 0:
+        return "sequence 0's data changed another sequence's output"
+    # query-head grouping: each group member matches a one-head attention
+    G = c.n_q_heads // c.n_kv_heads
+    for hq in range(c.n_q_heads):
+        h = hq // G
+        for b in range(c.batch):
+            K = o.reconstruct(c, layer, 0, h, b)
+            V = o.reconstruct(c, layer, 1, h, b)
+            ref = _sdpa(_q64(o, c, layer)[b, hq][None], K, V, 0.25)[0]
+            if _rel(out[b, hq], ref) > 1e-12:
+                return f"query head {hq} does not read KV head {h}"
+    return None
+
+
+def permute_tokens(cache, b, seed):
+    """Copy of ``cache`` with sequence b's tokens permuted, carrying every
+    per-token field and residual entry and rebuilding the offsets."""
+    c = copy.deepcopy(cache)
+    rng = np.random.default_rng(seed)
+    t0, t1 = int(cache.cu_seqlens[b]), int(cache.cu_seqlens[b + 1])
+    perm = t0 + rng.permutation(t1 - t0)
+    M, Hk = cache.rank_code.shape[:2]
+    levels = np.asarray(cache.levels)
+    for m in range(M):
+        for h in range(Hk):
+            c.rank_code[m, h, t0:t1] = cache.rank_code[m, h, perm]
+            c.res_off[m, h, 1:] = np.cumsum(levels[c.rank_code[m, h]])
+    for layer in range(cache.n_layers):
+        m = layer // cache.window
+        for z in range(2):
+            for h in range(Hk):
+                c.coef[layer, z, h, t0:t1] = cache.coef[layer, z, h, perm]
+                c.res_scale[layer, z, h, t0:t1] = cache.res_scale[layer, z, h, perm]
+                # gather entries token by token in the new order
+                idx, codes = [], []
+                for t in range(cache.total_tokens):
+                    src = perm[t - t0] if t0 <= t < t1 else t
+                    for e in range(int(cache.res_off[m, h, src]), int(cache.res_off[m, h, src + 1])):
+                        idx.append(int(cache.res_idx[layer, z, h, e]))
+                        byte = int(cache.res_val[layer, z, h, e >> 1])
+                        codes.append(_nibble_value(byte, e & 1))
+                c.res_idx[layer, z, h, :len(idx)] = idx
+                pk = _pack(codes)
+                c.res_val[layer, z, h, :pk.size] = pk
+    return c
+
+
+# ----------------------------------------------------------------- Eq. 3 probe
+def pin_probe(o):
+    # reference rows exactly representable in fp16: small-integer coefficients
+    # over one-hot bases, fp16-exact residuals.
+    c = small_cache(head_dim=16, basis_rank=4, context=20, ragged=None, batch=2,
+                    levels=(0, 2), probs=(0.5, 0.5))
+    _perm_basis(c, 13)
+    rng = np.random.default_rng(14)
+    c.coef[:] = rng.integers(-3, 4, size=c.coef.shape).astype(np.float16)
+    c.res_scale[:] = np.float16(0.5)
+    layer = 2
+    heads = [1, 0]
+    K = np.stack([np.concatenate([o.reconstruct(c, layer, 0, h, b) for b in range(c.batch)]) for h in heads])
+    V = np.stack([np.concatenate([o.reconstruct(c, layer, 1, h, b) for b in range(c.batch)]) for h in heads])
+    if not np.array_equal(K.astype(np.float16).astype(np.float64), K):
+        return "probe test setup: reference not fp16-exact"
+    e = o.probe(c, layer, heads, K.astype(np.float16), V.astype(np.float16))
+    if np.abs(e).max() != 0:
+        return "Eq. 3 error is not zero for an exact reference"
+    for cval in (2.0, -0.5):
+        eps = 1e-6
+        e = o.probe(c, layer, heads, K.astype(np.float16), (cval * V).astype(np.float16), eps=eps)
+        out = o.decode(c, layer)
+        G = c.n_q_heads // c.n_kv_heads
+        for i, h in enumerate(heads):
+            for g in range(G):
+                n = np.linalg.norm(out[:, h * G + g], axis=-1)
+                exp = abs(1 - cval) * n / (abs(cval) * n + eps)
+                if np.abs(e[:, i * G + g] - exp).max() > 1e-12:
+                    return f"Eq. 3 scaled-reference closed form wrong (c={cval})"
+    return None
+
+
+# -------------------------------------------------------------------- router
+def fp32_round(x: Fraction) -> Fraction:
+    """Round an exact rational to the nearest float32, ties to even."""
+    if x == 0:
+        return Fraction(0)
+    sign = -1 if x < 0 else 1
+    a = abs(x)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1
+    e = max(e, -126)
+    ulp = Fraction(2) ** (e - 23)
+    n = a / ulp
+    fl = n.numerator // n.denominator
+    rem = n - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    return sign * fl * ulp
+
+
+def exact_score(u, phi):
+    z = fp32_round(Fraction(float(u[0])) * Fraction(float(phi[0])))
+    for i in (1, 2, 3):
+        z = fp32_round(z + fp32_round(Fraction(float(u[i])) * Fraction(float(phi[i]))))
+    return z
+
+
+def pin_router(o):
+    w = small_workload(levels=(0, 4, 8, 16), probs=(0.25, 0.25, 0.25, 0.25))
+    phi, u, theta = router_inputs(w, n_windows=2, T=300)
+    rng = np.random.default_rng(21)
+    # per-operation rounded float32 score, checked in exact rational arithmetic
+    for m in range(2):
+        z = o.router_score(phi[m], u[m])
+        for h in range(phi.shape[1]):
+            for t in rng.integers(0, 300, size=60):
+                if Fraction(float(z[h, t])) != exact_score(u[m], phi[m, h, t]):
+                    return f"router score not the per-op rounded float32 sum at m={m} h={h} t={t}"
+    # adversarial magnitudes where fused or reordered sums round differently
+    u2 = np.array([1.0, 1e-8, -1.0, 3.0], np.float32)
+    ph = rng.standard_normal((500, 4)).astype(np.float32) * np.array([1e4, 1.0, 1e4, 1e-3], np.float32)
+    z = o.router_score(ph, u2)
+    for t in range(500):
+        if Fraction(float(z[t])) != exact_score(u2, ph[t]):
+            return "router score order/rounding differs on cancelling inputs"
+    codes, off = o.route(phi, u, theta, w.levels)
+    lev = np.asarray(w.levels)
+    # offsets by a running loop
+    for m in range(2):
+        for h in range(phi.shape[1]):
+            run = 0
+            for t in range(300):
+                if int(off[m, h, t]) != run:
+                    return "offsets are not the exclusive running sum of ranks"
+                run += int(lev[codes[m, h, t]])
+            if int(off[m, h, 300]) != run:
+                return "final offset is not the total rank"
+    # Eq. 2 with two levels, in float64 with the logistic gate, away from ties
+    tau = np.array([[0.7], [0.9]])
+    th = np.stack([o.theta_from_tau(t) for t in tau])
+    c2, _ = o.route(phi, u, th, (2, 8))
+    for m in range(2):
+        s = phi[m].astype(np.float64) @ u[m].astype(np.float64)
+        gate = 1 / (1 + np.exp(-s))
+        ref = np.where(gate > tau[m, 0], 1, 0)
+        far = np.abs(s - np.log(tau[m, 0] / (1 - tau[m, 0]))) > 1e-4
+        if not np.array_equal(c2[m][far], ref[far]):
+            return "two-level routing disagrees with Eq. 2"
+        if not np.any(ref == 1) or not np.any(ref == 0):
+            return "router pin setup does not reach both levels"
+    # infinite thresholds
+    inf = np.full_like(theta, np.inf)
+    c_hi, _ = o.route(phi, u, inf, w.levels)
+    c_lo, _ = o.route(phi, u, -inf, w.levels)
+    if c_hi.max() != 0 or c_lo.min() != len(w.levels) - 1:
+        return "infinite thresholds do not pin the extreme levels"
+    # exact ties: Eq. 2 uses a strict inequality, so z == theta keeps the lower level
+    ut = np.array([1.0, 0.0, 0.0, 0.0], np.float32)
+    pt = np.zeros((1, 1, 4, 4), np.float32)
+    pt[0, 0, :, 0] = [0.5, 1.5, 1.5000001, 2.5]
+    ct, _ = o.route(pt, ut[None], np.array([[0.5, 1.5, 2.5]], np.float32), (0, 2, 4, 6))
+    if [int(x) for x in ct[0, 0]] != [0, 1, 2, 2]:
+        return f"ties at the threshold must keep the lower level, got {ct[0, 0]}"
+    # monotone in each feature with positive weight
+    bump = phi.copy()
+    bump[..., 0] += 0.5
+    c_b, _ = o.route(bump, u, theta, w.levels)
+    if np.any(c_b < codes):
+        return "raising a positively weighted feature lowered the level"
+    return None
+
+
+# --------------------------------------------------------- nibble + residual map
+def pin_nibbles(o):
+    table = []
+    with open(os.path.join(GOLDEN, "int4_nibbles.txt")) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if line:
+                a, b = line.split()
+                table.append((int(a, 16), int(b)))
+    got = o.int4_from_nibble(np.array([a for a, _ in table]))
+    if [int(x) for x in got] != [b for _, b in table]:
+        return "int4 nibble decoding disagrees with the two's-complement table"
+    # byte order: entry e lives in byte e//2, low nibble when e is even
+    vb = np.array([0x1F, 0x72], dtype=np.uint8)
+    if [int(x) for x in o.entry_codes(vb, 0, 4)] != [-1, 1, 2, 7]:
+        return "entry -> (byte, nibble) placement wrong"
+    return None
+
+
+def pin_residual_map(o):
+    c = small_cache(levels=(2, 4), probs=(0.5, 0.5), head_dim=16, context=3, ragged=None, batch=1)
+    layer, z, h = 1, 1, 0
+    set_entries(c, layer, z, h, 1, [3, 0] + ([7, 9] if c.res_off[0, h, 2] - c.res_off[0, h, 1] == 4 else []),
+                [-7, 5] + ([1, -1] if c.res_off[0, h, 2] - c.res_off[0, h, 1] == 4 else []))
+    c.res_scale[layer, z, h, 1] = np.float16(0.125)
+    got = o.residual_map(c, layer, z, h, 1, 2)
+    exp = np.zeros((1, 16))
+    exp[0, 3], exp[0, 0] = -7 * 0.125, 5 * 0.125
+    if c.res_off[0, h, 2] - c.res_off[0, h, 1] == 4:
+        exp[0, 7], exp[0, 9] = 0.125, -0.125
+    if not np.array_equal(got, exp):
+        return "residual map of a hand-set token is wrong"
+    return None
+
+
+def pin_query_formats(o):
+    """fp16 / bf16 query bits decode as torch's own dtypes do."""
+    import torch
+    rng = np.random.default_rng(31)
+    bits = rng.integers(0, 2**16, size=4096, dtype=np.uint64).astype(np.uint16)
+    bits = bits[(bits & 0x7C00) != 0x7C00]                      # finite fp16 patterns
+    ref16 = torch.from_numpy(bits.astype(np.int16)).view(torch.float16).double().numpy()
+    if not np.array_equal(o.q_to_f64(bits, "f16"), ref16):
+        return "fp16 query decoding differs from torch.float16"
+    b2 = bits[(bits & 0x7F80) != 0x7F80]                        # finite bf16 patterns
+    ref_bf = torch.from_numpy(b2.astype(np.int16)).view(torch.bfloat16).double().numpy()
+    if not np.array_equal(o.q_to_f64(b2, "bf16"), ref_bf):
+        return "bf16 query decoding differs from torch.bfloat16"
+    return None
+
+
+ALL_PINS = [pin_query_formats, pin_nibbles, pin_residual_map, pin_brute_force, pin_closed_forms,
+            pin_reductions, pin_invariants, pin_probe, pin_router]
+
+
+def run_all(o):
+    """Run every pin; returns the list of failure messages (empty when all hold)."""
+    fails = []
+    for pin in ALL_PINS:
+        try:
+            r = pin(o)
+        except Exception as exc:                      # a mutant may also crash
+            r = f"{pin.__name__} raised {type(exc).__name__}: {exc}"
+        if r is not None:
+            fails.append(f"{pin.__name__}: {r}")
+    return fails

@@ -1,0 +1,145 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and check that at least
+one pin fails for each.  A pin suite that lets a mutant through is too weak to
+trust the oracle with."""
+import numpy as np
+import pytest
+
+import oracle
+import oracle.factorized as F
+import oracle.router as R
+import pins
+
+_orig_reconstruct = F.reconstruct
+_orig_attention = F.attention
+_orig_entry_codes = F.entry_codes
+
+
+def _reconstruct_variant(kind):
+    def rec(cache, layer, z, h, b):
+        m = F.window_of(layer, cache.window)
+        t0, t1 = int(cache.cu_seqlens[b]), int(cache.cu_seqlens[b + 1])
+        zb = 1 - z if kind == "other_basis" else z
+        A = cache.coef[layer, z, h, t0:t1].astype(np.float64)
+        if kind == "coef_shift":
+            A = cache.coef[layer, z, h, t0 + 1:t1 + 1].astype(np.float64)
+            A = np.concatenate([A, np.zeros((t1 - t0 - A.shape[0], A.shape[1]))])
+        X = A @ cache.basis[b, m, h, zb].astype(np.float64)
+        if kind == "no_residual":
+            return X
+        off = cache.res_off[m, h].astype(np.int64)
+        rho = off[t0 + 1:t1 + 1] - off[t0:t1]
+        e0, e1 = int(off[t0]), int(off[t1])
+        tok = np.repeat(np.arange(t1 - t0), rho)
+        chan = cache.res_idx[layer, z, h, e0:e1].astype(np.int64)
+        code = F.entry_codes(cache.res_val[layer, z, h], e0, e1 - e0)
+        gs = cache.res_scale[layer, z, h, t0:t1].astype(np.float64)
+        Rm = np.zeros_like(X)
+        Rm[tok, chan] = code
+        if kind == "residual_sign":
+            return X - gs[:, None] * Rm
+        if kind == "no_gate":
+            return X + Rm
+        if kind == "residual_layer":       # residual of the window's first layer
+            l0 = m * cache.window
+            chan = cache.res_idx[l0, z, h, e0:e1].astype(np.int64)
+            code = F.entry_codes(cache.res_val[l0, z, h], e0, e1 - e0)
+            Rm = np.zeros_like(X)
+            Rm[tok, chan] = code
+        return X + gs[:, None] * Rm
+    return rec
+
+
+def _attention_variant(kind):
+    def att(q, K, V, sm_scale):
+        if K.shape[0] == 0:
+            return np.zeros((q.shape[0], V.shape[1])), np.zeros((q.shape[0], 0))
+        s = (q @ K.T) * (1.0 if kind == "no_scale" else sm_scale)
+        s = s - s.max(axis=1, keepdims=True)
+        w = np.exp(s)
+        ax = 0 if kind == "wrong_axis" else 1
+        p = w / w.sum(axis=ax, keepdims=True)
+        return (p @ (K if kind == "keys_as_values" else V)), p
+    return att
+
+
+def _entry_codes_swapped(val_bytes, start, count):
+    e = np.arange(start, start + count, dtype=np.int64)
+    byte = val_bytes[e // 2].astype(np.int64)
+    nib = np.where(e % 2 == 1, byte & 0xF, byte >> 4)
+    return F.int4_from_nibble(nib)
+
+
+def _router_fused(phi, u):
+    phi = np.asarray(phi, dtype=np.float64)
+    u = np.asarray(u, dtype=np.float64)
+    return (phi @ u).astype(np.float32)
+
+
+def _router_reordered(phi, u):
+    phi = np.asarray(phi, dtype=np.float32)
+    u = np.asarray(u, dtype=np.float32)
+    z = np.float32(u[3]) * phi[..., 3]
+    for i in (2, 1, 0):
+        z = z + np.float32(u[i]) * phi[..., i]
+    return z
+
+
+def _level_ge(z, theta):
+    k = np.zeros(np.shape(z), dtype=np.int64)
+    for th in np.asarray(theta, dtype=np.float32):
+        k += (np.asarray(z, np.float32) >= th)
+    return k
+
+
+def _route_inclusive(phi, u, theta, levels):
+    codes, off = R.__dict__["_orig_route"](phi, u, theta, levels)
+    lev = np.asarray(levels)
+    off2 = np.zeros_like(off)
+    off2[..., :-1] = off[..., 1:]
+    off2[..., -1] = off[..., -1]
+    return codes, off2
+
+
+MUTANTS = {
+    "residual dropped": [(F, "reconstruct", _reconstruct_variant("no_residual"))],
+    "residual sign flipped": [(F, "reconstruct", _reconstruct_variant("residual_sign"))],
+    "gate scale dropped": [(F, "reconstruct", _reconstruct_variant("no_gate"))],
+    "K/V basis swapped": [(F, "reconstruct", _reconstruct_variant("other_basis"))],
+    "coefficient rows shifted by one token": [(F, "reconstruct", _reconstruct_variant("coef_shift"))],
+    "residual read from the window's first layer": [(F, "reconstruct", _reconstruct_variant("residual_layer"))],
+    "window index l % w": [(F, "window_of", lambda layer, w: layer % w)],
+    "interleaved GQA grouping": [(F, "kv_head_of", lambda hq, nq, nk: hq % nk)],
+    "softmax scale dropped": [(F, "attention", _attention_variant("no_scale"))],
+    "softmax over tokens of the wrong axis": [(F, "attention", _attention_variant("wrong_axis"))],
+    "keys used as values": [(F, "attention", _attention_variant("keys_as_values"))],
+    "unsigned int4": [(F, "int4_from_nibble", lambda nib: np.asarray(nib, dtype=np.int64))],
+    "nibble order swapped": [(F, "entry_codes", _entry_codes_swapped)],
+    "default scale 1/d": [(F, "default_scale", lambda d: 1.0 / d)],
+    "probe denominator uses the compressed output": [
+        (F, "probe_error", lambda o_ref, o, eps=1e-6: np.linalg.norm(np.asarray(o_ref) - o, axis=-1)
+         / (np.linalg.norm(o, axis=-1) + eps))],
+    "probe eps dropped": [
+        (F, "probe_error", lambda o_ref, o, eps=1e-6: np.linalg.norm(np.asarray(o_ref) - o, axis=-1)
+         / np.maximum(np.linalg.norm(o_ref, axis=-1), 1e-300))],
+    "router score in float64": [(R, "router_score", _router_fused)],
+    "router score summed in reverse": [(R, "router_score", _router_reordered)],
+    "router ties go up": [(R, "level_index", _level_ge)],
+    "inclusive offsets": [(R, "route", _route_inclusive)],
+    "bf16 query read as fp16": [(F, "q_to_f64", lambda bits, dtype: np.asarray(bits, np.uint16)
+                                 .view(np.float16).astype(np.float64))],
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, monkeypatch):
+    R.__dict__.setdefault("_orig_route", R.route)
+    for mod, attr, fn in MUTANTS[name]:
+        monkeypatch.setattr(mod, attr, fn)
+        if hasattr(oracle, attr):
+            monkeypatch.setattr(oracle, attr, fn)
+    fails = pins.run_all(oracle)
+    assert fails, f"no pin caught the mutant '{name}'"
+
+
+def test_unmutated_oracle_passes_every_pin():
+    assert pins.run_all(oracle) == []
