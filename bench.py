@@ -1,0 +1,207 @@
+"""Decode-attention throughput over the factorized KV cache on one MI355X.
+
+One step = one decode token through every layer: L per-layer dwkv_decode
+calls on one stream (the whole hot path: query projection, coefficient and
+residual streaming, softmax, value product, split merge).  Inputs are synthetic
+and already resident in HBM when the timed region starts.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes_per_layer(host) -> list[float]:
+    """Bytes one per-layer decode must move: the window's bases, the layer's
+    coefficient rows, the window's offsets, the layer's residual indices,
+    codes and scales, the query in and the fp32 output out."""
+    B, Hk, Hq, d = host.batch, host.n_kv_heads, host.n_q_heads, host.head_dim
+    T, rb = host.total_tokens, host.basis_rank
+    qbytes = 2
+    out = []
+    for l in range(host.n_layers):
+        m = l // host.window
+        ent = float(host.res_off[m, :, -1].astype(np.int64).sum())      # entries per Z over heads
+        out.append(B * Hk * 2 * rb * d * 2          # bases B^K, B^V (fp16)
+                   + 2 * Hk * T * rb * 2            # coefficients A^K, A^V (fp16)
+                   + Hk * (T + 1) * 4               # offsets
+                   + 2 * ent * 1 + 2 * ent / 2      # channel bytes + int4 codes, K and V
+                   + 2 * Hk * T * 2                 # residual scales (fp16), K and V
+                   + B * Hq * d * qbytes + B * Hq * d * 4)
+    return out
+
+
+def dense_fp16_bytes_per_layer(host) -> float:
+    return 2 * host.n_kv_heads * host.total_tokens * host.head_dim * 2
+
+
+def cpu_baseline(host, n_pairs: int, budget_s: float):
+    """The float64 oracle, as it stands, on a bounded sample of the same step:
+    n_pairs (layer, KV head) slabs; extrapolated to the whole step."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    L, Hk, B = host.n_layers, host.n_kv_heads, host.batch
+    pairs = [(l, h) for l in range(L) for h in range(Hk)]
+    rng = np.random.default_rng(0)
+    sample = [pairs[i] for i in rng.choice(len(pairs), size=min(n_pairs, len(pairs)), replace=False)]
+    t0 = time.perf_counter()
+    done = 0
+    for l, h in sample:
+        oracle.decode(host, l, heads=[(b, h) for b in range(B)])
+        done += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    step_s = dt / done * len(pairs)
+    return {"value": B / step_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} of {len(pairs)} (layer, KV head) slabs of one decode step, "
+                      f"{dt:.1f} s, extrapolated to the full step ({step_s:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama8b-64k")
+    ap.add_argument("--split", type=int, default=0, help="tokens per workgroup chunk (0 = automatic)")
+    ap.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
+    ap.add_argument("--cpu-pairs", type=int, default=24)
+    ap.add_argument("--cpu-budget", type=float, default=25.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              f"(the decode path shards by KV head across GPUs with no exchange, see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_06523_amd import DeviceCache, binding
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2607_06523_amd.build import build
+        build()
+    from synth import ALL, generate
+
+    wl = ALL[args.workload]
+    log(f"[bench] generating {wl.name} ({wl.description})")
+    t = time.time()
+    host = generate(wl)
+    log(f"[bench] generated in {time.time() - t:.1f} s")
+    dc = DeviceCache(host, split_tokens=args.split)
+    L = host.n_layers
+    stream = torch.cuda.current_stream()
+    ws = dc.workspace()
+    outs = [torch.empty((host.batch, host.n_q_heads, host.head_dim), dtype=torch.float32, device="cuda")
+            for _ in range(L)]
+
+    def step():
+        for l in range(L):
+            dc.decode(l, out=outs[l], workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    graph = None
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        for _ in range(2):
+            graph.replay()
+        torch.cuda.synchronize()
+
+    # timed region: K steps; per-call events on the stream the kernels run on
+    ev_step = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev_calls = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in range(L)] if graph is None else None
+    call_ms = []
+    torch.cuda.synchronize()
+    ev_step[0].record(stream)
+    wall0 = time.perf_counter()
+    for k in range(args.steps):
+        if graph is not None:
+            graph.replay()
+        elif k == args.steps - 1:
+            for l in range(L):       # last step: time every call on its own
+                ev_calls[l][0].record(stream)
+                dc.decode(l, out=outs[l], workspace=ws)
+                ev_calls[l][1].record(stream)
+        else:
+            step()
+    ev_step[1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = ev_step[0].elapsed_time(ev_step[1])
+    ms_per_step = total_ms / args.steps
+    if ev_calls is not None:
+        call_ms = [a.elapsed_time(b) for a, b in ev_calls]
+
+    bytes_layer = algorithmic_bytes_per_layer(host)
+    bytes_step = float(sum(bytes_layer))
+    tok_s = host.batch / (ms_per_step / 1e3)
+    step_gbps = bytes_step / (ms_per_step / 1e3) / 1e9
+    if call_ms:
+        avg_call_ms = float(np.mean(call_ms))
+        achieved = float(np.mean(bytes_layer)) / (avg_call_ms / 1e3) / 1e9
+    else:
+        avg_call_ms = ms_per_step / L
+        achieved = step_gbps
+    result = {
+        "metric": "compressed-KV decode attn tokens/s at 64K ctx (plus achieved HBM GB/s)",
+        "value": round(tok_s, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": host.batch, "context": wl.context,
+                   "layers": L, "window": wl.window, "kv_heads": wl.n_kv_heads,
+                   "q_heads": wl.n_q_heads, "head_dim": wl.head_dim, "basis_rank": wl.basis_rank,
+                   "levels": list(wl.levels), "split_tokens": dc.split_tokens,
+                   "graph": bool(graph is not None)},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None},
+        "step_gbps": round(step_gbps, 1),
+        "bytes_per_step": int(bytes_step),
+        "bytes_per_layer_call": int(np.mean(bytes_layer)),
+        "avg_layer_call_ms": round(avg_call_ms, 5),
+        "compression_vs_fp16": round(dense_fp16_bytes_per_layer(host) / np.mean(bytes_layer), 3),
+        "kv_token_layers_per_s": round(host.total_tokens * L / (ms_per_step / 1e3), 1),
+        "wall_s_timed": round(wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a sample")
+        result["cpu_baseline"] = cpu_baseline(host, args.cpu_pairs, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,175 @@
+/*
+ * dwkv.h -- C ABI of the MI355X (gfx950) decode path over a cross-depth
+ * factorized KV cache (DepthWeave-KV, Sec. 3 of the paper).
+ *
+ * The cache stores, for every depth window m (a run of `window` consecutive
+ * layers) and KV head h, shared channel bases B^K_{m,h}, B^V_{m,h} (r_b x d),
+ * and for every layer l, token t: a coefficient row A^Z_{l,h,t} (1 x r_b) and
+ * a routed residual of rho_{m,h,t} channels, each an int4 code, with one
+ * gate-folded scale g*s per (l, Z, h, t).  The key/value of token t is, by
+ * Eq. 1,  X_hat = A B + g R.  The decode entry point never materialises
+ * X_hat: it projects the query into basis space once, streams the
+ * coefficients and residual entries, and runs softmax attention on chip.
+ *
+ * Conventions for every entry point
+ *  - Pointers are DEVICE pointers unless the name ends in `_host`.
+ *  - All buffers are owned by the caller; the library allocates nothing and
+ *    keeps no global mutable state, so calls on different streams do not
+ *    interfere (calls sharing one workspace must be ordered by the caller).
+ *  - Argument errors are detected on the host before anything is enqueued and
+ *    returned synchronously; DWKV_E_HIP reports a failed HIP call or launch.
+ *  - Kernels run asynchronously on `stream` (a hipStream_t; NULL = the null
+ *    stream).  Decode trusts the layout; dwkv_validate is the checked path.
+ *  - No exception crosses the ABI.
+ */
+#ifndef DWKV_H
+#define DWKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DWKV_ABI_VERSION 1
+#define DWKV_MAX_LEVELS 8
+#define DWKV_MAX_PROBE_HEADS 64
+
+typedef enum dwkv_status {
+  DWKV_OK = 0,
+  DWKV_E_NULL = 1,        /* a required pointer is NULL                           */
+  DWKV_E_DIMS = 2,        /* sizes inconsistent with each other                   */
+  DWKV_E_UNSUPPORTED = 3, /* consistent but not built: head_dim != 128,
+                             G = Hq/Hkv not in {1,2,4,8,16}, r_b not a multiple of
+                             16 in [16,128], more than 8 levels, 32-bit offset
+                             overflow possible                                    */
+  DWKV_E_WORKSPACE = 4,   /* workspace smaller than the *_workspace_bytes value    */
+  DWKV_E_LAYOUT = 5,      /* dwkv_validate found a malformed cache                 */
+  DWKV_E_HIP = 6          /* a HIP runtime call or kernel launch failed            */
+} dwkv_status;
+
+typedef enum dwkv_qtype { DWKV_F16 = 0, DWKV_BF16 = 1 } dwkv_qtype;
+
+/* Shape of one factorized cache (all sequences packed along the token axis). */
+typedef struct dwkv_dims {
+  int32_t batch;          /* B sequences                                          */
+  int32_t n_layers;       /* L layers held; L % window == 0                        */
+  int32_t window;         /* w: layers per depth window (non-overlapping, m = l/w) */
+  int32_t n_kv_heads;     /* Hkv                                                   */
+  int32_t n_q_heads;      /* Hq; query head hq reads KV head hq / (Hq/Hkv)         */
+  int32_t head_dim;       /* d (must be 128)                                       */
+  int32_t basis_rank;     /* r_b                                                   */
+  int32_t n_levels;       /* routed residual-rank levels, 1..8                     */
+  int32_t levels[DWKV_MAX_LEVELS]; /* ascending, even, 0 <= level <= d             */
+  const int32_t* cu_seqlens_host;  /* [B+1] packed token starts, host copy         */
+  const int32_t* cu_seqlens;       /* the same [B+1], device copy                  */
+  int64_t total_tokens;   /* T = cu_seqlens_host[B]                                */
+  int64_t res_stride;     /* residual entries per (layer, Z, head) slab; a multiple
+                             of 256 and >= the largest slab total + 512            */
+  int32_t split_tokens;   /* tokens per workgroup chunk; 0 = automatic, otherwise a
+                             multiple of 64                                        */
+  int32_t reserved;
+} dwkv_dims;
+
+/* Compressed cache (Eq. 1 factors).  M = L / window, Z = 0 keys, Z = 1 values. */
+typedef struct dwkv_cache {
+  const void*     basis;     /* fp16 [B][M][Hkv][2][r_b][d]: rows of B^Z_{m,h} per sequence */
+  const void*     coef;      /* fp16 [L][2][Hkv][T][r_b]: A^Z_{l,h,t}                       */
+  const uint8_t*  rank_code; /* [M][Hkv][T] level index k of each token (rho = levels[k])  */
+  const uint32_t* res_off;   /* [M][Hkv][T+1] exclusive running sum of rho over the packed
+                                tokens: token t's entries are [res_off[t], res_off[t+1])   */
+  const uint8_t*  res_idx;   /* [L][2][Hkv][res_stride] channel index (< d) of each entry  */
+  const uint8_t*  res_val;   /* [L][2][Hkv][res_stride/2] int4 two's-complement codes;
+                                entry e in byte e/2, low nibble when e is even; -8 invalid */
+  const void*     res_scale; /* fp16 [L][2][Hkv][T] gate-folded residual scale g*s         */
+} dwkv_cache;
+
+/* Attention-output probe (Eq. 3) against a dense higher-fidelity cache. */
+typedef struct dwkv_probe {
+  int32_t n_heads;             /* probed KV heads, 1..min(Hkv, 64)                     */
+  const int32_t* kv_heads_host;/* [n_heads] distinct KV head ids                       */
+  const void* k_ref;           /* fp16 [n_heads][T][d] reference keys (packed tokens)  */
+  const void* v_ref;           /* fp16 [n_heads][T][d] reference values                */
+  float eps;                   /* Eq. 3 epsilon (e.g. 1e-6)                            */
+  float* err;                  /* out fp32 [B][n_heads*G]: probed head i, group member g
+                                  at column i*G+g                                      */
+  float* out_ref;              /* optional out fp32 [B][n_heads*G][d]: attention over the
+                                  reference cache; may be NULL                         */
+} dwkv_probe;
+
+int32_t dwkv_abi_version(void);
+const char* dwkv_status_str(dwkv_status s);
+
+/* Tokens per workgroup chunk the decode will use for these dims (the automatic
+ * choice when dims->split_tokens is 0), or -1 when the dims are invalid. */
+int32_t dwkv_split_tokens(const dwkv_dims* dims);
+
+/* Bytes of device workspace dwkv_decode needs (0 when dims are invalid).
+ * probe may be NULL. */
+size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe);
+
+/* Per-layer decode attention over the factorized cache (Eq. 1 folded into the
+ * attention, Sec. 3 fused data path): for every sequence b and query head hq,
+ *   out[b][hq] = softmax_t(sm_scale * q[b][hq] . K_hat_t) V_hat_t
+ * over the T_b cached tokens of sequence b (no mask; the decode token is
+ * already appended), K_hat/V_hat as in Eq. 1 for layer `layer` (0-based index
+ * into the layers held).  An empty sequence (T_b = 0) yields zeros.
+ *   q:        [B][Hq][d] in q_type (fp16 or bf16), read-only
+ *   sm_scale: softmax scale; <= 0 selects 1/sqrt(d)
+ *   out:      fp32 [B][Hq][d], written
+ *   probe:    NULL, or Eq. 3 error for the listed KV heads (see dwkv_probe)
+ *   workspace:>= dwkv_workspace_bytes(dims, probe) bytes of device memory;
+ *             contents need no initialisation and are clobbered.
+ * Returns DWKV_OK once enqueued. */
+dwkv_status dwkv_decode(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
+                        const void* q, int32_t q_type, float sm_scale, float* out,
+                        const dwkv_probe* probe, void* workspace, size_t ws_bytes,
+                        void* stream);
+
+/* Bytes of device workspace dwkv_route needs (0 when dims are invalid). */
+size_t dwkv_route_workspace_bytes(const dwkv_dims* dims);
+
+/* Token-conditional depth router (Eq. 2, multi-level reading) and the residual
+ * offsets it implies.  For every window m, KV head h and packed token t:
+ *   z = ((u0*phi0 + u1*phi1) + u2*phi2) + u3*phi3   (float32, each op rounded)
+ *   k = #{ j < n_levels-1 : z > theta[m][j] }      (strict: ties keep the lower level)
+ *   rank_code[m][h][t] = k,   rho = levels[k]
+ *   res_off[m][h][0] = 0,     res_off[m][h][t+1] = res_off[m][h][t] + rho
+ * theta holds logits of the gate thresholds tau (theta = log(tau/(1-tau))), so
+ * z > theta is sigma(z) > tau.
+ *   phi:   fp32 [M][Hkv][T][4] router features
+ *   u:     fp32 [M][4] router weights (shared by the layers of a window)
+ *   theta: fp32 [M][n_levels-1] ascending thresholds on z
+ *   rank_code: out uint8 [M][Hkv][T];  res_off: out uint32 [M][Hkv][T+1]
+ * Bit-exact by construction.  Returns DWKV_E_UNSUPPORTED when
+ * T * levels[n_levels-1] could exceed 2^32-1. */
+dwkv_status dwkv_route(const dwkv_dims* dims, const float* phi, const float* u,
+                       const float* theta, uint8_t* rank_code, uint32_t* res_off,
+                       void* workspace, size_t ws_bytes, void* stream);
+
+/* Dense residual term g*R of Eq. 1 for packed tokens [t0, t1) of slab
+ * (layer, z, kv_head): dense[t-t0][c] = res_scale * code for every stored entry
+ * of token t at channel c, zero elsewhere; fp32 [t1-t0][d].  Decodes entries
+ * with the same device routines the decode kernel uses (a test hook). */
+dwkv_status dwkv_residual_map(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
+                              int32_t z, int32_t kv_head, int64_t t0, int64_t t1,
+                              float* dense, void* stream);
+
+/* Bytes of device workspace dwkv_validate needs. */
+size_t dwkv_validate_workspace_bytes(void);
+
+/* Checks the layout (synchronous; blocks on `stream`): for every window, head
+ * and token, res_off[t+1]-res_off[t] == levels[rank_code[t]] and rank_code <
+ * n_levels; res_off[0] == 0 and res_off[T] + 512 <= res_stride; for every
+ * layer and Z, each token's channel indices are < d and distinct, no code is
+ * -8, and entries are ordered by descending |code|, then ascending channel.
+ * Returns DWKV_OK or DWKV_E_LAYOUT; *bad_index (if not NULL) receives a code
+ * locating the first failure found (-1 when none). */
+dwkv_status dwkv_validate(const dwkv_dims* dims, const dwkv_cache* cache, int64_t* bad_index,
+                          void* workspace, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DWKV_H */

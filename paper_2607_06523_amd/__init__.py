@@ -1,0 +1,194 @@
+"""MI355X-native decode attention over the DepthWeave-KV cross-depth factorized cache.
+
+The hot path lives in ``libdwkv.so`` (hand-written HIP for gfx950, C ABI in
+``include/dwkv.h``).  This package only marshals arguments: torch tensors
+provide device memory and the current HIP stream.
+
+    cache = DeviceCache(host_cache)        # upload the compressed layout
+    out = cache.decode(layer)              # fp32 [B, Hq, d]
+    out, err, out_ref = cache.decode(layer, probe=ProbeRef(heads, k_ref, v_ref))
+    codes, offsets = cache.route(phi, u, theta)
+"""
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import binding
+from .binding import DwkvError, F16, BF16
+
+__all__ = ["DeviceCache", "ProbeRef", "DwkvError", "load", "F16", "BF16"]
+
+
+def load():
+    return binding.load()
+
+
+def _ptr(t):
+    return C.c_void_p(t.data_ptr()) if t is not None else C.c_void_p(0)
+
+
+def _stream(torch, device):
+    return C.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+@dataclass
+class ProbeRef:
+    """Dense higher-fidelity reference cache for Eq. 3 (fp16 [n][T][d] device tensors)."""
+    kv_heads: list
+    k_ref: object
+    v_ref: object
+    eps: float = 1e-6
+
+
+class DeviceCache:
+    """One factorized cache resident on the GPU in the C-ABI layout.
+
+    ``host`` is any object carrying the layout arrays (basis, coef, rank_code,
+    res_off, res_idx, res_val, res_scale, q_bits, cu_seqlens, levels, ...), for
+    example a synthetic cache from ``synth.generate``."""
+
+    def __init__(self, host, device: str = "cuda", split_tokens: int = 0):
+        import torch
+        self.torch = torch
+        self.lib = binding.load()
+        self.device = torch.device(device)
+        dev = self.device
+        up = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).view(dt).to(dev)
+        self.basis = up(host.basis.view(np.uint16), torch.float16)
+        self.coef = up(host.coef.view(np.uint16), torch.float16)
+        self.rank_code = up(host.rank_code, torch.uint8)
+        self.res_off = up(host.res_off.view(np.int32), torch.int32)
+        self.res_idx = up(host.res_idx, torch.uint8)
+        self.res_val = up(host.res_val, torch.uint8)
+        self.res_scale = up(host.res_scale.view(np.uint16), torch.float16)
+        self.q_dtype = host.q_dtype
+        qdt = torch.float16 if host.q_dtype == "f16" else torch.bfloat16
+        self.q = up(host.q_bits.view(np.int16), torch.int16).view(qdt)
+        self.cu_host = np.ascontiguousarray(host.cu_seqlens, dtype=np.int32)
+        self.cu = torch.from_numpy(self.cu_host).to(dev)
+        self.batch = len(self.cu_host) - 1
+        self.n_layers = host.n_layers
+        self.window = host.window
+        self.n_kv_heads = host.n_kv_heads
+        self.n_q_heads = host.n_q_heads
+        self.head_dim = host.head_dim
+        self.basis_rank = host.basis_rank
+        self.levels = tuple(host.levels)
+        self.total_tokens = int(self.cu_host[-1])
+        self.res_stride = int(host.res_stride)
+        self.set_split(split_tokens)
+
+    # -- descriptors -----------------------------------------------------------------
+    def set_split(self, split_tokens: int):
+        self.dims, self._cu_keep = binding.make_dims(
+            batch=self.batch, n_layers=self.n_layers, window=self.window,
+            n_kv_heads=self.n_kv_heads, n_q_heads=self.n_q_heads, head_dim=self.head_dim,
+            basis_rank=self.basis_rank, levels=self.levels, cu_seqlens_host=self.cu_host,
+            cu_seqlens_dev_ptr=self.cu.data_ptr(), total_tokens=self.total_tokens,
+            res_stride=self.res_stride, split_tokens=split_tokens)
+        c = binding.Cache()
+        c.basis, c.coef, c.rank_code = self.basis.data_ptr(), self.coef.data_ptr(), self.rank_code.data_ptr()
+        c.res_off, c.res_idx, c.res_val = self.res_off.data_ptr(), self.res_idx.data_ptr(), self.res_val.data_ptr()
+        c.res_scale = self.res_scale.data_ptr()
+        self.cstruct = c
+        self._ws = None
+
+    @property
+    def split_tokens(self) -> int:
+        return int(self.lib.dwkv_split_tokens(C.byref(self.dims)))
+
+    def _probe_struct(self, probe: ProbeRef | None, err, out_ref):
+        if probe is None:
+            return None, None
+        heads = np.ascontiguousarray(probe.kv_heads, dtype=np.int32)
+        p = binding.Probe()
+        p.n_heads = len(heads)
+        p.kv_heads_host = heads.ctypes.data_as(C.POINTER(C.c_int32))
+        p.k_ref, p.v_ref = probe.k_ref.data_ptr(), probe.v_ref.data_ptr()
+        p.eps = probe.eps
+        p.err = err.data_ptr()
+        p.out_ref = out_ref.data_ptr() if out_ref is not None else None
+        return p, heads
+
+    def workspace_bytes(self, probe: ProbeRef | None = None) -> int:
+        torch = self.torch
+        G = self.n_q_heads // self.n_kv_heads
+        err = torch.empty(1, device=self.device)
+        p, keep = self._probe_struct(probe, err, None)
+        n = self.lib.dwkv_workspace_bytes(C.byref(self.dims), C.byref(p) if p is not None else None)
+        if n == 0:
+            raise DwkvError(2, "dwkv_workspace_bytes")
+        return int(n)
+
+    def workspace(self, probe: ProbeRef | None = None):
+        need = self.workspace_bytes(probe)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = self.torch.empty(need, dtype=self.torch.uint8, device=self.device)
+        return self._ws
+
+    # -- calls -----------------------------------------------------------------------
+    def decode(self, layer: int, q=None, sm_scale: float | None = None, probe: ProbeRef | None = None,
+               out=None, workspace=None, with_ref: bool = True):
+        """Per-layer decode attention; returns out [B,Hq,d] fp32, or
+        (out, err [B, n*G], out_ref [B, n*G, d]) with a probe."""
+        torch = self.torch
+        if q is None:
+            q = self.q[layer]
+        qt = F16 if q.dtype == torch.float16 else BF16
+        if q.dtype not in (torch.float16, torch.bfloat16):
+            raise TypeError("q must be float16 or bfloat16")
+        B, Hq, d = self.batch, self.n_q_heads, self.head_dim
+        if out is None:
+            out = torch.empty((B, Hq, d), dtype=torch.float32, device=self.device)
+        G = Hq // self.n_kv_heads
+        err = out_ref = None
+        if probe is not None:
+            n = len(probe.kv_heads)
+            err = torch.empty((B, n * G), dtype=torch.float32, device=self.device)
+            out_ref = torch.empty((B, n * G, d), dtype=torch.float32, device=self.device) if with_ref else None
+        p, keep = self._probe_struct(probe, err, out_ref)
+        ws = workspace if workspace is not None else self.workspace(probe)
+        st = self.lib.dwkv_decode(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(q), qt,
+                                  float(sm_scale or 0.0), _ptr(out), C.byref(p) if p is not None else None,
+                                  _ptr(ws), ws.numel(), _stream(torch, self.device))
+        binding.check(st, "dwkv_decode")
+        return out if probe is None else (out, err, out_ref)
+
+    def route(self, phi, u, theta, rank_code=None, res_off=None):
+        """Eq. 2 routing on the GPU; returns (rank_code uint8 [M,Hkv,T], res_off int32-view [M,Hkv,T+1])."""
+        torch = self.torch
+        M, Hk, T = self.n_layers // self.window, self.n_kv_heads, self.total_tokens
+        if rank_code is None:
+            rank_code = torch.empty((M, Hk, T), dtype=torch.uint8, device=self.device)
+        if res_off is None:
+            res_off = torch.empty((M, Hk, T + 1), dtype=torch.int32, device=self.device)
+        need = self.lib.dwkv_route_workspace_bytes(C.byref(self.dims))
+        ws = torch.empty(max(int(need), 1), dtype=torch.uint8, device=self.device)
+        st = self.lib.dwkv_route(C.byref(self.dims), _ptr(phi), _ptr(u), _ptr(theta), _ptr(rank_code),
+                                 _ptr(res_off), _ptr(ws), ws.numel(), _stream(torch, self.device))
+        binding.check(st, "dwkv_route")
+        return rank_code, res_off
+
+    def residual_map(self, layer: int, z: int, kv_head: int, t0: int, t1: int):
+        torch = self.torch
+        dense = torch.empty((max(t1 - t0, 0), self.head_dim), dtype=torch.float32, device=self.device)
+        st = self.lib.dwkv_residual_map(C.byref(self.dims), C.byref(self.cstruct), int(layer), int(z),
+                                        int(kv_head), int(t0), int(t1), _ptr(dense),
+                                        _stream(torch, self.device))
+        binding.check(st, "dwkv_residual_map")
+        return dense
+
+    def validate(self):
+        """Returns (ok, bad_index); raises on argument errors."""
+        torch = self.torch
+        ws = torch.empty(int(self.lib.dwkv_validate_workspace_bytes()), dtype=torch.uint8, device=self.device)
+        bad = C.c_int64(-1)
+        st = self.lib.dwkv_validate(C.byref(self.dims), C.byref(self.cstruct), C.byref(bad), _ptr(ws),
+                                    ws.numel(), _stream(torch, self.device))
+        if st == 5:
+            return False, int(bad.value)
+        binding.check(st, "dwkv_validate")
+        return True, -1

@@ -1,0 +1,112 @@
+"""ctypes binding of libdwkv.so: argument marshalling only.
+
+Every computation runs in the library's HIP kernels; torch supplies device
+memory and the current stream.  Loading fails loudly when the library is
+missing -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "_lib", "libdwkv.so")
+
+MAX_LEVELS = 8
+MAX_PROBE_HEADS = 64
+F16, BF16 = 0, 1
+
+STATUS = {0: "ok", 1: "null pointer", 2: "inconsistent dimensions", 3: "unsupported shape",
+          4: "workspace too small", 5: "malformed cache layout", 6: "HIP runtime error"}
+
+
+class DwkvError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {STATUS.get(status, status)} (status {status})")
+        self.status = status
+
+
+class Dims(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("n_layers", C.c_int32), ("window", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("n_q_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("basis_rank", C.c_int32), ("n_levels", C.c_int32),
+                ("levels", C.c_int32 * MAX_LEVELS),
+                ("cu_seqlens_host", C.POINTER(C.c_int32)), ("cu_seqlens", C.c_void_p),
+                ("total_tokens", C.c_int64), ("res_stride", C.c_int64),
+                ("split_tokens", C.c_int32), ("reserved", C.c_int32)]
+
+
+class Cache(C.Structure):
+    _fields_ = [("basis", C.c_void_p), ("coef", C.c_void_p), ("rank_code", C.c_void_p),
+                ("res_off", C.c_void_p), ("res_idx", C.c_void_p), ("res_val", C.c_void_p),
+                ("res_scale", C.c_void_p)]
+
+
+class Probe(C.Structure):
+    _fields_ = [("n_heads", C.c_int32), ("kv_heads_host", C.POINTER(C.c_int32)),
+                ("k_ref", C.c_void_p), ("v_ref", C.c_void_p), ("eps", C.c_float),
+                ("err", C.c_void_p), ("out_ref", C.c_void_p)]
+
+
+EXPORTS = ["dwkv_abi_version", "dwkv_status_str", "dwkv_split_tokens", "dwkv_workspace_bytes",
+           "dwkv_decode", "dwkv_route_workspace_bytes", "dwkv_route", "dwkv_residual_map",
+           "dwkv_validate_workspace_bytes", "dwkv_validate"]
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libdwkv.so (raises when it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with paper_2607_06523_amd.build.build()")
+    lib = C.CDLL(path)
+    P = C.POINTER
+    lib.dwkv_abi_version.restype = C.c_int32
+    lib.dwkv_status_str.restype = C.c_char_p
+    lib.dwkv_status_str.argtypes = [C.c_int]
+    lib.dwkv_split_tokens.restype = C.c_int32
+    lib.dwkv_split_tokens.argtypes = [P(Dims)]
+    lib.dwkv_workspace_bytes.restype = C.c_size_t
+    lib.dwkv_workspace_bytes.argtypes = [P(Dims), P(Probe)]
+    lib.dwkv_decode.restype = C.c_int
+    lib.dwkv_decode.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_void_p, C.c_int32, C.c_float,
+                                C.c_void_p, P(Probe), C.c_void_p, C.c_size_t, C.c_void_p]
+    lib.dwkv_route_workspace_bytes.restype = C.c_size_t
+    lib.dwkv_route_workspace_bytes.argtypes = [P(Dims)]
+    lib.dwkv_route.restype = C.c_int
+    lib.dwkv_route.argtypes = [P(Dims), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                               C.c_void_p, C.c_size_t, C.c_void_p]
+    lib.dwkv_residual_map.restype = C.c_int
+    lib.dwkv_residual_map.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_int32, C.c_int32, C.c_int64,
+                                      C.c_int64, C.c_void_p, C.c_void_p]
+    lib.dwkv_validate_workspace_bytes.restype = C.c_size_t
+    lib.dwkv_validate.restype = C.c_int
+    lib.dwkv_validate.argtypes = [P(Dims), P(Cache), P(C.c_int64), C.c_void_p, C.c_size_t, C.c_void_p]
+    _lib = lib
+    return lib
+
+
+def check(status: int, where: str):
+    if status != 0:
+        raise DwkvError(status, where)
+
+
+def make_dims(*, batch, n_layers, window, n_kv_heads, n_q_heads, head_dim, basis_rank, levels,
+              cu_seqlens_host, cu_seqlens_dev_ptr, total_tokens, res_stride, split_tokens=0):
+    """Fill a Dims struct; returns (dims, keepalive) -- keep both alive while in use."""
+    cu = np.ascontiguousarray(cu_seqlens_host, dtype=np.int32)
+    d = Dims()
+    d.batch, d.n_layers, d.window = batch, n_layers, window
+    d.n_kv_heads, d.n_q_heads, d.head_dim, d.basis_rank = n_kv_heads, n_q_heads, head_dim, basis_rank
+    d.n_levels = len(levels)
+    for i, v in enumerate(levels[:MAX_LEVELS]):
+        d.levels[i] = int(v)
+    d.cu_seqlens_host = cu.ctypes.data_as(C.POINTER(C.c_int32))
+    d.cu_seqlens = cu_seqlens_dev_ptr
+    d.total_tokens, d.res_stride, d.split_tokens = total_tokens, res_stride, split_tokens
+    return d, cu

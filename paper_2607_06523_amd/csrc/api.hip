@@ -1,0 +1,302 @@
+// C ABI of the library: argument checks, split planning, launches.
+#include <cmath>
+#include <cstring>
+
+#include "internal.h"
+
+using namespace dwkv;
+
+namespace {
+
+constexpr int kTargetWorkgroups = 512;   // ~2 decode workgroups per compute unit
+constexpr int kSplitQuantum = 256;       // automatic chunks are multiples of this
+constexpr int kSplitMax = 8192;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool is_pow2_group(int g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
+
+int max_level(const dwkv_dims* d) {
+  int mx = 0;
+  for (int i = 0; i < d->n_levels; ++i) mx = d->levels[i] > mx ? d->levels[i] : mx;
+  return mx;
+}
+
+// Shape checks shared by every entry point.
+dwkv_status check_dims(const dwkv_dims* d) {
+  if (!d) return DWKV_E_NULL;
+  if (d->batch < 1 || d->n_layers < 1 || d->window < 1 || d->n_kv_heads < 1 || d->n_q_heads < 1 ||
+      d->n_levels < 1 || d->total_tokens < 0 || d->split_tokens < 0)
+    return DWKV_E_DIMS;
+  if (d->n_layers % d->window != 0 || d->n_q_heads % d->n_kv_heads != 0) return DWKV_E_DIMS;
+  if (d->n_levels > DWKV_MAX_LEVELS) return DWKV_E_UNSUPPORTED;
+  if (d->head_dim != kHeadDim) return DWKV_E_UNSUPPORTED;
+  if (!is_pow2_group(d->n_q_heads / d->n_kv_heads)) return DWKV_E_UNSUPPORTED;
+  if (d->n_kv_heads > DWKV_MAX_PROBE_HEADS) return DWKV_E_UNSUPPORTED;
+  if (d->basis_rank < 16 || d->basis_rank > 128 || d->basis_rank % 16 != 0) return DWKV_E_UNSUPPORTED;
+  for (int i = 0; i < d->n_levels; ++i) {
+    const int lv = d->levels[i];
+    if (lv < 0 || lv > d->head_dim || (lv & 1)) return DWKV_E_DIMS;
+    if (i > 0 && lv <= d->levels[i - 1]) return DWKV_E_DIMS;
+  }
+  if (!d->cu_seqlens_host || !d->cu_seqlens) return DWKV_E_NULL;
+  if (d->cu_seqlens_host[0] != 0) return DWKV_E_DIMS;
+  for (int b = 0; b < d->batch; ++b)
+    if (d->cu_seqlens_host[b + 1] < d->cu_seqlens_host[b]) return DWKV_E_DIMS;
+  if ((int64_t)d->cu_seqlens_host[d->batch] != d->total_tokens) return DWKV_E_DIMS;
+  if (d->res_stride < kResTailPad || d->res_stride % 256 != 0) return DWKV_E_DIMS;
+  if (d->split_tokens % 64 != 0) return DWKV_E_DIMS;
+  // offsets, plus a few chunks of slack, must stay inside 32 bits
+  if ((double)d->total_tokens * (double)max_level(d) + 65536.0 > 4294967295.0) return DWKV_E_UNSUPPORTED;
+  return DWKV_OK;
+}
+
+int plan_split(const dwkv_dims* d) {
+  if (d->split_tokens > 0) return d->split_tokens;
+  const int64_t work = d->total_tokens * d->n_kv_heads;
+  int64_t c = (work + kTargetWorkgroups - 1) / kTargetWorkgroups;
+  c = (c + kSplitQuantum - 1) / kSplitQuantum * kSplitQuantum;
+  if (c < kSplitQuantum) c = kSplitQuantum;
+  if (c > kSplitMax) c = kSplitMax;
+  return (int)c;
+}
+
+int64_t count_work(const dwkv_dims* d, int split) {
+  int64_t n = 0;
+  for (int b = 0; b < d->batch; ++b) {
+    const int64_t tb = d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b];
+    n += (tb + split - 1) / split;
+  }
+  return n;
+}
+
+dwkv_status check_probe(const dwkv_dims* d, const dwkv_probe* p) {
+  if (!p) return DWKV_OK;
+  if (p->n_heads < 1 || p->n_heads > d->n_kv_heads || p->n_heads > DWKV_MAX_PROBE_HEADS) return DWKV_E_DIMS;
+  if (!p->kv_heads_host || !p->k_ref || !p->v_ref || !p->err) return DWKV_E_NULL;
+  bool seen[DWKV_MAX_PROBE_HEADS] = {};
+  for (int i = 0; i < p->n_heads; ++i) {
+    const int h = p->kv_heads_host[i];
+    if (h < 0 || h >= d->n_kv_heads || seen[h]) return DWKV_E_DIMS;
+    seen[h] = true;
+  }
+  if (!(p->eps >= 0.f)) return DWKV_E_DIMS;
+  return DWKV_OK;
+}
+
+struct WsLayout {
+  size_t main_bytes, ref_bytes, total;
+};
+
+WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
+  const int split = plan_split(d);
+  const int64_t nw = count_work(d, split);
+  const int g = d->n_q_heads / d->n_kv_heads;
+  WsLayout w;
+  w.main_bytes = align_up((size_t)nw * d->n_kv_heads * g * kPartStride * sizeof(float), 256);
+  w.ref_bytes = p ? align_up((size_t)nw * p->n_heads * g * kPartStride * sizeof(float), 256) : 0;
+  w.total = w.main_bytes + w.ref_bytes;
+  if (w.total == 0) w.total = 256;
+  return w;
+}
+
+dwkv_status hip_status(hipError_t e) { return e == hipSuccess ? DWKV_OK : DWKV_E_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t dwkv_abi_version(void) { return DWKV_ABI_VERSION; }
+
+const char* dwkv_status_str(dwkv_status s) {
+  switch (s) {
+    case DWKV_OK: return "ok";
+    case DWKV_E_NULL: return "null pointer";
+    case DWKV_E_DIMS: return "inconsistent dimensions";
+    case DWKV_E_UNSUPPORTED: return "unsupported shape";
+    case DWKV_E_WORKSPACE: return "workspace too small";
+    case DWKV_E_LAYOUT: return "malformed cache layout";
+    case DWKV_E_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+int32_t dwkv_split_tokens(const dwkv_dims* dims) {
+  if (check_dims(dims) != DWKV_OK) return -1;
+  return plan_split(dims);
+}
+
+size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe) {
+  if (check_dims(dims) != DWKV_OK || check_probe(dims, probe) != DWKV_OK) return 0;
+  return ws_layout(dims, probe).total;
+}
+
+dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
+                        int32_t q_type, float sm_scale, float* out, const dwkv_probe* probe,
+                        void* workspace, size_t ws_bytes, void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (!c || !q || !out || !workspace) return DWKV_E_NULL;
+  if (!c->basis || !c->coef || !c->res_off || !c->res_idx || !c->res_val || !c->res_scale)
+    return DWKV_E_NULL;
+  if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
+  if (q_type != DWKV_F16 && q_type != DWKV_BF16) return DWKV_E_DIMS;
+  if ((st = check_probe(d, probe)) != DWKV_OK) return st;
+  const WsLayout wl = ws_layout(d, probe);
+  if (ws_bytes < wl.total) return DWKV_E_WORKSPACE;
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int G = d->n_q_heads / d->n_kv_heads;
+  const int RB = d->basis_rank;
+  const int64_t T = d->total_tokens;
+  const int64_t Hk = d->n_kv_heads;
+  const int M = d->n_layers / d->window;
+  const int m = layer / d->window;
+  const int split = plan_split(d);
+  const int64_t nw = count_work(d, split);
+  if (nw > 0x7fffffff) return DWKV_E_UNSUPPORTED;
+  if (!(sm_scale > 0.f)) sm_scale = 1.0f / std::sqrt((float)kHeadDim);
+
+  const uint16_t* coef = static_cast<const uint16_t*>(c->coef);
+  const uint16_t* scale = static_cast<const uint16_t*>(c->res_scale);
+  float* part = static_cast<float*>(workspace);
+  float* part_ref = reinterpret_cast<float*>(static_cast<char*>(workspace) + wl.main_bytes);
+
+  SplitArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.coef_k = coef + ((int64_t)layer * 2 + 0) * Hk * T * RB;
+  a.coef_v = coef + ((int64_t)layer * 2 + 1) * Hk * T * RB;
+  a.basis = static_cast<const uint16_t*>(c->basis) + (int64_t)m * Hk * 2 * RB * kHeadDim;
+  a.basis_b_stride = (int64_t)M * Hk * 2 * RB * kHeadDim;
+  a.off = c->res_off + (int64_t)m * Hk * (T + 1);
+  a.idx_k = c->res_idx + ((int64_t)layer * 2 + 0) * Hk * d->res_stride;
+  a.idx_v = c->res_idx + ((int64_t)layer * 2 + 1) * Hk * d->res_stride;
+  a.val_k = c->res_val + ((int64_t)layer * 2 + 0) * Hk * (d->res_stride / 2);
+  a.val_v = c->res_val + ((int64_t)layer * 2 + 1) * Hk * (d->res_stride / 2);
+  a.scale_k = scale + ((int64_t)layer * 2 + 0) * Hk * T;
+  a.scale_v = scale + ((int64_t)layer * 2 + 1) * Hk * T;
+  a.q = static_cast<const uint16_t*>(q);
+  a.cu = d->cu_seqlens;
+  a.part = part;
+  a.T = T;
+  a.res_stride = d->res_stride;
+  a.batch = d->batch;
+  a.n_q_heads = d->n_q_heads;
+  a.n_kv_heads = d->n_kv_heads;
+  a.n_slots = d->n_kv_heads;
+  a.split = split;
+  a.q_bf16 = q_type == DWKV_BF16;
+  a.qscale = sm_scale * 1.4426950408889634f;
+  for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
+
+  const bool resid = max_level(d) > 0;
+  if (nw > 0) {
+    hipError_t e = launch_split(RB, G, resid, false, a, (int)nw, s);
+    if (e != hipSuccess) return DWKV_E_HIP;
+    if (probe) {
+      SplitArgs r = a;
+      r.coef_k = static_cast<const uint16_t*>(probe->k_ref);
+      r.coef_v = static_cast<const uint16_t*>(probe->v_ref);
+      r.part = part_ref;
+      r.n_slots = probe->n_heads;
+      for (int i = 0; i < probe->n_heads; ++i) r.kv_of_slot[i] = probe->kv_heads_host[i];
+      e = launch_split(kHeadDim, G, false, true, r, (int)nw, s);
+      if (e != hipSuccess) return DWKV_E_HIP;
+    }
+  }
+  MergeArgs mg;
+  std::memset(&mg, 0, sizeof(mg));
+  mg.part = part;
+  mg.part_ref = probe ? part_ref : nullptr;
+  mg.out = out;
+  mg.err = probe ? probe->err : nullptr;
+  mg.out_ref = probe ? probe->out_ref : nullptr;
+  mg.cu = d->cu_seqlens;
+  mg.batch = d->batch;
+  mg.n_q_heads = d->n_q_heads;
+  mg.n_kv_heads = d->n_kv_heads;
+  mg.split = split;
+  mg.n_probe = probe ? probe->n_heads : 0;
+  mg.eps = probe ? probe->eps : 0.f;
+  for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) mg.probe_slot_of_kv[h] = -1;
+  if (probe)
+    for (int i = 0; i < probe->n_heads; ++i) mg.probe_slot_of_kv[probe->kv_heads_host[i]] = i;
+  return hip_status(launch_merge(mg, s));
+}
+
+size_t dwkv_route_workspace_bytes(const dwkv_dims* d) {
+  if (check_dims(d) != DWKV_OK) return 0;
+  const int64_t nblk = (d->total_tokens + kRouteTokensPerBlock - 1) / kRouteTokensPerBlock;
+  const int64_t n_mh = (int64_t)(d->n_layers / d->window) * d->n_kv_heads;
+  const size_t b = align_up((size_t)(nblk > 0 ? nblk : 1) * n_mh * sizeof(uint32_t), 256);
+  return 2 * b;
+}
+
+dwkv_status dwkv_route(const dwkv_dims* d, const float* phi, const float* u, const float* theta,
+                       uint8_t* rank_code, uint32_t* res_off, void* workspace, size_t ws_bytes,
+                       void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (!u || !res_off || !workspace || !rank_code) return DWKV_E_NULL;
+  if (d->total_tokens > 0 && !phi) return DWKV_E_NULL;
+  if (d->n_levels > 1 && !theta) return DWKV_E_NULL;
+  const size_t need = dwkv_route_workspace_bytes(d);
+  if (ws_bytes < need) return DWKV_E_WORKSPACE;
+  const int64_t nblk = (d->total_tokens + kRouteTokensPerBlock - 1) / kRouteTokensPerBlock;
+  const int n_mh = (d->n_layers / d->window) * d->n_kv_heads;
+  if (nblk > 0x7fffffff) return DWKV_E_UNSUPPORTED;
+  RouteArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.phi = phi;
+  a.u = u;
+  a.theta = theta;
+  a.code = rank_code;
+  a.off = res_off;
+  a.bsum = static_cast<uint32_t*>(workspace);
+  a.bpre = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + need / 2);
+  a.T = d->total_tokens;
+  a.n_kv_heads = d->n_kv_heads;
+  a.n_levels = d->n_levels;
+  a.nblk = (int)nblk;
+  for (int i = 0; i < DWKV_MAX_LEVELS; ++i) a.levels[i] = i < d->n_levels ? d->levels[i] : 0;
+  return hip_status(launch_route(a, n_mh, reinterpret_cast<hipStream_t>(stream)));
+}
+
+dwkv_status dwkv_residual_map(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, int32_t z,
+                              int32_t kv_head, int64_t t0, int64_t t1, float* dense, void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (!c || !dense || !c->res_off || !c->res_idx || !c->res_val || !c->res_scale) return DWKV_E_NULL;
+  if (layer < 0 || layer >= d->n_layers || z < 0 || z > 1 || kv_head < 0 || kv_head >= d->n_kv_heads)
+    return DWKV_E_DIMS;
+  if (t0 < 0 || t1 < t0 || t1 > d->total_tokens) return DWKV_E_DIMS;
+  const int64_t T = d->total_tokens, Hk = d->n_kv_heads;
+  const int m = layer / d->window;
+  const int64_t slab = ((int64_t)layer * 2 + z) * Hk + kv_head;
+  return hip_status(launch_residual_map(
+      c->res_off + ((int64_t)m * Hk + kv_head) * (T + 1), c->res_idx + slab * d->res_stride,
+      c->res_val + slab * (d->res_stride / 2), static_cast<const uint16_t*>(c->res_scale) + slab * T,
+      t0, t1, d->res_stride, dense, reinterpret_cast<hipStream_t>(stream)));
+}
+
+size_t dwkv_validate_workspace_bytes(void) { return 256; }
+
+dwkv_status dwkv_validate(const dwkv_dims* d, const dwkv_cache* c, int64_t* bad_index, void* workspace,
+                          size_t ws_bytes, void* stream) {
+  if (bad_index) *bad_index = -1;
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (!c || !c->rank_code || !c->res_off || !c->res_idx || !c->res_val || !workspace) return DWKV_E_NULL;
+  if (ws_bytes < dwkv_validate_workspace_bytes()) return DWKV_E_WORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  unsigned long long* bad = static_cast<unsigned long long*>(workspace);
+  if (launch_validate(d, c, bad, s) != hipSuccess) return DWKV_E_HIP;
+  unsigned long long host = 0;
+  if (hipMemcpyAsync(&host, bad, sizeof(host), hipMemcpyDeviceToHost, s) != hipSuccess) return DWKV_E_HIP;
+  if (hipStreamSynchronize(s) != hipSuccess) return DWKV_E_HIP;
+  if (host == ~0ull) return DWKV_OK;
+  if (bad_index) *bad_index = (int64_t)host;
+  return DWKV_E_LAYOUT;
+}
+
+}  // extern "C"

@@ -1,0 +1,237 @@
+// Router (Eq. 2) with its residual-offset scan, the residual-map test hook and
+// the layout validator (gfx950).
+#include "entry.h"
+#include "internal.h"
+
+namespace dwkv {
+namespace {
+
+constexpr int D = kHeadDim;
+constexpr int kRT = 256;                                  // route block threads
+constexpr int kPerThread = kRouteTokensPerBlock / kRT;   // 4 tokens per thread
+
+// Router score, float32, left to right, each product and sum rounded on its own
+// (no fused multiply-add), so it reproduces bit for bit on any IEEE machine.
+__device__ __forceinline__ float router_score(const float4 u, const float4 f) {
+#pragma clang fp contract(off)
+  float z = u.x * f.x;
+  z = z + u.y * f.y;
+  z = z + u.z * f.z;
+  z = z + u.w * f.w;
+  return z;
+}
+
+__device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* red) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (lane == 0) red[wv] = v;
+  __syncthreads();
+  uint32_t t = 0;
+  for (int i = 0; i < kRT / 64; ++i) t += red[i];
+  return t;
+}
+
+// Exclusive prefix over the block's threads (kRT threads); returns the block total in *total.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* red, uint32_t* total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  uint32_t inc = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t n = __shfl_up(inc, o);
+    if (lane >= o) inc += n;
+  }
+  if (lane == 63) red[wv] = inc;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+  for (int i = 0; i < kRT / 64; ++i) {
+    if (i < wv) before += red[i];
+    all += red[i];
+  }
+  *total = all;
+  return before + inc - v;
+}
+
+// Level codes and per-block rank sums.  grid (nblk, M*Hkv)
+__global__ __launch_bounds__(kRT) void route_codes_kernel(const RouteArgs a) {
+  __shared__ uint32_t red[kRT / 64];
+  const int mh = blockIdx.y;
+  const int m = mh / a.n_kv_heads;
+  const float4 u = *reinterpret_cast<const float4*>(a.u + 4 * m);
+  const int nth = a.n_levels - 1;
+  float th[DWKV_MAX_LEVELS - 1];
+#pragma unroll
+  for (int j = 0; j < DWKV_MAX_LEVELS - 1; ++j) th[j] = j < nth ? a.theta[m * nth + j] : 0.f;
+  uint32_t sum = 0;
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    const int64_t t = (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
+    if (t < a.T) {
+      const float4 f = *reinterpret_cast<const float4*>(a.phi + ((int64_t)mh * a.T + t) * 4);
+      const float z = router_score(u, f);
+      int k = 0;
+#pragma unroll
+      for (int j = 0; j < DWKV_MAX_LEVELS - 1; ++j) k += (j < nth && z > th[j]) ? 1 : 0;
+      a.code[(int64_t)mh * a.T + t] = (uint8_t)k;
+      sum += (uint32_t)a.levels[k];
+    }
+  }
+  const uint32_t tot = block_sum(sum, red);
+  if (threadIdx.x == 0) a.bsum[(int64_t)mh * a.nblk + blockIdx.x] = tot;
+}
+
+// Exclusive scan of the block sums of one (window, head).  grid (M*Hkv)
+__global__ __launch_bounds__(kRT) void route_block_scan_kernel(const RouteArgs a) {
+  __shared__ uint32_t red[kRT / 64];
+  const int mh = blockIdx.x;
+  uint32_t carry = 0;
+  for (int b0 = 0; b0 < a.nblk; b0 += kRT) {
+    const int b = b0 + threadIdx.x;
+    const uint32_t v = b < a.nblk ? a.bsum[(int64_t)mh * a.nblk + b] : 0u;
+    uint32_t total;
+    const uint32_t ex = block_exclusive_scan(v, red, &total);
+    if (b < a.nblk) a.bpre[(int64_t)mh * a.nblk + b] = carry + ex;
+    carry += total;
+    __syncthreads();
+  }
+}
+
+// Offsets: off[t+1] = (block prefix) + (ranks of earlier tokens in the block) + rho_t.
+__global__ __launch_bounds__(kRT) void route_offsets_kernel(const RouteArgs a) {
+  __shared__ uint32_t red[kRT / 64];
+  const int mh = blockIdx.y;
+  uint32_t rho[kPerThread];
+  uint32_t mine = 0;
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    const int64_t t = (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
+    rho[i] = t < a.T ? (uint32_t)a.levels[a.code[(int64_t)mh * a.T + t]] : 0u;
+    mine += rho[i];
+  }
+  uint32_t total;
+  uint32_t run = (a.nblk > 0 ? a.bpre[(int64_t)mh * a.nblk + blockIdx.x] : 0u) +
+                 block_exclusive_scan(mine, red, &total);
+  uint32_t* off = a.off + (int64_t)mh * (a.T + 1);
+  if (blockIdx.x == 0 && threadIdx.x == 0) off[0] = 0u;
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    const int64_t t = (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
+    run += rho[i];
+    if (t < a.T) off[t + 1] = run;
+  }
+}
+
+// One thread per token: dense g*R row of the token.
+__global__ __launch_bounds__(256) void residual_map_kernel(const uint32_t* off, const uint8_t* idx,
+                                                           const uint8_t* val, const uint16_t* scale,
+                                                           int64_t t0, int64_t t1, int64_t slab_len,
+                                                           float* dense) {
+  const int64_t t = t0 + (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= t1) return;
+  float* row = dense + (t - t0) * D;
+  for (int c = 0; c < D; ++c) row[c] = 0.f;
+  const float s = half_bits_to_float(scale[t]);
+  const int64_t e0 = off[t], e1 = off[t + 1];
+  const int64_t end = min(min(e1, e0 + D), slab_len);   // bounded even for a corrupt table
+  for (int64_t e = e0; e < end; ++e)
+    row[idx[e] & (D - 1)] = s * (float)entry_code(val[e >> 1], e);
+}
+
+struct ValidateArgs {
+  const uint8_t* code;
+  const uint32_t* off;
+  const uint8_t* idx;
+  const uint8_t* val;
+  unsigned long long* bad;
+  int64_t T, res_stride;
+  int32_t n_kv_heads, window, n_levels;
+  int32_t levels[DWKV_MAX_LEVELS];
+};
+
+__device__ __forceinline__ void report(unsigned long long* bad, int64_t mh, int64_t T, int64_t t, int kind) {
+  atomicMin(bad, (unsigned long long)(((mh * (T + 1) + t) << 3) | kind));
+}
+
+__global__ void fill_u64_kernel(unsigned long long* p, unsigned long long v) { *p = v; }
+
+// grid (ceil((T+1)/256), M*Hkv)
+__global__ __launch_bounds__(256) void validate_kernel(const ValidateArgs a) {
+  const int64_t mh = blockIdx.y;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t > a.T) return;
+  const uint32_t* off = a.off + mh * (a.T + 1);
+  if (t == a.T) {              // global checks ride on the extra thread
+    if (off[0] != 0u || (int64_t)off[a.T] + kResTailPad > a.res_stride) report(a.bad, mh, a.T, t, 7);
+    return;
+  }
+  const uint32_t o0 = off[t], o1 = off[t + 1];
+  const uint32_t k = a.code[mh * a.T + t];
+  if (k >= (uint32_t)a.n_levels) { report(a.bad, mh, a.T, t, 2); return; }
+  if (o1 < o0 || o1 - o0 != (uint32_t)a.levels[k]) { report(a.bad, mh, a.T, t, 1); return; }
+  if ((int64_t)o1 > a.res_stride) { report(a.bad, mh, a.T, t, 7); return; }
+  const int m = (int)(mh / a.n_kv_heads), h = (int)(mh % a.n_kv_heads);
+  for (int li = 0; li < a.window; ++li) {
+    const int l = m * a.window + li;
+    for (int z = 0; z < 2; ++z) {
+      const int64_t slab = ((int64_t)(l * 2 + z) * a.n_kv_heads + h);
+      const uint8_t* ix = a.idx + slab * a.res_stride;
+      const uint8_t* vl = a.val + slab * (a.res_stride / 2);
+      uint32_t seen[4] = {0u, 0u, 0u, 0u};
+      int prev_abs = 8, prev_c = -1;
+      for (uint32_t e = o0; e < o1; ++e) {
+        const int c = ix[e];
+        if (c >= D) { report(a.bad, mh, a.T, t, 3); return; }
+        if (seen[c >> 5] & (1u << (c & 31))) { report(a.bad, mh, a.T, t, 4); return; }
+        seen[c >> 5] |= 1u << (c & 31);
+        const int code = entry_code(vl[e >> 1], e);
+        if (code == -8) { report(a.bad, mh, a.T, t, 5); return; }
+        const int ab = code < 0 ? -code : code;
+        if (ab > prev_abs || (ab == prev_abs && c < prev_c)) { report(a.bad, mh, a.T, t, 6); return; }
+        prev_abs = ab;
+        prev_c = c;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_route(const RouteArgs& a, int n_mh, hipStream_t s) {
+  const int nb = a.nblk > 0 ? a.nblk : 1;
+  if (a.nblk > 0) {
+    hipLaunchKernelGGL(route_codes_kernel, dim3(a.nblk, n_mh), dim3(kRT), 0, s, a);
+    hipLaunchKernelGGL(route_block_scan_kernel, dim3(n_mh), dim3(kRT), 0, s, a);
+  }
+  hipLaunchKernelGGL(route_offsets_kernel, dim3(nb, n_mh), dim3(kRT), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_residual_map(const uint32_t* off, const uint8_t* idx, const uint8_t* val,
+                               const uint16_t* scale, int64_t t0, int64_t t1, int64_t slab_len,
+                               float* dense, hipStream_t s) {
+  const int64_t n = t1 - t0;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(residual_map_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, off,
+                     idx, val, scale, t0, t1, slab_len, dense);
+  return hipGetLastError();
+}
+
+hipError_t launch_validate(const dwkv_dims* d, const dwkv_cache* c, unsigned long long* bad,
+                           hipStream_t s) {
+  ValidateArgs a;
+  a.code = c->rank_code;
+  a.off = c->res_off;
+  a.idx = c->res_idx;
+  a.val = c->res_val;
+  a.bad = bad;
+  a.T = d->total_tokens;
+  a.res_stride = d->res_stride;
+  a.n_kv_heads = d->n_kv_heads;
+  a.window = d->window;
+  a.n_levels = d->n_levels;
+  for (int i = 0; i < DWKV_MAX_LEVELS; ++i) a.levels[i] = d->levels[i];
+  const int n_mh = (d->n_layers / d->window) * d->n_kv_heads;
+  hipLaunchKernelGGL(fill_u64_kernel, dim3(1), dim3(1), 0, s, bad, ~0ull);
+  hipLaunchKernelGGL(validate_kernel, dim3((unsigned)((a.T + 1 + 255) / 256), n_mh), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace dwkv

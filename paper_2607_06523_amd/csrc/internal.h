@@ -1,0 +1,88 @@
+// Private to the library: kernel argument blocks and launcher entry points.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dwkv.h"
+
+namespace dwkv {
+
+constexpr int kHeadDim = 128;       // d
+constexpr int kWaves = 4;           // waves per decode workgroup
+constexpr int kThreads = 64 * kWaves;
+constexpr int kPartStride = kHeadDim + 4;   // floats per partial: o[d], m, l, pad
+constexpr int kEntChunk = 256;      // residual entries staged per LDS chunk
+constexpr int kResTailPad = 512;    // spare entries required after the longest slab
+
+// One split-K pass over a layer: grid = (work items, head slots).
+struct SplitArgs {
+  const uint16_t* coef_k;      // slot 0 coefficient (or dense reference) rows, keys
+  const uint16_t* coef_v;      // ... values; slot s adds s * T * RB
+  const uint16_t* basis;       // basis of window m, sequence 0: + (b*M*Hkv + h)*2*RB*d
+  int64_t basis_b_stride;      // halves between sequences (M*Hkv*2*RB*d)
+  const uint32_t* off;         // res_off of window m, head 0; head h adds h*(T+1)
+  const uint8_t* idx_k;        // res_idx of (layer, K), head 0; head h adds h*res_stride
+  const uint8_t* idx_v;
+  const uint8_t* val_k;        // res_val of (layer, K), head 0; head h adds h*res_stride/2
+  const uint8_t* val_v;
+  const uint16_t* scale_k;     // res_scale of (layer, K), head 0; head h adds h*T
+  const uint16_t* scale_v;
+  const uint16_t* q;           // [B][Hq][d] fp16 or bf16 bits
+  const int32_t* cu;           // [B+1] device
+  float* part;                 // [work][n_slots][G][kPartStride]
+  int64_t T;
+  int64_t res_stride;
+  int32_t batch;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t n_slots;             // grid.y
+  int32_t split;               // tokens per work item
+  int32_t q_bf16;
+  float qscale;                // sm_scale * log2(e)
+  int32_t kv_of_slot[DWKV_MAX_PROBE_HEADS];
+};
+
+struct MergeArgs {
+  const float* part;           // main partials [work][Hkv][G][kPartStride]
+  const float* part_ref;       // probe partials [work][n_probe][G][kPartStride] or null
+  float* out;                  // [B][Hq][d]
+  float* err;                  // [B][n_probe*G] or null
+  float* out_ref;              // [B][n_probe*G][d] or null
+  const int32_t* cu;
+  int32_t batch;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t split;
+  int32_t n_probe;
+  float eps;
+  int32_t probe_slot_of_kv[DWKV_MAX_PROBE_HEADS];   // -1 when the KV head is not probed
+};
+
+struct RouteArgs {
+  const float* phi;            // [M][Hkv][T][4]
+  const float* u;              // [M][4]
+  const float* theta;          // [M][n_levels-1]
+  uint8_t* code;               // [M][Hkv][T]
+  uint32_t* off;               // [M][Hkv][T+1]
+  uint32_t* bsum;              // [M*Hkv][nblk]
+  uint32_t* bpre;              // [M*Hkv][nblk]
+  int64_t T;
+  int32_t n_kv_heads;
+  int32_t n_levels;
+  int32_t nblk;
+  int32_t levels[DWKV_MAX_LEVELS];
+};
+
+constexpr int kRouteTokensPerBlock = 1024;
+
+hipError_t launch_split(int rb, int g, bool resid, bool ident, const SplitArgs& a, int n_work,
+                        hipStream_t s);
+hipError_t launch_merge(const MergeArgs& a, hipStream_t s);
+hipError_t launch_route(const RouteArgs& a, int n_mh, hipStream_t s);
+hipError_t launch_residual_map(const uint32_t* off, const uint8_t* idx, const uint8_t* val,
+                               const uint16_t* scale, int64_t t0, int64_t t1, int64_t slab_len,
+                               float* dense, hipStream_t s);
+hipError_t launch_validate(const dwkv_dims* dims, const dwkv_cache* c, unsigned long long* bad,
+                           hipStream_t s);
+
+}  // namespace dwkv

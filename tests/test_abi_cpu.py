@@ -1,0 +1,151 @@
+"""The C-ABI library on the CPU: it loads, exports every call include/dwkv.h
+declares, and rejects bad arguments on the host before anything is enqueued
+(no GPU needed: every case returns before the first HIP call)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2607_06523_amd import binding, build
+    if not os.path.exists(binding.LIB_PATH):
+        build.build()
+    return binding.load()
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "dwkv.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dwkv_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = header_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), f"libdwkv.so does not export {n}"
+    from paper_2607_06523_amd import binding
+    assert sorted(binding.EXPORTS) == names
+
+
+def test_abi_version_and_status_strings(lib):
+    assert lib.dwkv_abi_version() == 1
+    for s, text in [(0, b"ok"), (3, b"unsupported shape"), (5, b"malformed cache layout")]:
+        assert lib.dwkv_status_str(s) == text
+
+
+def dims(**kw):
+    from paper_2607_06523_amd import binding
+    base = dict(batch=2, n_layers=4, window=2, n_kv_heads=2, n_q_heads=8, head_dim=128,
+                basis_rank=32, levels=(0, 8, 16), cu_seqlens_host=[0, 1000, 3000],
+                cu_seqlens_dev_ptr=1, total_tokens=3000, res_stride=64 * 1024, split_tokens=0)
+    base.update(kw)
+    return binding.make_dims(**base)
+
+
+FAKE = 1 << 20   # never dereferenced: every call below fails its host-side checks
+
+
+def decode_status(lib, d, layer=0, qtype=0, ws=1 << 30, cache_ok=True, q=FAKE, out=FAKE, probe=None):
+    from paper_2607_06523_amd import binding
+    c = binding.Cache(*([FAKE] * 7)) if cache_ok else binding.Cache(FAKE, 0, FAKE, FAKE, FAKE, FAKE, FAKE)
+    return lib.dwkv_decode(C.byref(d), C.byref(c), layer, q, qtype, 0.0, out,
+                           C.byref(probe) if probe is not None else None, FAKE, ws, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=64), 3),
+    (dict(n_q_heads=7), 2),              # Hq % Hkv != 0
+    (dict(n_q_heads=6), 3),              # G = 3
+    (dict(n_q_heads=64, n_kv_heads=2), 3),   # G = 32
+    (dict(n_kv_heads=65, n_q_heads=65), 3),  # more KV heads than a launch carries
+    (dict(basis_rank=24), 3),
+    (dict(basis_rank=144), 3),
+    (dict(n_layers=5), 2),               # L % w != 0
+    (dict(levels=(0, 3)), 2),            # odd level
+    (dict(levels=(0, 8, 8)), 2),         # not ascending
+    (dict(levels=(0, 130)), 2),          # > d
+    (dict(levels=tuple(range(0, 18, 2))), 3),   # 9 levels
+    (dict(total_tokens=2999), 2),        # cu[B] != T
+    (dict(cu_seqlens_host=[1, 1000, 3000]), 2),
+    (dict(cu_seqlens_host=[0, 3001, 3000]), 2),
+    (dict(res_stride=1000), 2),          # not a multiple of 256
+    (dict(res_stride=256), 2),           # below the tail pad
+    (dict(split_tokens=100), 2),         # not a multiple of 64
+    (dict(batch=0, cu_seqlens_host=[0]), 2),
+    (dict(total_tokens=2**30, cu_seqlens_host=[0, 2**29, 2**30], levels=(0, 8)), 3),  # offsets overflow
+])
+def test_decode_rejects_bad_dims(lib, kw, status):
+    d, keep = dims(**kw)
+    assert decode_status(lib, d) == status
+
+
+def test_decode_rejects_bad_call_arguments(lib):
+    d, keep = dims()
+    assert decode_status(lib, d, layer=4) == 2
+    assert decode_status(lib, d, layer=-1) == 2
+    assert decode_status(lib, d, qtype=2) == 2
+    assert decode_status(lib, d, cache_ok=False) == 1
+    assert decode_status(lib, d, q=0) == 1
+    assert decode_status(lib, d, out=0) == 1
+    need = lib.dwkv_workspace_bytes(C.byref(d), None)
+    assert decode_status(lib, d, ws=need - 1) == 4
+    assert lib.dwkv_decode(None, None, 0, FAKE, 0, 0.0, FAKE, None, FAKE, 1 << 30, None) == 1
+
+
+def test_probe_argument_checks(lib):
+    from paper_2607_06523_amd import binding
+    d, keep = dims()
+    heads = np.array([1, 1], dtype=np.int32)
+    p = binding.Probe(2, heads.ctypes.data_as(C.POINTER(C.c_int32)), FAKE, FAKE, 1e-6, FAKE, 0)
+    assert decode_status(lib, d, probe=p) == 2           # duplicate head
+    heads[:] = [0, 2]
+    assert decode_status(lib, d, probe=p) == 2           # out of range
+    heads[:] = [1, 0]
+    p.err = 0
+    assert decode_status(lib, d, probe=p) == 1
+    p.err = FAKE
+    p.n_heads = 3
+    assert decode_status(lib, d, probe=p) == 2
+    p.n_heads = 2
+    need = lib.dwkv_workspace_bytes(C.byref(d), C.byref(p))
+    assert need > lib.dwkv_workspace_bytes(C.byref(d), None)
+    assert decode_status(lib, d, probe=p, ws=need - 1) == 4
+
+
+def test_workspace_and_split_plan(lib):
+    # automatic chunk: ceil(T*Hkv/512) rounded up to 256, clamped to [256, 8192]
+    for T, Hk, want in [(4096, 2, 256), (32768, 8, 512), (65536, 8, 1024), (262144, 8, 4096),
+                        (10**6, 8, 8192)]:
+        d, keep = dims(cu_seqlens_host=[0, T], batch=1, total_tokens=T, n_kv_heads=Hk, n_q_heads=4 * Hk,
+                       res_stride=T * 16 + 512 + (-(T * 16 + 512)) % 256)
+        assert lib.dwkv_split_tokens(C.byref(d)) == want
+        n_work = -(-T // want)
+        assert lib.dwkv_workspace_bytes(C.byref(d), None) == -(-(n_work * Hk * 4 * 132 * 4) // 256) * 256
+    d, keep = dims(split_tokens=640)
+    assert lib.dwkv_split_tokens(C.byref(d)) == 640
+    # ragged: per-sequence chunk counts, empty sequences contribute none
+    d, keep = dims(batch=3, cu_seqlens_host=[0, 700, 700, 1300], total_tokens=1300, split_tokens=256)
+    assert lib.dwkv_workspace_bytes(C.byref(d), None) == -(-((3 + 3) * 2 * 4 * 132 * 4) // 256) * 256
+
+
+def test_route_and_map_argument_checks(lib):
+    d, keep = dims()
+    assert lib.dwkv_route(C.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, None) == 4
+    need = lib.dwkv_route_workspace_bytes(C.byref(d))
+    assert need > 0
+    assert lib.dwkv_route(C.byref(d), FAKE, 0, FAKE, FAKE, FAKE, FAKE, need, None) == 1
+    from paper_2607_06523_amd import binding
+    c = binding.Cache(*([FAKE] * 7))
+    assert lib.dwkv_residual_map(C.byref(d), C.byref(c), 0, 2, 0, 0, 10, FAKE, None) == 2
+    assert lib.dwkv_residual_map(C.byref(d), C.byref(c), 0, 0, 0, 10, 5, FAKE, None) == 2
+    assert lib.dwkv_residual_map(C.byref(d), C.byref(c), 0, 0, 0, 0, 3001, FAKE, None) == 2
+    bad = C.c_int64(0)
+    assert lib.dwkv_validate(C.byref(d), C.byref(c), C.byref(bad), FAKE, 8, None) == 4
+    assert bad.value == -1

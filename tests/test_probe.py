@@ -1,0 +1,101 @@
+"""Eq. 3 probe error on the GPU (through the C ABI) against the oracle, plus
+its closed forms on a cache whose rebuilt rows are exact in fp16."""
+import numpy as np
+import pytest
+
+import oracle
+import pins
+from gpu_util import announce, compare, device_cache, torch_gpu
+from synth import LLAMA70B_128K, Workload, generate
+
+pytestmark = pytest.mark.gpu
+
+
+def _refs(host, layer, heads, noise, seed):
+    rng = np.random.default_rng(seed)
+    K = np.stack([np.concatenate([oracle.reconstruct(host, layer, 0, h, b) for b in range(host.batch)])
+                  for h in heads])
+    V = np.stack([np.concatenate([oracle.reconstruct(host, layer, 1, h, b) for b in range(host.batch)])
+                  for h in heads])
+    if noise:
+        K = K + rng.normal(0, noise, K.shape)
+        V = V + rng.normal(0, noise, V.shape)
+    return K.astype(np.float16), V.astype(np.float16)
+
+
+def _run_probe(dc, layer, heads, K, V, eps=1e-6):
+    torch = torch_gpu()
+    from paper_2607_06523_amd import ProbeRef
+    pr = ProbeRef(list(heads), torch.from_numpy(K.view(np.uint16)).view(torch.float16).cuda(),
+                  torch.from_numpy(V.view(np.uint16)).view(torch.float16).cuda(), eps)
+    out, err, out_ref = dc.decode(layer, probe=pr)
+    return out.cpu().numpy(), err.cpu().numpy(), out_ref.cpu().numpy()
+
+
+def test_probe_matches_oracle():
+    torch_gpu()
+    w = Workload(name="probe", batch=2, n_layers=2, window=2, n_kv_heads=4, n_q_heads=16,
+                 head_dim=128, context=3000, basis_rank=64, levels=(0, 4, 8, 16, 32),
+                 probs=(0.7, 0.12, 0.1, 0.06, 0.02), q_dtype="bf16", seed=55, ragged=(1500, 3000))
+    host = generate(w, threads=4)
+    dc = device_cache(host, split_tokens=512)
+    heads = [3, 0, 2]
+    K, V = _refs(host, 1, heads, 0.05, seed=3)
+    announce("probe layer 1, heads 3,0,2")
+    out, err, out_ref = _run_probe(dc, 1, heads, K, V)
+    e_ref = oracle.probe(host, 1, heads, K, V)
+    assert np.abs(err - e_ref).max() <= 1e-4 + 1e-3 * np.abs(e_ref).max(), (err, e_ref)
+    assert e_ref.min() > 0.01, "noise should give a visible probe error"
+    # the compressed output is unchanged by probing
+    compare(out, oracle.decode(host, 1), [(b, h) for b in range(2) for h in range(4)], 4, "probe out")
+    # the reference output is plain attention over the dense reference cache
+    G = 4
+    for i, h in enumerate(heads):
+        for b in range(2):
+            t0, t1 = int(host.cu_seqlens[b]), int(host.cu_seqlens[b + 1])
+            q = oracle.q_to_f64(host.q_bits[1], "bf16")[b, h * G:(h + 1) * G]
+            o, _ = oracle.attention(q, K[i, t0:t1].astype(np.float64), V[i, t0:t1].astype(np.float64),
+                                    1 / np.sqrt(128))
+            rel = np.linalg.norm(out_ref[b, i * G:(i + 1) * G] - o) / np.linalg.norm(o)
+            assert rel < 1e-4, rel
+
+
+def test_probe_closed_forms():
+    """Rebuilt rows exact in fp16 (one-hot bases, small-integer coefficients,
+    fp16-exact residuals): K_ref = K_hat, V_ref = V_hat gives e ~ 0, and
+    V_ref = c V_hat gives e = |1-c| ||O|| / (|c| ||O|| + eps)."""
+    torch_gpu()
+    w = Workload(name="probe-exact", batch=1, n_layers=2, window=2, n_kv_heads=2, n_q_heads=4,
+                 head_dim=128, context=700, basis_rank=16, levels=(0, 2), probs=(0.5, 0.5),
+                 q_dtype="f16", seed=9)
+    host = generate(w, threads=2)
+    pins._perm_basis(host, 21)
+    rng = np.random.default_rng(22)
+    host.coef[:] = rng.integers(-3, 4, size=host.coef.shape).astype(np.float16)
+    host.res_scale[:] = np.float16(0.5)
+    dc = device_cache(host, split_tokens=256)
+    K, V = _refs(host, 0, [0, 1], 0.0, 0)
+    assert np.array_equal(K.astype(np.float64)[0], oracle.reconstruct(host, 0, 0, 0, 0)), "reference not fp16-exact"
+    announce("probe exact reference")
+    out, err, _ = _run_probe(dc, 0, [0, 1], K, V)
+    assert err.max() < 2e-6, err
+    for c in (2.0, -0.5):
+        announce(f"probe scaled reference c={c}")
+        out, err, _ = _run_probe(dc, 0, [0, 1], K, (c * V.astype(np.float64)).astype(np.float16))
+        n = np.linalg.norm(oracle.decode(host, 0), axis=-1)       # [B, Hq]
+        want = abs(1 - c) * n / (abs(c) * n + 1e-6)
+        assert np.abs(err - want.reshape(err.shape)).max() < 1e-5, (err, want)
+
+
+def test_probe_full_size_70b_shape():
+    torch_gpu()
+    wl = LLAMA70B_128K
+    announce("generate 70b window for probe")
+    host = generate(wl, layers=(0, 4))
+    dc = device_cache(host)
+    heads = [6, 1]
+    K, V = _refs(host, 3, heads, 0.05, seed=8)
+    announce("probe 70b layer 3")
+    out, err, out_ref = _run_probe(dc, 3, heads, K, V)
+    e_ref = oracle.probe(host, 3, heads, K, V)
+    assert np.abs(err - e_ref).max() <= 1e-4 + 1e-3 * np.abs(e_ref).max(), (err, e_ref)
