@@ -85,6 +85,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama8b-64k")
     ap.add_argument("--split", type=int, default=0, help="tokens per workgroup chunk (0 = automatic)")
+    ap.add_argument("--variant", default="full", choices=["full", "bases-only"],
+                    help="bases-only: every routed residual rank 0 (shared bases only)")
     ap.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
     ap.add_argument("--cpu-pairs", type=int, default=24)
     ap.add_argument("--cpu-budget", type=float, default=25.0)
@@ -104,6 +106,8 @@ def main():
     from synth import ALL, generate
 
     wl = ALL[args.workload]
+    if args.variant == "bases-only":
+        wl = wl.with_(levels=(0,), probs=(1.0,), salient_frac=0.0, name=wl.name + "-bases-only")
     log(f"[bench] generating {wl.name} ({wl.description})")
     t = time.time()
     host = generate(wl)
@@ -182,7 +186,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f16",
         "data": "synthetic",
-        "config": {"workload": wl.name, "batch": host.batch, "context": wl.context,
+        "config": {"workload": wl.name, "variant": args.variant, "batch": host.batch, "context": wl.context,
                    "layers": L, "window": wl.window, "kv_heads": wl.n_kv_heads,
                    "q_heads": wl.n_q_heads, "head_dim": wl.head_dim, "basis_rank": wl.basis_rank,
                    "levels": list(wl.levels), "split_tokens": dc.split_tokens,

@@ -75,7 +75,11 @@ typedef struct dwkv_dims {
 /* Compressed cache (Eq. 1 factors).  M = L / window, Z = 0 keys, Z = 1 values. */
 typedef struct dwkv_cache {
   const void*     basis;     /* fp16 [B][M][Hkv][2][r_b][d]: rows of B^Z_{m,h} per sequence */
-  const void*     coef;      /* fp16 [L][2][Hkv][T][r_b]: A^Z_{l,h,t}                       */
+  const void*     coef_k;    /* fp16 [L][Hkv][T][r_b]: key coefficient rows A^K_{l,h,t}     */
+  const void*     coef_v;    /* fp16 [L][Hkv][T16/16][r_b][16]: value coefficients A^V_{l,h,t}
+                                in 16-token blocks, token index fastest: token t, coefficient
+                                i at [t/16][i][t%16]; T16 = T rounded up to 16; the padding
+                                tokens of the last block must be finite (zero)               */
   const uint8_t*  rank_code; /* [M][Hkv][T] level index k of each token (rho = levels[k])  */
   const uint32_t* res_off;   /* [M][Hkv][T+1] exclusive running sum of rho over the packed
                                 tokens: token t's entries are [res_off[t], res_off[t+1])   */
@@ -90,7 +94,8 @@ typedef struct dwkv_probe {
   int32_t n_heads;             /* probed KV heads, 1..min(Hkv, 64)                     */
   const int32_t* kv_heads_host;/* [n_heads] distinct KV head ids                       */
   const void* k_ref;           /* fp16 [n_heads][T][d] reference keys (packed tokens)  */
-  const void* v_ref;           /* fp16 [n_heads][T][d] reference values                */
+  const void* v_ref;           /* fp16 [n_heads][T16/16][d][16] reference values, in the
+                                  16-token blocked layout of coef_v (finite padding)   */
   float eps;                   /* Eq. 3 epsilon (e.g. 1e-6)                            */
   float* err;                  /* out fp32 [B][n_heads*G]: probed head i, group member g
                                   at column i*G+g                                      */
@@ -120,7 +125,9 @@ size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe);
  *   out:      fp32 [B][Hq][d], written
  *   probe:    NULL, or Eq. 3 error for the listed KV heads (see dwkv_probe)
  *   workspace:>= dwkv_workspace_bytes(dims, probe) bytes of device memory;
- *             contents need no initialisation and are clobbered.
+ *             contents need no initialisation and are clobbered; calls
+ *             sharing it must be ordered (same stream).
+ * Launches one split-K kernel (two with a probe) and one merge kernel.
  * Returns DWKV_OK once enqueued. */
 dwkv_status dwkv_decode(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
                         const void* q, int32_t q_type, float sm_scale, float* out,
@@ -150,7 +157,8 @@ dwkv_status dwkv_route(const dwkv_dims* dims, const float* phi, const float* u,
 
 /* Dense residual term g*R of Eq. 1 for packed tokens [t0, t1) of slab
  * (layer, z, kv_head): dense[t-t0][c] = res_scale * code for every stored entry
- * of token t at channel c, zero elsewhere; fp32 [t1-t0][d].  Decodes entries
+ * of token t at channel c, zero elsewhere; fp32 [t1-t0][d] (may be NULL when
+ * t1 == t0).  Decodes entries
  * with the same device routines the decode kernel uses (a test hook). */
 dwkv_status dwkv_residual_map(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
                               int32_t z, int32_t kv_head, int64_t t0, int64_t t1,

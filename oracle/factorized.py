@@ -57,6 +57,19 @@ def q_to_f64(bits: np.ndarray, dtype: str) -> np.ndarray:
     raise ValueError(dtype)
 
 
+def coefficient_rows(cache, layer: int, z: int, h: int, t0: int, t1: int) -> np.ndarray:
+    """Coefficient rows A^Z_{l,h,t} of packed tokens [t0, t1) as [t1-t0, r_b] float64.
+
+    Keys are stored row-major [T][r_b]; values in 16-token blocks with the token
+    index fastest ([T16/16][r_b][16]): row t of the values is column t % 16 of
+    block t // 16."""
+    if z == 0:
+        return cache.coef_k[layer, h, t0:t1].astype(np.float64)
+    blocks = cache.coef_v[layer, h]                                 # [NB, r_b, 16]
+    rows = np.swapaxes(blocks, 1, 2).reshape(-1, blocks.shape[1])   # [NB*16, r_b]
+    return rows[t0:t1].astype(np.float64)
+
+
 def window_of(layer: int, window: int) -> int:
     return layer // window
 
@@ -70,7 +83,7 @@ def reconstruct(cache, layer: int, z: int, h: int, b: int) -> np.ndarray:
     """Explicit Eq. 1 for every token of sequence b: returns [T_b, d] float64."""
     m = window_of(layer, cache.window)
     t0, t1 = int(cache.cu_seqlens[b]), int(cache.cu_seqlens[b + 1])
-    A = cache.coef[layer, z, h, t0:t1].astype(np.float64)          # [T_b, r_b]
+    A = coefficient_rows(cache, layer, z, h, t0, t1)                # [T_b, r_b]
     Bz = cache.basis[b, m, h, z].astype(np.float64)                 # [r_b, d]
     X = A @ Bz                                                      # shared-basis term
     off = cache.res_off[m, h].astype(np.int64)

@@ -58,7 +58,8 @@ class DeviceCache:
         dev = self.device
         up = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).view(dt).to(dev)
         self.basis = up(host.basis.view(np.uint16), torch.float16)
-        self.coef = up(host.coef.view(np.uint16), torch.float16)
+        self.coef_k = up(host.coef_k.view(np.uint16), torch.float16)
+        self.coef_v = up(host.coef_v.view(np.uint16), torch.float16)
         self.rank_code = up(host.rank_code, torch.uint8)
         self.res_off = up(host.res_off.view(np.int32), torch.int32)
         self.res_idx = up(host.res_idx, torch.uint8)
@@ -90,11 +91,12 @@ class DeviceCache:
             cu_seqlens_dev_ptr=self.cu.data_ptr(), total_tokens=self.total_tokens,
             res_stride=self.res_stride, split_tokens=split_tokens)
         c = binding.Cache()
-        c.basis, c.coef, c.rank_code = self.basis.data_ptr(), self.coef.data_ptr(), self.rank_code.data_ptr()
+        c.basis, c.rank_code = self.basis.data_ptr(), self.rank_code.data_ptr()
+        c.coef_k, c.coef_v = self.coef_k.data_ptr(), self.coef_v.data_ptr()
         c.res_off, c.res_idx, c.res_val = self.res_off.data_ptr(), self.res_idx.data_ptr(), self.res_val.data_ptr()
         c.res_scale = self.res_scale.data_ptr()
         self.cstruct = c
-        self._ws = None
+        self._ws = {}
 
     @property
     def split_tokens(self) -> int:
@@ -124,10 +126,14 @@ class DeviceCache:
         return int(n)
 
     def workspace(self, probe: ProbeRef | None = None):
+        """A decode workspace, allocated once per probe shape and reused."""
         need = self.workspace_bytes(probe)
-        if self._ws is None or self._ws.numel() < need:
-            self._ws = self.torch.empty(need, dtype=self.torch.uint8, device=self.device)
-        return self._ws
+        key = None if probe is None else len(probe.kv_heads)
+        ws = self._ws.get(key)
+        if ws is None or ws.numel() < need:
+            ws = self.torch.empty(need, dtype=self.torch.uint8, device=self.device)
+            self._ws[key] = ws
+        return ws
 
     # -- calls -----------------------------------------------------------------------
     def decode(self, layer: int, q=None, sm_scale: float | None = None, probe: ProbeRef | None = None,

@@ -39,7 +39,8 @@ class Dims(C.Structure):
 
 
 class Cache(C.Structure):
-    _fields_ = [("basis", C.c_void_p), ("coef", C.c_void_p), ("rank_code", C.c_void_p),
+    _fields_ = [("basis", C.c_void_p), ("coef_k", C.c_void_p), ("coef_v", C.c_void_p),
+                ("rank_code", C.c_void_p),
                 ("res_off", C.c_void_p), ("res_idx", C.c_void_p), ("res_val", C.c_void_p),
                 ("res_scale", C.c_void_p)]
 

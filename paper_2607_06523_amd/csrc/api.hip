@@ -84,6 +84,7 @@ dwkv_status check_probe(const dwkv_dims* d, const dwkv_probe* p) {
   return DWKV_OK;
 }
 
+// Workspace: the partials of the decode pass, then those of the probe pass.
 struct WsLayout {
   size_t main_bytes, ref_bytes, total;
 };
@@ -137,7 +138,8 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   dwkv_status st = check_dims(d);
   if (st != DWKV_OK) return st;
   if (!c || !q || !out || !workspace) return DWKV_E_NULL;
-  if (!c->basis || !c->coef || !c->res_off || !c->res_idx || !c->res_val || !c->res_scale)
+  if (!c->basis || !c->coef_k || !c->coef_v || !c->res_off || !c->res_idx || !c->res_val ||
+      !c->res_scale)
     return DWKV_E_NULL;
   if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
   if (q_type != DWKV_F16 && q_type != DWKV_BF16) return DWKV_E_DIMS;
@@ -149,6 +151,7 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   const int G = d->n_q_heads / d->n_kv_heads;
   const int RB = d->basis_rank;
   const int64_t T = d->total_tokens;
+  const int64_t T16 = (T + 15) / 16 * 16;
   const int64_t Hk = d->n_kv_heads;
   const int M = d->n_layers / d->window;
   const int m = layer / d->window;
@@ -156,16 +159,15 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   const int64_t nw = count_work(d, split);
   if (nw > 0x7fffffff) return DWKV_E_UNSUPPORTED;
   if (!(sm_scale > 0.f)) sm_scale = 1.0f / std::sqrt((float)kHeadDim);
-
-  const uint16_t* coef = static_cast<const uint16_t*>(c->coef);
+  char* ws = static_cast<char*>(workspace);
+  float* part = reinterpret_cast<float*>(ws);
+  float* part_ref = reinterpret_cast<float*>(ws + wl.main_bytes);
   const uint16_t* scale = static_cast<const uint16_t*>(c->res_scale);
-  float* part = static_cast<float*>(workspace);
-  float* part_ref = reinterpret_cast<float*>(static_cast<char*>(workspace) + wl.main_bytes);
 
   SplitArgs a;
   std::memset(&a, 0, sizeof(a));
-  a.coef_k = coef + ((int64_t)layer * 2 + 0) * Hk * T * RB;
-  a.coef_v = coef + ((int64_t)layer * 2 + 1) * Hk * T * RB;
+  a.coef_k = static_cast<const uint16_t*>(c->coef_k) + (int64_t)layer * Hk * T * RB;
+  a.coef_v = static_cast<const uint16_t*>(c->coef_v) + (int64_t)layer * Hk * T16 * RB;
   a.basis = static_cast<const uint16_t*>(c->basis) + (int64_t)m * Hk * 2 * RB * kHeadDim;
   a.basis_b_stride = (int64_t)M * Hk * 2 * RB * kHeadDim;
   a.off = c->res_off + (int64_t)m * Hk * (T + 1);
@@ -191,8 +193,7 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
 
   const bool resid = max_level(d) > 0;
   if (nw > 0) {
-    hipError_t e = launch_split(RB, G, resid, false, a, (int)nw, s);
-    if (e != hipSuccess) return DWKV_E_HIP;
+    if (launch_split(RB, G, resid, false, a, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
     if (probe) {
       SplitArgs r = a;
       r.coef_k = static_cast<const uint16_t*>(probe->k_ref);
@@ -200,10 +201,10 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
       r.part = part_ref;
       r.n_slots = probe->n_heads;
       for (int i = 0; i < probe->n_heads; ++i) r.kv_of_slot[i] = probe->kv_heads_host[i];
-      e = launch_split(kHeadDim, G, false, true, r, (int)nw, s);
-      if (e != hipSuccess) return DWKV_E_HIP;
+      if (launch_split(kHeadDim, G, false, true, r, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
     }
   }
+  // the merge also writes the zero outputs of empty sequences
   MergeArgs mg;
   std::memset(&mg, 0, sizeof(mg));
   mg.part = part;
@@ -266,7 +267,8 @@ dwkv_status dwkv_residual_map(const dwkv_dims* d, const dwkv_cache* c, int32_t l
                               int32_t kv_head, int64_t t0, int64_t t1, float* dense, void* stream) {
   dwkv_status st = check_dims(d);
   if (st != DWKV_OK) return st;
-  if (!c || !dense || !c->res_off || !c->res_idx || !c->res_val || !c->res_scale) return DWKV_E_NULL;
+  if (!c || !c->res_off || !c->res_idx || !c->res_val || !c->res_scale) return DWKV_E_NULL;
+  if (!dense && t1 > t0) return DWKV_E_NULL;          // an empty range writes nothing
   if (layer < 0 || layer >= d->n_layers || z < 0 || z > 1 || kv_head < 0 || kv_head >= d->n_kv_heads)
     return DWKV_E_DIMS;
   if (t0 < 0 || t1 < t0 || t1 > d->total_tokens) return DWKV_E_DIMS;

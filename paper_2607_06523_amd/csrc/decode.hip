@@ -6,30 +6,35 @@
 // HBM.  This kernel never rebuilds K/V at all.  Because Eq. 1 is linear,
 //   q . K_hat_t = A^K_t (B^K q) + g s sum_e code_e q[c_e]
 //   sum_t p_t V_hat_t = (sum_t p_t A^V_t) B^V + sum_t p_t g s sum_e code_e e_{c_e},
-// so the query is projected once into basis space (q~ = B^K q), the coefficient
+// so the query is projected once into basis space (q~ = B^K q), coefficient
 // rows stream through MFMA against q~ and against the probabilities, and the
 // routed residual entries touch only the score of their token (keys) or one
 // channel of a d-vector accumulator (values).
 //
 // Mapping (one workgroup = 4 waves = one chunk of `split` tokens of one
-// sequence and one KV head; every wave streams its own 64-token tiles):
-//  * scores  S[tok][g] = A^K[tok][:] . q~[:][g]: v_mfma_f32_16x16x16_f16 with
-//    A^K rows as the A operand straight from HBM (lane = token % 16, k-slice by
-//    lane/16) and q~ as the B operand held in registers for the whole split;
-//    q~ is split into fp16 hi + lo parts (two MFMAs) so the scores carry
-//    float32 accuracy; the G query heads of the group fill columns 0..G-1.
-//  * the MFMA result layout (lane = head, 4 consecutive tokens per lane) is
-//    exactly the A-operand layout of the value product, so probabilities feed
-//    a~[g][:] += P[g][tok] A^V[tok][:] without a shuffle (again hi + lo);
-//    A^V tiles are staged through LDS (rows padded 8 bytes, conflict-free
-//    transposed reads).
-//  * online softmax in exp2 units; running max over the tile via lane shuffles.
-//  * residual entries: entry-parallel (one lane per entry), token found by
-//    binary search over the tile's offsets; key entries add into an LDS score
-//    buffer, value entries into an LDS d-vector per head (ds_add_f32).
-//  * epilogue: the 4 waves merge their (m, l, a~, r) in LDS, project a~
-//    through B^V and write one partial (o, m, l) per query head; a second
-//    kernel merges the splits (and computes the Eq. 3 probe error).
+// sequence and one KV head; each wave streams every 4th tile of 16*NBK tokens):
+//  * scores S[tok][g] = A^K[tok][:] . q~[:][g] on v_mfma_f32_16x16x16_f16: key
+//    rows (row-major in HBM) are the A operand, loaded straight into registers
+//    (lane = token % 16, 4 coefficients by lane / 16); q~ is the B operand, held
+//    for the whole split as fp16 hi + lo parts (two MFMAs, float32-accurate
+//    scores); the G query heads of the group fill columns 0..G-1.
+//  * the MFMA result layout (lane = head, 4 consecutive tokens per lane) is the
+//    A-operand layout of a~[g][:] += P[g][tok] A^V[tok][:], so probabilities feed
+//    the value product with no shuffle; value coefficients are stored in
+//    16-token blocks with the token index fastest, so the B operand (4
+//    consecutive tokens of one channel per lane) is one 8-byte load per lane
+//    and 512 contiguous bytes per wave instruction, straight from HBM.
+//  * fragments are single-buffered with early release: the next tile's key
+//    fragments are requested right after this tile's score MFMAs, its value
+//    fragments right after the value MFMAs; offsets run two tiles ahead and
+//    residual entries one tile ahead.
+//  * online softmax in exp2 units; running max via lane shuffles.
+//  * residual entries: one lane per entry; token of an entry from an LDS map
+//    written by the token lanes; key entries add into an LDS score buffer,
+//    value entries into an LDS d-vector per head (ds_add_f32).
+//  * epilogue: the 4 waves merge (m, l, a~, r) in LDS, project a~ through B^V
+//    and write one partial (o, m, l) per query head; a merge kernel combines
+//    the splits (and computes Eq. 3's error for probed heads).
 #include "entry.h"
 #include "internal.h"
 
@@ -59,56 +64,66 @@ __device__ __forceinline__ uint32_t dword_at(const uint4& v, int i) {
   return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
 }
 
+__device__ __forceinline__ int64_t clamp64(int64_t v, int64_t lo, int64_t hi) {
+  return v < lo ? lo : (v > hi ? hi : v);
+}
+
 template <int RB>
 struct Cfg {
   static constexpr int NBK = RB <= 64 ? 4 : 2;     // 16-token blocks per tile
   static constexpr int TT = NBK * 16;              // tokens per tile
-  static constexpr int KH = RB / 4;                // halves of a row each lane holds
+  static constexpr int KH = RB / 4;                // key coefficients a lane holds per token
   static constexpr int NS = RB / 16;               // MFMA k-steps (K = 16)
-  static constexpr int VQ = TT * RB / 512;         // 16-byte V chunks per lane per tile
-  static constexpr int VROW = RB + 4;              // LDS row pitch in halves
   static_assert(RB % 16 == 0 && RB >= 16 && RB <= 128, "r_b");
-  static_assert((TT * RB) % 512 == 0, "tile");
 };
 
 template <int RB, int G, bool RESID>
-struct WaveSmem {
+struct alignas(16) WaveSmem {
   static constexpr int TT = Cfg<RB>::TT;
   static constexpr int RG = RESID ? G : 1;
   static constexpr int RT = RESID ? TT : 1;
   static constexpr int RD = RESID ? D : 1;
-  static constexpr int RE = RESID ? kEntChunk / 4 : 1;
-  _Float16 v[TT][Cfg<RB>::VROW];       // A^V tile (also the epilogue's a~ staging)
-  float resid[RT][RG];                 // key-residual score per token and head
+  static constexpr int RE = RESID ? kEntChunk : 8;
+  float resid[RG][RT];                 // key-residual score per head and token
   float p[RT][RG];                     // tile probabilities (for value residuals)
-  float rsk[RT];                       // gate-folded residual scale, keys
-  float rsv[RT];                       // ... values
-  uint32_t off[RESID ? TT + 1 : 1];    // absolute entry offsets of the tile
+  float rsv[RT];                       // gate-folded residual scale, values
   float racc[RG][RD];                  // value-residual accumulator
-  uint32_t eidx[2][RE];                // staged channel bytes (keys, values)
-  uint32_t eval[2][RE];                // staged code bytes
-  static_assert(sizeof(v) >= sizeof(float) * G * RB, "a~ overlay");
+  uint8_t eidx[2][RE];                 // staged channel bytes (keys, values)
+  uint8_t eval[2][RE / 2];             // staged code bytes (2 entries per byte)
+  uint8_t emap[RE];                    // tile token of each staged entry
 };
 
 template <int RB, int G, bool RESID>
 struct Smem {
   alignas(16) float qs[D][G];          // q * sm_scale * log2(e)
   float qt[G][RB];                     // q~ = B^K q (scaled)
+  alignas(16) uint16_t bvs[RB][D];     // B^V rows (fp16 bits) for the projection
   float ep_m[kWaves][G];
   float ep_l[kWaves][G];
+  float ep_a[kWaves][G][RB];
   float sw[kWaves][G];
   float mstar[G];
   float lstar[G];
   float acomb[G][RB];
+  int qmax[G];                         // bits of max |q~| per head
   WaveSmem<RB, G, RESID> w[kWaves];
 };
 
+// Registers holding one tile's coefficient fragments.
 template <int RB>
-struct Tile {
-  uint2 a[Cfg<RB>::NBK][Cfg<RB>::NS];   // A^K fragments: 4 halves per k-step
-  uint4 v[Cfg<RB>::VQ];                 // A^V tile chunks
-  uint32_t oa, ob;                      // off[t0+lane], off[t0+lane+1] (clamped)
-  uint32_t sk, sv;                      // residual scale bits of token t0+lane
+struct Frags {
+  uint2 k[Cfg<RB>::NBK][Cfg<RB>::NS];   // key rows: 4 coefficients per k-step
+  uint2 v[Cfg<RB>::NBK][Cfg<RB>::NS];   // value blocks: 4 tokens of one channel per step
+};
+
+struct Meta {
+  uint32_t oa, ob;                      // entry range of this lane's token
+  uint32_t sk, sv;                      // residual scale bits of this lane's token
+};
+
+struct Ent {
+  uint32_t ik[2], iv[2];                // staged chunk: channel bytes, 8 per lane (keys, values)
+  uint32_t vk, vv;                      // staged chunk: code bytes, 4 per lane (8 entries)
 };
 
 template <int RB>
@@ -119,180 +134,249 @@ struct State {
 };
 
 struct Ctx {
-  const uint16_t* ck;
-  const uint16_t* cv;
-  const uint32_t* off;
+  const uint16_t* ck;                   // key rows of this slab [T][RB]
+  const uint16_t* cv;                   // value blocks of this slab [NB][RB][16]
+  const uint32_t* off;                  // [T+1]
   const uint8_t* idx[2];
   const uint8_t* val[2];
   const uint16_t* sk;
   const uint16_t* sv;
-  int64_t c0, c1, res_stride;
+  int64_t c0, c1, tb;                   // chunk [c0, c1); tiles start at tb = c0 & ~15
+  int64_t T, nblk;                      // packed tokens, value blocks per slab
+  int64_t res_stride;
   int ntile;
 };
 
-template <int RB, bool RESID>
-__device__ __forceinline__ void load_tile(Tile<RB>& r, const Ctx& x, int j, int lane) {
+template <int RB>
+__device__ __forceinline__ int64_t tile_start(const Ctx& x, int j) {
+  return x.tb + (int64_t)j * Cfg<RB>::TT;
+}
+
+template <int RB>
+__device__ __forceinline__ void load_k(Frags<RB>& f, const Ctx& x, int j, int lane) {
   using C = Cfg<RB>;
-  const int64_t t0 = x.c0 + (int64_t)j * C::TT;
-  const int nv = (int)min((int64_t)C::TT, x.c1 - t0);
+  const int64_t t0 = tile_start<RB>(x, j);
   const int grp = lane >> 4, col = lane & 15;
 #pragma unroll
   for (int bk = 0; bk < C::NBK; ++bk) {
-    const int tok = min(16 * bk + col, nv - 1);
-    const uint2* p = reinterpret_cast<const uint2*>(x.ck + (t0 + tok) * RB + C::KH * grp);
+    const int64_t row = min(t0 + 16 * bk + col, x.T - 1);
+    const uint2* p = reinterpret_cast<const uint2*>(x.ck + row * RB + C::KH * grp);
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s) r.a[bk][s] = p[s];
-  }
-#pragma unroll
-  for (int q = 0; q < C::VQ; ++q) {
-    const int flat = (q * 64 + lane) * 8;
-    const int row = min(flat / RB, nv - 1);
-    r.v[q] = *reinterpret_cast<const uint4*>(x.cv + (t0 + row) * RB + flat % RB);
-  }
-  if constexpr (RESID) {
-    r.oa = x.off[t0 + min(lane, nv)];
-    r.ob = x.off[t0 + min(lane + 1, nv)];
-    r.sk = x.sk[t0 + min(lane, nv - 1)];
-    r.sv = x.sv[t0 + min(lane, nv - 1)];
+    for (int s = 0; s < C::NS; ++s) f.k[bk][s] = p[s];
   }
 }
 
-// Four dwords of residual storage starting at byte `pos` of a slab of `len`
-// bytes (0 beyond the slab; such bytes belong to no entry of the tile).
+template <int RB>
+__device__ __forceinline__ void load_v(Frags<RB>& f, const Ctx& x, int j, int lane) {
+  using C = Cfg<RB>;
+  const int64_t b0 = tile_start<RB>(x, j) >> 4;
+  const int grp = lane >> 4, col = lane & 15;
+#pragma unroll
+  for (int bk = 0; bk < C::NBK; ++bk) {
+    const int64_t blk = min(b0 + bk, x.nblk - 1);
+    const uint16_t* base = x.cv + blk * RB * 16 + col * 16 + 4 * grp;
+#pragma unroll
+    for (int s = 0; s < C::NS; ++s) f.v[bk][s] = *reinterpret_cast<const uint2*>(base + s * 256);
+  }
+}
+
+// Entry range of tile j's lane token, clipped to the chunk (tokens outside the
+// chunk own no entries).
+template <int RB>
+__device__ __forceinline__ void load_offsets(Meta& m, const Ctx& x, int j, int lane) {
+  const int64_t t = tile_start<RB>(x, j) + lane;
+  m.oa = x.off[clamp64(t, x.c0, x.c1)];
+  m.ob = x.off[clamp64(t + 1, x.c0, x.c1)];
+}
+
+template <int RB>
+__device__ __forceinline__ void load_scales(Meta& m, const Ctx& x, int j, int lane) {
+  const int64_t t = clamp64(tile_start<RB>(x, j) + lane, x.c0, x.c1 - 1);
+  m.sk = x.sk[t];
+  m.sv = x.sv[t];
+}
+
 __device__ __forceinline__ uint32_t load_dword_clamped(const uint8_t* base, int64_t pos, int64_t len) {
   return pos + 4 <= len ? *reinterpret_cast<const uint32_t*>(base + pos) : 0u;
 }
 
 template <int TT>
-__device__ __forceinline__ int token_of_entry(const uint32_t* off, uint32_t e) {
-  // largest t in [0, TT) with off[t] <= e  (off[0] <= e < off[TT])
-  int lo = 0, hi = TT;
-#pragma unroll
-  for (int it = 0; it < 7; ++it) {
-    if (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (off[mid] <= e) lo = mid; else hi = mid;
-    }
-  }
-  return lo;
+__device__ __forceinline__ void tile_entry_range(const Meta& m, uint32_t& e0, uint32_t& e1) {
+  e0 = (uint32_t)__shfl((int)m.oa, 0);
+  e1 = (uint32_t)__shfl((int)m.ob, TT - 1);
+  // a well-formed tile holds at most TT*d entries; the bound keeps a corrupt
+  // offset table from running the loops long
+  if (e1 < e0) e1 = e0;
+  if (e1 - e0 > (uint32_t)(TT * D)) e1 = e0 + TT * D;
 }
 
-// One residual pass over the tile's entries [e0, e1) of slab z (0 keys, 1 values).
-// The first 256-entry chunk is already staged in LDS at (ia, va); later chunks
-// are fetched here.
-template <int RB, int G, bool ISV>
-__device__ __forceinline__ void resid_pass(WaveSmem<RB, G, true>& ws, const Ctx& x,
-                                           const float (*qs)[G], uint32_t e0, uint32_t e1,
-                                           uint32_t ia, uint32_t va, int lane) {
+// The staged chunk of a tile starts at the 8-aligned entry at or below its
+// first entry; it holds kEntChunk entries (channel bytes) and their codes.
+__device__ __forceinline__ uint32_t chunk_base(uint32_t e0) { return e0 & ~7u; }
+
+template <int TT>
+__device__ __forceinline__ void load_entries(Ent& en, const Ctx& x, const Meta& m, int lane) {
+  uint32_t e0, e1;
+  tile_entry_range<TT>(m, e0, e1);
+  en.ik[0] = en.ik[1] = en.iv[0] = en.iv[1] = en.vk = en.vv = 0u;
+  if (e1 > e0) {
+    const int64_t ia = chunk_base(e0), va = ia >> 1;
+    en.ik[0] = load_dword_clamped(x.idx[0], ia + 4 * lane, x.res_stride);
+    en.ik[1] = load_dword_clamped(x.idx[0], ia + 256 + 4 * lane, x.res_stride);
+    en.iv[0] = load_dword_clamped(x.idx[1], ia + 4 * lane, x.res_stride);
+    en.iv[1] = load_dword_clamped(x.idx[1], ia + 256 + 4 * lane, x.res_stride);
+    en.vk = load_dword_clamped(x.val[0], va + 4 * lane, x.res_stride / 2);
+    en.vv = load_dword_clamped(x.val[1], va + 4 * lane, x.res_stride / 2);
+  }
+}
+
+// Key residual, one lane per token: the lane walks its own entries (no
+// atomics), adds code * q[c] per head, and records its index in the entry map
+// the value pass reads.  `staged`: every entry lies in the LDS chunk; else the
+// entries are read from HBM.
+template <int RB, int G>
+__device__ __forceinline__ void key_resid_tokens(WaveSmem<RB, G, true>& ws, const Ctx& x,
+                                                 const float (*qs)[G], const Meta& m, uint32_t ia,
+                                                 bool staged, int lane) {
   constexpr int TT = Cfg<RB>::TT;
-  constexpr int z = ISV ? 1 : 0;
-  uint32_t beg = e0;
-  for (;;) {
-    const uint32_t end = min(e1, ia + (uint32_t)kEntChunk);
-    for (uint32_t base = beg; base < end; base += 64) {
-      const uint32_t e = base + lane;
-      if (e < end) {
-        const int t = token_of_entry<TT>(ws.off, e);
-        const uint32_t c = reinterpret_cast<const uint8_t*>(ws.eidx[z])[e - ia] & (D - 1);
-        const uint32_t vb = reinterpret_cast<const uint8_t*>(ws.eval[z])[(e >> 1) - va];
-        const float code = (float)entry_code(vb, e);
-        if constexpr (!ISV) {
-          const float s = ws.rsk[t] * code;
+  if (lane >= TT) return;
+  float acc[G];
 #pragma unroll
-          for (int g = 0; g < G; ++g) atomicAdd(&ws.resid[t][g], s * qs[c][g]);
-        } else {
-          const float s = ws.rsv[t] * code;
+  for (int g = 0; g < G; ++g) acc[g] = 0.f;
+  uint32_t e = m.oa;
+  const uint32_t hi = m.ob;
+  if (staged) {
+    // four entries at a time while aligned (ranks that are multiples of 4 keep
+    // every token's entries 4-aligned), then pairs (ranks are even)
+    for (; e + 4 <= hi && ((e - ia) & 3) == 0; e += 4) {
+      const uint32_t r = e - ia;
+      const uint32_t cw = *reinterpret_cast<const uint32_t*>(&ws.eidx[0][r]);
+      const uint32_t vw = *reinterpret_cast<const uint16_t*>(&ws.eval[0][r >> 1]);
+      *reinterpret_cast<uint32_t*>(&ws.emap[r]) = 0x01010101u * (uint32_t)lane;
 #pragma unroll
-          for (int g = 0; g < G; ++g) atomicAdd(&ws.racc[g][c], ws.p[t][g] * s);
-        }
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t c = (cw >> (8 * j)) & (D - 1);
+        const float code = (float)int4_value(vw >> (4 * j));
+        const float* q = qs[c];
+#pragma unroll
+        for (int g = 0; g < G; ++g) acc[g] += code * q[g];
       }
     }
-    if (end >= e1) break;
-    // next chunk (rare: a tile with more than ~250 routed entries)
-    beg = end;
-    ia = end;
-    va = (end >> 1) & ~3u;
-    wave_lds_fence();
-    ws.eidx[z][lane] = load_dword_clamped(x.idx[z], (int64_t)ia + 4 * lane, x.res_stride);
-    ws.eval[z][lane] = load_dword_clamped(x.val[z], (int64_t)va + 4 * lane, x.res_stride / 2);
-    wave_lds_fence();
+    for (; e < hi; ++e) {
+      const uint32_t r = e - ia;
+      const uint32_t c = ws.eidx[0][r] & (D - 1);
+      const float code = (float)entry_code(ws.eval[0][r >> 1], e);
+      ws.emap[r] = (uint8_t)lane;
+#pragma unroll
+      for (int g = 0; g < G; ++g) acc[g] += code * qs[c][g];
+    }
+  } else {
+    for (; e < hi; ++e) {
+      const uint32_t c = x.idx[0][e] & (D - 1);
+      const float code = (float)entry_code(x.val[0][e >> 1], e);
+#pragma unroll
+      for (int g = 0; g < G; ++g) acc[g] += code * qs[c][g];
+    }
+  }
+  const float rs = half_bits_to_float((uint16_t)m.sk);
+#pragma unroll
+  for (int g = 0; g < G; ++g) ws.resid[g][lane] = acc[g] * rs;
+}
+
+// Value residual, one lane per entry: p * scale * code into its channel's
+// accumulator (ds_add_f32; channels of different tokens may coincide).
+template <int RB, int G>
+__device__ __forceinline__ void value_resid_entries(WaveSmem<RB, G, true>& ws, uint32_t e0, uint32_t e1,
+                                                    uint32_t ia, int lane) {
+  for (uint32_t base = e0; base < e1; base += 64) {
+    const uint32_t e = base + lane;
+    if (e < e1) {
+      const uint32_t r = e - ia;
+      const int t = ws.emap[r];
+      const uint32_t c = ws.eidx[1][r] & (D - 1);
+      const float code = (float)entry_code(ws.eval[1][r >> 1], e);
+      float pv[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) pv[g] = ws.p[t][g];
+      const float s = ws.rsv[t] * code;
+#pragma unroll
+      for (int g = 0; g < G; ++g) atomicAdd(&ws.racc[g][c], pv[g] * s);
+    }
+  }
+}
+
+// Value residual for a tile too large for the LDS chunk: one lane per token,
+// entries read from HBM.
+template <int RB, int G>
+__device__ __forceinline__ void value_resid_tokens_global(WaveSmem<RB, G, true>& ws, const Ctx& x,
+                                                          const Meta& m, int lane) {
+  if (lane >= Cfg<RB>::TT) return;
+  float pv[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) pv[g] = ws.p[lane][g];
+  const float rs = half_bits_to_float((uint16_t)m.sv);
+  for (uint32_t e = m.oa; e < m.ob; ++e) {
+    const uint32_t c = x.idx[1][e] & (D - 1);
+    const float s = rs * (float)entry_code(x.val[1][e >> 1], e);
+#pragma unroll
+    for (int g = 0; g < G; ++g) atomicAdd(&ws.racc[g][c], pv[g] * s);
   }
 }
 
 template <int RB, int G, bool RESID>
-__device__ __forceinline__ void step(State<RB>& st, Tile<RB>& cur, Tile<RB>& nxt, int j,
-                                     const Ctx& x, Smem<RB, G, RESID>& sm,
+__device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Meta& mn, Meta& mnn,
+                                     Ent& ec, Ent& en, int j, const Ctx& x, Smem<RB, G, RESID>& sm,
                                      WaveSmem<RB, G, RESID>& ws, int lane) {
   using C = Cfg<RB>;
   constexpr int TT = C::TT, NBK = C::NBK, NS = C::NS;
   const int grp = lane >> 4, col = lane & 15;
-  const int64_t t0 = x.c0 + (int64_t)j * TT;
-  const int nv = (int)min((int64_t)TT, x.c1 - t0);
+  const int64_t t0 = tile_start<RB>(x, j);
+  const int jn = j + kWaves, jnn = j + 2 * kWaves;
+  const bool has_next = jn < x.ntile;
 
-  // 1. residual entry range of the tile; first chunk fetched before the prefetch
-  uint32_t e0 = 0, e1 = 0, ia = 0, va = 0;
-  uint32_t ik = 0, iv = 0, vk = 0, vv = 0;
+  // 1. stage this tile's residual entries; request the next tiles' metadata
+  uint32_t e0 = 0, e1 = 0, ia = 0;
+  bool staged = true;
   if constexpr (RESID) {
-    e0 = (uint32_t)__shfl((int)cur.oa, 0);
-    e1 = (uint32_t)__shfl((int)cur.ob, 63);
-    // a well-formed tile holds at most TT*d entries; the bound keeps a corrupt
-    // offset table from running the passes long
-    e1 = (e1 > e0 && e1 - e0 > (uint32_t)(TT * D)) ? e0 + TT * D : e1;
-    ia = e0 & ~3u;
-    va = (e0 >> 1) & ~3u;
-    if (e1 > e0) {
-      ik = load_dword_clamped(x.idx[0], (int64_t)ia + 4 * lane, x.res_stride);
-      iv = load_dword_clamped(x.idx[1], (int64_t)ia + 4 * lane, x.res_stride);
-      vk = load_dword_clamped(x.val[0], (int64_t)va + 4 * lane, x.res_stride / 2);
-      vv = load_dword_clamped(x.val[1], (int64_t)va + 4 * lane, x.res_stride / 2);
+    tile_entry_range<TT>(mc, e0, e1);
+    ia = chunk_base(e0);
+    staged = e1 <= ia + (uint32_t)kEntChunk;
+    if (lane < TT) ws.rsv[lane] = half_bits_to_float((uint16_t)mc.sv);
+    reinterpret_cast<uint32_t*>(ws.eidx[0])[lane] = ec.ik[0];
+    reinterpret_cast<uint32_t*>(ws.eidx[0])[lane + 64] = ec.ik[1];
+    reinterpret_cast<uint32_t*>(ws.eidx[1])[lane] = ec.iv[0];
+    reinterpret_cast<uint32_t*>(ws.eidx[1])[lane + 64] = ec.iv[1];
+    reinterpret_cast<uint32_t*>(ws.eval[0])[lane] = ec.vk;
+    reinterpret_cast<uint32_t*>(ws.eval[1])[lane] = ec.vv;
+    if (has_next) {
+      if (jnn < x.ntile) load_offsets<RB>(mnn, x, jnn, lane);
+      load_entries<TT>(en, x, mn, lane);
+      load_scales<RB>(mn, x, jn, lane);
     }
+    wave_lds_fence();
   }
-  // 2. prefetch the wave's next tile
-  if (j + kWaves < x.ntile) load_tile<RB, RESID>(nxt, x, j + kWaves, lane);
 
-  // 3. stage the value tile (and the tile's residual metadata) in LDS
-#pragma unroll
-  for (int q = 0; q < C::VQ; ++q) {
-    const int flat = (q * 64 + lane) * 8;
-    uint2* dst = reinterpret_cast<uint2*>(&ws.v[flat / RB][flat % RB]);
-    dst[0] = make_uint2(cur.v[q].x, cur.v[q].y);
-    dst[1] = make_uint2(cur.v[q].z, cur.v[q].w);
-  }
-  if constexpr (RESID) {
-    if (lane < TT) {
-      ws.off[lane] = cur.oa;
-      ws.rsk[lane] = half_bits_to_float((uint16_t)cur.sk);
-      ws.rsv[lane] = half_bits_to_float((uint16_t)cur.sv);
-    }
-    if (lane == TT - 1) ws.off[TT] = cur.ob;
-    for (int i = lane; i < TT * G; i += 64) (&ws.resid[0][0])[i] = 0.f;
-    ws.eidx[0][lane] = ik;
-    ws.eidx[1][lane] = iv;
-    ws.eval[0][lane] = vk;
-    ws.eval[1][lane] = vv;
-  }
-  wave_lds_fence();
-
-  // 4. basis-space scores on MFMA (q~ hi + lo)
+  // 2. basis-space scores on MFMA (q~ hi + lo); then the next key fragments
   f4 sacc[NBK];
 #pragma unroll
   for (int bk = 0; bk < NBK; ++bk) {
     sacc[bk] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const h4 av = __builtin_bit_cast(h4, cur.a[bk][s]);
+      const h4 av = __builtin_bit_cast(h4, fr.k[bk][s]);
       sacc[bk] = mfma16(av, st.qhi[s], sacc[bk]);
       sacc[bk] = mfma16(av, st.qlo[s], sacc[bk]);
     }
   }
+  if (has_next) load_k<RB>(fr, x, jn, lane);
 
-  // 5. key residual entries add q[c]*code*scale to their token's score
+  // 3. key residual entries add q[c]*code*scale to their token's score
   if constexpr (RESID) {
-    if (e1 > e0) resid_pass<RB, G, false>(ws, x, sm.qs, e0, e1, ia, va, lane);
+    key_resid_tokens<RB, G>(ws, x, sm.qs, mc, ia, staged, lane);
     wave_lds_fence();
   }
 
-  // 6. online softmax (exp2 units); this lane holds head `col`, tokens 16bk+4grp+i
+  // 4. online softmax (exp2 units); this lane holds head `col`, tokens 16bk+4grp+i
   float sc[NBK][4];
   float mt = -INFINITY;
 #pragma unroll
@@ -300,33 +384,34 @@ __device__ __forceinline__ void step(State<RB>& st, Tile<RB>& cur, Tile<RB>& nxt
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int tok = 16 * bk + 4 * grp + i;
+      const int64_t t = t0 + tok;
       float s = sacc[bk][i] * st.down;
       if constexpr (RESID) {
-        if (col < G) s += ws.resid[tok][col];
+        if (col < G) s += ws.resid[col][tok];
       }
-      s = tok < nv ? s : -INFINITY;
+      s = (t >= x.c0 && t < x.c1) ? s : -INFINITY;
       sc[bk][i] = s;
       mt = fmaxf(mt, s);
     }
   }
   mt = fmaxf(mt, __shfl_xor(mt, 16));
   mt = fmaxf(mt, __shfl_xor(mt, 32));
-  const float mn = fmaxf(st.m, mt);
-  const float alpha = exp2_hw(st.m - mn);
+  const float mnew = fmaxf(st.m, mt);
+  const float alpha = exp2_hw(st.m - mnew);
   float psum = 0.f;
 #pragma unroll
   for (int bk = 0; bk < NBK; ++bk) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float p = col < G ? exp2_hw(sc[bk][i] - mn) : 0.f;
+      const float p = col < G ? exp2_hw(sc[bk][i] - mnew) : 0.f;
       sc[bk][i] = p;
       psum += p;
     }
   }
   st.l = st.l * alpha + psum;
-  st.m = mn;
+  st.m = mnew;
 
-  // 7. rescale the basis-space value accumulator (rows g = 4grp+i)
+  // 5. rescale the basis-space value accumulator (rows g = 4grp+i)
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const float ai = __shfl(alpha, 4 * grp + i);
@@ -335,7 +420,7 @@ __device__ __forceinline__ void step(State<RB>& st, Tile<RB>& cur, Tile<RB>& nxt
   }
 
   if constexpr (RESID) {
-    // 8. rescale the value-residual accumulator when a running max moved
+    // 6. rescale the value-residual accumulator when a running max moved
     const bool moved = (col < G) && (alpha != 1.0f);
     if (__ballot(moved) != 0) {
 #pragma unroll
@@ -345,7 +430,7 @@ __device__ __forceinline__ void step(State<RB>& st, Tile<RB>& cur, Tile<RB>& nxt
         (&ws.racc[0][0])[it * 64 + lane] *= ag;
       }
     }
-    // 9. probabilities to LDS for the value entries
+    // 7. probabilities to LDS for the value entries
     if (col < G) {
 #pragma unroll
       for (int bk = 0; bk < NBK; ++bk)
@@ -354,7 +439,7 @@ __device__ __forceinline__ void step(State<RB>& st, Tile<RB>& cur, Tile<RB>& nxt
     }
   }
 
-  // 10. a~ += P A^V on MFMA (P hi + lo); A^V read transposed from LDS
+  // 8. a~ += P A^V on MFMA (P hi + lo); then the next value fragments
 #pragma unroll
   for (int bk = 0; bk < NBK; ++bk) {
     h4 ph, pl;
@@ -366,26 +451,31 @@ __device__ __forceinline__ void step(State<RB>& st, Tile<RB>& cur, Tile<RB>& nxt
     }
 #pragma unroll
     for (int cb = 0; cb < NS; ++cb) {
-      h4 vf;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) vf[i] = ws.v[16 * bk + 4 * grp + i][16 * cb + col];
+      const h4 vf = __builtin_bit_cast(h4, fr.v[bk][cb]);
       st.acc[cb] = mfma16(ph, vf, st.acc[cb]);
       st.acc[cb] = mfma16(pl, vf, st.acc[cb]);
     }
   }
+  if (has_next) load_v<RB>(fr, x, jn, lane);
 
-  // 11. value residual entries scatter p*code*scale into their channel
+  // 9. value residual entries scatter p*code*scale into their channel
   if constexpr (RESID) {
     wave_lds_fence();
-    if (e1 > e0) resid_pass<RB, G, true>(ws, x, sm.qs, e0, e1, ia, va, lane);
+    if (e1 > e0) {
+      if (staged) value_resid_entries<RB, G>(ws, e0, e1, ia, lane);
+      else value_resid_tokens_global<RB, G>(ws, x, mc, lane);
+    }
+    wave_lds_fence();
+    mc = mn;
+    mn = mnn;
+    ec = en;
   }
-  wave_lds_fence();
 }
 
 template <int RB, int G, bool RESID, bool IDENT>
 __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   using C = Cfg<RB>;
-  constexpr int NS = C::NS;
+  constexpr int NS = C::NS, TT = C::TT;
   __shared__ Smem<RB, G, RESID> sm;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int grp = lane >> 4, col = lane & 15;
@@ -396,19 +486,22 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   const int w = blockIdx.x;
   int b = 0, base = 0;
   for (; b < a.batch - 1; ++b) {
-    const int tb = a.cu[b + 1] - a.cu[b];
-    const int ns = (tb + a.split - 1) / a.split;
+    const int ns = (a.cu[b + 1] - a.cu[b] + a.split - 1) / a.split;
     if (w < base + ns) break;
     base += ns;
   }
+  const int n_split_b = (a.cu[b + 1] - a.cu[b] + a.split - 1) / a.split;
   Ctx x;
   x.c0 = (int64_t)a.cu[b] + (int64_t)(w - base) * a.split;
   x.c1 = min(min((int64_t)a.cu[b + 1], x.c0 + a.split), a.T);
   x.c0 = min(x.c0, x.c1);
-  x.ntile = (int)((x.c1 - x.c0 + C::TT - 1) / C::TT);
+  x.tb = x.c0 & ~(int64_t)15;
+  x.ntile = (int)((x.c1 - x.tb + TT - 1) / TT);
+  x.T = a.T;
+  x.nblk = (a.T + 15) / 16;
   x.res_stride = a.res_stride;
   x.ck = a.coef_k + (int64_t)slot * a.T * RB;
-  x.cv = a.coef_v + (int64_t)slot * a.T * RB;
+  x.cv = a.coef_v + (int64_t)slot * x.nblk * 16 * RB;
   if constexpr (RESID) {
     x.off = a.off + (int64_t)kvh * (a.T + 1);
     x.idx[0] = a.idx_k + (int64_t)kvh * a.res_stride;
@@ -421,34 +514,72 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   const uint16_t* bk_rows = IDENT ? nullptr : a.basis + (int64_t)b * a.basis_b_stride + (int64_t)kvh * 2 * RB * D;
   const uint16_t* bv_rows = IDENT ? nullptr : bk_rows + RB * D;
 
-  // the first tile's loads go out before the query projection
-  Tile<RB> ta, tb;
-  if (wv < x.ntile) load_tile<RB, RESID>(ta, x, wv, lane);
-
-  // scaled query and q~ = B^K q
-  for (int i = tid; i < G * D; i += kThreads) {
-    const int g = i / D, c = i % D;
-    const uint16_t bits = a.q[((int64_t)b * a.n_q_heads + kvh * G + g) * D + c];
-    sm.qs[c][g] = (a.q_bf16 ? bf16_bits_to_float(bits) : half_bits_to_float(bits)) * a.qscale;
+  // the query, B^K rows and B^V rows are requested together
+  constexpr int NIT = (RB * 4 + kThreads - 1) / kThreads;   // q~ work items per thread
+  constexpr int QPT = (G * D + kThreads - 1) / kThreads;     // query elements per thread
+  constexpr int BVQ = IDENT ? 1 : RB * D / 8 / kThreads;     // 16-byte B^V chunks per thread
+  uint4 rv[NIT][4];
+  uint16_t qraw[QPT];
+  uint4 bvr[BVQ];
+  if constexpr (!IDENT) {
+#pragma unroll
+    for (int n = 0; n < NIT; ++n) {
+      const int it = tid + n * kThreads;
+      if (it < RB * 4) {
+        const uint4* row = reinterpret_cast<const uint4*>(bk_rows + (it >> 2) * D + (it & 3) * 32);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rv[n][i] = row[i];
+      }
+    }
+#pragma unroll
+    for (int n = 0; n < BVQ; ++n) bvr[n] = reinterpret_cast<const uint4*>(bv_rows)[tid + n * kThreads];
+  }
+#pragma unroll
+  for (int n = 0; n < QPT; ++n) {
+    const int i = tid + n * kThreads;
+    qraw[n] = i < G * D ? a.q[((int64_t)b * a.n_q_heads + kvh * G + i / D) * D + i % D] : 0;
+  }
+  // then the wave's first tile (its residual entries once its offsets are in)
+  Frags<RB> fr;
+  Meta mc{}, mn{}, mnn{};
+  Ent ec{}, en{};
+  if (wv < x.ntile) {
+    if constexpr (RESID) {
+      load_offsets<RB>(mc, x, wv, lane);
+      if (wv + kWaves < x.ntile) load_offsets<RB>(mn, x, wv + kWaves, lane);
+      load_scales<RB>(mc, x, wv, lane);
+    }
+    load_k<RB>(fr, x, wv, lane);
+    load_v<RB>(fr, x, wv, lane);
+    if constexpr (RESID) load_entries<TT>(ec, x, mc, lane);
+  }
+  if (tid < G) sm.qmax[tid] = 0;
+#pragma unroll
+  for (int n = 0; n < QPT; ++n) {
+    const int i = tid + n * kThreads;
+    if (i < G * D)
+      sm.qs[i % D][i / D] = (a.q_bf16 ? bf16_bits_to_float(qraw[n]) : half_bits_to_float(qraw[n])) * a.qscale;
+  }
+  if constexpr (!IDENT) {
+#pragma unroll
+    for (int n = 0; n < BVQ; ++n) reinterpret_cast<uint4*>(&sm.bvs[0][0])[tid + n * kThreads] = bvr[n];
   }
   __syncthreads();
   if constexpr (!IDENT) {
-    for (int it = tid; it < RB * 4; it += kThreads) {
+#pragma unroll
+    for (int n = 0; n < NIT; ++n) {
+      const int it = tid + n * kThreads;
+      if (it >= RB * 4) continue;
       const int k = it >> 2, qq = it & 3;
-      const uint16_t* row = bk_rows + k * D + qq * 32;
       float acc[G];
 #pragma unroll
       for (int g = 0; g < G; ++g) acc[g] = 0.f;
 #pragma unroll
-      for (int c8 = 0; c8 < 32; c8 += 8) {
-        const uint4 v = *reinterpret_cast<const uint4*>(row + c8);
+      for (int e = 0; e < 32; ++e) {
+        const uint32_t dw = dword_at(rv[n][e >> 3], (e >> 1) & 3);
+        const float xv = half_bits_to_float((uint16_t)((e & 1) ? (dw >> 16) : (dw & 0xFFFF)));
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint32_t dw = dword_at(v, e >> 1);
-          const float xv = half_bits_to_float((uint16_t)((e & 1) ? (dw >> 16) : (dw & 0xFFFF)));
-#pragma unroll
-          for (int g = 0; g < G; ++g) acc[g] += xv * sm.qs[qq * 32 + c8 + e][g];
-        }
+        for (int g = 0; g < G; ++g) acc[g] += xv * sm.qs[qq * 32 + e][g];
       }
 #pragma unroll
       for (int g = 0; g < G; ++g) {
@@ -457,11 +588,19 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
       }
       if (qq == 0) {
 #pragma unroll
-        for (int g = 0; g < G; ++g) sm.qt[g][k] = acc[g];
+        for (int g = 0; g < G; ++g) {
+          sm.qt[g][k] = acc[g];
+          atomicMax(&sm.qmax[g], __float_as_int(fabsf(acc[g])));
+        }
       }
     }
-    __syncthreads();
+  } else {
+    for (int i = tid; i < G * D; i += kThreads) {
+      const int g = i / D, c = i % D;
+      atomicMax(&sm.qmax[g], __float_as_int(fabsf(sm.qs[c][g])));
+    }
   }
+  __syncthreads();
 
   // q~ as MFMA B operand (column = head), scaled by a power of two so its
   // largest entry sits just under 2^14, split into fp16 hi + lo
@@ -469,8 +608,7 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   {
     int kexp = 0;
     if (col < G) {
-      float mx = 0.f;
-      for (int k = 0; k < RB; ++k) mx = fmaxf(mx, fabsf(IDENT ? sm.qs[k][col] : sm.qt[col][k]));
+      const float mx = __int_as_float(sm.qmax[col]);
       if (mx > 0.f) {
         int e;
         frexpf(mx, &e);
@@ -500,17 +638,13 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
     for (int i = lane; i < G * D; i += 64) (&ws.racc[0][0])[i] = 0.f;
   }
 
-  // stream the wave's tiles (ping-pong register buffers)
-  for (int j = wv; j < x.ntile; j += 2 * kWaves) {
-    step<RB, G, RESID>(st, ta, tb, j, x, sm, ws, lane);
-    if (j + kWaves >= x.ntile) break;
-    step<RB, G, RESID>(st, tb, ta, j + kWaves, x, sm, ws, lane);
-  }
+  // stream the wave's tiles
+  for (int j = wv; j < x.ntile; j += kWaves) step<RB, G, RESID>(st, fr, mc, mn, mnn, ec, en, j, x, sm, ws, lane);
 
   // epilogue: merge the 4 waves, project a~ through B^V, write the partial
+  const int c_out = tid % D, par = tid / D;
   st.l += __shfl_xor(st.l, 16);
   st.l += __shfl_xor(st.l, 32);
-  float* epa = reinterpret_cast<float*>(&ws.v[0][0]);        // [G][RB]
   if (grp == 0 && col < G) {
     sm.ep_m[wv][col] = st.m;
     sm.ep_l[wv][col] = st.l;
@@ -520,7 +654,7 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int g = 4 * grp + i;
-      if (g < G) epa[g * RB + 16 * cb + col] = st.acc[cb][i];
+      if (g < G) sm.ep_a[wv][g][16 * cb + col] = st.acc[cb][i];
     }
   __syncthreads();
   if (tid < G) {
@@ -540,75 +674,149 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   for (int i = tid; i < G * RB; i += kThreads) {
     const int g = i / RB, k = i % RB;
     float s = 0.f;
-    for (int v = 0; v < kWaves; ++v) s += sm.sw[v][g] * reinterpret_cast<const float*>(&sm.w[v].v[0][0])[g * RB + k];
+    for (int v = 0; v < kWaves; ++v) s += sm.sw[v][g] * sm.ep_a[v][g][k];
     sm.acomb[g][k] = s;
   }
   __syncthreads();
-  for (int i = tid; i < G * D; i += kThreads) {
-    const int g = i / D, c = i % D;
+  float* const part_ws = a.part;
+  for (int g = par; g < G; g += kThreads / D) {
     float o;
     if constexpr (IDENT) {
-      o = sm.acomb[g][c];
+      o = sm.acomb[g][c_out];
     } else {
       o = 0.f;
-      for (int k = 0; k < RB; ++k) o += sm.acomb[g][k] * half_bits_to_float(bv_rows[k * D + c]);
+#pragma unroll 16
+      for (int k = 0; k < RB; ++k) o += sm.acomb[g][k] * half_bits_to_float(sm.bvs[k][c_out]);
     }
     if constexpr (RESID) {
-      for (int v = 0; v < kWaves; ++v) o += sm.sw[v][g] * sm.w[v].racc[g][c];
+      for (int v = 0; v < kWaves; ++v) o += sm.sw[v][g] * sm.w[v].racc[g][c_out];
     }
-    float* dst = a.part + (((int64_t)w * a.n_slots + slot) * G + g) * kPartStride;
-    dst[c] = o;
-    if (c == 0) {
+    float* dst = part_ws + (((int64_t)w * a.n_slots + slot) * G + g) * kPartStride;
+    dst[c_out] = o;
+    if (c_out == 0) {
       dst[D] = sm.mstar[g];
       dst[D + 1] = sm.lstar[g];
     }
   }
+
 }
 
-// One workgroup per (query head, sequence): merges the split partials in a
-// fixed order; with a probe, also merges the reference partials and writes
-// Eq. 3's relative error.
-__global__ __launch_bounds__(D) void merge_kernel(const MergeArgs a) {
-  const int hq = blockIdx.x, b = blockIdx.y, c = threadIdx.x;
+
+// One workgroup per (query head, sequence) merges that head's split partials
+// in a fixed order: every partial's (m, l) and output slice are requested in
+// one round of loads.  For a probed KV head it also merges the reference
+// partials and writes Eq. 3's error.
+constexpr int kMergeThreads = 256;
+constexpr int kMergeGroups = kMergeThreads / (D / 4);     // split groups (8)
+constexpr int kMergePerThread = 8;                        // splits per thread per round
+
+__device__ __forceinline__ float4 merge_rows(const float* part, int64_t row0, int64_t row_step, int ns,
+                                             float* red_m, float* red_l, float4* red_o) {
+  const int tid = threadIdx.x, c4 = tid % (D / 4), sg = tid / (D / 4);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float mstar = -INFINITY, lstar = 0.f;
+  for (int s0 = 0; s0 < ns; s0 += kMergeGroups * kMergePerThread) {
+    // this round's splits: s0 + sg + kMergeGroups * i
+    float4 ov[kMergePerThread];
+    float mv[kMergePerThread], lv[kMergePerThread];
+#pragma unroll
+    for (int i = 0; i < kMergePerThread; ++i) {
+      const int s = s0 + sg + kMergeGroups * i;
+      if (s < ns) {
+        const float* p = part + (row0 + (int64_t)s * row_step) * kPartStride;
+        ov[i] = reinterpret_cast<const float4*>(p)[c4];
+        mv[i] = p[D];
+        lv[i] = p[D + 1];
+      } else {
+        ov[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        mv[i] = -INFINITY;
+        lv[i] = 0.f;
+      }
+    }
+    // running max and denominator over this round (all threads see every split
+    // of the round through LDS)
+    if (c4 == 0) {
+#pragma unroll
+      for (int i = 0; i < kMergePerThread; ++i) {
+        red_m[sg * kMergePerThread + i] = mv[i];
+        red_l[sg * kMergePerThread + i] = lv[i];
+      }
+    }
+    __syncthreads();
+    float mr = mstar;
+    for (int i = 0; i < kMergeGroups * kMergePerThread; ++i) mr = fmaxf(mr, red_m[i]);
+    const float resc = mstar == -INFINITY ? 0.f : exp2f(mstar - mr);
+    float lr = lstar * resc;
+    for (int i = 0; i < kMergeGroups * kMergePerThread; ++i)
+      if (red_m[i] != -INFINITY) lr += red_l[i] * exp2f(red_m[i] - mr);
+    acc.x *= resc; acc.y *= resc; acc.z *= resc; acc.w *= resc;
+#pragma unroll
+    for (int i = 0; i < kMergePerThread; ++i) {
+      if (mv[i] == -INFINITY) continue;
+      const float w = exp2f(mv[i] - mr);
+      acc.x += w * ov[i].x; acc.y += w * ov[i].y; acc.z += w * ov[i].z; acc.w += w * ov[i].w;
+    }
+    mstar = mr;
+    lstar = lr;
+    __syncthreads();
+  }
+  // combine the split groups of each 4-channel slice
+  red_o[tid] = acc;
+  __syncthreads();
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (sg == 0) {
+    for (int q = 0; q < kMergeGroups; ++q) {
+      const float4 u = red_o[q * (D / 4) + c4];
+      o.x += u.x; o.y += u.y; o.z += u.z; o.w += u.w;
+    }
+    const float inv = ns > 0 ? 1.0f / lstar : 0.f;
+    o.x *= inv; o.y *= inv; o.z *= inv; o.w *= inv;
+  }
+  __syncthreads();
+  return o;
+}
+
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a) {
+  __shared__ float red_m[kMergeGroups * kMergePerThread], red_l[kMergeGroups * kMergePerThread];
+  __shared__ float4 red_o[kMergeThreads];
+  __shared__ float red2[2][kMergeThreads / 64];
+  const int hq = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int G = a.n_q_heads / a.n_kv_heads, h = hq / G, g = hq % G;
   int base = 0;
   for (int i = 0; i < b; ++i) base += (a.cu[i + 1] - a.cu[i] + a.split - 1) / a.split;
   const int ns = (a.cu[b + 1] - a.cu[b] + a.split - 1) / a.split;
-
-  auto merge = [&](const float* part, int n_slots, int s_slot) -> float {
-    float mx = -INFINITY;
-    for (int s = 0; s < ns; ++s)
-      mx = fmaxf(mx, part[(((int64_t)(base + s) * n_slots + s_slot) * G + g) * kPartStride + D]);
-    float l = 0.f, acc = 0.f;
-    for (int s = 0; s < ns; ++s) {
-      const float* p = part + (((int64_t)(base + s) * n_slots + s_slot) * G + g) * kPartStride;
-      const float wgt = exp2f(p[D] - mx);
-      l += wgt * p[D + 1];
-      acc += wgt * p[c];
-    }
-    return ns > 0 ? acc / l : 0.f;
-  };
-
-  const float o = merge(a.part, a.n_kv_heads, h);
-  a.out[((int64_t)b * a.n_q_heads + hq) * D + c] = o;
+  const int c4 = tid % (D / 4), sg = tid / (D / 4);
+  // main partials: row (work, h, g) = (work * Hkv + h) * G + g
+  const float4 o = merge_rows(a.part, (int64_t)base * a.n_kv_heads * G + h * G + g,
+                              (int64_t)a.n_kv_heads * G, ns, red_m, red_l, red_o);
+  if (sg == 0) reinterpret_cast<float4*>(a.out + ((int64_t)b * a.n_q_heads + hq) * D)[c4] = o;
   if (a.n_probe > 0) {
     const int sl = a.probe_slot_of_kv[h];
     if (sl >= 0) {
-      const float r = merge(a.part_ref, a.n_probe, sl);
+      const float4 r = merge_rows(a.part_ref, (int64_t)base * a.n_probe * G + sl * G + g,
+                                  (int64_t)a.n_probe * G, ns, red_m, red_l, red_o);
       const int64_t col = (int64_t)b * a.n_probe * G + sl * G + g;
-      if (a.out_ref) a.out_ref[col * D + c] = r;
-      float d2 = (r - o) * (r - o), r2 = r * r;
+      float d2 = 0.f, r2 = 0.f;
+      if (sg == 0) {
+        if (a.out_ref) reinterpret_cast<float4*>(a.out_ref + col * D)[c4] = r;
+        const float dx = r.x - o.x, dy = r.y - o.y, dz = r.z - o.z, dw = r.w - o.w;
+        d2 = dx * dx + dy * dy + dz * dz + dw * dw;
+        r2 = r.x * r.x + r.y * r.y + r.z * r.z + r.w * r.w;
+      }
       for (int o2 = 32; o2 > 0; o2 >>= 1) {
         d2 += __shfl_xor(d2, o2);
         r2 += __shfl_xor(r2, o2);
       }
-      __shared__ float red[2][2];
-      if ((c & 63) == 0) {
-        red[c >> 6][0] = d2;
-        red[c >> 6][1] = r2;
+      if ((tid & 63) == 0) {
+        red2[0][tid >> 6] = d2;
+        red2[1][tid >> 6] = r2;
       }
       __syncthreads();
-      if (c == 0) a.err[col] = sqrtf(red[0][0] + red[1][0]) / (sqrtf(red[0][1] + red[1][1]) + a.eps);
+      if (tid == 0) {
+        float sd = 0.f, sr = 0.f;
+        for (int i = 0; i < kMergeThreads / 64; ++i) { sd += red2[0][i]; sr += red2[1][i]; }
+        a.err[col] = sqrtf(sd) / (sqrtf(sr) + a.eps);
+      }
     }
   }
 }
@@ -655,7 +863,7 @@ hipError_t launch_split(int rb, int g, bool resid, bool ident, const SplitArgs& 
 }
 
 hipError_t launch_merge(const MergeArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(merge_kernel, dim3(a.n_q_heads, a.batch), dim3(D), 0, s, a);
+  hipLaunchKernelGGL(merge_kernel, dim3(a.n_q_heads, a.batch), dim3(kMergeThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -11,13 +11,13 @@ constexpr int kHeadDim = 128;       // d
 constexpr int kWaves = 4;           // waves per decode workgroup
 constexpr int kThreads = 64 * kWaves;
 constexpr int kPartStride = kHeadDim + 4;   // floats per partial: o[d], m, l, pad
-constexpr int kEntChunk = 256;      // residual entries staged per LDS chunk
+constexpr int kEntChunk = 512;      // residual entries of a tile staged in LDS
 constexpr int kResTailPad = 512;    // spare entries required after the longest slab
 
 // One split-K pass over a layer: grid = (work items, head slots).
 struct SplitArgs {
-  const uint16_t* coef_k;      // slot 0 coefficient (or dense reference) rows, keys
-  const uint16_t* coef_v;      // ... values; slot s adds s * T * RB
+  const uint16_t* coef_k;      // slot 0 key rows [T][RB]; slot s adds s*T*RB
+  const uint16_t* coef_v;      // slot 0 value blocks [T16/16][RB][16]; slot s adds s*T16*RB
   const uint16_t* basis;       // basis of window m, sequence 0: + (b*M*Hkv + h)*2*RB*d
   int64_t basis_b_stride;      // halves between sequences (M*Hkv*2*RB*d)
   const uint32_t* off;         // res_off of window m, head 0; head h adds h*(T+1)
@@ -42,8 +42,9 @@ struct SplitArgs {
   int32_t kv_of_slot[DWKV_MAX_PROBE_HEADS];
 };
 
+// Split merge (and Eq. 3 for probed heads): grid = (Hq, B).
 struct MergeArgs {
-  const float* part;           // main partials [work][Hkv][G][kPartStride]
+  const float* part;           // decode partials [work][Hkv][G][kPartStride]
   const float* part_ref;       // probe partials [work][n_probe][G][kPartStride] or null
   float* out;                  // [B][Hq][d]
   float* err;                  // [B][n_probe*G] or null

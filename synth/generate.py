@@ -27,6 +27,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
+from .layout import BLOCK, padded_tokens
 from .workloads import Workload
 
 # tensor ids used to key the random streams
@@ -58,7 +59,10 @@ class CompressedCache:
 
     Shapes (M windows, L layers held, T packed tokens over all sequences):
       basis     fp16  [B][M][Hkv][2][r_b][d]   Z=0 keys, Z=1 values
-      coef      fp16  [L][2][Hkv][T][r_b]
+      coef_k    fp16  [L][Hkv][T][r_b]           key coefficient rows A^K
+      coef_v    fp16  [L][Hkv][T16/16][r_b][16]  value coefficients A^V in 16-token
+                                                 blocks, token fastest (T16 = T rounded
+                                                 up to 16, zero padded)
       rank_code uint8 [M][Hkv][T]
       res_off   uint32[M][Hkv][T+1]
       res_idx   uint8 [L][2][Hkv][res_stride]
@@ -74,7 +78,8 @@ class CompressedCache:
     levels: tuple
     res_stride: int
     basis: np.ndarray
-    coef: np.ndarray
+    coef_k: np.ndarray
+    coef_v: np.ndarray
     rank_code: np.ndarray
     res_off: np.ndarray
     res_idx: np.ndarray
@@ -217,7 +222,8 @@ def generate(w: Workload, layers: tuple | None = None, threads: int | None = Non
     list(pool.map(_basis, [(b, m, h, z) for b in range(B) for m in range(nM)
                            for h in range(Hk) for z in range(2)]))
 
-    coef = np.empty((nL, 2, Hk, T, rb), dtype=np.float16)
+    coef_k = np.empty((nL, Hk, T, rb), dtype=np.float16)
+    coef_v = np.zeros((nL, Hk, padded_tokens(T) // BLOCK, rb, BLOCK), dtype=np.float16)
     res_scale = np.empty((nL, 2, Hk, T), dtype=np.float16)
     res_idx = np.zeros((nL, 2, Hk, res_stride), dtype=np.uint8)
     res_val = np.zeros((nL, 2, Hk, res_stride // 2), dtype=np.uint8)
@@ -232,7 +238,12 @@ def generate(w: Workload, layers: tuple | None = None, threads: int | None = Non
             if n == 0:
                 continue
             g = rng_for(w.seed, _COEF, b, l, z, h)
-            coef[li, z, h, t0:t1] = g.standard_normal((n, rb), dtype=np.float32).astype(np.float16)
+            rows = g.standard_normal((n, rb), dtype=np.float32).astype(np.float16)
+            if z == 0:
+                coef_k[li, h, t0:t1] = rows
+            else:   # scatter into the token-fastest blocks
+                tt = np.arange(t0, t1)
+                coef_v[li, h, tt // BLOCK, :, tt % BLOCK] = rows
             s = rng_for(w.seed, _RES_SCALE, b, l, z, h).uniform(0.01, 0.1, size=n)
             res_scale[li, z, h, t0:t1] = s.astype(np.float16)
         # entries of every sequence, packed in token order
@@ -260,7 +271,7 @@ def generate(w: Workload, layers: tuple | None = None, threads: int | None = Non
     return CompressedCache(
         workload=w, layer0=L0, n_layers=nL, seqlens=list(seqlens), cu_seqlens=cu,
         levels=tuple(int(x) for x in w.levels), res_stride=res_stride, basis=basis,
-        coef=coef, rank_code=rank_code, res_off=res_off, res_idx=res_idx,
+        coef_k=coef_k, coef_v=coef_v, rank_code=rank_code, res_off=res_off, res_idx=res_idx,
         res_val=res_val, res_scale=res_scale, q_bits=q_bits, q_dtype=w.q_dtype)
 
 

@@ -29,6 +29,7 @@ from fractions import Fraction
 import numpy as np
 
 from synth import generate, router_inputs, Workload
+from synth.layout import block_values, unblock_values
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -55,6 +56,37 @@ def _rel(a, b):
 
 def _q64(o, cache, layer):
     return o.q_to_f64(cache.q_bits[layer], cache.q_dtype)
+
+
+def coef_rows(c, layer, z, h):
+    """Logical [T][r_b] coefficient rows (a copy)."""
+    if z == 0:
+        return c.coef_k[layer, h].copy()
+    return unblock_values(c.coef_v[layer, h], c.total_tokens).copy()
+
+
+def set_coef_rows(c, layer, z, h, rows):
+    if z == 0:
+        c.coef_k[layer, h] = rows
+    else:
+        c.coef_v[layer, h] = block_values(np.asarray(rows, dtype=np.float16))
+
+
+def coef_set(c, layer, z, h, t, i, value):
+    if z == 0:
+        c.coef_k[layer, h, t, i] = value
+    else:
+        c.coef_v[layer, h, t // 16, i, t % 16] = value
+
+
+def coef_get(c, layer, z, h, t, i):
+    return c.coef_k[layer, h, t, i] if z == 0 else c.coef_v[layer, h, t // 16, i, t % 16]
+
+
+def zero_coefs(c, layer=None):
+    sl = slice(None) if layer is None else layer
+    c.coef_k[sl] = 0
+    c.coef_v[sl] = 0
 
 
 def _pack(codes):
@@ -102,7 +134,7 @@ def brute_force_decode(cache, layer, b, hq, scale):
             for c in range(d):
                 acc = Decimal(0)
                 for i in range(rb):
-                    acc += Decimal(float(cache.coef[layer, z, h, t, i])) * Decimal(float(basis[i, c]))
+                    acc += Decimal(float(coef_get(cache, layer, z, h, t, i))) * Decimal(float(basis[i, c]))
                 x[c] = acc
             e = int(cache.res_off[m, h, t])
             while e < int(cache.res_off[m, h, t + 1]):
@@ -181,11 +213,13 @@ def pin_closed_forms(o):
     m = layer // c.window
     Hq, Hk = c.n_q_heads, c.n_kv_heads
     G = Hq // Hk
-    c.coef[layer] = 0
+    zero_coefs(c, layer)
     sel = rng.integers(0, c.basis_rank, size=(2, Hk, c.total_tokens))
     for z in range(2):
         for h in range(Hk):
-            c.coef[layer, z, h, np.arange(c.total_tokens), sel[z, h]] = 1
+            rows = np.zeros((c.total_tokens, c.basis_rank), np.float16)
+            rows[np.arange(c.total_tokens), sel[z, h]] = 1
+            set_coef_rows(c, layer, z, h, rows)
     q0 = np.zeros((c.batch, Hq, c.head_dim))
     out = o.decode(c, layer, q=q0)
     for b in range(c.batch):
@@ -204,11 +238,11 @@ def pin_closed_forms(o):
     perms = _perm_basis(c, 5)
     layer = 2
     m = layer // c.window
-    c.coef[layer] = 0
+    zero_coefs(c, layer)
     for h in range(Hk):
-        c.coef[layer, 0, h, 1, 2] = 2.0                  # K_hat_1 = 2 e_{pi_K(2)}, K_hat_0 = 0
-        c.coef[layer, 1, h, 0, 0] = 1.0                  # V_hat_0 = e_{pi_V(0)}
-        c.coef[layer, 1, h, 1, 1] = -4.0                 # V_hat_1 = -4 e_{pi_V(1)}
+        coef_set(c, layer, 0, h, 1, 2, 2.0)              # K_hat_1 = 2 e_{pi_K(2)}, K_hat_0 = 0
+        coef_set(c, layer, 1, h, 0, 0, 1.0)              # V_hat_0 = e_{pi_V(0)}
+        coef_set(c, layer, 1, h, 1, 1, -4.0)             # V_hat_1 = -4 e_{pi_V(1)}
     q = np.zeros((1, Hq, c.head_dim))
     for hq in range(Hq):
         h = hq // G
@@ -228,9 +262,9 @@ def pin_closed_forms(o):
     perms = _perm_basis(c, 7)
     layer = 1
     m = 0
-    c.coef[layer] = 0
+    zero_coefs(c, layer)
     for h in range(Hk):
-        c.coef[layer, 1, h, 0, 3] = 1.0
+        coef_set(c, layer, 1, h, 0, 3, 1.0)
         set_entries(c, layer, 1, h, 0, [5, 11], [-7, 3])
         c.res_scale[layer, 1, h, 0] = np.float16(0.0625)
     out = o.decode(c, layer)
@@ -246,14 +280,14 @@ def pin_closed_forms(o):
     c = small_cache(levels=(2,), probs=(1.0,), head_dim=16, basis_rank=4, batch=1,
                     ragged=None, context=2)
     layer = 0
-    c.coef[layer] = 0
+    zero_coefs(c, layer)
     for h in range(Hk):
         set_entries(c, layer, 0, h, 0, [1, 9], [2, 0])      # K_hat_0 = 2 s0 e_1
         set_entries(c, layer, 0, h, 1, [4, 9], [-1, 0])     # K_hat_1 = -s1 e_4
         c.res_scale[layer, 0, h, 0] = np.float16(0.5)
         c.res_scale[layer, 0, h, 1] = np.float16(0.25)
-        c.coef[layer, 1, h, 0, 0] = 1.0
-        c.coef[layer, 1, h, 1, 0] = 0.0
+        coef_set(c, layer, 1, h, 0, 0, 1.0)
+        coef_set(c, layer, 1, h, 1, 0, 0.0)
         set_entries(c, layer, 1, h, 0, [0, 1], [0, 0])
         set_entries(c, layer, 1, h, 1, [0, 1], [0, 0])
     q = np.zeros((1, Hq, c.head_dim))
@@ -292,9 +326,9 @@ def pin_reductions(o):
             t0, t1 = int(c.cu_seqlens[b]), int(c.cu_seqlens[b + 1])
             for hq in range(c.n_q_heads):
                 h = hq // 2
-                K = torch.tensor(c.coef[layer, 0, h, t0:t1].astype(np.float64)) @ \
+                K = torch.tensor(coef_rows(c, layer, 0, h)[t0:t1].astype(np.float64)) @ \
                     torch.tensor(c.basis[b, m, h, 0].astype(np.float64))
-                V = torch.tensor(c.coef[layer, 1, h, t0:t1].astype(np.float64)) @ \
+                V = torch.tensor(coef_rows(c, layer, 1, h)[t0:t1].astype(np.float64)) @ \
                     torch.tensor(c.basis[b, m, h, 1].astype(np.float64))
                 ref = _sdpa(_q64(o, c, layer)[b, hq][None], K.numpy(), V.numpy(), scale)[0]
                 if _rel(out[b, hq], ref) > 1e-12:
@@ -307,15 +341,15 @@ def pin_reductions(o):
         out = o.decode(c, layer)
         for hq in range(c.n_q_heads):
             h = hq // 2
-            ref = _sdpa(_q64(o, c, layer)[0, hq][None], c.coef[layer, 0, h].astype(np.float64),
-                        c.coef[layer, 1, h].astype(np.float64), 0.25)[0]
+            ref = _sdpa(_q64(o, c, layer)[0, hq][None], coef_rows(c, layer, 0, h).astype(np.float64),
+                        coef_rows(c, layer, 1, h).astype(np.float64), 0.25)[0]
             if _rel(out[0, hq], ref) > 1e-12:
                 return f"R1 mismatch layer={layer} hq={hq}"
     # R2: full-rank residual (every channel), no basis term: attention over the
     # dequantised dense int4 cache, built here entry by entry.
     c = small_cache(levels=(16,), probs=(1.0,), head_dim=16, basis_rank=4, context=25,
                     ragged=None, batch=1)
-    c.coef[:] = 0
+    zero_coefs(c)
     for layer in range(c.n_layers):
         out = o.decode(c, layer)
         m = layer // c.window
@@ -351,7 +385,12 @@ def pin_invariants(o):
     # another sequence's data does not leak
     c3 = copy.deepcopy(c)
     t0, t1 = int(c.cu_seqlens[0]), int(c.cu_seqlens[1])
-    c3.coef[:, :, :, t0:t1] = -c3.coef[:, :, :, t0:t1]
+    for layer in range(c3.n_layers):
+        for z in range(2):
+            for h in range(c3.n_kv_heads):
+                rows = coef_rows(c3, layer, z, h)
+                rows[t0:t1] = -rows[t0:t1]
+                set_coef_rows(c3, layer, z, h, rows)
     out3 = o.decode(c3, layer)
     if np.abs(out3[1:] - out[1:]).max() != 0:
         return "sequence 0's data changed another sequence's output"
@@ -385,7 +424,9 @@ def permute_tokens(cache, b, seed):
         m = layer // cache.window
         for z in range(2):
             for h in range(Hk):
-                c.coef[layer, z, h, t0:t1] = cache.coef[layer, z, h, perm]
+                rows = coef_rows(cache, layer, z, h)
+                rows[t0:t1] = rows[perm]
+                set_coef_rows(c, layer, z, h, rows)
                 c.res_scale[layer, z, h, t0:t1] = cache.res_scale[layer, z, h, perm]
                 # gather entries token by token in the new order
                 idx, codes = [], []
@@ -409,7 +450,8 @@ def pin_probe(o):
                     levels=(0, 2), probs=(0.5, 0.5))
     _perm_basis(c, 13)
     rng = np.random.default_rng(14)
-    c.coef[:] = rng.integers(-3, 4, size=c.coef.shape).astype(np.float16)
+    c.coef_k[:] = rng.integers(-3, 4, size=c.coef_k.shape).astype(np.float16)
+    c.coef_v[:] = rng.integers(-3, 4, size=c.coef_v.shape).astype(np.float16)
     c.res_scale[:] = np.float16(0.5)
     layer = 2
     heads = [1, 0]

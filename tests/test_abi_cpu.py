@@ -54,7 +54,7 @@ FAKE = 1 << 20   # never dereferenced: every call below fails its host-side chec
 
 def decode_status(lib, d, layer=0, qtype=0, ws=1 << 30, cache_ok=True, q=FAKE, out=FAKE, probe=None):
     from paper_2607_06523_amd import binding
-    c = binding.Cache(*([FAKE] * 7)) if cache_ok else binding.Cache(FAKE, 0, FAKE, FAKE, FAKE, FAKE, FAKE)
+    c = binding.Cache(*([FAKE] * 8)) if cache_ok else binding.Cache(FAKE, FAKE, 0, FAKE, FAKE, FAKE, FAKE, FAKE)
     return lib.dwkv_decode(C.byref(d), C.byref(c), layer, q, qtype, 0.0, out,
                            C.byref(probe) if probe is not None else None, FAKE, ws, None)
 
@@ -142,7 +142,7 @@ def test_route_and_map_argument_checks(lib):
     assert need > 0
     assert lib.dwkv_route(C.byref(d), FAKE, 0, FAKE, FAKE, FAKE, FAKE, need, None) == 1
     from paper_2607_06523_amd import binding
-    c = binding.Cache(*([FAKE] * 7))
+    c = binding.Cache(*([FAKE] * 8))
     assert lib.dwkv_residual_map(C.byref(d), C.byref(c), 0, 2, 0, 0, 10, FAKE, None) == 2
     assert lib.dwkv_residual_map(C.byref(d), C.byref(c), 0, 0, 0, 10, 5, FAKE, None) == 2
     assert lib.dwkv_residual_map(C.byref(d), C.byref(c), 0, 0, 0, 0, 3001, FAKE, None) == 2

@@ -91,7 +91,7 @@ def _needles(host, layer, n_needles, seed, scale_q=1.0):
             dirn = qt / np.linalg.norm(qt)
             lam = (np.log(t1 - t0) + 3.0) / (np.linalg.norm(qt) / np.sqrt(host.head_dim))
             for t in rng.choice(np.arange(t0, t1), size=min(n_needles, t1 - t0), replace=False):
-                host.coef[layer, 0, h, t] = (lam * dirn).astype(np.float16)
+                host.coef_k[layer, h, t] = (lam * dirn).astype(np.float16)
 
 
 def test_needles_and_peaked_queries():

@@ -19,9 +19,9 @@ def _reconstruct_variant(kind):
         m = F.window_of(layer, cache.window)
         t0, t1 = int(cache.cu_seqlens[b]), int(cache.cu_seqlens[b + 1])
         zb = 1 - z if kind == "other_basis" else z
-        A = cache.coef[layer, z, h, t0:t1].astype(np.float64)
+        A = F.coefficient_rows(cache, layer, z, h, t0, t1)
         if kind == "coef_shift":
-            A = cache.coef[layer, z, h, t0 + 1:t1 + 1].astype(np.float64)
+            A = F.coefficient_rows(cache, layer, z, h, t0 + 1, t1 + 1)
             A = np.concatenate([A, np.zeros((t1 - t0 - A.shape[0], A.shape[1]))])
         X = A @ cache.basis[b, m, h, zb].astype(np.float64)
         if kind == "no_residual":
@@ -125,6 +125,9 @@ MUTANTS = {
     "router score summed in reverse": [(R, "router_score", _router_reordered)],
     "router ties go up": [(R, "level_index", _level_ge)],
     "inclusive offsets": [(R, "route", _route_inclusive)],
+    "value blocks read row-major": [(F, "coefficient_rows", lambda cache, layer, z, h, t0, t1:
+        cache.coef_k[layer, h, t0:t1].astype(np.float64) if z == 0 else
+        cache.coef_v[layer, h].reshape(-1, cache.coef_v.shape[3])[t0:t1].astype(np.float64))],
     "bf16 query read as fp16": [(F, "q_to_f64", lambda bits, dtype: np.asarray(bits, np.uint16)
                                  .view(np.float16).astype(np.float64))],
 }

@@ -26,8 +26,10 @@ def _refs(host, layer, heads, noise, seed):
 def _run_probe(dc, layer, heads, K, V, eps=1e-6):
     torch = torch_gpu()
     from paper_2607_06523_amd import ProbeRef
+    from synth.layout import block_values
+    Vb = block_values(V)                       # values in the 16-token blocked layout
     pr = ProbeRef(list(heads), torch.from_numpy(K.view(np.uint16)).view(torch.float16).cuda(),
-                  torch.from_numpy(V.view(np.uint16)).view(torch.float16).cuda(), eps)
+                  torch.from_numpy(Vb.view(np.uint16)).view(torch.float16).cuda(), eps)
     out, err, out_ref = dc.decode(layer, probe=pr)
     return out.cpu().numpy(), err.cpu().numpy(), out_ref.cpu().numpy()
 
@@ -71,7 +73,8 @@ def test_probe_closed_forms():
     host = generate(w, threads=2)
     pins._perm_basis(host, 21)
     rng = np.random.default_rng(22)
-    host.coef[:] = rng.integers(-3, 4, size=host.coef.shape).astype(np.float16)
+    host.coef_k[:] = rng.integers(-3, 4, size=host.coef_k.shape).astype(np.float16)
+    host.coef_v[:] = rng.integers(-3, 4, size=host.coef_v.shape).astype(np.float16)
     host.res_scale[:] = np.float16(0.5)
     dc = device_cache(host, split_tokens=256)
     K, V = _refs(host, 0, [0, 1], 0.0, 0)
