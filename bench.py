@@ -53,7 +53,8 @@ def dense_fp16_bytes_per_layer(host) -> float:
 
 def cpu_baseline(host, n_pairs: int, budget_s: float):
     """The float64 oracle, as it stands, on a bounded sample of the same step:
-    n_pairs (layer, KV head) slabs; extrapolated to the whole step."""
+    up to n_pairs (layer, KV head) slabs within budget_s seconds, extrapolated
+    to the whole step when the sample is not all of it."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -63,7 +64,8 @@ def cpu_baseline(host, n_pairs: int, budget_s: float):
     L, Hk, B = host.n_layers, host.n_kv_heads, host.batch
     pairs = [(l, h) for l in range(L) for h in range(Hk)]
     rng = np.random.default_rng(0)
-    sample = [pairs[i] for i in rng.choice(len(pairs), size=min(n_pairs, len(pairs)), replace=False)]
+    n_pairs = len(pairs) if n_pairs <= 0 else min(n_pairs, len(pairs))
+    sample = [pairs[i] for i in rng.choice(len(pairs), size=n_pairs, replace=False)]
     t0 = time.perf_counter()
     done = 0
     for l, h in sample:
@@ -74,8 +76,27 @@ def cpu_baseline(host, n_pairs: int, budget_s: float):
     dt = time.perf_counter() - t0
     step_s = dt / done * len(pairs)
     return {"value": B / step_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} of {len(pairs)} (layer, KV head) slabs of one decode step, "
-                      f"{dt:.1f} s, extrapolated to the full step ({step_s:.1f} s)"}
+            "sample": (f"all {len(pairs)} (layer, KV head) slabs of one decode step, {dt:.1f} s"
+                       if done == len(pairs) else
+                       f"{done} of {len(pairs)} (layer, KV head) slabs of one decode step, "
+                       f"{dt:.1f} s, extrapolated to the full step ({step_s:.1f} s)")}
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per split-kernel launch from the committed rocprofv3 counter
+    profile, or None when that profile is missing or was taken on a different
+    kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"split_kernel_{workload}_hbm_bytes.json")
+    src = os.path.join(ROOT, "paper_2607_06523_amd", "csrc", "decode.hip")
+    try:
+        rec = json.load(open(path))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != sha:
+        return None
+    return float(rec["traffic_bytes_per_launch"])
 
 
 def main():
@@ -88,9 +109,12 @@ def main():
     ap.add_argument("--variant", default="full", choices=["full", "bases-only"],
                     help="bases-only: every routed residual rank 0 (shared bases only)")
     ap.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
-    ap.add_argument("--cpu-pairs", type=int, default=24)
-    ap.add_argument("--cpu-budget", type=float, default=25.0)
+    ap.add_argument("--cpu-pairs", type=int, default=0, help="slabs to time on the CPU (0 = all)")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="before timing, run one plain device copy of this many MiB (a known-size "
+                         "reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -123,6 +147,16 @@ def main():
         for l in range(L):
             dc.decode(l, out=outs[l], workspace=ws)
 
+    if args.copy_calib_mib > 0:
+        n = args.copy_calib_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log(f"[bench] calibration copy: {args.copy_calib_mib} MiB read + {args.copy_calib_mib} MiB written")
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -137,11 +171,15 @@ def main():
             graph.replay()
         torch.cuda.synchronize()
 
-    # timed region: K steps; per-call events on the stream the kernels run on
+    # timed region: K steps.  The last step runs every layer as its two halves:
+    # first the split-K pass of all L layers back to back (each layer into its
+    # own workspace), then the L merges, with one event pair around each run on
+    # the kernels' stream.  That times the split-K kernel (the dominant one) on
+    # its own without an event between every pair of launches.
     ev_step = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    ev_calls = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                for _ in range(L)] if graph is None else None
-    call_ms = []
+    ev_calls = [torch.cuda.Event(enable_timing=True) for _ in range(3)] if graph is None else None
+    ws_layer = [torch.empty(dc.workspace_bytes(), dtype=torch.uint8, device="cuda") for _ in range(L)] \
+        if graph is None else None
     torch.cuda.synchronize()
     ev_step[0].record(stream)
     wall0 = time.perf_counter()
@@ -149,10 +187,13 @@ def main():
         if graph is not None:
             graph.replay()
         elif k == args.steps - 1:
-            for l in range(L):       # last step: time every call on its own
-                ev_calls[l][0].record(stream)
-                dc.decode(l, out=outs[l], workspace=ws)
-                ev_calls[l][1].record(stream)
+            ev_calls[0].record(stream)
+            for l in range(L):
+                dc.decode_partials(l, workspace=ws_layer[l])
+            ev_calls[1].record(stream)
+            for l in range(L):
+                dc.decode_merge(out=outs[l], workspace=ws_layer[l])
+            ev_calls[2].record(stream)
         else:
             step()
     ev_step[1].record(stream)
@@ -160,19 +201,22 @@ def main():
     wall = time.perf_counter() - wall0
     total_ms = ev_step[0].elapsed_time(ev_step[1])
     ms_per_step = total_ms / args.steps
+    split_ms = merge_ms = None
     if ev_calls is not None:
-        call_ms = [a.elapsed_time(b) for a, b in ev_calls]
+        split_ms = ev_calls[0].elapsed_time(ev_calls[1]) / L
+        merge_ms = ev_calls[1].elapsed_time(ev_calls[2]) / L
 
     bytes_layer = algorithmic_bytes_per_layer(host)
     bytes_step = float(sum(bytes_layer))
     tok_s = host.batch / (ms_per_step / 1e3)
     step_gbps = bytes_step / (ms_per_step / 1e3) / 1e9
-    if call_ms:
-        avg_call_ms = float(np.mean(call_ms))
-        achieved = float(np.mean(bytes_layer)) / (avg_call_ms / 1e3) / 1e9
+    if split_ms is not None:
+        avg_split_ms = float(split_ms)
+        achieved = float(np.mean(bytes_layer)) / (avg_split_ms / 1e3) / 1e9
     else:
-        avg_call_ms = ms_per_step / L
+        avg_split_ms = ms_per_step / L
         achieved = step_gbps
+    traffic = measured_traffic(wl.name) if args.variant == "full" and args.split == 0 else None
     result = {
         "metric": "compressed-KV decode attn tokens/s at 64K ctx (plus achieved HBM GB/s)",
         "value": round(tok_s, 2),
@@ -192,11 +236,13 @@ def main():
                    "levels": list(wl.levels), "split_tokens": dc.split_tokens,
                    "graph": bool(graph is not None)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None},
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "kernel": "split_kernel (split-K partials pass)"},
         "step_gbps": round(step_gbps, 1),
         "bytes_per_step": int(bytes_step),
         "bytes_per_layer_call": int(np.mean(bytes_layer)),
-        "avg_layer_call_ms": round(avg_call_ms, 5),
+        "split_kernel_ms": round(avg_split_ms, 5),
+        "merge_kernel_ms": round(float(merge_ms), 5) if merge_ms is not None else None,
         "compression_vs_fp16": round(dense_fp16_bytes_per_layer(host) / np.mean(bytes_layer), 3),
         "kv_token_layers_per_s": round(host.total_tokens * L / (ms_per_step / 1e3), 1),
         "wall_s_timed": round(wall, 3),

@@ -163,6 +163,29 @@ class DeviceCache:
         binding.check(st, "dwkv_decode")
         return out if probe is None else (out, err, out_ref)
 
+    def decode_partials(self, layer: int, q=None, sm_scale: float | None = None, workspace=None):
+        """First half of decode: the split-K pass (no probe); dwkv_decode_merge finishes it."""
+        torch = self.torch
+        if q is None:
+            q = self.q[layer]
+        qt = F16 if q.dtype == torch.float16 else BF16
+        ws = workspace if workspace is not None else self.workspace(None)
+        st = self.lib.dwkv_decode_partials(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(q), qt,
+                                           float(sm_scale or 0.0), None, _ptr(ws), ws.numel(),
+                                           _stream(torch, self.device))
+        binding.check(st, "dwkv_decode_partials")
+
+    def decode_merge(self, out=None, workspace=None):
+        """Second half of decode: merges the split partials into out [B,Hq,d]."""
+        torch = self.torch
+        if out is None:
+            out = torch.empty((self.batch, self.n_q_heads, self.head_dim), dtype=torch.float32, device=self.device)
+        ws = workspace if workspace is not None else self.workspace(None)
+        st = self.lib.dwkv_decode_merge(C.byref(self.dims), _ptr(out), None, _ptr(ws), ws.numel(),
+                                        _stream(torch, self.device))
+        binding.check(st, "dwkv_decode_merge")
+        return out
+
     def route(self, phi, u, theta, rank_code=None, res_off=None):
         """Eq. 2 routing on the GPU; returns (rank_code uint8 [M,Hkv,T], res_off int32-view [M,Hkv,T+1])."""
         torch = self.torch

@@ -132,22 +132,31 @@ size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe) {
   return ws_layout(dims, probe).total;
 }
 
-dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
-                        int32_t q_type, float sm_scale, float* out, const dwkv_probe* probe,
-                        void* workspace, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+dwkv_status check_decode_common(const dwkv_dims* d, const dwkv_probe* probe, void* workspace,
+                                size_t ws_bytes) {
   dwkv_status st = check_dims(d);
   if (st != DWKV_OK) return st;
-  if (!c || !q || !out || !workspace) return DWKV_E_NULL;
+  if (!workspace) return DWKV_E_NULL;
+  if ((st = check_probe(d, probe)) != DWKV_OK) return st;
+  if (ws_bytes < ws_layout(d, probe).total) return DWKV_E_WORKSPACE;
+  return DWKV_OK;
+}
+
+// Split-K pass(es): partial (o, m, l) per (work item, head slot, group member).
+dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
+                           int32_t q_type, float sm_scale, const dwkv_probe* probe, void* workspace,
+                           hipStream_t s) {
+  if (!c || !q) return DWKV_E_NULL;
   if (!c->basis || !c->coef_k || !c->coef_v || !c->res_off || !c->res_idx || !c->res_val ||
       !c->res_scale)
     return DWKV_E_NULL;
   if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
   if (q_type != DWKV_F16 && q_type != DWKV_BF16) return DWKV_E_DIMS;
-  if ((st = check_probe(d, probe)) != DWKV_OK) return st;
   const WsLayout wl = ws_layout(d, probe);
-  if (ws_bytes < wl.total) return DWKV_E_WORKSPACE;
-
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int G = d->n_q_heads / d->n_kv_heads;
   const int RB = d->basis_rank;
   const int64_t T = d->total_tokens;
@@ -158,10 +167,9 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   const int split = plan_split(d);
   const int64_t nw = count_work(d, split);
   if (nw > 0x7fffffff) return DWKV_E_UNSUPPORTED;
+  if (nw == 0) return DWKV_OK;
   if (!(sm_scale > 0.f)) sm_scale = 1.0f / std::sqrt((float)kHeadDim);
   char* ws = static_cast<char*>(workspace);
-  float* part = reinterpret_cast<float*>(ws);
-  float* part_ref = reinterpret_cast<float*>(ws + wl.main_bytes);
   const uint16_t* scale = static_cast<const uint16_t*>(c->res_scale);
 
   SplitArgs a;
@@ -179,7 +187,7 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   a.scale_v = scale + ((int64_t)layer * 2 + 1) * Hk * T;
   a.q = static_cast<const uint16_t*>(q);
   a.cu = d->cu_seqlens;
-  a.part = part;
+  a.part = reinterpret_cast<float*>(ws);
   a.T = T;
   a.res_stride = d->res_stride;
   a.batch = d->batch;
@@ -190,25 +198,30 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   a.q_bf16 = q_type == DWKV_BF16;
   a.qscale = sm_scale * 1.4426950408889634f;
   for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
-
-  const bool resid = max_level(d) > 0;
-  if (nw > 0) {
-    if (launch_split(RB, G, resid, false, a, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
-    if (probe) {
-      SplitArgs r = a;
-      r.coef_k = static_cast<const uint16_t*>(probe->k_ref);
-      r.coef_v = static_cast<const uint16_t*>(probe->v_ref);
-      r.part = part_ref;
-      r.n_slots = probe->n_heads;
-      for (int i = 0; i < probe->n_heads; ++i) r.kv_of_slot[i] = probe->kv_heads_host[i];
-      if (launch_split(kHeadDim, G, false, true, r, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
-    }
+  if (launch_split(RB, G, max_level(d) > 0, false, a, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
+  if (probe) {
+    SplitArgs r = a;
+    r.coef_k = static_cast<const uint16_t*>(probe->k_ref);
+    r.coef_v = static_cast<const uint16_t*>(probe->v_ref);
+    r.part = reinterpret_cast<float*>(ws + wl.main_bytes);
+    r.n_slots = probe->n_heads;
+    for (int i = 0; i < probe->n_heads; ++i) r.kv_of_slot[i] = probe->kv_heads_host[i];
+    if (launch_split(kHeadDim, G, false, true, r, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
   }
-  // the merge also writes the zero outputs of empty sequences
+  return DWKV_OK;
+}
+
+// Merge pass: output rows (and Eq. 3 for probed heads); also writes the zero
+// outputs of empty sequences.
+dwkv_status merge_phase(const dwkv_dims* d, float* out, const dwkv_probe* probe, void* workspace,
+                        hipStream_t s) {
+  if (!out) return DWKV_E_NULL;
+  const WsLayout wl = ws_layout(d, probe);
+  char* ws = static_cast<char*>(workspace);
   MergeArgs mg;
   std::memset(&mg, 0, sizeof(mg));
-  mg.part = part;
-  mg.part_ref = probe ? part_ref : nullptr;
+  mg.part = reinterpret_cast<const float*>(ws);
+  mg.part_ref = probe ? reinterpret_cast<const float*>(ws + wl.main_bytes) : nullptr;
   mg.out = out;
   mg.err = probe ? probe->err : nullptr;
   mg.out_ref = probe ? probe->out_ref : nullptr;
@@ -216,13 +229,44 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   mg.batch = d->batch;
   mg.n_q_heads = d->n_q_heads;
   mg.n_kv_heads = d->n_kv_heads;
-  mg.split = split;
+  mg.split = plan_split(d);
   mg.n_probe = probe ? probe->n_heads : 0;
   mg.eps = probe ? probe->eps : 0.f;
   for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) mg.probe_slot_of_kv[h] = -1;
   if (probe)
     for (int i = 0; i < probe->n_heads; ++i) mg.probe_slot_of_kv[probe->kv_heads_host[i]] = i;
   return hip_status(launch_merge(mg, s));
+}
+
+}  // namespace
+
+extern "C" {
+
+dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
+                        int32_t q_type, float sm_scale, float* out, const dwkv_probe* probe,
+                        void* workspace, size_t ws_bytes, void* stream) {
+  dwkv_status st = check_decode_common(d, probe, workspace, ws_bytes);
+  if (st != DWKV_OK) return st;
+  if (!out) return DWKV_E_NULL;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if ((st = partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, s)) != DWKV_OK) return st;
+  return merge_phase(d, out, probe, workspace, s);
+}
+
+dwkv_status dwkv_decode_partials(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
+                                 int32_t q_type, float sm_scale, const dwkv_probe* probe, void* workspace,
+                                 size_t ws_bytes, void* stream) {
+  dwkv_status st = check_decode_common(d, probe, workspace, ws_bytes);
+  if (st != DWKV_OK) return st;
+  return partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace,
+                        reinterpret_cast<hipStream_t>(stream));
+}
+
+dwkv_status dwkv_decode_merge(const dwkv_dims* d, float* out, const dwkv_probe* probe, void* workspace,
+                              size_t ws_bytes, void* stream) {
+  dwkv_status st = check_decode_common(d, probe, workspace, ws_bytes);
+  if (st != DWKV_OK) return st;
+  return merge_phase(d, out, probe, workspace, reinterpret_cast<hipStream_t>(stream));
 }
 
 size_t dwkv_route_workspace_bytes(const dwkv_dims* d) {

@@ -166,3 +166,15 @@ def test_determinism_and_split_invariance():
     ref = oracle.decode(host, 2, heads=[(0, 0), (0, 3)])
     for split, o in outs.items():
         compare(o, ref, [(0, 0), (0, 3)], 4, f"split {split}")
+
+
+def test_two_phase_calls_equal_decode():
+    """dwkv_decode_partials + dwkv_decode_merge give dwkv_decode's output bit for bit."""
+    torch_gpu()
+    host = generate(BATCH16.with_(n_layers=2), layers=(0, 2))
+    dc = device_cache(host)
+    announce("two-phase decode batch16 layer 1")
+    full = dc.decode(1).cpu().numpy()
+    dc.decode_partials(1)
+    two = dc.decode_merge().cpu().numpy()
+    assert np.array_equal(full, two)
