@@ -198,7 +198,10 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   a.q_bf16 = q_type == DWKV_BF16;
   a.qscale = sm_scale * 1.4426950408889634f;
   for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
-  if (launch_split(RB, G, max_level(d) > 0, false, a, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
+  const hipError_t e = token_lane_supported(RB, G, max_level(d))
+                           ? launch_split_tl(RB, G, max_level(d) > 0, a, (int)nw, s)
+                           : launch_split(RB, G, max_level(d) > 0, false, a, (int)nw, s);
+  if (e != hipSuccess) return DWKV_E_HIP;
   if (probe) {
     SplitArgs r = a;
     r.coef_k = static_cast<const uint16_t*>(probe->k_ref);

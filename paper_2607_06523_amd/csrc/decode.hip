@@ -43,6 +43,7 @@ namespace {
 
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 
 constexpr int D = kHeadDim;
 
@@ -59,6 +60,9 @@ __device__ __forceinline__ void wave_lds_fence() {
 }
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// s_waitcnt immediate for gfx9: vmcnt(0), expcnt and lgkmcnt left at their maxima.
+constexpr int kWaitVmcnt0 = 0x0F70;
 
 __device__ __forceinline__ uint32_t dword_at(const uint4& v, int i) {
   return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
@@ -196,8 +200,13 @@ __device__ __forceinline__ void load_scales(Meta& m, const Ctx& x, int j, int la
   m.sv = x.sv[t];
 }
 
+// The load is unconditional, its address clamped into the slab, so every wave
+// issues the same sequence of vector loads whatever the data and the compiler
+// can wait for each load by its exact position in the queue.  Bytes at or past
+// the slab end are never used (a tile's entries end before it), so the value
+// read for a clamped position does not matter.
 __device__ __forceinline__ uint32_t load_dword_clamped(const uint8_t* base, int64_t pos, int64_t len) {
-  return pos + 4 <= len ? *reinterpret_cast<const uint32_t*>(base + pos) : 0u;
+  return *reinterpret_cast<const uint32_t*>(base + min(pos, len - 4));
 }
 
 template <int TT>
@@ -218,16 +227,13 @@ template <int TT>
 __device__ __forceinline__ void load_entries(Ent& en, const Ctx& x, const Meta& m, int lane) {
   uint32_t e0, e1;
   tile_entry_range<TT>(m, e0, e1);
-  en.ik[0] = en.ik[1] = en.iv[0] = en.iv[1] = en.vk = en.vv = 0u;
-  if (e1 > e0) {
-    const int64_t ia = chunk_base(e0), va = ia >> 1;
-    en.ik[0] = load_dword_clamped(x.idx[0], ia + 4 * lane, x.res_stride);
-    en.ik[1] = load_dword_clamped(x.idx[0], ia + 256 + 4 * lane, x.res_stride);
-    en.iv[0] = load_dword_clamped(x.idx[1], ia + 4 * lane, x.res_stride);
-    en.iv[1] = load_dword_clamped(x.idx[1], ia + 256 + 4 * lane, x.res_stride);
-    en.vk = load_dword_clamped(x.val[0], va + 4 * lane, x.res_stride / 2);
-    en.vv = load_dword_clamped(x.val[1], va + 4 * lane, x.res_stride / 2);
-  }
+  const int64_t ia = chunk_base(e0), va = ia >> 1;
+  en.ik[0] = load_dword_clamped(x.idx[0], ia + 4 * lane, x.res_stride);
+  en.ik[1] = load_dword_clamped(x.idx[0], ia + 256 + 4 * lane, x.res_stride);
+  en.iv[0] = load_dword_clamped(x.idx[1], ia + 4 * lane, x.res_stride);
+  en.iv[1] = load_dword_clamped(x.idx[1], ia + 256 + 4 * lane, x.res_stride);
+  en.vk = load_dword_clamped(x.val[0], va + 4 * lane, x.res_stride / 2);
+  en.vv = load_dword_clamped(x.val[1], va + 4 * lane, x.res_stride / 2);
 }
 
 // Key residual, one lane per token: the lane walks its own entries (no
@@ -333,6 +339,10 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
   const int64_t t0 = tile_start<RB>(x, j);
   const int jn = j + kWaves, jnn = j + 2 * kWaves;
   const bool has_next = jn < x.ntile;
+  // past the wave's last tile the prefetches re-read a tile of this chunk
+  // (cache resident, results unused) so the load sequence stays the same
+  const int jn_l = has_next ? jn : j;
+  const int jnn_l = jnn < x.ntile ? jnn : jn_l;
 
   // 1. stage this tile's residual entries; request the next tiles' metadata
   uint32_t e0 = 0, e1 = 0, ia = 0;
@@ -348,11 +358,9 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
     reinterpret_cast<uint32_t*>(ws.eidx[1])[lane + 64] = ec.iv[1];
     reinterpret_cast<uint32_t*>(ws.eval[0])[lane] = ec.vk;
     reinterpret_cast<uint32_t*>(ws.eval[1])[lane] = ec.vv;
-    if (has_next) {
-      if (jnn < x.ntile) load_offsets<RB>(mnn, x, jnn, lane);
-      load_entries<TT>(en, x, mn, lane);
-      load_scales<RB>(mn, x, jn, lane);
-    }
+    load_offsets<RB>(mnn, x, jnn_l, lane);
+    load_entries<TT>(en, x, mn, lane);
+    load_scales<RB>(mn, x, jn_l, lane);
     wave_lds_fence();
   }
 
@@ -368,7 +376,7 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
       sacc[bk] = mfma16(av, st.qlo[s], sacc[bk]);
     }
   }
-  if (has_next) load_k<RB>(fr, x, jn, lane);
+  load_k<RB>(fr, x, jn_l, lane);
 
   // 3. key residual entries add q[c]*code*scale to their token's score
   if constexpr (RESID) {
@@ -456,7 +464,7 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
       st.acc[cb] = mfma16(pl, vf, st.acc[cb]);
     }
   }
-  if (has_next) load_v<RB>(fr, x, jn, lane);
+  load_v<RB>(fr, x, jn_l, lane);
 
   // 9. value residual entries scatter p*code*scale into their channel
   if constexpr (RESID) {
@@ -514,55 +522,52 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   const uint16_t* bk_rows = IDENT ? nullptr : a.basis + (int64_t)b * a.basis_b_stride + (int64_t)kvh * 2 * RB * D;
   const uint16_t* bv_rows = IDENT ? nullptr : bk_rows + RB * D;
 
-  // the query, B^K rows and B^V rows are requested together
+  // Requests in issue order (vector loads complete in order): the first
+  // tile's offsets and scales; the query, B^K rows and B^V rows; the first
+  // tile's coefficient fragments; last its residual entries, whose addresses
+  // need the offsets.  Every load is unconditional (a wave with no tile reads
+  // the chunk's last one and never uses it).
   constexpr int NIT = (RB * 4 + kThreads - 1) / kThreads;   // q~ work items per thread
   constexpr int QPT = (G * D + kThreads - 1) / kThreads;     // query elements per thread
   constexpr int BVQ = IDENT ? 1 : RB * D / 8 / kThreads;     // 16-byte B^V chunks per thread
-  uint4 rv[NIT][4];
-  uint16_t qraw[QPT];
-  uint4 bvr[BVQ];
-  if constexpr (!IDENT) {
-#pragma unroll
-    for (int n = 0; n < NIT; ++n) {
-      const int it = tid + n * kThreads;
-      if (it < RB * 4) {
-        const uint4* row = reinterpret_cast<const uint4*>(bk_rows + (it >> 2) * D + (it & 3) * 32);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) rv[n][i] = row[i];
-      }
-    }
-#pragma unroll
-    for (int n = 0; n < BVQ; ++n) bvr[n] = reinterpret_cast<const uint4*>(bv_rows)[tid + n * kThreads];
-  }
-#pragma unroll
-  for (int n = 0; n < QPT; ++n) {
-    const int i = tid + n * kThreads;
-    qraw[n] = i < G * D ? a.q[((int64_t)b * a.n_q_heads + kvh * G + i / D) * D + i % D] : 0;
-  }
-  // then the wave's first tile (its residual entries once its offsets are in)
+  const int j0 = min(wv, x.ntile - 1);
+  const int j1 = min(wv + kWaves, x.ntile - 1);
   Frags<RB> fr;
   Meta mc{}, mn{}, mnn{};
   Ent ec{}, en{};
-  if (wv < x.ntile) {
-    if constexpr (RESID) {
-      load_offsets<RB>(mc, x, wv, lane);
-      if (wv + kWaves < x.ntile) load_offsets<RB>(mn, x, wv + kWaves, lane);
-      load_scales<RB>(mc, x, wv, lane);
-    }
-    load_k<RB>(fr, x, wv, lane);
-    load_v<RB>(fr, x, wv, lane);
-    if constexpr (RESID) load_entries<TT>(ec, x, mc, lane);
+  if constexpr (RESID) {
+    load_offsets<RB>(mc, x, j0, lane);
+    load_scales<RB>(mc, x, j0, lane);
+    load_offsets<RB>(mn, x, j1, lane);
   }
+  __builtin_amdgcn_sched_barrier(0);
+  uint4 rv[NIT][4];
+  uint16_t qraw[QPT];
+#pragma unroll
+  for (int n = 0; n < QPT; ++n) {
+    const int i = min(tid + n * kThreads, G * D - 1);
+    qraw[n] = a.q[((int64_t)b * a.n_q_heads + kvh * G + i / D) * D + i % D];
+  }
+  if constexpr (!IDENT) {
+#pragma unroll
+    for (int n = 0; n < NIT; ++n) {
+      const int it = min(tid + n * kThreads, RB * 4 - 1);
+      const uint4* row = reinterpret_cast<const uint4*>(bk_rows + (it >> 2) * D + (it & 3) * 32);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) rv[n][i] = row[i];
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  load_k<RB>(fr, x, j0, lane);
+  load_v<RB>(fr, x, j0, lane);
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (RESID) load_entries<TT>(ec, x, mc, lane);
   if (tid < G) sm.qmax[tid] = 0;
 #pragma unroll
   for (int n = 0; n < QPT; ++n) {
     const int i = tid + n * kThreads;
     if (i < G * D)
       sm.qs[i % D][i / D] = (a.q_bf16 ? bf16_bits_to_float(qraw[n]) : half_bits_to_float(qraw[n])) * a.qscale;
-  }
-  if constexpr (!IDENT) {
-#pragma unroll
-    for (int n = 0; n < BVQ; ++n) reinterpret_cast<uint4*>(&sm.bvs[0][0])[tid + n * kThreads] = bvr[n];
   }
   __syncthreads();
   if constexpr (!IDENT) {
@@ -638,10 +643,16 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
     for (int i = lane; i < G * D; i += 64) (&ws.racc[0][0])[i] = 0.f;
   }
 
+  // Every prologue load completes before the loop (the first iteration needs
+  // the last of them at once), so the loop's own waits count only the loop's
+  // loads and stay exact.
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+
   // stream the wave's tiles
   for (int j = wv; j < x.ntile; j += kWaves) step<RB, G, RESID>(st, fr, mc, mn, mnn, ec, en, j, x, sm, ws, lane);
 
-  // epilogue: merge the 4 waves, project a~ through B^V, write the partial
+  // epilogue: the 4 waves merge (B^V rows, needed only for the projection,
+  // are requested while they do), project a~ through B^V, write the partial
   const int c_out = tid % D, par = tid / D;
   st.l += __shfl_xor(st.l, 16);
   st.l += __shfl_xor(st.l, 32);
@@ -656,6 +667,11 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
       const int g = 4 * grp + i;
       if (g < G) sm.ep_a[wv][g][16 * cb + col] = st.acc[cb][i];
     }
+  u4v bvr[BVQ];
+  if constexpr (!IDENT) {
+#pragma unroll
+    for (int n = 0; n < BVQ; ++n) bvr[n] = reinterpret_cast<const u4v*>(bv_rows)[tid + n * kThreads];
+  }
   __syncthreads();
   if (tid < G) {
     const int g = tid;
@@ -669,6 +685,10 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
     }
     sm.mstar[g] = mx;
     sm.lstar[g] = l;
+  }
+  if constexpr (!IDENT) {
+#pragma unroll
+    for (int n = 0; n < BVQ; ++n) reinterpret_cast<u4v*>(&sm.bvs[0][0])[tid + n * kThreads] = bvr[n];
   }
   __syncthreads();
   for (int i = tid; i < G * RB; i += kThreads) {

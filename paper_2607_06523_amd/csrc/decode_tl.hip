@@ -1,0 +1,654 @@
+// Token-lane split-K decode attention over the cross-depth factorized KV cache,
+// gfx950, for query groups of at most 4 heads and basis ranks up to 64.
+//
+// Same arithmetic as the general kernel (Sec. 3, Eq. 1 used through its
+// linearity: scores A^K_t (B^K q) plus the routed residual channels, values
+// (sum_t p_t A^V_t) B^V plus the routed residual channels), organised so that
+// every lane of a wave owns one token of a 64-token tile for the whole step:
+//
+//  * scores on v_mfma_f32_16x16x16_f16 with the coefficient rows as the B
+//    operand (column = token) and q~ = B^K q as the A operand, its 4 head rows
+//    repeated in each of the 4 row groups.  The result of 16-token block bk then
+//    holds the 4 head scores of token 16bk+c in lane c of every lane group, and
+//    lane 16g+c keeps block g's copy: each lane ends up with its own token's
+//    scores for all heads, in registers.
+//  * the token's residual entries (channel bytes and int4 codes, one window per
+//    tile and lane straight from HBM) add code*q[c] to those scores (q from an
+//    LDS table) and, after the softmax, p*code*scale to a per-wave LDS
+//    accumulator of the value channels (ds_add_f32) - no staging, no entry map,
+//    no exchange between lanes.
+//  * softmax with a lazily moved reference: the running reference of a head
+//    moves only when a score exceeds it by more than 2^8, so probabilities stay
+//    below 256 and the rescaling of the value accumulators is rare.
+//  * values on v_mfma_f32_4x4x4f16 (16 blocks): a 4x4 transpose inside each
+//    lane quad turns the probabilities into (head, 4 tokens) rows; each
+//    instruction broadcasts one quad's rows to all blocks (CBSZ/ABID) and the
+//    blocks cover 64 coefficient channels, read as 4 consecutive tokens of one
+//    channel from the 16-token value blocks.  The accumulator holds, in lane c,
+//    the basis-space value of channel c for the 4 heads.
+//  * the epilogue and the partial format are those of the general kernel.
+#include <utility>
+
+#include "entry.h"
+#include "internal.h"
+
+namespace dwkv {
+namespace {
+
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+
+constexpr int D = kHeadDim;
+constexpr int TT = 64;                  // tokens per tile = lanes per wave
+constexpr int HG = 4;                   // head rows of the score and value products
+constexpr float kLazy = 8.0f;           // log2 headroom of the running reference
+constexpr int kMaxRank = 16;            // residual entries per token this kernel reads
+constexpr int kWaitVmcnt0 = 0x0F70;     // s_waitcnt immediate: vmcnt(0) only
+
+template <int RB>
+struct TCfg {
+  static constexpr int NS = RB / 16;    // k-steps of the score product
+  static constexpr int KH = RB / 4;     // coefficients of a row one lane holds
+  static_assert(RB % 16 == 0 && RB >= 16 && RB <= 64, "basis rank");
+};
+
+template <int RB, bool RESID>
+struct alignas(16) TSmem {
+  alignas(16) float qs[D][HG];          // q * sm_scale * log2(e), heads past G zero
+  float qt[HG][RB];                     // q~ = B^K q (scaled)
+  alignas(16) uint16_t bvs[RB][D];      // B^V rows (fp16 bits)
+  float ep_m[kWaves][HG];
+  float ep_l[kWaves][HG];
+  float ep_a[kWaves][HG][RB];
+  float sw[kWaves][HG];
+  float mstar[HG];
+  float lstar[HG];
+  float acomb[HG][RB];
+  int qmax[HG];
+  float racc[kWaves][RESID ? HG : 1][RESID ? D : 1];   // value-residual accumulators
+};
+
+template <int RB>
+struct TFrags {
+  uint2 k[4][TCfg<RB>::NS];             // key rows, block bk, k-step s
+  uint2 v[16];                          // value channel `lane`, token quad q
+};
+
+struct TMeta {
+  uint32_t oa, ob;                      // entry range of this lane's token
+  uint32_t sk, sv;                      // residual scale bits
+};
+
+struct TEnt {
+  uint32_t ck[5], vk[3];                // key channel bytes / codes around oa
+  uint32_t cv[5], vv[3];                // value channel bytes / codes around oa
+};
+
+template <int RB>
+struct TState {
+  h4 qhi[TCfg<RB>::NS], qlo[TCfg<RB>::NS];
+  f4 acc_h, acc_l;                      // a~[head][channel lane] from p hi / p lo
+  float m[HG], l[HG], down[HG];
+};
+
+struct TCtx {
+  const uint16_t* ck;
+  const uint16_t* cv;
+  const uint32_t* off;
+  const uint8_t* idx[2];
+  const uint8_t* val[2];
+  const uint16_t* sk;
+  const uint16_t* sv;
+  int64_t c0, c1, tb;
+  int64_t T, nblk, res_stride;
+  int ntile;
+};
+
+__device__ __forceinline__ int64_t clamp64(int64_t v, int64_t lo, int64_t hi) {
+  return v < lo ? lo : (v > hi ? hi : v);
+}
+
+__device__ __forceinline__ f4 mfma16(h4 a, h4 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ int64_t tstart(const TCtx& x, int j) { return x.tb + (int64_t)j * TT; }
+
+// signed 4-bit code in bits [4n, 4n+4) of w
+__device__ __forceinline__ float code_at(uint32_t w, int n) {
+  return (float)((int32_t)(w << (28 - 4 * n)) >> 28);
+}
+
+template <int RB>
+__device__ __forceinline__ void load_k(TFrags<RB>& f, const TCtx& x, int j, int lane) {
+  using C = TCfg<RB>;
+  const int64_t t0 = tstart(x, j);
+  const int grp = lane >> 4, col = lane & 15;
+#pragma unroll
+  for (int bk = 0; bk < 4; ++bk) {
+    const int64_t row = min(t0 + 16 * bk + col, x.T - 1);
+    const uint2* p = reinterpret_cast<const uint2*>(x.ck + row * RB + C::KH * grp);
+#pragma unroll
+    for (int s = 0; s < C::NS; ++s) f.k[bk][s] = p[s];
+  }
+}
+
+template <int RB>
+__device__ __forceinline__ void load_v(TFrags<RB>& f, const TCtx& x, int j, int lane) {
+  const int64_t b0 = tstart(x, j) >> 4;
+  const int c = min(lane, RB - 1);
+#pragma unroll
+  for (int q = 0; q < 16; q += 2) {
+    const int64_t blk = min(b0 + (q >> 2), x.nblk - 1);
+    const uint4 w = *reinterpret_cast<const uint4*>(x.cv + (blk * RB + c) * 16 + 4 * (q & 3));
+    f.v[q] = make_uint2(w.x, w.y);
+    f.v[q + 1] = make_uint2(w.z, w.w);
+  }
+}
+
+__device__ __forceinline__ void load_offsets(TMeta& m, const TCtx& x, int j, int lane) {
+  const int64_t t = tstart(x, j) + lane;
+  m.oa = x.off[clamp64(t, x.c0, x.c1)];
+  m.ob = x.off[clamp64(t + 1, x.c0, x.c1)];
+}
+
+__device__ __forceinline__ void load_scales(TMeta& m, const TCtx& x, int j, int lane) {
+  const int64_t t = clamp64(tstart(x, j) + lane, x.c0, x.c1 - 1);
+  m.sk = x.sk[t];
+  m.sv = x.sv[t];
+}
+
+// The windows around a token's entries: 20 channel bytes from oa rounded down
+// to 4 and 12 code bytes from oa/2 rounded down to 4 cover kMaxRank entries
+// (oa is even).  Addresses are clamped into the slab; bytes past a token's
+// entries are never used.
+__device__ __forceinline__ void load_entries(TEnt& e, const TCtx& x, const TMeta& m) {
+  const int64_t a = min((int64_t)(m.oa & ~3u), x.res_stride - 20);
+  const int64_t ca = min((int64_t)((m.oa >> 1) & ~3u), x.res_stride / 2 - 12);
+  const uint32_t* pk = reinterpret_cast<const uint32_t*>(x.idx[0] + a);
+  const uint32_t* pv = reinterpret_cast<const uint32_t*>(x.idx[1] + a);
+  const uint32_t* qk = reinterpret_cast<const uint32_t*>(x.val[0] + ca);
+  const uint32_t* qv = reinterpret_cast<const uint32_t*>(x.val[1] + ca);
+#pragma unroll
+  for (int i = 0; i < 5; ++i) e.ck[i] = pk[i];
+#pragma unroll
+  for (int i = 0; i < 3; ++i) e.vk[i] = qk[i];
+#pragma unroll
+  for (int i = 0; i < 5; ++i) e.cv[i] = pv[i];
+#pragma unroll
+  for (int i = 0; i < 3; ++i) e.vv[i] = qv[i];
+}
+
+// Channel bytes of entries [4w, 4w+4) of the token and its 16 codes, aligned.
+struct Window {
+  uint32_t ch[4];
+  uint32_t cd[2];
+};
+
+__device__ __forceinline__ Window align_window(const uint32_t* c5, const uint32_t* v3, uint32_t oa) {
+  Window w;
+  const uint32_t sc = oa & 3u, sv = (oa >> 1) & 3u;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w.ch[i] = __builtin_amdgcn_alignbyte(c5[i + 1], c5[i], sc);
+  w.cd[0] = __builtin_amdgcn_alignbyte(v3[1], v3[0], sv);
+  w.cd[1] = __builtin_amdgcn_alignbyte(v3[2], v3[1], sv);
+  return w;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// 4x4 transpose inside each lane quad: lane 4q+r holds row r (x[0..3]) on
+// entry and column r on exit.
+__device__ __forceinline__ void quad_transpose(float (&x)[4], int lane) {
+  const bool b1 = (lane & 2) != 0, b0 = (lane & 1) != 0;
+  float t[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)   // partner lane ^ 2
+    t[i] = __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x[i]), 0x4E, 0xF, 0xF, false));
+  if (b1) { x[0] = t[2]; x[1] = t[3]; } else { x[2] = t[0]; x[3] = t[1]; }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)   // partner lane ^ 1
+    t[i] = __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x[i]), 0xB1, 0xF, 0xF, false));
+  if (b0) { x[0] = t[1]; x[2] = t[3]; } else { x[1] = t[0]; x[3] = t[2]; }
+}
+
+template <int Q>
+__device__ __forceinline__ void pv_quad(f4& acc_h, f4& acc_l, h4 ph, h4 pl, uint2 v) {
+  const h4 b = __builtin_bit_cast(h4, v);
+  acc_h = __builtin_amdgcn_mfma_f32_4x4x4f16(ph, b, acc_h, 4, Q, 0);
+  acc_l = __builtin_amdgcn_mfma_f32_4x4x4f16(pl, b, acc_l, 4, Q, 0);
+}
+
+template <int... Q>
+__device__ __forceinline__ void pv_tile(f4& acc_h, f4& acc_l, h4 ph, h4 pl, const uint2 (&v)[16],
+                                        std::integer_sequence<int, Q...>) {
+  (pv_quad<Q>(acc_h, acc_l, ph, pl, v[Q]), ...);
+}
+
+template <int RB, int G, bool RESID>
+__device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc, TMeta& mn, TMeta& mnn,
+                                      TEnt& ec, TEnt& en, int j, const TCtx& x, TSmem<RB, RESID>& sm,
+                                      int wv, int lane) {
+  using C = TCfg<RB>;
+  constexpr int NS = C::NS;
+  const int grp = lane >> 4;
+  const int64_t t0 = tstart(x, j);
+  const int jn = j + kWaves, jnn = j + 2 * kWaves;
+  // past the wave's last tile the prefetches re-read a tile of this chunk
+  // (cache resident, results unused): the load sequence stays the same
+  const int jn_l = jn < x.ntile ? jn : j;
+  const int jnn_l = jnn < x.ntile ? jnn : jn_l;
+
+  // 1. metadata of the next tiles
+  if constexpr (RESID) {
+    load_offsets(mnn, x, jnn_l, lane);
+    load_entries(en, x, mn);
+    load_scales(mn, x, jn_l, lane);
+  }
+
+  // 2. scores: block bk lands in every lane group; lane group g keeps block g
+  f4 sacc[4];
+#pragma unroll
+  for (int bk = 0; bk < 4; ++bk) sacc[bk] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int bk = 0; bk < 4; ++bk) {
+      const h4 kf = __builtin_bit_cast(h4, fr.k[bk][s]);
+      sacc[bk] = mfma16(st.qhi[s], kf, sacc[bk]);
+      sacc[bk] = mfma16(st.qlo[s], kf, sacc[bk]);
+    }
+  load_k<RB>(fr, x, jn_l, lane);
+  float sc[HG];
+#pragma unroll
+  for (int i = 0; i < HG; ++i) {
+    const float a01 = grp == 0 ? sacc[0][i] : sacc[1][i];
+    const float a23 = grp == 2 ? sacc[2][i] : sacc[3][i];
+    sc[i] = (grp < 2 ? a01 : a23) * st.down[i];
+  }
+
+  // 3. key residual: this lane's entries add code * q[c] * scale
+  uint32_t rank = 0;
+  Window wk{}, wvv{};
+  if constexpr (RESID) {
+    rank = min(mc.ob - mc.oa, (uint32_t)kMaxRank);
+    if (mc.ob < mc.oa) rank = 0;
+    wk = align_window(ec.ck, ec.vk, mc.oa);
+    wvv = align_window(ec.cv, ec.vv, mc.oa);
+    float rk[HG] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int qd = 0; qd < kMaxRank / 4; ++qd) {
+      if (__ballot(rank > 4u * qd) == 0) break;
+      f4 qv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) qv[u] = *reinterpret_cast<const f4*>(&sm.qs[(wk.ch[qd] >> (8 * u)) & (D - 1)][0]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int k = 4 * qd + u;
+        const float code = (uint32_t)k < rank ? code_at(wk.cd[k >> 3], k & 7) : 0.f;
+#pragma unroll
+        for (int i = 0; i < G; ++i) rk[i] += code * qv[u][i];
+      }
+    }
+    const float rs = half_bits_to_float((uint16_t)mc.sk);
+#pragma unroll
+    for (int i = 0; i < G; ++i) sc[i] += rk[i] * rs;
+  }
+  {
+    const int64_t t = t0 + lane;
+    const bool valid = t >= x.c0 && t < x.c1;
+#pragma unroll
+    for (int i = 0; i < HG; ++i) sc[i] = (valid && i < G) ? sc[i] : -INFINITY;
+  }
+
+  // 4. softmax against the lazily moved reference
+  {
+    bool need = false;
+#pragma unroll
+    for (int i = 0; i < G; ++i) need |= sc[i] > st.m[i] + kLazy;
+    if (__ballot(need) != 0) {
+      float alpha[HG];
+#pragma unroll
+      for (int i = 0; i < HG; ++i) {
+        const float mnew = i < G ? fmaxf(st.m[i], wave_max(sc[i])) : st.m[i];
+        alpha[i] = mnew == -INFINITY ? 1.0f : exp2f(st.m[i] - mnew);
+        st.m[i] = mnew;
+        st.l[i] *= alpha[i];
+        st.acc_h[i] *= alpha[i];
+        st.acc_l[i] *= alpha[i];
+      }
+      if constexpr (RESID) {
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+          sm.racc[wv][i][lane] *= alpha[i];
+          sm.racc[wv][i][lane + 64] *= alpha[i];
+        }
+      }
+    }
+  }
+  float p[HG];
+#pragma unroll
+  for (int i = 0; i < HG; ++i) {
+    p[i] = sc[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[i] - st.m[i]);
+    st.l[i] += p[i];
+  }
+
+  // 5. a~ += P A^V: quad transpose, fp16 hi + lo, one 4x4x4 pair per quad
+  {
+    float pt[4] = {p[0], p[1], p[2], p[3]};
+    quad_transpose(pt, lane);
+    h4 ph, pl;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const _Float16 hh = (_Float16)pt[i];
+      ph[i] = hh;
+      pl[i] = (_Float16)(pt[i] - (float)hh);
+    }
+    pv_tile(st.acc_h, st.acc_l, ph, pl, fr.v, std::make_integer_sequence<int, 16>{});
+  }
+  load_v<RB>(fr, x, jn_l, lane);
+
+  // 6. value residual: p * code * scale into the channel accumulators
+  if constexpr (RESID) {
+    const float rs = half_bits_to_float((uint16_t)mc.sv);
+#pragma unroll
+    for (int qd = 0; qd < kMaxRank / 4; ++qd) {
+      if (__ballot(rank > 4u * qd) == 0) break;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int k = 4 * qd + u;
+        if ((uint32_t)k < rank) {
+          const uint32_t c = (wvv.ch[qd] >> (8 * u)) & (D - 1);
+          const float w = code_at(wvv.cd[k >> 3], k & 7) * rs;
+#pragma unroll
+          for (int i = 0; i < G; ++i) atomicAdd(&sm.racc[wv][i][c], p[i] * w);
+        }
+      }
+    }
+    mc = mn;
+    mn = mnn;
+    ec = en;
+  }
+}
+
+template <int RB, int G, bool RESID>
+__global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
+  using C = TCfg<RB>;
+  constexpr int NS = C::NS;
+  __shared__ TSmem<RB, RESID> sm;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int grp = lane >> 4, col = lane & 15;
+  const int slot = blockIdx.y;
+  const int kvh = a.kv_of_slot[slot];
+
+  // work item -> (sequence, chunk)
+  const int w = blockIdx.x;
+  int b = 0, base = 0;
+  for (; b < a.batch - 1; ++b) {
+    const int ns = (a.cu[b + 1] - a.cu[b] + a.split - 1) / a.split;
+    if (w < base + ns) break;
+    base += ns;
+  }
+  TCtx x;
+  x.c0 = (int64_t)a.cu[b] + (int64_t)(w - base) * a.split;
+  x.c1 = min(min((int64_t)a.cu[b + 1], x.c0 + a.split), a.T);
+  x.c0 = min(x.c0, x.c1);
+  x.tb = x.c0 & ~(int64_t)15;
+  x.ntile = (int)((x.c1 - x.tb + TT - 1) / TT);
+  x.T = a.T;
+  x.nblk = (a.T + 15) / 16;
+  x.res_stride = a.res_stride;
+  x.ck = a.coef_k + (int64_t)slot * a.T * RB;
+  x.cv = a.coef_v + (int64_t)slot * x.nblk * 16 * RB;
+  if constexpr (RESID) {
+    x.off = a.off + (int64_t)kvh * (a.T + 1);
+    x.idx[0] = a.idx_k + (int64_t)kvh * a.res_stride;
+    x.idx[1] = a.idx_v + (int64_t)kvh * a.res_stride;
+    x.val[0] = a.val_k + (int64_t)kvh * (a.res_stride / 2);
+    x.val[1] = a.val_v + (int64_t)kvh * (a.res_stride / 2);
+    x.sk = a.scale_k + (int64_t)kvh * a.T;
+    x.sv = a.scale_v + (int64_t)kvh * a.T;
+  }
+  const uint16_t* bk_rows = a.basis + (int64_t)b * a.basis_b_stride + (int64_t)kvh * 2 * RB * D;
+  const uint16_t* bv_rows = bk_rows + RB * D;
+
+  // Requests in issue order (vector loads complete in order): the first
+  // tile's offsets and scales; the query and B^K rows; the first tile's
+  // coefficient fragments; last its residual entries, whose addresses need the
+  // offsets.  Every load is unconditional (a wave with no tile reads the
+  // chunk's last one and never uses it).
+  constexpr int NIT = (RB * 4 + kThreads - 1) / kThreads;   // q~ work items per thread
+  constexpr int QPT = (G * D + kThreads - 1) / kThreads;     // query elements per thread
+  constexpr int BVQ = RB * D / 8 / kThreads;                 // 16-byte B^V chunks per thread
+  const int j0 = min(wv, x.ntile - 1);
+  const int j1 = min(wv + kWaves, x.ntile - 1);
+  TFrags<RB> fr;
+  TMeta mc{}, mn{}, mnn{};
+  TEnt ec{}, en{};
+  if constexpr (RESID) {
+    load_offsets(mc, x, j0, lane);
+    load_scales(mc, x, j0, lane);
+    load_offsets(mn, x, j1, lane);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  u4v rv[NIT][4];
+  uint16_t qraw[QPT];
+#pragma unroll
+  for (int n = 0; n < QPT; ++n) {
+    const int i = min(tid + n * kThreads, G * D - 1);
+    qraw[n] = a.q[((int64_t)b * a.n_q_heads + kvh * G + i / D) * D + i % D];
+  }
+#pragma unroll
+  for (int n = 0; n < NIT; ++n) {
+    const int it = min(tid + n * kThreads, RB * 4 - 1);
+    const u4v* row = reinterpret_cast<const u4v*>(bk_rows + (it >> 2) * D + (it & 3) * 32);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rv[n][i] = row[i];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  load_k<RB>(fr, x, j0, lane);
+  load_v<RB>(fr, x, j0, lane);
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (RESID) load_entries(ec, x, mc);
+
+  if (tid < HG) sm.qmax[tid] = 0;
+  for (int i = tid; i < D * HG; i += kThreads) (&sm.qs[0][0])[i] = 0.f;
+  __syncthreads();
+#pragma unroll
+  for (int n = 0; n < QPT; ++n) {
+    const int i = tid + n * kThreads;
+    if (i < G * D)
+      sm.qs[i % D][i / D] = (a.q_bf16 ? bf16_bits_to_float(qraw[n]) : half_bits_to_float(qraw[n])) * a.qscale;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int n = 0; n < NIT; ++n) {
+    const int it = tid + n * kThreads;
+    if (it >= RB * 4) continue;
+    const int k = it >> 2, qq = it & 3;
+    float acc[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[g] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 32; ++e) {
+      const uint32_t dw = rv[n][e >> 3][(e >> 1) & 3];
+      const float xv = half_bits_to_float((uint16_t)((e & 1) ? (dw >> 16) : (dw & 0xFFFF)));
+#pragma unroll
+      for (int g = 0; g < G; ++g) acc[g] += xv * sm.qs[qq * 32 + e][g];
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      acc[g] += __shfl_xor(acc[g], 1);
+      acc[g] += __shfl_xor(acc[g], 2);
+    }
+    if (qq == 0) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        sm.qt[g][k] = acc[g];
+        atomicMax(&sm.qmax[g], __float_as_int(fabsf(acc[g])));
+      }
+    }
+  }
+  __syncthreads();
+
+  // q~ as the A operand (row = head, repeated per 4 rows), scaled per head by
+  // a power of two so its largest entry sits just under 2^14, split into fp16
+  // hi + lo; the score of head i is scaled back by down[i]
+  TState<RB> st;
+  {
+    const int h = col & 3;
+    float up = 1.0f;
+#pragma unroll
+    for (int i = 0; i < HG; ++i) {
+      int kexp = 0;
+      if (i < G) {
+        const float mx = __int_as_float(sm.qmax[i]);
+        if (mx > 0.f) {
+          int e;
+          frexpf(mx, &e);
+          kexp = 14 - e;
+        }
+      }
+      kexp = max(-100, min(100, kexp));
+      st.down[i] = ldexpf(1.0f, -kexp);
+      if (i == h) up = ldexpf(1.0f, kexp);
+    }
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int k = C::KH * grp + 4 * s + i;
+        const float v = h < G ? sm.qt[h][k] * up : 0.f;
+        const _Float16 hh = (_Float16)v;
+        st.qhi[s][i] = hh;
+        st.qlo[s][i] = (_Float16)(v - (float)hh);
+      }
+    }
+    st.acc_h = f4{0.f, 0.f, 0.f, 0.f};
+    st.acc_l = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < HG; ++i) {
+      st.m[i] = -INFINITY;
+      st.l[i] = 0.f;
+    }
+  }
+  if constexpr (RESID) {
+    for (int i = lane; i < HG * D; i += 64) (&sm.racc[wv][0][0])[i] = 0.f;
+  }
+
+  // Every prologue load completes before the loop (the first iteration needs
+  // the last of them at once), so the loop's own waits count only the loop's
+  // loads and stay exact.
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+
+  for (int j = wv; j < x.ntile; j += kWaves)
+    tstep<RB, G, RESID>(st, fr, mc, mn, mnn, ec, en, j, x, sm, wv, lane);
+
+  // epilogue: the 4 waves merge (B^V rows are requested while they do),
+  // project a~ through B^V, write the partial
+#pragma unroll
+  for (int i = 0; i < HG; ++i) st.l[i] = wave_sum(st.l[i]);
+  if (lane == 0) {
+#pragma unroll
+    for (int i = 0; i < HG; ++i) {
+      sm.ep_m[wv][i] = st.m[i];
+      sm.ep_l[wv][i] = st.l[i];
+    }
+  }
+  if (lane < RB) {
+#pragma unroll
+    for (int i = 0; i < HG; ++i) sm.ep_a[wv][i][lane] = st.acc_h[i] + st.acc_l[i];
+  }
+  u4v bvr[BVQ];
+#pragma unroll
+  for (int n = 0; n < BVQ; ++n) bvr[n] = reinterpret_cast<const u4v*>(bv_rows)[tid + n * kThreads];
+  __syncthreads();
+  if (tid < G) {
+    const int g = tid;
+    float mx = -INFINITY;
+    for (int v = 0; v < kWaves; ++v) mx = fmaxf(mx, sm.ep_m[v][g]);
+    float l = 0.f;
+    for (int v = 0; v < kWaves; ++v) {
+      const float s = sm.ep_m[v][g] == -INFINITY ? 0.f : exp2f(sm.ep_m[v][g] - mx);
+      sm.sw[v][g] = s;
+      l += s * sm.ep_l[v][g];
+    }
+    sm.mstar[g] = mx;
+    sm.lstar[g] = l;
+  }
+#pragma unroll
+  for (int n = 0; n < BVQ; ++n) reinterpret_cast<u4v*>(&sm.bvs[0][0])[tid + n * kThreads] = bvr[n];
+  __syncthreads();
+  for (int i = tid; i < G * RB; i += kThreads) {
+    const int g = i / RB, k = i % RB;
+    float s = 0.f;
+    for (int v = 0; v < kWaves; ++v) s += sm.sw[v][g] * sm.ep_a[v][g][k];
+    sm.acomb[g][k] = s;
+  }
+  __syncthreads();
+  const int c_out = tid % D, par = tid / D;
+  for (int g = par; g < G; g += kThreads / D) {
+    float o = 0.f;
+#pragma unroll 16
+    for (int k = 0; k < RB; ++k) o += sm.acomb[g][k] * half_bits_to_float(sm.bvs[k][c_out]);
+    if constexpr (RESID) {
+      for (int v = 0; v < kWaves; ++v) o += sm.sw[v][g] * sm.racc[v][g][c_out];
+    }
+    float* dst = a.part + (((int64_t)w * a.n_slots + slot) * G + g) * kPartStride;
+    dst[c_out] = o;
+    if (c_out == 0) {
+      dst[D] = sm.mstar[g];
+      dst[D + 1] = sm.lstar[g];
+    }
+  }
+}
+
+template <int RB, int G, bool R>
+hipError_t launch_tl_t(const SplitArgs& a, int n_work, hipStream_t s) {
+  hipLaunchKernelGGL((tl_kernel<RB, G, R>), dim3(n_work, a.n_slots), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int RB, bool R>
+hipError_t launch_tl_g(int g, const SplitArgs& a, int n_work, hipStream_t s) {
+  switch (g) {
+    case 1: return launch_tl_t<RB, 1, R>(a, n_work, s);
+    case 2: return launch_tl_t<RB, 2, R>(a, n_work, s);
+    case 4: return launch_tl_t<RB, 4, R>(a, n_work, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <bool R>
+hipError_t launch_tl_rb(int rb, int g, const SplitArgs& a, int n_work, hipStream_t s) {
+  switch (rb) {
+    case 16: return launch_tl_g<16, R>(g, a, n_work, s);
+    case 32: return launch_tl_g<32, R>(g, a, n_work, s);
+    case 48: return launch_tl_g<48, R>(g, a, n_work, s);
+    case 64: return launch_tl_g<64, R>(g, a, n_work, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+bool token_lane_supported(int rb, int g, int max_level) {
+  return (g == 1 || g == 2 || g == 4) && rb % 16 == 0 && rb >= 16 && rb <= 64 && max_level <= kMaxRank;
+}
+
+hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {
+  return resid ? launch_tl_rb<true>(rb, g, a, n_work, s) : launch_tl_rb<false>(rb, g, a, n_work, s);
+}
+
+}  // namespace dwkv
