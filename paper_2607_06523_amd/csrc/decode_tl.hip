@@ -12,11 +12,14 @@
 //    holds the 4 head scores of token 16bk+c in lane c of every lane group, and
 //    lane 16g+c keeps block g's copy: each lane ends up with its own token's
 //    scores for all heads, in registers.
-//  * the token's residual entries (channel bytes and int4 codes, one window per
-//    tile and lane straight from HBM) add code*q[c] to those scores (q from an
-//    LDS table) and, after the softmax, p*code*scale to a per-wave LDS
-//    accumulator of the value channels (ds_add_f32) - no staging, no entry map,
-//    no exchange between lanes.
+//  * key residual, one lane per token: the token's entries (a window of
+//    channel bytes and int4 codes per lane, straight from HBM) add code*q[c]
+//    to its scores (q from an LDS table) with no exchange between lanes.
+//  * value residual, one lane per entry: token lanes publish p*scale and mark
+//    their entries in an entry->token map; entry lanes add p*code*scale into
+//    a per-wave accumulator of the value channels.  The accumulator is fixed
+//    point in int64 (ds_add_u64): integer LDS atomics cost a few cycles per
+//    instruction, float ones a few cycles per active lane.
 //  * softmax with a lazily moved reference: the running reference of a head
 //    moves only when a score exceeds it by more than 2^8, so probabilities stay
 //    below 256 and the rescaling of the value accumulators is rare.
@@ -44,6 +47,9 @@ constexpr int TT = 64;                  // tokens per tile = lanes per wave
 constexpr int HG = 4;                   // head rows of the score and value products
 constexpr float kLazy = 8.0f;           // log2 headroom of the running reference
 constexpr int kMaxRank = 16;            // residual entries per token this kernel reads
+constexpr int kStage = 512;             // value entries of a tile staged in LDS
+constexpr int kEmap = TT * kMaxRank;    // entries a tile can hold
+constexpr int kFxTop = 34;              // fixed-point fraction bits = kFxTop - scale exponent bound
 constexpr int kWaitVmcnt0 = 0x0F70;     // s_waitcnt immediate: vmcnt(0) only
 
 template <int RB>
@@ -66,7 +72,15 @@ struct alignas(16) TSmem {
   float lstar[HG];
   float acomb[HG][RB];
   int qmax[HG];
-  float racc[kWaves][RESID ? HG : 1][RESID ? D : 1];   // value-residual accumulators
+  // Value residual, per wave.  Accumulators are fixed point (units 2^-fx[w]):
+  // integer LDS atomics run at one instruction per few cycles whatever the
+  // active lanes, float LDS atomics at a few cycles per lane.
+  long long racc[kWaves][RESID ? HG : 1][RESID ? D : 1];
+  uint8_t stg_idx[kWaves][RESID ? kStage : 4];      // staged channel bytes of the tile
+  uint8_t stg_val[kWaves][RESID ? kStage / 2 : 4];  // staged code bytes
+  alignas(4) uint8_t emap[kWaves][RESID ? kEmap : 4];  // tile entry -> token lane
+  alignas(16) float pw[kWaves][RESID ? TT : 1][HG];  // p * value scale per token lane
+  int fx[kWaves];
 };
 
 template <int RB>
@@ -81,8 +95,9 @@ struct TMeta {
 };
 
 struct TEnt {
-  uint32_t ck[5], vk[3];                // key channel bytes / codes around oa
-  uint32_t cv[5], vv[3];                // value channel bytes / codes around oa
+  uint32_t ck[5], vk[3];                // key channel bytes / codes around this lane's oa
+  uint32_t vi[2], vc;                   // value entries of the tile from its first entry
+                                        // rounded down to 8: channel bytes (2 x 256), codes
 };
 
 template <int RB>
@@ -90,6 +105,7 @@ struct TState {
   h4 qhi[TCfg<RB>::NS], qlo[TCfg<RB>::NS];
   f4 acc_h, acc_l;                      // a~[head][channel lane] from p hi / p lo
   float m[HG], l[HG], down[HG];
+  int ex;                               // bound on the value scales seen: |s_v| < 2^ex
 };
 
 struct TCtx {
@@ -159,25 +175,44 @@ __device__ __forceinline__ void load_scales(TMeta& m, const TCtx& x, int j, int 
   m.sv = x.sv[t];
 }
 
-// The windows around a token's entries: 20 channel bytes from oa rounded down
-// to 4 and 12 code bytes from oa/2 rounded down to 4 cover kMaxRank entries
-// (oa is even).  Addresses are clamped into the slab; bytes past a token's
-// entries are never used.
-__device__ __forceinline__ void load_entries(TEnt& e, const TCtx& x, const TMeta& m) {
+__device__ __forceinline__ uint32_t load_dword_clamped(const uint8_t* base, int64_t pos, int64_t len) {
+  return *reinterpret_cast<const uint32_t*>(base + min(pos, len - 4));
+}
+
+// Key entries: the window around the lane's own entries, 20 channel bytes
+// from oa rounded down to 4 and 12 code bytes from oa/2 rounded down to 4
+// (kMaxRank entries; oa is even).  Value entries: the tile's first 512 from
+// its first entry rounded down to 8, one dword per lane and block.  Addresses
+// are clamped into the slab; bytes past the entries in use are never read.
+__device__ __forceinline__ void load_entries(TEnt& e, const TCtx& x, const TMeta& m, int lane) {
   const int64_t a = min((int64_t)(m.oa & ~3u), x.res_stride - 20);
   const int64_t ca = min((int64_t)((m.oa >> 1) & ~3u), x.res_stride / 2 - 12);
   const uint32_t* pk = reinterpret_cast<const uint32_t*>(x.idx[0] + a);
-  const uint32_t* pv = reinterpret_cast<const uint32_t*>(x.idx[1] + a);
   const uint32_t* qk = reinterpret_cast<const uint32_t*>(x.val[0] + ca);
-  const uint32_t* qv = reinterpret_cast<const uint32_t*>(x.val[1] + ca);
 #pragma unroll
   for (int i = 0; i < 5; ++i) e.ck[i] = pk[i];
 #pragma unroll
   for (int i = 0; i < 3; ++i) e.vk[i] = qk[i];
-#pragma unroll
-  for (int i = 0; i < 5; ++i) e.cv[i] = pv[i];
-#pragma unroll
-  for (int i = 0; i < 3; ++i) e.vv[i] = qv[i];
+  const int64_t ia = (uint32_t)__builtin_amdgcn_readfirstlane((int)m.oa) & ~7u;
+  e.vi[0] = load_dword_clamped(x.idx[1], ia + 4 * lane, x.res_stride);
+  e.vi[1] = load_dword_clamped(x.idx[1], ia + 256 + 4 * lane, x.res_stride);
+  e.vc = load_dword_clamped(x.val[1], ia / 2 + 4 * lane, x.res_stride / 2);
+}
+
+// Fixed point: round(v * scale) as a two's complement int64 for
+// |v * scale| < 2^51 (adding 1.5 * 2^52 leaves the rounded integer in the low
+// mantissa bits).
+__device__ __forceinline__ unsigned long long to_fixed(float v, double scale) {
+  const double magic = 6755399441055744.0;
+  const double t = __builtin_fma((double)v, scale, magic);
+  return (unsigned long long)(__double_as_longlong(t) - __double_as_longlong(magic));
+}
+
+// Order LDS traffic between lanes of one wave.
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // Channel bytes of entries [4w, 4w+4) of the token and its 16 codes, aligned.
@@ -253,7 +288,7 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   // 1. metadata of the next tiles
   if constexpr (RESID) {
     load_offsets(mnn, x, jnn_l, lane);
-    load_entries(en, x, mn);
+    load_entries(en, x, mn, lane);
     load_scales(mn, x, jn_l, lane);
   }
 
@@ -280,12 +315,10 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
 
   // 3. key residual: this lane's entries add code * q[c] * scale
   uint32_t rank = 0;
-  Window wk{}, wvv{};
   if constexpr (RESID) {
     rank = min(mc.ob - mc.oa, (uint32_t)kMaxRank);
     if (mc.ob < mc.oa) rank = 0;
-    wk = align_window(ec.ck, ec.vk, mc.oa);
-    wvv = align_window(ec.cv, ec.vv, mc.oa);
+    const Window wk = align_window(ec.ck, ec.vk, mc.oa);
     float rk[HG] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int qd = 0; qd < kMaxRank / 4; ++qd) {
@@ -331,8 +364,9 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
       if constexpr (RESID) {
 #pragma unroll
         for (int i = 0; i < G; ++i) {
-          sm.racc[wv][i][lane] *= alpha[i];
-          sm.racc[wv][i][lane + 64] *= alpha[i];
+          long long* r = &sm.racc[wv][i][0];
+          r[lane] = __double2ll_rn((double)r[lane] * (double)alpha[i]);
+          r[lane + 64] = __double2ll_rn((double)r[lane + 64] * (double)alpha[i]);
         }
       }
     }
@@ -359,23 +393,75 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   }
   load_v<RB>(fr, x, jn_l, lane);
 
-  // 6. value residual: p * code * scale into the channel accumulators
+  // 6. value residual, one lane per entry: p * code * scale into the channel
+  // accumulators.  Token lanes publish p * scale and mark their entries in the
+  // entry -> token map; entry lanes then add into their channel.
   if constexpr (RESID) {
-    const float rs = half_bits_to_float((uint16_t)mc.sv);
+    const uint32_t e0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)mc.oa);
+    const uint32_t e1 = (uint32_t)__builtin_amdgcn_readlane((int)mc.ob, 63);
+    const uint32_t n = e1 > e0 ? min(e1 - e0, (uint32_t)kEmap) : 0u;
+    const uint32_t ia = e0 & ~7u;
+    const bool staged = e0 + n <= ia + kStage;
+    // keep |p * code * s_v| * 2^fx below 2^45 (2^8 * 2^3 * 2^ex): a larger
+    // scale exponent shifts the accumulators down first
+    {
+      const uint32_t eb = (mc.sv >> 10) & 31u;
+      const int el = (int)max(eb, 1u) - 14;
+      if (__ballot(el > st.ex) != 0) {
+        int emax = el;
 #pragma unroll
-    for (int qd = 0; qd < kMaxRank / 4; ++qd) {
-      if (__ballot(rank > 4u * qd) == 0) break;
+        for (int o = 32; o >= 1; o >>= 1) emax = max(emax, __shfl_xor(emax, o));
+        const double f = ldexp(1.0, st.ex - emax);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int k = 4 * qd + u;
-        if ((uint32_t)k < rank) {
-          const uint32_t c = (wvv.ch[qd] >> (8 * u)) & (D - 1);
-          const float w = code_at(wvv.cd[k >> 3], k & 7) * rs;
-#pragma unroll
-          for (int i = 0; i < G; ++i) atomicAdd(&sm.racc[wv][i][c], p[i] * w);
+        for (int i = 0; i < G; ++i) {
+          long long* r = &sm.racc[wv][i][0];
+          r[lane] = __double2ll_rn((double)r[lane] * f);
+          r[lane + 64] = __double2ll_rn((double)r[lane + 64] * f);
         }
+        st.ex = emax;
       }
     }
+    const double scale = ldexp(1.0, kFxTop - st.ex);
+    const float rs = half_bits_to_float((uint16_t)mc.sv);
+    *reinterpret_cast<f4*>(&sm.pw[wv][lane][0]) = f4{p[0] * rs, p[1] * rs, p[2] * rs, p[3] * rs};
+    if (staged) {
+      reinterpret_cast<uint32_t*>(sm.stg_idx[wv])[lane] = ec.vi[0];
+      reinterpret_cast<uint32_t*>(sm.stg_idx[wv])[lane + 64] = ec.vi[1];
+      reinterpret_cast<uint32_t*>(sm.stg_val[wv])[lane] = ec.vc;
+    }
+    {
+      const uint32_t ls = (mc.oa - e0) & ~1u;
+#pragma unroll
+      for (int kk = 0; kk < kMaxRank / 2; ++kk) {
+        if (__ballot(rank > 2u * kk) == 0) break;
+        if (2u * kk < rank && ls + 2u * kk + 1u < (uint32_t)kEmap)
+          *reinterpret_cast<uint16_t*>(&sm.emap[wv][ls + 2 * kk]) = (uint16_t)(lane * 0x0101);
+      }
+    }
+    wave_lds_fence();
+    for (uint32_t b0 = 0; b0 < n; b0 += 64) {
+      const uint32_t e = b0 + lane;
+      if (e < n) {
+        const uint32_t ea = e0 + e;
+        uint32_t ch, cb;
+        if (staged) {
+          ch = sm.stg_idx[wv][ea - ia];
+          cb = sm.stg_val[wv][(ea - ia) >> 1];
+        } else {
+          const int64_t ec_ = min((int64_t)ea, x.res_stride - 1);
+          ch = x.idx[1][ec_];
+          cb = x.val[1][ec_ >> 1];
+        }
+        const int t = sm.emap[wv][e];
+        const f4 w = *reinterpret_cast<const f4*>(&sm.pw[wv][t][0]);
+        const float code = (float)int4_value(cb >> ((ea & 1u) * 4u));
+        const uint32_t c = ch & (D - 1);
+#pragma unroll
+        for (int i = 0; i < G; ++i)
+          atomicAdd(reinterpret_cast<unsigned long long*>(&sm.racc[wv][i][c]), to_fixed(w[i] * code, scale));
+      }
+    }
+    wave_lds_fence();
     mc = mn;
     mn = mnn;
     ec = en;
@@ -460,7 +546,7 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
   load_k<RB>(fr, x, j0, lane);
   load_v<RB>(fr, x, j0, lane);
   __builtin_amdgcn_sched_barrier(0);
-  if constexpr (RESID) load_entries(ec, x, mc);
+  if constexpr (RESID) load_entries(ec, x, mc, lane);
 
   if (tid < HG) sm.qmax[tid] = 0;
   for (int i = tid; i < D * HG; i += kThreads) (&sm.qs[0][0])[i] = 0.f;
@@ -542,9 +628,10 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
       st.m[i] = -INFINITY;
       st.l[i] = 0.f;
     }
+    st.ex = -14;
   }
   if constexpr (RESID) {
-    for (int i = lane; i < HG * D; i += 64) (&sm.racc[wv][0][0])[i] = 0.f;
+    for (int i = lane; i < HG * D; i += 64) (&sm.racc[wv][0][0])[i] = 0;
   }
 
   // Every prologue load completes before the loop (the first iteration needs
@@ -565,6 +652,7 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
       sm.ep_m[wv][i] = st.m[i];
       sm.ep_l[wv][i] = st.l[i];
     }
+    sm.fx[wv] = kFxTop - st.ex;
   }
   if (lane < RB) {
 #pragma unroll
@@ -603,7 +691,8 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
 #pragma unroll 16
     for (int k = 0; k < RB; ++k) o += sm.acomb[g][k] * half_bits_to_float(sm.bvs[k][c_out]);
     if constexpr (RESID) {
-      for (int v = 0; v < kWaves; ++v) o += sm.sw[v][g] * sm.racc[v][g][c_out];
+      for (int v = 0; v < kWaves; ++v)
+        o += sm.sw[v][g] * (float)ldexp((double)sm.racc[v][g][c_out], -sm.fx[v]);
     }
     float* dst = a.part + (((int64_t)w * a.n_slots + slot) * G + g) * kPartStride;
     dst[c_out] = o;
