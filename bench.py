@@ -192,7 +192,7 @@ def main():
                 dc.decode_partials(l, workspace=ws_layer[l])
             ev_calls[1].record(stream)
             for l in range(L):
-                dc.decode_merge(out=outs[l], workspace=ws_layer[l])
+                dc.decode_merge(l, out=outs[l], workspace=ws_layer[l])
             ev_calls[2].record(stream)
         else:
             step()

@@ -136,15 +136,17 @@ dwkv_status dwkv_decode(const dwkv_dims* dims, const dwkv_cache* cache, int32_t 
 
 /* dwkv_decode in two ordered steps on one stream, same arguments and
  * semantics: dwkv_decode_partials launches the split-K pass(es), writing one
- * partial (o, m, l) per (work item, KV head, group member) into the
- * workspace; dwkv_decode_merge merges them into `out` (and, with a probe,
- * writes err / out_ref).  The probe pointer must be the same in both calls. */
+ * partial per (work item, KV head, group member) into the workspace;
+ * dwkv_decode_merge merges them into `out` (and, with a probe, writes err /
+ * out_ref).  Both calls take the same dims, cache, layer and probe pointer;
+ * the merge reads the cache's bases (it may finish the value product). */
 dwkv_status dwkv_decode_partials(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
                                  const void* q, int32_t q_type, float sm_scale,
                                  const dwkv_probe* probe, void* workspace, size_t ws_bytes,
                                  void* stream);
-dwkv_status dwkv_decode_merge(const dwkv_dims* dims, float* out, const dwkv_probe* probe,
-                              void* workspace, size_t ws_bytes, void* stream);
+dwkv_status dwkv_decode_merge(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
+                              float* out, const dwkv_probe* probe, void* workspace,
+                              size_t ws_bytes, void* stream);
 
 /* Bytes of device workspace dwkv_route needs (0 when dims are invalid). */
 size_t dwkv_route_workspace_bytes(const dwkv_dims* dims);

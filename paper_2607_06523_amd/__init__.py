@@ -175,14 +175,14 @@ class DeviceCache:
                                            _stream(torch, self.device))
         binding.check(st, "dwkv_decode_partials")
 
-    def decode_merge(self, out=None, workspace=None):
-        """Second half of decode: merges the split partials into out [B,Hq,d]."""
+    def decode_merge(self, layer: int, out=None, workspace=None):
+        """Second half of decode: merges the split partials of `layer` into out [B,Hq,d]."""
         torch = self.torch
         if out is None:
             out = torch.empty((self.batch, self.n_q_heads, self.head_dim), dtype=torch.float32, device=self.device)
         ws = workspace if workspace is not None else self.workspace(None)
-        st = self.lib.dwkv_decode_merge(C.byref(self.dims), _ptr(out), None, _ptr(ws), ws.numel(),
-                                        _stream(torch, self.device))
+        st = self.lib.dwkv_decode_merge(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(out), None,
+                                        _ptr(ws), ws.numel(), _stream(torch, self.device))
         binding.check(st, "dwkv_decode_merge")
         return out
 

@@ -81,7 +81,8 @@ def load(path: str = LIB_PATH):
     lib.dwkv_decode_partials.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_void_p, C.c_int32, C.c_float,
                                          P(Probe), C.c_void_p, C.c_size_t, C.c_void_p]
     lib.dwkv_decode_merge.restype = C.c_int
-    lib.dwkv_decode_merge.argtypes = [P(Dims), C.c_void_p, P(Probe), C.c_void_p, C.c_size_t, C.c_void_p]
+    lib.dwkv_decode_merge.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_void_p, P(Probe), C.c_void_p,
+                                      C.c_size_t, C.c_void_p]
     lib.dwkv_route_workspace_bytes.restype = C.c_size_t
     lib.dwkv_route_workspace_bytes.argtypes = [P(Dims)]
     lib.dwkv_route.restype = C.c_int

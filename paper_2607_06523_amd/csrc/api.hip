@@ -89,12 +89,19 @@ struct WsLayout {
   size_t main_bytes, ref_bytes, total;
 };
 
+// The token-lane split kernel serves query groups of up to 4 heads with
+// basis ranks up to 64 and ranks up to 16; the general kernel the rest.
+bool uses_token_lane(const dwkv_dims* d) {
+  return token_lane_supported(d->basis_rank, d->n_q_heads / d->n_kv_heads, max_level(d));
+}
+
 WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
   const int split = plan_split(d);
   const int64_t nw = count_work(d, split);
   const int g = d->n_q_heads / d->n_kv_heads;
+  const int stride = uses_token_lane(d) ? kPartStrideTL : kPartStride;
   WsLayout w;
-  w.main_bytes = align_up((size_t)nw * d->n_kv_heads * g * kPartStride * sizeof(float), 256);
+  w.main_bytes = align_up((size_t)nw * d->n_kv_heads * g * stride * sizeof(float), 256);
   w.ref_bytes = p ? align_up((size_t)nw * p->n_heads * g * kPartStride * sizeof(float), 256) : 0;
   w.total = w.main_bytes + w.ref_bytes;
   if (w.total == 0) w.total = 256;
@@ -102,6 +109,19 @@ WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
 }
 
 dwkv_status hip_status(hipError_t e) { return e == hipSuccess ? DWKV_OK : DWKV_E_HIP; }
+
+WorkTable work_table(const dwkv_dims* d, int split) {
+  WorkTable t;
+  std::memset(&t, 0, sizeof(t));
+  if (d->batch > kKernargSeqs) return t;
+  t.n_seq = d->batch;
+  for (int b = 0; b <= d->batch; ++b) t.tok[b] = d->cu_seqlens_host[b];
+  for (int b = 0; b < d->batch; ++b) {
+    const int64_t len = d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b];
+    t.work[b + 1] = t.work[b] + (int32_t)((len + split - 1) / split);
+  }
+  return t;
+}
 
 }  // namespace
 
@@ -198,7 +218,8 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   a.q_bf16 = q_type == DWKV_BF16;
   a.qscale = sm_scale * 1.4426950408889634f;
   for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
-  const hipError_t e = token_lane_supported(RB, G, max_level(d))
+  a.wt = work_table(d, split);
+  const hipError_t e = uses_token_lane(d)
                            ? launch_split_tl(RB, G, max_level(d) > 0, a, (int)nw, s)
                            : launch_split(RB, G, max_level(d) > 0, false, a, (int)nw, s);
   if (e != hipSuccess) return DWKV_E_HIP;
@@ -216,9 +237,10 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
 
 // Merge pass: output rows (and Eq. 3 for probed heads); also writes the zero
 // outputs of empty sequences.
-dwkv_status merge_phase(const dwkv_dims* d, float* out, const dwkv_probe* probe, void* workspace,
-                        hipStream_t s) {
-  if (!out) return DWKV_E_NULL;
+dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, float* out,
+                        const dwkv_probe* probe, void* workspace, hipStream_t s) {
+  if (!out || !c || !c->basis) return DWKV_E_NULL;
+  if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
   const WsLayout wl = ws_layout(d, probe);
   char* ws = static_cast<char*>(workspace);
   MergeArgs mg;
@@ -233,6 +255,14 @@ dwkv_status merge_phase(const dwkv_dims* d, float* out, const dwkv_probe* probe,
   mg.n_q_heads = d->n_q_heads;
   mg.n_kv_heads = d->n_kv_heads;
   mg.split = plan_split(d);
+  mg.wt = work_table(d, mg.split);
+  mg.tl = uses_token_lane(d);
+  mg.rb = d->basis_rank;
+  {
+    const int64_t Hk = d->n_kv_heads, M = d->n_layers / d->window, m = layer / d->window;
+    mg.basis = static_cast<const uint16_t*>(c->basis) + m * Hk * 2 * d->basis_rank * kHeadDim;
+    mg.basis_b_stride = M * Hk * 2 * d->basis_rank * kHeadDim;
+  }
   mg.n_probe = probe ? probe->n_heads : 0;
   mg.eps = probe ? probe->eps : 0.f;
   for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) mg.probe_slot_of_kv[h] = -1;
@@ -253,7 +283,7 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   if (!out) return DWKV_E_NULL;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if ((st = partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, s)) != DWKV_OK) return st;
-  return merge_phase(d, out, probe, workspace, s);
+  return merge_phase(d, c, layer, out, probe, workspace, s);
 }
 
 dwkv_status dwkv_decode_partials(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
@@ -265,11 +295,11 @@ dwkv_status dwkv_decode_partials(const dwkv_dims* d, const dwkv_cache* c, int32_
                         reinterpret_cast<hipStream_t>(stream));
 }
 
-dwkv_status dwkv_decode_merge(const dwkv_dims* d, float* out, const dwkv_probe* probe, void* workspace,
-                              size_t ws_bytes, void* stream) {
+dwkv_status dwkv_decode_merge(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, float* out,
+                              const dwkv_probe* probe, void* workspace, size_t ws_bytes, void* stream) {
   dwkv_status st = check_decode_common(d, probe, workspace, ws_bytes);
   if (st != DWKV_OK) return st;
-  return merge_phase(d, out, probe, workspace, reinterpret_cast<hipStream_t>(stream));
+  return merge_phase(d, c, layer, out, probe, workspace, reinterpret_cast<hipStream_t>(stream));
 }
 
 size_t dwkv_route_workspace_bytes(const dwkv_dims* d) {

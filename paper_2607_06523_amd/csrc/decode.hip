@@ -489,19 +489,14 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   const int grp = lane >> 4, col = lane & 15;
   const int slot = blockIdx.y;
   const int kvh = a.kv_of_slot[slot];
+  pin_split_args(a, kvh);
 
   // work item -> (sequence, chunk)
   const int w = blockIdx.x;
-  int b = 0, base = 0;
-  for (; b < a.batch - 1; ++b) {
-    const int ns = (a.cu[b + 1] - a.cu[b] + a.split - 1) / a.split;
-    if (w < base + ns) break;
-    base += ns;
-  }
-  const int n_split_b = (a.cu[b + 1] - a.cu[b] + a.split - 1) / a.split;
+  int b;
   Ctx x;
-  x.c0 = (int64_t)a.cu[b] + (int64_t)(w - base) * a.split;
-  x.c1 = min(min((int64_t)a.cu[b + 1], x.c0 + a.split), a.T);
+  work_item(a.wt, a.cu, a.batch, a.split, w, b, x.c0, x.c1);
+  x.c1 = min(x.c1, a.T);
   x.c0 = min(x.c0, x.c1);
   x.tb = x.c0 & ~(int64_t)15;
   x.ntile = (int)((x.c1 - x.tb + TT - 1) / TT);
@@ -730,95 +725,173 @@ constexpr int kMergeThreads = 256;
 constexpr int kMergeGroups = kMergeThreads / (D / 4);     // split groups (8)
 constexpr int kMergePerThread = 8;                        // splits per thread per round
 
-__device__ __forceinline__ float4 merge_rows(const float* part, int64_t row0, int64_t row_step, int ns,
-                                             float* red_m, float* red_l, float4* red_o) {
+// Merges the first ncols (<= 2d) columns of the rows row0 + s * row_step
+// (s < ns) of partials with `stride` floats and (m, l) at m_off.  A thread
+// owns columns 4*c4.. and d + 4*c4..; split group 0 returns them divided by
+// the merged l (x: first slice, y: second slice).
+struct Merged {
+  f4 x, y;
+};
+
+__device__ __forceinline__ Merged merge_rows(const float* part, int64_t row0, int64_t row_step, int ns,
+                                             int stride, int m_off, int ncols, float* red_m, float* red_l,
+                                             f4* red_o) {
   const int tid = threadIdx.x, c4 = tid % (D / 4), sg = tid / (D / 4);
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  float mstar = -INFINITY, lstar = 0.f;
+  const bool two = D + 4 * c4 < ncols;
+  const f4 z4 = f4{0.f, 0.f, 0.f, 0.f};
+  f4 acc = z4, acc2 = z4;
+  float mstar = -INFINITY, lsum = 0.f;
   for (int s0 = 0; s0 < ns; s0 += kMergeGroups * kMergePerThread) {
-    // this round's splits: s0 + sg + kMergeGroups * i
-    float4 ov[kMergePerThread];
+    // this round's splits: s0 + sg + kMergeGroups * i, all requested at once
+    f4 ov[kMergePerThread], ov2[kMergePerThread];
     float mv[kMergePerThread], lv[kMergePerThread];
+    // unconditional loads (split index clamped), selected afterwards, so every
+    // request of the round is in flight before the first wait
 #pragma unroll
     for (int i = 0; i < kMergePerThread; ++i) {
-      const int s = s0 + sg + kMergeGroups * i;
-      if (s < ns) {
-        const float* p = part + (row0 + (int64_t)s * row_step) * kPartStride;
-        ov[i] = reinterpret_cast<const float4*>(p)[c4];
-        mv[i] = p[D];
-        lv[i] = p[D + 1];
-      } else {
-        ov[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-        mv[i] = -INFINITY;
-        lv[i] = 0.f;
-      }
+      const int s = min(s0 + sg + kMergeGroups * i, ns - 1);
+      const float* p = part + (row0 + (int64_t)s * row_step) * stride;
+      ov[i] = *reinterpret_cast<const f4*>(p + 4 * c4);
+      ov2[i] = *reinterpret_cast<const f4*>(p + (two ? D : 0) + 4 * c4);
+      mv[i] = p[m_off];
+      lv[i] = p[m_off + 1];
     }
-    // running max and denominator over this round (all threads see every split
-    // of the round through LDS)
-    if (c4 == 0) {
 #pragma unroll
-      for (int i = 0; i < kMergePerThread; ++i) {
-        red_m[sg * kMergePerThread + i] = mv[i];
-        red_l[sg * kMergePerThread + i] = lv[i];
-      }
+    for (int i = 0; i < kMergePerThread; ++i) {
+      const bool ok = s0 + sg + kMergeGroups * i < ns;
+      ov[i] = ok ? ov[i] : z4;
+      ov2[i] = ok && two ? ov2[i] : z4;
+      mv[i] = ok ? mv[i] : -INFINITY;
+      lv[i] = ok ? lv[i] : 0.f;
     }
+    // the round's maximum: per thread, then over the split groups through LDS
+    float mr = mv[0];
+#pragma unroll
+    for (int i = 1; i < kMergePerThread; ++i) mr = fmaxf(mr, mv[i]);
+    if (c4 == 0) red_m[sg] = mr;
     __syncthreads();
-    float mr = mstar;
-    for (int i = 0; i < kMergeGroups * kMergePerThread; ++i) mr = fmaxf(mr, red_m[i]);
+    mr = mstar;
+#pragma unroll
+    for (int q = 0; q < kMergeGroups; ++q) mr = fmaxf(mr, red_m[q]);
+    __syncthreads();
+    // rescale what the earlier rounds accumulated, then add this round's splits
     const float resc = mstar == -INFINITY ? 0.f : exp2f(mstar - mr);
-    float lr = lstar * resc;
-    for (int i = 0; i < kMergeGroups * kMergePerThread; ++i)
-      if (red_m[i] != -INFINITY) lr += red_l[i] * exp2f(red_m[i] - mr);
     acc.x *= resc; acc.y *= resc; acc.z *= resc; acc.w *= resc;
+    acc2.x *= resc; acc2.y *= resc; acc2.z *= resc; acc2.w *= resc;
+    lsum *= resc;
 #pragma unroll
     for (int i = 0; i < kMergePerThread; ++i) {
       if (mv[i] == -INFINITY) continue;
       const float w = exp2f(mv[i] - mr);
       acc.x += w * ov[i].x; acc.y += w * ov[i].y; acc.z += w * ov[i].z; acc.w += w * ov[i].w;
+      acc2.x += w * ov2[i].x; acc2.y += w * ov2[i].y; acc2.z += w * ov2[i].z; acc2.w += w * ov2[i].w;
+      lsum += w * lv[i];
     }
     mstar = mr;
-    lstar = lr;
-    __syncthreads();
   }
-  // combine the split groups of each 4-channel slice
+  // combine the split groups of each 4-channel slice (fixed order)
+  Merged o{z4, z4};
   red_o[tid] = acc;
+  if (c4 == 0) red_l[sg] = lsum;
   __syncthreads();
-  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  float l = 0.f;
   if (sg == 0) {
     for (int q = 0; q < kMergeGroups; ++q) {
-      const float4 u = red_o[q * (D / 4) + c4];
-      o.x += u.x; o.y += u.y; o.z += u.z; o.w += u.w;
+      const f4 u = red_o[q * (D / 4) + c4];
+      o.x.x += u.x; o.x.y += u.y; o.x.z += u.z; o.x.w += u.w;
+      l += red_l[q];
     }
-    const float inv = ns > 0 ? 1.0f / lstar : 0.f;
-    o.x *= inv; o.y *= inv; o.z *= inv; o.w *= inv;
   }
   __syncthreads();
+  if (ncols > D) {
+    red_o[tid] = acc2;
+    __syncthreads();
+    if (sg == 0) {
+      for (int q = 0; q < kMergeGroups; ++q) {
+        const f4 u = red_o[q * (D / 4) + c4];
+        o.y.x += u.x; o.y.y += u.y; o.y.z += u.z; o.y.w += u.w;
+      }
+    }
+    __syncthreads();
+  }
+  if (sg == 0) {
+    const float inv = ns > 0 ? 1.0f / l : 0.f;
+    o.x.x *= inv; o.x.y *= inv; o.x.z *= inv; o.x.w *= inv;
+    o.y.x *= inv; o.y.y *= inv; o.y.z *= inv; o.y.w *= inv;
+  }
   return o;
 }
 
+constexpr int kMergeMaxRB = 64;      // basis ranks of token-lane partials
+
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a) {
-  __shared__ float red_m[kMergeGroups * kMergePerThread], red_l[kMergeGroups * kMergePerThread];
-  __shared__ float4 red_o[kMergeThreads];
+  __shared__ float red_m[kMergeGroups], red_l[kMergeGroups];
+  __shared__ f4 red_o[kMergeThreads];
   __shared__ float red2[2][kMergeThreads / 64];
+  __shared__ alignas(16) uint16_t bvs[kMergeMaxRB][D];
+  __shared__ float abar[kMergeMaxRB];
   const int hq = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  asm volatile("" ::"s"(a.part), "s"(a.out), "s"(a.basis), "s"(a.basis_b_stride), "s"(a.n_q_heads),
+               "s"(a.n_kv_heads), "s"(a.tl), "s"(a.rb), "s"(a.wt.n_seq), "s"(a.wt.work[0]), "s"(a.wt.work[1]));
   const int G = a.n_q_heads / a.n_kv_heads, h = hq / G, g = hq % G;
-  int base = 0;
-  for (int i = 0; i < b; ++i) base += (a.cu[i + 1] - a.cu[i] + a.split - 1) / a.split;
-  const int ns = (a.cu[b + 1] - a.cu[b] + a.split - 1) / a.split;
+  int base, ns;
+  seq_work(a.wt, a.cu, a.split, b, base, ns);
   const int c4 = tid % (D / 4), sg = tid / (D / 4);
-  // main partials: row (work, h, g) = (work * Hkv + h) * G + g
-  const float4 o = merge_rows(a.part, (int64_t)base * a.n_kv_heads * G + h * G + g,
-                              (int64_t)a.n_kv_heads * G, ns, red_m, red_l, red_o);
-  if (sg == 0) reinterpret_cast<float4*>(a.out + ((int64_t)b * a.n_q_heads + hq) * D)[c4] = o;
+  const int64_t row0 = (int64_t)base * a.n_kv_heads * G + h * G + g;
+  const int64_t row_step = (int64_t)a.n_kv_heads * G;
+  f4 o;
+  if (a.tl) {
+    // token-lane partials: merge r and a~ together, then o = r + a~ B^V with
+    // the k range split over the 8 thread groups
+    typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+    const int nch = a.rb * D / 8;                   // 16-byte chunks of B^V (multiple of 256)
+    const u4v* bv = reinterpret_cast<const u4v*>(a.basis + (int64_t)b * a.basis_b_stride +
+                                                  ((int64_t)h * 2 + 1) * a.rb * D);
+    u4v bvr[kMergeMaxRB * D / 8 / kMergeThreads];
+#pragma unroll
+    for (int n = 0; n < kMergeMaxRB * D / 8 / kMergeThreads; ++n) bvr[n] = bv[min(tid + n * kMergeThreads, nch - 1)];
+    const Merged mg = merge_rows(a.part, row0, row_step, ns, kPartStrideTL, kPartTLM, D + a.rb, red_m, red_l,
+                                 red_o);
+#pragma unroll
+    for (int n = 0; n < kMergeMaxRB * D / 8 / kMergeThreads; ++n)
+      if (tid + n * kMergeThreads < nch) reinterpret_cast<u4v*>(&bvs[0][0])[tid + n * kMergeThreads] = bvr[n];
+    if (sg == 0 && 4 * c4 < a.rb) {
+      abar[4 * c4] = mg.y.x; abar[4 * c4 + 1] = mg.y.y; abar[4 * c4 + 2] = mg.y.z; abar[4 * c4 + 3] = mg.y.w;
+    }
+    __syncthreads();
+    const int kp = (a.rb + kMergeGroups - 1) / kMergeGroups;
+    f4 pr = f4{0.f, 0.f, 0.f, 0.f};
+    for (int k = sg * kp; k < min(a.rb, sg * kp + kp); ++k) {
+      const uint2 w2 = *reinterpret_cast<const uint2*>(&bvs[k][4 * c4]);
+      const float ak = abar[k];
+      pr.x += ak * half_bits_to_float((uint16_t)(w2.x & 0xFFFF));
+      pr.y += ak * half_bits_to_float((uint16_t)(w2.x >> 16));
+      pr.z += ak * half_bits_to_float((uint16_t)(w2.y & 0xFFFF));
+      pr.w += ak * half_bits_to_float((uint16_t)(w2.y >> 16));
+    }
+    red_o[tid] = pr;
+    __syncthreads();
+    o = mg.x;
+    if (sg == 0) {
+      for (int q = 0; q < kMergeGroups; ++q) {
+        const f4 u = red_o[q * (D / 4) + c4];
+        o.x += u.x; o.y += u.y; o.z += u.z; o.w += u.w;
+      }
+    }
+    __syncthreads();
+  } else {
+    o = merge_rows(a.part, row0, row_step, ns, kPartStride, D, D, red_m, red_l, red_o).x;
+  }
+  if (sg == 0) reinterpret_cast<f4*>(a.out + ((int64_t)b * a.n_q_heads + hq) * D)[c4] = o;
   if (a.n_probe > 0) {
     const int sl = a.probe_slot_of_kv[h];
     if (sl >= 0) {
-      const float4 r = merge_rows(a.part_ref, (int64_t)base * a.n_probe * G + sl * G + g,
-                                  (int64_t)a.n_probe * G, ns, red_m, red_l, red_o);
+      const f4 r = merge_rows(a.part_ref, (int64_t)base * a.n_probe * G + sl * G + g,
+                                  (int64_t)a.n_probe * G, ns, kPartStride, D, D, red_m, red_l, red_o).x;
       const int64_t col = (int64_t)b * a.n_probe * G + sl * G + g;
       float d2 = 0.f, r2 = 0.f;
       if (sg == 0) {
-        if (a.out_ref) reinterpret_cast<float4*>(a.out_ref + col * D)[c4] = r;
+        if (a.out_ref) reinterpret_cast<f4*>(a.out_ref + col * D)[c4] = r;
         const float dx = r.x - o.x, dy = r.y - o.y, dz = r.z - o.z, dw = r.w - o.w;
         d2 = dx * dx + dy * dy + dz * dz + dw * dw;
         r2 = r.x * r.x + r.y * r.y + r.z * r.z + r.w * r.w;

@@ -29,7 +29,8 @@
 //    blocks cover 64 coefficient channels, read as 4 consecutive tokens of one
 //    channel from the 16-token value blocks.  The accumulator holds, in lane c,
 //    the basis-space value of channel c for the 4 heads.
-//  * the epilogue and the partial format are those of the general kernel.
+//  * the epilogue combines the 4 waves and writes the partial in basis space
+//    (a~, the residual channels, m, l); the merge kernel applies B^V.
 #include <utility>
 
 #include "entry.h"
@@ -63,14 +64,9 @@ template <int RB, bool RESID>
 struct alignas(16) TSmem {
   alignas(16) float qs[D][HG];          // q * sm_scale * log2(e), heads past G zero
   float qt[HG][RB];                     // q~ = B^K q (scaled)
-  alignas(16) uint16_t bvs[RB][D];      // B^V rows (fp16 bits)
   float ep_m[kWaves][HG];
   float ep_l[kWaves][HG];
   float ep_a[kWaves][HG][RB];
-  float sw[kWaves][HG];
-  float mstar[HG];
-  float lstar[HG];
-  float acomb[HG][RB];
   int qmax[HG];
   // Value residual, per wave.  Accumulators are fixed point (units 2^-fx[w]):
   // integer LDS atomics run at one instruction per few cycles whatever the
@@ -477,18 +473,14 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
   const int grp = lane >> 4, col = lane & 15;
   const int slot = blockIdx.y;
   const int kvh = a.kv_of_slot[slot];
+  pin_split_args(a, kvh);
 
   // work item -> (sequence, chunk)
   const int w = blockIdx.x;
-  int b = 0, base = 0;
-  for (; b < a.batch - 1; ++b) {
-    const int ns = (a.cu[b + 1] - a.cu[b] + a.split - 1) / a.split;
-    if (w < base + ns) break;
-    base += ns;
-  }
+  int b;
   TCtx x;
-  x.c0 = (int64_t)a.cu[b] + (int64_t)(w - base) * a.split;
-  x.c1 = min(min((int64_t)a.cu[b + 1], x.c0 + a.split), a.T);
+  work_item(a.wt, a.cu, a.batch, a.split, w, b, x.c0, x.c1);
+  x.c1 = min(x.c1, a.T);
   x.c0 = min(x.c0, x.c1);
   x.tb = x.c0 & ~(int64_t)15;
   x.ntile = (int)((x.c1 - x.tb + TT - 1) / TT);
@@ -507,40 +499,42 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
     x.sv = a.scale_v + (int64_t)kvh * a.T;
   }
   const uint16_t* bk_rows = a.basis + (int64_t)b * a.basis_b_stride + (int64_t)kvh * 2 * RB * D;
-  const uint16_t* bv_rows = bk_rows + RB * D;
 
-  // Requests in issue order (vector loads complete in order): the first
-  // tile's offsets and scales; the query and B^K rows; the first tile's
-  // coefficient fragments; last its residual entries, whose addresses need the
-  // offsets.  Every load is unconditional (a wave with no tile reads the
-  // chunk's last one and never uses it).
-  constexpr int NIT = (RB * 4 + kThreads - 1) / kThreads;   // q~ work items per thread
+  // Requests in issue order (vector loads complete in order): the fragments
+  // of the q~ product (B^K rows, q); the query for the LDS table; the first
+  // tile's offsets and scales; its coefficient fragments; last its residual
+  // entries, whose addresses need the offsets.  Every load is unconditional (a
+  // wave with no tile reads the chunk's last one and never uses it; a wave
+  // past the basis blocks repeats the last block).
   constexpr int QPT = (G * D + kThreads - 1) / kThreads;     // query elements per thread
-  constexpr int BVQ = RB * D / 8 / kThreads;                 // 16-byte B^V chunks per thread
   const int j0 = min(wv, x.ntile - 1);
   const int j1 = min(wv + kWaves, x.ntile - 1);
   TFrags<RB> fr;
   TMeta mc{}, mn{}, mnn{};
   TEnt ec{}, en{};
-  if constexpr (RESID) {
-    load_offsets(mc, x, j0, lane);
-    load_scales(mc, x, j0, lane);
-    load_offsets(mn, x, j1, lane);
+  // q~ fragments: wave w takes basis rows [16w, 16w+16): A = B^K rows (row =
+  // lane % 16, channels 16s + 4(lane/16) + i), B = q (column = head lane % 16)
+  const int qmb = min(wv, NS - 1);
+  uint2 bkf[8], qf[8];
+  {
+    const uint16_t* brow = bk_rows + (int64_t)(16 * qmb + col) * D + 4 * grp;
+    const uint16_t* qrow = a.q + ((int64_t)b * a.n_q_heads + kvh * G + min(col, G - 1)) * D + 4 * grp;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) bkf[s] = *reinterpret_cast<const uint2*>(brow + 16 * s);
+#pragma unroll
+    for (int s = 0; s < 8; ++s) qf[s] = *reinterpret_cast<const uint2*>(qrow + 16 * s);
   }
-  __builtin_amdgcn_sched_barrier(0);
-  u4v rv[NIT][4];
   uint16_t qraw[QPT];
 #pragma unroll
   for (int n = 0; n < QPT; ++n) {
     const int i = min(tid + n * kThreads, G * D - 1);
     qraw[n] = a.q[((int64_t)b * a.n_q_heads + kvh * G + i / D) * D + i % D];
   }
-#pragma unroll
-  for (int n = 0; n < NIT; ++n) {
-    const int it = min(tid + n * kThreads, RB * 4 - 1);
-    const u4v* row = reinterpret_cast<const u4v*>(bk_rows + (it >> 2) * D + (it & 3) * 32);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) rv[n][i] = row[i];
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (RESID) {
+    load_offsets(mc, x, j0, lane);
+    load_scales(mc, x, j0, lane);
+    load_offsets(mn, x, j1, lane);
   }
   __builtin_amdgcn_sched_barrier(0);
   load_k<RB>(fr, x, j0, lane);
@@ -558,32 +552,55 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
       sm.qs[i % D][i / D] = (a.q_bf16 ? bf16_bits_to_float(qraw[n]) : half_bits_to_float(qraw[n])) * a.qscale;
   }
   __syncthreads();
+  {
+    // q * qscale for head col, scaled by a power of two so the head's largest
+    // entry sits just under 2^14 and split into fp16 hi + lo
+    float qv[8][4];
+    float mq = 0.f;
 #pragma unroll
-  for (int n = 0; n < NIT; ++n) {
-    const int it = tid + n * kThreads;
-    if (it >= RB * 4) continue;
-    const int k = it >> 2, qq = it & 3;
-    float acc[G];
+    for (int s = 0; s < 8; ++s)
 #pragma unroll
-    for (int g = 0; g < G; ++g) acc[g] = 0.f;
-#pragma unroll
-    for (int e = 0; e < 32; ++e) {
-      const uint32_t dw = rv[n][e >> 3][(e >> 1) & 3];
-      const float xv = half_bits_to_float((uint16_t)((e & 1) ? (dw >> 16) : (dw & 0xFFFF)));
-#pragma unroll
-      for (int g = 0; g < G; ++g) acc[g] += xv * sm.qs[qq * 32 + e][g];
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      acc[g] += __shfl_xor(acc[g], 1);
-      acc[g] += __shfl_xor(acc[g], 2);
-    }
-    if (qq == 0) {
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        sm.qt[g][k] = acc[g];
-        atomicMax(&sm.qmax[g], __float_as_int(fabsf(acc[g])));
+      for (int i = 0; i < 4; ++i) {
+        const uint16_t bits = (uint16_t)(i < 2 ? (qf[s].x >> (16 * i)) : (qf[s].y >> (16 * (i - 2))));
+        const float v = col < G ? (a.q_bf16 ? bf16_bits_to_float(bits) : half_bits_to_float(bits)) * a.qscale : 0.f;
+        qv[s][i] = v;
+        mq = fmaxf(mq, fabsf(v));
       }
+    mq = fmaxf(mq, __shfl_xor(mq, 16));
+    mq = fmaxf(mq, __shfl_xor(mq, 32));
+    int eq = 0;
+    if (mq > 0.f) {
+      int e;
+      frexpf(mq, &e);
+      eq = max(-100, min(100, 14 - e));
+    }
+    const float upq = ldexpf(1.0f, eq);
+    f4 dq = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      h4 qh, ql;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float v = qv[s][i] * upq;
+        const _Float16 hh = (_Float16)v;
+        qh[i] = hh;
+        ql[i] = (_Float16)(v - (float)hh);
+      }
+      const h4 bkv = __builtin_bit_cast(h4, bkf[s]);
+      dq = mfma16(bkv, qh, dq);
+      dq = mfma16(bkv, ql, dq);
+    }
+    // lane (grp, col): q~[head col][row 16w + 4grp + i] = dq[i] / 2^eq
+    if (wv < NS && col < G) {
+      const float dn = ldexpf(1.0f, -eq);
+      float am = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float v = dq[i] * dn;
+        sm.qt[col][16 * wv + 4 * grp + i] = v;
+        am = fmaxf(am, fabsf(v));
+      }
+      atomicMax(&sm.qmax[col], __float_as_int(am));
     }
   }
   __syncthreads();
@@ -642,8 +659,8 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
   for (int j = wv; j < x.ntile; j += kWaves)
     tstep<RB, G, RESID>(st, fr, mc, mn, mnn, ec, en, j, x, sm, wv, lane);
 
-  // epilogue: the 4 waves merge (B^V rows are requested while they do),
-  // project a~ through B^V, write the partial
+  // epilogue: the 4 waves merge; the partial keeps a~ in basis space (the
+  // merge kernel projects it through B^V once per sequence and head)
 #pragma unroll
   for (int i = 0; i < HG; ++i) st.l[i] = wave_sum(st.l[i]);
   if (lane == 0) {
@@ -658,47 +675,40 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
 #pragma unroll
     for (int i = 0; i < HG; ++i) sm.ep_a[wv][i][lane] = st.acc_h[i] + st.acc_l[i];
   }
-  u4v bvr[BVQ];
-#pragma unroll
-  for (int n = 0; n < BVQ; ++n) bvr[n] = reinterpret_cast<const u4v*>(bv_rows)[tid + n * kThreads];
   __syncthreads();
-  if (tid < G) {
-    const int g = tid;
+  constexpr int ROW = D + RB;                 // r[d] then a~[r_b]
+  constexpr int TPH = kThreads / G;           // threads per head
+  {
+    const int g = tid / TPH;
     float mx = -INFINITY;
-    for (int v = 0; v < kWaves; ++v) mx = fmaxf(mx, sm.ep_m[v][g]);
-    float l = 0.f;
-    for (int v = 0; v < kWaves; ++v) {
-      const float s = sm.ep_m[v][g] == -INFINITY ? 0.f : exp2f(sm.ep_m[v][g] - mx);
-      sm.sw[v][g] = s;
-      l += s * sm.ep_l[v][g];
-    }
-    sm.mstar[g] = mx;
-    sm.lstar[g] = l;
-  }
 #pragma unroll
-  for (int n = 0; n < BVQ; ++n) reinterpret_cast<u4v*>(&sm.bvs[0][0])[tid + n * kThreads] = bvr[n];
-  __syncthreads();
-  for (int i = tid; i < G * RB; i += kThreads) {
-    const int g = i / RB, k = i % RB;
-    float s = 0.f;
-    for (int v = 0; v < kWaves; ++v) s += sm.sw[v][g] * sm.ep_a[v][g][k];
-    sm.acomb[g][k] = s;
-  }
-  __syncthreads();
-  const int c_out = tid % D, par = tid / D;
-  for (int g = par; g < G; g += kThreads / D) {
-    float o = 0.f;
-#pragma unroll 16
-    for (int k = 0; k < RB; ++k) o += sm.acomb[g][k] * half_bits_to_float(sm.bvs[k][c_out]);
-    if constexpr (RESID) {
-      for (int v = 0; v < kWaves; ++v)
-        o += sm.sw[v][g] * (float)ldexp((double)sm.racc[v][g][c_out], -sm.fx[v]);
+    for (int v = 0; v < kWaves; ++v) mx = fmaxf(mx, sm.ep_m[v][g]);
+    float sw[kWaves], l = 0.f;
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) {
+      sw[v] = sm.ep_m[v][g] == -INFINITY ? 0.f : exp2f(sm.ep_m[v][g] - mx);
+      l += sw[v] * sm.ep_l[v][g];
     }
-    float* dst = a.part + (((int64_t)w * a.n_slots + slot) * G + g) * kPartStride;
-    dst[c_out] = o;
-    if (c_out == 0) {
-      dst[D] = sm.mstar[g];
-      dst[D + 1] = sm.lstar[g];
+    float rw[kWaves];                          // fixed-point units folded into the weights
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) rw[v] = sw[v] * ldexpf(1.0f, -sm.fx[v]);
+    float* dst = a.part + (((int64_t)w * a.n_slots + slot) * G + g) * kPartStrideTL;
+    for (int c = tid % TPH; c < ROW; c += TPH) {
+      float o = 0.f;
+      if (c < D) {
+        if constexpr (RESID) {
+#pragma unroll
+          for (int v = 0; v < kWaves; ++v) o += rw[v] * (float)sm.racc[v][g][c];
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < kWaves; ++v) o += sw[v] * sm.ep_a[v][g][c - D];
+      }
+      dst[c] = o;
+    }
+    if (tid % TPH == 0) {
+      dst[kPartTLM] = mx;
+      dst[kPartTLM + 1] = l;
     }
   }
 }

@@ -11,8 +11,25 @@ constexpr int kHeadDim = 128;       // d
 constexpr int kWaves = 4;           // waves per decode workgroup
 constexpr int kThreads = 64 * kWaves;
 constexpr int kPartStride = kHeadDim + 4;   // floats per partial: o[d], m, l, pad
+// Token-lane partials keep the value in basis space: r[d] (residual part),
+// a~[r_b] (r_b <= 64) at d, m at d+64, l at d+65; the merge projects a~
+// through B^V once per sequence and head.
+constexpr int kPartStrideTL = kHeadDim + 64 + 4;
+constexpr int kPartTLM = kHeadDim + 64;
 constexpr int kEntChunk = 512;      // residual entries of a tile staged in LDS
 constexpr int kResTailPad = 512;    // spare entries required after the longest slab
+
+constexpr int kKernargSeqs = 16;    // sequences whose work split travels in the kernel arguments
+
+// Work items of a batch, resolved on the host when it has at most
+// kKernargSeqs sequences (n_seq > 0): items [work[b], work[b+1]) cover
+// sequence b, whose packed tokens are [tok[b], tok[b+1]).  With n_seq == 0
+// the kernels walk the device cu_seqlens instead.
+struct WorkTable {
+  int32_t n_seq;
+  int32_t work[kKernargSeqs + 1];
+  int32_t tok[kKernargSeqs + 1];
+};
 
 // One split-K pass over a layer: grid = (work items, head slots).
 struct SplitArgs {
@@ -40,6 +57,7 @@ struct SplitArgs {
   int32_t q_bf16;
   float qscale;                // sm_scale * log2(e)
   int32_t kv_of_slot[DWKV_MAX_PROBE_HEADS];
+  WorkTable wt;
 };
 
 // Split merge (and Eq. 3 for probed heads): grid = (Hq, B).
@@ -57,7 +75,68 @@ struct MergeArgs {
   int32_t n_probe;
   float eps;
   int32_t probe_slot_of_kv[DWKV_MAX_PROBE_HEADS];   // -1 when the KV head is not probed
+  WorkTable wt;
+  int32_t tl;                  // main partials in the token-lane layout
+  int32_t rb;
+  const uint16_t* basis;       // basis of window m, sequence 0: + (b*M*Hkv + h)*2*RB*d (tl only)
+  int64_t basis_b_stride;
 };
+
+// Makes the kernel-argument values the whole split kernel needs live in scalar
+// registers at this point, so their loads are issued together at kernel entry
+// rather than one after another behind the work-item decode.
+__device__ __forceinline__ void pin_split_args(const SplitArgs& a, int kvh) {
+  asm volatile("" ::"s"(a.coef_k), "s"(a.coef_v), "s"(a.basis), "s"(a.basis_b_stride), "s"(a.q), "s"(a.off), "s"(a.idx_k),
+               "s"(a.idx_v), "s"(a.val_k), "s"(a.val_v), "s"(a.scale_k), "s"(a.scale_v), "s"(a.T),
+               "s"(a.res_stride), "s"(a.split), "s"(kvh), "s"(a.wt.n_seq), "s"(a.wt.tok[0]), "s"(a.wt.tok[1]));
+}
+
+// Sequence b and token chunk [c0, c1) of work item w.
+__device__ __forceinline__ void work_item(const WorkTable& wt, const int32_t* cu, int batch, int split,
+                                          int w, int& b, int64_t& c0, int64_t& c1) {
+  if (__builtin_expect(wt.n_seq > 0, 1)) {
+    // branch-free scan of the whole table: every read is at a fixed argument
+    // offset, so they are all issued at once
+    int bw = 0, t0 = wt.tok[0], t1 = wt.tok[1], w0 = 0;
+    if (wt.n_seq > 1) {
+#pragma unroll
+      for (int i = 1; i < kKernargSeqs; ++i) {
+        const bool here = i < wt.n_seq && w >= wt.work[i];
+        bw = here ? i : bw;
+        w0 = here ? wt.work[i] : w0;
+        t0 = here ? wt.tok[i] : t0;
+        t1 = here ? wt.tok[i + 1] : t1;
+      }
+    }
+    b = bw;
+    c0 = (int64_t)t0 + (int64_t)(w - w0) * split;
+    c1 = t1;
+  } else {
+    int base = 0;
+    for (b = 0; b < batch - 1; ++b) {
+      const int ns = (cu[b + 1] - cu[b] + split - 1) / split;
+      if (w < base + ns) break;
+      base += ns;
+    }
+    c0 = (int64_t)cu[b] + (int64_t)(w - base) * split;
+    c1 = cu[b + 1];
+  }
+  c1 = c1 < c0 + split ? c1 : c0 + split;
+  c0 = c0 < c1 ? c0 : c1;
+}
+
+// First work item and number of work items of sequence b.
+__device__ __forceinline__ void seq_work(const WorkTable& wt, const int32_t* cu, int split, int b,
+                                         int& base, int& ns) {
+  if (wt.n_seq > 0) {
+    base = wt.work[b];
+    ns = wt.work[b + 1] - base;
+  } else {
+    base = 0;
+    for (int i = 0; i < b; ++i) base += (cu[i + 1] - cu[i] + split - 1) / split;
+    ns = (cu[b + 1] - cu[b] + split - 1) / split;
+  }
+}
 
 struct RouteArgs {
   const float* phi;            // [M][Hkv][T][4]

@@ -127,12 +127,17 @@ def test_workspace_and_split_plan(lib):
                        res_stride=T * 16 + 512 + (-(T * 16 + 512)) % 256)
         assert lib.dwkv_split_tokens(C.byref(d)) == want
         n_work = -(-T // want)
-        assert lib.dwkv_workspace_bytes(C.byref(d), None) == -(-(n_work * Hk * 4 * 132 * 4) // 256) * 256
+        # token-lane partials (group of 4, r_b 32, ranks <= 16): d + 64 + 4 floats
+        assert lib.dwkv_workspace_bytes(C.byref(d), None) == -(-(n_work * Hk * 4 * 196 * 4) // 256) * 256
     d, keep = dims(split_tokens=640)
     assert lib.dwkv_split_tokens(C.byref(d)) == 640
     # ragged: per-sequence chunk counts, empty sequences contribute none
     d, keep = dims(batch=3, cu_seqlens_host=[0, 700, 700, 1300], total_tokens=1300, split_tokens=256)
-    assert lib.dwkv_workspace_bytes(C.byref(d), None) == -(-((3 + 3) * 2 * 4 * 132 * 4) // 256) * 256
+    assert lib.dwkv_workspace_bytes(C.byref(d), None) == -(-((3 + 3) * 2 * 4 * 196 * 4) // 256) * 256
+    # general kernel partials (group of 8): d + 4 floats
+    d, keep = dims(batch=3, cu_seqlens_host=[0, 700, 700, 1300], total_tokens=1300, split_tokens=256,
+                   n_q_heads=16)
+    assert lib.dwkv_workspace_bytes(C.byref(d), None) == -(-((3 + 3) * 2 * 8 * 132 * 4) // 256) * 256
 
 
 def test_route_and_map_argument_checks(lib):

@@ -176,5 +176,5 @@ def test_two_phase_calls_equal_decode():
     announce("two-phase decode batch16 layer 1")
     full = dc.decode(1).cpu().numpy()
     dc.decode_partials(1)
-    two = dc.decode_merge().cpu().numpy()
+    two = dc.decode_merge(1).cpu().numpy()
     assert np.array_equal(full, two)
