@@ -51,10 +51,18 @@ dwkv_status check_dims(const dwkv_dims* d) {
   return DWKV_OK;
 }
 
+// The token-lane split kernel serves query groups of up to 4 heads with
+// basis ranks up to 64 and ranks up to 16; the general kernel the rest.
+bool uses_token_lane(const dwkv_dims* d) {
+  return token_lane_supported(d->basis_rank, d->n_q_heads / d->n_kv_heads, max_level(d));
+}
+
 int plan_split(const dwkv_dims* d) {
   if (d->split_tokens > 0) return d->split_tokens;
   const int64_t work = d->total_tokens * d->n_kv_heads;
-  int64_t c = (work + kTargetWorkgroups - 1) / kTargetWorkgroups;
+  // one workgroup per CU for the token-lane kernel (8 waves), two for the general one (4 waves)
+  const int64_t target = uses_token_lane(d) ? kTargetWorkgroups / 2 : kTargetWorkgroups;
+  int64_t c = (work + target - 1) / target;
   c = (c + kSplitQuantum - 1) / kSplitQuantum * kSplitQuantum;
   if (c < kSplitQuantum) c = kSplitQuantum;
   if (c > kSplitMax) c = kSplitMax;
@@ -88,12 +96,6 @@ dwkv_status check_probe(const dwkv_dims* d, const dwkv_probe* p) {
 struct WsLayout {
   size_t main_bytes, ref_bytes, total;
 };
-
-// The token-lane split kernel serves query groups of up to 4 heads with
-// basis ranks up to 64 and ranks up to 16; the general kernel the rest.
-bool uses_token_lane(const dwkv_dims* d) {
-  return token_lane_supported(d->basis_rank, d->n_q_heads / d->n_kv_heads, max_level(d));
-}
 
 WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
   const int split = plan_split(d);

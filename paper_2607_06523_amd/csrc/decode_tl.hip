@@ -48,10 +48,12 @@ constexpr int TT = 64;                  // tokens per tile = lanes per wave
 constexpr int HG = 4;                   // head rows of the score and value products
 constexpr float kLazy = 8.0f;           // log2 headroom of the running reference
 constexpr int kMaxRank = 16;            // residual entries per token this kernel reads
-constexpr int kStage = 512;             // value entries of a tile staged in LDS
+constexpr int kVB = 3;                  // value-entry batches of 64 loaded ahead per tile
 constexpr int kEmap = TT * kMaxRank;    // entries a tile can hold
 constexpr int kFxTop = 34;              // fixed-point fraction bits = kFxTop - scale exponent bound
 constexpr int kWaitVmcnt0 = 0x0F70;     // s_waitcnt immediate: vmcnt(0) only
+constexpr int kTW = kTLWaves;           // waves per workgroup (one workgroup per CU)
+constexpr int kTThreads = 64 * kTW;
 
 template <int RB>
 struct TCfg {
@@ -64,19 +66,17 @@ template <int RB, bool RESID>
 struct alignas(16) TSmem {
   alignas(16) float qs[D][HG];          // q * sm_scale * log2(e), heads past G zero
   float qt[HG][RB];                     // q~ = B^K q (scaled)
-  float ep_m[kWaves][HG];
-  float ep_l[kWaves][HG];
-  float ep_a[kWaves][HG][RB];
+  float ep_m[kTW][HG];
+  float ep_l[kTW][HG];
+  float ep_a[kTW][HG][RB];
   int qmax[HG];
   // Value residual, per wave.  Accumulators are fixed point (units 2^-fx[w]):
   // integer LDS atomics run at one instruction per few cycles whatever the
   // active lanes, float LDS atomics at a few cycles per lane.
-  long long racc[kWaves][RESID ? HG : 1][RESID ? D : 1];
-  uint8_t stg_idx[kWaves][RESID ? kStage : 4];      // staged channel bytes of the tile
-  uint8_t stg_val[kWaves][RESID ? kStage / 2 : 4];  // staged code bytes
-  alignas(4) uint8_t emap[kWaves][RESID ? kEmap : 4];  // tile entry -> token lane
-  alignas(16) float pw[kWaves][RESID ? TT : 1][HG];  // p * value scale per token lane
-  int fx[kWaves];
+  long long racc[kTW][RESID ? HG : 1][RESID ? D : 1];
+  alignas(4) uint8_t emap[kTW][RESID ? kEmap : 4];  // token lane + 1 at each token's first entry
+  alignas(16) float pw[kTW][RESID ? TT : 1][HG];  // p * value scale per token lane
+  int fx[kTW];
 };
 
 template <int RB>
@@ -92,8 +92,7 @@ struct TMeta {
 
 struct TEnt {
   uint32_t ck[5], vk[3];                // key channel bytes / codes around this lane's oa
-  uint32_t vi[2], vc;                   // value entries of the tile from its first entry
-                                        // rounded down to 8: channel bytes (2 x 256), codes
+  uint32_t vc[kVB], vv[kVB];            // value entries e0 + 64b + lane: channel byte, code byte
 };
 
 template <int RB>
@@ -177,9 +176,9 @@ __device__ __forceinline__ uint32_t load_dword_clamped(const uint8_t* base, int6
 
 // Key entries: the window around the lane's own entries, 20 channel bytes
 // from oa rounded down to 4 and 12 code bytes from oa/2 rounded down to 4
-// (kMaxRank entries; oa is even).  Value entries: the tile's first 512 from
-// its first entry rounded down to 8, one dword per lane and block.  Addresses
-// are clamped into the slab; bytes past the entries in use are never read.
+// (kMaxRank entries; oa is even).  Value entries: the tile's first 64*kVB,
+// one per lane and batch.  Addresses are clamped into the slab; bytes past
+// the entries in use are never read.
 __device__ __forceinline__ void load_entries(TEnt& e, const TCtx& x, const TMeta& m, int lane) {
   const int64_t a = min((int64_t)(m.oa & ~3u), x.res_stride - 20);
   const int64_t ca = min((int64_t)((m.oa >> 1) & ~3u), x.res_stride / 2 - 12);
@@ -189,10 +188,13 @@ __device__ __forceinline__ void load_entries(TEnt& e, const TCtx& x, const TMeta
   for (int i = 0; i < 5; ++i) e.ck[i] = pk[i];
 #pragma unroll
   for (int i = 0; i < 3; ++i) e.vk[i] = qk[i];
-  const int64_t ia = (uint32_t)__builtin_amdgcn_readfirstlane((int)m.oa) & ~7u;
-  e.vi[0] = load_dword_clamped(x.idx[1], ia + 4 * lane, x.res_stride);
-  e.vi[1] = load_dword_clamped(x.idx[1], ia + 256 + 4 * lane, x.res_stride);
-  e.vc = load_dword_clamped(x.val[1], ia / 2 + 4 * lane, x.res_stride / 2);
+  const int64_t e0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)m.oa);
+#pragma unroll
+  for (int b = 0; b < kVB; ++b) {
+    const int64_t pos = min(e0 + 64 * b + lane, x.res_stride - 1);
+    e.vc[b] = x.idx[1][pos];
+    e.vv[b] = x.val[1][pos >> 1];
+  }
 }
 
 // Fixed point: round(v * scale) as a two's complement int64 for
@@ -233,6 +235,18 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Inclusive running maximum over the lanes of a wave (non-negative values):
+// DPP shifts within rows of 16, then row broadcasts across rows.
+__device__ __forceinline__ int wave_incl_max(int v) {
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false));   // row_shr:1
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false));   // row_shr:2
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false));   // row_shr:4
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false));   // row_shr:8
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false));   // row_bcast:15
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false));   // row_bcast:31
+  return v;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
@@ -269,13 +283,12 @@ __device__ __forceinline__ void pv_tile(f4& acc_h, f4& acc_l, h4 ph, h4 pl, cons
 
 template <int RB, int G, bool RESID>
 __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc, TMeta& mn, TMeta& mnn,
-                                      TEnt& ec, TEnt& en, int j, const TCtx& x, TSmem<RB, RESID>& sm,
-                                      int wv, int lane) {
+                                      TEnt& ec, TEnt& en, int j, int jn, int jnn, const TCtx& x,
+                                      TSmem<RB, RESID>& sm, int wv, int lane) {
   using C = TCfg<RB>;
   constexpr int NS = C::NS;
   const int grp = lane >> 4;
   const int64_t t0 = tstart(x, j);
-  const int jn = j + kWaves, jnn = j + 2 * kWaves;
   // past the wave's last tile the prefetches re-read a tile of this chunk
   // (cache resident, results unused): the load sequence stays the same
   const int jn_l = jn < x.ntile ? jn : j;
@@ -390,14 +403,12 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   load_v<RB>(fr, x, jn_l, lane);
 
   // 6. value residual, one lane per entry: p * code * scale into the channel
-  // accumulators.  Token lanes publish p * scale and mark their entries in the
-  // entry -> token map; entry lanes then add into their channel.
+  // accumulators.  Token lanes publish p * scale and mark their first entry;
+  // a running maximum over the entry lanes gives each entry its token.
   if constexpr (RESID) {
     const uint32_t e0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)mc.oa);
     const uint32_t e1 = (uint32_t)__builtin_amdgcn_readlane((int)mc.ob, 63);
     const uint32_t n = e1 > e0 ? min(e1 - e0, (uint32_t)kEmap) : 0u;
-    const uint32_t ia = e0 & ~7u;
-    const bool staged = e0 + n <= ia + kStage;
     // keep |p * code * s_v| * 2^fx below 2^45 (2^8 * 2^3 * 2^ex): a larger
     // scale exponent shifts the accumulators down first
     {
@@ -420,36 +431,30 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
     const double scale = ldexp(1.0, kFxTop - st.ex);
     const float rs = half_bits_to_float((uint16_t)mc.sv);
     *reinterpret_cast<f4*>(&sm.pw[wv][lane][0]) = f4{p[0] * rs, p[1] * rs, p[2] * rs, p[3] * rs};
-    if (staged) {
-      reinterpret_cast<uint32_t*>(sm.stg_idx[wv])[lane] = ec.vi[0];
-      reinterpret_cast<uint32_t*>(sm.stg_idx[wv])[lane + 64] = ec.vi[1];
-      reinterpret_cast<uint32_t*>(sm.stg_val[wv])[lane] = ec.vc;
-    }
-    {
-      const uint32_t ls = (mc.oa - e0) & ~1u;
-#pragma unroll
-      for (int kk = 0; kk < kMaxRank / 2; ++kk) {
-        if (__ballot(rank > 2u * kk) == 0) break;
-        if (2u * kk < rank && ls + 2u * kk + 1u < (uint32_t)kEmap)
-          *reinterpret_cast<uint16_t*>(&sm.emap[wv][ls + 2 * kk]) = (uint16_t)(lane * 0x0101);
-      }
-    }
+    for (uint32_t i = 4 * lane; i < n; i += 256) *reinterpret_cast<uint32_t*>(&sm.emap[wv][i]) = 0u;
+    if (rank > 0 && mc.oa - e0 < n) sm.emap[wv][mc.oa - e0] = (uint8_t)(lane + 1);
     wave_lds_fence();
+    int carry = 0;
     for (uint32_t b0 = 0; b0 < n; b0 += 64) {
       const uint32_t e = b0 + lane;
+      // token of entry e: the last token lane whose first entry is <= e
+      int tk = e < n ? sm.emap[wv][e] : 0;
+      tk = wave_incl_max(tk);
+      tk = max(tk, carry);
+      carry = __builtin_amdgcn_readlane(tk, 63);
       if (e < n) {
         const uint32_t ea = e0 + e;
         uint32_t ch, cb;
-        if (staged) {
-          ch = sm.stg_idx[wv][ea - ia];
-          cb = sm.stg_val[wv][(ea - ia) >> 1];
+        const int bb = b0 >> 6;
+        if (bb < kVB) {
+          ch = bb == 0 ? ec.vc[0] : (bb == 1 ? ec.vc[1] : ec.vc[2]);
+          cb = bb == 0 ? ec.vv[0] : (bb == 1 ? ec.vv[1] : ec.vv[2]);
         } else {
           const int64_t ec_ = min((int64_t)ea, x.res_stride - 1);
           ch = x.idx[1][ec_];
           cb = x.val[1][ec_ >> 1];
         }
-        const int t = sm.emap[wv][e];
-        const f4 w = *reinterpret_cast<const f4*>(&sm.pw[wv][t][0]);
+        const f4 w = *reinterpret_cast<const f4*>(&sm.pw[wv][tk - 1][0]);
         const float code = (float)int4_value(cb >> ((ea & 1u) * 4u));
         const uint32_t c = ch & (D - 1);
 #pragma unroll
@@ -457,7 +462,6 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
           atomicAdd(reinterpret_cast<unsigned long long*>(&sm.racc[wv][i][c]), to_fixed(w[i] * code, scale));
       }
     }
-    wave_lds_fence();
     mc = mn;
     mn = mnn;
     ec = en;
@@ -465,7 +469,7 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
 }
 
 template <int RB, int G, bool RESID>
-__global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
+__global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   using C = TCfg<RB>;
   constexpr int NS = C::NS;
   __shared__ TSmem<RB, RESID> sm;
@@ -506,9 +510,9 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
   // entries, whose addresses need the offsets.  Every load is unconditional (a
   // wave with no tile reads the chunk's last one and never uses it; a wave
   // past the basis blocks repeats the last block).
-  constexpr int QPT = (G * D + kThreads - 1) / kThreads;     // query elements per thread
+  constexpr int QPT = (G * D + kTThreads - 1) / kTThreads;     // query elements per thread
   const int j0 = min(wv, x.ntile - 1);
-  const int j1 = min(wv + kWaves, x.ntile - 1);
+  const int j1 = min(wv + kTW, x.ntile - 1);
   TFrags<RB> fr;
   TMeta mc{}, mn{}, mnn{};
   TEnt ec{}, en{};
@@ -527,7 +531,7 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
   uint16_t qraw[QPT];
 #pragma unroll
   for (int n = 0; n < QPT; ++n) {
-    const int i = min(tid + n * kThreads, G * D - 1);
+    const int i = min(tid + n * kTThreads, G * D - 1);
     qraw[n] = a.q[((int64_t)b * a.n_q_heads + kvh * G + i / D) * D + i % D];
   }
   __builtin_amdgcn_sched_barrier(0);
@@ -543,11 +547,11 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
   if constexpr (RESID) load_entries(ec, x, mc, lane);
 
   if (tid < HG) sm.qmax[tid] = 0;
-  for (int i = tid; i < D * HG; i += kThreads) (&sm.qs[0][0])[i] = 0.f;
+  for (int i = tid; i < D * HG; i += kTThreads) (&sm.qs[0][0])[i] = 0.f;
   __syncthreads();
 #pragma unroll
   for (int n = 0; n < QPT; ++n) {
-    const int i = tid + n * kThreads;
+    const int i = tid + n * kTThreads;
     if (i < G * D)
       sm.qs[i % D][i / D] = (a.q_bf16 ? bf16_bits_to_float(qraw[n]) : half_bits_to_float(qraw[n])) * a.qscale;
   }
@@ -651,13 +655,11 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
     for (int i = lane; i < HG * D; i += 64) (&sm.racc[wv][0][0])[i] = 0;
   }
 
-  // Every prologue load completes before the loop (the first iteration needs
-  // the last of them at once), so the loop's own waits count only the loop's
-  // loads and stay exact.
-  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 
-  for (int j = wv; j < x.ntile; j += kWaves)
-    tstep<RB, G, RESID>(st, fr, mc, mn, mnn, ec, en, j, x, sm, wv, lane);
+  // tiles wv, wv + 8, wv + 16, ...: a fixed assignment keeps the summation
+  // order, and so the result, independent of timing
+  for (int j = wv; j < x.ntile; j += kTW)
+    tstep<RB, G, RESID>(st, fr, mc, mn, mnn, ec, en, j, j + kTW, j + 2 * kTW, x, sm, wv, lane);
 
   // epilogue: the 4 waves merge; the partial keeps a~ in basis space (the
   // merge kernel projects it through B^V once per sequence and head)
@@ -677,32 +679,32 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
   }
   __syncthreads();
   constexpr int ROW = D + RB;                 // r[d] then a~[r_b]
-  constexpr int TPH = kThreads / G;           // threads per head
+  constexpr int TPH = kTThreads / G;           // threads per head
   {
     const int g = tid / TPH;
     float mx = -INFINITY;
 #pragma unroll
-    for (int v = 0; v < kWaves; ++v) mx = fmaxf(mx, sm.ep_m[v][g]);
-    float sw[kWaves], l = 0.f;
+    for (int v = 0; v < kTW; ++v) mx = fmaxf(mx, sm.ep_m[v][g]);
+    float sw[kTW], l = 0.f;
 #pragma unroll
-    for (int v = 0; v < kWaves; ++v) {
+    for (int v = 0; v < kTW; ++v) {
       sw[v] = sm.ep_m[v][g] == -INFINITY ? 0.f : exp2f(sm.ep_m[v][g] - mx);
       l += sw[v] * sm.ep_l[v][g];
     }
-    float rw[kWaves];                          // fixed-point units folded into the weights
+    float rw[kTW];                          // fixed-point units folded into the weights
 #pragma unroll
-    for (int v = 0; v < kWaves; ++v) rw[v] = sw[v] * ldexpf(1.0f, -sm.fx[v]);
+    for (int v = 0; v < kTW; ++v) rw[v] = sw[v] * ldexpf(1.0f, -sm.fx[v]);
     float* dst = a.part + (((int64_t)w * a.n_slots + slot) * G + g) * kPartStrideTL;
     for (int c = tid % TPH; c < ROW; c += TPH) {
       float o = 0.f;
       if (c < D) {
         if constexpr (RESID) {
 #pragma unroll
-          for (int v = 0; v < kWaves; ++v) o += rw[v] * (float)sm.racc[v][g][c];
+          for (int v = 0; v < kTW; ++v) o += rw[v] * (float)sm.racc[v][g][c];
         }
       } else {
 #pragma unroll
-        for (int v = 0; v < kWaves; ++v) o += sw[v] * sm.ep_a[v][g][c - D];
+        for (int v = 0; v < kTW; ++v) o += sw[v] * sm.ep_a[v][g][c - D];
       }
       dst[c] = o;
     }
@@ -715,7 +717,7 @@ __global__ __launch_bounds__(kThreads) void tl_kernel(const SplitArgs a) {
 
 template <int RB, int G, bool R>
 hipError_t launch_tl_t(const SplitArgs& a, int n_work, hipStream_t s) {
-  hipLaunchKernelGGL((tl_kernel<RB, G, R>), dim3(n_work, a.n_slots), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL((tl_kernel<RB, G, R>), dim3(n_work, a.n_slots), dim3(kTThreads), 0, s, a);
   return hipGetLastError();
 }
 

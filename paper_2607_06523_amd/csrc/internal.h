@@ -9,6 +9,7 @@ namespace dwkv {
 
 constexpr int kHeadDim = 128;       // d
 constexpr int kWaves = 4;           // waves per decode workgroup
+constexpr int kTLWaves = 8;         // waves per token-lane decode workgroup
 constexpr int kThreads = 64 * kWaves;
 constexpr int kPartStride = kHeadDim + 4;   // floats per partial: o[d], m, l, pad
 // Token-lane partials keep the value in basis space: r[d] (residual part),

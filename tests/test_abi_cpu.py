@@ -120,8 +120,9 @@ def test_probe_argument_checks(lib):
 
 
 def test_workspace_and_split_plan(lib):
-    # automatic chunk: ceil(T*Hkv/512) rounded up to 256, clamped to [256, 8192]
-    for T, Hk, want in [(4096, 2, 256), (32768, 8, 512), (65536, 8, 1024), (262144, 8, 4096),
+    # automatic chunk: ceil(T*Hkv/n) rounded up to 256, clamped to [256, 8192], with n = 256
+    # workgroups for the token-lane kernel (groups of 4, r_b 32, ranks <= 16) and 512 otherwise
+    for T, Hk, want in [(4096, 2, 256), (32768, 8, 1024), (65536, 8, 2048), (262144, 8, 8192),
                         (10**6, 8, 8192)]:
         d, keep = dims(cu_seqlens_host=[0, T], batch=1, total_tokens=T, n_kv_heads=Hk, n_q_heads=4 * Hk,
                        res_stride=T * 16 + 512 + (-(T * 16 + 512)) % 256)
@@ -129,6 +130,9 @@ def test_workspace_and_split_plan(lib):
         n_work = -(-T // want)
         # token-lane partials (group of 4, r_b 32, ranks <= 16): d + 64 + 4 floats
         assert lib.dwkv_workspace_bytes(C.byref(d), None) == -(-(n_work * Hk * 4 * 196 * 4) // 256) * 256
+    d, keep = dims(cu_seqlens_host=[0, 65536], batch=1, total_tokens=65536, n_kv_heads=8, n_q_heads=64,
+                   res_stride=65536 * 16 + 512)
+    assert lib.dwkv_split_tokens(C.byref(d)) == 1024      # group of 8: general kernel
     d, keep = dims(split_tokens=640)
     assert lib.dwkv_split_tokens(C.byref(d)) == 640
     # ragged: per-sequence chunk counts, empty sequences contribute none
