@@ -54,7 +54,8 @@ dwkv_status check_dims(const dwkv_dims* d) {
 // The token-lane split kernel serves query groups of up to 4 heads with
 // basis ranks up to 64 and ranks up to 16; the general kernel the rest.
 bool uses_token_lane(const dwkv_dims* d) {
-  return token_lane_supported(d->basis_rank, d->n_q_heads / d->n_kv_heads, max_level(d));
+  return token_lane_supported(d->basis_rank, d->n_q_heads / d->n_kv_heads, max_level(d), d->total_tokens,
+                              d->res_stride);
 }
 
 int plan_split(const dwkv_dims* d) {

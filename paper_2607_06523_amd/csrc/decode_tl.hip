@@ -42,6 +42,8 @@ namespace {
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u3v __attribute__((ext_vector_type(3)));
+typedef uint32_t u2v __attribute__((ext_vector_type(2)));
 
 constexpr int D = kHeadDim;
 constexpr int TT = 64;                  // tokens per tile = lanes per wave
@@ -103,28 +105,29 @@ struct TState {
   int ex;                               // bound on the value scales seen: |s_v| < 2^ex
 };
 
-struct TCtx {
-  const uint16_t* ck;
-  const uint16_t* cv;
-  const uint32_t* off;
-  const uint8_t* idx[2];
-  const uint8_t* val[2];
-  const uint16_t* sk;
-  const uint16_t* sv;
-  int64_t c0, c1, tb;
-  int64_t T, nblk, res_stride;
-  int ntile;
-};
+// Every stream is read through a raw buffer resource over its slab: offsets
+// are 32-bit and a read past the slab returns zero, so no load needs a clamp
+// for safety (the host keeps every slab below 2^31 bytes).
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRsrcWord3 = 0x00020000;  // raw (untyped) buffer, gfx9 family
 
-__device__ __forceinline__ int64_t clamp64(int64_t v, int64_t lo, int64_t hi) {
-  return v < lo ? lo : (v > hi ? hi : v);
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kRsrcWord3);
 }
+
+struct TCtx {
+  rsrc_t ck, cv;                        // coefficient slabs (bytes)
+  rsrc_t off, sk, sv;                   // offsets and residual scales of the slab
+  rsrc_t idx[2], val[2];                // residual channel bytes and code bytes (K, V)
+  int32_t c0, c1, tb;                   // chunk [c0, c1); tiles start at tb = c0 & ~15
+  int32_t ntile;
+};
 
 __device__ __forceinline__ f4 mfma16(h4 a, h4 b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ int64_t tstart(const TCtx& x, int j) { return x.tb + (int64_t)j * TT; }
+__device__ __forceinline__ int32_t tstart(const TCtx& x, int j) { return x.tb + j * TT; }
 
 // signed 4-bit code in bits [4n, 4n+4) of w
 __device__ __forceinline__ float code_at(uint32_t w, int n) {
@@ -134,66 +137,62 @@ __device__ __forceinline__ float code_at(uint32_t w, int n) {
 template <int RB>
 __device__ __forceinline__ void load_k(TFrags<RB>& f, const TCtx& x, int j, int lane) {
   using C = TCfg<RB>;
-  const int64_t t0 = tstart(x, j);
   const int grp = lane >> 4, col = lane & 15;
+  const uint32_t base = (uint32_t)(tstart(x, j) + col) * (RB * 2) + C::KH * grp * 2;
 #pragma unroll
   for (int bk = 0; bk < 4; ++bk) {
-    const int64_t row = min(t0 + 16 * bk + col, x.T - 1);
-    const uint2* p = reinterpret_cast<const uint2*>(x.ck + row * RB + C::KH * grp);
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s) f.k[bk][s] = p[s];
+    for (int s = 0; s < C::NS; ++s) {
+      const u2v w = __builtin_amdgcn_raw_buffer_load_b64(x.ck, base + bk * 16 * RB * 2 + 8 * s, 0, 0);
+      f.k[bk][s] = make_uint2(w.x, w.y);
+    }
   }
 }
 
 template <int RB>
 __device__ __forceinline__ void load_v(TFrags<RB>& f, const TCtx& x, int j, int lane) {
-  const int64_t b0 = tstart(x, j) >> 4;
-  const int c = min(lane, RB - 1);
+  // lanes past r_b read neighbouring data whose products are never used
+  const uint32_t base = ((uint32_t)(tstart(x, j) >> 4) * RB + lane) * 32;
 #pragma unroll
   for (int q = 0; q < 16; q += 2) {
-    const int64_t blk = min(b0 + (q >> 2), x.nblk - 1);
-    const uint4 w = *reinterpret_cast<const uint4*>(x.cv + (blk * RB + c) * 16 + 4 * (q & 3));
+    const u4v w = __builtin_amdgcn_raw_buffer_load_b128(x.cv, base + (q >> 2) * RB * 32 + 8 * (q & 3), 0, 0);
     f.v[q] = make_uint2(w.x, w.y);
     f.v[q + 1] = make_uint2(w.z, w.w);
   }
 }
 
+// Entry range of the lane's token, clipped to the chunk (tokens outside it own
+// no entries).
 __device__ __forceinline__ void load_offsets(TMeta& m, const TCtx& x, int j, int lane) {
-  const int64_t t = tstart(x, j) + lane;
-  m.oa = x.off[clamp64(t, x.c0, x.c1)];
-  m.ob = x.off[clamp64(t + 1, x.c0, x.c1)];
+  const int32_t t = tstart(x, j) + lane;
+  m.oa = __builtin_amdgcn_raw_buffer_load_b32(x.off, (uint32_t)min(max(t, x.c0), x.c1) * 4, 0, 0);
+  m.ob = __builtin_amdgcn_raw_buffer_load_b32(x.off, (uint32_t)min(max(t + 1, x.c0), x.c1) * 4, 0, 0);
 }
 
+// Scales of tokens outside the chunk are read but never used.
 __device__ __forceinline__ void load_scales(TMeta& m, const TCtx& x, int j, int lane) {
-  const int64_t t = clamp64(tstart(x, j) + lane, x.c0, x.c1 - 1);
-  m.sk = x.sk[t];
-  m.sv = x.sv[t];
-}
-
-__device__ __forceinline__ uint32_t load_dword_clamped(const uint8_t* base, int64_t pos, int64_t len) {
-  return *reinterpret_cast<const uint32_t*>(base + min(pos, len - 4));
+  const uint32_t t = (uint32_t)(tstart(x, j) + lane);
+  m.sk = __builtin_amdgcn_raw_buffer_load_b16(x.sk, t * 2, 0, 0);
+  m.sv = __builtin_amdgcn_raw_buffer_load_b16(x.sv, t * 2, 0, 0);
 }
 
 // Key entries: the window around the lane's own entries, 20 channel bytes
 // from oa rounded down to 4 and 12 code bytes from oa/2 rounded down to 4
 // (kMaxRank entries; oa is even).  Value entries: the tile's first 64*kVB,
-// one per lane and batch.  Addresses are clamped into the slab; bytes past
-// the entries in use are never read.
+// one per lane and batch.  Bytes past the entries in use are never used.
 __device__ __forceinline__ void load_entries(TEnt& e, const TCtx& x, const TMeta& m, int lane) {
-  const int64_t a = min((int64_t)(m.oa & ~3u), x.res_stride - 20);
-  const int64_t ca = min((int64_t)((m.oa >> 1) & ~3u), x.res_stride / 2 - 12);
-  const uint32_t* pk = reinterpret_cast<const uint32_t*>(x.idx[0] + a);
-  const uint32_t* qk = reinterpret_cast<const uint32_t*>(x.val[0] + ca);
-#pragma unroll
-  for (int i = 0; i < 5; ++i) e.ck[i] = pk[i];
-#pragma unroll
-  for (int i = 0; i < 3; ++i) e.vk[i] = qk[i];
-  const int64_t e0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)m.oa);
+  const uint32_t a = m.oa & ~3u, ca = (m.oa >> 1) & ~3u;
+  const u4v c4 = __builtin_amdgcn_raw_buffer_load_b128(x.idx[0], a, 0, 0);
+  e.ck[0] = c4.x; e.ck[1] = c4.y; e.ck[2] = c4.z; e.ck[3] = c4.w;
+  e.ck[4] = __builtin_amdgcn_raw_buffer_load_b32(x.idx[0], a + 16, 0, 0);
+  const u3v v3 = __builtin_amdgcn_raw_buffer_load_b96(x.val[0], ca, 0, 0);
+  e.vk[0] = v3.x; e.vk[1] = v3.y; e.vk[2] = v3.z;
+  const uint32_t e0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)m.oa);
 #pragma unroll
   for (int b = 0; b < kVB; ++b) {
-    const int64_t pos = min(e0 + 64 * b + lane, x.res_stride - 1);
-    e.vc[b] = x.idx[1][pos];
-    e.vv[b] = x.val[1][pos >> 1];
+    const uint32_t pos = e0 + 64 * b + lane;
+    e.vc[b] = __builtin_amdgcn_raw_buffer_load_b8(x.idx[1], pos, 0, 0);
+    e.vv[b] = __builtin_amdgcn_raw_buffer_load_b8(x.val[1], pos >> 1, 0, 0);
   }
 }
 
@@ -288,18 +287,20 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   using C = TCfg<RB>;
   constexpr int NS = C::NS;
   const int grp = lane >> 4;
-  const int64_t t0 = tstart(x, j);
+  const int32_t t0 = tstart(x, j);
   // past the wave's last tile the prefetches re-read a tile of this chunk
   // (cache resident, results unused): the load sequence stays the same
   const int jn_l = jn < x.ntile ? jn : j;
   const int jnn_l = jnn < x.ntile ? jnn : jn_l;
 
-  // 1. metadata of the next tiles
+  // 1. metadata of the next tiles, issued here, ahead of this tile's work (the
+  // registers rotate at the end of the step and the copies wait for them)
   if constexpr (RESID) {
     load_offsets(mnn, x, jnn_l, lane);
     load_entries(en, x, mn, lane);
     load_scales(mn, x, jn_l, lane);
   }
+  __builtin_amdgcn_sched_barrier(0);
 
   // 2. scores: block bk lands in every lane group; lane group g keeps block g
   f4 sacc[4];
@@ -348,7 +349,7 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
     for (int i = 0; i < G; ++i) sc[i] += rk[i] * rs;
   }
   {
-    const int64_t t = t0 + lane;
+    const int32_t t = t0 + lane;
     const bool valid = t >= x.c0 && t < x.c1;
 #pragma unroll
     for (int i = 0; i < HG; ++i) sc[i] = (valid && i < G) ? sc[i] : -INFINITY;
@@ -450,9 +451,8 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
           ch = bb == 0 ? ec.vc[0] : (bb == 1 ? ec.vc[1] : ec.vc[2]);
           cb = bb == 0 ? ec.vv[0] : (bb == 1 ? ec.vv[1] : ec.vv[2]);
         } else {
-          const int64_t ec_ = min((int64_t)ea, x.res_stride - 1);
-          ch = x.idx[1][ec_];
-          cb = x.val[1][ec_ >> 1];
+          ch = __builtin_amdgcn_raw_buffer_load_b8(x.idx[1], ea, 0, 0);
+          cb = __builtin_amdgcn_raw_buffer_load_b8(x.val[1], ea >> 1, 0, 0);
         }
         const f4 w = *reinterpret_cast<const f4*>(&sm.pw[wv][tk - 1][0]);
         const float code = (float)int4_value(cb >> ((ea & 1u) * 4u));
@@ -483,24 +483,29 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   const int w = blockIdx.x;
   int b;
   TCtx x;
-  work_item(a.wt, a.cu, a.batch, a.split, w, b, x.c0, x.c1);
-  x.c1 = min(x.c1, a.T);
-  x.c0 = min(x.c0, x.c1);
-  x.tb = x.c0 & ~(int64_t)15;
-  x.ntile = (int)((x.c1 - x.tb + TT - 1) / TT);
-  x.T = a.T;
-  x.nblk = (a.T + 15) / 16;
-  x.res_stride = a.res_stride;
-  x.ck = a.coef_k + (int64_t)slot * a.T * RB;
-  x.cv = a.coef_v + (int64_t)slot * x.nblk * 16 * RB;
-  if constexpr (RESID) {
-    x.off = a.off + (int64_t)kvh * (a.T + 1);
-    x.idx[0] = a.idx_k + (int64_t)kvh * a.res_stride;
-    x.idx[1] = a.idx_v + (int64_t)kvh * a.res_stride;
-    x.val[0] = a.val_k + (int64_t)kvh * (a.res_stride / 2);
-    x.val[1] = a.val_v + (int64_t)kvh * (a.res_stride / 2);
-    x.sk = a.scale_k + (int64_t)kvh * a.T;
-    x.sv = a.scale_v + (int64_t)kvh * a.T;
+  {
+    int64_t c0, c1;
+    work_item(a.wt, a.cu, a.batch, a.split, w, b, c0, c1);
+    c1 = min(c1, a.T);
+    c0 = min(c0, c1);
+    x.c0 = (int32_t)c0;
+    x.c1 = (int32_t)c1;
+  }
+  x.tb = x.c0 & ~15;
+  x.ntile = (x.c1 - x.tb + TT - 1) / TT;
+  {
+    const int64_t T = a.T, nblk = (T + 15) / 16, rs = a.res_stride;
+    x.ck = make_rsrc(a.coef_k + (int64_t)slot * T * RB, (uint32_t)(T * RB * 2));
+    x.cv = make_rsrc(a.coef_v + (int64_t)slot * nblk * 16 * RB, (uint32_t)(nblk * 16 * RB * 2));
+    if constexpr (RESID) {
+      x.off = make_rsrc(a.off + (int64_t)kvh * (T + 1), (uint32_t)((T + 1) * 4));
+      x.idx[0] = make_rsrc(a.idx_k + (int64_t)kvh * rs, (uint32_t)rs);
+      x.idx[1] = make_rsrc(a.idx_v + (int64_t)kvh * rs, (uint32_t)rs);
+      x.val[0] = make_rsrc(a.val_k + (int64_t)kvh * (rs / 2), (uint32_t)(rs / 2));
+      x.val[1] = make_rsrc(a.val_v + (int64_t)kvh * (rs / 2), (uint32_t)(rs / 2));
+      x.sk = make_rsrc(a.scale_k + (int64_t)kvh * T, (uint32_t)(T * 2));
+      x.sv = make_rsrc(a.scale_v + (int64_t)kvh * T, (uint32_t)(T * 2));
+    }
   }
   const uint16_t* bk_rows = a.basis + (int64_t)b * a.basis_b_stride + (int64_t)kvh * 2 * RB * D;
 
@@ -744,8 +749,11 @@ hipError_t launch_tl_rb(int rb, int g, const SplitArgs& a, int n_work, hipStream
 
 }  // namespace
 
-bool token_lane_supported(int rb, int g, int max_level) {
-  return (g == 1 || g == 2 || g == 4) && rb % 16 == 0 && rb >= 16 && rb <= 64 && max_level <= kMaxRank;
+bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t res_stride) {
+  // every slab must stay below 2^31 bytes for the 32-bit buffer offsets
+  const int64_t lim = (int64_t)1 << 31;
+  return (g == 1 || g == 2 || g == 4) && rb % 16 == 0 && rb >= 16 && rb <= 64 && max_level <= kMaxRank &&
+         (tokens + 64) * rb * 2 < lim && (tokens + 64) * 4 < lim && res_stride < lim;
 }
 
 hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {

@@ -160,7 +160,7 @@ hipError_t launch_split(int rb, int g, bool resid, bool ident, const SplitArgs& 
                         hipStream_t s);
 // Token-lane variant of the split pass (query groups of 1, 2 or 4 heads, basis
 // ranks 16..64, at most 16 residual entries per token); same partials.
-bool token_lane_supported(int rb, int g, int max_level);
+bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t res_stride);
 hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, int n_mh, hipStream_t s);
