@@ -171,21 +171,28 @@ def main():
             graph.replay()
         torch.cuda.synchronize()
 
-    # timed region: K steps.  The last step runs every layer as its two halves:
-    # first the split-K pass of all L layers back to back (each layer into its
-    # own workspace), then the L merges, with one event pair around each run on
-    # the kernels' stream.  That times the split-K kernel (the dominant one) on
-    # its own without an event between every pair of launches.
+    # timed region: K steps.  The last step carries events on the kernels'
+    # stream.  When one decode is one launch (the split kernel merges itself),
+    # a pair around the step times that kernel: span / L.  Otherwise the step
+    # runs every layer as its two halves, first the split-K pass of all L
+    # layers back to back (each layer into its own workspace), then the L
+    # merges, with one event pair around each run.
+    fused = dc.decode_launches == 1
     ev_step = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     ev_calls = [torch.cuda.Event(enable_timing=True) for _ in range(3)] if graph is None else None
-    ws_layer = [torch.empty(dc.workspace_bytes(), dtype=torch.uint8, device="cuda") for _ in range(L)] \
-        if graph is None else None
+    ws_layer = [dc.new_workspace() for _ in range(L)] \
+        if graph is None and not fused else None
     torch.cuda.synchronize()
     ev_step[0].record(stream)
     wall0 = time.perf_counter()
     for k in range(args.steps):
         if graph is not None:
             graph.replay()
+        elif k == args.steps - 1 and fused:
+            ev_calls[0].record(stream)
+            step()
+            ev_calls[1].record(stream)
+            ev_calls[2].record(stream)
         elif k == args.steps - 1:
             ev_calls[0].record(stream)
             for l in range(L):
@@ -204,7 +211,7 @@ def main():
     split_ms = merge_ms = None
     if ev_calls is not None:
         split_ms = ev_calls[0].elapsed_time(ev_calls[1]) / L
-        merge_ms = ev_calls[1].elapsed_time(ev_calls[2]) / L
+        merge_ms = None if fused else ev_calls[1].elapsed_time(ev_calls[2]) / L
 
     bytes_layer = algorithmic_bytes_per_layer(host)
     bytes_step = float(sum(bytes_layer))
@@ -237,10 +244,12 @@ def main():
                    "graph": bool(graph is not None)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "kernel": "split_kernel (split-K partials pass)"},
+                     "kernel": ("tl_kernel (split-K pass with the merge in its last workgroups)" if fused
+                                else "split-K partials pass")},
         "step_gbps": round(step_gbps, 1),
         "bytes_per_step": int(bytes_step),
         "bytes_per_layer_call": int(np.mean(bytes_layer)),
+        "launches_per_layer": dc.decode_launches,
         "split_kernel_ms": round(avg_split_ms, 5),
         "merge_kernel_ms": round(float(merge_ms), 5) if merge_ms is not None else None,
         "compression_vs_fp16": round(dense_fp16_bytes_per_layer(host) / np.mean(bytes_layer), 3),

@@ -102,6 +102,11 @@ class DeviceCache:
     def split_tokens(self) -> int:
         return int(self.lib.dwkv_split_tokens(C.byref(self.dims)))
 
+    @property
+    def decode_launches(self) -> int:
+        """Kernel launches of one decode call without a probe (1: the split kernel merges itself)."""
+        return int(self.lib.dwkv_decode_launches(C.byref(self.dims), None))
+
     def _probe_struct(self, probe: ProbeRef | None, err, out_ref):
         if probe is None:
             return None, None
@@ -125,13 +130,17 @@ class DeviceCache:
             raise DwkvError(2, "dwkv_workspace_bytes")
         return int(n)
 
+    def new_workspace(self, probe: ProbeRef | None = None):
+        """A zero-filled decode workspace (its arrival counters must start at zero)."""
+        return self.torch.zeros(self.workspace_bytes(probe), dtype=self.torch.uint8, device=self.device)
+
     def workspace(self, probe: ProbeRef | None = None):
         """A decode workspace, allocated once per probe shape and reused."""
         need = self.workspace_bytes(probe)
         key = None if probe is None else len(probe.kv_heads)
         ws = self._ws.get(key)
         if ws is None or ws.numel() < need:
-            ws = self.torch.empty(need, dtype=self.torch.uint8, device=self.device)
+            ws = self.new_workspace(probe)
             self._ws[key] = ws
         return ws
 

@@ -52,7 +52,7 @@ class Probe(C.Structure):
 
 
 EXPORTS = ["dwkv_abi_version", "dwkv_status_str", "dwkv_split_tokens", "dwkv_workspace_bytes",
-           "dwkv_decode", "dwkv_decode_partials", "dwkv_decode_merge", "dwkv_route_workspace_bytes", "dwkv_route", "dwkv_residual_map",
+           "dwkv_decode_launches", "dwkv_decode", "dwkv_decode_partials", "dwkv_decode_merge", "dwkv_route_workspace_bytes", "dwkv_route", "dwkv_residual_map",
            "dwkv_validate_workspace_bytes", "dwkv_validate"]
 
 _lib = None
@@ -74,6 +74,8 @@ def load(path: str = LIB_PATH):
     lib.dwkv_split_tokens.argtypes = [P(Dims)]
     lib.dwkv_workspace_bytes.restype = C.c_size_t
     lib.dwkv_workspace_bytes.argtypes = [P(Dims), P(Probe)]
+    lib.dwkv_decode_launches.restype = C.c_int32
+    lib.dwkv_decode_launches.argtypes = [P(Dims), P(Probe)]
     lib.dwkv_decode.restype = C.c_int
     lib.dwkv_decode.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_void_p, C.c_int32, C.c_float,
                                 C.c_void_p, P(Probe), C.c_void_p, C.c_size_t, C.c_void_p]

@@ -1,4 +1,5 @@
 // C ABI of the library: argument checks, split planning, launches.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 
@@ -93,9 +94,10 @@ dwkv_status check_probe(const dwkv_dims* d, const dwkv_probe* p) {
   return DWKV_OK;
 }
 
-// Workspace: the partials of the decode pass, then those of the probe pass.
+// Workspace: the partials of the decode pass, those of the probe pass, then
+// one arrival counter per (sequence, KV head) for the fused merge.
 struct WsLayout {
-  size_t main_bytes, ref_bytes, total;
+  size_t main_bytes, ref_bytes, cnt_off, total;
 };
 
 WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
@@ -106,8 +108,8 @@ WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
   WsLayout w;
   w.main_bytes = align_up((size_t)nw * d->n_kv_heads * g * stride * sizeof(float), 256);
   w.ref_bytes = p ? align_up((size_t)nw * p->n_heads * g * kPartStride * sizeof(float), 256) : 0;
-  w.total = w.main_bytes + w.ref_bytes;
-  if (w.total == 0) w.total = 256;
+  w.cnt_off = w.main_bytes + w.ref_bytes;
+  w.total = w.cnt_off + align_up((size_t)d->batch * d->n_kv_heads * sizeof(uint32_t), 256);
   return w;
 }
 
@@ -124,6 +126,23 @@ WorkTable work_table(const dwkv_dims* d, int split) {
     t.work[b + 1] = t.work[b] + (int32_t)((len + split - 1) / split);
   }
   return t;
+}
+
+// The split kernel merges in its last workgroup per (sequence, KV head) when
+// it is the token-lane kernel, there is no probe pass, every sequence has a
+// token (an empty one has no workgroup to write its zero output) and the
+// partials of a sequence span less than 2^31 bytes (32-bit buffer offsets).
+bool fused_merge(const dwkv_dims* d, const dwkv_probe* p) {
+  if (p || !uses_token_lane(d)) return false;
+  const int split = plan_split(d);
+  int64_t most = 0;
+  for (int b = 0; b < d->batch; ++b) {
+    const int64_t len = d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b];
+    if (len == 0) return false;
+    most = std::max<int64_t>(most, (len + split - 1) / split);
+  }
+  const int64_t g = d->n_q_heads / d->n_kv_heads;
+  return most * d->n_kv_heads * g * kPartStrideTL * (int64_t)sizeof(float) < ((int64_t)1 << 31);
 }
 
 }  // namespace
@@ -155,6 +174,11 @@ size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe) {
   return ws_layout(dims, probe).total;
 }
 
+int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe) {
+  if (check_dims(dims) != DWKV_OK || check_probe(dims, probe) != DWKV_OK) return -1;
+  return fused_merge(dims, probe) ? 1 : probe ? 3 : 2;
+}
+
 }  // extern "C"
 
 namespace {
@@ -170,9 +194,10 @@ dwkv_status check_decode_common(const dwkv_dims* d, const dwkv_probe* probe, voi
 }
 
 // Split-K pass(es): partial (o, m, l) per (work item, head slot, group member).
+// With `out` set (only when fused_merge holds) the split kernel also merges.
 dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
                            int32_t q_type, float sm_scale, const dwkv_probe* probe, void* workspace,
-                           hipStream_t s) {
+                           float* out, hipStream_t s) {
   if (!c || !q) return DWKV_E_NULL;
   if (!c->basis || !c->coef_k || !c->coef_v || !c->res_off || !c->res_idx || !c->res_val ||
       !c->res_scale)
@@ -211,6 +236,8 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   a.q = static_cast<const uint16_t*>(q);
   a.cu = d->cu_seqlens;
   a.part = reinterpret_cast<float*>(ws);
+  a.out = out;
+  a.cnt = reinterpret_cast<uint32_t*>(ws + wl.cnt_off);
   a.T = T;
   a.res_stride = d->res_stride;
   a.batch = d->batch;
@@ -231,6 +258,7 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
     r.coef_k = static_cast<const uint16_t*>(probe->k_ref);
     r.coef_v = static_cast<const uint16_t*>(probe->v_ref);
     r.part = reinterpret_cast<float*>(ws + wl.main_bytes);
+    r.out = nullptr;
     r.n_slots = probe->n_heads;
     for (int i = 0; i < probe->n_heads; ++i) r.kv_of_slot[i] = probe->kv_heads_host[i];
     if (launch_split(kHeadDim, G, false, true, r, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
@@ -246,6 +274,24 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
   const WsLayout wl = ws_layout(d, probe);
   char* ws = static_cast<char*>(workspace);
+  if (!probe && uses_token_lane(d)) {
+    SplitArgs a;
+    std::memset(&a, 0, sizeof(a));
+    const int64_t Hk = d->n_kv_heads, M = d->n_layers / d->window, m = layer / d->window;
+    a.basis = static_cast<const uint16_t*>(c->basis) + m * Hk * 2 * d->basis_rank * kHeadDim;
+    a.basis_b_stride = M * Hk * 2 * d->basis_rank * kHeadDim;
+    a.cu = d->cu_seqlens;
+    a.part = reinterpret_cast<float*>(ws);
+    a.out = out;
+    a.batch = d->batch;
+    a.n_q_heads = d->n_q_heads;
+    a.n_kv_heads = d->n_kv_heads;
+    a.n_slots = d->n_kv_heads;
+    a.split = plan_split(d);
+    for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
+    a.wt = work_table(d, a.split);
+    return hip_status(launch_merge_tl(d->basis_rank, d->n_q_heads / d->n_kv_heads, a, s));
+  }
   MergeArgs mg;
   std::memset(&mg, 0, sizeof(mg));
   mg.part = reinterpret_cast<const float*>(ws);
@@ -285,7 +331,8 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   if (st != DWKV_OK) return st;
   if (!out) return DWKV_E_NULL;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if ((st = partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, s)) != DWKV_OK) return st;
+  if (fused_merge(d, probe)) return partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, out, s);
+  if ((st = partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, nullptr, s)) != DWKV_OK) return st;
   return merge_phase(d, c, layer, out, probe, workspace, s);
 }
 
@@ -294,7 +341,7 @@ dwkv_status dwkv_decode_partials(const dwkv_dims* d, const dwkv_cache* c, int32_
                                  size_t ws_bytes, void* stream) {
   dwkv_status st = check_decode_common(d, probe, workspace, ws_bytes);
   if (st != DWKV_OK) return st;
-  return partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace,
+  return partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, nullptr,
                         reinterpret_cast<hipStream_t>(stream));
 }
 

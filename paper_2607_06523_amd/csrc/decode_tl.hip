@@ -29,8 +29,11 @@
 //    blocks cover 64 coefficient channels, read as 4 consecutive tokens of one
 //    channel from the 16-token value blocks.  The accumulator holds, in lane c,
 //    the basis-space value of channel c for the 4 heads.
-//  * the epilogue combines the 4 waves and writes the partial in basis space
-//    (a~, the residual channels, m, l); the merge kernel applies B^V.
+//  * the epilogue combines the waves and writes the partial in basis space
+//    (a~, the residual channels, m, l).  The last workgroup of a (sequence,
+//    KV head) to finish merges its partials in a fixed order and applies B^V;
+//    the partials travel through device-coherent stores and loads and one
+//    arrival counter, so no cache write-back is needed.
 #include <utility>
 
 #include "entry.h"
@@ -64,6 +67,17 @@ struct TCfg {
   static_assert(RB % 16 == 0 && RB >= 16 && RB <= 64, "basis rank");
 };
 
+// LDS of the merge of a (sequence, KV head)'s partials.
+template <int RB>
+struct TMSmem {
+  f4 red[kTThreads];                    // per lane: its merged column quad
+  float wm[kTW], wl[kTW];               // per wave: running maximum and sum
+  alignas(16) float rfin[HG][D];        // merged residual channels / l
+  float abar[HG][RB];                   // merged a~ / l
+  float pr[kTW][HG][D];                 // projection sums of each wave's basis rows
+  int last;
+};
+
 template <int RB, bool RESID>
 struct alignas(16) TSmem {
   alignas(16) float qs[D][HG];          // q * sm_scale * log2(e), heads past G zero
@@ -79,6 +93,7 @@ struct alignas(16) TSmem {
   alignas(4) uint8_t emap[kTW][RESID ? kEmap : 4];  // token lane + 1 at each token's first entry
   alignas(16) float pw[kTW][RESID ? TT : 1][HG];  // p * value scale per token lane
   int fx[kTW];
+  TMSmem<RB> mg;
 };
 
 template <int RB>
@@ -468,6 +483,123 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   }
 }
 
+constexpr int kSc1 = 16;                // buffer cache policy: device-coherent access
+
+// Merges the partials of sequence b, slot `slot` (work items base .. base+ns-1)
+// in a fixed order and writes o = r + a~ B^V for the slot's G heads.  A wave
+// of head g merges every NWH-th partial, one column quad per lane (the row's
+// m and l come in one lane each and are broadcast); the waves of a head then
+// combine.  The projection gives each wave RB/8 rows of B^V for all G heads.
+// The partials are read with device-coherent loads: other workgroups,
+// possibly on other XCDs, wrote them in this launch.
+template <int RB, int G>
+__device__ __forceinline__ void tl_merge(const SplitArgs& a, TMSmem<RB>& sm, int b, int slot, int base,
+                                         int ns) {
+  constexpr int TPH = kTThreads / G;    // threads per head
+  constexpr int NWH = TPH / 64;         // waves per head
+  constexpr int Q = (D + RB) / 4;       // column quads of a row: r, then a~
+  constexpr int KB = RB / kTW;          // basis rows per wave in the projection
+  constexpr int RPL = 32 / NWH;         // partials per lane per round: 32 per head
+  static_assert(Q <= 64 && RB % kTW == 0 && RPL <= 64, "merge layout");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar addressing
+  const int g = wv / NWH, wh = wv % NWH, w0 = wv - wh;
+  const int kvh = a.kv_of_slot[slot];
+  // B^V rows [wv KB, wv KB + KB), channels 2 lane and 2 lane + 1
+  const uint16_t* bv = a.basis + (int64_t)b * a.basis_b_stride + ((int64_t)kvh * 2 + 1) * RB * D;
+  uint32_t bvr[KB];
+#pragma unroll
+  for (int k = 0; k < KB; ++k) bvr[k] = *reinterpret_cast<const uint32_t*>(bv + (wv * KB + k) * D + 2 * lane);
+  // partial s of head g at float offset s * rs from p0
+  const int64_t rs = (int64_t)a.n_slots * G * kPartStrideTL;
+  const float* p0 = a.part + (((int64_t)base * a.n_slots + slot) * G + g) * kPartStrideTL;
+  const rsrc_t pr = make_rsrc(p0, (uint32_t)(max(ns, 1) * rs * 4));
+  const int q = min(lane, Q - 1);       // lanes past Q repeat the last quad, unused
+  f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+  float mstar = -INFINITY, lsum = 0.f;
+  for (int s0 = 0; s0 < ns; s0 += NWH * RPL) {
+    u4v xv[RPL];
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+      const uint32_t s = (uint32_t)min(s0 + wh + NWH * i, ns - 1);
+      xv[i] = __builtin_amdgcn_raw_buffer_load_b128(pr, (uint32_t)((s * rs + 4 * q) * 4), 0, kSc1);
+    }
+    // lane i < RPL: (m, l) of the round's i-th partial
+    const uint32_t sl = (uint32_t)min(s0 + wh + NWH * min(lane, RPL - 1), ns - 1);
+    const u2v ml = __builtin_amdgcn_raw_buffer_load_b64(pr, (uint32_t)((sl * rs + kPartTLM) * 4), 0, kSc1);
+    __builtin_amdgcn_sched_barrier(0);  // every request of the round in flight before the first wait
+    float mv[RPL];
+    float mr = mstar;
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+      mv[i] = s0 + wh + NWH * i < ns ? __int_as_float(__builtin_amdgcn_readlane((int)ml.x, i)) : -INFINITY;
+      mr = fmaxf(mr, mv[i]);
+    }
+    const float resc = mstar == -INFINITY ? 0.f : exp2f(mstar - mr);
+    acc *= resc;
+    lsum *= resc;
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+      const float w = mv[i] == -INFINITY ? 0.f : exp2f(mv[i] - mr);
+      acc += w * __builtin_bit_cast(f4, xv[i]);
+      lsum += w * __int_as_float(__builtin_amdgcn_readlane((int)ml.y, i));
+    }
+    mstar = mr;
+  }
+  sm.red[tid] = acc;
+  if (lane == 0) {
+    sm.wm[wv] = mstar;
+    sm.wl[wv] = lsum;
+  }
+  __syncthreads();
+  if (wh == 0 && lane < Q) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < NWH; ++j) mx = fmaxf(mx, sm.wm[w0 + j]);
+    f4 o = f4{0.f, 0.f, 0.f, 0.f};
+    float l = 0.f;
+#pragma unroll
+    for (int j = 0; j < NWH; ++j) {
+      const float e = sm.wm[w0 + j] == -INFINITY ? 0.f : exp2f(sm.wm[w0 + j] - mx);
+      o += e * sm.red[(w0 + j) * 64 + lane];
+      l += e * sm.wl[w0 + j];
+    }
+    o *= l > 0.f ? 1.0f / l : 0.f;
+    if (lane < D / 4) *reinterpret_cast<f4*>(&sm.rfin[g][4 * lane]) = o;
+    else *reinterpret_cast<f4*>(&sm.abar[g][4 * (lane - D / 4)]) = o;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float o0 = 0.f, o1 = 0.f;
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+      const float ak = sm.abar[h][wv * KB + k];
+      o0 += ak * half_bits_to_float((uint16_t)(bvr[k] & 0xFFFF));
+      o1 += ak * half_bits_to_float((uint16_t)(bvr[k] >> 16));
+    }
+    sm.pr[wv][h][2 * lane] = o0;
+    sm.pr[wv][h][2 * lane + 1] = o1;
+  }
+  __syncthreads();
+  if (tid < G * D) {
+    const int h = tid / D, c = tid % D;
+    float o = sm.rfin[h][c];
+#pragma unroll
+    for (int w = 0; w < kTW; ++w) o += sm.pr[w][h][c];
+    a.out[((int64_t)b * a.n_q_heads + kvh * G + h) * D + c] = o;
+  }
+}
+
+template <int RB, int G>
+__global__ __launch_bounds__(kTThreads) void tl_merge_kernel(const SplitArgs a) {
+  __shared__ TMSmem<RB> sm;
+  const int slot = blockIdx.x, b = blockIdx.y;
+  int base, ns;
+  seq_work(a.wt, a.cu, a.split, b, base, ns);
+  tl_merge<RB, G>(a, sm, b, slot, base, ns);
+}
+
 template <int RB, int G, bool RESID>
 __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   using C = TCfg<RB>;
@@ -711,13 +843,30 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
 #pragma unroll
         for (int v = 0; v < kTW; ++v) o += sw[v] * sm.ep_a[v][g][c - D];
       }
-      dst[c] = o;
+      __hip_atomic_store(dst + c, o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     if (tid % TPH == 0) {
-      dst[kPartTLM] = mx;
-      dst[kPartTLM + 1] = l;
+      __hip_atomic_store(dst + kPartTLM, mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(dst + kPartTLM + 1, l, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
+  if (a.out == nullptr) return;         // a separate merge launch finishes
+  // Fused merge: once this workgroup's partial stores are complete (they are
+  // device-coherent, so completion makes them visible to every XCD), count
+  // its arrival; the last arrival of the (sequence, slot) merges.
+  int base, ns;
+  seq_work(a.wt, a.cu, a.split, b, base, ns);
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  __syncthreads();
+  uint32_t* cnt = a.cnt + (int64_t)b * a.n_slots + slot;
+  if (tid == 0) {
+    const uint32_t seen = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    sm.mg.last = seen == (uint32_t)(ns - 1);
+    if (seen == (uint32_t)(ns - 1)) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!sm.mg.last) return;
+  tl_merge<RB, G>(a, sm.mg, b, slot, base, ns);
 }
 
 template <int RB, int G, bool R>
@@ -749,6 +898,18 @@ hipError_t launch_tl_rb(int rb, int g, const SplitArgs& a, int n_work, hipStream
 
 }  // namespace
 
+template <int RB>
+hipError_t launch_merge_tl_rb(int g, const SplitArgs& a, hipStream_t s) {
+  const dim3 grid(a.n_slots, a.batch);
+  switch (g) {
+    case 1: hipLaunchKernelGGL((tl_merge_kernel<RB, 1>), grid, dim3(kTThreads), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((tl_merge_kernel<RB, 2>), grid, dim3(kTThreads), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((tl_merge_kernel<RB, 4>), grid, dim3(kTThreads), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t res_stride) {
   // every slab must stay below 2^31 bytes for the 32-bit buffer offsets
   const int64_t lim = (int64_t)1 << 31;
@@ -758,6 +919,16 @@ bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t 
 
 hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {
   return resid ? launch_tl_rb<true>(rb, g, a, n_work, s) : launch_tl_rb<false>(rb, g, a, n_work, s);
+}
+
+hipError_t launch_merge_tl(int rb, int g, const SplitArgs& a, hipStream_t s) {
+  switch (rb) {
+    case 16: return launch_merge_tl_rb<16>(g, a, s);
+    case 32: return launch_merge_tl_rb<32>(g, a, s);
+    case 48: return launch_merge_tl_rb<48>(g, a, s);
+    case 64: return launch_merge_tl_rb<64>(g, a, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace dwkv
