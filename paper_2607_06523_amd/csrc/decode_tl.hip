@@ -6,9 +6,10 @@
 // (sum_t p_t A^V_t) B^V plus the routed residual channels), organised so that
 // every lane of a wave owns one token of a 64-token tile for the whole step:
 //
-//  * scores on v_mfma_f32_16x16x16_f16 with the coefficient rows as the B
-//    operand (column = token) and q~ = B^K q as the A operand, its 4 head rows
-//    repeated in each of the 4 row groups.  The result of 16-token block bk then
+//  * scores on v_mfma_f32_16x16x32_f16 (16x16x16 for an odd 16-deep rest of
+//    r_b) with the coefficient rows as the B operand (column = token) and
+//    q~ = B^K q as the A operand, its 4 head rows repeated in each of the 4
+//    row groups.  The result of 16-token block bk then
 //    holds the 4 head scores of token 16bk+c in lane c of every lane group, and
 //    lane 16g+c keeps block g's copy: each lane ends up with its own token's
 //    scores for all heads, in registers.
@@ -43,6 +44,7 @@ namespace dwkv {
 namespace {
 
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 typedef uint32_t u3v __attribute__((ext_vector_type(3)));
@@ -142,6 +144,15 @@ __device__ __forceinline__ f4 mfma16(h4 a, h4 b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
 }
 
+// 16x16x32: same cost per instruction as 16x16x16 on gfx950, twice the depth.
+// The operand k index of (lane group, element) only has to agree between A
+// and B, so two 4-element quads of a lane form one 8-element operand.
+__device__ __forceinline__ f4 mfma32(h4 a0, h4 a1, h4 b0, h4 b1, f4 c) {
+  const h8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+  const h8 b = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
 __device__ __forceinline__ int32_t tstart(const TCtx& x, int j) { return x.tb + j * TT; }
 
 // signed 4-bit code in bits [4n, 4n+4) of w
@@ -157,9 +168,14 @@ __device__ __forceinline__ void load_k(TFrags<RB>& f, const TCtx& x, int j, int 
 #pragma unroll
   for (int bk = 0; bk < 4; ++bk) {
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s) {
-      const u2v w = __builtin_amdgcn_raw_buffer_load_b64(x.ck, base + bk * 16 * RB * 2 + 8 * s, 0, 0);
+    for (int s = 0; s + 1 < C::NS; s += 2) {
+      const u4v w = __builtin_amdgcn_raw_buffer_load_b128(x.ck, base + bk * 16 * RB * 2 + 8 * s, 0, 0);
       f.k[bk][s] = make_uint2(w.x, w.y);
+      f.k[bk][s + 1] = make_uint2(w.z, w.w);
+    }
+    if constexpr (C::NS % 2 == 1) {
+      const u2v w = __builtin_amdgcn_raw_buffer_load_b64(x.ck, base + bk * 16 * RB * 2 + 8 * (C::NS - 1), 0, 0);
+      f.k[bk][C::NS - 1] = make_uint2(w.x, w.y);
     }
   }
 }
@@ -322,13 +338,21 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
 #pragma unroll
   for (int bk = 0; bk < 4; ++bk) sacc[bk] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int s = 0; s < NS; ++s)
+  for (int s = 0; s + 1 < NS; s += 2)
 #pragma unroll
     for (int bk = 0; bk < 4; ++bk) {
-      const h4 kf = __builtin_bit_cast(h4, fr.k[bk][s]);
-      sacc[bk] = mfma16(st.qhi[s], kf, sacc[bk]);
-      sacc[bk] = mfma16(st.qlo[s], kf, sacc[bk]);
+      const h4 k0 = __builtin_bit_cast(h4, fr.k[bk][s]), k1 = __builtin_bit_cast(h4, fr.k[bk][s + 1]);
+      sacc[bk] = mfma32(st.qhi[s], st.qhi[s + 1], k0, k1, sacc[bk]);
+      sacc[bk] = mfma32(st.qlo[s], st.qlo[s + 1], k0, k1, sacc[bk]);
     }
+  if constexpr (NS % 2 == 1) {
+#pragma unroll
+    for (int bk = 0; bk < 4; ++bk) {
+      const h4 kf = __builtin_bit_cast(h4, fr.k[bk][NS - 1]);
+      sacc[bk] = mfma16(st.qhi[NS - 1], kf, sacc[bk]);
+      sacc[bk] = mfma16(st.qlo[NS - 1], kf, sacc[bk]);
+    }
+  }
   load_k<RB>(fr, x, jn_l, lane);
   float sc[HG];
 #pragma unroll
