@@ -83,12 +83,12 @@ def cpu_baseline(host, n_pairs: int, budget_s: float):
 
 
 def measured_traffic(workload: str):
-    """HBM bytes per split-kernel launch from the committed rocprofv3 counter
-    profile, or None when that profile is missing or was taken on a different
-    kernel source."""
+    """HBM bytes per launch of the token-lane decode kernel from the committed
+    rocprofv3 counter profile, or None when that profile is missing or was
+    taken on a different kernel source."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"split_kernel_{workload}_hbm_bytes.json")
-    src = os.path.join(ROOT, "paper_2607_06523_amd", "csrc", "decode.hip")
+    path = os.path.join(ROOT, "profiles", f"tl_kernel_{workload}_hbm_bytes.json")
+    src = os.path.join(ROOT, "paper_2607_06523_amd", "csrc", "decode_tl.hip")
     try:
         rec = json.load(open(path))
         sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
@@ -244,7 +244,7 @@ def main():
                    "graph": bool(graph is not None)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "kernel": ("tl_kernel (split-K pass with the merge in its last workgroups)" if fused
+                     "kernel": ("tl_kernel (token-lane split-K pass, merge in its last workgroups)" if fused
                                 else "split-K partials pass")},
         "step_gbps": round(step_gbps, 1),
         "bytes_per_step": int(bytes_step),
