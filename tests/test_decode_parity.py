@@ -38,6 +38,10 @@ SMALL = [
     ("rb112-g2", 112, 2, (0, 2, 6), (0.3, 0.3, 0.4), [777], 256, "bf16"),
     ("rb128-g4-full-rank-residual", 128, 4, (0, 128), (0.5, 0.5), [257, 70], 128, "bf16"),
     ("rb32-g16-many-entries", 32, 16, (32, 64), (0.5, 0.5), [200, 4097], 0, "bf16"),
+    # token-lane kernel: ~900 entries per 64-token tile (past the preloaded batches)
+    ("rb64-g4-entry-heavy", 64, 4, (0, 16), (0.1, 0.9), [1500, 64], 256, "bf16"),
+    # token-lane kernel, more sequences than the kernel-argument work table holds
+    ("rb32-g4-20-seqs", 32, 4, (0, 8), (0.7, 0.3), [37 + 23 * i for i in range(20)], 64, "bf16"),
 ]
 
 
