@@ -12,7 +12,11 @@
  * coefficients and residual entries, and runs softmax attention on chip.
  *
  * Conventions for every entry point
- *  - Pointers are DEVICE pointers unless the name ends in `_host`.
+ *  - Pointers are DEVICE pointers unless the name ends in `_host`.  The decode
+ *    calls read and write them with 16-byte vector accesses: every device
+ *    pointer they take (cache arrays, q, out, workspace) must be 16-byte
+ *    aligned (hipMalloc and torch allocations are; so is any whole-row slice
+ *    of them), else they return DWKV_E_ALIGN.
  *  - All buffers are owned by the caller; the library allocates nothing and
  *    keeps no global mutable state, so calls on different streams do not
  *    interfere (calls sharing one workspace must be ordered by the caller).
@@ -46,7 +50,8 @@ typedef enum dwkv_status {
                              overflow possible                                    */
   DWKV_E_WORKSPACE = 4,   /* workspace smaller than the *_workspace_bytes value    */
   DWKV_E_LAYOUT = 5,      /* dwkv_validate found a malformed cache                 */
-  DWKV_E_HIP = 6          /* a HIP runtime call or kernel launch failed            */
+  DWKV_E_HIP = 6,         /* a HIP runtime call or kernel launch failed            */
+  DWKV_E_ALIGN = 7        /* a decode device pointer is not 16-byte aligned         */
 } dwkv_status;
 
 typedef enum dwkv_qtype { DWKV_F16 = 0, DWKV_BF16 = 1 } dwkv_qtype;

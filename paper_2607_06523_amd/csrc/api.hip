@@ -14,6 +14,7 @@ constexpr int kSplitQuantum = 256;       // automatic chunks are multiples of th
 constexpr int kSplitMax = 8192;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 bool is_pow2_group(int g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
 
@@ -84,6 +85,7 @@ dwkv_status check_probe(const dwkv_dims* d, const dwkv_probe* p) {
   if (!p) return DWKV_OK;
   if (p->n_heads < 1 || p->n_heads > d->n_kv_heads || p->n_heads > DWKV_MAX_PROBE_HEADS) return DWKV_E_DIMS;
   if (!p->kv_heads_host || !p->k_ref || !p->v_ref || !p->err) return DWKV_E_NULL;
+  if (!aligned16(p->k_ref) || !aligned16(p->v_ref) || !aligned16(p->out_ref)) return DWKV_E_ALIGN;
   bool seen[DWKV_MAX_PROBE_HEADS] = {};
   for (int i = 0; i < p->n_heads; ++i) {
     const int h = p->kv_heads_host[i];
@@ -160,6 +162,7 @@ const char* dwkv_status_str(dwkv_status s) {
     case DWKV_E_WORKSPACE: return "workspace too small";
     case DWKV_E_LAYOUT: return "malformed cache layout";
     case DWKV_E_HIP: return "HIP runtime error";
+    case DWKV_E_ALIGN: return "device pointer not 16-byte aligned";
   }
   return "unknown status";
 }
@@ -188,6 +191,7 @@ dwkv_status check_decode_common(const dwkv_dims* d, const dwkv_probe* probe, voi
   dwkv_status st = check_dims(d);
   if (st != DWKV_OK) return st;
   if (!workspace) return DWKV_E_NULL;
+  if (!aligned16(workspace)) return DWKV_E_ALIGN;
   if ((st = check_probe(d, probe)) != DWKV_OK) return st;
   if (ws_bytes < ws_layout(d, probe).total) return DWKV_E_WORKSPACE;
   return DWKV_OK;
@@ -204,6 +208,9 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
     return DWKV_E_NULL;
   if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
   if (q_type != DWKV_F16 && q_type != DWKV_BF16) return DWKV_E_DIMS;
+  const void* const ptrs[] = {q, c->basis, c->coef_k, c->coef_v, c->res_off, c->res_idx, c->res_val, c->res_scale};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return DWKV_E_ALIGN;
   const WsLayout wl = ws_layout(d, probe);
   const int G = d->n_q_heads / d->n_kv_heads;
   const int RB = d->basis_rank;
@@ -272,6 +279,7 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
                         const dwkv_probe* probe, void* workspace, hipStream_t s) {
   if (!out || !c || !c->basis) return DWKV_E_NULL;
   if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
+  if (!aligned16(out) || !aligned16(c->basis)) return DWKV_E_ALIGN;
   const WsLayout wl = ws_layout(d, probe);
   char* ws = static_cast<char*>(workspace);
   if (!probe && uses_token_lane(d)) {
@@ -330,6 +338,7 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   dwkv_status st = check_decode_common(d, probe, workspace, ws_bytes);
   if (st != DWKV_OK) return st;
   if (!out) return DWKV_E_NULL;
+  if (!aligned16(out)) return DWKV_E_ALIGN;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if (fused_merge(d, probe)) return partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, out, s);
   if ((st = partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, nullptr, s)) != DWKV_OK) return st;

@@ -668,26 +668,26 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   // Requests in issue order (vector loads complete in order): the fragments
   // of the q~ product (B^K rows, q); the query for the LDS table; the first
   // tile's offsets and scales; its coefficient fragments; last its residual
-  // entries, whose addresses need the offsets.  Every load is unconditional (a
-  // wave with no tile reads the chunk's last one and never uses it; a wave
-  // past the basis blocks repeats the last block).
+  // entries, whose addresses need the offsets.  Every tile load is
+  // unconditional (a wave with no tile reads the chunk's last one and never
+  // uses it); only the waves that own basis rows request q~ fragments.
   constexpr int QPT = (G * D + kTThreads - 1) / kTThreads;     // query elements per thread
   const int j0 = min(wv, x.ntile - 1);
   const int j1 = min(wv + kTW, x.ntile - 1);
   TFrags<RB> fr;
   TMeta mc{}, mn{}, mnn{};
   TEnt ec{}, en{};
-  // q~ fragments: wave w takes basis rows [16w, 16w+16): A = B^K rows (row =
-  // lane % 16, channels 16s + 4(lane/16) + i), B = q (column = head lane % 16)
-  const int qmb = min(wv, NS - 1);
-  uint2 bkf[8], qf[8];
-  {
-    const uint16_t* brow = bk_rows + (int64_t)(16 * qmb + col) * D + 4 * grp;
-    const uint16_t* qrow = a.q + ((int64_t)b * a.n_q_heads + kvh * G + min(col, G - 1)) * D + 4 * grp;
+  // q~ fragments, waves below NS only: wave w takes basis rows [16w, 16w+16)
+  // on 16x16x32 MFMA, A = B^K rows (row = lane % 16, channels 32s + 8(lane/16)
+  // + i), B = q (column = head lane % 16)
+  u4v bkf[4], qf[4];
+  if (wv < NS) {
+    const uint16_t* brow = bk_rows + (int64_t)(16 * wv + col) * D + 8 * grp;
+    const uint16_t* qrow = a.q + ((int64_t)b * a.n_q_heads + kvh * G + min(col, G - 1)) * D + 8 * grp;
 #pragma unroll
-    for (int s = 0; s < 8; ++s) bkf[s] = *reinterpret_cast<const uint2*>(brow + 16 * s);
+    for (int s = 0; s < 4; ++s) bkf[s] = *reinterpret_cast<const u4v*>(brow + 32 * s);
 #pragma unroll
-    for (int s = 0; s < 8; ++s) qf[s] = *reinterpret_cast<const uint2*>(qrow + 16 * s);
+    for (int s = 0; s < 4; ++s) qf[s] = *reinterpret_cast<const u4v*>(qrow + 32 * s);
   }
   uint16_t qraw[QPT];
 #pragma unroll
@@ -717,16 +717,16 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
       sm.qs[i % D][i / D] = (a.q_bf16 ? bf16_bits_to_float(qraw[n]) : half_bits_to_float(qraw[n])) * a.qscale;
   }
   __syncthreads();
-  {
+  if (wv < NS) {
     // q * qscale for head col, scaled by a power of two so the head's largest
     // entry sits just under 2^14 and split into fp16 hi + lo
-    float qv[8][4];
+    float qv[4][8];
     float mq = 0.f;
 #pragma unroll
-    for (int s = 0; s < 8; ++s)
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint16_t bits = (uint16_t)(i < 2 ? (qf[s].x >> (16 * i)) : (qf[s].y >> (16 * (i - 2))));
+      for (int i = 0; i < 8; ++i) {
+        const uint16_t bits = (uint16_t)(qf[s][i >> 1] >> (16 * (i & 1)));
         const float v = col < G ? (a.q_bf16 ? bf16_bits_to_float(bits) : half_bits_to_float(bits)) * a.qscale : 0.f;
         qv[s][i] = v;
         mq = fmaxf(mq, fabsf(v));
@@ -742,21 +742,21 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
     const float upq = ldexpf(1.0f, eq);
     f4 dq = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      h4 qh, ql;
+    for (int s = 0; s < 4; ++s) {
+      h8 qh, ql;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < 8; ++i) {
         const float v = qv[s][i] * upq;
         const _Float16 hh = (_Float16)v;
         qh[i] = hh;
         ql[i] = (_Float16)(v - (float)hh);
       }
-      const h4 bkv = __builtin_bit_cast(h4, bkf[s]);
-      dq = mfma16(bkv, qh, dq);
-      dq = mfma16(bkv, ql, dq);
+      const h8 bkv = __builtin_bit_cast(h8, bkf[s]);
+      dq = __builtin_amdgcn_mfma_f32_16x16x32_f16(bkv, qh, dq, 0, 0, 0);
+      dq = __builtin_amdgcn_mfma_f32_16x16x32_f16(bkv, ql, dq, 0, 0, 0);
     }
     // lane (grp, col): q~[head col][row 16w + 4grp + i] = dq[i] / 2^eq
-    if (wv < NS && col < G) {
+    if (col < G) {
       const float dn = ldexpf(1.0f, -eq);
       float am = 0.f;
 #pragma unroll

@@ -36,8 +36,21 @@ def test_exports_every_declared_symbol(lib):
 
 def test_abi_version_and_status_strings(lib):
     assert lib.dwkv_abi_version() == 1
-    for s, text in [(0, b"ok"), (3, b"unsupported shape"), (5, b"malformed cache layout")]:
+    for s, text in [(0, b"ok"), (3, b"unsupported shape"), (5, b"malformed cache layout"),
+                    (7, b"device pointer not 16-byte aligned")]:
         assert lib.dwkv_status_str(s) == text
+
+
+def test_decode_rejects_misaligned_pointers(lib):
+    d, keep = dims()
+    assert decode_status(lib, d, q=FAKE + 8) == 7
+    assert decode_status(lib, d, out=FAKE + 4) == 7
+    from paper_2607_06523_amd import binding
+    c = binding.Cache(*([FAKE] * 8))
+    c.coef_v = FAKE + 2
+    assert lib.dwkv_decode(C.byref(d), C.byref(c), 0, FAKE, 0, 0.0, FAKE, None, FAKE, 1 << 30, None) == 7
+    assert lib.dwkv_decode(C.byref(d), C.byref(binding.Cache(*([FAKE] * 8))), 0, FAKE, 0, 0.0, FAKE, None,
+                           FAKE + 32 + 8, 1 << 30, None) == 7
 
 
 def dims(**kw):
