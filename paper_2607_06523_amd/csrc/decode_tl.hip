@@ -88,13 +88,14 @@ struct alignas(16) TSmem {
   float ep_l[kTW][HG];
   float ep_a[kTW][HG][RB];
   int qmax[HG];
-  // Value residual, per wave.  Accumulators are fixed point (units 2^-fx[w]):
-  // integer LDS atomics run at one instruction per few cycles whatever the
-  // active lanes, float LDS atomics at a few cycles per lane.
+  // Value residual, per wave.  Accumulators are fixed point in units of
+  // 2^(ex - kFxTop) (ex: the wave's bound on the value scales): integer LDS
+  // atomics run at one instruction per few cycles whatever the active lanes,
+  // float LDS atomics at a few cycles per lane.  After its loop a wave
+  // rewrites its accumulators as floats [HG][D] in the same storage.
   long long racc[kTW][RESID ? HG : 1][RESID ? D : 1];
   alignas(4) uint8_t emap[kTW][RESID ? kEmap : 4];  // token lane + 1 at each token's first entry
   alignas(16) float pw[kTW][RESID ? TT : 1][HG];  // p * value scale per token lane
-  int fx[kTW];
   TMSmem<RB> mg;
 };
 
@@ -822,8 +823,26 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   for (int j = wv; j < x.ntile; j += kTW)
     tstep<RB, G, RESID>(st, fr, mc, mn, mnn, ec, en, j, j + kTW, j + 2 * kTW, x, sm, wv, lane);
 
-  // epilogue: the 4 waves merge; the partial keeps a~ in basis space (the
-  // merge kernel projects it through B^V once per sequence and head)
+  // epilogue: the waves combine; the partial keeps a~ in basis space (the
+  // merge projects it through B^V once per sequence and head).  Each wave
+  // first turns its fixed-point residual accumulators into floats in place
+  // (its LDS operations run in order: every lane has read its integers before
+  // the first float is written).
+  if constexpr (RESID) {
+    long long rv[G][2];
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      rv[i][0] = sm.racc[wv][i][lane];
+      rv[i][1] = sm.racc[wv][i][lane + 64];
+    }
+    const float fs = ldexpf(1.0f, st.ex - kFxTop);
+    float* rf = reinterpret_cast<float*>(&sm.racc[wv][0][0]);
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      rf[i * D + lane] = (float)rv[i][0] * fs;
+      rf[i * D + lane + 64] = (float)rv[i][1] * fs;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < HG; ++i) st.l[i] = wave_sum(st.l[i]);
   if (lane == 0) {
@@ -832,7 +851,6 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
       sm.ep_m[wv][i] = st.m[i];
       sm.ep_l[wv][i] = st.l[i];
     }
-    sm.fx[wv] = kFxTop - st.ex;
   }
   if (lane < RB) {
 #pragma unroll
@@ -852,16 +870,13 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
       sw[v] = sm.ep_m[v][g] == -INFINITY ? 0.f : exp2f(sm.ep_m[v][g] - mx);
       l += sw[v] * sm.ep_l[v][g];
     }
-    float rw[kTW];                          // fixed-point units folded into the weights
-#pragma unroll
-    for (int v = 0; v < kTW; ++v) rw[v] = sw[v] * ldexpf(1.0f, -sm.fx[v]);
     float* dst = a.part + (((int64_t)w * a.n_slots + slot) * G + g) * kPartStrideTL;
     for (int c = tid % TPH; c < ROW; c += TPH) {
       float o = 0.f;
       if (c < D) {
         if constexpr (RESID) {
 #pragma unroll
-          for (int v = 0; v < kTW; ++v) o += rw[v] * (float)sm.racc[v][g][c];
+          for (int v = 0; v < kTW; ++v) o += sw[v] * reinterpret_cast<const float*>(&sm.racc[v][0][0])[g * D + c];
         }
       } else {
 #pragma unroll
