@@ -369,6 +369,11 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
     rank = min(mc.ob - mc.oa, (uint32_t)kMaxRank);
     if (mc.ob < mc.oa) rank = 0;
     const Window wk = align_window(ec.ck, ec.vk, mc.oa);
+    // codes past the token's rank read as zero: mask the packed code words
+    // once (rank <= 16, 4 bits per entry)
+    const uint32_t nb = 4u * rank;
+    const uint32_t cd0 = nb >= 32u ? wk.cd[0] : wk.cd[0] & ((1u << nb) - 1u);
+    const uint32_t cd1 = nb <= 32u ? 0u : (nb >= 64u ? wk.cd[1] : wk.cd[1] & ((1u << (nb - 32u)) - 1u));
     float rk[HG] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int qd = 0; qd < kMaxRank / 4; ++qd) {
@@ -379,7 +384,7 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int k = 4 * qd + u;
-        const float code = (uint32_t)k < rank ? code_at(wk.cd[k >> 3], k & 7) : 0.f;
+        const float code = code_at(k < 8 ? cd0 : cd1, k & 7);
 #pragma unroll
         for (int i = 0; i < G; ++i) rk[i] += code * qv[u][i];
       }
