@@ -334,6 +334,32 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   }
   __builtin_amdgcn_sched_barrier(0);
 
+  // 1b. residual work that does not need the scores, requested here so that
+  // its LDS round trips overlap the score MFMAs: the key residual's first
+  // query-table lookups, and the entry->token map of the value residual
+  // (token lanes mark their first entry; a running maximum over the entry
+  // lanes resolves it after the scores)
+  uint32_t rank = 0, e0 = 0, n = 0, cd0 = 0, cd1 = 0;
+  Window wk{};
+  f4 qv0[4];
+  if constexpr (RESID) {
+    rank = min(mc.ob - mc.oa, (uint32_t)kMaxRank);
+    if (mc.ob < mc.oa) rank = 0;
+    wk = align_window(ec.ck, ec.vk, mc.oa);
+    // codes past the token's rank read as zero: mask the packed code words
+    // once (rank <= 16, 4 bits per entry)
+    const uint32_t nb = 4u * rank;
+    cd0 = nb >= 32u ? wk.cd[0] : wk.cd[0] & ((1u << nb) - 1u);
+    cd1 = nb <= 32u ? 0u : (nb >= 64u ? wk.cd[1] : wk.cd[1] & ((1u << (nb - 32u)) - 1u));
+#pragma unroll
+    for (int u = 0; u < 4; ++u) qv0[u] = *reinterpret_cast<const f4*>(&sm.qs[(wk.ch[0] >> (8 * u)) & (D - 1)][0]);
+    e0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)mc.oa);
+    const uint32_t e1 = (uint32_t)__builtin_amdgcn_readlane((int)mc.ob, 63);
+    n = e1 > e0 ? min(e1 - e0, (uint32_t)kEmap) : 0u;
+    for (uint32_t i = 4 * lane; i < n; i += 256) *reinterpret_cast<uint32_t*>(&sm.emap[wv][i]) = 0u;
+    if (rank > 0 && mc.oa - e0 < n) sm.emap[wv][mc.oa - e0] = (uint8_t)(lane + 1);
+  }
+
   // 2. scores: block bk lands in every lane group; lane group g keeps block g
   f4 sacc[4];
 #pragma unroll
@@ -364,19 +390,18 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   }
 
   // 3. key residual: this lane's entries add code * q[c] * scale
-  uint32_t rank = 0;
+  int tk[kVB];                          // value residual: token lane + 1 of each preloaded entry
+  int carry = 0;
   if constexpr (RESID) {
-    rank = min(mc.ob - mc.oa, (uint32_t)kMaxRank);
-    if (mc.ob < mc.oa) rank = 0;
-    const Window wk = align_window(ec.ck, ec.vk, mc.oa);
-    // codes past the token's rank read as zero: mask the packed code words
-    // once (rank <= 16, 4 bits per entry)
-    const uint32_t nb = 4u * rank;
-    const uint32_t cd0 = nb >= 32u ? wk.cd[0] : wk.cd[0] & ((1u << nb) - 1u);
-    const uint32_t cd1 = nb <= 32u ? 0u : (nb >= 64u ? wk.cd[1] : wk.cd[1] & ((1u << (nb - 32u)) - 1u));
     float rk[HG] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int qd = 0; qd < kMaxRank / 4; ++qd) {
+    for (int u = 0; u < 4; ++u) {
+      const float code = code_at(cd0, u);
+#pragma unroll
+      for (int i = 0; i < G; ++i) rk[i] += code * qv0[u][i];
+    }
+#pragma unroll
+    for (int qd = 1; qd < kMaxRank / 4; ++qd) {
       if (__ballot(rank > 4u * qd) == 0) break;
       f4 qv[4];
 #pragma unroll
@@ -392,6 +417,17 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
     const float rs = half_bits_to_float((uint16_t)mc.sk);
 #pragma unroll
     for (int i = 0; i < G; ++i) sc[i] += rk[i] * rs;
+    // the value residual's entry->token map: entry e's token is the last
+    // token lane whose first entry is <= e
+    wave_lds_fence();
+#pragma unroll
+    for (int bb = 0; bb < kVB; ++bb) tk[bb] = sm.emap[wv][64 * bb + lane];
+#pragma unroll
+    for (int bb = 0; bb < kVB; ++bb) {
+      tk[bb] = 64u * bb + lane < n ? tk[bb] : 0;
+      tk[bb] = max(wave_incl_max(tk[bb]), carry);
+      carry = __builtin_amdgcn_readlane(tk[bb], 63);
+    }
   }
   {
     const int32_t t = t0 + lane;
@@ -449,12 +485,9 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   load_v<RB>(fr, x, jn_l, lane);
 
   // 6. value residual, one lane per entry: p * code * scale into the channel
-  // accumulators.  Token lanes publish p * scale and mark their first entry;
-  // a running maximum over the entry lanes gives each entry its token.
+  // accumulators.  Token lanes publish p * scale; entry lanes read their
+  // token's through the map built in step 3.
   if constexpr (RESID) {
-    const uint32_t e0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)mc.oa);
-    const uint32_t e1 = (uint32_t)__builtin_amdgcn_readlane((int)mc.ob, 63);
-    const uint32_t n = e1 > e0 ? min(e1 - e0, (uint32_t)kEmap) : 0u;
     // keep |p * code * s_v| * 2^fx below 2^45 (2^8 * 2^3 * 2^ex): a larger
     // scale exponent shifts the accumulators down first
     {
@@ -477,29 +510,33 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
     const double scale = ldexp(1.0, kFxTop - st.ex);
     const float rs = half_bits_to_float((uint16_t)mc.sv);
     *reinterpret_cast<f4*>(&sm.pw[wv][lane][0]) = f4{p[0] * rs, p[1] * rs, p[2] * rs, p[3] * rs};
-    for (uint32_t i = 4 * lane; i < n; i += 256) *reinterpret_cast<uint32_t*>(&sm.emap[wv][i]) = 0u;
-    if (rank > 0 && mc.oa - e0 < n) sm.emap[wv][mc.oa - e0] = (uint8_t)(lane + 1);
     wave_lds_fence();
-    int carry = 0;
-    for (uint32_t b0 = 0; b0 < n; b0 += 64) {
-      const uint32_t e = b0 + lane;
-      // token of entry e: the last token lane whose first entry is <= e
-      int tk = e < n ? sm.emap[wv][e] : 0;
-      tk = wave_incl_max(tk);
-      tk = max(tk, carry);
-      carry = __builtin_amdgcn_readlane(tk, 63);
+    f4 wv4[kVB];
+#pragma unroll
+    for (int bb = 0; bb < kVB; ++bb) wv4[bb] = *reinterpret_cast<const f4*>(&sm.pw[wv][max(tk[bb] - 1, 0)][0]);
+#pragma unroll
+    for (int bb = 0; bb < kVB; ++bb) {
+      const uint32_t e = 64u * bb + lane;
       if (e < n) {
         const uint32_t ea = e0 + e;
-        uint32_t ch, cb;
-        const int bb = b0 >> 6;
-        if (bb < kVB) {
-          ch = bb == 0 ? ec.vc[0] : (bb == 1 ? ec.vc[1] : ec.vc[2]);
-          cb = bb == 0 ? ec.vv[0] : (bb == 1 ? ec.vv[1] : ec.vv[2]);
-        } else {
-          ch = __builtin_amdgcn_raw_buffer_load_b8(x.idx[1], ea, 0, 0);
-          cb = __builtin_amdgcn_raw_buffer_load_b8(x.val[1], ea >> 1, 0, 0);
-        }
-        const f4 w = *reinterpret_cast<const f4*>(&sm.pw[wv][tk - 1][0]);
+        const float code = (float)int4_value(ec.vv[bb] >> ((ea & 1u) * 4u));
+        const uint32_t c = ec.vc[bb] & (D - 1);
+#pragma unroll
+        for (int i = 0; i < G; ++i)
+          atomicAdd(reinterpret_cast<unsigned long long*>(&sm.racc[wv][i][c]), to_fixed(wv4[bb][i] * code, scale));
+      }
+    }
+    // entries past the preloaded batches (tiles with more than 64 kVB)
+    for (uint32_t b0 = 64u * kVB; b0 < n; b0 += 64) {
+      const uint32_t e = b0 + lane;
+      int t = e < n ? sm.emap[wv][e] : 0;
+      t = max(wave_incl_max(t), carry);
+      carry = __builtin_amdgcn_readlane(t, 63);
+      if (e < n) {
+        const uint32_t ea = e0 + e;
+        const uint32_t ch = __builtin_amdgcn_raw_buffer_load_b8(x.idx[1], ea, 0, 0);
+        const uint32_t cb = __builtin_amdgcn_raw_buffer_load_b8(x.val[1], ea >> 1, 0, 0);
+        const f4 w = *reinterpret_cast<const f4*>(&sm.pw[wv][t - 1][0]);
         const float code = (float)int4_value(cb >> ((ea & 1u) * 4u));
         const uint32_t c = ch & (D - 1);
 #pragma unroll
