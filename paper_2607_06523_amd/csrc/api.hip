@@ -54,10 +54,18 @@ dwkv_status check_dims(const dwkv_dims* d) {
 }
 
 // The token-lane split kernel serves query groups of up to 4 heads with
-// basis ranks up to 64 and ranks up to 16; the general kernel the rest.
+// basis ranks up to 64 and ranks up to 16, as long as one (KV head, query
+// head)'s partials of a sequence span less than 2^31 bytes (its merge reads
+// them through 32-bit offsets); the general kernel serves the rest.
 bool uses_token_lane(const dwkv_dims* d) {
-  return token_lane_supported(d->basis_rank, d->n_q_heads / d->n_kv_heads, max_level(d), d->total_tokens,
-                              d->res_stride);
+  const int g = d->n_q_heads / d->n_kv_heads;
+  const int64_t min_split = d->split_tokens > 0 ? d->split_tokens : kSplitQuantum;
+  int64_t longest = 0;
+  for (int b = 0; b < d->batch; ++b)
+    longest = std::max<int64_t>(longest, d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b]);
+  const int64_t chunks = (longest + min_split - 1) / min_split;
+  return token_lane_supported(d->basis_rank, g, max_level(d), d->total_tokens, d->res_stride) &&
+         chunks * g * kPartStrideTL * (int64_t)sizeof(float) < ((int64_t)1 << 31);
 }
 
 int plan_split(const dwkv_dims* d) {
@@ -131,20 +139,13 @@ WorkTable work_table(const dwkv_dims* d, int split) {
 }
 
 // The split kernel merges in its last workgroup per (sequence, KV head) when
-// it is the token-lane kernel, there is no probe pass, every sequence has a
-// token (an empty one has no workgroup to write its zero output) and the
-// partials of a sequence span less than 2^31 bytes (32-bit buffer offsets).
+// it is the token-lane kernel, there is no probe pass and every sequence has
+// a token (an empty one has no workgroup to write its zero output).
 bool fused_merge(const dwkv_dims* d, const dwkv_probe* p) {
   if (p || !uses_token_lane(d)) return false;
-  const int split = plan_split(d);
-  int64_t most = 0;
-  for (int b = 0; b < d->batch; ++b) {
-    const int64_t len = d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b];
-    if (len == 0) return false;
-    most = std::max<int64_t>(most, (len + split - 1) / split);
-  }
-  const int64_t g = d->n_q_heads / d->n_kv_heads;
-  return most * d->n_kv_heads * g * kPartStrideTL * (int64_t)sizeof(float) < ((int64_t)1 << 31);
+  for (int b = 0; b < d->batch; ++b)
+    if (d->cu_seqlens_host[b + 1] == d->cu_seqlens_host[b]) return false;
+  return true;
 }
 
 }  // namespace
@@ -252,6 +253,7 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   a.n_kv_heads = d->n_kv_heads;
   a.n_slots = d->n_kv_heads;
   a.split = split;
+  a.n_work = (int32_t)nw;
   a.q_bf16 = q_type == DWKV_BF16;
   a.qscale = sm_scale * 1.4426950408889634f;
   for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
@@ -296,6 +298,7 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
     a.n_kv_heads = d->n_kv_heads;
     a.n_slots = d->n_kv_heads;
     a.split = plan_split(d);
+    a.n_work = (int32_t)count_work(d, a.split);
     for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
     a.wt = work_table(d, a.split);
     return hip_status(launch_merge_tl(d->basis_rank, d->n_q_heads / d->n_kv_heads, a, s));
@@ -314,6 +317,7 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   mg.split = plan_split(d);
   mg.wt = work_table(d, mg.split);
   mg.tl = uses_token_lane(d);
+  mg.n_work = (int32_t)count_work(d, mg.split);
   mg.rb = d->basis_rank;
   {
     const int64_t Hk = d->n_kv_heads, M = d->n_layers / d->window, m = layer / d->window;

@@ -850,8 +850,8 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
     u4v bvr[kMergeMaxRB * D / 8 / kMergeThreads];
 #pragma unroll
     for (int n = 0; n < kMergeMaxRB * D / 8 / kMergeThreads; ++n) bvr[n] = bv[min(tid + n * kMergeThreads, nch - 1)];
-    const Merged mg = merge_rows(a.part, row0, row_step, ns, kPartStrideTL, kPartTLM, D + a.rb, red_m, red_l,
-                                 red_o);
+    const Merged mg = merge_rows(a.part, ((int64_t)h * a.n_work + base) * G + g, G, ns, kPartStrideTL, kPartTLM,
+                                 D + a.rb, red_m, red_l, red_o);
 #pragma unroll
     for (int n = 0; n < kMergeMaxRB * D / 8 / kMergeThreads; ++n)
       if (tid + n * kMergeThreads < nch) reinterpret_cast<u4v*>(&bvs[0][0])[tid + n * kMergeThreads] = bvr[n];

@@ -577,9 +577,10 @@ __device__ __forceinline__ void tl_merge(const SplitArgs& a, TMSmem<RB>& sm, int
   uint32_t bvr[KB];
 #pragma unroll
   for (int k = 0; k < KB; ++k) bvr[k] = *reinterpret_cast<const uint32_t*>(bv + (wv * KB + k) * D + 2 * lane);
-  // partial s of head g at float offset s * rs from p0
-  const int64_t rs = (int64_t)a.n_slots * G * kPartStrideTL;
-  const float* p0 = a.part + (((int64_t)base * a.n_slots + slot) * G + g) * kPartStrideTL;
+  // partial s of head g at float offset s * rs from p0 (a slot's partials
+  // are contiguous)
+  const int64_t rs = (int64_t)G * kPartStrideTL;
+  const float* p0 = a.part + (((int64_t)slot * a.n_work + base) * G + g) * kPartStrideTL;
   const rsrc_t pr = make_rsrc(p0, (uint32_t)(max(ns, 1) * rs * 4));
   const int q = min(lane, Q - 1);       // lanes past Q repeat the last quad, unused
   f4 acc = f4{0.f, 0.f, 0.f, 0.f};
@@ -912,7 +913,7 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
       sw[v] = sm.ep_m[v][g] == -INFINITY ? 0.f : exp2f(sm.ep_m[v][g] - mx);
       l += sw[v] * sm.ep_l[v][g];
     }
-    float* dst = a.part + (((int64_t)w * a.n_slots + slot) * G + g) * kPartStrideTL;
+    float* dst = a.part + (((int64_t)slot * a.n_work + w) * G + g) * kPartStrideTL;
     for (int c = tid % TPH; c < ROW; c += TPH) {
       float o = 0.f;
       if (c < D) {

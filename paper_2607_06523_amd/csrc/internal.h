@@ -47,7 +47,7 @@ struct SplitArgs {
   const uint16_t* scale_v;
   const uint16_t* q;           // [B][Hq][d] fp16 or bf16 bits
   const int32_t* cu;           // [B+1] device
-  float* part;                 // [work][n_slots][G][kPartStride]
+  float* part;                 // [work][n_slots][G][kPartStride]; token-lane: [n_slots][work][G][kPartStrideTL]
   float* out;                  // [B][Hq][d]: when set, the last workgroup of each (sequence, slot) merges
   uint32_t* cnt;               // [B][n_slots] arrival counters for that merge (zero between calls)
   int64_t T;
@@ -57,6 +57,7 @@ struct SplitArgs {
   int32_t n_kv_heads;
   int32_t n_slots;             // grid.y
   int32_t split;               // tokens per work item
+  int32_t n_work;              // work items of the launch
   int32_t q_bf16;
   float qscale;                // sm_scale * log2(e)
   int32_t kv_of_slot[DWKV_MAX_PROBE_HEADS];
@@ -65,7 +66,7 @@ struct SplitArgs {
 
 // Split merge (and Eq. 3 for probed heads): grid = (Hq, B).
 struct MergeArgs {
-  const float* part;           // decode partials [work][Hkv][G][kPartStride]
+  const float* part;           // decode partials [work][Hkv][G][kPartStride] (token-lane: [Hkv][work][G][kPartStrideTL])
   const float* part_ref;       // probe partials [work][n_probe][G][kPartStride] or null
   float* out;                  // [B][Hq][d]
   float* err;                  // [B][n_probe*G] or null
@@ -80,6 +81,7 @@ struct MergeArgs {
   int32_t probe_slot_of_kv[DWKV_MAX_PROBE_HEADS];   // -1 when the KV head is not probed
   WorkTable wt;
   int32_t tl;                  // main partials in the token-lane layout
+  int32_t n_work;              // work items (token-lane layout)
   int32_t rb;
   const uint16_t* basis;       // basis of window m, sequence 0: + (b*M*Hkv + h)*2*RB*d (tl only)
   int64_t basis_b_stride;
