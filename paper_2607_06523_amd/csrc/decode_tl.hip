@@ -341,7 +341,7 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   // lanes resolves it after the scores)
   uint32_t rank = 0, e0 = 0, n = 0, cd0 = 0, cd1 = 0;
   Window wk{};
-  f4 qv0[4];
+  f4 qv0[8];
   if constexpr (RESID) {
     rank = min(mc.ob - mc.oa, (uint32_t)kMaxRank);
     if (mc.ob < mc.oa) rank = 0;
@@ -352,7 +352,8 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
     cd0 = nb >= 32u ? wk.cd[0] : wk.cd[0] & ((1u << nb) - 1u);
     cd1 = nb <= 32u ? 0u : (nb >= 64u ? wk.cd[1] : wk.cd[1] & ((1u << (nb - 32u)) - 1u));
 #pragma unroll
-    for (int u = 0; u < 4; ++u) qv0[u] = *reinterpret_cast<const f4*>(&sm.qs[(wk.ch[0] >> (8 * u)) & (D - 1)][0]);
+    for (int u = 0; u < 8; ++u)
+      qv0[u] = *reinterpret_cast<const f4*>(&sm.qs[(wk.ch[u >> 2] >> (8 * (u & 3))) & (D - 1)][0]);
     e0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)mc.oa);
     const uint32_t e1 = (uint32_t)__builtin_amdgcn_readlane((int)mc.ob, 63);
     n = e1 > e0 ? min(e1 - e0, (uint32_t)kEmap) : 0u;
@@ -394,22 +395,21 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   int carry = 0;
   if constexpr (RESID) {
     float rk[HG] = {0.f, 0.f, 0.f, 0.f};
+    // entries 0..7 from the lookups of step 1b, 8..15 in one more round
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 8; ++u) {
       const float code = code_at(cd0, u);
 #pragma unroll
       for (int i = 0; i < G; ++i) rk[i] += code * qv0[u][i];
     }
+    if (__ballot(rank > 8u) != 0) {
+      f4 qv[8];
 #pragma unroll
-    for (int qd = 1; qd < kMaxRank / 4; ++qd) {
-      if (__ballot(rank > 4u * qd) == 0) break;
-      f4 qv[4];
+      for (int u = 0; u < 8; ++u)
+        qv[u] = *reinterpret_cast<const f4*>(&sm.qs[(wk.ch[2 + (u >> 2)] >> (8 * (u & 3))) & (D - 1)][0]);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) qv[u] = *reinterpret_cast<const f4*>(&sm.qs[(wk.ch[qd] >> (8 * u)) & (D - 1)][0]);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int k = 4 * qd + u;
-        const float code = code_at(k < 8 ? cd0 : cd1, k & 7);
+      for (int u = 0; u < 8; ++u) {
+        const float code = code_at(cd1, u);
 #pragma unroll
         for (int i = 0; i < G; ++i) rk[i] += code * qv[u][i];
       }
