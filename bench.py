@@ -171,28 +171,20 @@ def main():
             graph.replay()
         torch.cuda.synchronize()
 
-    # timed region: K steps.  The last step carries events on the kernels'
-    # stream.  When one decode is one launch (the split kernel merges itself),
-    # a pair around the step times that kernel: span / L.  Otherwise the step
-    # runs every layer as its two halves, first the split-K pass of all L
-    # layers back to back (each layer into its own workspace), then the L
-    # merges, with one event pair around each run.
-    fused = dc.decode_launches == 1
+    # timed region: K steps.  The last step runs every layer as its two
+    # halves: first the split-K pass of all L layers back to back (each layer
+    # into its own workspace), then the L merges, with one event pair around
+    # each run on the kernels' stream.  That times the split-K kernel (the
+    # dominant one) on its own without an event between every pair of launches.
     ev_step = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     ev_calls = [torch.cuda.Event(enable_timing=True) for _ in range(3)] if graph is None else None
-    ws_layer = [dc.new_workspace() for _ in range(L)] \
-        if graph is None and not fused else None
+    ws_layer = [dc.new_workspace() for _ in range(L)] if graph is None else None
     torch.cuda.synchronize()
     ev_step[0].record(stream)
     wall0 = time.perf_counter()
     for k in range(args.steps):
         if graph is not None:
             graph.replay()
-        elif k == args.steps - 1 and fused:
-            ev_calls[0].record(stream)
-            step()
-            ev_calls[1].record(stream)
-            ev_calls[2].record(stream)
         elif k == args.steps - 1:
             ev_calls[0].record(stream)
             for l in range(L):
@@ -211,7 +203,7 @@ def main():
     split_ms = merge_ms = None
     if ev_calls is not None:
         split_ms = ev_calls[0].elapsed_time(ev_calls[1]) / L
-        merge_ms = None if fused else ev_calls[1].elapsed_time(ev_calls[2]) / L
+        merge_ms = ev_calls[1].elapsed_time(ev_calls[2]) / L
 
     bytes_layer = algorithmic_bytes_per_layer(host)
     bytes_step = float(sum(bytes_layer))
@@ -244,8 +236,7 @@ def main():
                    "graph": bool(graph is not None)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "kernel": ("tl_kernel (token-lane split-K pass, merge in its last workgroups)" if fused
-                                else "split-K partials pass")},
+                     "kernel": "split-K partials pass (tl_kernel at this workload)"},
         "step_gbps": round(step_gbps, 1),
         "bytes_per_step": int(bytes_step),
         "bytes_per_layer_call": int(np.mean(bytes_layer)),

@@ -119,9 +119,9 @@ int32_t dwkv_split_tokens(const dwkv_dims* dims);
  * probe may be NULL. */
 size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe);
 
-/* Kernel launches one dwkv_decode call enqueues for these dims (1 when the
- * split kernel merges itself, 2 with a separate merge, 3 with a probe pass),
- * or -1 when the dims or probe are invalid.  probe may be NULL. */
+/* Kernel launches one dwkv_decode call enqueues for these dims (2: the
+ * split-K pass and the merge; 3 with a probe pass), or -1 when the dims or
+ * probe are invalid.  probe may be NULL. */
 int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe);
 
 /* Per-layer decode attention over the factorized cache (Eq. 1 folded into the
@@ -134,17 +134,11 @@ int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe);
  *   sm_scale: softmax scale; <= 0 selects 1/sqrt(d)
  *   out:      fp32 [B][Hq][d], written
  *   probe:    NULL, or Eq. 3 error for the listed KV heads (see dwkv_probe)
- *   workspace:>= dwkv_workspace_bytes(dims, probe) bytes of device memory,
- *             ZERO-FILLED before its first use: its last bytes hold one
- *             arrival counter per (sequence, KV head), which every call
- *             leaves at zero again (a zero-filled allocation stays valid for
- *             any later dims).  The rest is clobbered.  Calls sharing a
- *             workspace must be ordered (same stream).  A workspace whose
- *             counters are not zero gives wrong outputs, never a fault.
- * Launches one split-K kernel whose last workgroup per (sequence, KV head)
- * merges, when the token-lane kernel serves the shape, there is no probe and
- * no sequence is empty; otherwise the split-K kernel(s) (two with a probe)
- * and one merge kernel.  Returns DWKV_OK once enqueued. */
+ *   workspace:>= dwkv_workspace_bytes(dims, probe) bytes of device memory;
+ *             contents need no initialisation and are clobbered; calls
+ *             sharing it must be ordered (same stream).
+ * Launches the split-K kernel(s) (two with a probe) and one merge kernel.
+ * Returns DWKV_OK once enqueued. */
 dwkv_status dwkv_decode(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
                         const void* q, int32_t q_type, float sm_scale, float* out,
                         const dwkv_probe* probe, void* workspace, size_t ws_bytes,
@@ -156,7 +150,7 @@ dwkv_status dwkv_decode(const dwkv_dims* dims, const dwkv_cache* cache, int32_t 
  * dwkv_decode_merge merges them into `out` (and, with a probe, writes err /
  * out_ref).  Both calls take the same dims, cache, layer and probe pointer;
  * the merge reads the cache's bases (it may finish the value product).
- * The outputs equal dwkv_decode's bit for bit; the counters are not used. */
+ * The outputs equal dwkv_decode's bit for bit. */
 dwkv_status dwkv_decode_partials(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
                                  const void* q, int32_t q_type, float sm_scale,
                                  const dwkv_probe* probe, void* workspace, size_t ws_bytes,

@@ -104,7 +104,7 @@ class DeviceCache:
 
     @property
     def decode_launches(self) -> int:
-        """Kernel launches of one decode call without a probe (1: the split kernel merges itself)."""
+        """Kernel launches of one decode call without a probe (the split-K pass and the merge)."""
         return int(self.lib.dwkv_decode_launches(C.byref(self.dims), None))
 
     def _probe_struct(self, probe: ProbeRef | None, err, out_ref):
@@ -131,7 +131,7 @@ class DeviceCache:
         return int(n)
 
     def new_workspace(self, probe: ProbeRef | None = None):
-        """A zero-filled decode workspace (its arrival counters must start at zero)."""
+        """A fresh decode workspace (zero-filled; the library needs no initial contents)."""
         return self.torch.zeros(self.workspace_bytes(probe), dtype=self.torch.uint8, device=self.device)
 
     def workspace(self, probe: ProbeRef | None = None):

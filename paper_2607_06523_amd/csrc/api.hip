@@ -104,10 +104,9 @@ dwkv_status check_probe(const dwkv_dims* d, const dwkv_probe* p) {
   return DWKV_OK;
 }
 
-// Workspace: the partials of the decode pass, those of the probe pass, then
-// one arrival counter per (sequence, KV head) for the fused merge.
+// Workspace: the partials of the decode pass, then those of the probe pass.
 struct WsLayout {
-  size_t main_bytes, ref_bytes, cnt_off, total;
+  size_t main_bytes, ref_bytes, total;
 };
 
 WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
@@ -118,8 +117,8 @@ WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
   WsLayout w;
   w.main_bytes = align_up((size_t)nw * d->n_kv_heads * g * stride * sizeof(float), 256);
   w.ref_bytes = p ? align_up((size_t)nw * p->n_heads * g * kPartStride * sizeof(float), 256) : 0;
-  w.cnt_off = w.main_bytes + w.ref_bytes;
-  w.total = w.cnt_off + align_up((size_t)d->batch * d->n_kv_heads * sizeof(uint32_t), 256);
+  w.total = w.main_bytes + w.ref_bytes;
+  if (w.total == 0) w.total = 256;
   return w;
 }
 
@@ -136,16 +135,6 @@ WorkTable work_table(const dwkv_dims* d, int split) {
     t.work[b + 1] = t.work[b] + (int32_t)((len + split - 1) / split);
   }
   return t;
-}
-
-// The split kernel merges in its last workgroup per (sequence, KV head) when
-// it is the token-lane kernel, there is no probe pass and every sequence has
-// a token (an empty one has no workgroup to write its zero output).
-bool fused_merge(const dwkv_dims* d, const dwkv_probe* p) {
-  if (p || !uses_token_lane(d)) return false;
-  for (int b = 0; b < d->batch; ++b)
-    if (d->cu_seqlens_host[b + 1] == d->cu_seqlens_host[b]) return false;
-  return true;
 }
 
 }  // namespace
@@ -180,7 +169,7 @@ size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe) {
 
 int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe) {
   if (check_dims(dims) != DWKV_OK || check_probe(dims, probe) != DWKV_OK) return -1;
-  return fused_merge(dims, probe) ? 1 : probe ? 3 : 2;
+  return probe ? 3 : 2;
 }
 
 }  // extern "C"
@@ -199,10 +188,9 @@ dwkv_status check_decode_common(const dwkv_dims* d, const dwkv_probe* probe, voi
 }
 
 // Split-K pass(es): partial (o, m, l) per (work item, head slot, group member).
-// With `out` set (only when fused_merge holds) the split kernel also merges.
 dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
                            int32_t q_type, float sm_scale, const dwkv_probe* probe, void* workspace,
-                           float* out, hipStream_t s) {
+                           hipStream_t s) {
   if (!c || !q) return DWKV_E_NULL;
   if (!c->basis || !c->coef_k || !c->coef_v || !c->res_off || !c->res_idx || !c->res_val ||
       !c->res_scale)
@@ -244,8 +232,6 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   a.q = static_cast<const uint16_t*>(q);
   a.cu = d->cu_seqlens;
   a.part = reinterpret_cast<float*>(ws);
-  a.out = out;
-  a.cnt = reinterpret_cast<uint32_t*>(ws + wl.cnt_off);
   a.T = T;
   a.res_stride = d->res_stride;
   a.batch = d->batch;
@@ -267,7 +253,6 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
     r.coef_k = static_cast<const uint16_t*>(probe->k_ref);
     r.coef_v = static_cast<const uint16_t*>(probe->v_ref);
     r.part = reinterpret_cast<float*>(ws + wl.main_bytes);
-    r.out = nullptr;
     r.n_slots = probe->n_heads;
     for (int i = 0; i < probe->n_heads; ++i) r.kv_of_slot[i] = probe->kv_heads_host[i];
     if (launch_split(kHeadDim, G, false, true, r, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
@@ -344,8 +329,7 @@ dwkv_status dwkv_decode(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   if (!out) return DWKV_E_NULL;
   if (!aligned16(out)) return DWKV_E_ALIGN;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (fused_merge(d, probe)) return partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, out, s);
-  if ((st = partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, nullptr, s)) != DWKV_OK) return st;
+  if ((st = partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, s)) != DWKV_OK) return st;
   return merge_phase(d, c, layer, out, probe, workspace, s);
 }
 
@@ -354,7 +338,7 @@ dwkv_status dwkv_decode_partials(const dwkv_dims* d, const dwkv_cache* c, int32_
                                  size_t ws_bytes, void* stream) {
   dwkv_status st = check_decode_common(d, probe, workspace, ws_bytes);
   if (st != DWKV_OK) return st;
-  return partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace, nullptr,
+  return partials_phase(d, c, layer, q, q_type, sm_scale, probe, workspace,
                         reinterpret_cast<hipStream_t>(stream));
 }
 

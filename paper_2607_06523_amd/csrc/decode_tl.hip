@@ -31,10 +31,9 @@
 //    channel from the 16-token value blocks.  The accumulator holds, in lane c,
 //    the basis-space value of channel c for the 4 heads.
 //  * the epilogue combines the waves and writes the partial in basis space
-//    (a~, the residual channels, m, l).  The last workgroup of a (sequence,
-//    KV head) to finish merges its partials in a fixed order and applies B^V;
-//    the partials travel through device-coherent stores and loads and one
-//    arrival counter, so no cache write-back is needed.
+//    (a~, the residual channels, m, l).  A second, wide launch merges them in
+//    a fixed order and applies B^V: one workgroup per (KV head, query head,
+//    16 output channels), so that every CU reads a small share.
 #include <utility>
 
 #include "entry.h"
@@ -69,17 +68,6 @@ struct TCfg {
   static_assert(RB % 16 == 0 && RB >= 16 && RB <= 64, "basis rank");
 };
 
-// LDS of the merge of a (sequence, KV head)'s partials.
-template <int RB>
-struct TMSmem {
-  f4 red[kTThreads];                    // per lane: its merged column quad
-  float wm[kTW], wl[kTW];               // per wave: running maximum and sum
-  alignas(16) float rfin[HG][D];        // merged residual channels / l
-  float abar[HG][RB];                   // merged a~ / l
-  float pr[kTW][HG][D];                 // projection sums of each wave's basis rows
-  int last;
-};
-
 template <int RB, bool RESID>
 struct alignas(16) TSmem {
   alignas(16) float qs[D][HG];          // q * sm_scale * log2(e), heads past G zero
@@ -96,7 +84,6 @@ struct alignas(16) TSmem {
   long long racc[kTW][RESID ? HG : 1][RESID ? D : 1];
   alignas(4) uint8_t emap[kTW][RESID ? kEmap : 4];  // token lane + 1 at each token's first entry
   alignas(16) float pw[kTW][RESID ? TT : 1][HG];  // p * value scale per token lane
-  TMSmem<RB> mg;
 };
 
 template <int RB>
@@ -552,120 +539,114 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
 
 constexpr int kSc1 = 16;                // buffer cache policy: device-coherent access
 
-// Merges the partials of sequence b, slot `slot` (work items base .. base+ns-1)
-// in a fixed order and writes o = r + a~ B^V for the slot's G heads.  A wave
-// of head g merges every NWH-th partial, one column quad per lane (the row's
-// m and l come in one lane each and are broadcast); the waves of a head then
-// combine.  The projection gives each wave RB/8 rows of B^V for all G heads.
-// The partials are read with device-coherent loads: other workgroups,
-// possibly on other XCDs, wrote them in this launch.
+// Wide merge: one workgroup per (slot, head, 16 output channels).  Each
+// reads, from every partial of its (sequence, slot, head), its 16 residual
+// channels and all of a~ (plus m, l), merges them in a fixed order and writes
+// o = r + a~ B^V for its channels.  Spreading one slot's merge over G * d/16
+// workgroups keeps every CU's share of the partials small: the loads of one
+// CU, not the bytes, bound a merge that a single workgroup does.
+constexpr int kWmThreads = 256;
+constexpr int kWmCh = 16;                       // output channels per workgroup
+
 template <int RB, int G>
-__device__ __forceinline__ void tl_merge(const SplitArgs& a, TMSmem<RB>& sm, int b, int slot, int base,
-                                         int ns) {
-  constexpr int TPH = kTThreads / G;    // threads per head
-  constexpr int NWH = TPH / 64;         // waves per head
-  constexpr int Q = (D + RB) / 4;       // column quads of a row: r, then a~
-  constexpr int KB = RB / kTW;          // basis rows per wave in the projection
-  constexpr int RPL = 32 / NWH;         // partials per lane per round: 32 per head
-  static_assert(Q <= 64 && RB % kTW == 0 && RPL <= 64, "merge layout");
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar addressing
-  const int g = wv / NWH, wh = wv % NWH, w0 = wv - wh;
+__global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const SplitArgs a) {
+  constexpr int QW = kWmCh / 4 + RB / 4;        // quads per row: the r chunk, then a~
+  constexpr int RG = kWmThreads / QW;           // row groups
+  constexpr int RPT = 2;                        // partials per thread per round (32 per round at r_b 48)
+  constexpr int KG = kWmThreads / kWmCh;        // k groups of the projection
+  constexpr int KPG = (RB + KG - 1) / KG;       // basis rows per k group
+  constexpr int NCH = D / kWmCh;
+  __shared__ f4 red[RG][QW];
+  __shared__ float wm[RG], wl[RG];
+  __shared__ alignas(16) float fin[4 * QW];
+  __shared__ float red2[KG][kWmCh];
+  const int tid = threadIdx.x;
+  const int ch = blockIdx.x % NCH, g = (blockIdx.x / NCH) % G, slot = blockIdx.x / (NCH * G), b = blockIdx.y;
+  const int c0 = ch * kWmCh;
   const int kvh = a.kv_of_slot[slot];
-  // B^V rows [wv KB, wv KB + KB), channels 2 lane and 2 lane + 1
-  const uint16_t* bv = a.basis + (int64_t)b * a.basis_b_stride + ((int64_t)kvh * 2 + 1) * RB * D;
-  uint32_t bvr[KB];
+  int base, ns;
+  seq_work(a.wt, a.cu, a.split, b, base, ns);
+  // B^V rows [kg KPG, kg KPG + KPG) of channel c0 + tid % 16
+  const int pc = tid % kWmCh, kg = tid / kWmCh;
+  const uint16_t* bv = a.basis + (int64_t)b * a.basis_b_stride + ((int64_t)kvh * 2 + 1) * RB * D + c0 + pc;
+  uint16_t bvr[KPG];
 #pragma unroll
-  for (int k = 0; k < KB; ++k) bvr[k] = *reinterpret_cast<const uint32_t*>(bv + (wv * KB + k) * D + 2 * lane);
-  // partial s of head g at float offset s * rs from p0 (a slot's partials
-  // are contiguous)
+  for (int k = 0; k < KPG; ++k) bvr[k] = bv[(int64_t)min(kg * KPG + k, RB - 1) * D];
+  // this thread's quad of every RG-th partial
+  const int qi = tid % QW, rg = min(tid / QW, RG - 1);
+  const bool active = tid < RG * QW;
   const int64_t rs = (int64_t)G * kPartStrideTL;
   const float* p0 = a.part + (((int64_t)slot * a.n_work + base) * G + g) * kPartStrideTL;
   const rsrc_t pr = make_rsrc(p0, (uint32_t)(max(ns, 1) * rs * 4));
-  const int q = min(lane, Q - 1);       // lanes past Q repeat the last quad, unused
+  const uint32_t qoff = qi < kWmCh / 4 ? (uint32_t)(c0 + 4 * qi) : (uint32_t)(D + 4 * (qi - kWmCh / 4));
   f4 acc = f4{0.f, 0.f, 0.f, 0.f};
   float mstar = -INFINITY, lsum = 0.f;
-  for (int s0 = 0; s0 < ns; s0 += NWH * RPL) {
-    u4v xv[RPL];
+  for (int s0 = 0; s0 < ns; s0 += RG * RPT) {
+    u4v xv[RPT];
+    u2v ml[RPT];
 #pragma unroll
-    for (int i = 0; i < RPL; ++i) {
-      const uint32_t s = (uint32_t)min(s0 + wh + NWH * i, ns - 1);
-      xv[i] = __builtin_amdgcn_raw_buffer_load_b128(pr, (uint32_t)((s * rs + 4 * q) * 4), 0, kSc1);
+    for (int i = 0; i < RPT; ++i) {
+      const uint32_t s = (uint32_t)min(s0 + rg + RG * i, ns - 1);
+      xv[i] = __builtin_amdgcn_raw_buffer_load_b128(pr, (uint32_t)((s * rs + qoff) * 4), 0, kSc1);
+      ml[i] = __builtin_amdgcn_raw_buffer_load_b64(pr, (uint32_t)((s * rs + kPartTLM) * 4), 0, kSc1);
     }
-    // lane i < RPL: (m, l) of the round's i-th partial
-    const uint32_t sl = (uint32_t)min(s0 + wh + NWH * min(lane, RPL - 1), ns - 1);
-    const u2v ml = __builtin_amdgcn_raw_buffer_load_b64(pr, (uint32_t)((sl * rs + kPartTLM) * 4), 0, kSc1);
-    __builtin_amdgcn_sched_barrier(0);  // every request of the round in flight before the first wait
-    float mv[RPL];
+    float mv[RPT];
     float mr = mstar;
 #pragma unroll
-    for (int i = 0; i < RPL; ++i) {
-      mv[i] = s0 + wh + NWH * i < ns ? __int_as_float(__builtin_amdgcn_readlane((int)ml.x, i)) : -INFINITY;
+    for (int i = 0; i < RPT; ++i) {
+      mv[i] = s0 + rg + RG * i < ns ? __uint_as_float(ml[i].x) : -INFINITY;
       mr = fmaxf(mr, mv[i]);
     }
     const float resc = mstar == -INFINITY ? 0.f : exp2f(mstar - mr);
     acc *= resc;
     lsum *= resc;
 #pragma unroll
-    for (int i = 0; i < RPL; ++i) {
+    for (int i = 0; i < RPT; ++i) {
       const float w = mv[i] == -INFINITY ? 0.f : exp2f(mv[i] - mr);
       acc += w * __builtin_bit_cast(f4, xv[i]);
-      lsum += w * __int_as_float(__builtin_amdgcn_readlane((int)ml.y, i));
+      lsum += w * __uint_as_float(ml[i].y);
     }
     mstar = mr;
   }
-  sm.red[tid] = acc;
-  if (lane == 0) {
-    sm.wm[wv] = mstar;
-    sm.wl[wv] = lsum;
+  if (active) {
+    red[rg][qi] = acc;
+    if (qi == 0) {
+      wm[rg] = mstar;
+      wl[rg] = lsum;
+    }
   }
   __syncthreads();
-  if (wh == 0 && lane < Q) {
+  if (tid < QW) {
     float mx = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < NWH; ++j) mx = fmaxf(mx, sm.wm[w0 + j]);
+    for (int j = 0; j < RG; ++j) mx = fmaxf(mx, wm[j]);
     f4 o = f4{0.f, 0.f, 0.f, 0.f};
     float l = 0.f;
 #pragma unroll
-    for (int j = 0; j < NWH; ++j) {
-      const float e = sm.wm[w0 + j] == -INFINITY ? 0.f : exp2f(sm.wm[w0 + j] - mx);
-      o += e * sm.red[(w0 + j) * 64 + lane];
-      l += e * sm.wl[w0 + j];
+    for (int j = 0; j < RG; ++j) {
+      const float e = wm[j] == -INFINITY ? 0.f : exp2f(wm[j] - mx);
+      o += e * red[j][tid];
+      l += e * wl[j];
     }
     o *= l > 0.f ? 1.0f / l : 0.f;
-    if (lane < D / 4) *reinterpret_cast<f4*>(&sm.rfin[g][4 * lane]) = o;
-    else *reinterpret_cast<f4*>(&sm.abar[g][4 * (lane - D / 4)]) = o;
+    *reinterpret_cast<f4*>(&fin[4 * tid]) = o;
   }
   __syncthreads();
+  {
+    // fin: [r chunk (16) | a~ (RB)]
+    float o = 0.f;
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    float o0 = 0.f, o1 = 0.f;
-#pragma unroll
-    for (int k = 0; k < KB; ++k) {
-      const float ak = sm.abar[h][wv * KB + k];
-      o0 += ak * half_bits_to_float((uint16_t)(bvr[k] & 0xFFFF));
-      o1 += ak * half_bits_to_float((uint16_t)(bvr[k] >> 16));
-    }
-    sm.pr[wv][h][2 * lane] = o0;
-    sm.pr[wv][h][2 * lane + 1] = o1;
+    for (int k = 0; k < KPG; ++k)
+      if (kg * KPG + k < RB) o += fin[kWmCh + kg * KPG + k] * half_bits_to_float(bvr[k]);
+    red2[kg][pc] = o;
   }
   __syncthreads();
-  if (tid < G * D) {
-    const int h = tid / D, c = tid % D;
-    float o = sm.rfin[h][c];
+  if (tid < kWmCh) {
+    float o = fin[tid];
 #pragma unroll
-    for (int w = 0; w < kTW; ++w) o += sm.pr[w][h][c];
-    a.out[((int64_t)b * a.n_q_heads + kvh * G + h) * D + c] = o;
+    for (int j = 0; j < KG; ++j) o += red2[j][tid];
+    a.out[((int64_t)b * a.n_q_heads + kvh * G + g) * D + c0 + tid] = o;
   }
-}
-
-template <int RB, int G>
-__global__ __launch_bounds__(kTThreads) void tl_merge_kernel(const SplitArgs a) {
-  __shared__ TMSmem<RB> sm;
-  const int slot = blockIdx.x, b = blockIdx.y;
-  int base, ns;
-  seq_work(a.wt, a.cu, a.split, b, base, ns);
-  tl_merge<RB, G>(a, sm, b, slot, base, ns);
 }
 
 template <int RB, int G, bool RESID>
@@ -932,23 +913,6 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
       __hip_atomic_store(dst + kPartTLM + 1, l, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
-  if (a.out == nullptr) return;         // a separate merge launch finishes
-  // Fused merge: once this workgroup's partial stores are complete (they are
-  // device-coherent, so completion makes them visible to every XCD), count
-  // its arrival; the last arrival of the (sequence, slot) merges.
-  int base, ns;
-  seq_work(a.wt, a.cu, a.split, b, base, ns);
-  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-  __syncthreads();
-  uint32_t* cnt = a.cnt + (int64_t)b * a.n_slots + slot;
-  if (tid == 0) {
-    const uint32_t seen = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    sm.mg.last = seen == (uint32_t)(ns - 1);
-    if (seen == (uint32_t)(ns - 1)) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __syncthreads();
-  if (!sm.mg.last) return;
-  tl_merge<RB, G>(a, sm.mg, b, slot, base, ns);
 }
 
 template <int RB, int G, bool R>
@@ -982,11 +946,11 @@ hipError_t launch_tl_rb(int rb, int g, const SplitArgs& a, int n_work, hipStream
 
 template <int RB>
 hipError_t launch_merge_tl_rb(int g, const SplitArgs& a, hipStream_t s) {
-  const dim3 grid(a.n_slots, a.batch);
+  const dim3 grid(a.n_slots * g * (D / kWmCh), a.batch);
   switch (g) {
-    case 1: hipLaunchKernelGGL((tl_merge_kernel<RB, 1>), grid, dim3(kTThreads), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((tl_merge_kernel<RB, 2>), grid, dim3(kTThreads), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((tl_merge_kernel<RB, 4>), grid, dim3(kTThreads), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 1>), grid, dim3(kWmThreads), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 2>), grid, dim3(kWmThreads), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 4>), grid, dim3(kWmThreads), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -48,8 +48,7 @@ struct SplitArgs {
   const uint16_t* q;           // [B][Hq][d] fp16 or bf16 bits
   const int32_t* cu;           // [B+1] device
   float* part;                 // [work][n_slots][G][kPartStride]; token-lane: [n_slots][work][G][kPartStrideTL]
-  float* out;                  // [B][Hq][d]: when set, the last workgroup of each (sequence, slot) merges
-  uint32_t* cnt;               // [B][n_slots] arrival counters for that merge (zero between calls)
+  float* out;                  // [B][Hq][d], written by the token-lane merge launch
   int64_t T;
   int64_t res_stride;
   int32_t batch;
@@ -166,7 +165,8 @@ hipError_t launch_split(int rb, int g, bool resid, bool ident, const SplitArgs& 
 // ranks 16..64, at most 16 residual entries per token); same partials.
 bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t res_stride);
 hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s);
-// Token-lane merge on its own: grid = (n_slots, B); reads a.part, writes a.out.
+// Token-lane merge: reads a.part, writes a.out (one workgroup per slot, head
+// and 16 output channels).
 hipError_t launch_merge_tl(int rb, int g, const SplitArgs& a, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, int n_mh, hipStream_t s);
