@@ -42,6 +42,9 @@ SMALL = [
     ("rb64-g4-entry-heavy", 64, 4, (0, 16), (0.1, 0.9), [1500, 64], 256, "bf16"),
     # token-lane kernel, more sequences than the kernel-argument work table holds
     ("rb32-g4-20-seqs", 32, 4, (0, 8), (0.7, 0.3), [37 + 23 * i for i in range(20)], 64, "bf16"),
+    # token-lane merge over more chunks than one load round covers (79 and 47 partials)
+    ("rb48-g4-many-chunks", 48, 4, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), [5000, 37], 64, "bf16"),
+    ("rb64-g2-many-chunks", 64, 2, (0, 8, 16), (0.8, 0.15, 0.05), [3000], 64, "f16"),
 ]
 
 
