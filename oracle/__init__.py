@@ -8,14 +8,18 @@ inputs.
 
 * ``factorized``: Eq. 1 reconstruction, softmax decode attention, Eq. 3 probe
   error and the dense residual map.
-* ``router``: Eq. 2 rank routing (multi-level reading) and residual offsets.
+* ``router``: Eq. 2 rank routing (multi-level reading) and residual offsets,
+  for the whole packed axis or a token range continuing an existing table.
+* ``compress``: the storage half of Eq. 1 for new tokens: projection onto the
+  window basis, routed residual channels, int4 codes, gate-folded scale.
 
 Every function is pinned by the CPU tests (brute force in exact arithmetic,
 closed forms, reductions to library attention, invariants); none is marked
 "parity unpinned".
 """
-from . import factorized, router
+from . import factorized, router, compress
 from .factorized import (attention, decode, probe, probe_error, reconstruct,
                          residual_map, int4_from_nibble, entry_codes, q_to_f64,
                          default_scale)
-from .router import route, router_score, level_index, theta_from_tau
+from .router import route, route_range, router_score, level_index, theta_from_tau
+from .compress import compress_vectors

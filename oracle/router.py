@@ -70,3 +70,24 @@ def theta_from_tau(tau) -> np.ndarray:
     rounded to float32)."""
     tau = np.asarray(tau, dtype=np.float64)
     return np.log(tau / (1.0 - tau)).astype(np.float32)
+
+
+def route_range(phi: np.ndarray, u: np.ndarray, theta: np.ndarray, levels, t0: int, t1: int,
+                codes: np.ndarray, off: np.ndarray):
+    """Route packed tokens [t0, t1) in place, continuing an existing table:
+    codes[m][h][t] for those tokens and off[m][h][t+1] = off[m][h][t] + rho,
+    starting from the off[m][h][t0] already there (0 when t0 == 0).  The
+    append of a decode token is the range [T-1, T)."""
+    M, Hk = codes.shape[0], codes.shape[1]
+    lev = np.asarray(levels, dtype=np.int64)
+    if t0 == 0:
+        off[:, :, 0] = 0
+    for m in range(M):
+        z = router_score(phi[m, :, t0:t1], u[m])
+        k = level_index(z, theta[m])
+        codes[m, :, t0:t1] = k
+        run = off[m, :, t0:t0 + 1].astype(np.int64) + np.cumsum(lev[k], axis=1)
+        if run.size and run.max() > np.iinfo(np.uint32).max:
+            raise OverflowError("residual offsets exceed 32 bits")
+        off[m, :, t0 + 1:t1 + 1] = run
+    return codes, off

@@ -16,7 +16,13 @@ says what disagreed.  The pins are:
 * the router score in exact rational arithmetic rounded per operation, Eq. 2 in
   float64 for two levels, infinite thresholds, monotonicity, and offsets by a
   running loop;
-* the int4 nibble table in ``tests/golden/int4_nibbles.txt``.
+* the int4 nibble table in ``tests/golden/int4_nibbles.txt``;
+* the append/compress step: signed-permutation bases (exact projection and
+  residual), the round-half-even tie table in ``tests/golden/int4_rne_ties.txt``,
+  the float32 decision path in exact rational arithmetic, enumeration of the
+  kept channels, float64 error bounds with an orthonormal basis, the rebuilt
+  Eq. 1 vectors after writing into the layout, and range routing against a
+  running loop.
 """
 from __future__ import annotations
 
@@ -619,8 +625,320 @@ def pin_query_formats(o):
     return None
 
 
+
+# ------------------------------------------------------------ append/compress
+def fp16_round(x: Fraction) -> Fraction:
+    """Round an exact rational to the nearest float16, ties to even."""
+    if x == 0:
+        return Fraction(0)
+    sign = -1 if x < 0 else 1
+    a = abs(x)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1
+    e = max(e, -14)
+    ulp = Fraction(2) ** (e - 10)
+    n = a / ulp
+    fl = n.numerator // n.denominator
+    rem = n - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    return sign * fl * ulp
+
+
+def _expected_entries(r, rho, S):
+    """Kept channels by the pairwise definition (every kept channel beats every
+    dropped one: larger |r|, or equal |r| and lower channel), codes rounded
+    half to even in exact arithmetic from the float32 quotient, storage order
+    by descending |code| then channel.  r, S exact rationals."""
+    d = len(r)
+    beats = lambda a, b: abs(r[a]) > abs(r[b]) or (abs(r[a]) == abs(r[b]) and a < b)
+    kept = [c for c in range(d) if sum(1 for c2 in range(d) if beats(c2, c)) < rho]
+    assert len(kept) == rho
+    codes = {}
+    for c in kept:
+        q = Fraction(0) if S == 0 else fp32_round(r[c] / S)
+        codes[c] = max(-7, min(7, round(q)))           # Fraction rounds half to even
+    order = sorted(kept, key=lambda c: (-abs(codes[c]), c))
+    return [(c, codes[c]) for c in order]
+
+
+def _f16(vals):
+    return np.asarray(vals, dtype=np.float64).astype(np.float16)
+
+
+def pin_compress_closed_forms(o):
+    """Signed-permutation bases make the projection and residual exact:
+    A_i = s_i x_{pi(i)}, r = x off the basis channels and 0 on them."""
+    C = o.compress
+    rng = np.random.default_rng(41)
+    d, r_b = 16, 4
+    for trial in range(6):
+        perm = rng.permutation(d)
+        sgn = rng.choice([-1.0, 1.0], size=r_b)
+        B = np.zeros((r_b, d))
+        for i in range(r_b):
+            B[i, perm[i]] = sgn[i]
+        B = _f16(B)
+        x = _f16(rng.uniform(0.05, 2.0, size=(3, d)) * rng.choice([-1, 1], size=(3, d)))
+        x[1, perm[r_b]] = x[1, perm[r_b + 1]]          # an exact |r| tie
+        x[2, perm[r_b + 2]] = -x[2, perm[r_b + 3]]
+        gates = np.array([1.0, 0.5, 0.3], np.float32)
+        for rho in (0, 2, 6, 12, d):
+            a16, entries, scales = C.compress_vectors(x, B, [rho] * 3, gates)
+            for k in range(3):
+                xs = [Fraction(float(v)) for v in x[k]]
+                exp_a = [sgn[i] * xs[perm[i]] for i in range(r_b)]
+                if [Fraction(float(v)) for v in a16[k]] != exp_a:
+                    return f"projection on a signed permutation basis is not A_i = s_i x_pi(i) (trial {trial})"
+                on_basis = set(int(perm[i]) for i in range(r_b))
+                rr = [Fraction(0) if c in on_basis else xs[c] for c in range(d)]
+                S = fp32_round(max(abs(v) for v in rr) / 7)
+                want = _expected_entries(rr, rho, S) if rho else []
+                got = [(int(c), int(q)) for c, q in zip(*entries[k])]
+                if got != want:
+                    return f"kept channels / codes / order wrong (trial {trial}, rho {rho}): {got} vs {want}"
+                exp_s = Fraction(0) if rho == 0 else fp16_round(fp32_round(Fraction(float(gates[k])) * S))
+                if Fraction(float(scales[k])) != exp_s:
+                    return f"stored scale is not fp16(g * max|r| / 7) (trial {trial}, rho {rho})"
+    return None
+
+
+def pin_compress_rne_table(o):
+    """Codes at and around rounding ties against tests/golden/int4_rne_ties.txt."""
+    C = o.compress
+    rows = []
+    with open(os.path.join(GOLDEN, "int4_rne_ties.txt")) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if line:
+                v, k = line.split()
+                rows.append((float(v), int(k)))
+    d, r_b = 32, 2
+    B = np.zeros((r_b, d))
+    B[0, 0] = B[1, 1] = 1.0                           # identity rows: r = x off channels 0, 1
+    S = 2.0 ** -6
+    x = np.zeros(d)
+    x[0], x[1] = 0.75, -1.25
+    for j, (v, _) in enumerate(rows):
+        x[2 + j] = v * S
+    a16, entries, scales = C.compress_vectors(_f16(x[None]), _f16(B), [d])
+    got = dict(zip((int(c) for c in entries[0][0]), (int(q) for q in entries[0][1])))
+    for j, (v, k) in enumerate(rows):
+        if got.get(2 + j) != k:
+            return f"r/S = {v} quantized to {got.get(2 + j)}, expected {k}"
+    if float(scales[0]) != S:
+        return "scale of the tie table is not max|r| / 7"
+    return None
+
+
+def _exact_project(x, B):
+    """A_i = fp16(left-to-right float32 sum of x_j B_ij), each op rounded."""
+    out = []
+    for i in range(B.shape[0]):
+        acc = fp32_round(Fraction(float(x[0])) * Fraction(float(B[i, 0])))
+        for j in range(1, len(x)):
+            acc = fp32_round(acc + fp32_round(Fraction(float(x[j])) * Fraction(float(B[i, j]))))
+        out.append(fp16_round(acc))
+    return out
+
+
+def _exact_residual(x, B, a):
+    out = []
+    for c in range(len(x)):
+        p = fp32_round(a[0] * Fraction(float(B[0, c])))
+        for i in range(1, B.shape[0]):
+            p = fp32_round(p + fp32_round(a[i] * Fraction(float(B[i, c]))))
+        out.append(fp32_round(Fraction(float(x[c])) - p))
+    return out
+
+
+def pin_compress_arithmetic(o):
+    """The float32 decision path in exact rational arithmetic, each operation
+    rounded, on inputs whose magnitudes span many binades (so a reordered or
+    fused sum rounds differently), and the kept set by enumeration on a tiny
+    case."""
+    from itertools import combinations
+    C = o.compress
+    rng = np.random.default_rng(43)
+    d, r_b = 24, 6
+    B = _f16(rng.standard_normal((r_b, d)) * 2.0 ** rng.integers(-6, 3, size=(r_b, d)))
+    x = _f16(rng.standard_normal((4, d)) * 2.0 ** rng.integers(-8, 6, size=(4, d)))
+    a16 = C.project(x, B)
+    r = C.residual(x, B, a16)
+    for k in range(4):
+        ea = _exact_project(x[k], B)
+        if [Fraction(float(v)) for v in a16[k]] != ea:
+            return f"projection is not the per-op rounded left-to-right float32 sum (vector {k})"
+        er = _exact_residual(x[k], B, ea)
+        if [Fraction(float(v)) for v in r[k]] != er:
+            return f"residual is not x - (left-to-right float32 basis term) (vector {k})"
+        for rho in (2, 8):
+            S = fp32_round(max(abs(v) for v in er) / 7)
+            want = _expected_entries(er, rho, S)
+            _, entries, _ = C.compress_vectors(x[k:k + 1], B, [rho])
+            if [(int(c), int(q)) for c, q in zip(*entries[0])] != want:
+                return f"entries of vector {k} at rho {rho} differ from the exact computation"
+    # cancelling pairs: small terms, then +1024 and -1024, then more small
+    # terms, so the float32 running sum absorbs a different set of the small
+    # terms in any other order (and a float64 or fused sum keeps them all)
+    x2 = _f16(rng.uniform(0.01, 0.02, size=(3, d)) * rng.choice([-1, 1], size=(3, d)))
+    B2 = _f16(rng.uniform(0.01, 0.02, size=(r_b, d)) * rng.choice([-1, 1], size=(r_b, d)))
+    x2[:, d // 3] = 32.0
+    x2[:, 2 * d // 3] = 32.0
+    B2[:, d // 3] = 32.0
+    B2[:, 2 * d // 3] = -32.0
+    B2[0, 2 * d // 3] = 32.0              # one row that does not cancel: large A_0
+    a2 = C.project(x2, B2)
+    r2 = C.residual(x2, B2, a2)
+    for k in range(3):
+        ea = _exact_project(x2[k], B2)
+        if [Fraction(float(v)) for v in a2[k]] != ea:
+            return f"projection of cancelling terms is not the left-to-right float32 sum (vector {k})"
+        if [Fraction(float(v)) for v in r2[k]] != _exact_residual(x2[k], B2, ea):
+            return f"residual of cancelling terms is not the left-to-right float32 sum (vector {k})"
+    # enumeration: on 6 channels with repeated magnitudes, the kept set is the
+    # lexicographically first subset (by channel) among those with the largest
+    # sorted |r| profile
+    rr = np.array([0.5, -0.25, 0.5, 0.125, -0.5, 0.25], np.float32)
+    for rho in range(0, 7):
+        best = None
+        for sub in combinations(range(6), rho):
+            prof = sorted((abs(float(rr[c])) for c in sub), reverse=True)
+            key = ([-v for v in prof], list(sub))
+            if best is None or key < best[0]:
+                best = (key, sub)
+        got = sorted(int(c) for c in C.select_channels(rr, rho))
+        if got != list(best[1]):
+            return f"top-{rho} channels {got}, enumeration gives {list(best[1])}"
+    return None
+
+
+def pin_compress_bounds(o):
+    """With a realistic orthonormal basis (d = 128): A matches the float64
+    projection to fp16 rounding, every kept channel is reproduced within
+    S/2 (+ rounding), every dropped channel is no larger than any kept one, and
+    the stored scale is max|r|/7 to fp16 accuracy."""
+    C = o.compress
+    rng = np.random.default_rng(47)
+    d, r_b = 128, 32
+    q, _ = np.linalg.qr(rng.standard_normal((d, r_b)))
+    B16 = _f16(q.T)
+    B = B16.astype(np.float64)
+    x16 = _f16(rng.standard_normal((40, d)))
+    x = x16.astype(np.float64)
+    rhos = rng.choice([0, 4, 8, 16, 32], size=40)
+    a16, entries, scales = C.compress_vectors(x16, B16, rhos)
+    a_exact = x @ B.T
+    tol_a = np.abs(a_exact) * 2.0 ** -11 + 1e-5
+    if np.any(np.abs(a16.astype(np.float64) - a_exact) > tol_a):
+        return "coefficients are not the projection x B^T"
+    r = x - a16.astype(np.float64) @ B
+    for k in range(40):
+        ch, codes = entries[k]
+        if len(ch) != rhos[k] or len(set(int(c) for c in ch)) != len(ch):
+            return f"vector {k}: {len(ch)} distinct channels kept, routed rank {rhos[k]}"
+        if rhos[k] == 0:
+            if float(scales[k]) != 0.0:
+                return "a rank-0 vector must store scale 0"
+            continue
+        S = np.abs(r[k]).max() / 7
+        if abs(float(scales[k]) - S) > S * 2.0 ** -10 + 1e-7:
+            return f"vector {k}: stored scale {float(scales[k])} vs max|r|/7 = {S}"
+        err = np.abs(r[k, ch] - S * codes)
+        if np.any(err > S * (0.5 + 1e-3) + 1e-6):
+            return f"vector {k}: a kept channel is off by more than half a step"
+        dropped = np.setdiff1d(np.arange(d), ch)
+        if dropped.size and np.abs(r[k, dropped]).max() > np.abs(r[k, ch]).min() + 1e-6:
+            return f"vector {k}: a dropped channel is larger than a kept one"
+        mags = np.abs(codes)
+        if np.any(np.diff(mags) > 0) or np.any((np.diff(mags) == 0) & (np.diff(ch) < 0)):
+            return f"vector {k}: entries not ordered by |code| then channel"
+    return None
+
+
+def pin_compress_into_cache(o):
+    """Writing the factors into the layout: the rebuilt Eq. 1 vectors of the
+    compressed tokens approximate the dense inputs within the quantization
+    bound, tokens outside the range are untouched, gates scale the residual."""
+    C = o.compress
+    c = small_cache(levels=(0, 2, 4, 16), probs=(0.25, 0.25, 0.25, 0.25), context=20,
+                    ragged=(13, 30), basis_rank=4)
+    layer, m = 3, 1
+    before = {(z, h, b): o.reconstruct(c, layer, z, h, b)
+              for z in range(2) for h in range(c.n_kv_heads) for b in range(c.batch)}
+    T, Hk, d = c.total_tokens, c.n_kv_heads, c.head_dim
+    t0, t1 = int(c.cu_seqlens[0]) + 5, int(c.cu_seqlens[1]) + 4      # spans both sequences
+    rng = np.random.default_rng(53)
+    xk = _f16(rng.standard_normal((t1 - t0, Hk, d)))
+    xv = _f16(rng.standard_normal((t1 - t0, Hk, d)))
+    gate = rng.uniform(0.2, 1.0, size=(2, Hk, t1 - t0)).astype(np.float32)
+    c2 = copy.deepcopy(c)
+    C.compress(c2, layer, xk, xv, t0, t1, gate)
+    lev = np.asarray(c.levels)
+    for z, X in ((0, xk), (1, xv)):
+        for h in range(Hk):
+            for b in range(c.batch):
+                s0, s1 = int(c.cu_seqlens[b]), int(c.cu_seqlens[b + 1])
+                got = o.reconstruct(c2, layer, z, h, b)
+                Bm = c.basis[b, m, h, z].astype(np.float64)
+                for t in range(s0, s1):
+                    if not (t0 <= t < t1):
+                        if not np.array_equal(got[t - s0], before[(z, h, b)][t - s0]):
+                            return "a token outside the compressed range changed"
+                        continue
+                    x = X[t - t0, h].astype(np.float64)
+                    a = (x @ Bm.T).astype(np.float16).astype(np.float64)
+                    rr = x - a @ Bm
+                    rho = lev[c.rank_code[m, h, t]]
+                    g = float(gate[z, h, t - t0])
+                    kept = np.argsort(-np.abs(rr), kind="stable")[:rho]
+                    want = a @ Bm
+                    want[kept] += g * rr[kept]
+                    S = np.abs(rr).max() / 7
+                    if np.abs(got[t - s0] - want).max() > g * S * 0.51 + 2e-3:
+                        return f"rebuilt vector of token {t} (z={z}, h={h}) is not A B + g R"
+    for l in range(c.n_layers):
+        if l == layer:
+            continue
+        for name in ("coef_k", "coef_v", "res_idx", "res_val", "res_scale"):
+            if not np.array_equal(getattr(c2, name)[l], getattr(c, name)[l]):
+                return f"{name} of another layer changed"
+    return None
+
+
+def pin_route_range(o):
+    """Routing a token range continues the offset table: the result equals a
+    running loop over all tokens, and the decode-token append [T-1, T) adds
+    exactly one rank."""
+    w = small_workload(levels=(0, 4, 8, 16), probs=(0.25, 0.25, 0.25, 0.25))
+    phi, u, theta = router_inputs(w, n_windows=2, T=200)
+    M, Hk, T = phi.shape[0], phi.shape[1], phi.shape[2]
+    lev = np.asarray(w.levels)
+    codes = np.zeros((M, Hk, T), np.uint8)
+    off = np.full((M, Hk, T + 1), 7, np.uint32)
+    for a, b in ((0, 37), (37, 120), (120, 199), (199, 200)):
+        o.route_range(phi, u, theta, w.levels, a, b, codes, off)
+    for m in range(M):
+        for h in range(Hk):
+            run = 0
+            for t in range(T):
+                z = exact_score(u[m], phi[m, h, t])
+                k = sum(1 for th in theta[m] if z > Fraction(float(th)))
+                if int(codes[m, h, t]) != k:
+                    return f"range routing code differs at m={m} h={h} t={t}"
+                if int(off[m, h, t]) != run:
+                    return f"range routing offsets break at m={m} h={h} t={t}"
+                run += int(lev[k])
+            if int(off[m, h, T]) != run:
+                return "range routing final offset wrong"
+    return None
+
+
 ALL_PINS = [pin_query_formats, pin_nibbles, pin_residual_map, pin_brute_force, pin_closed_forms,
-            pin_reductions, pin_invariants, pin_probe, pin_router]
+            pin_reductions, pin_invariants, pin_probe, pin_router, pin_compress_closed_forms,
+            pin_compress_rne_table, pin_compress_arithmetic, pin_compress_bounds,
+            pin_compress_into_cache, pin_route_range]
 
 
 def run_all(o):

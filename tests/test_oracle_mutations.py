@@ -7,6 +7,7 @@ import pytest
 import oracle
 import oracle.factorized as F
 import oracle.router as R
+import oracle.compress as CP
 import pins
 
 _orig_reconstruct = F.reconstruct
@@ -100,6 +101,77 @@ def _route_inclusive(phi, u, theta, levels):
     return codes, off2
 
 
+def _project_reversed(x, B):
+    x = np.asarray(x, dtype=np.float16).astype(np.float32)
+    B = np.asarray(B, dtype=np.float16).astype(np.float32)
+    d = x.shape[1]
+    acc = x[:, d - 1:d] * B[None, :, d - 1]
+    for j in range(d - 2, -1, -1):
+        acc = acc + x[:, j:j + 1] * B[None, :, j]
+    return acc.astype(np.float16)
+
+
+def _project_f64(x, B):
+    return (np.asarray(x, np.float64) @ np.asarray(B, np.float64).T).astype(np.float16)
+
+
+def _residual_unrounded_a(x, B, a16):
+    xx = np.asarray(x, dtype=np.float16).astype(np.float32)
+    BB = np.asarray(B, dtype=np.float16).astype(np.float32)
+    a = xx[:, 0:1] * BB[None, :, 0]
+    for j in range(1, xx.shape[1]):
+        a = a + xx[:, j:j + 1] * BB[None, :, j]
+    p = a[:, 0:1] * BB[None, 0, :]
+    for i in range(1, BB.shape[0]):
+        p = p + a[:, i:i + 1] * BB[None, i, :]
+    return xx - p
+
+
+def _residual_reversed(x, B, a16):
+    xx = np.asarray(x, dtype=np.float16).astype(np.float32)
+    BB = np.asarray(B, dtype=np.float16).astype(np.float32)
+    a = np.asarray(a16, dtype=np.float16).astype(np.float32)
+    r = BB.shape[0]
+    p = a[:, r - 1:r] * BB[None, r - 1, :]
+    for i in range(r - 2, -1, -1):
+        p = p + a[:, i:i + 1] * BB[None, i, :]
+    return xx - p
+
+
+def _select_ties_up(r, rho):
+    mag = np.abs(np.asarray(r, dtype=np.float32))
+    order = sorted(range(mag.size), key=lambda c: (-float(mag[c]), -c))
+    return np.asarray(order[:rho], dtype=np.int64)
+
+
+def _quantize_half_away(values, S):
+    v = np.asarray(values, dtype=np.float32)
+    if S == 0:
+        return np.zeros(v.shape, dtype=np.int64)
+    q = v / np.float32(S)
+    return np.clip(np.sign(q) * np.floor(np.abs(q) + 0.5), -7, 7).astype(np.int64)
+
+
+def _store_values_row_major(cache, layer, z, h, t, row):
+    if z == 0:
+        cache.coef_k[layer, h, t] = row
+    else:
+        cache.coef_v[layer, h].reshape(-1, cache.coef_v.shape[3])[t] = row
+
+
+def _store_entries_at_next(cache, layer, z, h, t, chans, codes):
+    m = layer // cache.window
+    e0 = int(cache.res_off[m, h, t + 1])
+    cache.res_idx[layer, z, h, e0:e0 + len(chans)] = chans
+    if len(chans):
+        cache.res_val[layer, z, h, e0 // 2:(e0 + len(chans)) // 2] = CP._pack_pairs(codes)
+
+
+def _route_range_from_zero(phi, u, theta, levels, t0, t1, codes, off):
+    off[:, :, t0] = 0
+    return R.__dict__["_orig_route_range"](phi, u, theta, levels, t0, t1, codes, off)
+
+
 MUTANTS = {
     "residual dropped": [(F, "reconstruct", _reconstruct_variant("no_residual"))],
     "residual sign flipped": [(F, "reconstruct", _reconstruct_variant("residual_sign"))],
@@ -128,6 +200,22 @@ MUTANTS = {
     "value blocks read row-major": [(F, "coefficient_rows", lambda cache, layer, z, h, t0, t1:
         cache.coef_k[layer, h, t0:t1].astype(np.float64) if z == 0 else
         cache.coef_v[layer, h].reshape(-1, cache.coef_v.shape[3])[t0:t1].astype(np.float64))],
+    "projection summed right to left": [(CP, "project", _project_reversed)],
+    "projection in float64": [(CP, "project", _project_f64)],
+    "residual from the unrounded coefficients": [(CP, "residual", _residual_unrounded_a)],
+    "residual basis term summed right to left": [(CP, "residual", _residual_reversed)],
+    "residual sign flipped in compress": [(CP, "residual", lambda x, B, a16:
+        -_residual_reversed.__globals__["CP"].__dict__["_orig_residual"](x, B, a16))],
+    "kept-channel ties go to the higher channel": [(CP, "select_channels", _select_ties_up)],
+    "int4 scale max|r| / 8": [(CP, "quant_scale", lambda r: np.float32(np.abs(np.asarray(r, np.float32)).max())
+                                / np.float32(8.0))],
+    "codes round half away from zero": [(CP, "quantize", _quantize_half_away)],
+    "entries stored in channel order": [(CP, "entry_order", lambda ch, k: (np.asarray(ch)[np.argsort(ch)],
+                                                                        np.asarray(k)[np.argsort(ch)]))],
+    "gate not folded into the scale": [(CP, "fold_gate", lambda S, g: np.float16(S))],
+    "value coefficients written row-major": [(CP, "store_coefficients", _store_values_row_major)],
+    "entries written at the next token's offset": [(CP, "store_entries", _store_entries_at_next)],
+    "range routing restarts the offsets at zero": [(R, "route_range", _route_range_from_zero)],
     "bf16 query read as fp16": [(F, "q_to_f64", lambda bits, dtype: np.asarray(bits, np.uint16)
                                  .view(np.float16).astype(np.float64))],
 }
@@ -136,6 +224,8 @@ MUTANTS = {
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_mutant_is_caught(name, monkeypatch):
     R.__dict__.setdefault("_orig_route", R.route)
+    R.__dict__.setdefault("_orig_route_range", R.route_range)
+    CP.__dict__.setdefault("_orig_residual", CP.residual)
     for mod, attr, fn in MUTANTS[name]:
         monkeypatch.setattr(mod, attr, fn)
         if hasattr(oracle, attr):
