@@ -180,6 +180,50 @@ dwkv_status dwkv_route(const dwkv_dims* dims, const float* phi, const float* u,
                        const float* theta, uint8_t* rank_code, uint32_t* res_off,
                        void* workspace, size_t ws_bytes, void* stream);
 
+/* dwkv_route for packed tokens [t0, t1) only, continuing an existing table:
+ * writes rank_code[m][h][t] for those tokens and
+ *   res_off[m][h][t+1] = res_off[m][h][t] + rho
+ * starting from the res_off[m][h][t0] already in the table (when t0 == 0,
+ * res_off[m][h][0] is set to 0 first).  Appending a decode token to the end of
+ * the packed layout is the range [T-1, T).  Same arguments, layout and
+ * workspace size (dwkv_route_workspace_bytes) as dwkv_route;
+ * 0 <= t0 <= t1 <= T, else DWKV_E_DIMS.  Bit-exact by construction. */
+dwkv_status dwkv_route_range(const dwkv_dims* dims, const float* phi, const float* u,
+                             const float* theta, int64_t t0, int64_t t1, uint8_t* rank_code,
+                             uint32_t* res_off, void* workspace, size_t ws_bytes, void* stream);
+
+/* Append/compress (Sec. 3: coefficients by projection onto the window's
+ * current basis, residuals 4-bit quantized at the routed rank, the gate of
+ * Eq. 1 folded into the scale).  For packed tokens [t0, t1) of layer `layer`,
+ * every KV head h and both Z, from the dense vector x (1 x d, fp16):
+ *   A_i   = fp16(sum_j x_j B_ij)                      (B = B^Z of the token's
+ *                                                      sequence, window, head)
+ *   r_c   = x_c - sum_i A_i B_ic
+ *   kept  = the rho channels of largest |r_c|, ties to the lower channel,
+ *           rho = levels[rank_code[m][h][t]]
+ *   S     = max_c |r_c| / 7;  code_c = round-half-even(r_c / S) in [-7, 7]
+ *           (0 when S == 0)
+ *   res_scale = fp16(g * S) (0 for a rank-0 token); entries stored at
+ *           [res_off[t], res_off[t+1]) ordered by descending |code|, then
+ *           ascending channel.
+ * Arithmetic: float32, every product and sum rounded on its own, sums left to
+ * right over the contracted index; the integer results are therefore exact
+ * functions of the inputs.
+ *   x_k, x_v: fp16 [t1-t0][Hkv][d] dense keys / values of the tokens
+ *             (keys post positional encoding, as the decode expects)
+ *   gate:     NULL (g = 1) or fp32 [2][Hkv][t1-t0], g in [0, 1]
+ * WRITES through the cache's pointers (coef_k, coef_v, res_idx, res_val,
+ * res_scale of `layer`, only at the range's tokens and entries; coef_v padding
+ * is untouched); reads basis, rank_code and res_off, which must already hold
+ * the tokens' routing (dwkv_route / dwkv_route_range).  A token whose rank code
+ * or offsets are inconsistent gets its coefficients and scale 0 but no entries
+ * (dwkv_validate reports it).  basis, coef_k, coef_v, x_k, x_v must be 16-byte
+ * aligned, res_idx and res_scale 2-byte, gate 4-byte (else DWKV_E_ALIGN).
+ * One launch; the library allocates nothing. */
+dwkv_status dwkv_compress(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
+                          const void* x_k, const void* x_v, const float* gate, int64_t t0,
+                          int64_t t1, void* stream);
+
 /* Dense residual term g*R of Eq. 1 for packed tokens [t0, t1) of slab
  * (layer, z, kv_head): dense[t-t0][c] = res_scale * code for every stored entry
  * of token t at channel c, zero elsewhere; fp32 [t1-t0][d] (may be NULL when

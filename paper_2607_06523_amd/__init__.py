@@ -8,6 +8,8 @@ provide device memory and the current HIP stream.
     out = cache.decode(layer)              # fp32 [B, Hq, d]
     out, err, out_ref = cache.decode(layer, probe=ProbeRef(heads, k_ref, v_ref))
     codes, offsets = cache.route(phi, u, theta)
+    cache.route_range(phi, u, theta, t0, t1)      # routing of new tokens, in place
+    cache.compress(layer, x_k, x_v, t0, t1)       # their Eq. 1 factors, in place
 """
 from __future__ import annotations
 
@@ -209,6 +211,33 @@ class DeviceCache:
                                  _ptr(res_off), _ptr(ws), ws.numel(), _stream(torch, self.device))
         binding.check(st, "dwkv_route")
         return rank_code, res_off
+
+    def route_range(self, phi, u, theta, t0: int, t1: int, rank_code=None, res_off=None):
+        """Eq. 2 routing of packed tokens [t0, t1), continuing the offset table in
+        place (by default the cache's own rank_code / res_off)."""
+        torch = self.torch
+        rank_code = self.rank_code if rank_code is None else rank_code
+        res_off = self.res_off if res_off is None else res_off
+        need = self.lib.dwkv_route_workspace_bytes(C.byref(self.dims))
+        ws = torch.empty(max(int(need), 1), dtype=torch.uint8, device=self.device)
+        st = self.lib.dwkv_route_range(C.byref(self.dims), _ptr(phi), _ptr(u), _ptr(theta), int(t0), int(t1),
+                                       _ptr(rank_code), _ptr(res_off), _ptr(ws), ws.numel(),
+                                       _stream(torch, self.device))
+        binding.check(st, "dwkv_route_range")
+        return rank_code, res_off
+
+    def compress(self, layer: int, x_k, x_v, t0: int, t1: int, gate=None):
+        """Append/compress packed tokens [t0, t1) of `layer` in place from dense
+        fp16 keys / values x_k, x_v [t1-t0, Hkv, d]; gate: None or fp32 [2, Hkv, t1-t0]."""
+        torch = self.torch
+        for x in (x_k, x_v):
+            if x.dtype != torch.float16 or not x.is_contiguous():
+                raise TypeError("x_k / x_v must be contiguous float16")
+        if gate is not None and (gate.dtype != torch.float32 or not gate.is_contiguous()):
+            raise TypeError("gate must be contiguous float32")
+        st = self.lib.dwkv_compress(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(x_k), _ptr(x_v),
+                                    _ptr(gate), int(t0), int(t1), _stream(torch, self.device))
+        binding.check(st, "dwkv_compress")
 
     def residual_map(self, layer: int, z: int, kv_head: int, t0: int, t1: int):
         torch = self.torch

@@ -357,17 +357,20 @@ size_t dwkv_route_workspace_bytes(const dwkv_dims* d) {
   return 2 * b;
 }
 
-dwkv_status dwkv_route(const dwkv_dims* d, const float* phi, const float* u, const float* theta,
-                       uint8_t* rank_code, uint32_t* res_off, void* workspace, size_t ws_bytes,
-                       void* stream) {
+dwkv_status dwkv_route_range(const dwkv_dims* d, const float* phi, const float* u, const float* theta,
+                             int64_t t0, int64_t t1, uint8_t* rank_code, uint32_t* res_off,
+                             void* workspace, size_t ws_bytes, void* stream) {
   dwkv_status st = check_dims(d);
   if (st != DWKV_OK) return st;
+  if (t0 < 0 || t1 < t0 || t1 > d->total_tokens) return DWKV_E_DIMS;
   if (!u || !res_off || !workspace || !rank_code) return DWKV_E_NULL;
-  if (d->total_tokens > 0 && !phi) return DWKV_E_NULL;
+  if (t1 > t0 && !phi) return DWKV_E_NULL;
   if (d->n_levels > 1 && !theta) return DWKV_E_NULL;
   const size_t need = dwkv_route_workspace_bytes(d);
   if (ws_bytes < need) return DWKV_E_WORKSPACE;
-  const int64_t nblk = (d->total_tokens + kRouteTokensPerBlock - 1) / kRouteTokensPerBlock;
+  const int64_t n = t1 - t0;
+  if (n == 0 && t0 > 0) return DWKV_OK;           // nothing to route, no offset to reset
+  const int64_t nblk = (n + kRouteTokensPerBlock - 1) / kRouteTokensPerBlock;
   const int n_mh = (d->n_layers / d->window) * d->n_kv_heads;
   if (nblk > 0x7fffffff) return DWKV_E_UNSUPPORTED;
   RouteArgs a;
@@ -380,11 +383,71 @@ dwkv_status dwkv_route(const dwkv_dims* d, const float* phi, const float* u, con
   a.bsum = static_cast<uint32_t*>(workspace);
   a.bpre = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + need / 2);
   a.T = d->total_tokens;
+  a.t0 = t0;
+  a.n = n;
   a.n_kv_heads = d->n_kv_heads;
   a.n_levels = d->n_levels;
   a.nblk = (int)nblk;
   for (int i = 0; i < DWKV_MAX_LEVELS; ++i) a.levels[i] = i < d->n_levels ? d->levels[i] : 0;
   return hip_status(launch_route(a, n_mh, reinterpret_cast<hipStream_t>(stream)));
+}
+
+dwkv_status dwkv_route(const dwkv_dims* d, const float* phi, const float* u, const float* theta,
+                       uint8_t* rank_code, uint32_t* res_off, void* workspace, size_t ws_bytes,
+                       void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  return dwkv_route_range(d, phi, u, theta, 0, d->total_tokens, rank_code, res_off, workspace,
+                          ws_bytes, stream);
+}
+
+dwkv_status dwkv_compress(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* x_k,
+                          const void* x_v, const float* gate, int64_t t0, int64_t t1, void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (!c || !c->basis || !c->coef_k || !c->coef_v || !c->rank_code || !c->res_off || !c->res_idx ||
+      !c->res_val || !c->res_scale)
+    return DWKV_E_NULL;
+  if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
+  if (t0 < 0 || t1 < t0 || t1 > d->total_tokens) return DWKV_E_DIMS;
+  if (t1 == t0) return DWKV_OK;
+  if (!x_k || !x_v) return DWKV_E_NULL;
+  const void* const ptrs[] = {c->basis, c->coef_k, c->coef_v, x_k, x_v};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return DWKV_E_ALIGN;
+  if ((reinterpret_cast<uintptr_t>(c->res_idx) & 1u) || (reinterpret_cast<uintptr_t>(c->res_scale) & 1u) ||
+      (reinterpret_cast<uintptr_t>(gate) & 3u))
+    return DWKV_E_ALIGN;
+  const int64_t T = d->total_tokens, Hk = d->n_kv_heads, rb = d->basis_rank;
+  const int64_t T16 = (T + 15) / 16 * 16;
+  const int M = d->n_layers / d->window, m = layer / d->window;
+  CompressArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.basis = static_cast<const uint16_t*>(c->basis) + (int64_t)m * Hk * 2 * rb * kHeadDim;
+  a.basis_b_stride = (int64_t)M * Hk * 2 * rb * kHeadDim;
+  a.code = c->rank_code + (int64_t)m * Hk * T;
+  a.off = c->res_off + (int64_t)m * Hk * (T + 1);
+  a.cu = d->cu_seqlens;
+  a.xk = static_cast<const uint16_t*>(x_k);
+  a.xv = static_cast<const uint16_t*>(x_v);
+  a.gate = gate;
+  // the cache's arrays are written in place (the pointers are const only for decode)
+  a.coef_k = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->coef_k)) + (int64_t)layer * Hk * T * rb;
+  a.coef_v = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->coef_v)) + (int64_t)layer * Hk * T16 * rb;
+  a.res_idx = const_cast<uint8_t*>(c->res_idx) + (int64_t)layer * 2 * Hk * d->res_stride;
+  a.res_val = const_cast<uint8_t*>(c->res_val) + (int64_t)layer * 2 * Hk * (d->res_stride / 2);
+  a.res_scale = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->res_scale)) + (int64_t)layer * 2 * Hk * T;
+  a.T = T;
+  a.T16 = T16;
+  a.t0 = t0;
+  a.n = t1 - t0;
+  a.res_stride = d->res_stride;
+  a.batch = d->batch;
+  a.n_kv_heads = d->n_kv_heads;
+  a.rb = d->basis_rank;
+  a.n_levels = d->n_levels;
+  for (int i = 0; i < DWKV_MAX_LEVELS; ++i) a.levels[i] = i < d->n_levels ? d->levels[i] : 0;
+  return hip_status(launch_compress(a, reinterpret_cast<hipStream_t>(stream)));
 }
 
 dwkv_status dwkv_residual_map(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, int32_t z,

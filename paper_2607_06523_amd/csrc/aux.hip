@@ -1,4 +1,5 @@
-// Router (Eq. 2) with its residual-offset scan, the residual-map test hook and
+// Router (Eq. 2) with its residual-offset scan (over the whole packed axis or a
+// token range that continues an existing table), the residual-map test hook and
 // the layout validator (gfx950).
 #include "entry.h"
 #include "internal.h"
@@ -63,8 +64,8 @@ __global__ __launch_bounds__(kRT) void route_codes_kernel(const RouteArgs a) {
   uint32_t sum = 0;
 #pragma unroll
   for (int i = 0; i < kPerThread; ++i) {
-    const int64_t t = (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
-    if (t < a.T) {
+    const int64_t t = a.t0 + (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
+    if (t < a.t0 + a.n) {
       const float4 f = *reinterpret_cast<const float4*>(a.phi + ((int64_t)mh * a.T + t) * 4);
       const float z = router_score(u, f);
       int k = 0;
@@ -98,24 +99,27 @@ __global__ __launch_bounds__(kRT) void route_block_scan_kernel(const RouteArgs a
 __global__ __launch_bounds__(kRT) void route_offsets_kernel(const RouteArgs a) {
   __shared__ uint32_t red[kRT / 64];
   const int mh = blockIdx.y;
+  const int64_t end = a.t0 + a.n;
   uint32_t rho[kPerThread];
   uint32_t mine = 0;
 #pragma unroll
   for (int i = 0; i < kPerThread; ++i) {
-    const int64_t t = (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
-    rho[i] = t < a.T ? (uint32_t)a.levels[a.code[(int64_t)mh * a.T + t]] : 0u;
+    const int64_t t = a.t0 + (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
+    rho[i] = t < end ? (uint32_t)a.levels[a.code[(int64_t)mh * a.T + t]] : 0u;
     mine += rho[i];
   }
-  uint32_t total;
-  uint32_t run = (a.nblk > 0 ? a.bpre[(int64_t)mh * a.nblk + blockIdx.x] : 0u) +
-                 block_exclusive_scan(mine, red, &total);
   uint32_t* off = a.off + (int64_t)mh * (a.T + 1);
-  if (blockIdx.x == 0 && threadIdx.x == 0) off[0] = 0u;
+  // carry-in: the offset of the range's first token (0 for a table that starts here)
+  const uint32_t base = a.t0 == 0 ? 0u : off[a.t0];
+  uint32_t total;
+  uint32_t run = base + (a.nblk > 0 ? a.bpre[(int64_t)mh * a.nblk + blockIdx.x] : 0u) +
+                 block_exclusive_scan(mine, red, &total);
+  if (a.t0 == 0 && blockIdx.x == 0 && threadIdx.x == 0) off[0] = 0u;
 #pragma unroll
   for (int i = 0; i < kPerThread; ++i) {
-    const int64_t t = (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
+    const int64_t t = a.t0 + (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
     run += rho[i];
-    if (t < a.T) off[t + 1] = run;
+    if (t < end) off[t + 1] = run;
   }
 }
 

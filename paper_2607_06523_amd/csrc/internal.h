@@ -150,7 +150,8 @@ struct RouteArgs {
   uint32_t* off;               // [M][Hkv][T+1]
   uint32_t* bsum;              // [M*Hkv][nblk]
   uint32_t* bpre;              // [M*Hkv][nblk]
-  int64_t T;
+  int64_t T;                   // token stride of code / off / phi
+  int64_t t0, n;               // routed range [t0, t0 + n); off[t0] holds the carry-in
   int32_t n_kv_heads;
   int32_t n_levels;
   int32_t nblk;
@@ -158,6 +159,27 @@ struct RouteArgs {
 };
 
 constexpr int kRouteTokensPerBlock = 1024;
+
+// Append/compress of packed tokens [t0, t0 + n) of one layer.
+struct CompressArgs {
+  const uint16_t* basis;       // window m of sequence 0; sequence b adds b*basis_b_stride,
+                               // head h and Z add (h*2 + z)*rb*d
+  int64_t basis_b_stride;
+  const uint8_t* code;         // rank_code of window m: [Hkv][T]
+  const uint32_t* off;         // res_off of window m: [Hkv][T+1]
+  const int32_t* cu;           // device cu_seqlens [batch+1]
+  const uint16_t* xk;          // [n][Hkv][d] fp16
+  const uint16_t* xv;
+  const float* gate;           // [2][Hkv][n] or null (g = 1)
+  uint16_t* coef_k;            // layer's [Hkv][T][rb]
+  uint16_t* coef_v;            // layer's [Hkv][T16/16][rb][16]
+  uint8_t* res_idx;            // layer's [2][Hkv][res_stride]
+  uint8_t* res_val;            // layer's [2][Hkv][res_stride/2]
+  uint16_t* res_scale;         // layer's [2][Hkv][T]
+  int64_t T, T16, t0, n, res_stride;
+  int32_t batch, n_kv_heads, rb, n_levels;
+  int32_t levels[DWKV_MAX_LEVELS];
+};
 
 hipError_t launch_split(int rb, int g, bool resid, bool ident, const SplitArgs& a, int n_work,
                         hipStream_t s);
@@ -170,6 +192,7 @@ hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_
 hipError_t launch_merge_tl(int rb, int g, const SplitArgs& a, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, int n_mh, hipStream_t s);
+hipError_t launch_compress(const CompressArgs& a, hipStream_t s);
 hipError_t launch_residual_map(const uint32_t* off, const uint8_t* idx, const uint8_t* val,
                                const uint16_t* scale, int64_t t0, int64_t t1, int64_t slab_len,
                                float* dense, hipStream_t s);

@@ -189,3 +189,38 @@ def test_decode_launch_count(lib):
     assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3
     d, keep = dims(n_q_heads=7)
     assert lib.dwkv_decode_launches(C.byref(d), None) == -1
+
+
+def test_route_range_and_compress_argument_checks(lib):
+    """Both new calls reject bad ranges, null and misaligned pointers on the host."""
+    from paper_2607_06523_amd import binding
+    d, keep = dims()
+    need = lib.dwkv_route_workspace_bytes(C.byref(d))
+    rr = lambda t0, t1, ws=need, u=FAKE, phi=FAKE: lib.dwkv_route_range(
+        C.byref(d), phi, u, FAKE, t0, t1, FAKE, FAKE, FAKE, ws, None)
+    assert rr(10, 5) == 2
+    assert rr(-1, 5) == 2
+    assert rr(0, 3001) == 2
+    assert rr(0, 10, ws=need - 1) == 4
+    assert rr(0, 10, u=0) == 1
+    assert rr(0, 10, phi=0) == 1
+    assert rr(2999, 2999, phi=0) == 0         # empty range past the start: nothing to do
+    c = binding.Cache(*([FAKE] * 8))
+    cp = lambda layer=0, t0=2990, t1=3000, xk=FAKE, xv=FAKE, gate=None, cache=c: lib.dwkv_compress(
+        C.byref(d), C.byref(cache), layer, xk, xv, gate, t0, t1, None)
+    assert cp(layer=4) == 2
+    assert cp(layer=-1) == 2
+    assert cp(t0=5, t1=4) == 2
+    assert cp(t1=3001) == 2
+    assert cp(xk=0) == 1
+    assert cp(t0=7, t1=7, xk=0, xv=0) == 0    # empty range
+    assert cp(xv=FAKE + 8) == 7
+    assert cp(gate=FAKE + 2) == 7
+    c2 = binding.Cache(*([FAKE] * 8))
+    c2.res_scale = FAKE + 1
+    assert cp(cache=c2) == 7
+    c3 = binding.Cache(*([FAKE] * 8))
+    c3.coef_k = 0
+    assert cp(cache=c3) == 1
+    d2, keep2 = dims(head_dim=64)
+    assert lib.dwkv_compress(C.byref(d2), C.byref(c), 0, FAKE, FAKE, None, 0, 1, None) == 3
