@@ -82,6 +82,63 @@ def cpu_baseline(host, n_pairs: int, budget_s: float):
                        f"{dt:.1f} s, extrapolated to the full step ({step_s:.1f} s)")}
 
 
+def measure_append(dc, host, wl, torch, reps: int = 20):
+    """The append/compress path at this workload: one decode token routed in
+    every window (dwkv_route_range over [T-1, T)) and compressed in every layer
+    (dwkv_compress per layer), replayed as a captured graph so the figure is
+    GPU time; and a whole-layer compress of all T tokens (the prefill side).
+    Writes into the cache, so it runs after the decode timing."""
+    from synth import router_inputs
+    T, Hk, d, L = host.total_tokens, host.n_kv_heads, host.head_dim, host.n_layers
+    phi, u, theta = router_inputs(wl, host.n_windows, T)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    phi_d, u_d, th_d = dev(phi), dev(u), dev(theta)
+    g = torch.Generator(device="cuda").manual_seed(1)
+    x1 = [(torch.randn((1, Hk, d), generator=g, device="cuda").half(),
+           torch.randn((1, Hk, d), generator=g, device="cuda").half()) for _ in range(L)]
+
+    def append_step():
+        dc.route_range(phi_d, u_d, th_d, T - 1, T)
+        for l in range(L):
+            dc.compress(l, x1[l][0], x1[l][1], T - 1, T)
+
+    append_step()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        append_step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    graph.replay()
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for _ in range(reps):
+        graph.replay()
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    step_us = ev[0].elapsed_time(ev[1]) / reps * 1e3
+    del graph
+    # prefill side: every token of one layer
+    xk = torch.randn((T, Hk, d), generator=g, device="cuda").half()
+    xv = torch.randn((T, Hk, d), generator=g, device="cuda").half()
+    dc.compress(0, xk, xv, 0, T)
+    torch.cuda.synchronize()
+    n_rep = 3
+    ev[0].record(stream)
+    for _ in range(n_rep):
+        dc.compress(0, xk, xv, 0, T)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    layer_ms = ev[0].elapsed_time(ev[1]) / n_rep
+    return {"decode_token_append_us_per_step": round(step_us, 2),
+            "append_launches_per_step": 3 + L,
+            "prefill_compress_ms_per_layer": round(layer_ms, 4),
+            "prefill_compress_vectors_per_s": round(2 * Hk * T / (layer_ms / 1e3), 1),
+            "note": "route_range of the new token in every window plus one dwkv_compress per layer "
+                    "(graph replay); prefill = dwkv_compress of all T tokens of one layer, K and V"}
+
+
 def measured_traffic(workload: str):
     """HBM bytes per launch of the token-lane decode kernel from the committed
     rocprofv3 counter profile, or None when that profile is missing or was
@@ -112,6 +169,7 @@ def main():
     ap.add_argument("--cpu-pairs", type=int, default=0, help="slabs to time on the CPU (0 = all)")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-append", action="store_true", help="skip the append/compress measurement")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before timing, run one plain device copy of this many MiB (a known-size "
                          "reference for HBM byte counters)")
@@ -247,6 +305,9 @@ def main():
         "kv_token_layers_per_s": round(host.total_tokens * L / (ms_per_step / 1e3), 1),
         "wall_s_timed": round(wall, 3),
     }
+    if not args.no_append and args.variant == "full":
+        log("[bench] timing the append/compress path")
+        result["append"] = measure_append(dc, host, wl, torch)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
         result["cpu_baseline"] = cpu_baseline(host, args.cpu_pairs, args.cpu_budget)

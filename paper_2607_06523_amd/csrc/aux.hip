@@ -51,10 +51,10 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* r
   return before + inc - v;
 }
 
-// Level codes and per-block rank sums.  grid (nblk, M*Hkv)
-__global__ __launch_bounds__(kRT) void route_codes_kernel(const RouteArgs a) {
-  __shared__ uint32_t red[kRT / 64];
-  const int mh = blockIdx.y;
+// Level codes of this thread's tokens of block `blk`, written to a.code; the
+// routed ranks go to rho[] (0 past the range).  Returns their sum.
+__device__ __forceinline__ uint32_t route_block_tokens(const RouteArgs& a, int mh, int blk,
+                                                       uint32_t (&rho)[kPerThread]) {
   const int m = mh / a.n_kv_heads;
   const float4 u = *reinterpret_cast<const float4*>(a.u + 4 * m);
   const int nth = a.n_levels - 1;
@@ -64,7 +64,8 @@ __global__ __launch_bounds__(kRT) void route_codes_kernel(const RouteArgs a) {
   uint32_t sum = 0;
 #pragma unroll
   for (int i = 0; i < kPerThread; ++i) {
-    const int64_t t = a.t0 + (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
+    const int64_t t = a.t0 + (int64_t)blk * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
+    rho[i] = 0u;
     if (t < a.t0 + a.n) {
       const float4 f = *reinterpret_cast<const float4*>(a.phi + ((int64_t)mh * a.T + t) * 4);
       const float z = router_score(u, f);
@@ -72,9 +73,49 @@ __global__ __launch_bounds__(kRT) void route_codes_kernel(const RouteArgs a) {
 #pragma unroll
       for (int j = 0; j < DWKV_MAX_LEVELS - 1; ++j) k += (j < nth && z > th[j]) ? 1 : 0;
       a.code[(int64_t)mh * a.T + t] = (uint8_t)k;
-      sum += (uint32_t)a.levels[k];
+      rho[i] = (uint32_t)a.levels[k];
+      sum += rho[i];
     }
   }
+  return sum;
+}
+
+// Offsets of this thread's tokens: off[t+1] = carry + (ranks of earlier tokens) + rho_t,
+// with `carry` the offset of the block's first token.
+__device__ __forceinline__ void route_write_offsets(const RouteArgs& a, int mh, int blk, uint32_t carry,
+                                                    const uint32_t (&rho)[kPerThread], uint32_t* red) {
+  uint32_t mine = 0;
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) mine += rho[i];
+  uint32_t total;
+  uint32_t run = carry + block_exclusive_scan(mine, red, &total);
+  uint32_t* off = a.off + (int64_t)mh * (a.T + 1);
+  if (a.t0 == 0 && blk == 0 && threadIdx.x == 0) off[0] = 0u;
+  const int64_t end = a.t0 + a.n;
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    const int64_t t = a.t0 + (int64_t)blk * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
+    run += rho[i];
+    if (t < end) off[t + 1] = run;
+  }
+}
+
+// A range of at most one block of tokens in one launch: codes, scan, offsets.  grid (M*Hkv)
+__global__ __launch_bounds__(kRT) void route_small_kernel(const RouteArgs a) {
+  __shared__ uint32_t red[kRT / 64];
+  const int mh = blockIdx.x;
+  uint32_t rho[kPerThread];
+  route_block_tokens(a, mh, 0, rho);
+  const uint32_t carry = a.t0 == 0 ? 0u : a.off[(int64_t)mh * (a.T + 1) + a.t0];
+  route_write_offsets(a, mh, 0, carry, rho, red);
+}
+
+// Level codes and per-block rank sums.  grid (nblk, M*Hkv)
+__global__ __launch_bounds__(kRT) void route_codes_kernel(const RouteArgs a) {
+  __shared__ uint32_t red[kRT / 64];
+  const int mh = blockIdx.y;
+  uint32_t rho[kPerThread];
+  const uint32_t sum = route_block_tokens(a, mh, blockIdx.x, rho);
   const uint32_t tot = block_sum(sum, red);
   if (threadIdx.x == 0) a.bsum[(int64_t)mh * a.nblk + blockIdx.x] = tot;
 }
@@ -95,32 +136,20 @@ __global__ __launch_bounds__(kRT) void route_block_scan_kernel(const RouteArgs a
   }
 }
 
-// Offsets: off[t+1] = (block prefix) + (ranks of earlier tokens in the block) + rho_t.
+// Offsets of a multi-block range from the codes and the scanned block sums.
 __global__ __launch_bounds__(kRT) void route_offsets_kernel(const RouteArgs a) {
   __shared__ uint32_t red[kRT / 64];
   const int mh = blockIdx.y;
   const int64_t end = a.t0 + a.n;
   uint32_t rho[kPerThread];
-  uint32_t mine = 0;
 #pragma unroll
   for (int i = 0; i < kPerThread; ++i) {
     const int64_t t = a.t0 + (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
     rho[i] = t < end ? (uint32_t)a.levels[a.code[(int64_t)mh * a.T + t]] : 0u;
-    mine += rho[i];
   }
-  uint32_t* off = a.off + (int64_t)mh * (a.T + 1);
   // carry-in: the offset of the range's first token (0 for a table that starts here)
-  const uint32_t base = a.t0 == 0 ? 0u : off[a.t0];
-  uint32_t total;
-  uint32_t run = base + (a.nblk > 0 ? a.bpre[(int64_t)mh * a.nblk + blockIdx.x] : 0u) +
-                 block_exclusive_scan(mine, red, &total);
-  if (a.t0 == 0 && blockIdx.x == 0 && threadIdx.x == 0) off[0] = 0u;
-#pragma unroll
-  for (int i = 0; i < kPerThread; ++i) {
-    const int64_t t = a.t0 + (int64_t)blockIdx.x * kRouteTokensPerBlock + threadIdx.x * kPerThread + i;
-    run += rho[i];
-    if (t < end) off[t + 1] = run;
-  }
+  const uint32_t base = a.t0 == 0 ? 0u : a.off[(int64_t)mh * (a.T + 1) + a.t0];
+  route_write_offsets(a, mh, blockIdx.x, base + a.bpre[(int64_t)mh * a.nblk + blockIdx.x], rho, red);
 }
 
 // One thread per token: dense g*R row of the token.
@@ -199,12 +228,13 @@ __global__ __launch_bounds__(256) void validate_kernel(const ValidateArgs a) {
 }  // namespace
 
 hipError_t launch_route(const RouteArgs& a, int n_mh, hipStream_t s) {
-  const int nb = a.nblk > 0 ? a.nblk : 1;
-  if (a.nblk > 0) {
+  if (a.nblk <= 1) {                     // one block per (window, head): a single launch
+    hipLaunchKernelGGL(route_small_kernel, dim3(n_mh), dim3(kRT), 0, s, a);
+  } else {
     hipLaunchKernelGGL(route_codes_kernel, dim3(a.nblk, n_mh), dim3(kRT), 0, s, a);
     hipLaunchKernelGGL(route_block_scan_kernel, dim3(n_mh), dim3(kRT), 0, s, a);
+    hipLaunchKernelGGL(route_offsets_kernel, dim3(a.nblk, n_mh), dim3(kRT), 0, s, a);
   }
-  hipLaunchKernelGGL(route_offsets_kernel, dim3(nb, n_mh), dim3(kRT), 0, s, a);
   return hipGetLastError();
 }
 

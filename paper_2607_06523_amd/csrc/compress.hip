@@ -5,13 +5,19 @@
 // One workgroup (4 waves) takes up to 64 tokens of one (KV head, Z) and holds
 // the window basis of the tokens' sequence in LDS; each wave compresses one
 // token at a time:
-//   A_i   = fp16( x_0 B_i0 + x_1 B_i1 + ... )        lane i, left to right over d
-//   r_c   = x_c - (A_0 B_0c + A_1 B_1c + ...)         lanes own channels 2l, 2l+1
-//   kept  = rho largest |r_c|, ties to the lower channel (rank by a 64-bit key)
+//   A_i   = fp16( sum_j x_j B_ij )                    lane i
+//   r_c   = x_c - sum_i A_i B_ic                      lanes own channels 2l, 2l+1
+//   (each sum in four contiguous quarters of its index, each left to right,
+//   combined as (q0 + q1) + (q2 + q3): four independent chains per lane)
+//   kept  = rho largest |r_c|, ties to the lower channel (threshold search on
+//           64-bit keys, one ballot pair per key bit)
 //   S     = max |r| / 7,  code = rne(r_c / S) in [-7, 7],  scale = fp16(g S)
 //   entries in storage order (|code| descending, then channel) via ballots.
-// Every product and sum is rounded to float32 on its own (no contraction), so
-// the integer results do not depend on the compiler's choice of instructions.
+// Every sum is rounded to float32 term by term in that fixed order; products of
+// two fp16 values are exact in float32, so they are accumulated with fused
+// multiply-adds (the same numbers as separately rounded products and sums) and
+// nothing else is contracted, so the integer results are exact functions of
+// the inputs.
 #include "entry.h"
 #include "internal.h"
 
@@ -36,6 +42,15 @@ __device__ __forceinline__ uint16_t float_to_half_bits(float v) {
   return __builtin_bit_cast(uint16_t, (_Float16)v);      // round to nearest even
 }
 
+// acc + x*b for fp16 values x, b.  Their product is exact in float32, so one
+// fused multiply-add (a single mixed-precision instruction) gives the same
+// number as the product rounded to float32 followed by a rounded sum.  The
+// first term of a sum is fma(x, b, -0), which is the product itself, signed
+// zero included.
+__device__ __forceinline__ float fma_exact(float x_f16_valued, uint16_t b_bits, float acc) {
+  return __builtin_fmaf(x_f16_valued, half_bits_to_float(b_bits), acc);
+}
+
 __device__ __forceinline__ int mbcnt64(unsigned long long m) {
   return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
@@ -45,7 +60,6 @@ struct Smem {
   uint16_t bas[kMaxRB * kBRow];          // basis rows of (sequence, window, head, Z)
   float xs[kCW][D];                      // the wave's input vector
   float as[kCW][kMaxRB];                 // its fp16-rounded coefficients
-  unsigned long long key[kCW][D];        // selection keys
   uint8_t ech[kCW][D];                   // entries in storage order: channel
   uint8_t ecode[kCW][D];                 //                          int4 nibble
 };
@@ -70,38 +84,64 @@ struct Slab {
   uint16_t* res_scale;         // [T]
 };
 
-__device__ __forceinline__ void compress_token(const CompressArgs& a, const Slab& sl, Smem& sm, int wv,
-                                               int lane, int h, int z, int64_t t) {
-#pragma clang fp contract(off)
+// Global inputs of one token, loaded ahead of its arithmetic.
+struct TokenIn {
+  uint32_t xw;                 // x[2 lane], x[2 lane + 1] (fp16 pair)
+  uint32_t lvl;                // routed level index
+  int64_t e0, e1;              // its residual entries [e0, e1)
+  float g;                     // gate
+};
+
+__device__ __forceinline__ TokenIn load_token(const CompressArgs& a, const Slab& sl, int lane, int h, int z,
+                                              int64_t t) {
   const int64_t k = t - a.t0;
-  const int rb = a.rb;
   const uint16_t* X = (z ? a.xv : a.xk) + (k * a.n_kv_heads + h) * D;
-  const uint32_t xw = reinterpret_cast<const uint32_t*>(X)[lane];
-  const float x0 = half_bits_to_float((uint16_t)(xw & 0xffffu));
-  const float x1 = half_bits_to_float((uint16_t)(xw >> 16));
+  TokenIn in;
+  in.xw = reinterpret_cast<const uint32_t*>(X)[lane];
+  in.lvl = sl.code[t];
+  in.e0 = sl.off[t];
+  in.e1 = sl.off[t + 1];
+  in.g = a.gate ? a.gate[(int64_t)(z * a.n_kv_heads + h) * a.n + k] : 1.0f;
+  return in;
+}
+
+__device__ __forceinline__ void compress_token(const CompressArgs& a, const Slab& sl, Smem& sm, int wv,
+                                               int lane, int z, int64_t t, const TokenIn& in) {
+#pragma clang fp contract(off)
+  const int rb = a.rb;
+  const float x0 = half_bits_to_float((uint16_t)(in.xw & 0xffffu));
+  const float x1 = half_bits_to_float((uint16_t)(in.xw >> 16));
+  const uint32_t lvl = in.lvl;
+  const int64_t e0 = in.e0, e1 = in.e1;
+  const float g = in.g;
   wave_lds_sync();                       // the previous token is done with the wave's arrays
   *reinterpret_cast<float2*>(&sm.xs[wv][2 * lane]) = make_float2(x0, x1);
   wave_lds_sync();
 
-  // ---- coefficients: lane i sums x_j B_ij left to right over the d channels
+  // ---- coefficients: lane i sums x_j B_ij over the four channel quarters
+  // (32 channels each, left to right) as four independent chains
+  constexpr int QD = D / 4;
   for (int i = lane; i < rb; i += 64) {
     const uint16_t* row = sm.bas + i * kBRow;
-    float acc = 0.f;
+    float s[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 2
-    for (int q = 0; q < D / 8; ++q) {
-      const uint4 bw = *reinterpret_cast<const uint4*>(row + 8 * q);
-      const float4 xa = *reinterpret_cast<const float4*>(&sm.xs[wv][8 * q]);
-      const float4 xb = *reinterpret_cast<const float4*>(&sm.xs[wv][8 * q + 4]);
-      const float xv8[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
-      const uint32_t bw4[4] = {bw.x, bw.y, bw.z, bw.w};
+    for (int j0 = 0; j0 < QD; j0 += 8) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t w = bw4[j >> 1];
-        const float bij = half_bits_to_float((uint16_t)((j & 1) ? (w >> 16) : (w & 0xffffu)));
-        const float prod = xv8[j] * bij;
-        acc = (q == 0 && j == 0) ? prod : acc + prod;
+      for (int q = 0; q < 4; ++q) {
+        const uint4 bw = *reinterpret_cast<const uint4*>(row + q * QD + j0);
+        const float4 xa = *reinterpret_cast<const float4*>(&sm.xs[wv][q * QD + j0]);
+        const float4 xb = *reinterpret_cast<const float4*>(&sm.xs[wv][q * QD + j0 + 4]);
+        const float xv8[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+        const uint32_t bw4[4] = {bw.x, bw.y, bw.z, bw.w};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const uint32_t w = bw4[j >> 1];
+          const uint16_t bij = (uint16_t)((j & 1) ? (w >> 16) : (w & 0xffffu));
+          s[q] = fma_exact(xv8[j], bij, (j0 == 0 && j == 0) ? -0.0f : s[q]);
+        }
       }
     }
+    const float acc = (s[0] + s[1]) + (s[2] + s[3]);
     const uint16_t ab = float_to_half_bits(acc);
     sm.as[wv][i] = half_bits_to_float(ab);
     if (z == 0)
@@ -111,25 +151,30 @@ __device__ __forceinline__ void compress_token(const CompressArgs& a, const Slab
   }
   wave_lds_sync();
 
-  // ---- residual of channels c0 = 2 lane, c1 = 2 lane + 1
-  float p0 = 0.f, p1 = 0.f;
-  for (int i0 = 0; i0 < rb; i0 += 4) {
-    const float4 a4 = *reinterpret_cast<const float4*>(&sm.as[wv][i0]);
-    const float av[4] = {a4.x, a4.y, a4.z, a4.w};
+  // ---- residual of channels c0 = 2 lane, c1 = 2 lane + 1: the basis term
+  // summed over the four quarters of the basis rows (rb/4 rows each, in order)
+  const int qr = rb >> 2;                // a multiple of 4
+  float u0[4] = {0.f, 0.f, 0.f, 0.f}, u1[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int i0 = 0; i0 < qr; i0 += 4) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const uint32_t bw = *reinterpret_cast<const uint32_t*>(sm.bas + (i0 + u) * kBRow + 2 * lane);
-      const float q0 = av[u] * half_bits_to_float((uint16_t)(bw & 0xffffu));
-      const float q1 = av[u] * half_bits_to_float((uint16_t)(bw >> 16));
-      if (i0 == 0 && u == 0) { p0 = q0; p1 = q1; } else { p0 = p0 + q0; p1 = p1 + q1; }
+    for (int q = 0; q < 4; ++q) {
+      const float4 a4 = *reinterpret_cast<const float4*>(&sm.as[wv][q * qr + i0]);
+      const float av[4] = {a4.x, a4.y, a4.z, a4.w};
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const uint32_t bw = *reinterpret_cast<const uint32_t*>(sm.bas + (q * qr + i0 + v) * kBRow + 2 * lane);
+        const bool first = i0 == 0 && v == 0;
+        u0[q] = fma_exact(av[v], (uint16_t)(bw & 0xffffu), first ? -0.0f : u0[q]);
+        u1[q] = fma_exact(av[v], (uint16_t)(bw >> 16), first ? -0.0f : u1[q]);
+      }
     }
   }
+  const float p0 = (u0[0] + u0[1]) + (u0[2] + u0[3]);
+  const float p1 = (u1[0] + u1[1]) + (u1[2] + u1[3]);
   const float r0 = x0 - p0, r1 = x1 - p1;
 
   // ---- routed rank of the token (shared by the window's layers and K/V)
-  const uint32_t lvl = sl.code[t];
   const int rho = lvl < (uint32_t)a.n_levels ? a.levels[lvl] : -1;
-  const int64_t e0 = sl.off[t], e1 = sl.off[t + 1];
   const bool entries_ok = rho > 0 && e1 - e0 == rho && e1 <= a.res_stride && (e0 & 1) == 0;
   if (rho <= 0) {                        // rank 0 (or a malformed code): no entries, scale 0
     if (lane == 0) sl.res_scale[t] = 0;
@@ -141,30 +186,32 @@ __device__ __forceinline__ void compress_token(const CompressArgs& a, const Slab
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
   const float S = mx / 7.0f;
-  const float g = a.gate ? a.gate[(int64_t)(z * a.n_kv_heads + h) * a.n + k] : 1.0f;
   // g * S is rounded to float32 before the fp16 conversion (the value is
   // uniform; taking it through readfirstlane keeps the two roundings apart
   // instead of one mixed-precision multiply that would round once)
   const float gS = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, g * S)));
   if (lane == 0) sl.res_scale[t] = float_to_half_bits(gS);
 
-  // ---- kept channels: rank of each channel under (|r| descending, channel ascending)
+  // ---- kept channels: the rho largest keys (|r| bits, then 127 - channel;
+  // keys are distinct and below 2^38).  The rho-th largest key is the largest
+  // threshold that at least rho keys reach; its bits are fixed from the top.
   const int c0 = 2 * lane, c1 = 2 * lane + 1;
   const unsigned long long k0 =
       ((unsigned long long)__builtin_bit_cast(uint32_t, fabsf(r0)) << 7) | (uint32_t)(D - 1 - c0);
   const unsigned long long k1 =
       ((unsigned long long)__builtin_bit_cast(uint32_t, fabsf(r1)) << 7) | (uint32_t)(D - 1 - c1);
-  sm.key[wv][c0] = k0;
-  sm.key[wv][c1] = k1;
-  wave_lds_sync();
-  int rank0 = 0, rank1 = 0;
-#pragma unroll 4
-  for (int c = 0; c < D; c += 2) {
-    const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&sm.key[wv][c]);
-    rank0 += (kk.x > k0) + (kk.y > k0);
-    rank1 += (kk.x > k1) + (kk.y > k1);
+  // Stops as soon as exactly rho keys reach the threshold (then they are the
+  // rho largest); rho == d stops at once.
+  unsigned long long thr = 0;
+  if (rho < D) {
+    for (int bit = 37; bit >= 0; --bit) {
+      const unsigned long long cand = thr | (1ull << bit);
+      const int cnt = __popcll(__ballot(k0 >= cand)) + __popcll(__ballot(k1 >= cand));
+      if (cnt >= rho) thr = cand;
+      if (cnt == rho) break;
+    }
   }
-  const bool sel0 = rank0 < rho, sel1 = rank1 < rho;
+  const bool sel0 = k0 >= thr, sel1 = k1 >= thr;
 
   // ---- codes and storage order (|code| descending, then channel ascending)
   int q0 = 0, q1 = 0;
@@ -213,6 +260,9 @@ __global__ __launch_bounds__(kCW * 64) void compress_kernel(const CompressArgs a
   for (int b = sequence_of(a.cu, a.batch, c0); b < a.batch && (int64_t)a.cu[b] < c1; ++b) {
     const int64_t s0 = max(c0, (int64_t)a.cu[b]), s1 = min(c1, (int64_t)a.cu[b + 1]);
     if (s1 <= s0) continue;              // empty sequence (uniform over the workgroup)
+    int64_t t = s0 + wv;
+    TokenIn cur = {};
+    if (t < s1) cur = load_token(a, sl, lane, h, z, t);   // in flight while the basis loads
     __syncthreads();                     // every wave is done with the previous basis
     const uint16_t* src = a.basis + (int64_t)b * a.basis_b_stride + (int64_t)(h * 2 + z) * rb * D;
     for (int e = threadIdx.x; e < rb * (D / 8); e += kCW * 64) {
@@ -221,7 +271,12 @@ __global__ __launch_bounds__(kCW * 64) void compress_kernel(const CompressArgs a
           *reinterpret_cast<const uint4*>(src + (int64_t)i * D + 8 * q);
     }
     __syncthreads();
-    for (int64_t t = s0 + wv; t < s1; t += kCW) compress_token(a, sl, sm, wv, lane, h, z, t);
+    for (; t < s1; t += kCW) {
+      TokenIn nxt = cur;
+      if (t + kCW < s1) nxt = load_token(a, sl, lane, h, z, t + kCW);
+      compress_token(a, sl, sm, wv, lane, z, t, cur);
+      cur = nxt;
+    }
   }
 }
 

@@ -732,24 +732,36 @@ def pin_compress_rne_table(o):
     return None
 
 
+def _exact_quarter_sum(terms):
+    """Exact-arithmetic model of the fixed float32 order: four contiguous
+    chunks [floor(q n/4), floor((q+1) n/4)), each summed left to right with
+    every addition rounded to float32, then (q0 + q1) + (q2 + q3)."""
+    n = len(terms)
+    b = [q * n // 4 for q in range(5)]
+    part = []
+    for q in range(4):
+        chunk = terms[b[q]:b[q + 1]]
+        acc = chunk[0] if chunk else Fraction(0)
+        for t in chunk[1:]:
+            acc = fp32_round(acc + t)
+        part.append(acc)
+    return fp32_round(fp32_round(part[0] + part[1]) + fp32_round(part[2] + part[3]))
+
+
 def _exact_project(x, B):
-    """A_i = fp16(left-to-right float32 sum of x_j B_ij), each op rounded."""
+    """A_i = fp16 of the fixed-order float32 sum of the rounded products x_j B_ij."""
     out = []
     for i in range(B.shape[0]):
-        acc = fp32_round(Fraction(float(x[0])) * Fraction(float(B[i, 0])))
-        for j in range(1, len(x)):
-            acc = fp32_round(acc + fp32_round(Fraction(float(x[j])) * Fraction(float(B[i, j]))))
-        out.append(fp16_round(acc))
+        terms = [fp32_round(Fraction(float(x[j])) * Fraction(float(B[i, j]))) for j in range(len(x))]
+        out.append(fp16_round(_exact_quarter_sum(terms)))
     return out
 
 
 def _exact_residual(x, B, a):
     out = []
     for c in range(len(x)):
-        p = fp32_round(a[0] * Fraction(float(B[0, c])))
-        for i in range(1, B.shape[0]):
-            p = fp32_round(p + fp32_round(a[i] * Fraction(float(B[i, c]))))
-        out.append(fp32_round(Fraction(float(x[c])) - p))
+        terms = [fp32_round(a[i] * Fraction(float(B[i, c]))) for i in range(B.shape[0])]
+        out.append(fp32_round(Fraction(float(x[c])) - _exact_quarter_sum(terms)))
     return out
 
 
@@ -769,10 +781,10 @@ def pin_compress_arithmetic(o):
     for k in range(4):
         ea = _exact_project(x[k], B)
         if [Fraction(float(v)) for v in a16[k]] != ea:
-            return f"projection is not the per-op rounded left-to-right float32 sum (vector {k})"
+            return f"projection is not the per-op rounded fixed-order float32 sum (vector {k})"
         er = _exact_residual(x[k], B, ea)
         if [Fraction(float(v)) for v in r[k]] != er:
-            return f"residual is not x - (left-to-right float32 basis term) (vector {k})"
+            return f"residual is not x - (fixed-order float32 basis term) (vector {k})"
         for rho in (2, 8):
             S = fp32_round(max(abs(v) for v in er) / 7)
             want = _expected_entries(er, rho, S)
@@ -794,9 +806,9 @@ def pin_compress_arithmetic(o):
     for k in range(3):
         ea = _exact_project(x2[k], B2)
         if [Fraction(float(v)) for v in a2[k]] != ea:
-            return f"projection of cancelling terms is not the left-to-right float32 sum (vector {k})"
+            return f"projection of cancelling terms is not the fixed-order float32 sum (vector {k})"
         if [Fraction(float(v)) for v in r2[k]] != _exact_residual(x2[k], B2, ea):
-            return f"residual of cancelling terms is not the left-to-right float32 sum (vector {k})"
+            return f"residual of cancelling terms is not the fixed-order float32 sum (vector {k})"
     # enumeration: on 6 channels with repeated magnitudes, the kept set is the
     # lexicographically first subset (by channel) among those with the largest
     # sorted |r| profile

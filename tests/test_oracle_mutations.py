@@ -111,6 +111,25 @@ def _project_reversed(x, B):
     return acc.astype(np.float16)
 
 
+def _project_left_to_right(x, B):
+    x = np.asarray(x, dtype=np.float16).astype(np.float32)
+    B = np.asarray(B, dtype=np.float16).astype(np.float32)
+    acc = x[:, 0:1] * B[None, :, 0]
+    for j in range(1, x.shape[1]):
+        acc = acc + x[:, j:j + 1] * B[None, :, j]
+    return acc.astype(np.float16)
+
+
+def _residual_left_to_right(x, B, a16):
+    xx = np.asarray(x, dtype=np.float16).astype(np.float32)
+    BB = np.asarray(B, dtype=np.float16).astype(np.float32)
+    a = np.asarray(a16, dtype=np.float16).astype(np.float32)
+    p = a[:, 0:1] * BB[None, 0, :]
+    for i in range(1, BB.shape[0]):
+        p = p + a[:, i:i + 1] * BB[None, i, :]
+    return xx - p
+
+
 def _project_f64(x, B):
     return (np.asarray(x, np.float64) @ np.asarray(B, np.float64).T).astype(np.float16)
 
@@ -202,6 +221,8 @@ MUTANTS = {
         cache.coef_v[layer, h].reshape(-1, cache.coef_v.shape[3])[t0:t1].astype(np.float64))],
     "projection summed right to left": [(CP, "project", _project_reversed)],
     "projection in float64": [(CP, "project", _project_f64)],
+    "projection summed left to right without quarters": [(CP, "project", _project_left_to_right)],
+    "basis term summed left to right without quarters": [(CP, "residual", _residual_left_to_right)],
     "residual from the unrounded coefficients": [(CP, "residual", _residual_unrounded_a)],
     "residual basis term summed right to left": [(CP, "residual", _residual_reversed)],
     "residual sign flipped in compress": [(CP, "residual", lambda x, B, a16:
