@@ -139,6 +139,54 @@ def measure_append(dc, host, wl, torch, reps: int = 20):
                     "(graph replay); prefill = dwkv_compress of all T tokens of one layer, K and V"}
 
 
+def measure_comparators(dc, host, torch, steps: int = 3):
+    """The decode's comparison paths on the same GPU and workload: a dense fp16
+    cache decode (every layer's K/V resident, 2 bytes per element) and the
+    unfused path (each layer's cache rebuilt into fp16 buffers, then the dense
+    decode over them).  Times whole 32-layer steps with HIP events, plus the
+    per-layer kernels."""
+    T, Hk, d, L, B = host.total_tokens, host.n_kv_heads, host.head_dim, host.n_layers, host.batch
+    T16 = -(-T // 16) * 16
+    g = torch.Generator(device="cuda").manual_seed(2)
+    ks = [torch.randn((Hk, T, d), generator=g, device="cuda", dtype=torch.float16) for _ in range(L)]
+    vs = [torch.randn((Hk, T16 // 16, d, 16), generator=g, device="cuda", dtype=torch.float16) for _ in range(L)]
+    kb = torch.empty((Hk, T, d), dtype=torch.float16, device="cuda")
+    vb = torch.empty((Hk, T16 // 16, d, 16), dtype=torch.float16, device="cuda")
+    outs = [torch.empty((B, host.n_q_heads, d), dtype=torch.float32, device="cuda") for _ in range(L)]
+    ws = torch.empty(int(dc.lib.dwkv_dense_workspace_bytes(__import__("ctypes").byref(dc.dims))),
+                     dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, n):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        fn()
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for _ in range(n):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / n
+
+    dense_step = timed(lambda: [dc.dense_decode(ks[l], vs[l], dc.q[l], out=outs[l], workspace=ws)
+                                for l in range(L)], steps)
+    unfused_step = timed(lambda: [(dc.materialize(l, kb, vb), dc.dense_decode(kb, vb, dc.q[l], out=outs[l],
+                                                                              workspace=ws))
+                                  for l in range(L)], steps)
+    mat_layer = timed(lambda: [dc.materialize(l, kb, vb) for l in range(L)], steps) / L
+    dense_bytes = 2 * Hk * T * d * 2 + B * host.n_q_heads * d * (2 + 4)
+    dense_layer = dense_step / L
+    del ks, vs
+    return {"dense_fp16_tokens_per_s": round(B / (dense_step / 1e3), 2),
+            "dense_fp16_ms_per_step": round(dense_step, 4),
+            "dense_fp16_gbps": round(dense_bytes / (dense_layer / 1e3) / 1e9, 1),
+            "unfused_tokens_per_s": round(B / (unfused_step / 1e3), 2),
+            "unfused_ms_per_step": round(unfused_step, 4),
+            "materialize_ms_per_layer": round(mat_layer, 5),
+            "note": "dense: dwkv_dense_decode per layer over resident fp16 K/V; unfused: dwkv_materialize "
+                    "then dwkv_dense_decode per layer (rebuilt cache written to and re-read from HBM)"}
+
+
 def measured_traffic(workload: str):
     """HBM bytes per launch of the token-lane decode kernel from the committed
     rocprofv3 counter profile, or None when that profile is missing or was
@@ -170,6 +218,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-append", action="store_true", help="skip the append/compress measurement")
+    ap.add_argument("--no-comparators", action="store_true",
+                    help="skip the dense fp16 and unfused comparison paths")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before timing, run one plain device copy of this many MiB (a known-size "
                          "reference for HBM byte counters)")
@@ -308,6 +358,9 @@ def main():
     if not args.no_append and args.variant == "full":
         log("[bench] timing the append/compress path")
         result["append"] = measure_append(dc, host, wl, torch)
+    if not args.no_comparators and args.variant == "full":
+        log("[bench] timing the dense fp16 and unfused comparison paths")
+        result["comparators"] = measure_comparators(dc, host, torch)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
         result["cpu_baseline"] = cpu_baseline(host, args.cpu_pairs, args.cpu_budget)

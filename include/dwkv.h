@@ -233,6 +233,37 @@ dwkv_status dwkv_residual_map(const dwkv_dims* dims, const dwkv_cache* cache, in
                               int32_t z, int32_t kv_head, int64_t t0, int64_t t1,
                               float* dense, void* stream);
 
+/* Comparison paths (the fused decode's alternatives: the paper's "full KV"
+ * baseline and its "w/o fused kernel" ablation, Table 1 and Table 2).
+ *
+ * dwkv_materialize: Eq. 1 written out for every packed token and KV head of
+ * layer `layer`: K_hat = A^K B^K + g R^K, V_hat = A^V B^V + g R^V, summed in
+ * float32 and rounded once to fp16.
+ *   k_out: fp16 [Hkv][T][d] (row-major, packed tokens), written
+ *   v_out: fp16 [Hkv][T16/16][d][16] (16-token blocks, token index fastest,
+ *          the layout of dwkv_probe.v_ref), written; padding tokens zeroed
+ * Reads the cache as dwkv_decode does (residual entries past res_stride or a
+ * rank above d are not added).  basis, coef_k, coef_v, k_out and v_out must be
+ * 16-byte aligned, res_scale 2-byte (else DWKV_E_ALIGN).  One launch. */
+dwkv_status dwkv_materialize(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
+                             void* k_out, void* v_out, void* stream);
+
+/* Bytes of device workspace dwkv_dense_decode needs (0 when dims are invalid). */
+size_t dwkv_dense_workspace_bytes(const dwkv_dims* dims);
+
+/* Decode attention over a dense fp16 cache (no factorization): for every
+ * sequence b and query head hq, out[b][hq] = softmax_t(sm_scale q.K_t) V_t
+ * over the T_b packed tokens of sequence b, KV head hq / (Hq/Hkv).
+ *   k: fp16 [Hkv][T][d];  v: fp16 [Hkv][T16/16][d][16] (blocked as above)
+ *   q, q_type, sm_scale, out: as in dwkv_decode
+ *   workspace: >= dwkv_dense_workspace_bytes(dims) bytes, no initial contents
+ * Uses dims for the shape only (cu_seqlens, heads, T, split_tokens); the
+ * cache fields of dims must still be valid.  Every pointer 16-byte aligned.
+ * Two launches (split-K pass, merge). */
+dwkv_status dwkv_dense_decode(const dwkv_dims* dims, const void* k, const void* v, const void* q,
+                              int32_t q_type, float sm_scale, float* out, void* workspace,
+                              size_t ws_bytes, void* stream);
+
 /* Bytes of device workspace dwkv_validate needs. */
 size_t dwkv_validate_workspace_bytes(void);
 

@@ -239,6 +239,36 @@ class DeviceCache:
                                     _ptr(gate), int(t0), int(t1), _stream(torch, self.device))
         binding.check(st, "dwkv_compress")
 
+    def materialize(self, layer: int, k_out=None, v_out=None):
+        """Eq. 1 written out for `layer`: K_hat fp16 [Hkv, T, d] and V_hat fp16
+        [Hkv, T16/16, d, 16] (the blocked layout of the dense decode)."""
+        torch = self.torch
+        Hk, T, d = self.n_kv_heads, self.total_tokens, self.head_dim
+        T16 = -(-T // 16) * 16
+        if k_out is None:
+            k_out = torch.empty((Hk, T, d), dtype=torch.float16, device=self.device)
+        if v_out is None:
+            v_out = torch.empty((Hk, T16 // 16, d, 16), dtype=torch.float16, device=self.device)
+        st = self.lib.dwkv_materialize(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(k_out),
+                                       _ptr(v_out), _stream(torch, self.device))
+        binding.check(st, "dwkv_materialize")
+        return k_out, v_out
+
+    def dense_decode(self, k, v, q, sm_scale: float | None = None, out=None, workspace=None):
+        """Decode attention over a dense fp16 cache k [Hkv, T, d], v [Hkv, T16/16, d, 16]."""
+        torch = self.torch
+        qt = F16 if q.dtype == torch.float16 else BF16
+        if out is None:
+            out = torch.empty((self.batch, self.n_q_heads, self.head_dim), dtype=torch.float32, device=self.device)
+        if workspace is None:
+            workspace = torch.empty(int(self.lib.dwkv_dense_workspace_bytes(C.byref(self.dims))),
+                                    dtype=torch.uint8, device=self.device)
+        st = self.lib.dwkv_dense_decode(C.byref(self.dims), _ptr(k), _ptr(v), _ptr(q), qt, float(sm_scale or 0.0),
+                                        _ptr(out), _ptr(workspace), workspace.numel(),
+                                        _stream(torch, self.device))
+        binding.check(st, "dwkv_dense_decode")
+        return out
+
     def residual_map(self, layer: int, z: int, kv_head: int, t0: int, t1: int):
         torch = self.torch
         dense = torch.empty((max(t1 - t0, 0), self.head_dim), dtype=torch.float32, device=self.device)

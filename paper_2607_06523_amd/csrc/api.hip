@@ -80,6 +80,18 @@ int plan_split(const dwkv_dims* d) {
   return (int)c;
 }
 
+// Chunk size of the general split kernel alone (the dense decode): about two
+// workgroups per compute unit.
+int plan_split_general(const dwkv_dims* d) {
+  if (d->split_tokens > 0) return d->split_tokens;
+  const int64_t work = d->total_tokens * d->n_kv_heads;
+  int64_t c = (work + kTargetWorkgroups - 1) / kTargetWorkgroups;
+  c = (c + kSplitQuantum - 1) / kSplitQuantum * kSplitQuantum;
+  if (c < kSplitQuantum) c = kSplitQuantum;
+  if (c > kSplitMax) c = kSplitMax;
+  return (int)c;
+}
+
 int64_t count_work(const dwkv_dims* d, int split) {
   int64_t n = 0;
   for (int b = 0; b < d->batch; ++b) {
@@ -466,6 +478,106 @@ dwkv_status dwkv_residual_map(const dwkv_dims* d, const dwkv_cache* c, int32_t l
       c->res_off + ((int64_t)m * Hk + kv_head) * (T + 1), c->res_idx + slab * d->res_stride,
       c->res_val + slab * (d->res_stride / 2), static_cast<const uint16_t*>(c->res_scale) + slab * T,
       t0, t1, d->res_stride, dense, reinterpret_cast<hipStream_t>(stream)));
+}
+
+dwkv_status dwkv_materialize(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, void* k_out,
+                             void* v_out, void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (!c || !c->basis || !c->coef_k || !c->coef_v || !c->res_off || !c->res_idx || !c->res_val ||
+      !c->res_scale || !k_out || !v_out)
+    return DWKV_E_NULL;
+  if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
+  const void* const ptrs[] = {c->basis, c->coef_k, c->coef_v, k_out, v_out};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return DWKV_E_ALIGN;
+  if (reinterpret_cast<uintptr_t>(c->res_scale) & 1u) return DWKV_E_ALIGN;
+  const int64_t T = d->total_tokens, Hk = d->n_kv_heads, rb = d->basis_rank;
+  const int M = d->n_layers / d->window, m = layer / d->window;
+  MatArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.basis = static_cast<const uint16_t*>(c->basis) + (int64_t)m * Hk * 2 * rb * kHeadDim;
+  a.basis_b_stride = (int64_t)M * Hk * 2 * rb * kHeadDim;
+  a.T = T;
+  a.T16 = (T + 15) / 16 * 16;
+  a.coef_k = static_cast<const uint16_t*>(c->coef_k) + (int64_t)layer * Hk * T * rb;
+  a.coef_v = static_cast<const uint16_t*>(c->coef_v) + (int64_t)layer * Hk * a.T16 * rb;
+  a.off = c->res_off + (int64_t)m * Hk * (T + 1);
+  a.idx = c->res_idx + (int64_t)layer * 2 * Hk * d->res_stride;
+  a.val = c->res_val + (int64_t)layer * 2 * Hk * (d->res_stride / 2);
+  a.scale = static_cast<const uint16_t*>(c->res_scale) + (int64_t)layer * 2 * Hk * T;
+  a.cu = d->cu_seqlens;
+  a.k_out = static_cast<uint16_t*>(k_out);
+  a.v_out = static_cast<uint16_t*>(v_out);
+  a.res_stride = d->res_stride;
+  a.batch = d->batch;
+  a.n_kv_heads = d->n_kv_heads;
+  a.rb = d->basis_rank;
+  return hip_status(launch_materialize(a, reinterpret_cast<hipStream_t>(stream)));
+}
+
+size_t dwkv_dense_workspace_bytes(const dwkv_dims* d) {
+  if (check_dims(d) != DWKV_OK) return 0;
+  const int split = plan_split_general(d);
+  const int64_t nw = count_work(d, split);
+  const size_t n = align_up((size_t)nw * d->n_kv_heads * (d->n_q_heads / d->n_kv_heads) * kPartStride *
+                                sizeof(float), 256);
+  return n > 0 ? n : 256;
+}
+
+dwkv_status dwkv_dense_decode(const dwkv_dims* d, const void* k, const void* v, const void* q,
+                              int32_t q_type, float sm_scale, float* out, void* workspace,
+                              size_t ws_bytes, void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (!k || !v || !q || !out || !workspace) return DWKV_E_NULL;
+  if (q_type != DWKV_F16 && q_type != DWKV_BF16) return DWKV_E_DIMS;
+  const void* const ptrs[] = {k, v, q, out, workspace};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return DWKV_E_ALIGN;
+  if (ws_bytes < dwkv_dense_workspace_bytes(d)) return DWKV_E_WORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int split = plan_split_general(d);
+  const int64_t nw = count_work(d, split);
+  if (nw > 0x7fffffff) return DWKV_E_UNSUPPORTED;
+  if (!(sm_scale > 0.f)) sm_scale = 1.0f / std::sqrt((float)kHeadDim);
+  if (nw > 0) {
+    SplitArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.coef_k = static_cast<const uint16_t*>(k);
+    a.coef_v = static_cast<const uint16_t*>(v);
+    a.q = static_cast<const uint16_t*>(q);
+    a.cu = d->cu_seqlens;
+    a.part = static_cast<float*>(workspace);
+    a.T = d->total_tokens;
+    a.batch = d->batch;
+    a.n_q_heads = d->n_q_heads;
+    a.n_kv_heads = d->n_kv_heads;
+    a.n_slots = d->n_kv_heads;
+    a.split = split;
+    a.n_work = (int32_t)nw;
+    a.q_bf16 = q_type == DWKV_BF16;
+    a.qscale = sm_scale * 1.4426950408889634f;
+    for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
+    a.wt = work_table(d, split);
+    if (launch_split(kHeadDim, d->n_q_heads / d->n_kv_heads, false, true, a, (int)nw, s) != hipSuccess)
+      return DWKV_E_HIP;
+  }
+  MergeArgs mg;
+  std::memset(&mg, 0, sizeof(mg));
+  mg.part = static_cast<const float*>(workspace);
+  mg.out = out;
+  mg.cu = d->cu_seqlens;
+  mg.batch = d->batch;
+  mg.n_q_heads = d->n_q_heads;
+  mg.n_kv_heads = d->n_kv_heads;
+  mg.split = split;
+  mg.wt = work_table(d, split);
+  mg.tl = 0;
+  mg.n_work = (int32_t)nw;
+  mg.rb = kHeadDim;
+  for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) mg.probe_slot_of_kv[h] = -1;
+  return hip_status(launch_merge(mg, s));
 }
 
 size_t dwkv_validate_workspace_bytes(void) { return 256; }

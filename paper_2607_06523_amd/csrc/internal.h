@@ -193,6 +193,24 @@ hipError_t launch_merge_tl(int rb, int g, const SplitArgs& a, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, int n_mh, hipStream_t s);
 hipError_t launch_compress(const CompressArgs& a, hipStream_t s);
+
+// Materialization of one layer's rebuilt keys and values (Eq. 1) as fp16.
+struct MatArgs {
+  const uint16_t* basis;       // window m, sequence 0; sequence b adds b*basis_b_stride, (h, z) add (h*2+z)*rb*d
+  int64_t basis_b_stride;
+  const uint16_t* coef_k;      // layer's [Hkv][T][rb]
+  const uint16_t* coef_v;      // layer's [Hkv][T16/16][rb][16]
+  const uint32_t* off;         // window's [Hkv][T+1]
+  const uint8_t* idx;          // layer's [2][Hkv][res_stride]
+  const uint8_t* val;          // layer's [2][Hkv][res_stride/2]
+  const uint16_t* scale;       // layer's [2][Hkv][T]
+  const int32_t* cu;           // device cu_seqlens
+  uint16_t* k_out;             // [Hkv][T][d]
+  uint16_t* v_out;             // [Hkv][T16/16][d][16]
+  int64_t T, T16, res_stride;
+  int32_t batch, n_kv_heads, rb;
+};
+hipError_t launch_materialize(const MatArgs& a, hipStream_t s);
 hipError_t launch_residual_map(const uint32_t* off, const uint8_t* idx, const uint8_t* val,
                                const uint16_t* scale, int64_t t0, int64_t t1, int64_t slab_len,
                                float* dense, hipStream_t s);

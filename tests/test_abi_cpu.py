@@ -224,3 +224,25 @@ def test_route_range_and_compress_argument_checks(lib):
     assert cp(cache=c3) == 1
     d2, keep2 = dims(head_dim=64)
     assert lib.dwkv_compress(C.byref(d2), C.byref(c), 0, FAKE, FAKE, None, 0, 1, None) == 3
+
+
+def test_materialize_and_dense_argument_checks(lib):
+    from paper_2607_06523_amd import binding
+    d, keep = dims()
+    c = binding.Cache(*([FAKE] * 8))
+    assert lib.dwkv_materialize(C.byref(d), C.byref(c), 4, FAKE, FAKE, None) == 2
+    assert lib.dwkv_materialize(C.byref(d), C.byref(c), 0, 0, FAKE, None) == 1
+    assert lib.dwkv_materialize(C.byref(d), C.byref(c), 0, FAKE, FAKE + 8, None) == 7
+    c.res_scale = FAKE + 1
+    assert lib.dwkv_materialize(C.byref(d), C.byref(c), 0, FAKE, FAKE, None) == 7
+    need = lib.dwkv_dense_workspace_bytes(C.byref(d))
+    # general-kernel chunks: ceil(T*Hkv/512) rounded to 256 -> 256; (4 + 8) chunks x 2 heads x 4 x 132 floats
+    assert need == up256((4 + 8) * 2 * 4 * 132 * 4)
+    dd = lambda **kw: lib.dwkv_dense_decode(C.byref(d), kw.get("k", FAKE), FAKE, FAKE, kw.get("qt", 0), 0.0,
+                                            kw.get("out", FAKE), FAKE, kw.get("ws", need), None)
+    assert dd(ws=need - 1) == 4
+    assert dd(k=0) == 1
+    assert dd(qt=3) == 2
+    assert dd(out=FAKE + 4) == 7
+    d2, keep2 = dims(n_q_heads=7)
+    assert lib.dwkv_dense_workspace_bytes(C.byref(d2)) == 0
