@@ -22,7 +22,9 @@ says what disagreed.  The pins are:
   the float32 decision path in exact rational arithmetic, enumeration of the
   kept channels, float64 error bounds with an orthonormal basis, the rebuilt
   Eq. 1 vectors after writing into the layout, and range routing against a
-  running loop.
+  running loop;
+* the router's attention features: per-sequence masses summing to G, spike
+  below mass below G spike, uniform and ln-3 closed forms, the table fold.
 """
 from __future__ import annotations
 
@@ -947,10 +949,58 @@ def pin_route_range(o):
     return None
 
 
+def pin_attention_features(o):
+    """Mass and spike of the decode's own probabilities: a sequence's masses sum
+    to G (each head's probabilities sum to one), spike <= mass <= G spike; a
+    zero query spreads 1/T_b over every token; two tokens whose scores differ
+    by ln 3 get 1/4 and 3/4 per head; the table folds sums and maxima."""
+    OF = o.features
+    c = small_cache(levels=(0, 2, 4), probs=(0.4, 0.3, 0.3), context=9, ragged=(0, 9), batch=4)
+    G = c.n_q_heads // c.n_kv_heads
+    for layer in range(c.n_layers):
+        mass, spike = OF.attention_features(c, layer)
+        for b in range(c.batch):
+            t0, t1 = int(c.cu_seqlens[b]), int(c.cu_seqlens[b + 1])
+            for h in range(c.n_kv_heads):
+                if t1 > t0 and abs(mass[h, t0:t1].sum() - G) > 1e-9:
+                    return f"masses of sequence {b}, head {h} sum to {mass[h, t0:t1].sum()}, not G = {G}"
+                if np.any(spike[h, t0:t1] > mass[h, t0:t1] + 1e-15) or \
+                        np.any(mass[h, t0:t1] > G * spike[h, t0:t1] + 1e-12):
+                    return "spike and mass out of order"
+        q0 = np.zeros((c.batch, c.n_q_heads, c.head_dim))
+        mass0, spike0 = OF.attention_features(c, layer, q=q0)
+        for b in range(c.batch):
+            t0, t1 = int(c.cu_seqlens[b]), int(c.cu_seqlens[b + 1])
+            if t1 > t0 and (not np.allclose(mass0[:, t0:t1], G / (t1 - t0), rtol=0, atol=1e-12)
+                            or not np.allclose(spike0[:, t0:t1], 1.0 / (t1 - t0), rtol=0, atol=1e-12)):
+                return "a zero query must give mass G/T_b and spike 1/T_b"
+    # two tokens, one-hot coefficients over a permutation basis: scores 0 and ln 3
+    c2 = small_cache(levels=(0,), probs=(1.0,), context=2, ragged=None, batch=1, basis_rank=4)
+    zero_coefs(c2)
+    for z in range(2):
+        c2.basis[0, 0, 0, z] = 0
+        c2.basis[0, 0, 0, z, 0, 0] = 1.0
+    coef_set(c2, 0, 0, 0, 1, 0, 1.0)
+    q = np.zeros((1, c2.n_q_heads, c2.head_dim))
+    q[0, :, 0] = np.log(3.0) * np.sqrt(c2.head_dim)
+    mass2, spike2 = OF.attention_features(c2, 0, q=q)
+    G2 = c2.n_q_heads // c2.n_kv_heads
+    if not (np.allclose(mass2[0], [G2 / 4, 3 * G2 / 4], atol=1e-12) and np.allclose(spike2[0], [0.25, 0.75], atol=1e-12)):
+        return f"ln 3 score gap must give 1/4, 3/4 per head, got mass {mass2[0]}, spike {spike2[0]}"
+    phi = np.zeros((1, 1, 2, 4))
+    phi[0, 0, :, 1] = [0.5, 0.1]
+    phi[0, 0, :, 2:] = 7.0
+    OF.update_features(phi, 0, np.array([[0.2, 0.3]]), np.array([[0.4, 0.2]]))
+    OF.update_features(phi, 0, np.array([[0.1, 0.1]]), np.array([[0.1, 0.6]]))
+    if not np.allclose(phi[0, 0], [[0.3, 0.5, 7, 7], [0.4, 0.6, 7, 7]]):
+        return f"feature table must add masses and keep maxima, got {phi[0, 0]}"
+    return None
+
+
 ALL_PINS = [pin_query_formats, pin_nibbles, pin_residual_map, pin_brute_force, pin_closed_forms,
             pin_reductions, pin_invariants, pin_probe, pin_router, pin_compress_closed_forms,
             pin_compress_rne_table, pin_compress_arithmetic, pin_compress_bounds,
-            pin_compress_into_cache, pin_route_range]
+            pin_compress_into_cache, pin_route_range, pin_attention_features]
 
 
 def run_all(o):

@@ -8,6 +8,7 @@ import oracle
 import oracle.factorized as F
 import oracle.router as R
 import oracle.compress as CP
+import oracle.features as FE
 import pins
 
 _orig_reconstruct = F.reconstruct
@@ -191,6 +192,35 @@ def _route_range_from_zero(phi, u, theta, levels, t0, t1, codes, off):
     return R.__dict__["_orig_route_range"](phi, u, theta, levels, t0, t1, codes, off)
 
 
+def _features_variant(kind):
+    def feat(cache, layer, q=None, sm_scale=None):
+        _, probs = F.decode(cache, layer, q, sm_scale, with_probs=True)
+        Hk, T = cache.n_kv_heads, int(cache.cu_seqlens[-1])
+        mass, spike = np.zeros((Hk, T)), np.zeros((Hk, T))
+        for (b, h), p in probs.items():
+            t0, t1 = int(cache.cu_seqlens[b]), int(cache.cu_seqlens[b + 1])
+            if t1 > t0:
+                if kind == "mean":
+                    mass[h, t0:t1] = p.mean(axis=0)
+                else:
+                    mass[h, t0:t1] = p.sum(axis=0)
+                spike[h, t0:t1] = p.sum(axis=0) if kind == "spike_sum" else p.max(axis=0)
+        return mass, spike
+    return feat
+
+
+def _update_overwrite(phi, window, mass, spike):
+    phi[window, :, :, 0] = mass
+    phi[window, :, :, 1] = np.maximum(phi[window, :, :, 1], spike)
+    return phi
+
+
+def _update_spike_last(phi, window, mass, spike):
+    phi[window, :, :, 0] += mass
+    phi[window, :, :, 1] = spike
+    return phi
+
+
 MUTANTS = {
     "residual dropped": [(F, "reconstruct", _reconstruct_variant("no_residual"))],
     "residual sign flipped": [(F, "reconstruct", _reconstruct_variant("residual_sign"))],
@@ -237,6 +267,10 @@ MUTANTS = {
     "value coefficients written row-major": [(CP, "store_coefficients", _store_values_row_major)],
     "entries written at the next token's offset": [(CP, "store_entries", _store_entries_at_next)],
     "range routing restarts the offsets at zero": [(R, "route_range", _route_range_from_zero)],
+    "attention mass averaged over heads": [(FE, "attention_features", _features_variant("mean"))],
+    "attention spike summed over heads": [(FE, "attention_features", _features_variant("spike_sum"))],
+    "feature mass overwritten instead of accumulated": [(FE, "update_features", _update_overwrite)],
+    "feature spike keeps the last value": [(FE, "update_features", _update_spike_last)],
     "bf16 query read as fp16": [(F, "q_to_f64", lambda bits, dtype: np.asarray(bits, np.uint16)
                                  .view(np.float16).astype(np.float64))],
 }
