@@ -139,6 +139,36 @@ def measure_append(dc, host, wl, torch, reps: int = 20):
                     "(graph replay); prefill = dwkv_compress of all T tokens of one layer, K and V"}
 
 
+def measure_features(dc, host, torch, outs, steps: int = 5):
+    """A decode step that also emits the router's attention features
+    (dwkv_decode_features per layer: the scores-storing split pass, the merge
+    and the normalizing features launch), against the plain decode step."""
+    import ctypes
+    L = host.n_layers
+    phi = torch.zeros((host.n_windows, host.n_kv_heads, host.total_tokens, 4), dtype=torch.float32, device="cuda")
+    ws = torch.empty(int(dc.lib.dwkv_features_workspace_bytes(ctypes.byref(dc.dims))), dtype=torch.uint8,
+                     device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        for l in range(L):
+            dc.decode_features(l, phi, out=outs[l], workspace=ws)
+
+    step()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record(stream)
+    for _ in range(steps):
+        step()
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / steps
+    return {"tokens_per_s": round(host.batch / (ms / 1e3), 2), "ms_per_step": round(ms, 4),
+            "launches_per_layer": 3,
+            "note": "dwkv_decode_features per layer: decode plus per-token attention mass and spike folded "
+                    "into the window's router features"}
+
+
 def measure_comparators(dc, host, torch, steps: int = 3):
     """The decode's comparison paths on the same GPU and workload: a dense fp16
     cache decode (every layer's K/V resident, 2 bytes per element) and the
@@ -355,6 +385,9 @@ def main():
         "kv_token_layers_per_s": round(host.total_tokens * L / (ms_per_step / 1e3), 1),
         "wall_s_timed": round(wall, 3),
     }
+    if not args.no_comparators and args.variant == "full":
+        log("[bench] timing the decode with router features")
+        result["with_features"] = measure_features(dc, host, torch, outs)
     if not args.no_append and args.variant == "full":
         log("[bench] timing the append/compress path")
         result["append"] = measure_append(dc, host, wl, torch)

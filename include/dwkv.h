@@ -233,6 +233,28 @@ dwkv_status dwkv_residual_map(const dwkv_dims* dims, const dwkv_cache* cache, in
                               int32_t z, int32_t kv_head, int64_t t0, int64_t t1,
                               float* dense, void* stream);
 
+/* Bytes of device workspace dwkv_decode_features needs (0 when the dims are
+ * invalid or the shape is not on the token-lane path: G = Hq/Hkv in {1, 2, 4},
+ * r_b <= 64, levels <= 16). */
+size_t dwkv_features_workspace_bytes(const dwkv_dims* dims);
+
+/* dwkv_decode (no probe), plus the attention features the router reads
+ * (Sec. 3: accumulated attention mass, maximum attention spike).  With p the
+ * softmax probability of token t for query head hq at this layer:
+ *   phi[m][h][t][0] += sum over the query heads hq of KV head h of p
+ *   phi[m][h][t][1]  = max(phi[m][h][t][1], max over those heads of p)
+ * for every packed token t of every sequence, m = layer / window; columns 2
+ * and 3 are untouched.  Calling it for every layer of a window and every
+ * decode step accumulates the features over both.
+ *   phi: fp32 [M][Hkv][T][4] (the layout dwkv_route reads), read and written
+ *   workspace: >= dwkv_features_workspace_bytes(dims) bytes, no initial contents
+ * `out` equals dwkv_decode's bit for bit.  Three launches (split-K pass that
+ * also stores the scores, merge, features).  DWKV_E_UNSUPPORTED off the
+ * token-lane path. */
+dwkv_status dwkv_decode_features(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
+                                 const void* q, int32_t q_type, float sm_scale, float* out, float* phi,
+                                 void* workspace, size_t ws_bytes, void* stream);
+
 /* Comparison paths (the fused decode's alternatives: the paper's "full KV"
  * baseline and its "w/o fused kernel" ablation, Table 1 and Table 2).
  *

@@ -239,6 +239,26 @@ class DeviceCache:
                                     _ptr(gate), int(t0), int(t1), _stream(torch, self.device))
         binding.check(st, "dwkv_compress")
 
+    def decode_features(self, layer: int, phi, q=None, sm_scale: float | None = None, out=None, workspace=None):
+        """dwkv_decode plus the router's attention features: phi fp32 [M, Hkv, T, 4]
+        (columns 0 mass, 1 spike) is updated in place; returns out [B, Hq, d]."""
+        torch = self.torch
+        if q is None:
+            q = self.q[layer]
+        qt = F16 if q.dtype == torch.float16 else BF16
+        if out is None:
+            out = torch.empty((self.batch, self.n_q_heads, self.head_dim), dtype=torch.float32, device=self.device)
+        if workspace is None:
+            n = int(self.lib.dwkv_features_workspace_bytes(C.byref(self.dims)))
+            if n == 0:
+                raise DwkvError(3, "dwkv_features_workspace_bytes")
+            workspace = torch.empty(n, dtype=torch.uint8, device=self.device)
+        st = self.lib.dwkv_decode_features(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(q), qt,
+                                           float(sm_scale or 0.0), _ptr(out), _ptr(phi), _ptr(workspace),
+                                           workspace.numel(), _stream(torch, self.device))
+        binding.check(st, "dwkv_decode_features")
+        return out
+
     def materialize(self, layer: int, k_out=None, v_out=None):
         """Eq. 1 written out for `layer`: K_hat fp16 [Hkv, T, d] and V_hat fp16
         [Hkv, T16/16, d, 16] (the blocked layout of the dense decode)."""

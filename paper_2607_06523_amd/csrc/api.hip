@@ -202,7 +202,7 @@ dwkv_status check_decode_common(const dwkv_dims* d, const dwkv_probe* probe, voi
 // Split-K pass(es): partial (o, m, l) per (work item, head slot, group member).
 dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
                            int32_t q_type, float sm_scale, const dwkv_probe* probe, void* workspace,
-                           hipStream_t s) {
+                           hipStream_t s, float* scores = nullptr) {
   if (!c || !q) return DWKV_E_NULL;
   if (!c->basis || !c->coef_k || !c->coef_v || !c->res_off || !c->res_idx || !c->res_val ||
       !c->res_scale)
@@ -256,8 +256,10 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   a.qscale = sm_scale * 1.4426950408889634f;
   for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
   a.wt = work_table(d, split);
+  a.scores = scores;
   const hipError_t e = uses_token_lane(d)
-                           ? launch_split_tl(RB, G, max_level(d) > 0, a, (int)nw, s)
+                           ? (scores ? launch_split_tl_scores(RB, G, max_level(d) > 0, a, (int)nw, s)
+                                     : launch_split_tl(RB, G, max_level(d) > 0, a, (int)nw, s))
                            : launch_split(RB, G, max_level(d) > 0, false, a, (int)nw, s);
   if (e != hipSuccess) return DWKV_E_HIP;
   if (probe) {
@@ -578,6 +580,43 @@ dwkv_status dwkv_dense_decode(const dwkv_dims* d, const void* k, const void* v, 
   mg.rb = kHeadDim;
   for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) mg.probe_slot_of_kv[h] = -1;
   return hip_status(launch_merge(mg, s));
+}
+
+size_t dwkv_features_workspace_bytes(const dwkv_dims* d) {
+  if (check_dims(d) != DWKV_OK || !uses_token_lane(d)) return 0;
+  const size_t sc = align_up((size_t)d->n_q_heads * (size_t)d->total_tokens * sizeof(float), 256);
+  return ws_layout(d, nullptr).total + sc;
+}
+
+dwkv_status dwkv_decode_features(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
+                                 int32_t q_type, float sm_scale, float* out, float* phi, void* workspace,
+                                 size_t ws_bytes, void* stream) {
+  dwkv_status st = check_decode_common(d, nullptr, workspace, ws_bytes);
+  if (st != DWKV_OK) return st;
+  if (!uses_token_lane(d)) return DWKV_E_UNSUPPORTED;
+  if (!out || !phi) return DWKV_E_NULL;
+  if (!aligned16(out) || !aligned16(phi)) return DWKV_E_ALIGN;
+  if (ws_bytes < dwkv_features_workspace_bytes(d)) return DWKV_E_WORKSPACE;
+  if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  float* scores = reinterpret_cast<float*>(ws + ws_layout(d, nullptr).total);
+  if ((st = partials_phase(d, c, layer, q, q_type, sm_scale, nullptr, workspace, s, scores)) != DWKV_OK) return st;
+  if ((st = merge_phase(d, c, layer, out, nullptr, workspace, s)) != DWKV_OK) return st;
+  const int split = plan_split(d);
+  FeatArgs f;
+  std::memset(&f, 0, sizeof(f));
+  f.part = reinterpret_cast<const float*>(ws);
+  f.scores = scores;
+  f.phi = phi + (int64_t)(layer / d->window) * d->n_kv_heads * d->total_tokens * 4;
+  f.cu = d->cu_seqlens;
+  f.wt = work_table(d, split);
+  f.T = d->total_tokens;
+  f.batch = d->batch;
+  f.n_kv_heads = d->n_kv_heads;
+  f.split = split;
+  f.n_work = (int32_t)count_work(d, split);
+  return hip_status(launch_features(d->n_q_heads / d->n_kv_heads, f, s));
 }
 
 size_t dwkv_validate_workspace_bytes(void) { return 256; }

@@ -126,6 +126,7 @@ struct TCtx {
   rsrc_t idx[2], val[2];                // residual channel bytes and code bytes (K, V)
   int32_t c0, c1, tb;                   // chunk [c0, c1); tiles start at tb = c0 & ~15
   int32_t ntile;
+  float* sco;                           // raw scores of this slot [T][G] (score-storing pass only)
 };
 
 __device__ __forceinline__ f4 mfma16(h4 a, h4 b, f4 c) {
@@ -299,7 +300,7 @@ __device__ __forceinline__ void pv_tile(f4& acc_h, f4& acc_l, h4 ph, h4 pl, cons
   (pv_quad<Q>(acc_h, acc_l, ph, pl, v[Q]), ...);
 }
 
-template <int RB, int G, bool RESID>
+template <int RB, int G, bool RESID, bool SCORES>
 __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc, TMeta& mn, TMeta& mnn,
                                       TEnt& ec, TEnt& en, int j, int jn, int jnn, const TCtx& x,
                                       TSmem<RB, RESID>& sm, int wv, int lane) {
@@ -421,6 +422,14 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
     const bool valid = t >= x.c0 && t < x.c1;
 #pragma unroll
     for (int i = 0; i < HG; ++i) sc[i] = (valid && i < G) ? sc[i] : -INFINITY;
+    if constexpr (SCORES) {             // the token's scores, for the attention-mass features
+      if (valid) {
+        float* dst = x.sco + (int64_t)t * G;
+        if constexpr (G == 4) *reinterpret_cast<f4*>(dst) = f4{sc[0], sc[1], sc[2], sc[3]};
+        else if constexpr (G == 2) *reinterpret_cast<float2*>(dst) = make_float2(sc[0], sc[1]);
+        else dst[0] = sc[0];
+      }
+    }
   }
 
   // 4. softmax against the lazily moved reference
@@ -649,7 +658,7 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const SplitArgs a
   }
 }
 
-template <int RB, int G, bool RESID>
+template <int RB, int G, bool RESID, bool SCORES>
 __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   using C = TCfg<RB>;
   constexpr int NS = C::NS;
@@ -674,6 +683,7 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   }
   x.tb = x.c0 & ~15;
   x.ntile = (x.c1 - x.tb + TT - 1) / TT;
+  x.sco = SCORES ? a.scores + (int64_t)slot * a.T * G : nullptr;
   {
     const int64_t T = a.T, nblk = (T + 15) / 16, rs = a.res_stride;
     x.ck = make_rsrc(a.coef_k + (int64_t)slot * T * RB, (uint32_t)(T * RB * 2));
@@ -845,7 +855,7 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   // tiles wv, wv + 8, wv + 16, ...: a fixed assignment keeps the summation
   // order, and so the result, independent of timing
   for (int j = wv; j < x.ntile; j += kTW)
-    tstep<RB, G, RESID>(st, fr, mc, mn, mnn, ec, en, j, j + kTW, j + 2 * kTW, x, sm, wv, lane);
+    tstep<RB, G, RESID, SCORES>(st, fr, mc, mn, mnn, ec, en, j, j + kTW, j + 2 * kTW, x, sm, wv, lane);
 
   // epilogue: the waves combine; the partial keeps a~ in basis space (the
   // merge projects it through B^V once per sequence and head).  Each wave
@@ -915,29 +925,29 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   }
 }
 
-template <int RB, int G, bool R>
+template <int RB, int G, bool R, bool S>
 hipError_t launch_tl_t(const SplitArgs& a, int n_work, hipStream_t s) {
-  hipLaunchKernelGGL((tl_kernel<RB, G, R>), dim3(n_work, a.n_slots), dim3(kTThreads), 0, s, a);
+  hipLaunchKernelGGL((tl_kernel<RB, G, R, S>), dim3(n_work, a.n_slots), dim3(kTThreads), 0, s, a);
   return hipGetLastError();
 }
 
-template <int RB, bool R>
+template <int RB, bool R, bool S>
 hipError_t launch_tl_g(int g, const SplitArgs& a, int n_work, hipStream_t s) {
   switch (g) {
-    case 1: return launch_tl_t<RB, 1, R>(a, n_work, s);
-    case 2: return launch_tl_t<RB, 2, R>(a, n_work, s);
-    case 4: return launch_tl_t<RB, 4, R>(a, n_work, s);
+    case 1: return launch_tl_t<RB, 1, R, S>(a, n_work, s);
+    case 2: return launch_tl_t<RB, 2, R, S>(a, n_work, s);
+    case 4: return launch_tl_t<RB, 4, R, S>(a, n_work, s);
   }
   return hipErrorInvalidValue;
 }
 
-template <bool R>
+template <bool R, bool S>
 hipError_t launch_tl_rb(int rb, int g, const SplitArgs& a, int n_work, hipStream_t s) {
   switch (rb) {
-    case 16: return launch_tl_g<16, R>(g, a, n_work, s);
-    case 32: return launch_tl_g<32, R>(g, a, n_work, s);
-    case 48: return launch_tl_g<48, R>(g, a, n_work, s);
-    case 64: return launch_tl_g<64, R>(g, a, n_work, s);
+    case 16: return launch_tl_g<16, R, S>(g, a, n_work, s);
+    case 32: return launch_tl_g<32, R, S>(g, a, n_work, s);
+    case 48: return launch_tl_g<48, R, S>(g, a, n_work, s);
+    case 64: return launch_tl_g<64, R, S>(g, a, n_work, s);
   }
   return hipErrorInvalidValue;
 }
@@ -964,7 +974,11 @@ bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t 
 }
 
 hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {
-  return resid ? launch_tl_rb<true>(rb, g, a, n_work, s) : launch_tl_rb<false>(rb, g, a, n_work, s);
+  return resid ? launch_tl_rb<true, false>(rb, g, a, n_work, s) : launch_tl_rb<false, false>(rb, g, a, n_work, s);
+}
+
+hipError_t launch_split_tl_scores(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {
+  return resid ? launch_tl_rb<true, true>(rb, g, a, n_work, s) : launch_tl_rb<false, true>(rb, g, a, n_work, s);
 }
 
 hipError_t launch_merge_tl(int rb, int g, const SplitArgs& a, hipStream_t s) {

@@ -1,0 +1,87 @@
+// Router features from the decode (Sec. 3: the router scores a token by,
+// among others, its accumulated attention mass and its maximum attention
+// spike).  After a decode pass that stored every token's raw scores, this
+// launch normalizes them with the merged softmax statistics of its sequence
+// and query head, p = 2^(s - m*) / l*, and folds one layer's contribution into
+// the window's feature table:
+//   phi[t][0] += sum over the KV head's query heads of p
+//   phi[t][1]  = max(phi[t][1], max over those heads of p)
+// One workgroup per 256 packed tokens of one KV head; m* and l* of each
+// sequence come from the split partials (m, l of every chunk).
+#include "internal.h"
+
+namespace dwkv {
+namespace {
+
+constexpr int kFT = 256;                 // tokens (threads) per workgroup
+
+__device__ __forceinline__ int seq_at(const int32_t* cu, int batch, int64_t t) {
+  int lo = 0, hi = batch;                // cu[lo] <= t < cu[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if ((int64_t)cu[mid] <= t) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+template <int G>
+__global__ __launch_bounds__(kFT) void features_kernel(const FeatArgs a) {
+  __shared__ float mstar[G], linv[G];
+  const int h = blockIdx.y, tid = threadIdx.x;
+  const int64_t g0 = (int64_t)blockIdx.x * kFT;
+  const int64_t gend = min(g0 + (int64_t)kFT, a.T);
+  const int64_t t = g0 + tid;
+  float s[G];
+  if (t < gend) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) s[g] = a.scores[((int64_t)h * a.T + t) * G + g];
+  }
+  for (int b = seq_at(a.cu, a.batch, g0); b < a.batch && (int64_t)a.cu[b] < gend; ++b) {
+    const int64_t s0 = max(g0, (int64_t)a.cu[b]), s1 = min(gend, (int64_t)a.cu[b + 1]);
+    if (s1 <= s0) continue;              // empty sequence (uniform)
+    __syncthreads();                     // the previous sequence's statistics are read
+    if (tid < G) {                       // merged softmax statistics of (b, h, head tid)
+      int base, ns;
+      seq_work(a.wt, a.cu, a.split, b, base, ns);
+      const float* pr = a.part + ((int64_t)h * a.n_work + base) * G * kPartStrideTL + (int64_t)tid * kPartStrideTL;
+      float m = -INFINITY;
+      for (int i = 0; i < ns; ++i) m = fmaxf(m, pr[(int64_t)i * G * kPartStrideTL + kPartTLM]);
+      float l = 0.f;
+      for (int i = 0; i < ns; ++i) {
+        const float* r = pr + (int64_t)i * G * kPartStrideTL;
+        l += exp2f(r[kPartTLM] - m) * r[kPartTLM + 1];
+      }
+      mstar[tid] = m;
+      linv[tid] = 1.0f / l;
+    }
+    __syncthreads();
+    if (t >= s0 && t < s1) {
+      float mass = 0.f, spike = 0.f;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float p = exp2f(s[g] - mstar[g]) * linv[g];
+        mass += p;
+        spike = fmaxf(spike, p);
+      }
+      float* f = a.phi + ((int64_t)h * a.T + t) * 4;
+      f[0] += mass;
+      f[1] = fmaxf(f[1], spike);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_features(int g, const FeatArgs& a, hipStream_t s) {
+  if (a.T <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((a.T + kFT - 1) / kFT), a.n_kv_heads);
+  switch (g) {
+    case 1: hipLaunchKernelGGL(features_kernel<1>, grid, dim3(kFT), 0, s, a); break;
+    case 2: hipLaunchKernelGGL(features_kernel<2>, grid, dim3(kFT), 0, s, a); break;
+    case 4: hipLaunchKernelGGL(features_kernel<4>, grid, dim3(kFT), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace dwkv

@@ -49,6 +49,7 @@ struct SplitArgs {
   const int32_t* cu;           // [B+1] device
   float* part;                 // [work][n_slots][G][kPartStride]; token-lane: [n_slots][work][G][kPartStrideTL]
   float* out;                  // [B][Hq][d], written by the token-lane merge launch
+  float* scores;               // [n_slots][T][G] raw scores in exp2 units (token-lane pass with scores only)
   int64_t T;
   int64_t res_stride;
   int32_t batch;
@@ -187,6 +188,9 @@ hipError_t launch_split(int rb, int g, bool resid, bool ident, const SplitArgs& 
 // ranks 16..64, at most 16 residual entries per token); same partials.
 bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t res_stride);
 hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s);
+// The same pass that also stores every token's raw scores (a.scores), for the
+// attention-mass features.
+hipError_t launch_split_tl_scores(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s);
 // Token-lane merge: reads a.part, writes a.out (one workgroup per slot, head
 // and 16 output channels).
 hipError_t launch_merge_tl(int rb, int g, const SplitArgs& a, hipStream_t s);
@@ -211,6 +215,18 @@ struct MatArgs {
   int32_t batch, n_kv_heads, rb;
 };
 hipError_t launch_materialize(const MatArgs& a, hipStream_t s);
+
+// Attention-mass features of one decode (token-lane partials and stored scores).
+struct FeatArgs {
+  const float* part;           // token-lane partials [Hkv][n_work][G][kPartStrideTL]
+  const float* scores;         // [Hkv][T][G] raw scores (exp2 units)
+  float* phi;                  // the window's features [Hkv][T][4] (columns 0, 1 updated)
+  const int32_t* cu;           // device cu_seqlens
+  WorkTable wt;
+  int64_t T;
+  int32_t batch, n_kv_heads, split, n_work;
+};
+hipError_t launch_features(int g, const FeatArgs& a, hipStream_t s);
 hipError_t launch_residual_map(const uint32_t* off, const uint8_t* idx, const uint8_t* val,
                                const uint16_t* scale, int64_t t0, int64_t t1, int64_t slab_len,
                                float* dense, hipStream_t s);

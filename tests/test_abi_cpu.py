@@ -246,3 +246,22 @@ def test_materialize_and_dense_argument_checks(lib):
     assert dd(out=FAKE + 4) == 7
     d2, keep2 = dims(n_q_heads=7)
     assert lib.dwkv_dense_workspace_bytes(C.byref(d2)) == 0
+
+
+def test_features_argument_checks(lib):
+    from paper_2607_06523_amd import binding
+    d, keep = dims()                          # groups of 4, r_b 32, ranks <= 16: token-lane path
+    base = lib.dwkv_workspace_bytes(C.byref(d), None)
+    need = lib.dwkv_features_workspace_bytes(C.byref(d))
+    assert need == base + up256(8 * 3000 * 4)
+    d8, keep8 = dims(n_q_heads=16)            # groups of 8: general kernel, no features
+    assert lib.dwkv_features_workspace_bytes(C.byref(d8)) == 0
+    c = binding.Cache(*([FAKE] * 8))
+    f = lambda dd=d, **kw: lib.dwkv_decode_features(C.byref(dd), C.byref(c), kw.get("layer", 0), FAKE, 0, 0.0,
+                                                    kw.get("out", FAKE), kw.get("phi", FAKE), FAKE,
+                                                    kw.get("ws", need), None)
+    assert f(ws=need - 1) == 4
+    assert f(phi=0) == 1
+    assert f(phi=FAKE + 4) == 7
+    assert f(layer=4) == 2
+    assert f(dd=d8, ws=1 << 30) == 3
