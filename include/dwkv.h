@@ -255,6 +255,33 @@ dwkv_status dwkv_decode_features(const dwkv_dims* dims, const dwkv_cache* cache,
                                  const void* q, int32_t q_type, float sm_scale, float* out, float* phi,
                                  void* workspace, size_t ws_bytes, void* stream);
 
+/* Probe-feedback threshold control (Sec. 3): when a window's probe error
+ * (Eq. 3) exceeds its tolerance the router lowers the window's threshold;
+ * after several probe intervals below tolerance it raises it.  The paper
+ * gives no constants; they are the caller's. */
+typedef struct dwkv_controller {
+  float tol;              /* tolerance on the window's probe error               */
+  float step_down;        /* logit step down of every threshold on e > tol (>= 0) */
+  float step_up;          /* logit step up after `patience` intervals (>= 0)     */
+  int32_t patience;       /* consecutive intervals at or below tol before a step up (>= 1) */
+  float theta_min;        /* clamp of every threshold (theta_min <= theta_max)   */
+  float theta_max;
+} dwkv_controller;
+
+/* One probe interval for n_windows windows, on HOST arrays:
+ *   err_host:   [n_windows] the window's probe error (the largest Eq. 3 error
+ *               over its probed layers, heads and sequences); NaN counts as
+ *               above tolerance
+ *   theta_host: [n_windows][n_thresholds] router thresholds on z (logits of
+ *               tau, as dwkv_route reads them), updated in place: every
+ *               threshold of a window moves by the same step (float32), then
+ *               is clamped to [theta_min, theta_max], so their order is kept
+ *   below_host: [n_windows] consecutive intervals at or below tol, updated;
+ *               reset to 0 on every step
+ * Synchronous host code; DWKV_E_DIMS for bad counts or constants. */
+dwkv_status dwkv_controller_update(const dwkv_controller* ctl, int32_t n_windows, int32_t n_thresholds,
+                                   const float* err_host, float* theta_host, int32_t* below_host);
+
 /* Comparison paths (the fused decode's alternatives: the paper's "full KV"
  * baseline and its "w/o fused kernel" ablation, Table 1 and Table 2).
  *

@@ -14,12 +14,13 @@ inputs.
   window basis, routed residual channels, int4 codes, gate-folded scale.
 * ``features``: the router's attention-mass and attention-spike features of a
   decode.
+* ``control``: probe-feedback threshold updates and budget-driven selection.
 
 Every function is pinned by the CPU tests (brute force in exact arithmetic,
 closed forms, reductions to library attention, invariants); none is marked
 "parity unpinned".
 """
-from . import factorized, router, compress, features
+from . import factorized, router, compress, features, control
 from .factorized import (attention, decode, probe, probe_error, reconstruct,
                          residual_map, int4_from_nibble, entry_codes, q_to_f64,
                          default_scale)

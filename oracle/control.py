@@ -1,0 +1,56 @@
+"""Plain reference for the router's threshold control (Sec. 3).
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the library imports or calls this module.
+
+Probe feedback: when a window's probe error (Eq. 3) exceeds its tolerance the
+router lowers the window's threshold, so more tokens get the higher residual
+rank; when the error stays below tolerance for several probe intervals in a
+row it raises the threshold and residual storage shrinks.  The paper gives no
+constants.  Reading used here: thresholds are logits theta = logit(tau) (as the
+router compares them); every threshold of the window moves by the same step
+(down by step_down on an error above tol, up by step_up after `patience`
+consecutive intervals at or below tol), clamped to [theta_min, theta_max]; the
+window's error is the largest Eq. 3 error over its probed layers, heads and
+sequences; an error that is not a number counts as above tolerance; the
+interval counter resets on every move.
+
+Budget: tau_m is chosen to satisfy the memory budget.  Reading used here, for
+the two-level form of Eq. 2 (rho_min, rho_max): with E residual entries
+allowed for the window and head, and N tokens, the n = floor((E - N rho_min) /
+(rho_max - rho_min)) tokens of largest router score z (ties to the lower token
+index; clamped to [0, N]) get rho_max and the rest rho_min.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+
+def controller_update(theta, below, err, tol, step_down, step_up, patience, theta_min, theta_max):
+    """One probe interval: theta [M][n_thr] and below [M] updated in place."""
+    theta = np.asarray(theta)
+    for m in range(theta.shape[0]):
+        e = float(err[m])
+        if math.isnan(e) or e > tol:
+            theta[m] = np.clip(theta[m] - np.float32(step_down), theta_min, theta_max)
+            below[m] = 0
+        else:
+            below[m] += 1
+            if below[m] >= patience:
+                theta[m] = np.clip(theta[m] + np.float32(step_up), theta_min, theta_max)
+                below[m] = 0
+    return theta, below
+
+
+def budget_select(z: np.ndarray, entries: int, rho_min: int, rho_max: int) -> np.ndarray:
+    """Two-level codes (0 = rho_min, 1 = rho_max) for router scores z [N] under a
+    budget of `entries` residual entries: the largest-z tokens first, ties to
+    the lower index."""
+    N = len(z)
+    n = (entries - N * rho_min) // (rho_max - rho_min) if rho_max > rho_min else 0
+    n = max(0, min(N, n))
+    order = sorted(range(N), key=lambda t: (-float(z[t]), t))
+    codes = np.zeros(N, dtype=np.uint8)
+    codes[order[:n]] = 1
+    return codes

@@ -45,6 +45,11 @@ class Cache(C.Structure):
                 ("res_scale", C.c_void_p)]
 
 
+class Controller(C.Structure):
+    _fields_ = [("tol", C.c_float), ("step_down", C.c_float), ("step_up", C.c_float), ("patience", C.c_int32),
+                ("theta_min", C.c_float), ("theta_max", C.c_float)]
+
+
 class Probe(C.Structure):
     _fields_ = [("n_heads", C.c_int32), ("kv_heads_host", C.POINTER(C.c_int32)),
                 ("k_ref", C.c_void_p), ("v_ref", C.c_void_p), ("eps", C.c_float),
@@ -54,7 +59,7 @@ class Probe(C.Structure):
 EXPORTS = ["dwkv_abi_version", "dwkv_status_str", "dwkv_split_tokens", "dwkv_workspace_bytes",
            "dwkv_decode_launches", "dwkv_decode", "dwkv_decode_partials", "dwkv_decode_merge", "dwkv_route_workspace_bytes", "dwkv_route",
            "dwkv_route_range", "dwkv_compress", "dwkv_features_workspace_bytes", "dwkv_decode_features",
-           "dwkv_materialize", "dwkv_dense_workspace_bytes",
+           "dwkv_controller_update", "dwkv_materialize", "dwkv_dense_workspace_bytes",
            "dwkv_dense_decode", "dwkv_residual_map",
            "dwkv_validate_workspace_bytes", "dwkv_validate"]
 
@@ -104,6 +109,9 @@ def load(path: str = LIB_PATH):
     lib.dwkv_decode_features.restype = C.c_int
     lib.dwkv_decode_features.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_void_p, C.c_int32, C.c_float,
                                          C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
+    lib.dwkv_controller_update.restype = C.c_int
+    lib.dwkv_controller_update.argtypes = [P(Controller), C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
+                                           C.c_void_p]
     lib.dwkv_materialize.restype = C.c_int
     lib.dwkv_materialize.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
     lib.dwkv_dense_workspace_bytes.restype = C.c_size_t

@@ -619,6 +619,31 @@ dwkv_status dwkv_decode_features(const dwkv_dims* d, const dwkv_cache* c, int32_
   return hip_status(launch_features(d->n_q_heads / d->n_kv_heads, f, s));
 }
 
+dwkv_status dwkv_controller_update(const dwkv_controller* ctl, int32_t n_windows, int32_t n_thresholds,
+                                   const float* err_host, float* theta_host, int32_t* below_host) {
+  if (!ctl || !err_host || !below_host || (n_thresholds > 0 && !theta_host)) return DWKV_E_NULL;
+  if (n_windows < 0 || n_thresholds < 0 || ctl->patience < 1 || !(ctl->step_down >= 0.f) ||
+      !(ctl->step_up >= 0.f) || !(ctl->theta_min <= ctl->theta_max))
+    return DWKV_E_DIMS;
+  for (int32_t m = 0; m < n_windows; ++m) {
+    const float e = err_host[m];
+    float step = 0.f;
+    if (!(e <= ctl->tol)) {                       // above tolerance, or not a number
+      step = -ctl->step_down;
+      below_host[m] = 0;
+    } else if (++below_host[m] >= ctl->patience) {
+      step = ctl->step_up;
+      below_host[m] = 0;
+    }
+    if (step != 0.f)
+      for (int32_t j = 0; j < n_thresholds; ++j) {
+        float& th = theta_host[(int64_t)m * n_thresholds + j];
+        th = std::min(std::max(th + step, ctl->theta_min), ctl->theta_max);
+      }
+  }
+  return DWKV_OK;
+}
+
 size_t dwkv_validate_workspace_bytes(void) { return 256; }
 
 dwkv_status dwkv_validate(const dwkv_dims* d, const dwkv_cache* c, int64_t* bad_index, void* workspace,

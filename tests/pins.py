@@ -24,7 +24,9 @@ says what disagreed.  The pins are:
   Eq. 1 vectors after writing into the layout, and range routing against a
   running loop;
 * the router's attention features: per-sequence masses summing to G, spike
-  below mass below G spike, uniform and ln-3 closed forms, the table fold.
+  below mass below G spike, uniform and ln-3 closed forms, the table fold;
+* threshold control: a hand-worked feedback trace with clamps, and the
+  budget-driven selection against enumeration of the promoted sets.
 """
 from __future__ import annotations
 
@@ -997,10 +999,51 @@ def pin_attention_features(o):
     return None
 
 
+def pin_control(o):
+    """Threshold feedback on a hand-worked trace (down on an error above
+    tolerance or a NaN, up after `patience` quiet intervals, clamps) and the
+    budget selection against enumeration."""
+    OC = o.control
+    theta = np.array([[0.0, 1.0]], np.float32)
+    below = np.array([0])
+    want = [([-0.5, 0.5], 0), ([-0.5, 0.5], 1), ([-0.5, 0.5], 2), ([-0.25, 0.75], 0), ([-0.75, 0.25], 0),
+            ([-1.25, -0.25], 0)]
+    for e, (th, bl) in zip([0.2, 0.05, 0.1, 0.05, 0.3, float("nan")], want):
+        OC.controller_update(theta, below, [e], 0.1, 0.5, 0.25, 3, -4.0, 4.0)
+        if not (np.allclose(theta[0], th) and below[0] == bl):
+            return f"feedback trace: after error {e} got theta {theta[0]}, below {below[0]}; want {th}, {bl}"
+    theta = np.array([[-3.8, 3.9]], np.float32)
+    below = np.array([2])
+    OC.controller_update(theta, below, [0.0], 0.1, 0.5, 0.25, 3, -4.0, 4.0)
+    if not (np.allclose(theta[0], [-3.55, 4.0]) and below[0] == 0):
+        return f"step up must clamp at theta_max, got {theta[0]}"
+    OC.controller_update(theta, below, [1.0], 0.1, 1.0, 0.25, 3, -4.0, 4.0)
+    if not np.allclose(theta[0], [-4.0, 3.0]):
+        return f"step down must clamp at theta_min, got {theta[0]}"
+    from itertools import combinations
+    z = np.array([0.5, 0.9, 0.5, -1.0, 0.9, 0.5], np.float32)
+    for rmin, rmax in ((0, 8), (2, 8), (4, 16)):
+        for E in range(0, 6 * rmax + 3):
+            got = OC.budget_select(z, E, rmin, rmax)
+            # enumeration: the largest promoted set within the budget whose
+            # members all beat every other token (larger z, or equal z and lower index)
+            best = ()
+            for n in range(len(z) + 1):
+                if len(z) * rmin + n * (rmax - rmin) > E:
+                    break
+                for sub in combinations(range(len(z)), n):
+                    rest = [t for t in range(len(z)) if t not in sub]
+                    if all(z[a] > z[b] or (z[a] == z[b] and a < b) for a in sub for b in rest):
+                        best = sub
+            if [int(t) for t in np.nonzero(got)[0]] != sorted(best):
+                return f"budget {E} at levels ({rmin}, {rmax}): promoted {np.nonzero(got)[0]}, want {sorted(best)}"
+    return None
+
+
 ALL_PINS = [pin_query_formats, pin_nibbles, pin_residual_map, pin_brute_force, pin_closed_forms,
             pin_reductions, pin_invariants, pin_probe, pin_router, pin_compress_closed_forms,
             pin_compress_rne_table, pin_compress_arithmetic, pin_compress_bounds,
-            pin_compress_into_cache, pin_route_range, pin_attention_features]
+            pin_compress_into_cache, pin_route_range, pin_attention_features, pin_control]
 
 
 def run_all(o):

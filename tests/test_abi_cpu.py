@@ -265,3 +265,32 @@ def test_features_argument_checks(lib):
     assert f(phi=FAKE + 4) == 7
     assert f(layer=4) == 2
     assert f(dd=d8, ws=1 << 30) == 3
+
+
+def test_controller_update_matches_oracle(lib):
+    """The host controller against the oracle's rule on random traces (bitwise:
+    both step and clamp in float32)."""
+    import oracle.control as OC
+    from paper_2607_06523_amd import binding
+    rng = np.random.default_rng(17)
+    for trial in range(20):
+        M, J = int(rng.integers(1, 6)), int(rng.integers(0, 4))
+        ctl = binding.Controller(0.05, float(rng.uniform(0, 1)), float(rng.uniform(0, 1)), int(rng.integers(1, 4)),
+                                 -3.0, 3.0)
+        theta = np.sort(rng.uniform(-3, 3, size=(M, J)).astype(np.float32), axis=1)
+        below = rng.integers(0, 3, size=M).astype(np.int32)
+        th_ref, bl_ref = theta.copy(), below.astype(np.int64).copy()
+        for step in range(12):
+            err = rng.uniform(0, 0.1, size=M).astype(np.float32)
+            err[rng.random(M) < 0.1] = np.nan
+            st = lib.dwkv_controller_update(C.byref(ctl), M, J, err.ctypes.data, theta.ctypes.data,
+                                            below.ctypes.data)
+            assert st == 0
+            OC.controller_update(th_ref, bl_ref, err, ctl.tol, ctl.step_down, ctl.step_up, ctl.patience,
+                                 ctl.theta_min, ctl.theta_max)
+            assert np.array_equal(theta.view(np.uint32), th_ref.astype(np.float32).view(np.uint32)), (trial, step)
+            assert np.array_equal(below, bl_ref), (trial, step)
+    bad = binding.Controller(0.1, -1.0, 0.5, 2, -1.0, 1.0)
+    one = np.zeros(1, np.float32)
+    assert lib.dwkv_controller_update(C.byref(bad), 1, 1, one.ctypes.data, one.ctypes.data,
+                                      np.zeros(1, np.int32).ctypes.data) == 2

@@ -9,6 +9,7 @@ import oracle.factorized as F
 import oracle.router as R
 import oracle.compress as CP
 import oracle.features as FE
+import oracle.control as CT
 import pins
 
 _orig_reconstruct = F.reconstruct
@@ -221,6 +222,46 @@ def _update_spike_last(phi, window, mass, spike):
     return phi
 
 
+def _ctl_variant(kind):
+    def upd(theta, below, err, tol, step_down, step_up, patience, theta_min, theta_max):
+        theta = np.asarray(theta)
+        for m in range(theta.shape[0]):
+            e = float(err[m])
+            above = (e > tol) if kind == "nan_quiet" else (np.isnan(e) or e > tol)
+            if above:
+                theta[m] = theta[m] - np.float32(step_down)
+                if kind != "no_clamp":
+                    theta[m] = np.clip(theta[m], theta_min, theta_max)
+                below[m] = 0
+            else:
+                below[m] += 1
+                if (below[m] > patience) if kind == "patience_late" else (below[m] >= patience):
+                    theta[m] = theta[m] + np.float32(step_up)
+                    if kind != "no_clamp":
+                        theta[m] = np.clip(theta[m], theta_min, theta_max)
+                    below[m] = 0
+        return theta, below
+    return upd
+
+
+def _budget_ties_up(z, entries, rho_min, rho_max):
+    N = len(z)
+    n = max(0, min(N, (entries - N * rho_min) // (rho_max - rho_min)))
+    order = sorted(range(N), key=lambda t: (-float(z[t]), -t))
+    codes = np.zeros(N, dtype=np.uint8)
+    codes[order[:n]] = 1
+    return codes
+
+
+def _budget_ceil(z, entries, rho_min, rho_max):
+    N = len(z)
+    n = max(0, min(N, -(-(entries - N * rho_min) // (rho_max - rho_min))))
+    order = sorted(range(N), key=lambda t: (-float(z[t]), t))
+    codes = np.zeros(N, dtype=np.uint8)
+    codes[order[:n]] = 1
+    return codes
+
+
 MUTANTS = {
     "residual dropped": [(F, "reconstruct", _reconstruct_variant("no_residual"))],
     "residual sign flipped": [(F, "reconstruct", _reconstruct_variant("residual_sign"))],
@@ -271,6 +312,11 @@ MUTANTS = {
     "attention spike summed over heads": [(FE, "attention_features", _features_variant("spike_sum"))],
     "feature mass overwritten instead of accumulated": [(FE, "update_features", _update_overwrite)],
     "feature spike keeps the last value": [(FE, "update_features", _update_spike_last)],
+    "threshold steps not clamped": [(CT, "controller_update", _ctl_variant("no_clamp"))],
+    "NaN probe error counted as quiet": [(CT, "controller_update", _ctl_variant("nan_quiet"))],
+    "step up one interval late": [(CT, "controller_update", _ctl_variant("patience_late"))],
+    "budget ties go to the higher token": [(CT, "budget_select", _budget_ties_up)],
+    "budget count rounded up": [(CT, "budget_select", _budget_ceil)],
     "bf16 query read as fp16": [(F, "q_to_f64", lambda bits, dtype: np.asarray(bits, np.uint16)
                                  .view(np.float16).astype(np.float64))],
 }
