@@ -192,6 +192,27 @@ dwkv_status dwkv_route_range(const dwkv_dims* dims, const float* phi, const floa
                              const float* theta, int64_t t0, int64_t t1, uint8_t* rank_code,
                              uint32_t* res_off, void* workspace, size_t ws_bytes, void* stream);
 
+/* Bytes of device workspace dwkv_route_budget needs (0 when dims are invalid). */
+size_t dwkv_route_budget_workspace_bytes(const dwkv_dims* dims);
+
+/* Budget-driven routing (Sec. 3: the threshold tau_m is chosen to satisfy the
+ * current memory budget), for the two-level form of Eq. 2 (n_levels == 2,
+ * else DWKV_E_UNSUPPORTED).  For every window m and KV head h, over packed
+ * tokens [t0, t1) (N of them), with z the router score of dwkv_route:
+ *   n = floor((E - N levels[0]) / (levels[1] - levels[0])), clamped to [0, N]
+ *   the n tokens of largest z get rank code 1, the others 0; equal scores go
+ *   to the lower token (the n-th largest score is the effective tau)
+ * and res_off continues from res_off[m][h][t0] as in dwkv_route_range.
+ *   entries: DEVICE int64 [M][Hkv], E, the residual entries allowed over the
+ *            range for (m, h) (8-byte aligned)
+ *   phi, u, rank_code, res_off: as dwkv_route (phi and u 16-byte aligned)
+ *   workspace: >= dwkv_route_budget_workspace_bytes(dims), no initial contents
+ * phi must be finite (a NaN score has no defined place).  Bit-exact by
+ * construction.  One launch, one workgroup per (window, head). */
+dwkv_status dwkv_route_budget(const dwkv_dims* dims, const float* phi, const float* u, const int64_t* entries,
+                              int64_t t0, int64_t t1, uint8_t* rank_code, uint32_t* res_off, void* workspace,
+                              size_t ws_bytes, void* stream);
+
 /* Append/compress (Sec. 3: coefficients by projection onto the window's
  * current basis, residuals 4-bit quantized at the routed rank, the gate of
  * Eq. 1 folded into the scale).  For packed tokens [t0, t1) of layer `layer`,

@@ -54,3 +54,22 @@ def budget_select(z: np.ndarray, entries: int, rho_min: int, rho_max: int) -> np
     codes = np.zeros(N, dtype=np.uint8)
     codes[order[:n]] = 1
     return codes
+
+
+def route_budget(phi, u, entries, levels, t0: int, t1: int, codes, off):
+    """Two-level routing of tokens [t0, t1) under a budget per (window, head):
+    entries [M][Hkv] residual entries allowed over the range.  Writes
+    codes[m][h][t] (0 or 1) and continues off[m][h][t+1] from off[m][h][t0]
+    (0 when t0 == 0).  Router scores as the router computes them (Eq. 2)."""
+    from .router import router_score
+    lev = np.asarray(levels, dtype=np.int64)
+    M, Hk = codes.shape[0], codes.shape[1]
+    if t0 == 0:
+        off[:, :, 0] = 0
+    for m in range(M):
+        z = router_score(phi[m, :, t0:t1], u[m])
+        for h in range(Hk):
+            k = budget_select(z[h], int(entries[m][h]), int(lev[0]), int(lev[1]))
+            codes[m, h, t0:t1] = k
+            off[m, h, t0 + 1:t1 + 1] = int(off[m, h, t0]) + np.cumsum(lev[k.astype(np.int64)])
+    return codes, off

@@ -226,6 +226,20 @@ class DeviceCache:
         binding.check(st, "dwkv_route_range")
         return rank_code, res_off
 
+    def route_budget(self, phi, u, entries, t0: int, t1: int, rank_code=None, res_off=None):
+        """Two-level Eq. 2 routing of tokens [t0, t1) under a budget of entries
+        (int64 [M, Hkv], device) per (window, head); in place by default."""
+        torch = self.torch
+        rank_code = self.rank_code if rank_code is None else rank_code
+        res_off = self.res_off if res_off is None else res_off
+        need = int(self.lib.dwkv_route_budget_workspace_bytes(C.byref(self.dims)))
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        st = self.lib.dwkv_route_budget(C.byref(self.dims), _ptr(phi), _ptr(u), _ptr(entries), int(t0), int(t1),
+                                        _ptr(rank_code), _ptr(res_off), _ptr(ws), ws.numel(),
+                                        _stream(torch, self.device))
+        binding.check(st, "dwkv_route_budget")
+        return rank_code, res_off
+
     def compress(self, layer: int, x_k, x_v, t0: int, t1: int, gate=None):
         """Append/compress packed tokens [t0, t1) of `layer` in place from dense
         fp16 keys / values x_k, x_v [t1-t0, Hkv, d]; gate: None or fp32 [2, Hkv, t1-t0]."""

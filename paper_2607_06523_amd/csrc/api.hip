@@ -415,6 +415,43 @@ dwkv_status dwkv_route(const dwkv_dims* d, const float* phi, const float* u, con
                           ws_bytes, stream);
 }
 
+size_t dwkv_route_budget_workspace_bytes(const dwkv_dims* d) {
+  if (check_dims(d) != DWKV_OK) return 0;
+  const size_t n = (size_t)(d->n_layers / d->window) * d->n_kv_heads * (size_t)d->total_tokens * 8;
+  return n > 0 ? align_up(n, 256) : 256;
+}
+
+dwkv_status dwkv_route_budget(const dwkv_dims* d, const float* phi, const float* u, const int64_t* entries,
+                              int64_t t0, int64_t t1, uint8_t* rank_code, uint32_t* res_off, void* workspace,
+                              size_t ws_bytes, void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (d->n_levels != 2) return DWKV_E_UNSUPPORTED;
+  if (t0 < 0 || t1 < t0 || t1 > d->total_tokens) return DWKV_E_DIMS;
+  if (!u || !entries || !rank_code || !res_off || !workspace) return DWKV_E_NULL;
+  if (t1 > t0 && !phi) return DWKV_E_NULL;
+  if (!aligned16(phi) || !aligned16(u) || !aligned16(workspace) || (reinterpret_cast<uintptr_t>(entries) & 7u))
+    return DWKV_E_ALIGN;
+  if (ws_bytes < dwkv_route_budget_workspace_bytes(d)) return DWKV_E_WORKSPACE;
+  if (t1 == t0 && t0 > 0) return DWKV_OK;
+  RouteArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.phi = phi;
+  a.u = u;
+  a.code = rank_code;
+  a.off = res_off;
+  a.entries = entries;
+  a.keys = static_cast<unsigned long long*>(workspace);
+  a.T = d->total_tokens;
+  a.t0 = t0;
+  a.n = t1 - t0;
+  a.n_kv_heads = d->n_kv_heads;
+  a.n_levels = d->n_levels;
+  for (int i = 0; i < DWKV_MAX_LEVELS; ++i) a.levels[i] = i < d->n_levels ? d->levels[i] : 0;
+  const int n_mh = (d->n_layers / d->window) * d->n_kv_heads;
+  return hip_status(launch_route_budget(a, n_mh, reinterpret_cast<hipStream_t>(stream)));
+}
+
 dwkv_status dwkv_compress(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* x_k,
                           const void* x_v, const float* gate, int64_t t0, int64_t t1, void* stream) {
   dwkv_status st = check_dims(d);

@@ -152,6 +152,98 @@ __global__ __launch_bounds__(kRT) void route_offsets_kernel(const RouteArgs a) {
   route_write_offsets(a, mh, blockIdx.x, base + a.bpre[(int64_t)mh * a.nblk + blockIdx.x], rho, red);
 }
 
+// Budget routing (two levels, Eq. 2 with tau chosen for a memory budget): the
+// n = floor((E - N rho_min) / (rho_max - rho_min)) tokens of largest score z
+// get level 1, ties to the lower token.  Keys are (order-preserving bits of z,
+// then the complement of the token's index), all distinct; the n-th largest
+// is found one byte at a time from the top (a 256-bin histogram of the
+// candidates that match the bytes fixed so far), then codes and offsets are
+// written in one ordered sweep.  grid (M*Hkv)
+__global__ __launch_bounds__(kRT) void route_budget_kernel(const RouteArgs a) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t red[kRT / 64];
+  __shared__ unsigned long long s_prefix;
+  __shared__ int64_t s_rem;
+  const int mh = blockIdx.x;
+  const int m = mh / a.n_kv_heads;
+  const int64_t N = a.n;
+  unsigned long long* keys = a.keys + (int64_t)mh * a.T;
+  const float4 u = *reinterpret_cast<const float4*>(a.u + 4 * m);
+  for (int64_t i = threadIdx.x; i < N; i += kRT) {
+    const int64_t t = a.t0 + i;
+    const float4 f = *reinterpret_cast<const float4*>(a.phi + ((int64_t)mh * a.T + t) * 4);
+    const float z = router_score(u, f) + 0.0f;           // -0 -> +0: equal scores tie
+    const uint32_t b = __float_as_uint(z);
+    const uint32_t ord = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+    keys[i] = ((unsigned long long)ord << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)i);
+  }
+  const int64_t rmin = a.levels[0], rmax = a.levels[1];
+  int64_t n = rmax > rmin ? (a.entries[mh] - N * rmin) / (rmax - rmin) : 0;
+  if (a.entries[mh] - N * rmin < 0) n = 0;
+  n = min(max(n, (int64_t)0), N);
+  unsigned long long thr = ~0ull;                        // n == 0: nothing reaches it
+  if (n == N) {
+    thr = 0;
+  } else if (n > 0) {
+    if (threadIdx.x == 0) { s_prefix = 0; s_rem = n; }
+    unsigned long long mask = 0;
+    for (int sh = 56; sh >= 0; sh -= 8) {
+      __syncthreads();                                   // keys written / previous pass read
+      hist[threadIdx.x] = 0u;                            // kRT == 256 bins
+      __syncthreads();
+      const unsigned long long prefix = s_prefix;
+      for (int64_t i = threadIdx.x; i < N; i += kRT) {
+        const unsigned long long k = keys[i];
+        if ((k & mask) == prefix) atomicAdd(&hist[(k >> sh) & 255u], 1u);
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) {                            // the byte of the rem-th largest candidate
+        int64_t rem = s_rem, above = 0;
+        int d = 255;
+        for (; d > 0; --d) {
+          if (above + hist[d] >= rem) break;
+          above += hist[d];
+        }
+        s_rem = rem - above;
+        s_prefix = prefix | ((unsigned long long)d << sh);
+      }
+      mask |= 255ull << sh;
+    }
+    __syncthreads();
+    thr = s_prefix;                                      // the n-th largest key
+  }
+  // codes and offsets, in token order, continuing the table from off[t0]
+  uint32_t* off = a.off + (int64_t)mh * (a.T + 1);
+  uint8_t* code = a.code + (int64_t)mh * a.T;
+  uint32_t carry = a.t0 == 0 ? 0u : off[a.t0];
+  __syncthreads();
+  if (a.t0 == 0 && threadIdx.x == 0) off[0] = 0u;
+  for (int64_t c0 = 0; c0 < N; c0 += kRouteTokensPerBlock) {
+    uint32_t rho[kPerThread], mine = 0;
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+      const int64_t j = c0 + threadIdx.x * kPerThread + i;
+      rho[i] = 0u;
+      if (j < N) {
+        const int k = keys[j] >= thr ? 1 : 0;
+        code[a.t0 + j] = (uint8_t)k;
+        rho[i] = (uint32_t)a.levels[k];
+      }
+      mine += rho[i];
+    }
+    uint32_t total;
+    uint32_t run = carry + block_exclusive_scan(mine, red, &total);
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+      const int64_t j = c0 + threadIdx.x * kPerThread + i;
+      run += rho[i];
+      if (j < N) off[a.t0 + j + 1] = run;
+    }
+    carry += total;
+    __syncthreads();                                     // red[] is reused by the next chunk
+  }
+}
+
 // One thread per token: dense g*R row of the token.
 __global__ __launch_bounds__(256) void residual_map_kernel(const uint32_t* off, const uint8_t* idx,
                                                            const uint8_t* val, const uint16_t* scale,
@@ -235,6 +327,11 @@ hipError_t launch_route(const RouteArgs& a, int n_mh, hipStream_t s) {
     hipLaunchKernelGGL(route_block_scan_kernel, dim3(n_mh), dim3(kRT), 0, s, a);
     hipLaunchKernelGGL(route_offsets_kernel, dim3(a.nblk, n_mh), dim3(kRT), 0, s, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_route_budget(const RouteArgs& a, int n_mh, hipStream_t s) {
+  hipLaunchKernelGGL(route_budget_kernel, dim3(n_mh), dim3(kRT), 0, s, a);
   return hipGetLastError();
 }
 

@@ -153,6 +153,8 @@ struct RouteArgs {
   uint32_t* bpre;              // [M*Hkv][nblk]
   int64_t T;                   // token stride of code / off / phi
   int64_t t0, n;               // routed range [t0, t0 + n); off[t0] holds the carry-in
+  const int64_t* entries;      // budget routing: residual entries allowed per (window, head)
+  unsigned long long* keys;    // budget routing: selection keys [M*Hkv][T]
   int32_t n_kv_heads;
   int32_t n_levels;
   int32_t nblk;
@@ -196,6 +198,9 @@ hipError_t launch_split_tl_scores(int rb, int g, bool resid, const SplitArgs& a,
 hipError_t launch_merge_tl(int rb, int g, const SplitArgs& a, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, int n_mh, hipStream_t s);
+// Two-level routing under a budget: a.entries [M*Hkv] (device), keys scratch
+// a.keys [M*Hkv][T]; one workgroup per (window, head).
+hipError_t launch_route_budget(const RouteArgs& a, int n_mh, hipStream_t s);
 hipError_t launch_compress(const CompressArgs& a, hipStream_t s);
 
 // Materialization of one layer's rebuilt keys and values (Eq. 1) as fp16.

@@ -294,3 +294,19 @@ def test_controller_update_matches_oracle(lib):
     one = np.zeros(1, np.float32)
     assert lib.dwkv_controller_update(C.byref(bad), 1, 1, one.ctypes.data, one.ctypes.data,
                                       np.zeros(1, np.int32).ctypes.data) == 2
+
+
+def test_route_budget_argument_checks(lib):
+    d, keep = dims(levels=(0, 8))
+    need = lib.dwkv_route_budget_workspace_bytes(C.byref(d))
+    assert need == up256(2 * 2 * 3000 * 8)
+    rb = lambda dd=d, **kw: lib.dwkv_route_budget(C.byref(dd), kw.get("phi", FAKE), FAKE, kw.get("ent", FAKE),
+                                                  kw.get("t0", 0), kw.get("t1", 3000), FAKE, FAKE, FAKE,
+                                                  kw.get("ws", need), None)
+    assert rb(ws=need - 1) == 4
+    assert rb(t1=3001) == 2
+    assert rb(ent=0) == 1
+    assert rb(ent=FAKE + 4) == 7
+    assert rb(phi=FAKE + 8) == 7
+    d3, keep3 = dims()                                   # three levels
+    assert rb(dd=d3, ws=1 << 30) == 3
