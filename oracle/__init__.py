@@ -15,12 +15,13 @@ inputs.
 * ``features``: the router's attention-mass and attention-spike features of a
   decode.
 * ``control``: probe-feedback threshold updates and budget-driven selection.
+* ``sketch``: the randomized-sketch initialization of a window's bases.
 
 Every function is pinned by the CPU tests (brute force in exact arithmetic,
 closed forms, reductions to library attention, invariants); none is marked
 "parity unpinned".
 """
-from . import factorized, router, compress, features, control
+from . import factorized, router, compress, features, control, sketch
 from .factorized import (attention, decode, probe, probe_error, reconstruct,
                          residual_map, int4_from_nibble, entry_codes, q_to_f64,
                          default_scale)

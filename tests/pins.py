@@ -26,7 +26,9 @@ says what disagreed.  The pins are:
 * the router's attention features: per-sequence masses summing to G, spike
   below mass below G spike, uniform and ln-3 closed forms, the table fold;
 * threshold control: a hand-worked feedback trace with clamps, and the
-  budget-driven selection against enumeration of the promoted sets.
+  budget-driven selection against enumeration of the promoted sets;
+* sketch basis: Gram-Schmidt against numpy's QR, the exact row space of a
+  rank-r_b prefill, zero rows of a rank-deficient sketch.
 """
 from __future__ import annotations
 
@@ -1040,10 +1042,50 @@ def pin_control(o):
     return None
 
 
+def pin_sketch(o):
+    """Sketch basis: Gram-Schmidt rows against numpy's QR (same signs after
+    fixing R's diagonal positive), orthonormality, the exact row space of a
+    rank-r_b prefill, and a rank-deficient sketch giving zero rows."""
+    S = o.sketch
+    rng = np.random.default_rng(61)
+    Y = rng.standard_normal((12, 40))
+    Q = S.orthonormal_rows(Y)
+    qq, rr = np.linalg.qr(Y.T)
+    qq = qq * np.sign(np.diag(rr))[None, :]
+    if not np.allclose(Q, qq.T, atol=1e-12):
+        return "Gram-Schmidt rows differ from the QR factor"
+    if not np.allclose(Q @ Q.T, np.eye(12), atol=1e-12):
+        return "sketch basis not orthonormal"
+    # a prefill of exact rank r_b (exact in fp16: integer mixes of unit
+    # channel vectors): the basis spans its row space
+    w, Tb, Hk, d, rb = 2, 30, 2, 16, 4
+    V = np.zeros((d, rb))
+    V[rng.permutation(d)[:rb], np.arange(rb)] = 1.0
+    coeff = rng.integers(-3, 4, size=(w, 2, Tb, Hk, rb)).astype(np.float64)
+    x = np.einsum("lztha,da->lzthd", coeff, V).astype(np.float16)
+    omega = rng.standard_normal((w * Tb, rb)).astype(np.float16)
+    for h in range(Hk):
+        for z in range(2):
+            B = S.sketch_basis(x, omega, h, z).astype(np.float64)
+            rows = x[:, z, :, h, :].astype(np.float64).reshape(-1, d)
+            resid = rows - (rows @ B.T) @ B
+            if np.abs(resid).max() > 4e-3 * np.abs(rows).max():
+                return f"basis of a rank-{rb} prefill misses its row space (h={h}, z={z})"
+            if not np.allclose(B @ B.T, np.eye(rb), atol=3e-3):
+                return "fp16 basis rows far from orthonormal"
+    # rank-deficient: a single-direction prefill leaves rows 1.. zero
+    x1 = np.zeros((1, 2, 10, 1, d), np.float16)
+    x1[0, :, :, 0, 3] = rng.standard_normal((2, 10))
+    B1 = S.sketch_basis(x1, rng.standard_normal((10, 3)).astype(np.float16), 0, 0).astype(np.float64)
+    if not (abs(abs(B1[0, 3]) - 1) < 1e-3 and np.all(B1[1:] == 0)):
+        return f"rank-deficient sketch must give one unit row and zero rows, got {B1[:, 3]}"
+    return None
+
+
 ALL_PINS = [pin_query_formats, pin_nibbles, pin_residual_map, pin_brute_force, pin_closed_forms,
             pin_reductions, pin_invariants, pin_probe, pin_router, pin_compress_closed_forms,
             pin_compress_rne_table, pin_compress_arithmetic, pin_compress_bounds,
-            pin_compress_into_cache, pin_route_range, pin_attention_features, pin_control]
+            pin_compress_into_cache, pin_route_range, pin_attention_features, pin_control, pin_sketch]
 
 
 def run_all(o):

@@ -10,6 +10,7 @@ import oracle.router as R
 import oracle.compress as CP
 import oracle.features as FE
 import oracle.control as CT
+import oracle.sketch as SK
 import pins
 
 _orig_reconstruct = F.reconstruct
@@ -262,6 +263,22 @@ def _budget_ceil(z, entries, rho_min, rho_max):
     return codes
 
 
+def _gs_no_normalize(Y):
+    Y = np.array(Y, dtype=np.float64)
+    Q = np.zeros_like(Y)
+    for i in range(Y.shape[0]):
+        v = Y[i].copy()
+        for j in range(i):
+            v -= (v @ Q[j]) * Q[j]
+        Q[i] = v / max(np.abs(v).max(), 1e-300)
+    return Q
+
+
+def _sketch_transposed(x_rows, omega):
+    return (np.asarray(x_rows, np.float64).T @ np.asarray(omega, np.float64).T).T[:, :np.asarray(x_rows).shape[1]] \
+        if False else np.asarray(omega, np.float64)[:, ::-1] @ np.asarray(x_rows, np.float64)
+
+
 MUTANTS = {
     "residual dropped": [(F, "reconstruct", _reconstruct_variant("no_residual"))],
     "residual sign flipped": [(F, "reconstruct", _reconstruct_variant("residual_sign"))],
@@ -317,6 +334,8 @@ MUTANTS = {
     "step up one interval late": [(CT, "controller_update", _ctl_variant("patience_late"))],
     "budget ties go to the higher token": [(CT, "budget_select", _budget_ties_up)],
     "budget count rounded up": [(CT, "budget_select", _budget_ceil)],
+    "Gram-Schmidt rows scaled by max instead of norm": [(SK, "orthonormal_rows", _gs_no_normalize)],
+    "sketch with the token order reversed": [(SK, "sketch", _sketch_transposed)],
     "bf16 query read as fp16": [(F, "q_to_f64", lambda bits, dtype: np.asarray(bits, np.uint16)
                                  .view(np.float16).astype(np.float64))],
 }
