@@ -276,6 +276,29 @@ dwkv_status dwkv_decode_features(const dwkv_dims* dims, const dwkv_cache* cache,
                                  const void* q, int32_t q_type, float sm_scale, float* out, float* phi,
                                  void* workspace, size_t ws_bytes, void* stream);
 
+/* Bytes of device workspace dwkv_sketch_basis needs for a prefill of
+ * n_tokens tokens (0 when invalid). */
+size_t dwkv_sketch_workspace_bytes(const dwkv_dims* dims, int64_t n_tokens);
+
+/* Online basis initialization (Sec. 3: a small randomized low-rank sketch of
+ * the window's cached keys and values after prefill, per head, K and V apart).
+ * For sequence `seq`, window `window`, every KV head h and Z:
+ *   X     = the window's prefill vectors of head h, rows (layer l, token t),
+ *           ((w n_tokens) x d)
+ *   Y     = Omega X   (r_b x d, float64 sums of exact fp16 products)
+ *   basis = Gram-Schmidt orthonormalization of Y's rows in order (float64),
+ *           rounded to fp16; a row whose remaining norm is below 1e-9 of the
+ *           largest row norm of Y (a rank-deficient sketch) becomes zero
+ *   x:     fp16 [w][2][n_tokens][Hkv][d]  (Z = 0 keys, post positional
+ *          encoding, Z = 1 values)
+ *   omega: fp16 [w * n_tokens][r_b], row l * n_tokens + t: the random sketch
+ *          matrix (transposed), drawn by the caller and shared by heads and Z
+ * WRITES cache->basis[seq][window] (all heads, both Z); nothing else.  Two
+ * launches.  All pointers 16-byte aligned. */
+dwkv_status dwkv_sketch_basis(const dwkv_dims* dims, const dwkv_cache* cache, int32_t window, int32_t seq,
+                              const void* x, const void* omega, int64_t n_tokens, void* workspace,
+                              size_t ws_bytes, void* stream);
+
 /* Probe-feedback threshold control (Sec. 3): when a window's probe error
  * (Eq. 3) exceeds its tolerance the router lowers the window's threshold;
  * after several probe intervals below tolerance it raises it.  The paper

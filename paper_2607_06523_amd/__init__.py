@@ -273,6 +273,17 @@ class DeviceCache:
         binding.check(st, "dwkv_decode_features")
         return out
 
+    def sketch_basis(self, window: int, seq: int, x, omega):
+        """Randomized-sketch bases of (seq, window) from its prefill x fp16
+        [w, 2, n, Hkv, d] and sketch matrix omega fp16 [w*n, r_b]; in place."""
+        torch = self.torch
+        n = int(x.shape[2])
+        need = int(self.lib.dwkv_sketch_workspace_bytes(C.byref(self.dims), n))
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        st = self.lib.dwkv_sketch_basis(C.byref(self.dims), C.byref(self.cstruct), int(window), int(seq), _ptr(x),
+                                        _ptr(omega), n, _ptr(ws), ws.numel(), _stream(torch, self.device))
+        binding.check(st, "dwkv_sketch_basis")
+
     def materialize(self, layer: int, k_out=None, v_out=None):
         """Eq. 1 written out for `layer`: K_hat fp16 [Hkv, T, d] and V_hat fp16
         [Hkv, T16/16, d, 16] (the blocked layout of the dense decode)."""

@@ -59,7 +59,7 @@ class Probe(C.Structure):
 EXPORTS = ["dwkv_abi_version", "dwkv_status_str", "dwkv_split_tokens", "dwkv_workspace_bytes",
            "dwkv_decode_launches", "dwkv_decode", "dwkv_decode_partials", "dwkv_decode_merge", "dwkv_route_workspace_bytes", "dwkv_route",
            "dwkv_route_range", "dwkv_route_budget_workspace_bytes", "dwkv_route_budget", "dwkv_compress", "dwkv_features_workspace_bytes", "dwkv_decode_features",
-           "dwkv_controller_update", "dwkv_materialize", "dwkv_dense_workspace_bytes",
+           "dwkv_controller_update", "dwkv_sketch_workspace_bytes", "dwkv_sketch_basis", "dwkv_materialize", "dwkv_dense_workspace_bytes",
            "dwkv_dense_decode", "dwkv_residual_map",
            "dwkv_validate_workspace_bytes", "dwkv_validate"]
 
@@ -117,6 +117,11 @@ def load(path: str = LIB_PATH):
     lib.dwkv_controller_update.restype = C.c_int
     lib.dwkv_controller_update.argtypes = [P(Controller), C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
                                            C.c_void_p]
+    lib.dwkv_sketch_workspace_bytes.restype = C.c_size_t
+    lib.dwkv_sketch_workspace_bytes.argtypes = [P(Dims), C.c_int64]
+    lib.dwkv_sketch_basis.restype = C.c_int
+    lib.dwkv_sketch_basis.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_int64,
+                                      C.c_void_p, C.c_size_t, C.c_void_p]
     lib.dwkv_materialize.restype = C.c_int
     lib.dwkv_materialize.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
     lib.dwkv_dense_workspace_bytes.restype = C.c_size_t

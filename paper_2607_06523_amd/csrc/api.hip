@@ -519,6 +519,42 @@ dwkv_status dwkv_residual_map(const dwkv_dims* d, const dwkv_cache* c, int32_t l
       t0, t1, d->res_stride, dense, reinterpret_cast<hipStream_t>(stream)));
 }
 
+size_t dwkv_sketch_workspace_bytes(const dwkv_dims* d, int64_t n_tokens) {
+  if (check_dims(d) != DWKV_OK || n_tokens < 1) return 0;
+  const size_t row = (size_t)d->n_kv_heads * 2 * d->basis_rank * kHeadDim * sizeof(double);
+  return align_up((size_t)sketch_chunks((int64_t)d->window * n_tokens) * row, 256) + align_up(row, 256);
+}
+
+dwkv_status dwkv_sketch_basis(const dwkv_dims* d, const dwkv_cache* c, int32_t window, int32_t seq,
+                              const void* x, const void* omega, int64_t n_tokens, void* workspace,
+                              size_t ws_bytes, void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (!c || !c->basis || !x || !omega || !workspace) return DWKV_E_NULL;
+  const int M = d->n_layers / d->window;
+  if (window < 0 || window >= M || seq < 0 || seq >= d->batch || n_tokens < 1) return DWKV_E_DIMS;
+  if ((double)d->window * (double)n_tokens > 2147483647.0) return DWKV_E_UNSUPPORTED;
+  if (!aligned16(c->basis) || !aligned16(x) || !aligned16(omega) || !aligned16(workspace)) return DWKV_E_ALIGN;
+  if (ws_bytes < dwkv_sketch_workspace_bytes(d, n_tokens)) return DWKV_E_WORKSPACE;
+  const int64_t rb = d->basis_rank, Hk = d->n_kv_heads;
+  SketchArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.x = static_cast<const uint16_t*>(x);
+  a.omega = static_cast<const uint16_t*>(omega);
+  a.n_chunks = sketch_chunks((int64_t)d->window * n_tokens);
+  a.part = static_cast<double*>(workspace);
+  a.q = reinterpret_cast<double*>(static_cast<char*>(workspace) +
+                                  align_up((size_t)a.n_chunks * Hk * 2 * rb * kHeadDim * sizeof(double), 256));
+  // the cache's bases are written in place (the pointer is const only for decode)
+  a.basis = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->basis)) +
+            (((int64_t)seq * M + window) * Hk) * 2 * rb * kHeadDim;
+  a.n_tokens = n_tokens;
+  a.w = d->window;
+  a.n_kv_heads = d->n_kv_heads;
+  a.rb = d->basis_rank;
+  return hip_status(launch_sketch(a, reinterpret_cast<hipStream_t>(stream)));
+}
+
 dwkv_status dwkv_materialize(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, void* k_out,
                              void* v_out, void* stream) {
   dwkv_status st = check_dims(d);

@@ -232,6 +232,19 @@ struct FeatArgs {
   int32_t batch, n_kv_heads, split, n_work;
 };
 hipError_t launch_features(int g, const FeatArgs& a, hipStream_t s);
+
+// Randomized-sketch basis initialization of one (sequence, window).
+struct SketchArgs {
+  const uint16_t* x;           // fp16 [w][2][n_tokens][Hkv][d] prefill keys (Z = 0) and values (Z = 1)
+  const uint16_t* omega;       // fp16 [w * n_tokens][rb] sketch matrix, row l * n_tokens + t
+  double* part;                // [n_chunks][Hkv][2][rb][d] sketch partials
+  double* q;                   // [Hkv][2][rb][d] orthonormal rows
+  uint16_t* basis;             // the (sequence, window)'s basis [Hkv][2][rb][d], written
+  int64_t n_tokens;
+  int32_t w, n_kv_heads, rb, n_chunks;
+};
+int sketch_chunks(int64_t rows);
+hipError_t launch_sketch(const SketchArgs& a, hipStream_t s);
 hipError_t launch_residual_map(const uint32_t* off, const uint8_t* idx, const uint8_t* val,
                                const uint16_t* scale, int64_t t0, int64_t t1, int64_t slab_len,
                                float* dense, hipStream_t s);

@@ -310,3 +310,22 @@ def test_route_budget_argument_checks(lib):
     assert rb(phi=FAKE + 8) == 7
     d3, keep3 = dims()                                   # three levels
     assert rb(dd=d3, ws=1 << 30) == 3
+
+
+def test_sketch_argument_checks(lib):
+    from paper_2607_06523_amd import binding
+    d, keep = dims()
+    need = lib.dwkv_sketch_workspace_bytes(C.byref(d), 5000)
+    row = 2 * 2 * 32 * 128 * 8
+    assert need == up256(3 * row) + up256(row)          # 10000 sketch rows: 3 chunks of 4096
+    assert lib.dwkv_sketch_workspace_bytes(C.byref(d), 0) == 0
+    c = binding.Cache(*([FAKE] * 8))
+    sk = lambda **kw: lib.dwkv_sketch_basis(C.byref(d), C.byref(c), kw.get("win", 0), kw.get("seq", 0),
+                                            kw.get("x", FAKE), FAKE, kw.get("n", 5000), FAKE, kw.get("ws", need),
+                                            None)
+    assert sk(ws=need - 1) == 4
+    assert sk(win=2) == 2
+    assert sk(seq=2) == 2
+    assert sk(n=0) == 2
+    assert sk(x=0) == 1
+    assert sk(x=FAKE + 2) == 7
