@@ -169,6 +169,72 @@ def measure_features(dc, host, torch, outs, steps: int = 5):
                     "into the window's router features"}
 
 
+def measure_control(dc, host, wl, torch, reps: int = 3):
+    """The control steps at this workload: budget-driven routing of every
+    window and head over all T tokens (two levels: the workload's lowest and
+    highest), and the sketch initialization of one window's bases from a
+    synthetic prefill.  Both write into the cache, so this runs last."""
+    import ctypes
+    from synth import router_inputs
+    T, Hk, d, w, rb, M = (host.total_tokens, host.n_kv_heads, host.head_dim, host.window, host.basis_rank,
+                          host.n_windows)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, n):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        fn()
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for _ in range(n):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / n
+
+    res = {}
+    two = DeviceCache2(dc, (host.levels[0], host.levels[-1]))
+    phi, u, _ = router_inputs(wl, M, T)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    phi_d, u_d = dev(phi), dev(u)
+    entries = torch.full((M, Hk), T * host.levels[-1] // 10, dtype=torch.int64, device="cuda")
+    codes = torch.empty((M, Hk, T), dtype=torch.uint8, device="cuda")
+    offs = torch.empty((M, Hk, T + 1), dtype=torch.int32, device="cuda")
+    res["route_budget_ms"] = round(timed(lambda: two.route_budget(phi_d, u_d, entries, 0, T, codes, offs), reps), 4)
+    g = torch.Generator(device="cuda").manual_seed(3)
+    x = torch.randn((w, 2, T, Hk, d), generator=g, device="cuda", dtype=torch.float16)
+    omega = torch.randn((w * T, rb), generator=g, device="cuda", dtype=torch.float16)
+    res["sketch_basis_ms_per_window"] = round(timed(lambda: dc.sketch_basis(0, 0, x, omega), reps), 4)
+    res["note"] = ("route_budget: all windows and heads over T tokens (levels {lo, hi}); sketch: one window, "
+                   "w x T prefill rows per head and Z")
+    del x, omega
+    return res
+
+
+class DeviceCache2:
+    """The same device cache seen with a two-level table (for budget routing)."""
+    def __init__(self, dc, levels):
+        from paper_2607_06523_amd import binding
+        self.dc = dc
+        self.dims, self._keep = binding.make_dims(
+            batch=dc.batch, n_layers=dc.n_layers, window=dc.window, n_kv_heads=dc.n_kv_heads,
+            n_q_heads=dc.n_q_heads, head_dim=dc.head_dim, basis_rank=dc.basis_rank, levels=tuple(levels),
+            cu_seqlens_host=dc.cu_host, cu_seqlens_dev_ptr=dc.cu.data_ptr(), total_tokens=dc.total_tokens,
+            res_stride=dc.res_stride, split_tokens=0)
+
+    def route_budget(self, phi, u, entries, t0, t1, codes, offs):
+        import ctypes
+        from paper_2607_06523_amd import binding
+        lib, torch = self.dc.lib, self.dc.torch
+        need = int(lib.dwkv_route_budget_workspace_bytes(ctypes.byref(self.dims)))
+        ws = getattr(self, "_ws", None)
+        if ws is None or ws.numel() < need:
+            ws = self._ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        p = lambda t: ctypes.c_void_p(t.data_ptr())
+        st = lib.dwkv_route_budget(ctypes.byref(self.dims), p(phi), p(u), p(entries), int(t0), int(t1), p(codes),
+                                   p(offs), p(ws), ws.numel(), ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        binding.check(st, "dwkv_route_budget")
+
+
 def measure_comparators(dc, host, torch, steps: int = 3):
     """The decode's comparison paths on the same GPU and workload: a dense fp16
     cache decode (every layer's K/V resident, 2 bytes per element) and the
@@ -394,6 +460,9 @@ def main():
     if not args.no_comparators and args.variant == "full":
         log("[bench] timing the dense fp16 and unfused comparison paths")
         result["comparators"] = measure_comparators(dc, host, torch)
+    if not args.no_comparators and args.variant == "full":
+        log("[bench] timing the control steps (budget routing, sketch bases)")
+        result["control"] = measure_control(dc, host, wl, torch)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
         result["cpu_baseline"] = cpu_baseline(host, args.cpu_pairs, args.cpu_budget)
