@@ -62,12 +62,20 @@ def coefficient_rows(cache, layer: int, z: int, h: int, t0: int, t1: int) -> np.
 
     Keys are stored row-major [T][r_b]; values in 16-token blocks with the token
     index fastest ([T16/16][r_b][16]): row t of the values is column t % 16 of
-    block t // 16."""
+    block t // 16.  In the 8-bit blockwise form (Sec. 3 stores coefficients
+    8-bit blockwise quantized) the stored entries are int8 codes and
+    A_{t,i} = code_{t,i} * scale[i // 16][t], one fp16 scale per token and
+    block of 16 coefficients."""
     if z == 0:
-        return cache.coef_k[layer, h, t0:t1].astype(np.float64)
-    blocks = cache.coef_v[layer, h]                                 # [NB, r_b, 16]
-    rows = np.swapaxes(blocks, 1, 2).reshape(-1, blocks.shape[1])   # [NB*16, r_b]
-    return rows[t0:t1].astype(np.float64)
+        rows = cache.coef_k[layer, h, t0:t1].astype(np.float64)
+    else:
+        blocks = cache.coef_v[layer, h]                                 # [NB, r_b, 16]
+        rows = np.swapaxes(blocks, 1, 2).reshape(-1, blocks.shape[1])   # [NB*16, r_b]
+        rows = rows[t0:t1].astype(np.float64)
+    if getattr(cache, "coef_format", "f16") == "int8":
+        sc = (cache.coef_scale_k if z == 0 else cache.coef_scale_v)[layer, h, :, t0:t1]   # [r_b/16, n]
+        rows = rows * np.repeat(sc.astype(np.float64).T, 16, axis=1)
+    return rows
 
 
 def window_of(layer: int, window: int) -> int:

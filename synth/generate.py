@@ -6,7 +6,9 @@ K-or-V, head) regenerates on its own and equals the same slab of a full
 generation.  The draws follow the workload's stated distributions:
 
 * shared bases: r_b x d N(0,1) rows, orthonormalised in float64, rounded to fp16;
-* per-token basis coefficients: N(0,1) rounded to fp16;
+* per-token basis coefficients: N(0,1) rounded to fp16; or, for the 8-bit
+  blockwise form, int8 codes Binomial(254, 1/2) - 127 (mean 0, sd about 8)
+  with one fp16 scale per 16-coefficient block drawn U(0.11, 0.14);
 * routed residual rank: categorical over the level table (salient spans, when
   the workload has them, force one level for every window and head);
 * residual entries: the routed number of distinct channels drawn uniformly,
@@ -33,6 +35,7 @@ from .workloads import Workload
 # tensor ids used to key the random streams
 _BASIS, _COEF, _RANK, _RES_CH, _RES_CODE, _RES_SCALE, _Q, _SPANS = 1, 2, 3, 4, 5, 6, 7, 8
 _PHI, _ROUTER_U, _PROBE = 10, 11, 12
+_COEF8, _COEF8_SCALE = 13, 14
 
 RES_TAIL_PAD = 512      # spare entries after the longest slab
 RES_ALIGN = 256         # res_stride is a multiple of this
@@ -69,6 +72,9 @@ class CompressedCache:
       res_val   uint8 [L][2][Hkv][res_stride/2]  two int4 codes per byte, low nibble first
       res_scale fp16  [L][2][Hkv][T]
       q_bits    uint16[L][B][Hq][d]              fp16 or bf16 bit patterns
+    With coef_format "int8" (the 8-bit blockwise form), coef_k / coef_v hold
+    int8 codes in the same shapes and coef_scale_k / coef_scale_v fp16
+    [L][Hkv][r_b/16][T] the scale of each 16-coefficient block.
     """
     workload: Workload
     layer0: int                 # absolute index of the first layer held
@@ -87,6 +93,9 @@ class CompressedCache:
     res_scale: np.ndarray
     q_bits: np.ndarray
     q_dtype: str
+    coef_format: str = "f16"
+    coef_scale_k: np.ndarray | None = None
+    coef_scale_v: np.ndarray | None = None
 
     @property
     def batch(self): return len(self.seqlens)
@@ -111,7 +120,7 @@ class CompressedCache:
         Hk, T, rb, d = self.n_kv_heads, self.total_tokens, self.basis_rank, self.head_dim
         B, Hq = self.batch, self.n_q_heads
         basis = B * Hk * 2 * rb * d * 2
-        coef = 2 * Hk * T * rb * 2
+        coef = 2 * Hk * T * rb * 2 if self.coef_format == "f16" else 2 * Hk * T * (rb + 2 * (rb // 16))
         off = Hk * (T + 1) * 4
         ent = 0
         for h in range(Hk):      # average over windows of the entries per slab
@@ -222,8 +231,12 @@ def generate(w: Workload, layers: tuple | None = None, threads: int | None = Non
     list(pool.map(_basis, [(b, m, h, z) for b in range(B) for m in range(nM)
                            for h in range(Hk) for z in range(2)]))
 
-    coef_k = np.empty((nL, Hk, T, rb), dtype=np.float16)
-    coef_v = np.zeros((nL, Hk, padded_tokens(T) // BLOCK, rb, BLOCK), dtype=np.float16)
+    c8 = getattr(w, "coef_format", "f16") == "int8"
+    cdt = np.int8 if c8 else np.float16
+    coef_k = np.empty((nL, Hk, T, rb), dtype=cdt)
+    coef_v = np.zeros((nL, Hk, padded_tokens(T) // BLOCK, rb, BLOCK), dtype=cdt)
+    cs_k = np.empty((nL, Hk, rb // 16, T), dtype=np.float16) if c8 else None
+    cs_v = np.empty((nL, Hk, rb // 16, T), dtype=np.float16) if c8 else None
     res_scale = np.empty((nL, 2, Hk, T), dtype=np.float16)
     res_idx = np.zeros((nL, 2, Hk, res_stride), dtype=np.uint8)
     res_val = np.zeros((nL, 2, Hk, res_stride // 2), dtype=np.uint8)
@@ -237,8 +250,13 @@ def generate(w: Workload, layers: tuple | None = None, threads: int | None = Non
             n = t1 - t0
             if n == 0:
                 continue
-            g = rng_for(w.seed, _COEF, b, l, z, h)
-            rows = g.standard_normal((n, rb), dtype=np.float32).astype(np.float16)
+            if c8:
+                rows = (rng_for(w.seed, _COEF8, b, l, z, h).binomial(254, 0.5, size=(n, rb)) - 127).astype(np.int8)
+                sc = rng_for(w.seed, _COEF8_SCALE, b, l, z, h).uniform(0.11, 0.14, size=(rb // 16, n))
+                (cs_k if z == 0 else cs_v)[li, h, :, t0:t1] = sc.astype(np.float16)
+            else:
+                g = rng_for(w.seed, _COEF, b, l, z, h)
+                rows = g.standard_normal((n, rb), dtype=np.float32).astype(np.float16)
             if z == 0:
                 coef_k[li, h, t0:t1] = rows
             else:   # scatter into the token-fastest blocks
@@ -272,7 +290,8 @@ def generate(w: Workload, layers: tuple | None = None, threads: int | None = Non
         workload=w, layer0=L0, n_layers=nL, seqlens=list(seqlens), cu_seqlens=cu,
         levels=tuple(int(x) for x in w.levels), res_stride=res_stride, basis=basis,
         coef_k=coef_k, coef_v=coef_v, rank_code=rank_code, res_off=res_off, res_idx=res_idx,
-        res_val=res_val, res_scale=res_scale, q_bits=q_bits, q_dtype=w.q_dtype)
+        res_val=res_val, res_scale=res_scale, q_bits=q_bits, q_dtype=w.q_dtype,
+        coef_format="int8" if c8 else "f16", coef_scale_k=cs_k, coef_scale_v=cs_v)
 
 
 def router_inputs(w: Workload, n_windows: int, T: int, window0: int = 0):

@@ -34,6 +34,7 @@ class Workload:
     salient_span: int = 64           # span length (tokens)
     salient_level: int = 0           # level index forced inside spans
     probe: bool = False              # attention-output probe on every layer
+    coef_format: str = "f16"         # "f16" coefficient rows, or "int8" (8-bit blockwise)
     description: str = field(default="", compare=False)
 
     @property

@@ -28,7 +28,9 @@ says what disagreed.  The pins are:
 * threshold control: a hand-worked feedback trace with clamps, and the
   budget-driven selection against enumeration of the promoted sets;
 * sketch basis: Gram-Schmidt against numpy's QR, the exact row space of a
-  rank-r_b prefill, zero rows of a rank-deficient sketch.
+  rank-r_b prefill, zero rows of a rank-deficient sketch;
+* 8-bit blockwise coefficients: a scalar loop over code * block scale, and an
+  fp16 twin with power-of-two scales decoding identically.
 """
 from __future__ import annotations
 
@@ -1082,10 +1084,41 @@ def pin_sketch(o):
     return None
 
 
+def pin_int8_coefficients(o):
+    """The 8-bit blockwise coefficient form: a scalar loop over (token, i) gives
+    code * scale of block i // 16; with power-of-two scales the int8 cache and
+    the fp16 cache holding the same products decode identically."""
+    c = small_cache(coef_format="int8", head_dim=128, basis_rank=48, context=20, ragged=(5, 40))
+    F = o.factorized
+    for layer in range(c.n_layers):
+        for z in range(2):
+            for h in range(c.n_kv_heads):
+                t0, t1 = 3, c.total_tokens - 2
+                rows = F.coefficient_rows(c, layer, z, h, t0, t1)
+                sc = c.coef_scale_k if z == 0 else c.coef_scale_v
+                for t in (t0, t0 + 1, t1 - 1):
+                    for i in (0, 1, 15, 16, 20, 31, 32, 33, 47):
+                        code = int(c.coef_k[layer, h, t, i]) if z == 0 else int(c.coef_v[layer, h, t // 16, i, t % 16])
+                        want = code * float(sc[layer, h, i // 16, t])
+                        if rows[t - t0, i] != want:
+                            return f"int8 coefficient (layer {layer}, z {z}, h {h}, t {t}, i {i}) is not code * block scale"
+    c.coef_scale_k[:] = np.float16(0.125)
+    c.coef_scale_v[:] = np.float16(0.25)
+    twin = copy.deepcopy(c)
+    twin.coef_format = "f16"
+    twin.coef_k = (c.coef_k.astype(np.float64) * 0.125).astype(np.float16)
+    twin.coef_v = (c.coef_v.astype(np.float64) * 0.25).astype(np.float16)
+    for layer in range(c.n_layers):
+        if not np.array_equal(o.decode(c, layer), o.decode(twin, layer)):
+            return "int8 cache with power-of-two scales decodes differently from its fp16 twin"
+    return None
+
+
 ALL_PINS = [pin_query_formats, pin_nibbles, pin_residual_map, pin_brute_force, pin_closed_forms,
             pin_reductions, pin_invariants, pin_probe, pin_router, pin_compress_closed_forms,
             pin_compress_rne_table, pin_compress_arithmetic, pin_compress_bounds,
-            pin_compress_into_cache, pin_route_range, pin_attention_features, pin_control, pin_sketch]
+            pin_compress_into_cache, pin_route_range, pin_attention_features, pin_control, pin_sketch,
+            pin_int8_coefficients]
 
 
 def run_all(o):

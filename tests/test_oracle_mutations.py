@@ -279,6 +279,28 @@ def _sketch_transposed(x_rows, omega):
         if False else np.asarray(omega, np.float64)[:, ::-1] @ np.asarray(x_rows, np.float64)
 
 
+def _coef_rows_variant(kind):
+    orig = F.__dict__.setdefault("_orig_coefficient_rows", F.coefficient_rows)
+    def rows(cache, layer, z, h, t0, t1):
+        if getattr(cache, "coef_format", "f16") != "int8":
+            return orig(cache, layer, z, h, t0, t1)
+        if z == 0:
+            r = cache.coef_k[layer, h, t0:t1].astype(np.float64)
+        else:
+            blocks = cache.coef_v[layer, h]
+            r = np.swapaxes(blocks, 1, 2).reshape(-1, blocks.shape[1])[t0:t1].astype(np.float64)
+        sc = (cache.coef_scale_k if z == 0 else cache.coef_scale_v)[layer, h].astype(np.float64)   # [NB, T]
+        nb = sc.shape[0]
+        if kind == "block_mod":
+            idx = np.arange(r.shape[1]) % nb
+            return r * sc[idx][:, t0:t1].T
+        if kind == "next_token":
+            return r * np.repeat(sc[:, t0 + 1:t1 + 1].T if t1 < sc.shape[1] else
+                                 np.concatenate([sc[:, t0 + 1:t1], sc[:, t1 - 1:t1]], axis=1).T, 16, axis=1)
+        return r
+    return rows
+
+
 MUTANTS = {
     "residual dropped": [(F, "reconstruct", _reconstruct_variant("no_residual"))],
     "residual sign flipped": [(F, "reconstruct", _reconstruct_variant("residual_sign"))],
@@ -336,6 +358,9 @@ MUTANTS = {
     "budget count rounded up": [(CT, "budget_select", _budget_ceil)],
     "Gram-Schmidt rows scaled by max instead of norm": [(SK, "orthonormal_rows", _gs_no_normalize)],
     "sketch with the token order reversed": [(SK, "sketch", _sketch_transposed)],
+    "int8 block scale indexed by i mod blocks": [(F, "coefficient_rows", _coef_rows_variant("block_mod"))],
+    "int8 block scale of the next token": [(F, "coefficient_rows", _coef_rows_variant("next_token"))],
+    "int8 block scale ignored": [(F, "coefficient_rows", _coef_rows_variant("none"))],
     "bf16 query read as fp16": [(F, "q_to_f64", lambda bits, dtype: np.asarray(bits, np.uint16)
                                  .view(np.float16).astype(np.float64))],
 }
