@@ -29,17 +29,20 @@ def log(*a):
 
 def algorithmic_bytes_per_layer(host) -> list[float]:
     """Bytes one per-layer decode must move: the window's bases, the layer's
-    coefficient rows, the window's offsets, the layer's residual indices,
-    codes and scales, the query in and the fp32 output out."""
+    coefficient rows (fp16, or int8 codes with an fp16 scale per 16), the
+    window's offsets, the layer's residual indices, codes and scales, the query
+    in and the fp32 output out."""
     B, Hk, Hq, d = host.batch, host.n_kv_heads, host.n_q_heads, host.head_dim
     T, rb = host.total_tokens, host.basis_rank
     qbytes = 2
     out = []
+    c8 = getattr(host, "coef_format", "f16") == "int8"
+    coef_bytes = 2 * Hk * T * (rb + 2 * (rb // 16)) if c8 else 2 * Hk * T * rb * 2
     for l in range(host.n_layers):
         m = l // host.window
         ent = float(host.res_off[m, :, -1].astype(np.int64).sum())      # entries per Z over heads
         out.append(B * Hk * 2 * rb * d * 2          # bases B^K, B^V (fp16)
-                   + 2 * Hk * T * rb * 2            # coefficients A^K, A^V (fp16)
+                   + coef_bytes                     # coefficients A^K, A^V (fp16, or int8 + block scales)
                    + Hk * (T + 1) * 4               # offsets
                    + 2 * ent * 1 + 2 * ent / 2      # channel bytes + int4 codes, K and V
                    + 2 * Hk * T * 2                 # residual scales (fp16), K and V
@@ -137,6 +140,52 @@ def measure_append(dc, host, wl, torch, reps: int = 20):
             "prefill_compress_vectors_per_s": round(2 * Hk * T / (layer_ms / 1e3), 1),
             "note": "route_range of the new token in every window plus one dwkv_compress per layer "
                     "(graph replay); prefill = dwkv_compress of all T tokens of one layer, K and V"}
+
+
+def measure_int8(wl, torch, steps: int = 20, warmup: int = 5):
+    """The same workload with the paper's 8-bit blockwise coefficient form
+    (int8 codes, one fp16 scale per token and 16 coefficients): tokens/s of the
+    32-layer step and the split-K kernel's achieved bandwidth on its own bytes."""
+    from paper_2607_06523_amd import DeviceCache
+    from synth import generate
+    host = generate(wl.with_(coef_format="int8", name=wl.name + "-int8"))
+    dc = DeviceCache(host)
+    L = host.n_layers
+    stream = torch.cuda.current_stream()
+    ws = dc.workspace()
+    ws_layer = [dc.new_workspace() for _ in range(L)]
+    outs = [torch.empty((host.batch, host.n_q_heads, host.head_dim), dtype=torch.float32, device="cuda")
+            for _ in range(L)]
+    for _ in range(warmup):
+        for l in range(L):
+            dc.decode(l, out=outs[l], workspace=ws)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    ev[0].record(stream)
+    for _ in range(steps):
+        for l in range(L):
+            dc.decode(l, out=outs[l], workspace=ws)
+    ev[1].record(stream)
+    for l in range(L):
+        dc.decode_partials(l, workspace=ws_layer[l])
+    ev[2].record(stream)
+    for l in range(L):
+        dc.decode_merge(l, out=outs[l], workspace=ws_layer[l])
+    ev[3].record(stream)
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / steps
+    split_ms = ev[1].elapsed_time(ev[2]) / L
+    bl = float(np.mean(algorithmic_bytes_per_layer(host)))
+    achieved = bl / (split_ms / 1e3) / 1e9
+    res = {"tokens_per_s": round(host.batch / (ms / 1e3), 2), "ms_per_step": round(ms, 4),
+           "split_kernel_ms": round(split_ms, 5), "merge_kernel_ms": round(ev[2].elapsed_time(ev[3]) / L, 5),
+           "bytes_per_layer_call": int(bl), "achieved_gbps": round(achieved, 1),
+           "frac": round(achieved / HBM_PEAK_GBPS, 4),
+           "compression_vs_fp16": round(dense_fp16_bytes_per_layer(host) / bl, 3),
+           "note": "coefficients in the 8-bit blockwise form: int8 codes, one fp16 scale per token and 16 "
+                   "coefficients (tl_kernel int8 variant)"}
+    del dc, host
+    return res
 
 
 def measure_features(dc, host, torch, outs, steps: int = 5):
@@ -452,6 +501,8 @@ def main():
         "wall_s_timed": round(wall, 3),
     }
     if not args.no_comparators and args.variant == "full":
+        log("[bench] timing the 8-bit blockwise coefficient form")
+        result["coef_int8"] = measure_int8(wl, torch)
         log("[bench] timing the decode with router features")
         result["with_features"] = measure_features(dc, host, torch, outs)
     if not args.no_append and args.variant == "full":

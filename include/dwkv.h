@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define DWKV_ABI_VERSION 1
+#define DWKV_ABI_VERSION 2
 #define DWKV_MAX_LEVELS 8
 #define DWKV_MAX_PROBE_HEADS 64
 
@@ -47,7 +47,10 @@ typedef enum dwkv_status {
   DWKV_E_UNSUPPORTED = 3, /* consistent but not built: head_dim != 128,
                              G = Hq/Hkv not in {1,2,4,8,16}, r_b not a multiple of
                              16 in [16,128], more than 8 levels, 32-bit offset
-                             overflow possible                                    */
+                             overflow possible; int8 coefficients off the
+                             token-lane path (G <= 4, r_b <= 64, levels <= 16),
+                             with a probe, or in the calls that write or
+                             rebuild fp16 coefficients                            */
   DWKV_E_WORKSPACE = 4,   /* workspace smaller than the *_workspace_bytes value    */
   DWKV_E_LAYOUT = 5,      /* dwkv_validate found a malformed cache                 */
   DWKV_E_HIP = 6,         /* a HIP runtime call or kernel launch failed            */
@@ -74,8 +77,14 @@ typedef struct dwkv_dims {
                              of 256 and >= the largest slab total + 512            */
   int32_t split_tokens;   /* tokens per workgroup chunk; 0 = automatic, otherwise a
                              multiple of 64                                        */
-  int32_t reserved;
+  int32_t coef_format;    /* DWKV_COEF_F16 or DWKV_COEF_I8 (see dwkv_cache)        */
 } dwkv_dims;
+
+/* Coefficient storage.  DWKV_COEF_F16: fp16 rows.  DWKV_COEF_I8: the paper's
+ * 8-bit blockwise form (Sec. 3): per token, each block of 16 coefficients
+ * [16 s, 16 s + 16) is an fp16 scale times int8 codes in [-127, 127],
+ * A_i = scale_{t, i/16} * code_i. */
+typedef enum dwkv_coef_format { DWKV_COEF_F16 = 0, DWKV_COEF_I8 = 1 } dwkv_coef_format;
 
 /* Compressed cache (Eq. 1 factors).  M = L / window, Z = 0 keys, Z = 1 values. */
 typedef struct dwkv_cache {
@@ -92,6 +101,12 @@ typedef struct dwkv_cache {
   const uint8_t*  res_val;   /* [L][2][Hkv][res_stride/2] int4 two's-complement codes;
                                 entry e in byte e/2, low nibble when e is even; -8 invalid */
   const void*     res_scale; /* fp16 [L][2][Hkv][T] gate-folded residual scale g*s         */
+  const void*     coef_k_scale; /* DWKV_COEF_I8 only (else ignored): fp16 [L][Hkv][r_b/16][T]
+                                block scales of the key coefficients; coef_k then holds int8
+                                codes [L][Hkv][T][r_b]                                      */
+  const void*     coef_v_scale; /* DWKV_COEF_I8 only: fp16 [L][Hkv][r_b/16][T] value block
+                                scales; coef_v then holds int8 codes [L][Hkv][T16/16][r_b][16]
+                                (the blocked layout, one byte per entry)                      */
 } dwkv_cache;
 
 /* Attention-output probe (Eq. 3) against a dense higher-fidelity cache. */

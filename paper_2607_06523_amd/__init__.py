@@ -60,8 +60,16 @@ class DeviceCache:
         dev = self.device
         up = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).view(dt).to(dev)
         self.basis = up(host.basis.view(np.uint16), torch.float16)
-        self.coef_k = up(host.coef_k.view(np.uint16), torch.float16)
-        self.coef_v = up(host.coef_v.view(np.uint16), torch.float16)
+        self.coef_format = getattr(host, "coef_format", "f16")
+        if self.coef_format == "int8":        # codes and their fp16 block scales
+            self.coef_k = up(host.coef_k.view(np.uint8), torch.uint8)
+            self.coef_v = up(host.coef_v.view(np.uint8), torch.uint8)
+            self.coef_scale_k = up(host.coef_scale_k.view(np.uint16), torch.float16)
+            self.coef_scale_v = up(host.coef_scale_v.view(np.uint16), torch.float16)
+        else:
+            self.coef_k = up(host.coef_k.view(np.uint16), torch.float16)
+            self.coef_v = up(host.coef_v.view(np.uint16), torch.float16)
+            self.coef_scale_k = self.coef_scale_v = None
         self.rank_code = up(host.rank_code, torch.uint8)
         self.res_off = up(host.res_off.view(np.int32), torch.int32)
         self.res_idx = up(host.res_idx, torch.uint8)
@@ -91,12 +99,15 @@ class DeviceCache:
             n_kv_heads=self.n_kv_heads, n_q_heads=self.n_q_heads, head_dim=self.head_dim,
             basis_rank=self.basis_rank, levels=self.levels, cu_seqlens_host=self.cu_host,
             cu_seqlens_dev_ptr=self.cu.data_ptr(), total_tokens=self.total_tokens,
-            res_stride=self.res_stride, split_tokens=split_tokens)
+            res_stride=self.res_stride, split_tokens=split_tokens,
+            coef_format=binding.COEF_I8 if self.coef_format == "int8" else binding.COEF_F16)
         c = binding.Cache()
         c.basis, c.rank_code = self.basis.data_ptr(), self.rank_code.data_ptr()
         c.coef_k, c.coef_v = self.coef_k.data_ptr(), self.coef_v.data_ptr()
         c.res_off, c.res_idx, c.res_val = self.res_off.data_ptr(), self.res_idx.data_ptr(), self.res_val.data_ptr()
         c.res_scale = self.res_scale.data_ptr()
+        if self.coef_scale_k is not None:
+            c.coef_k_scale, c.coef_v_scale = self.coef_scale_k.data_ptr(), self.coef_scale_v.data_ptr()
         self.cstruct = c
         self._ws = {}
 

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(HERE, "_lib", "libdwkv.so")
 MAX_LEVELS = 8
 MAX_PROBE_HEADS = 64
 F16, BF16 = 0, 1
+COEF_F16, COEF_I8 = 0, 1
 
 STATUS = {0: "ok", 1: "null pointer", 2: "inconsistent dimensions", 3: "unsupported shape",
           4: "workspace too small", 5: "malformed cache layout", 6: "HIP runtime error"}
@@ -35,14 +36,14 @@ class Dims(C.Structure):
                 ("levels", C.c_int32 * MAX_LEVELS),
                 ("cu_seqlens_host", C.POINTER(C.c_int32)), ("cu_seqlens", C.c_void_p),
                 ("total_tokens", C.c_int64), ("res_stride", C.c_int64),
-                ("split_tokens", C.c_int32), ("reserved", C.c_int32)]
+                ("split_tokens", C.c_int32), ("coef_format", C.c_int32)]
 
 
 class Cache(C.Structure):
     _fields_ = [("basis", C.c_void_p), ("coef_k", C.c_void_p), ("coef_v", C.c_void_p),
                 ("rank_code", C.c_void_p),
                 ("res_off", C.c_void_p), ("res_idx", C.c_void_p), ("res_val", C.c_void_p),
-                ("res_scale", C.c_void_p)]
+                ("res_scale", C.c_void_p), ("coef_k_scale", C.c_void_p), ("coef_v_scale", C.c_void_p)]
 
 
 class Controller(C.Structure):
@@ -145,7 +146,7 @@ def check(status: int, where: str):
 
 
 def make_dims(*, batch, n_layers, window, n_kv_heads, n_q_heads, head_dim, basis_rank, levels,
-              cu_seqlens_host, cu_seqlens_dev_ptr, total_tokens, res_stride, split_tokens=0):
+              cu_seqlens_host, cu_seqlens_dev_ptr, total_tokens, res_stride, split_tokens=0, coef_format=0):
     """Fill a Dims struct; returns (dims, keepalive) -- keep both alive while in use."""
     cu = np.ascontiguousarray(cu_seqlens_host, dtype=np.int32)
     d = Dims()
@@ -157,4 +158,5 @@ def make_dims(*, batch, n_layers, window, n_kv_heads, n_q_heads, head_dim, basis
     d.cu_seqlens_host = cu.ctypes.data_as(C.POINTER(C.c_int32))
     d.cu_seqlens = cu_seqlens_dev_ptr
     d.total_tokens, d.res_stride, d.split_tokens = total_tokens, res_stride, split_tokens
+    d.coef_format = coef_format
     return d, cu

@@ -48,6 +48,7 @@ dwkv_status check_dims(const dwkv_dims* d) {
   if ((int64_t)d->cu_seqlens_host[d->batch] != d->total_tokens) return DWKV_E_DIMS;
   if (d->res_stride < kResTailPad || d->res_stride % 256 != 0) return DWKV_E_DIMS;
   if (d->split_tokens % 64 != 0) return DWKV_E_DIMS;
+  if (d->coef_format != DWKV_COEF_F16 && d->coef_format != DWKV_COEF_I8) return DWKV_E_DIMS;
   // offsets, plus a few chunks of slack, must stay inside 32 bits
   if ((double)d->total_tokens * (double)max_level(d) + 65536.0 > 4294967295.0) return DWKV_E_UNSUPPORTED;
   return DWKV_OK;
@@ -209,6 +210,13 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
     return DWKV_E_NULL;
   if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
   if (q_type != DWKV_F16 && q_type != DWKV_BF16) return DWKV_E_DIMS;
+  const bool c8 = d->coef_format == DWKV_COEF_I8;
+  if (c8) {
+    if (!uses_token_lane(d) || probe || scores) return DWKV_E_UNSUPPORTED;
+    if (!c->coef_k_scale || !c->coef_v_scale) return DWKV_E_NULL;
+    if ((reinterpret_cast<uintptr_t>(c->coef_k_scale) | reinterpret_cast<uintptr_t>(c->coef_v_scale)) & 1u)
+      return DWKV_E_ALIGN;
+  }
   const void* const ptrs[] = {q, c->basis, c->coef_k, c->coef_v, c->res_off, c->res_idx, c->res_val, c->res_scale};
   for (const void* p : ptrs)
     if (!aligned16(p)) return DWKV_E_ALIGN;
@@ -230,8 +238,15 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
 
   SplitArgs a;
   std::memset(&a, 0, sizeof(a));
-  a.coef_k = static_cast<const uint16_t*>(c->coef_k) + (int64_t)layer * Hk * T * RB;
-  a.coef_v = static_cast<const uint16_t*>(c->coef_v) + (int64_t)layer * Hk * T16 * RB;
+  if (c8) {                     // int8 codes: one byte per coefficient
+    a.coef_k = reinterpret_cast<const uint16_t*>(static_cast<const uint8_t*>(c->coef_k) + (int64_t)layer * Hk * T * RB);
+    a.coef_v = reinterpret_cast<const uint16_t*>(static_cast<const uint8_t*>(c->coef_v) + (int64_t)layer * Hk * T16 * RB);
+    a.cscale_k = static_cast<const uint16_t*>(c->coef_k_scale) + (int64_t)layer * Hk * (RB / 16) * T;
+    a.cscale_v = static_cast<const uint16_t*>(c->coef_v_scale) + (int64_t)layer * Hk * (RB / 16) * T;
+  } else {
+    a.coef_k = static_cast<const uint16_t*>(c->coef_k) + (int64_t)layer * Hk * T * RB;
+    a.coef_v = static_cast<const uint16_t*>(c->coef_v) + (int64_t)layer * Hk * T16 * RB;
+  }
   a.basis = static_cast<const uint16_t*>(c->basis) + (int64_t)m * Hk * 2 * RB * kHeadDim;
   a.basis_b_stride = (int64_t)M * Hk * 2 * RB * kHeadDim;
   a.off = c->res_off + (int64_t)m * Hk * (T + 1);
@@ -257,7 +272,8 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
   a.wt = work_table(d, split);
   a.scores = scores;
-  const hipError_t e = uses_token_lane(d)
+  const hipError_t e = c8 ? launch_split_tl_c8(RB, G, max_level(d) > 0, a, (int)nw, s)
+                       : uses_token_lane(d)
                            ? (scores ? launch_split_tl_scores(RB, G, max_level(d) > 0, a, (int)nw, s)
                                      : launch_split_tl(RB, G, max_level(d) > 0, a, (int)nw, s))
                            : launch_split(RB, G, max_level(d) > 0, false, a, (int)nw, s);
@@ -456,6 +472,7 @@ dwkv_status dwkv_compress(const dwkv_dims* d, const dwkv_cache* c, int32_t layer
                           const void* x_v, const float* gate, int64_t t0, int64_t t1, void* stream) {
   dwkv_status st = check_dims(d);
   if (st != DWKV_OK) return st;
+  if (d->coef_format != DWKV_COEF_F16) return DWKV_E_UNSUPPORTED;
   if (!c || !c->basis || !c->coef_k || !c->coef_v || !c->rank_code || !c->res_off || !c->res_idx ||
       !c->res_val || !c->res_scale)
     return DWKV_E_NULL;
@@ -559,6 +576,7 @@ dwkv_status dwkv_materialize(const dwkv_dims* d, const dwkv_cache* c, int32_t la
                              void* v_out, void* stream) {
   dwkv_status st = check_dims(d);
   if (st != DWKV_OK) return st;
+  if (d->coef_format != DWKV_COEF_F16) return DWKV_E_UNSUPPORTED;
   if (!c || !c->basis || !c->coef_k || !c->coef_v || !c->res_off || !c->res_idx || !c->res_val ||
       !c->res_scale || !k_out || !v_out)
     return DWKV_E_NULL;
@@ -666,6 +684,7 @@ dwkv_status dwkv_decode_features(const dwkv_dims* d, const dwkv_cache* c, int32_
                                  size_t ws_bytes, void* stream) {
   dwkv_status st = check_decode_common(d, nullptr, workspace, ws_bytes);
   if (st != DWKV_OK) return st;
+  if (d->coef_format != DWKV_COEF_F16) return DWKV_E_UNSUPPORTED;
   if (!uses_token_lane(d)) return DWKV_E_UNSUPPORTED;
   if (!out || !phi) return DWKV_E_NULL;
   if (!aligned16(out) || !aligned16(phi)) return DWKV_E_ALIGN;

@@ -86,10 +86,20 @@ struct alignas(16) TSmem {
   alignas(16) float pw[kTW][RESID ? TT : 1][HG];  // p * value scale per token lane
 };
 
-template <int RB>
+template <int RB, bool C8>
 struct TFrags {
   uint2 k[4][TCfg<RB>::NS];             // key rows, block bk, k-step s
   uint2 v[16];                          // value channel `lane`, token quad q
+};
+
+// int8-blockwise coefficients: 4 codes per dword, and the lane's own token's
+// block scales (block s covers coefficients [16 s, 16 s + 16))
+template <int RB>
+struct TFrags<RB, true> {
+  uint32_t k[4][TCfg<RB>::NS];          // token 16 bk + col, coefficients 16 s + 4 grp + (0..3)
+  uint32_t v[16];                       // channel `lane`, the 4 tokens of quad q
+  uint32_t ks[TCfg<RB>::NS];            // key scale bits of block s, token `lane`
+  uint32_t vs[TCfg<RB>::NS];            // value scale bits of block s, token `lane`
 };
 
 struct TMeta {
@@ -102,10 +112,12 @@ struct TEnt {
   uint32_t vc[kVB], vv[kVB];            // value entries e0 + 64b + lane: channel byte, code byte
 };
 
-template <int RB>
+template <int RB, bool C8>
 struct TState {
+  static constexpr int NACC = C8 ? TCfg<RB>::NS : 1;
   h4 qhi[TCfg<RB>::NS], qlo[TCfg<RB>::NS];
-  f4 acc_h, acc_l;                      // a~[head][channel lane] from p hi / p lo
+  f4 acc_h[NACC], acc_l[NACC];          // a~[head][channel lane] from p hi / p lo (int8: one pair
+                                        // per coefficient block, each valid in its block's lanes)
   float m[HG], l[HG], down[HG];
   int ex;                               // bound on the value scales seen: |s_v| < 2^ex
 };
@@ -127,6 +139,8 @@ struct TCtx {
   int32_t c0, c1, tb;                   // chunk [c0, c1); tiles start at tb = c0 & ~15
   int32_t ntile;
   float* sco;                           // raw scores of this slot [T][G] (score-storing pass only)
+  rsrc_t cks, cvs;                      // int8 coefficients: block scales [NS][T] (fp16)
+  int32_t T;
 };
 
 __device__ __forceinline__ f4 mfma16(h4 a, h4 b, f4 c) {
@@ -150,7 +164,7 @@ __device__ __forceinline__ float code_at(uint32_t w, int n) {
 }
 
 template <int RB>
-__device__ __forceinline__ void load_k(TFrags<RB>& f, const TCtx& x, int j, int lane) {
+__device__ __forceinline__ void load_k(TFrags<RB, false>& f, const TCtx& x, int j, int lane) {
   using C = TCfg<RB>;
   const int grp = lane >> 4, col = lane & 15;
   const uint32_t base = (uint32_t)(tstart(x, j) + col) * (RB * 2) + C::KH * grp * 2;
@@ -170,7 +184,7 @@ __device__ __forceinline__ void load_k(TFrags<RB>& f, const TCtx& x, int j, int 
 }
 
 template <int RB>
-__device__ __forceinline__ void load_v(TFrags<RB>& f, const TCtx& x, int j, int lane) {
+__device__ __forceinline__ void load_v(TFrags<RB, false>& f, const TCtx& x, int j, int lane) {
   // lanes past r_b read neighbouring data whose products are never used
   const uint32_t base = ((uint32_t)(tstart(x, j) >> 4) * RB + lane) * 32;
 #pragma unroll
@@ -179,6 +193,52 @@ __device__ __forceinline__ void load_v(TFrags<RB>& f, const TCtx& x, int j, int 
     f.v[q] = make_uint2(w.x, w.y);
     f.v[q + 1] = make_uint2(w.z, w.w);
   }
+}
+
+// 4 signed bytes to fp16, in the order (b0, b2, b1, b3): each byte, offset by
+// 128, becomes the low byte of the fp16 number 1024 + byte, exact, then
+// 1152 is subtracted.  Operands built from these take the same k order.
+__device__ __forceinline__ h4 i8x4_to_h4(uint32_t w) {
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  const uint32_t u = w ^ 0x80808080u;
+  const h2 lo = __builtin_bit_cast(h2, __builtin_amdgcn_perm(0x64646464u, u, 0x04020400u)) - h2{1152, 1152};
+  const h2 hi = __builtin_bit_cast(h2, __builtin_amdgcn_perm(0x64646464u, u, 0x04030401u)) - h2{1152, 1152};
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3);
+}
+
+template <int RB>
+__device__ __forceinline__ void load_k8(TFrags<RB, true>& f, const TCtx& x, int j, int lane) {
+  using C = TCfg<RB>;
+  const int grp = lane >> 4, col = lane & 15;
+  const uint32_t base = (uint32_t)(tstart(x, j) + col) * RB + 4 * grp;
+#pragma unroll
+  for (int bk = 0; bk < 4; ++bk)
+#pragma unroll
+    for (int s = 0; s < C::NS; ++s)
+      f.k[bk][s] = __builtin_amdgcn_raw_buffer_load_b32(x.ck, base + bk * 16 * RB + 16 * s, 0, 0);
+  const uint32_t t = (uint32_t)(tstart(x, j) + lane);
+#pragma unroll
+  for (int s = 0; s < C::NS; ++s)
+    f.ks[s] = __builtin_amdgcn_raw_buffer_load_b16(x.cks, ((uint32_t)s * (uint32_t)x.T + t) * 2, 0, 0);
+}
+
+template <int RB>
+__device__ __forceinline__ void load_v8(TFrags<RB, true>& f, const TCtx& x, int j, int lane) {
+  using C = TCfg<RB>;
+  // 16 bytes per (16-token block, channel): the 16 tokens' codes of channel `lane`
+  const uint32_t base = ((uint32_t)(tstart(x, j) >> 4) * RB + lane) * 16;
+#pragma unroll
+  for (int tb = 0; tb < 4; ++tb) {
+    const u4v w = __builtin_amdgcn_raw_buffer_load_b128(x.cv, base + tb * RB * 16, 0, 0);
+    f.v[4 * tb] = w.x;
+    f.v[4 * tb + 1] = w.y;
+    f.v[4 * tb + 2] = w.z;
+    f.v[4 * tb + 3] = w.w;
+  }
+  const uint32_t t = (uint32_t)(tstart(x, j) + lane);
+#pragma unroll
+  for (int s = 0; s < C::NS; ++s)
+    f.vs[s] = __builtin_amdgcn_raw_buffer_load_b16(x.cvs, ((uint32_t)s * (uint32_t)x.T + t) * 2, 0, 0);
 }
 
 // Entry range of the lane's token, clipped to the chunk (tokens outside it own
@@ -300,8 +360,15 @@ __device__ __forceinline__ void pv_tile(f4& acc_h, f4& acc_l, h4 ph, h4 pl, cons
   (pv_quad<Q>(acc_h, acc_l, ph, pl, v[Q]), ...);
 }
 
-template <int RB, int G, bool RESID, bool SCORES>
-__device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc, TMeta& mn, TMeta& mnn,
+template <int... Q>
+__device__ __forceinline__ void pv_tile_h(f4& acc_h, f4& acc_l, h4 ph, h4 pl, const h4 (&v)[16],
+                                          std::integer_sequence<int, Q...>) {
+  ((acc_h = __builtin_amdgcn_mfma_f32_4x4x4f16(ph, v[Q], acc_h, 4, Q, 0),
+    acc_l = __builtin_amdgcn_mfma_f32_4x4x4f16(pl, v[Q], acc_l, 4, Q, 0)), ...);
+}
+
+template <int RB, int G, bool RESID, bool SCORES, bool C8>
+__device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TMeta& mc, TMeta& mn, TMeta& mnn,
                                       TEnt& ec, TEnt& en, int j, int jn, int jnn, const TCtx& x,
                                       TSmem<RB, RESID>& sm, int wv, int lane) {
   using C = TCfg<RB>;
@@ -353,23 +420,41 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   f4 sacc[4];
 #pragma unroll
   for (int bk = 0; bk < 4; ++bk) sacc[bk] = f4{0.f, 0.f, 0.f, 0.f};
+  if constexpr (C8) {
+    // one 16-deep product per coefficient block, scaled by the lane's own
+    // token's block scale (other blocks' lanes are discarded below)
 #pragma unroll
-  for (int s = 0; s + 1 < NS; s += 2)
+    for (int s = 0; s < NS; ++s) {
+      const float ksc = half_bits_to_float((uint16_t)fr.ks[s]);
 #pragma unroll
-    for (int bk = 0; bk < 4; ++bk) {
-      const h4 k0 = __builtin_bit_cast(h4, fr.k[bk][s]), k1 = __builtin_bit_cast(h4, fr.k[bk][s + 1]);
-      sacc[bk] = mfma32(st.qhi[s], st.qhi[s + 1], k0, k1, sacc[bk]);
-      sacc[bk] = mfma32(st.qlo[s], st.qlo[s + 1], k0, k1, sacc[bk]);
+      for (int bk = 0; bk < 4; ++bk) {
+        const h4 kf = i8x4_to_h4(fr.k[bk][s]);
+        f4 o = mfma16(st.qhi[s], kf, f4{0.f, 0.f, 0.f, 0.f});
+        o = mfma16(st.qlo[s], kf, o);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sacc[bk][i] += o[i] * ksc;
+      }
     }
-  if constexpr (NS % 2 == 1) {
+    load_k8<RB>(fr, x, jn_l, lane);
+  } else {
 #pragma unroll
-    for (int bk = 0; bk < 4; ++bk) {
-      const h4 kf = __builtin_bit_cast(h4, fr.k[bk][NS - 1]);
-      sacc[bk] = mfma16(st.qhi[NS - 1], kf, sacc[bk]);
-      sacc[bk] = mfma16(st.qlo[NS - 1], kf, sacc[bk]);
+    for (int s = 0; s + 1 < NS; s += 2)
+#pragma unroll
+      for (int bk = 0; bk < 4; ++bk) {
+        const h4 k0 = __builtin_bit_cast(h4, fr.k[bk][s]), k1 = __builtin_bit_cast(h4, fr.k[bk][s + 1]);
+        sacc[bk] = mfma32(st.qhi[s], st.qhi[s + 1], k0, k1, sacc[bk]);
+        sacc[bk] = mfma32(st.qlo[s], st.qlo[s + 1], k0, k1, sacc[bk]);
+      }
+    if constexpr (NS % 2 == 1) {
+#pragma unroll
+      for (int bk = 0; bk < 4; ++bk) {
+        const h4 kf = __builtin_bit_cast(h4, fr.k[bk][NS - 1]);
+        sacc[bk] = mfma16(st.qhi[NS - 1], kf, sacc[bk]);
+        sacc[bk] = mfma16(st.qlo[NS - 1], kf, sacc[bk]);
+      }
     }
+    load_k<RB>(fr, x, jn_l, lane);
   }
-  load_k<RB>(fr, x, jn_l, lane);
   float sc[HG];
 #pragma unroll
   for (int i = 0; i < HG; ++i) {
@@ -445,8 +530,11 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
         alpha[i] = mnew == -INFINITY ? 1.0f : exp2f(st.m[i] - mnew);
         st.m[i] = mnew;
         st.l[i] *= alpha[i];
-        st.acc_h[i] *= alpha[i];
-        st.acc_l[i] *= alpha[i];
+#pragma unroll
+        for (int b = 0; b < TState<RB, C8>::NACC; ++b) {
+          st.acc_h[b][i] *= alpha[i];
+          st.acc_l[b][i] *= alpha[i];
+        }
       }
       if constexpr (RESID) {
 #pragma unroll
@@ -466,7 +554,29 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
   }
 
   // 5. a~ += P A^V: quad transpose, fp16 hi + lo, one 4x4x4 pair per quad
-  {
+  if constexpr (C8) {
+    // int8: the codes are exact fp16 operands; the value block scale of each
+    // token goes into its probabilities, one pass per coefficient block
+    h4 vb[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) vb[q] = i8x4_to_h4(fr.v[q]);
+#pragma unroll
+    for (int b = 0; b < NS; ++b) {
+      const float vsc = half_bits_to_float((uint16_t)fr.vs[b]);
+      float pt[4] = {p[0] * vsc, p[1] * vsc, p[2] * vsc, p[3] * vsc};
+      quad_transpose(pt, lane);
+      h4 ph, pl;
+      constexpr int ord[4] = {0, 2, 1, 3};      // the k order of i8x4_to_h4
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const _Float16 hh = (_Float16)pt[ord[i]];
+        ph[i] = hh;
+        pl[i] = (_Float16)(pt[ord[i]] - (float)hh);
+      }
+      pv_tile_h(st.acc_h[b], st.acc_l[b], ph, pl, vb, std::make_integer_sequence<int, 16>{});
+    }
+    load_v8<RB>(fr, x, jn_l, lane);
+  } else {
     float pt[4] = {p[0], p[1], p[2], p[3]};
     quad_transpose(pt, lane);
     h4 ph, pl;
@@ -476,9 +586,9 @@ __device__ __forceinline__ void tstep(TState<RB>& st, TFrags<RB>& fr, TMeta& mc,
       ph[i] = hh;
       pl[i] = (_Float16)(pt[i] - (float)hh);
     }
-    pv_tile(st.acc_h, st.acc_l, ph, pl, fr.v, std::make_integer_sequence<int, 16>{});
+    pv_tile(st.acc_h[0], st.acc_l[0], ph, pl, fr.v, std::make_integer_sequence<int, 16>{});
+    load_v<RB>(fr, x, jn_l, lane);
   }
-  load_v<RB>(fr, x, jn_l, lane);
 
   // 6. value residual, one lane per entry: p * code * scale into the channel
   // accumulators.  Token lanes publish p * scale; entry lanes read their
@@ -658,7 +768,7 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const SplitArgs a
   }
 }
 
-template <int RB, int G, bool RESID, bool SCORES>
+template <int RB, int G, bool RESID, bool SCORES, bool C8>
 __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   using C = TCfg<RB>;
   constexpr int NS = C::NS;
@@ -686,8 +796,18 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   x.sco = SCORES ? a.scores + (int64_t)slot * a.T * G : nullptr;
   {
     const int64_t T = a.T, nblk = (T + 15) / 16, rs = a.res_stride;
-    x.ck = make_rsrc(a.coef_k + (int64_t)slot * T * RB, (uint32_t)(T * RB * 2));
-    x.cv = make_rsrc(a.coef_v + (int64_t)slot * nblk * 16 * RB, (uint32_t)(nblk * 16 * RB * 2));
+    x.T = (int32_t)T;
+    if constexpr (C8) {
+      const uint8_t* ck8 = reinterpret_cast<const uint8_t*>(a.coef_k);
+      const uint8_t* cv8 = reinterpret_cast<const uint8_t*>(a.coef_v);
+      x.ck = make_rsrc(ck8 + (int64_t)slot * T * RB, (uint32_t)(T * RB));
+      x.cv = make_rsrc(cv8 + (int64_t)slot * nblk * 16 * RB, (uint32_t)(nblk * 16 * RB));
+      x.cks = make_rsrc(a.cscale_k + (int64_t)slot * C::NS * T, (uint32_t)(C::NS * T * 2));
+      x.cvs = make_rsrc(a.cscale_v + (int64_t)slot * C::NS * T, (uint32_t)(C::NS * T * 2));
+    } else {
+      x.ck = make_rsrc(a.coef_k + (int64_t)slot * T * RB, (uint32_t)(T * RB * 2));
+      x.cv = make_rsrc(a.coef_v + (int64_t)slot * nblk * 16 * RB, (uint32_t)(nblk * 16 * RB * 2));
+    }
     if constexpr (RESID) {
       x.off = make_rsrc(a.off + (int64_t)kvh * (T + 1), (uint32_t)((T + 1) * 4));
       x.idx[0] = make_rsrc(a.idx_k + (int64_t)kvh * rs, (uint32_t)rs);
@@ -709,7 +829,7 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   constexpr int QPT = (G * D + kTThreads - 1) / kTThreads;     // query elements per thread
   const int j0 = min(wv, x.ntile - 1);
   const int j1 = min(wv + kTW, x.ntile - 1);
-  TFrags<RB> fr;
+  TFrags<RB, C8> fr;
   TMeta mc{}, mn{}, mnn{};
   TEnt ec{}, en{};
   // q~ fragments, waves below NS only: wave w takes basis rows [16w, 16w+16)
@@ -737,8 +857,13 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
     load_offsets(mn, x, j1, lane);
   }
   __builtin_amdgcn_sched_barrier(0);
-  load_k<RB>(fr, x, j0, lane);
-  load_v<RB>(fr, x, j0, lane);
+  if constexpr (C8) {
+    load_k8<RB>(fr, x, j0, lane);
+    load_v8<RB>(fr, x, j0, lane);
+  } else {
+    load_k<RB>(fr, x, j0, lane);
+    load_v<RB>(fr, x, j0, lane);
+  }
   __builtin_amdgcn_sched_barrier(0);
   if constexpr (RESID) load_entries(ec, x, mc, lane);
 
@@ -808,7 +933,7 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   // q~ as the A operand (row = head, repeated per 4 rows), scaled per head by
   // a power of two so its largest entry sits just under 2^14, split into fp16
   // hi + lo; the score of head i is scaled back by down[i]
-  TState<RB> st;
+  TState<RB, C8> st;
   {
     const int h = col & 3;
     float up = 1.0f;
@@ -831,15 +956,21 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
     for (int s = 0; s < NS; ++s) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int k = C::KH * grp + 4 * s + i;
+        // fp16: lane group grp holds coefficients [KH grp, KH grp + KH); int8:
+        // k-step s is coefficient block s, in the byte order of i8x4_to_h4
+        constexpr int ord[4] = {0, 2, 1, 3};
+        const int k = C8 ? 16 * s + 4 * grp + ord[i] : C::KH * grp + 4 * s + i;
         const float v = h < G ? sm.qt[h][k] * up : 0.f;
         const _Float16 hh = (_Float16)v;
         st.qhi[s][i] = hh;
         st.qlo[s][i] = (_Float16)(v - (float)hh);
       }
     }
-    st.acc_h = f4{0.f, 0.f, 0.f, 0.f};
-    st.acc_l = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int b = 0; b < TState<RB, C8>::NACC; ++b) {
+      st.acc_h[b] = f4{0.f, 0.f, 0.f, 0.f};
+      st.acc_l[b] = f4{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
     for (int i = 0; i < HG; ++i) {
       st.m[i] = -INFINITY;
@@ -855,7 +986,7 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   // tiles wv, wv + 8, wv + 16, ...: a fixed assignment keeps the summation
   // order, and so the result, independent of timing
   for (int j = wv; j < x.ntile; j += kTW)
-    tstep<RB, G, RESID, SCORES>(st, fr, mc, mn, mnn, ec, en, j, j + kTW, j + 2 * kTW, x, sm, wv, lane);
+    tstep<RB, G, RESID, SCORES, C8>(st, fr, mc, mn, mnn, ec, en, j, j + kTW, j + 2 * kTW, x, sm, wv, lane);
 
   // epilogue: the waves combine; the partial keeps a~ in basis space (the
   // merge projects it through B^V once per sequence and head).  Each wave
@@ -887,8 +1018,14 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
     }
   }
   if (lane < RB) {
+    f4 ah = st.acc_h[0], al = st.acc_l[0];
+    if constexpr (C8) {                 // lane c keeps the pass of its coefficient block c / 16
 #pragma unroll
-    for (int i = 0; i < HG; ++i) sm.ep_a[wv][i][lane] = st.acc_h[i] + st.acc_l[i];
+      for (int b = 1; b < TState<RB, C8>::NACC; ++b)
+        if ((lane >> 4) == b) { ah = st.acc_h[b]; al = st.acc_l[b]; }
+    }
+#pragma unroll
+    for (int i = 0; i < HG; ++i) sm.ep_a[wv][i][lane] = ah[i] + al[i];
   }
   __syncthreads();
   constexpr int ROW = D + RB;                 // r[d] then a~[r_b]
@@ -925,29 +1062,29 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   }
 }
 
-template <int RB, int G, bool R, bool S>
+template <int RB, int G, bool R, bool S, bool C8>
 hipError_t launch_tl_t(const SplitArgs& a, int n_work, hipStream_t s) {
-  hipLaunchKernelGGL((tl_kernel<RB, G, R, S>), dim3(n_work, a.n_slots), dim3(kTThreads), 0, s, a);
+  hipLaunchKernelGGL((tl_kernel<RB, G, R, S, C8>), dim3(n_work, a.n_slots), dim3(kTThreads), 0, s, a);
   return hipGetLastError();
 }
 
-template <int RB, bool R, bool S>
+template <int RB, bool R, bool S, bool C8>
 hipError_t launch_tl_g(int g, const SplitArgs& a, int n_work, hipStream_t s) {
   switch (g) {
-    case 1: return launch_tl_t<RB, 1, R, S>(a, n_work, s);
-    case 2: return launch_tl_t<RB, 2, R, S>(a, n_work, s);
-    case 4: return launch_tl_t<RB, 4, R, S>(a, n_work, s);
+    case 1: return launch_tl_t<RB, 1, R, S, C8>(a, n_work, s);
+    case 2: return launch_tl_t<RB, 2, R, S, C8>(a, n_work, s);
+    case 4: return launch_tl_t<RB, 4, R, S, C8>(a, n_work, s);
   }
   return hipErrorInvalidValue;
 }
 
-template <bool R, bool S>
+template <bool R, bool S, bool C8>
 hipError_t launch_tl_rb(int rb, int g, const SplitArgs& a, int n_work, hipStream_t s) {
   switch (rb) {
-    case 16: return launch_tl_g<16, R, S>(g, a, n_work, s);
-    case 32: return launch_tl_g<32, R, S>(g, a, n_work, s);
-    case 48: return launch_tl_g<48, R, S>(g, a, n_work, s);
-    case 64: return launch_tl_g<64, R, S>(g, a, n_work, s);
+    case 16: return launch_tl_g<16, R, S, C8>(g, a, n_work, s);
+    case 32: return launch_tl_g<32, R, S, C8>(g, a, n_work, s);
+    case 48: return launch_tl_g<48, R, S, C8>(g, a, n_work, s);
+    case 64: return launch_tl_g<64, R, S, C8>(g, a, n_work, s);
   }
   return hipErrorInvalidValue;
 }
@@ -974,11 +1111,18 @@ bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t 
 }
 
 hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {
-  return resid ? launch_tl_rb<true, false>(rb, g, a, n_work, s) : launch_tl_rb<false, false>(rb, g, a, n_work, s);
+  return resid ? launch_tl_rb<true, false, false>(rb, g, a, n_work, s)
+               : launch_tl_rb<false, false, false>(rb, g, a, n_work, s);
 }
 
 hipError_t launch_split_tl_scores(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {
-  return resid ? launch_tl_rb<true, true>(rb, g, a, n_work, s) : launch_tl_rb<false, true>(rb, g, a, n_work, s);
+  return resid ? launch_tl_rb<true, true, false>(rb, g, a, n_work, s)
+               : launch_tl_rb<false, true, false>(rb, g, a, n_work, s);
+}
+
+hipError_t launch_split_tl_c8(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {
+  return resid ? launch_tl_rb<true, false, true>(rb, g, a, n_work, s)
+               : launch_tl_rb<false, false, true>(rb, g, a, n_work, s);
 }
 
 hipError_t launch_merge_tl(int rb, int g, const SplitArgs& a, hipStream_t s) {

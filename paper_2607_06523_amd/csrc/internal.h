@@ -50,6 +50,8 @@ struct SplitArgs {
   float* part;                 // [work][n_slots][G][kPartStride]; token-lane: [n_slots][work][G][kPartStrideTL]
   float* out;                  // [B][Hq][d], written by the token-lane merge launch
   float* scores;               // [n_slots][T][G] raw scores in exp2 units (token-lane pass with scores only)
+  const uint16_t* cscale_k;    // int8 coefficients: key block scales, slot 0 [r_b/16][T]; slot s adds s*(r_b/16)*T
+  const uint16_t* cscale_v;    // value block scales, same layout
   int64_t T;
   int64_t res_stride;
   int32_t batch;
@@ -193,6 +195,9 @@ hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_
 // The same pass that also stores every token's raw scores (a.scores), for the
 // attention-mass features.
 hipError_t launch_split_tl_scores(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s);
+// The pass over int8-blockwise coefficients (coef_k / coef_v point at int8
+// codes, cscale_k / cscale_v at their fp16 block scales).
+hipError_t launch_split_tl_c8(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s);
 // Token-lane merge: reads a.part, writes a.out (one workgroup per slot, head
 // and 16 output channels).
 hipError_t launch_merge_tl(int rb, int g, const SplitArgs& a, hipStream_t s);

@@ -1,0 +1,92 @@
+"""Decode over the 8-bit blockwise coefficient form (dwkv_decode with int8
+codes and per-block fp16 scales) on the GPU against the float64 oracle, which
+rebuilds A = code * scale explicitly: every token-lane basis rank and group
+size, ragged lengths with partial tiles, empty sequences, several splits, the
+no-residual path, and the 64K-token shape on sampled heads.  The calls that
+write or rebuild fp16 coefficients refuse the format."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import announce, compare, device_cache, torch_gpu
+from synth import LLAMA8B_64K, Workload, generate
+
+pytestmark = pytest.mark.gpu
+
+
+class _Fixed:
+    def __init__(self, w, lengths):
+        self._w, self._lengths = w, list(lengths)
+
+    def __getattr__(self, k):
+        if k.startswith("_"):
+            raise AttributeError(k)
+        return getattr(self._w, k)
+
+    def seqlens(self):
+        return list(self._lengths)
+
+
+CASES = [
+    # name, r_b, G, levels, probs, lengths, split
+    ("i8-rb16-g1-tails", 16, 1, (0, 2), (0.6, 0.4), [1, 63, 65, 300], 64),
+    ("i8-rb32-g4", 32, 4, (0, 8, 16), (0.8, 0.15, 0.05), [4096], 0),
+    ("i8-rb48-g2-empty-seq", 48, 2, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), [0, 129, 700], 128),
+    ("i8-rb64-g4-entry-heavy", 64, 4, (0, 16), (0.1, 0.9), [1500, 64], 256),
+    ("i8-rb48-g4-no-residual", 48, 4, (0,), (1.0,), [2000, 37], 0),
+    ("i8-rb48-g4-many-chunks", 48, 4, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), [5000, 37], 64),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_int8_small_shapes(case):
+    torch = torch_gpu()
+    name, rb, G, levels, probs, lengths, split = case
+    w = _Fixed(Workload(name=name, batch=len(lengths), n_layers=2, window=2, n_kv_heads=2, n_q_heads=2 * G,
+                        head_dim=128, context=max(lengths), basis_rank=rb, levels=levels, probs=probs,
+                        q_dtype="bf16", seed=900 + len(name), coef_format="int8"), lengths)
+    host = generate(w, threads=4)
+    dc = device_cache(host, split_tokens=split)
+    pairs = [(b, h) for b in range(host.batch) for h in range(host.n_kv_heads)]
+    for layer in range(host.n_layers):
+        announce(f"int8 decode {name} layer={layer}")
+        out = dc.decode(layer).cpu().numpy()
+        torch.cuda.synchronize()
+        compare(out, oracle.decode(host, layer), pairs, G, f"{name} layer {layer}")
+        for b, L in enumerate(lengths):
+            if L == 0:
+                assert np.all(out[b] == 0)
+
+
+def test_int8_refused_where_unsupported():
+    torch = torch_gpu()
+    from paper_2607_06523_amd import DwkvError
+    w = Workload(name="i8-refuse", batch=1, n_layers=2, window=2, n_kv_heads=2, n_q_heads=16, head_dim=128,
+                 context=300, basis_rank=32, levels=(0, 8), probs=(0.5, 0.5), q_dtype="bf16", seed=3,
+                 coef_format="int8")
+    host = generate(w, threads=4)
+    dc = device_cache(host)                    # groups of 8: off the token-lane path
+    with pytest.raises(DwkvError) as e:
+        dc.decode(0)
+    assert e.value.status == 3
+    w4 = w.with_(n_q_heads=8)
+    dc4 = device_cache(generate(w4, threads=4))
+    for call in (lambda: dc4.materialize(0),
+                 lambda: dc4.compress(0, torch.zeros((1, 2, 128), dtype=torch.float16, device="cuda"),
+                                      torch.zeros((1, 2, 128), dtype=torch.float16, device="cuda"), 299, 300)):
+        with pytest.raises(DwkvError) as e:
+            call()
+        assert e.value.status == 3
+
+
+def test_int8_full_size_sampled():
+    torch = torch_gpu()
+    host = generate(LLAMA8B_64K.with_(coef_format="int8"), layers=(28, 32))
+    dc = device_cache(host)
+    G = host.n_q_heads // host.n_kv_heads
+    for layer in (0, 3):
+        announce(f"int8 decode 64k layer={layer}")
+        out = dc.decode(layer).cpu().numpy()
+        torch.cuda.synchronize()
+        pairs = [(0, 2), (0, 7)]
+        compare(out, oracle.decode(host, layer, heads=pairs), pairs, G, f"int8 64k layer {layer}")
