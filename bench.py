@@ -355,6 +355,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama8b-64k")
+    ap.add_argument("--context", type=int, default=0,
+                    help="override the workload's context length in tokens (same shape otherwise)")
     ap.add_argument("--split", type=int, default=0, help="tokens per workgroup chunk (0 = automatic)")
     ap.add_argument("--variant", default="full", choices=["full", "bases-only"],
                     help="bases-only: every routed residual rank 0 (shared bases only)")
@@ -383,6 +385,8 @@ def main():
     from synth import ALL, generate
 
     wl = ALL[args.workload]
+    if args.context > 0 and args.context != wl.context:
+        wl = wl.with_(context=args.context, name=f"{wl.name.rsplit('-', 1)[0]}-{args.context // 1024}k")
     if args.variant == "bases-only":
         wl = wl.with_(levels=(0,), probs=(1.0,), salient_frac=0.0, name=wl.name + "-bases-only")
     log(f"[bench] generating {wl.name} ({wl.description})")
