@@ -831,11 +831,15 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   __shared__ alignas(16) uint16_t bvs[kMergeMaxRB][D];
   __shared__ float abar[kMergeMaxRB];
   const int hq = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
-  asm volatile("" ::"s"(a.part), "s"(a.out), "s"(a.basis), "s"(a.basis_b_stride), "s"(a.n_q_heads),
-               "s"(a.n_kv_heads), "s"(a.tl), "s"(a.rb), "s"(a.wt.n_seq), "s"(a.wt.work[0]), "s"(a.wt.work[1]));
-  const int G = a.n_q_heads / a.n_kv_heads, h = hq / G, g = hq % G;
+  // the head counts pass through the statement so that nothing computed from
+  // them is scheduled ahead of the one batch of argument loads it requests
+  int nq = a.n_q_heads, nkv = a.n_kv_heads;
+  asm volatile("" : "+s"(nq), "+s"(nkv) : "s"(a.part), "s"(a.out), "s"(a.basis), "s"(a.basis_b_stride), "s"(a.tl),
+               "s"(a.rb), "s"(a.split), "s"(a.n_work), "s"(a.n_probe), "s"(a.wt.n_seq), "s"(a.wt.work[min(b, kKernargSeqs - 1)]),
+               "s"(a.wt.work[min(b, kKernargSeqs - 1) + 1]));
+  const int G = nq / nkv, h = hq / G, g = hq % G;
   int base, ns;
-  seq_work(a.wt, a.cu, a.split, b, base, ns);
+  seq_work_entry(a.wt, a.cu, a.split, b, base, ns);
   const int c4 = tid % (D / 4), sg = tid / (D / 4);
   const int64_t row0 = (int64_t)base * a.n_kv_heads * G + h * G + g;
   const int64_t row_step = (int64_t)a.n_kv_heads * G;

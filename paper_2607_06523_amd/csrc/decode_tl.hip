@@ -683,8 +683,11 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const SplitArgs a
   const int ch = blockIdx.x % NCH, g = (blockIdx.x / NCH) % G, slot = blockIdx.x / (NCH * G), b = blockIdx.y;
   const int c0 = ch * kWmCh;
   const int kvh = a.kv_of_slot[slot];
+  // every kernel argument the merge needs, loaded in one batch at entry
+  asm volatile("" ::"s"(a.part), "s"(a.basis), "s"(a.basis_b_stride), "s"(a.out), "s"(a.n_q_heads), "s"(a.n_work),
+               "s"(a.split), "s"(kvh));
   int base, ns;
-  seq_work(a.wt, a.cu, a.split, b, base, ns);
+  seq_work_entry(a.wt, a.cu, a.split, b, base, ns);
   // B^V rows [kg KPG, kg KPG + KPG) of channel c0 + tid % 16
   const int pc = tid % kWmCh, kg = tid / kWmCh;
   const uint16_t* bv = a.basis + (int64_t)b * a.basis_b_stride + ((int64_t)kvh * 2 + 1) * RB * D + c0 + pc;

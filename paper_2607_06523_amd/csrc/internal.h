@@ -95,7 +95,8 @@ struct MergeArgs {
 __device__ __forceinline__ void pin_split_args(const SplitArgs& a, int kvh) {
   asm volatile("" ::"s"(a.coef_k), "s"(a.coef_v), "s"(a.basis), "s"(a.basis_b_stride), "s"(a.q), "s"(a.off), "s"(a.idx_k),
                "s"(a.idx_v), "s"(a.val_k), "s"(a.val_v), "s"(a.scale_k), "s"(a.scale_v), "s"(a.T),
-               "s"(a.res_stride), "s"(a.split), "s"(kvh), "s"(a.wt.n_seq), "s"(a.wt.tok[0]), "s"(a.wt.tok[1]));
+               "s"(a.res_stride), "s"(a.split), "s"(kvh), "s"(a.wt.n_seq), "s"(a.wt.tok[0]), "s"(a.wt.tok[1]),
+               "s"(a.n_q_heads), "s"(a.q_bf16), "s"(a.qscale), "s"(a.part), "s"(a.n_work));
 }
 
 // Sequence b and token chunk [c0, c1) of work item w.
@@ -142,6 +143,23 @@ __device__ __forceinline__ void seq_work(const WorkTable& wt, const int32_t* cu,
     base = 0;
     for (int i = 0; i < b; ++i) base += (cu[i + 1] - cu[i] + split - 1) / split;
     ns = (cu[b + 1] - cu[b] + split - 1) / split;
+  }
+}
+
+// seq_work at a kernel's entry (b uniform): the table entries are read
+// unconditionally, at an index kept inside the table, and held in scalar
+// registers, so their loads join the kernel's first batch of argument loads
+// instead of waiting behind the n_seq test.
+__device__ __forceinline__ void seq_work_entry(const WorkTable& wt, const int32_t* cu, int split, int b,
+                                               int& base, int& ns) {
+  const int bi = min(b, kKernargSeqs - 1);
+  const int wa = wt.work[bi], wb = wt.work[bi + 1];
+  asm volatile("" ::"s"(wt.n_seq), "s"(wa), "s"(wb));
+  if (wt.n_seq > 0) {
+    base = wa;
+    ns = wb - wa;
+  } else {
+    seq_work(wt, cu, split, b, base, ns);
   }
 }
 
