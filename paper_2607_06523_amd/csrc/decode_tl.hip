@@ -367,7 +367,7 @@ __device__ __forceinline__ void pv_tile_h(f4& acc_h, f4& acc_l, h4 ph, h4 pl, co
     acc_l = __builtin_amdgcn_mfma_f32_4x4x4f16(pl, v[Q], acc_l, 4, Q, 0)), ...);
 }
 
-template <int RB, int G, bool RESID, bool SCORES, bool C8>
+template <int RB, int G, bool RESID, bool SCORES, bool C8, bool LAST>
 __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TMeta& mc, TMeta& mn, TMeta& mnn,
                                       TEnt& ec, TEnt& en, int j, int jn, int jnn, const TCtx& x,
                                       TSmem<RB, RESID>& sm, int wv, int lane) {
@@ -375,14 +375,15 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
   constexpr int NS = C::NS;
   const int grp = lane >> 4;
   const int32_t t0 = tstart(x, j);
-  // past the wave's last tile the prefetches re-read a tile of this chunk
-  // (cache resident, results unused): the load sequence stays the same
+  // two tiles ahead of the wave's second-to-last tile the offset prefetch
+  // re-reads a tile of this chunk (cache resident, results unused)
   const int jn_l = jn < x.ntile ? jn : j;
   const int jnn_l = jnn < x.ntile ? jnn : jn_l;
 
   // 1. metadata of the next tiles, issued here, ahead of this tile's work (the
-  // registers rotate at the end of the step and the copies wait for them)
-  if constexpr (RESID) {
+  // registers rotate at the end of the step and the copies wait for them).
+  // The wave's last step requests nothing.
+  if constexpr (RESID && !LAST) {
     load_offsets(mnn, x, jnn_l, lane);
     load_entries(en, x, mn, lane);
     load_scales(mn, x, jn_l, lane);
@@ -435,7 +436,7 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
         for (int i = 0; i < 4; ++i) sacc[bk][i] += o[i] * ksc;
       }
     }
-    load_k8<RB>(fr, x, jn_l, lane);
+    if constexpr (!LAST) load_k8<RB>(fr, x, jn_l, lane);
   } else {
 #pragma unroll
     for (int s = 0; s + 1 < NS; s += 2)
@@ -453,7 +454,7 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
         sacc[bk] = mfma16(st.qlo[NS - 1], kf, sacc[bk]);
       }
     }
-    load_k<RB>(fr, x, jn_l, lane);
+    if constexpr (!LAST) load_k<RB>(fr, x, jn_l, lane);
   }
   float sc[HG];
 #pragma unroll
@@ -575,7 +576,7 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
       }
       pv_tile_h(st.acc_h[b], st.acc_l[b], ph, pl, vb, std::make_integer_sequence<int, 16>{});
     }
-    load_v8<RB>(fr, x, jn_l, lane);
+    if constexpr (!LAST) load_v8<RB>(fr, x, jn_l, lane);
   } else {
     float pt[4] = {p[0], p[1], p[2], p[3]};
     quad_transpose(pt, lane);
@@ -587,7 +588,7 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
       pl[i] = (_Float16)(pt[i] - (float)hh);
     }
     pv_tile(st.acc_h[0], st.acc_l[0], ph, pl, fr.v, std::make_integer_sequence<int, 16>{});
-    load_v<RB>(fr, x, jn_l, lane);
+    if constexpr (!LAST) load_v<RB>(fr, x, jn_l, lane);
   }
 
   // 6. value residual, one lane per entry: p * code * scale into the channel
@@ -987,9 +988,13 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
 
 
   // tiles wv, wv + 8, wv + 16, ...: a fixed assignment keeps the summation
-  // order, and so the result, independent of timing
-  for (int j = wv; j < x.ntile; j += kTW)
-    tstep<RB, G, RESID, SCORES, C8>(st, fr, mc, mn, mnn, ec, en, j, j + kTW, j + 2 * kTW, x, sm, wv, lane);
+  // order, and so the result, independent of timing.  The last tile of the
+  // wave runs without the next tiles' loads.
+  int j = wv;
+  for (; j + kTW < x.ntile; j += kTW)
+    tstep<RB, G, RESID, SCORES, C8, false>(st, fr, mc, mn, mnn, ec, en, j, j + kTW, j + 2 * kTW, x, sm, wv, lane);
+  if (j < x.ntile)
+    tstep<RB, G, RESID, SCORES, C8, true>(st, fr, mc, mn, mnn, ec, en, j, j + kTW, j + 2 * kTW, x, sm, wv, lane);
 
   // epilogue: the waves combine; the partial keeps a~ in basis space (the
   // merge projects it through B^V once per sequence and head).  Each wave
