@@ -308,10 +308,25 @@ __device__ __forceinline__ Window align_window(const uint32_t* c5, const uint32_
   return w;
 }
 
+// Whole-wave reductions without LDS: DPP inside each row of 16 (lane xor 1,
+// xor 2, then the half-row and row mirrors), which leaves every lane of a
+// row with the row's result, then the four rows' results read into scalar
+// registers and combined in a fixed order.  Every lane returns the same bits.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  v = fmaxf(v, dpp_f<0xB1>(v));        // quad_perm(1,0,3,2)
+  v = fmaxf(v, dpp_f<0x4E>(v));        // quad_perm(2,3,0,1)
+  v = fmaxf(v, dpp_f<0x141>(v));       // row_half_mirror
+  v = fmaxf(v, dpp_f<0x140>(v));       // row_mirror
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
 }
 
 // Inclusive running maximum over the lanes of a wave (non-negative values):
@@ -326,10 +341,25 @@ __device__ __forceinline__ int wave_incl_max(int v) {
   return v;
 }
 
+__device__ __forceinline__ int wave_imax(int v) {
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false));
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false));
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false));
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false));
+  return max(max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
+             max(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x141>(v);
+  v += dpp_f<0x140>(v);
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return (r0 + r1) + (r2 + r3);
 }
 
 // 4x4 transpose inside each lane quad: lane 4q+r holds row r (x[0..3]) on
@@ -601,9 +631,7 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
       const uint32_t eb = (mc.sv >> 10) & 31u;
       const int el = (int)max(eb, 1u) - 14;
       if (__ballot(el > st.ex) != 0) {
-        int emax = el;
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) emax = max(emax, __shfl_xor(emax, o));
+        const int emax = wave_imax(el);
         const double f = ldexp(1.0, st.ex - emax);
 #pragma unroll
         for (int i = 0; i < G; ++i) {
