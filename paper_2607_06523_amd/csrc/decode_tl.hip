@@ -285,6 +285,15 @@ __device__ __forceinline__ unsigned long long to_fixed(float v, double scale) {
   return (unsigned long long)(__double_as_longlong(t) - __double_as_longlong(magic));
 }
 
+// A fixed-point accumulator as float.  Below 2^53 in magnitude the two
+// halves combine exactly in double and the result is rounded once (terms stay
+// below 2^45, so this holds while a wave adds at most 256 tokens to a
+// channel); above it a second rounding can move the result by one float ulp.
+__device__ __forceinline__ float fixed_to_float(long long v) {
+  const double hi = (double)(int32_t)(v >> 32), lo = (double)(uint32_t)(v & 0xFFFFFFFFll);
+  return (float)__builtin_fma(hi, 4294967296.0, lo);
+}
+
 // Order LDS traffic between lanes of one wave.
 __device__ __forceinline__ void wave_lds_fence() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -1040,8 +1049,8 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
     float* rf = reinterpret_cast<float*>(&sm.racc[wv][0][0]);
 #pragma unroll
     for (int i = 0; i < G; ++i) {
-      rf[i * D + lane] = (float)rv[i][0] * fs;
-      rf[i * D + lane + 64] = (float)rv[i][1] * fs;
+      rf[i * D + lane] = fixed_to_float(rv[i][0]) * fs;
+      rf[i * D + lane + 64] = fixed_to_float(rv[i][1]) * fs;
     }
   }
 #pragma unroll
