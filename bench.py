@@ -332,6 +332,28 @@ def measure_comparators(dc, host, torch, steps: int = 3):
                     "then dwkv_dense_decode per layer (rebuilt cache written to and re-read from HBM)"}
 
 
+def measure_hbm_ceiling(torch, gib: int = 4, reps: int = 10):
+    """Practical HBM read ceiling: dwkv_hbm_read over a buffer far beyond the
+    last-level caches, timed with HIP events on the current stream."""
+    from paper_2607_06523_amd import hbm_read, hbm_read_blocks
+    buf = torch.ones(gib << 28, dtype=torch.int32, device="cuda")
+    sink = torch.empty(hbm_read_blocks(), dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        hbm_read(buf, sink)
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record(stream)
+    for _ in range(reps):
+        hbm_read(buf, sink)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / reps
+    nbytes = buf.numel() * 4
+    del buf, sink
+    return {"gbps": round(nbytes / (ms / 1e3) / 1e9, 1), "bytes": nbytes, "ms": round(ms, 4), "reps": reps,
+            "kernel": "stream_read_kernel (dwkv_hbm_read): 1 KB nontemporal loads per wave instruction"}
+
+
 def measured_traffic(workload: str):
     """HBM bytes per launch of the token-lane decode kernel from the committed
     rocprofv3 counter profile, or None when that profile is missing or was
@@ -370,6 +392,8 @@ def main():
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before timing, run one plain device copy of this many MiB (a known-size "
                          "reference for HBM byte counters)")
+    ap.add_argument("--hbm-ceiling-only", action="store_true",
+                    help="only time the HBM read stream (dwkv_hbm_read) and print its JSON")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -382,6 +406,9 @@ def main():
     if not os.path.exists(binding.LIB_PATH):
         from paper_2607_06523_amd.build import build
         build()
+    if args.hbm_ceiling_only:
+        print(json.dumps({"hbm_read_ceiling": measure_hbm_ceiling(torch)}), flush=True)
+        return
     from synth import ALL, generate
 
     wl = ALL[args.workload]
@@ -473,6 +500,7 @@ def main():
         avg_split_ms = ms_per_step / L
         achieved = step_gbps
     traffic = measured_traffic(wl.name) if args.variant == "full" and args.split == 0 else None
+    ceiling = measure_hbm_ceiling(torch)
     result = {
         "metric": "compressed-KV decode attn tokens/s at 64K ctx (plus achieved HBM GB/s)",
         "value": round(tok_s, 2),
@@ -493,7 +521,9 @@ def main():
                    "graph": bool(graph is not None)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "kernel": "split-K partials pass (tl_kernel at this workload)"},
+                     "kernel": "split-K partials pass (tl_kernel at this workload)",
+                     "measured_ceiling": ceiling["gbps"], "frac_of_measured_ceiling": round(achieved / ceiling["gbps"], 4)},
+        "hbm_read_ceiling": ceiling,
         "step_gbps": round(step_gbps, 1),
         "bytes_per_step": int(bytes_step),
         "bytes_per_layer_call": int(np.mean(bytes_layer)),

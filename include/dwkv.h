@@ -372,6 +372,26 @@ dwkv_status dwkv_dense_decode(const dwkv_dims* dims, const void* k, const void* 
                               int32_t q_type, float sm_scale, float* out, void* workspace,
                               size_t ws_bytes, void* stream);
 
+/* Number of sink words dwkv_hbm_read writes (its block count). */
+int32_t dwkv_hbm_read_blocks(void);
+
+/* HBM read stream, for measurement; it implements no operation of the paper.
+ * It reads `bytes` bytes of device memory once, each wave load covering 1 KB
+ * of consecutive bytes with the nontemporal hint.  Timed on a buffer well
+ * beyond the last-level caches, it gives the practical read-bandwidth
+ * ceiling that the decode's achieved bandwidth is set against, next to the
+ * published 8 TB/s (the paper's speed figures are tokens/s, Sec. 4).
+ *   buf: device, 16-byte aligned; bytes: a multiple of 16 (0 allowed)
+ *   sink: device uint32 [sink_words], 4-byte aligned, sink_words >=
+ *     dwkv_hbm_read_blocks(); block b writes sink[b] = the xor of the 32-bit
+ *     words it read, so the xor of sink[0 .. blocks) is the xor of every
+ *     32-bit word of buf (0 for an empty buffer).  Words past the block
+ *     count are not touched.
+ * Errors: DWKV_E_NULL (sink, or buf with bytes > 0), DWKV_E_DIMS (bytes not
+ * a multiple of 16), DWKV_E_WORKSPACE (sink too small), DWKV_E_ALIGN.  One
+ * launch. */
+dwkv_status dwkv_hbm_read(const void* buf, size_t bytes, uint32_t* sink, int32_t sink_words, void* stream);
+
 /* Bytes of device workspace dwkv_validate needs. */
 size_t dwkv_validate_workspace_bytes(void);
 

@@ -21,7 +21,7 @@ import numpy as np
 from . import binding
 from .binding import DwkvError, F16, BF16
 
-__all__ = ["DeviceCache", "ProbeRef", "DwkvError", "load", "F16", "BF16"]
+__all__ = ["DeviceCache", "ProbeRef", "DwkvError", "load", "F16", "BF16", "hbm_read", "hbm_read_blocks"]
 
 
 def load():
@@ -34,6 +34,24 @@ def _ptr(t):
 
 def _stream(torch, device):
     return C.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def hbm_read_blocks() -> int:
+    """Words of the sink that ``hbm_read`` writes."""
+    return int(binding.load().dwkv_hbm_read_blocks())
+
+
+def hbm_read(buf, sink):
+    """Enqueue one read of the device tensor ``buf`` (its bytes, a multiple of
+    16) on the current stream; ``sink`` is a device int32 tensor of at least
+    ``hbm_read_blocks()`` elements whose xor becomes the xor of buf's 32-bit
+    words.  The HBM read-stream ceiling of the device is its bytes over its
+    time."""
+    import torch
+    lib = binding.load()
+    nbytes = buf.numel() * buf.element_size()
+    binding.check(lib.dwkv_hbm_read(_ptr(buf), nbytes, _ptr(sink), sink.numel(), _stream(torch, buf.device)),
+                  "dwkv_hbm_read")
 
 
 @dataclass

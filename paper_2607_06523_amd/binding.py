@@ -62,7 +62,7 @@ EXPORTS = ["dwkv_abi_version", "dwkv_status_str", "dwkv_split_tokens", "dwkv_wor
            "dwkv_route_range", "dwkv_route_budget_workspace_bytes", "dwkv_route_budget", "dwkv_compress", "dwkv_features_workspace_bytes", "dwkv_decode_features",
            "dwkv_controller_update", "dwkv_sketch_workspace_bytes", "dwkv_sketch_basis", "dwkv_materialize", "dwkv_dense_workspace_bytes",
            "dwkv_dense_decode", "dwkv_residual_map",
-           "dwkv_validate_workspace_bytes", "dwkv_validate"]
+           "dwkv_validate_workspace_bytes", "dwkv_validate", "dwkv_hbm_read_blocks", "dwkv_hbm_read"]
 
 _lib = None
 
@@ -133,6 +133,10 @@ def load(path: str = LIB_PATH):
     lib.dwkv_residual_map.restype = C.c_int
     lib.dwkv_residual_map.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_int32, C.c_int32, C.c_int64,
                                       C.c_int64, C.c_void_p, C.c_void_p]
+    lib.dwkv_hbm_read_blocks.restype = C.c_int32
+    lib.dwkv_hbm_read_blocks.argtypes = []
+    lib.dwkv_hbm_read.restype = C.c_int
+    lib.dwkv_hbm_read.argtypes = [C.c_void_p, C.c_size_t, C.c_void_p, C.c_int32, C.c_void_p]
     lib.dwkv_validate_workspace_bytes.restype = C.c_size_t
     lib.dwkv_validate.restype = C.c_int
     lib.dwkv_validate.argtypes = [P(Dims), P(Cache), P(C.c_int64), C.c_void_p, C.c_size_t, C.c_void_p]

@@ -20,7 +20,7 @@ LIB_DIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(LIB_DIR, "libdwkv.so")
 ARCH = "gfx950"
 
-SOURCES = ["decode.hip", "decode_tl.hip", "aux.hip", "compress.hip", "dense.hip", "features.hip", "sketch.hip", "api.hip"]
+SOURCES = ["decode.hip", "decode_tl.hip", "aux.hip", "compress.hip", "dense.hip", "features.hip", "sketch.hip", "stream.hip", "api.hip"]
 # -packed-fp32-ops: never emit packed fp32 VALU ops (v_pk_{add,mul,fma}_f32)
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wno-unused-result"]

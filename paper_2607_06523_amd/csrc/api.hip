@@ -609,6 +609,16 @@ dwkv_status dwkv_materialize(const dwkv_dims* d, const dwkv_cache* c, int32_t la
   return hip_status(launch_materialize(a, reinterpret_cast<hipStream_t>(stream)));
 }
 
+int32_t dwkv_hbm_read_blocks(void) { return kStreamBlocks; }
+
+dwkv_status dwkv_hbm_read(const void* buf, size_t bytes, uint32_t* sink, int32_t sink_words, void* stream) {
+  if (!sink || (bytes > 0 && !buf)) return DWKV_E_NULL;
+  if (bytes % 16 != 0) return DWKV_E_DIMS;
+  if (sink_words < kStreamBlocks) return DWKV_E_WORKSPACE;
+  if (!aligned16(buf) || (reinterpret_cast<uintptr_t>(sink) & 3u)) return DWKV_E_ALIGN;
+  return hip_status(launch_stream_read(buf, (uint64_t)(bytes / 16), sink, reinterpret_cast<hipStream_t>(stream)));
+}
+
 size_t dwkv_dense_workspace_bytes(const dwkv_dims* d) {
   if (check_dims(d) != DWKV_OK) return 0;
   const int split = plan_split_general(d);

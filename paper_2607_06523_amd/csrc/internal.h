@@ -244,6 +244,10 @@ struct MatArgs {
 };
 hipError_t launch_materialize(const MatArgs& a, hipStream_t s);
 
+// HBM read stream: kStreamBlocks blocks; block b writes sink[b].
+constexpr int kStreamBlocks = 2048;
+hipError_t launch_stream_read(const void* buf, uint64_t n16, uint32_t* sink, hipStream_t s);
+
 // Attention-mass features of one decode (token-lane partials and stored scores).
 struct FeatArgs {
   const float* part;           // token-lane partials [Hkv][n_work][G][kPartStrideTL]

@@ -329,3 +329,14 @@ def test_sketch_argument_checks(lib):
     assert sk(n=0) == 2
     assert sk(x=0) == 1
     assert sk(x=FAKE + 2) == 7
+
+
+def test_hbm_read_rejects_bad_arguments(lib):
+    blocks = lib.dwkv_hbm_read_blocks()
+    assert blocks >= 256
+    assert lib.dwkv_hbm_read(FAKE, 1024, None, blocks, None) == 1              # no sink
+    assert lib.dwkv_hbm_read(None, 1024, FAKE, blocks, None) == 1              # no buffer
+    assert lib.dwkv_hbm_read(FAKE, 1000, FAKE, blocks, None) == 2              # not a multiple of 16
+    assert lib.dwkv_hbm_read(FAKE, 1024, FAKE, blocks - 1, None) == 4          # sink too small
+    assert lib.dwkv_hbm_read(FAKE + 8, 1024, FAKE, blocks, None) == 7          # buffer alignment
+    assert lib.dwkv_hbm_read(FAKE, 1024, FAKE + 2, blocks, None) == 7          # sink alignment
