@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define DWKV_ABI_VERSION 2
+#define DWKV_ABI_VERSION 3
 #define DWKV_MAX_LEVELS 8
 #define DWKV_MAX_PROBE_HEADS 64
 
@@ -89,11 +89,15 @@ typedef enum dwkv_coef_format { DWKV_COEF_F16 = 0, DWKV_COEF_I8 = 1 } dwkv_coef_
 /* Compressed cache (Eq. 1 factors).  M = L / window, Z = 0 keys, Z = 1 values. */
 typedef struct dwkv_cache {
   const void*     basis;     /* fp16 [B][M][Hkv][2][r_b][d]: rows of B^Z_{m,h} per sequence */
-  const void*     coef_k;    /* fp16 [L][Hkv][T][r_b]: key coefficient rows A^K_{l,h,t}     */
-  const void*     coef_v;    /* fp16 [L][Hkv][T16/16][r_b][16]: value coefficients A^V_{l,h,t}
-                                in 16-token blocks, token index fastest: token t, coefficient
-                                i at [t/16][i][t%16]; T16 = T rounded up to 16; the padding
-                                tokens of the last block must be finite (zero)               */
+  const void*     coef_k;    /* fp16 [L][Hkv][T16/16][r_b/8][16][8]: key coefficients
+                                A^K_{l,h,t} in tiles of 16 tokens x 8 coefficients,
+                                coefficient index fastest: token t, coefficient i at
+                                [t/16][i/8][t%16][i%8]; T16 = T rounded up to 16       */
+  const void*     coef_v;    /* fp16 [L][Hkv][T16/8][r_b][8]: value coefficients A^V_{l,h,t}
+                                in 8-token blocks, token index fastest: token t,
+                                coefficient i at [t/8][i][t%8].  In both, the padding
+                                tokens past T must be finite (zero).  These layouts let
+                                each wave load of the decode read whole 128-byte lines. */
   const uint8_t*  rank_code; /* [M][Hkv][T] level index k of each token (rho = levels[k])  */
   const uint32_t* res_off;   /* [M][Hkv][T+1] exclusive running sum of rho over the packed
                                 tokens: token t's entries are [res_off[t], res_off[t+1])   */
@@ -103,10 +107,10 @@ typedef struct dwkv_cache {
   const void*     res_scale; /* fp16 [L][2][Hkv][T] gate-folded residual scale g*s         */
   const void*     coef_k_scale; /* DWKV_COEF_I8 only (else ignored): fp16 [L][Hkv][r_b/16][T]
                                 block scales of the key coefficients; coef_k then holds int8
-                                codes [L][Hkv][T][r_b]                                      */
+                                codes in rows [L][Hkv][T][r_b]                              */
   const void*     coef_v_scale; /* DWKV_COEF_I8 only: fp16 [L][Hkv][r_b/16][T] value block
-                                scales; coef_v then holds int8 codes [L][Hkv][T16/16][r_b][16]
-                                (the blocked layout, one byte per entry)                      */
+                                scales; coef_v then holds int8 codes in 16-token blocks
+                                [L][Hkv][T16/16][r_b][16], token fastest                    */
 } dwkv_cache;
 
 /* Attention-output probe (Eq. 3) against a dense higher-fidelity cache. */
@@ -114,8 +118,9 @@ typedef struct dwkv_probe {
   int32_t n_heads;             /* probed KV heads, 1..min(Hkv, 64)                     */
   const int32_t* kv_heads_host;/* [n_heads] distinct KV head ids                       */
   const void* k_ref;           /* fp16 [n_heads][T][d] reference keys (packed tokens)  */
-  const void* v_ref;           /* fp16 [n_heads][T16/16][d][16] reference values, in the
-                                  16-token blocked layout of coef_v (finite padding)   */
+  const void* v_ref;           /* fp16 [n_heads][T16/16][d][16] reference values in
+                                  16-token blocks, token index fastest: token t, channel
+                                  c at [t/16][c][t%16] (finite padding)                */
   float eps;                   /* Eq. 3 epsilon (e.g. 1e-6)                            */
   float* err;                  /* out fp32 [B][n_heads*G]: probed head i, group member g
                                   at column i*G+g                                      */

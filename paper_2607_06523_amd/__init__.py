@@ -18,7 +18,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from . import binding
+from . import binding, layout
 from .binding import DwkvError, F16, BF16
 
 __all__ = ["DeviceCache", "ProbeRef", "DwkvError", "load", "F16", "BF16", "hbm_read", "hbm_read_blocks"]
@@ -84,9 +84,9 @@ class DeviceCache:
             self.coef_v = up(host.coef_v.view(np.uint8), torch.uint8)
             self.coef_scale_k = up(host.coef_scale_k.view(np.uint16), torch.float16)
             self.coef_scale_v = up(host.coef_scale_v.view(np.uint16), torch.float16)
-        else:
-            self.coef_k = up(host.coef_k.view(np.uint16), torch.float16)
-            self.coef_v = up(host.coef_v.view(np.uint16), torch.float16)
+        else:                                 # fp16: the ABI's tiled layouts
+            self.coef_k = up(layout.keys_to_abi(host.coef_k.view(np.uint16)), torch.float16)
+            self.coef_v = up(layout.values_to_abi(host.coef_v.view(np.uint16)), torch.float16)
             self.coef_scale_k = self.coef_scale_v = None
         self.rank_code = up(host.rank_code, torch.uint8)
         self.res_off = up(host.res_off.view(np.int32), torch.int32)
@@ -351,6 +351,20 @@ class DeviceCache:
                                         _stream(torch, self.device))
         binding.check(st, "dwkv_residual_map")
         return dense
+
+    def coef_host(self):
+        """The device coefficients in the host layout (fp16 as uint16): keys
+        [L][Hkv][T][r_b], values [L][Hkv][T16/16][r_b][16]; int8 codes as stored."""
+        k = self.coef_k.cpu().numpy()
+        v = self.coef_v.cpu().numpy()
+        if self.coef_format == "int8":
+            return k, v
+        k, v = k.view(np.uint16), v.view(np.uint16)
+        L, Hk, T, rb = self.n_layers, self.n_kv_heads, self.total_tokens, self.basis_rank
+        T16 = -(-T // 16) * 16
+        keys = layout.keys_from_abi(k.reshape(L, Hk, T16 // 16, rb // 8, 16, 8), T)
+        vals = layout.values_from_abi(v.reshape(L, Hk, T16 // 8, rb, 8))
+        return keys, vals
 
     def validate(self):
         """Returns (ok, bad_index); raises on argument errors."""

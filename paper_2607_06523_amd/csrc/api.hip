@@ -244,7 +244,7 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
     a.cscale_k = static_cast<const uint16_t*>(c->coef_k_scale) + (int64_t)layer * Hk * (RB / 16) * T;
     a.cscale_v = static_cast<const uint16_t*>(c->coef_v_scale) + (int64_t)layer * Hk * (RB / 16) * T;
   } else {
-    a.coef_k = static_cast<const uint16_t*>(c->coef_k) + (int64_t)layer * Hk * T * RB;
+    a.coef_k = static_cast<const uint16_t*>(c->coef_k) + (int64_t)layer * Hk * T16 * RB;
     a.coef_v = static_cast<const uint16_t*>(c->coef_v) + (int64_t)layer * Hk * T16 * RB;
   }
   a.basis = static_cast<const uint16_t*>(c->basis) + (int64_t)m * Hk * 2 * RB * kHeadDim;
@@ -500,7 +500,7 @@ dwkv_status dwkv_compress(const dwkv_dims* d, const dwkv_cache* c, int32_t layer
   a.xv = static_cast<const uint16_t*>(x_v);
   a.gate = gate;
   // the cache's arrays are written in place (the pointers are const only for decode)
-  a.coef_k = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->coef_k)) + (int64_t)layer * Hk * T * rb;
+  a.coef_k = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->coef_k)) + (int64_t)layer * Hk * T16 * rb;
   a.coef_v = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->coef_v)) + (int64_t)layer * Hk * T16 * rb;
   a.res_idx = const_cast<uint8_t*>(c->res_idx) + (int64_t)layer * 2 * Hk * d->res_stride;
   a.res_val = const_cast<uint8_t*>(c->res_val) + (int64_t)layer * 2 * Hk * (d->res_stride / 2);
@@ -593,7 +593,7 @@ dwkv_status dwkv_materialize(const dwkv_dims* d, const dwkv_cache* c, int32_t la
   a.basis_b_stride = (int64_t)M * Hk * 2 * rb * kHeadDim;
   a.T = T;
   a.T16 = (T + 15) / 16 * 16;
-  a.coef_k = static_cast<const uint16_t*>(c->coef_k) + (int64_t)layer * Hk * T * rb;
+  a.coef_k = static_cast<const uint16_t*>(c->coef_k) + (int64_t)layer * Hk * a.T16 * rb;
   a.coef_v = static_cast<const uint16_t*>(c->coef_v) + (int64_t)layer * Hk * a.T16 * rb;
   a.off = c->res_off + (int64_t)m * Hk * (T + 1);
   a.idx = c->res_idx + (int64_t)layer * 2 * Hk * d->res_stride;

@@ -145,9 +145,9 @@ __device__ __forceinline__ void compress_token(const CompressArgs& a, const Slab
     const uint16_t ab = float_to_half_bits(acc);
     sm.as[wv][i] = half_bits_to_float(ab);
     if (z == 0)
-      sl.coef[t * rb + i] = ab;
+      sl.coef[key_index(t, i, rb)] = ab;
     else
-      sl.coef[((t >> 4) * rb + i) * 16 + (t & 15)] = ab;
+      sl.coef[value_index(t, i, rb)] = ab;
   }
   wave_lds_sync();
 
@@ -250,7 +250,7 @@ __global__ __launch_bounds__(kCW * 64) void compress_kernel(const CompressArgs a
   Slab sl;
   sl.code = a.code + (int64_t)h * a.T;
   sl.off = a.off + (int64_t)h * (a.T + 1);
-  sl.coef = z == 0 ? a.coef_k + (int64_t)h * a.T * a.rb : a.coef_v + (int64_t)h * a.T16 * a.rb;
+  sl.coef = (z == 0 ? a.coef_k : a.coef_v) + (int64_t)h * a.T16 * a.rb;
   sl.res_idx = a.res_idx + slab * a.res_stride;
   sl.res_val = a.res_val + slab * (a.res_stride / 2);
   sl.res_scale = a.res_scale + slab * a.T;

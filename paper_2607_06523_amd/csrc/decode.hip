@@ -138,8 +138,8 @@ struct State {
 };
 
 struct Ctx {
-  const uint16_t* ck;                   // key rows of this slab [T][RB]
-  const uint16_t* cv;                   // value blocks of this slab [NB][RB][16]
+  const uint16_t* ck;                   // key tiles of this slab (key_index); dense: rows [T][RB]
+  const uint16_t* cv;                   // value blocks of this slab (value_index); dense: [NB][RB][16]
   const uint32_t* off;                  // [T+1]
   const uint8_t* idx[2];
   const uint8_t* val[2];
@@ -156,7 +156,9 @@ __device__ __forceinline__ int64_t tile_start(const Ctx& x, int j) {
   return x.tb + (int64_t)j * Cfg<RB>::TT;
 }
 
-template <int RB>
+// Key rows (tile row = token, 4 consecutive coefficients per k-step): from the
+// coefficient tiles (key_index) or, for a dense cache (TILED false), rows [T][RB].
+template <int RB, bool TILED>
 __device__ __forceinline__ void load_k(Frags<RB>& f, const Ctx& x, int j, int lane) {
   using C = Cfg<RB>;
   const int64_t t0 = tile_start<RB>(x, j);
@@ -164,13 +166,18 @@ __device__ __forceinline__ void load_k(Frags<RB>& f, const Ctx& x, int j, int la
 #pragma unroll
   for (int bk = 0; bk < C::NBK; ++bk) {
     const int64_t row = min(t0 + 16 * bk + col, x.T - 1);
-    const uint2* p = reinterpret_cast<const uint2*>(x.ck + row * RB + C::KH * grp);
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s) f.k[bk][s] = p[s];
+    for (int s = 0; s < C::NS; ++s) {
+      const int k0 = C::KH * grp + 4 * s;
+      const int64_t e = TILED ? key_index(row, k0, RB) : row * RB + k0;
+      f.k[bk][s] = *reinterpret_cast<const uint2*>(x.ck + e);
+    }
   }
 }
 
-template <int RB>
+// Value rows (4 consecutive tokens of one channel): from the coefficient
+// blocks (value_index) or, for a dense cache, 16-token blocks [T16/16][RB][16].
+template <int RB, bool TILED>
 __device__ __forceinline__ void load_v(Frags<RB>& f, const Ctx& x, int j, int lane) {
   using C = Cfg<RB>;
   const int64_t b0 = tile_start<RB>(x, j) >> 4;
@@ -178,9 +185,12 @@ __device__ __forceinline__ void load_v(Frags<RB>& f, const Ctx& x, int j, int la
 #pragma unroll
   for (int bk = 0; bk < C::NBK; ++bk) {
     const int64_t blk = min(b0 + bk, x.nblk - 1);
-    const uint16_t* base = x.cv + blk * RB * 16 + col * 16 + 4 * grp;
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s) f.v[bk][s] = *reinterpret_cast<const uint2*>(base + s * 256);
+    for (int s = 0; s < C::NS; ++s) {
+      const int c = col + 16 * s;
+      const int64_t e = TILED ? value_index(16 * blk + 4 * grp, c, RB) : (blk * RB + c) * 16 + 4 * grp;
+      f.v[bk][s] = *reinterpret_cast<const uint2*>(x.cv + e);
+    }
   }
 }
 
@@ -329,7 +339,7 @@ __device__ __forceinline__ void value_resid_tokens_global(WaveSmem<RB, G, true>&
   }
 }
 
-template <int RB, int G, bool RESID>
+template <int RB, int G, bool RESID, bool TILED>
 __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Meta& mn, Meta& mnn,
                                      Ent& ec, Ent& en, int j, const Ctx& x, Smem<RB, G, RESID>& sm,
                                      WaveSmem<RB, G, RESID>& ws, int lane) {
@@ -376,7 +386,7 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
       sacc[bk] = mfma16(av, st.qlo[s], sacc[bk]);
     }
   }
-  load_k<RB>(fr, x, jn_l, lane);
+  load_k<RB, TILED>(fr, x, jn_l, lane);
 
   // 3. key residual entries add q[c]*code*scale to their token's score
   if constexpr (RESID) {
@@ -464,7 +474,7 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
       st.acc[cb] = mfma16(pl, vf, st.acc[cb]);
     }
   }
-  load_v<RB>(fr, x, jn_l, lane);
+  load_v<RB, TILED>(fr, x, jn_l, lane);
 
   // 9. value residual entries scatter p*code*scale into their channel
   if constexpr (RESID) {
@@ -503,7 +513,7 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   x.T = a.T;
   x.nblk = (a.T + 15) / 16;
   x.res_stride = a.res_stride;
-  x.ck = a.coef_k + (int64_t)slot * a.T * RB;
+  x.ck = a.coef_k + (int64_t)slot * (IDENT ? a.T : x.nblk * 16) * RB;
   x.cv = a.coef_v + (int64_t)slot * x.nblk * 16 * RB;
   if constexpr (RESID) {
     x.off = a.off + (int64_t)kvh * (a.T + 1);
@@ -553,8 +563,8 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
     }
   }
   __builtin_amdgcn_sched_barrier(0);
-  load_k<RB>(fr, x, j0, lane);
-  load_v<RB>(fr, x, j0, lane);
+  load_k<RB, !IDENT>(fr, x, j0, lane);
+  load_v<RB, !IDENT>(fr, x, j0, lane);
   __builtin_amdgcn_sched_barrier(0);
   if constexpr (RESID) load_entries<TT>(ec, x, mc, lane);
   if (tid < G) sm.qmax[tid] = 0;
@@ -644,7 +654,7 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 
   // stream the wave's tiles
-  for (int j = wv; j < x.ntile; j += kWaves) step<RB, G, RESID>(st, fr, mc, mn, mnn, ec, en, j, x, sm, ws, lane);
+  for (int j = wv; j < x.ntile; j += kWaves) step<RB, G, RESID, !IDENT>(st, fr, mc, mn, mnn, ec, en, j, x, sm, ws, lane);
 
   // epilogue: the 4 waves merge (B^V rows, needed only for the projection,
   // are requested while they do), project a~ through B^V, write the partial

@@ -58,6 +58,7 @@ constexpr int kVB = 3;                  // value-entry batches of 64 loaded ahea
 constexpr int kEmap = TT * kMaxRank;    // entries a tile can hold
 constexpr int kFxTop = 34;              // fixed-point fraction bits = kFxTop - scale exponent bound
 constexpr int kWaitVmcnt0 = 0x0F70;     // s_waitcnt immediate: vmcnt(0) only
+constexpr int kNT = 2;                  // buffer cache policy: nontemporal (whole lines read once)
 constexpr int kTW = kTLWaves;           // waves per workgroup (one workgroup per CU)
 constexpr int kTThreads = 64 * kTW;
 
@@ -163,35 +164,53 @@ __device__ __forceinline__ float code_at(uint32_t w, int n) {
   return (float)((int32_t)(w << (28 - 4 * n)) >> 28);
 }
 
+// Key tiles (16 tokens x 8 coefficients, key_index): for a pair of 16-deep
+// k-steps lane group g reads coefficient group 4 m + g of its token, 16 bytes;
+// for an odd last k-step lane groups 2 i and 2 i + 1 read the two halves of
+// group 4 m + i.  Every instruction reads whole 256-byte tile rows.
 template <int RB>
 __device__ __forceinline__ void load_k(TFrags<RB, false>& f, const TCtx& x, int j, int lane) {
   using C = TCfg<RB>;
   const int grp = lane >> 4, col = lane & 15;
-  const uint32_t base = (uint32_t)(tstart(x, j) + col) * (RB * 2) + C::KH * grp * 2;
+  const uint32_t blk0 = (uint32_t)tstart(x, j) >> 4;
 #pragma unroll
   for (int bk = 0; bk < 4; ++bk) {
+    const uint32_t tile = (blk0 + bk) * (RB / 8);
 #pragma unroll
     for (int s = 0; s + 1 < C::NS; s += 2) {
-      const u4v w = __builtin_amdgcn_raw_buffer_load_b128(x.ck, base + bk * 16 * RB * 2 + 8 * s, 0, 0);
+      const uint32_t g8 = 2 * s + grp;
+      const u4v w = __builtin_amdgcn_raw_buffer_load_b128(x.ck, ((tile + g8) * 128 + col * 8) * 2, 0, kNT);
       f.k[bk][s] = make_uint2(w.x, w.y);
       f.k[bk][s + 1] = make_uint2(w.z, w.w);
     }
     if constexpr (C::NS % 2 == 1) {
-      const u2v w = __builtin_amdgcn_raw_buffer_load_b64(x.ck, base + bk * 16 * RB * 2 + 8 * (C::NS - 1), 0, 0);
+      const uint32_t g8 = 2 * (C::NS - 1) + (grp >> 1);
+      const u2v w = __builtin_amdgcn_raw_buffer_load_b64(x.ck, ((tile + g8) * 128 + col * 8 + 4 * (grp & 1)) * 2, 0, kNT);
       f.k[bk][C::NS - 1] = make_uint2(w.x, w.y);
     }
   }
 }
 
+// Coefficient k held in element i of k-step s by lane group g (the same
+// order on both operands of the score product).
+template <int NS>
+__device__ __forceinline__ int key_k(int s, int g, int i) {
+  return s < NS - (NS & 1) ? 32 * (s >> 1) + 8 * g + 4 * (s & 1) + i : 32 * (NS >> 1) + 4 * g + i;
+}
+
+// Value blocks (8 tokens, value_index): lane c reads channel c's 8 tokens of
+// each block, quads 2 u and 2 u + 1; one instruction reads a whole block.
+// Lanes past r_b read nothing (their products are never used).
 template <int RB>
 __device__ __forceinline__ void load_v(TFrags<RB, false>& f, const TCtx& x, int j, int lane) {
-  // lanes past r_b read neighbouring data whose products are never used
-  const uint32_t base = ((uint32_t)(tstart(x, j) >> 4) * RB + lane) * 32;
+  if (lane < RB) {
+    const uint32_t base = ((uint32_t)(tstart(x, j) >> 3) * RB + lane) * 16;
 #pragma unroll
-  for (int q = 0; q < 16; q += 2) {
-    const u4v w = __builtin_amdgcn_raw_buffer_load_b128(x.cv, base + (q >> 2) * RB * 32 + 8 * (q & 3), 0, 0);
-    f.v[q] = make_uint2(w.x, w.y);
-    f.v[q + 1] = make_uint2(w.z, w.w);
+    for (int u = 0; u < 8; ++u) {
+      const u4v w = __builtin_amdgcn_raw_buffer_load_b128(x.cv, base + u * RB * 16, 0, kNT);
+      f.v[2 * u] = make_uint2(w.x, w.y);
+      f.v[2 * u + 1] = make_uint2(w.z, w.w);
+    }
   }
 }
 
@@ -846,7 +865,7 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
       x.cks = make_rsrc(a.cscale_k + (int64_t)slot * C::NS * T, (uint32_t)(C::NS * T * 2));
       x.cvs = make_rsrc(a.cscale_v + (int64_t)slot * C::NS * T, (uint32_t)(C::NS * T * 2));
     } else {
-      x.ck = make_rsrc(a.coef_k + (int64_t)slot * T * RB, (uint32_t)(T * RB * 2));
+      x.ck = make_rsrc(a.coef_k + (int64_t)slot * nblk * 16 * RB, (uint32_t)(nblk * 16 * RB * 2));
       x.cv = make_rsrc(a.coef_v + (int64_t)slot * nblk * 16 * RB, (uint32_t)(nblk * 16 * RB * 2));
     }
     if constexpr (RESID) {
@@ -870,7 +889,7 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   constexpr int QPT = (G * D + kTThreads - 1) / kTThreads;     // query elements per thread
   const int j0 = min(wv, x.ntile - 1);
   const int j1 = min(wv + kTW, x.ntile - 1);
-  TFrags<RB, C8> fr;
+  TFrags<RB, C8> fr{};                  // lanes past r_b never load values: keep them zero
   TMeta mc{}, mn{}, mnn{};
   TEnt ec{}, en{};
   // q~ fragments, waves below NS only: wave w takes basis rows [16w, 16w+16)
@@ -997,10 +1016,10 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
     for (int s = 0; s < NS; ++s) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        // fp16: lane group grp holds coefficients [KH grp, KH grp + KH); int8:
-        // k-step s is coefficient block s, in the byte order of i8x4_to_h4
+        // fp16: the key tiles' order (key_k); int8: k-step s is coefficient
+        // block s, in the byte order of i8x4_to_h4
         constexpr int ord[4] = {0, 2, 1, 3};
-        const int k = C8 ? 16 * s + 4 * grp + ord[i] : C::KH * grp + 4 * s + i;
+        const int k = C8 ? 16 * s + 4 * grp + ord[i] : key_k<NS>(s, grp, i);
         const float v = h < G ? sm.qt[h][k] * up : 0.f;
         const _Float16 hh = (_Float16)v;
         st.qhi[s][i] = hh;

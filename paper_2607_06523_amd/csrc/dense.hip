@@ -79,11 +79,11 @@ __device__ __forceinline__ void mat_load(MBlock<RB>& m, int64_t w0, int64_t a0, 
     uint2 w = make_uint2(0u, 0u);
     if (mine) {
       if (z == 0) {
-        w = *reinterpret_cast<const uint2*>(ck + t * RB + 16 * s + 4 * grp);
-      } else {
-        const uint16_t* p = cv + ((t >> 4) * RB + 16 * s + 4 * grp) * 16 + (t & 15);
-        w.x = (uint32_t)p[0] | ((uint32_t)p[16] << 16);
-        w.y = (uint32_t)p[32] | ((uint32_t)p[48] << 16);
+        w = *reinterpret_cast<const uint2*>(ck + key_index(t, 16 * s + 4 * grp, RB));
+      } else {                          // 4 channels of token t, 8 elements apart
+        const uint16_t* p = cv + value_index(t, 16 * s + 4 * grp, RB);
+        w.x = (uint32_t)p[0] | ((uint32_t)p[8] << 16);
+        w.y = (uint32_t)p[16] | ((uint32_t)p[24] << 16);
       }
     }
     m.af[s] = __builtin_bit_cast(h4, w);
@@ -201,7 +201,7 @@ __global__ __launch_bounds__(kMW * 64) void materialize_kernel(const MatArgs a) 
   const int64_t g0 = (int64_t)blockIdx.x * kMTok;         // a multiple of 16
   const int64_t gend = min(g0 + (int64_t)kMTok, T);
   const int64_t slab = (int64_t)z * a.n_kv_heads + h;
-  const uint16_t* ck = a.coef_k + (int64_t)h * T * RB;
+  const uint16_t* ck = a.coef_k + (int64_t)h * a.T16 * RB;
   const uint16_t* cv = a.coef_v + (int64_t)h * a.T16 * RB;
   const uint32_t* off = a.off + (int64_t)h * (T + 1);
   const uint8_t* idx = a.idx + slab * a.res_stride;

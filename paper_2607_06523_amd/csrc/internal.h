@@ -32,10 +32,22 @@ struct WorkTable {
   int32_t tok[kKernargSeqs + 1];
 };
 
+// fp16 coefficient layouts, element index inside one (layer, KV head) slab of
+// T16 = T rounded up to 16 tokens (padding zero).  Keys: tiles of 16 tokens x
+// 8 coefficients, [T16/16][rb/8][16][8]; values: 8-token blocks, [T16/8][rb][8].
+// A wave reading a key tile's 16 tokens for 4 coefficient groups, or a value
+// block for 64 channels, reads whole 128-byte lines with one instruction.
+__host__ __device__ __forceinline__ int64_t key_index(int64_t t, int k, int rb) {
+  return (((t >> 4) * (rb >> 3) + (k >> 3)) << 7) + ((t & 15) << 3) + (k & 7);
+}
+__host__ __device__ __forceinline__ int64_t value_index(int64_t t, int c, int rb) {
+  return ((t >> 3) * rb + c) * 8 + (t & 7);
+}
+
 // One split-K pass over a layer: grid = (work items, head slots).
 struct SplitArgs {
-  const uint16_t* coef_k;      // slot 0 key rows [T][RB]; slot s adds s*T*RB
-  const uint16_t* coef_v;      // slot 0 value blocks [T16/16][RB][16]; slot s adds s*T16*RB
+  const uint16_t* coef_k;      // slot 0 key tiles (key_index; int8: rows [T][RB]); slot s adds s*T16*RB (int8 s*T*RB)
+  const uint16_t* coef_v;      // slot 0 value blocks (value_index; int8: [T16/16][RB][16]); slot s adds s*T16*RB
   const uint16_t* basis;       // basis of window m, sequence 0: + (b*M*Hkv + h)*2*RB*d
   int64_t basis_b_stride;      // halves between sequences (M*Hkv*2*RB*d)
   const uint32_t* off;         // res_off of window m, head 0; head h adds h*(T+1)
@@ -194,8 +206,8 @@ struct CompressArgs {
   const uint16_t* xk;          // [n][Hkv][d] fp16
   const uint16_t* xv;
   const float* gate;           // [2][Hkv][n] or null (g = 1)
-  uint16_t* coef_k;            // layer's [Hkv][T][rb]
-  uint16_t* coef_v;            // layer's [Hkv][T16/16][rb][16]
+  uint16_t* coef_k;            // layer's [Hkv] slabs of T16*rb (key_index)
+  uint16_t* coef_v;            // layer's [Hkv] slabs of T16*rb (value_index)
   uint8_t* res_idx;            // layer's [2][Hkv][res_stride]
   uint8_t* res_val;            // layer's [2][Hkv][res_stride/2]
   uint16_t* res_scale;         // layer's [2][Hkv][T]
@@ -230,8 +242,8 @@ hipError_t launch_compress(const CompressArgs& a, hipStream_t s);
 struct MatArgs {
   const uint16_t* basis;       // window m, sequence 0; sequence b adds b*basis_b_stride, (h, z) add (h*2+z)*rb*d
   int64_t basis_b_stride;
-  const uint16_t* coef_k;      // layer's [Hkv][T][rb]
-  const uint16_t* coef_v;      // layer's [Hkv][T16/16][rb][16]
+  const uint16_t* coef_k;      // layer's [Hkv] slabs of T16*rb (key_index)
+  const uint16_t* coef_v;      // layer's [Hkv] slabs of T16*rb (value_index)
   const uint32_t* off;         // window's [Hkv][T+1]
   const uint8_t* idx;          // layer's [2][Hkv][res_stride]
   const uint8_t* val;          // layer's [2][Hkv][res_stride/2]

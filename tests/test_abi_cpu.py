@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.dwkv_abi_version() == 2
+    assert lib.dwkv_abi_version() == 3
     for s, text in [(0, b"ok"), (3, b"unsupported shape"), (5, b"malformed cache layout"),
                     (7, b"device pointer not 16-byte aligned")]:
         assert lib.dwkv_status_str(s) == text

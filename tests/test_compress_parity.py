@@ -43,9 +43,10 @@ WRITTEN = ("coef_k", "coef_v", "res_idx", "res_val", "res_scale")
 
 
 def _host_arrays(dc):
+    keys, values = dc.coef_host()       # back from the ABI's tiled layouts
     return {
-        "coef_k": dc.coef_k.cpu().numpy().view(np.float16),
-        "coef_v": dc.coef_v.cpu().numpy().view(np.float16),
+        "coef_k": keys.view(np.float16),
+        "coef_v": values.view(np.float16),
         "res_idx": dc.res_idx.cpu().numpy(),
         "res_val": dc.res_val.cpu().numpy(),
         "res_scale": dc.res_scale.cpu().numpy().view(np.float16),
