@@ -107,7 +107,9 @@ typedef struct dwkv_cache {
   const void*     res_scale; /* fp16 [L][2][Hkv][T] gate-folded residual scale g*s         */
   const void*     coef_k_scale; /* DWKV_COEF_I8 only (else ignored): fp16 [L][Hkv][r_b/16][T]
                                 block scales of the key coefficients; coef_k then holds int8
-                                codes in rows [L][Hkv][T][r_b]                              */
+                                codes in tiles of 16 tokens x 16 codes,
+                                [L][Hkv][T16/16][r_b/16][16][16]: token t, code i at
+                                [t/16][i/16][t%16][i%16] (padding tokens zero)            */
   const void*     coef_v_scale; /* DWKV_COEF_I8 only: fp16 [L][Hkv][r_b/16][T] value block
                                 scales; coef_v then holds int8 codes in 16-token blocks
                                 [L][Hkv][T16/16][r_b][16], token fastest                    */

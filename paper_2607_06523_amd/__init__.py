@@ -80,7 +80,7 @@ class DeviceCache:
         self.basis = up(host.basis.view(np.uint16), torch.float16)
         self.coef_format = getattr(host, "coef_format", "f16")
         if self.coef_format == "int8":        # codes and their fp16 block scales
-            self.coef_k = up(host.coef_k.view(np.uint8), torch.uint8)
+            self.coef_k = up(layout.keys_to_abi(host.coef_k.view(np.uint8), group=16), torch.uint8)
             self.coef_v = up(host.coef_v.view(np.uint8), torch.uint8)
             self.coef_scale_k = up(host.coef_scale_k.view(np.uint16), torch.float16)
             self.coef_scale_v = up(host.coef_scale_v.view(np.uint16), torch.float16)
@@ -354,14 +354,14 @@ class DeviceCache:
 
     def coef_host(self):
         """The device coefficients in the host layout (fp16 as uint16): keys
-        [L][Hkv][T][r_b], values [L][Hkv][T16/16][r_b][16]; int8 codes as stored."""
+        [L][Hkv][T][r_b], values [L][Hkv][T16/16][r_b][16] (int8: codes, same shapes)."""
         k = self.coef_k.cpu().numpy()
         v = self.coef_v.cpu().numpy()
-        if self.coef_format == "int8":
-            return k, v
-        k, v = k.view(np.uint16), v.view(np.uint16)
         L, Hk, T, rb = self.n_layers, self.n_kv_heads, self.total_tokens, self.basis_rank
         T16 = -(-T // 16) * 16
+        if self.coef_format == "int8":
+            return layout.keys_from_abi(k.reshape(L, Hk, T16 // 16, rb // 16, 16, 16), T), v
+        k, v = k.view(np.uint16), v.view(np.uint16)
         keys = layout.keys_from_abi(k.reshape(L, Hk, T16 // 16, rb // 8, 16, 8), T)
         vals = layout.values_from_abi(v.reshape(L, Hk, T16 // 8, rb, 8))
         return keys, vals

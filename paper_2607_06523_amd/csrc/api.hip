@@ -239,7 +239,7 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   SplitArgs a;
   std::memset(&a, 0, sizeof(a));
   if (c8) {                     // int8 codes: one byte per coefficient
-    a.coef_k = reinterpret_cast<const uint16_t*>(static_cast<const uint8_t*>(c->coef_k) + (int64_t)layer * Hk * T * RB);
+    a.coef_k = reinterpret_cast<const uint16_t*>(static_cast<const uint8_t*>(c->coef_k) + (int64_t)layer * Hk * T16 * RB);
     a.coef_v = reinterpret_cast<const uint16_t*>(static_cast<const uint8_t*>(c->coef_v) + (int64_t)layer * Hk * T16 * RB);
     a.cscale_k = static_cast<const uint16_t*>(c->coef_k_scale) + (int64_t)layer * Hk * (RB / 16) * T;
     a.cscale_v = static_cast<const uint16_t*>(c->coef_v_scale) + (int64_t)layer * Hk * (RB / 16) * T;

@@ -225,16 +225,20 @@ __device__ __forceinline__ h4 i8x4_to_h4(uint32_t w) {
   return __builtin_shufflevector(lo, hi, 0, 1, 2, 3);
 }
 
+// int8 key tiles (16 tokens x 16 codes): k-step s of lane (grp, col) is codes
+// 16 s + 4 grp .. + 4 of token col, so one instruction reads a whole 256-byte
+// tile.  Value blocks: lane c reads channel c's 16 codes, lanes past r_b
+// nothing.  Scales: one 2-byte load per lane and block.
 template <int RB>
 __device__ __forceinline__ void load_k8(TFrags<RB, true>& f, const TCtx& x, int j, int lane) {
   using C = TCfg<RB>;
   const int grp = lane >> 4, col = lane & 15;
-  const uint32_t base = (uint32_t)(tstart(x, j) + col) * RB + 4 * grp;
+  const uint32_t blk0 = (uint32_t)tstart(x, j) >> 4;
 #pragma unroll
   for (int bk = 0; bk < 4; ++bk)
 #pragma unroll
     for (int s = 0; s < C::NS; ++s)
-      f.k[bk][s] = __builtin_amdgcn_raw_buffer_load_b32(x.ck, base + bk * 16 * RB + 16 * s, 0, 0);
+      f.k[bk][s] = __builtin_amdgcn_raw_buffer_load_b32(x.ck, ((blk0 + bk) * C::NS + s) * 256 + col * 16 + 4 * grp, 0, kNT);
   const uint32_t t = (uint32_t)(tstart(x, j) + lane);
 #pragma unroll
   for (int s = 0; s < C::NS; ++s)
@@ -244,15 +248,17 @@ __device__ __forceinline__ void load_k8(TFrags<RB, true>& f, const TCtx& x, int 
 template <int RB>
 __device__ __forceinline__ void load_v8(TFrags<RB, true>& f, const TCtx& x, int j, int lane) {
   using C = TCfg<RB>;
-  // 16 bytes per (16-token block, channel): the 16 tokens' codes of channel `lane`
-  const uint32_t base = ((uint32_t)(tstart(x, j) >> 4) * RB + lane) * 16;
+  if (lane < RB) {
+    // 16 bytes per (16-token block, channel): the 16 tokens' codes of channel `lane`
+    const uint32_t base = ((uint32_t)(tstart(x, j) >> 4) * RB + lane) * 16;
 #pragma unroll
-  for (int tb = 0; tb < 4; ++tb) {
-    const u4v w = __builtin_amdgcn_raw_buffer_load_b128(x.cv, base + tb * RB * 16, 0, 0);
-    f.v[4 * tb] = w.x;
-    f.v[4 * tb + 1] = w.y;
-    f.v[4 * tb + 2] = w.z;
-    f.v[4 * tb + 3] = w.w;
+    for (int tb = 0; tb < 4; ++tb) {
+      const u4v w = __builtin_amdgcn_raw_buffer_load_b128(x.cv, base + tb * RB * 16, 0, kNT);
+      f.v[4 * tb] = w.x;
+      f.v[4 * tb + 1] = w.y;
+      f.v[4 * tb + 2] = w.z;
+      f.v[4 * tb + 3] = w.w;
+    }
   }
   const uint32_t t = (uint32_t)(tstart(x, j) + lane);
 #pragma unroll
@@ -860,7 +866,7 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
     if constexpr (C8) {
       const uint8_t* ck8 = reinterpret_cast<const uint8_t*>(a.coef_k);
       const uint8_t* cv8 = reinterpret_cast<const uint8_t*>(a.coef_v);
-      x.ck = make_rsrc(ck8 + (int64_t)slot * T * RB, (uint32_t)(T * RB));
+      x.ck = make_rsrc(ck8 + (int64_t)slot * nblk * 16 * RB, (uint32_t)(nblk * 16 * RB));
       x.cv = make_rsrc(cv8 + (int64_t)slot * nblk * 16 * RB, (uint32_t)(nblk * 16 * RB));
       x.cks = make_rsrc(a.cscale_k + (int64_t)slot * C::NS * T, (uint32_t)(C::NS * T * 2));
       x.cvs = make_rsrc(a.cscale_v + (int64_t)slot * C::NS * T, (uint32_t)(C::NS * T * 2));
