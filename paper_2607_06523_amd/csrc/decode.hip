@@ -14,16 +14,17 @@
 // Mapping (one workgroup = 4 waves = one chunk of `split` tokens of one
 // sequence and one KV head; each wave streams every 4th tile of 16*NBK tokens):
 //  * scores S[tok][g] = A^K[tok][:] . q~[:][g] on v_mfma_f32_16x16x16_f16: key
-//    rows (row-major in HBM) are the A operand, loaded straight into registers
-//    (lane = token % 16, 4 coefficients by lane / 16); q~ is the B operand, held
+//    coefficients are the A operand, loaded straight into registers (lane =
+//    token % 16, 4 consecutive coefficients by lane / 16: one 8-byte load from
+//    the key tiles, or from a dense cache's rows); q~ is the B operand, held
 //    for the whole split as fp16 hi + lo parts (two MFMAs, float32-accurate
 //    scores); the G query heads of the group fill columns 0..G-1.
 //  * the MFMA result layout (lane = head, 4 consecutive tokens per lane) is the
 //    A-operand layout of a~[g][:] += P[g][tok] A^V[tok][:], so probabilities feed
 //    the value product with no shuffle; value coefficients are stored in
-//    16-token blocks with the token index fastest, so the B operand (4
-//    consecutive tokens of one channel per lane) is one 8-byte load per lane
-//    and 512 contiguous bytes per wave instruction, straight from HBM.
+//    8-token blocks (a dense cache's values in 16-token blocks) with the token
+//    index fastest, so the B operand (4 consecutive tokens of one channel per
+//    lane) is one 8-byte load per lane, straight from HBM.
 //  * fragments are single-buffered with early release: the next tile's key
 //    fragments are requested right after this tile's score MFMAs, its value
 //    fragments right after the value MFMAs; offsets run two tiles ahead and
@@ -116,7 +117,7 @@ struct Smem {
 // Registers holding one tile's coefficient fragments.
 template <int RB>
 struct Frags {
-  uint2 k[Cfg<RB>::NBK][Cfg<RB>::NS];   // key rows: 4 coefficients per k-step
+  uint2 k[Cfg<RB>::NBK][Cfg<RB>::NS];   // key fragments: 4 coefficients per k-step
   uint2 v[Cfg<RB>::NBK][Cfg<RB>::NS];   // value blocks: 4 tokens of one channel per step
 };
 

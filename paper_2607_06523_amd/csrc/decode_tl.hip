@@ -28,7 +28,7 @@
 //    lane quad turns the probabilities into (head, 4 tokens) rows; each
 //    instruction broadcasts one quad's rows to all blocks (CBSZ/ABID) and the
 //    blocks cover 64 coefficient channels, read as 4 consecutive tokens of one
-//    channel from the 16-token value blocks.  The accumulator holds, in lane c,
+//    channel from the 8-token value blocks.  The accumulator holds, in lane c,
 //    the basis-space value of channel c for the 4 heads.
 //  * the epilogue combines the waves and writes the partial in basis space
 //    (a~, the residual channels, m, l).  A second, wide launch merges them in
@@ -89,7 +89,7 @@ struct alignas(16) TSmem {
 
 template <int RB, bool C8>
 struct TFrags {
-  uint2 k[4][TCfg<RB>::NS];             // key rows, block bk, k-step s
+  uint2 k[4][TCfg<RB>::NS];             // key fragments (tile order, key_k), block bk, k-step s
   uint2 v[16];                          // value channel `lane`, token quad q
 };
 
