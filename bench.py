@@ -284,6 +284,45 @@ class DeviceCache2:
         binding.check(st, "dwkv_route_budget")
 
 
+def measure_probe(dc, host, torch, steps: int = 5, warmup: int = 2):
+    """The decode step with the Eq. 3 probe on one KV head and on all of them:
+    each layer runs the factorized decode plus the dense reference pass over
+    the probed heads' fp16 reference cache and the probe error.  One synthetic
+    reference (random fp16, all T tokens) serves every layer."""
+    from paper_2607_06523_amd import ProbeRef
+    L, T, d, Hk = host.n_layers, host.total_tokens, host.head_dim, host.n_kv_heads
+    T16 = -(-T // 16) * 16
+    stream = torch.cuda.current_stream()
+    res = {}
+    for heads in ((0,), tuple(range(Hk))):
+        n = len(heads)
+        gen = torch.Generator(device="cuda").manual_seed(7)
+        k_ref = torch.randn((n, T, d), device="cuda", generator=gen).half()
+        v_ref = torch.randn((n, T16 // 16, d, 16), device="cuda", generator=gen).half()
+        probe = ProbeRef(list(heads), k_ref, v_ref)
+        ws = dc.new_workspace(probe)
+
+        def step():
+            for l in range(L):
+                dc.decode(l, probe=probe, workspace=ws)
+        for _ in range(warmup):
+            step()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for _ in range(steps):
+            step()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / steps
+        res[f"probe_{n}_heads"] = {"tokens_per_s": round(host.batch / (ms / 1e3), 2), "ms_per_step": round(ms, 4),
+                                   "reference_bytes_per_layer": int(n * T * d * 2 * 2)}
+        del k_ref, v_ref, ws
+    res["note"] = ("dwkv_decode with a probe on every layer: the factorized decode plus a dense split pass over "
+                   "the probed heads' fp16 reference and the Eq. 3 error in the merge")
+    return res
+
+
 def measure_comparators(dc, host, torch, steps: int = 3):
     """The decode's comparison paths on the same GPU and workload: a dense fp16
     cache decode (every layer's K/V resident, 2 bytes per element) and the
@@ -545,6 +584,9 @@ def main():
     if not args.no_comparators and args.variant == "full":
         log("[bench] timing the dense fp16 and unfused comparison paths")
         result["comparators"] = measure_comparators(dc, host, torch)
+    if not args.no_comparators and args.variant == "full":
+        log("[bench] timing the decode with the Eq. 3 probe")
+        result["with_probe"] = measure_probe(dc, host, torch)
     if not args.no_comparators and args.variant == "full":
         log("[bench] timing the control steps (budget routing, sketch bases)")
         result["control"] = measure_control(dc, host, wl, torch)

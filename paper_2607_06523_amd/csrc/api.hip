@@ -93,6 +93,20 @@ int plan_split_general(const dwkv_dims* d) {
   return (int)c;
 }
 
+// Chunk size of the probe's dense reference pass over n_heads probed KV
+// heads: about kTargetWorkgroups / 2 workgroups for the pass, so that one
+// probed head is not streamed by a handful of workgroups, while its merge
+// still reads few partials.  An explicit split_tokens applies here too.
+int plan_split_ref(const dwkv_dims* d, int n_heads) {
+  if (d->split_tokens > 0) return d->split_tokens;
+  const int64_t work = d->total_tokens * n_heads, target = kTargetWorkgroups / 2;
+  int64_t c = (work + target - 1) / target;
+  c = (c + kSplitQuantum - 1) / kSplitQuantum * kSplitQuantum;
+  if (c < kSplitQuantum) c = kSplitQuantum;
+  if (c > kSplitMax) c = kSplitMax;
+  return (int)c;
+}
+
 int64_t count_work(const dwkv_dims* d, int split) {
   int64_t n = 0;
   for (int b = 0; b < d->batch; ++b) {
@@ -129,7 +143,8 @@ WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
   const int stride = uses_token_lane(d) ? kPartStrideTL : kPartStride;
   WsLayout w;
   w.main_bytes = align_up((size_t)nw * d->n_kv_heads * g * stride * sizeof(float), 256);
-  w.ref_bytes = p ? align_up((size_t)nw * p->n_heads * g * kPartStride * sizeof(float), 256) : 0;
+  const int64_t nw_ref = p ? count_work(d, plan_split_ref(d, p->n_heads)) : 0;
+  w.ref_bytes = p ? align_up((size_t)nw_ref * p->n_heads * g * kPartStride * sizeof(float), 256) : 0;
   w.total = w.main_bytes + w.ref_bytes;
   if (w.total == 0) w.total = 256;
   return w;
@@ -285,7 +300,11 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
     r.part = reinterpret_cast<float*>(ws + wl.main_bytes);
     r.n_slots = probe->n_heads;
     for (int i = 0; i < probe->n_heads; ++i) r.kv_of_slot[i] = probe->kv_heads_host[i];
-    if (launch_split(kHeadDim, G, false, true, r, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
+    r.split = plan_split_ref(d, probe->n_heads);
+    const int64_t nw_ref = count_work(d, r.split);
+    r.n_work = (int32_t)nw_ref;
+    r.wt = work_table(d, r.split);
+    if (launch_split(kHeadDim, G, false, true, r, (int)nw_ref, s) != hipSuccess) return DWKV_E_HIP;
   }
   return DWKV_OK;
 }
@@ -341,6 +360,8 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   }
   mg.n_probe = probe ? probe->n_heads : 0;
   mg.eps = probe ? probe->eps : 0.f;
+  mg.ref_split = probe ? plan_split_ref(d, probe->n_heads) : mg.split;
+  mg.ref_wt = work_table(d, mg.ref_split);
   for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) mg.probe_slot_of_kv[h] = -1;
   if (probe)
     for (int i = 0; i < probe->n_heads; ++i) mg.probe_slot_of_kv[probe->kv_heads_host[i]] = i;

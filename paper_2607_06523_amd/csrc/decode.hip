@@ -901,8 +901,10 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   if (a.n_probe > 0) {
     const int sl = a.probe_slot_of_kv[h];
     if (sl >= 0) {
-      const f4 r = merge_rows(a.part_ref, (int64_t)base * a.n_probe * G + sl * G + g,
-                                  (int64_t)a.n_probe * G, ns, kPartStride, D, D, red_m, red_l, red_o).x;
+      int base_r, ns_r;                  // the probe pass has its own work split
+      seq_work(a.ref_wt, a.cu, a.ref_split, b, base_r, ns_r);
+      const f4 r = merge_rows(a.part_ref, (int64_t)base_r * a.n_probe * G + sl * G + g,
+                                  (int64_t)a.n_probe * G, ns_r, kPartStride, D, D, red_m, red_l, red_o).x;
       const int64_t col = (int64_t)b * a.n_probe * G + sl * G + g;
       float d2 = 0.f, r2 = 0.f;
       if (sg == 0) {

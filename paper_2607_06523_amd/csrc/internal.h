@@ -99,6 +99,8 @@ struct MergeArgs {
   int32_t rb;
   const uint16_t* basis;       // basis of window m, sequence 0: + (b*M*Hkv + h)*2*RB*d (tl only)
   int64_t basis_b_stride;
+  int32_t ref_split;           // the probe pass's chunk size and work split
+  WorkTable ref_wt;
 };
 
 // Makes the kernel-argument values the whole split kernel needs live in scalar
