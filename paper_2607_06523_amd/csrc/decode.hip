@@ -36,6 +36,8 @@
 //  * epilogue: the 4 waves merge (m, l, a~, r) in LDS, project a~ through B^V
 //    and write one partial (o, m, l) per query head; a merge kernel combines
 //    the splits (and computes Eq. 3's error for probed heads).
+#include <type_traits>
+
 #include "entry.h"
 #include "internal.h"
 
@@ -82,6 +84,15 @@ struct Cfg {
   static_assert(RB % 16 == 0 && RB >= 16 && RB <= 128, "r_b");
 };
 
+// Value residuals accumulate in int64 fixed point (units of 2^(ex - kFxTopG),
+// ex the wave's bound on the value scales: |p code s| 2^(kFxTopG - ex) < 2^45
+// with p <= 1) wherever the workgroup's LDS still fits with 8-byte
+// accumulators (every G <= 8; G = 16 up to r_b = 96), else in float.
+constexpr int kFxTopG = 42;
+
+template <int RB, int G>
+constexpr bool kFixedResid = G <= 8 || RB <= 96;
+
 template <int RB, int G, bool RESID>
 struct alignas(16) WaveSmem {
   static constexpr int TT = Cfg<RB>::TT;
@@ -89,10 +100,12 @@ struct alignas(16) WaveSmem {
   static constexpr int RT = RESID ? TT : 1;
   static constexpr int RD = RESID ? D : 1;
   static constexpr int RE = RESID ? kEntChunk : 8;
+  using Acc = std::conditional_t<kFixedResid<RB, G>, long long, float>;
   float resid[RG][RT];                 // key-residual score per head and token
   float p[RT][RG];                     // tile probabilities (for value residuals)
   float rsv[RT];                       // gate-folded residual scale, values
-  float racc[RG][RD];                  // value-residual accumulator
+  Acc racc[RG][RD];                    // value-residual accumulator
+  int ex;                              // fixed point: the wave's scale bound, for the epilogue
   uint8_t eidx[2][RE];                 // staged channel bytes (keys, values)
   uint8_t eval[2][RE / 2];             // staged code bytes (2 entries per byte)
   uint8_t emap[RE];                    // tile token of each staged entry
@@ -136,7 +149,15 @@ struct State {
   h4 qhi[Cfg<RB>::NS], qlo[Cfg<RB>::NS];
   f4 acc[Cfg<RB>::NS];                  // a~ in MFMA result layout
   float m, l, down;
+  int ex;                               // fixed point: bound on the value scales seen, |s_v| < 2^ex
 };
+
+// One value-residual term into its accumulator (fixed point or float).
+template <typename Acc>
+__device__ __forceinline__ void resid_add(Acc* r, float v, double scale) {
+  if constexpr (sizeof(Acc) == 8) atomicAdd(reinterpret_cast<unsigned long long*>(r), to_fixed(v, scale));
+  else atomicAdd(r, v);
+}
 
 struct Ctx {
   const uint16_t* ck;                   // key tiles of this slab (key_index); dense: rows [T][RB]
@@ -304,7 +325,7 @@ __device__ __forceinline__ void key_resid_tokens(WaveSmem<RB, G, true>& ws, cons
 // accumulator (ds_add_f32; channels of different tokens may coincide).
 template <int RB, int G>
 __device__ __forceinline__ void value_resid_entries(WaveSmem<RB, G, true>& ws, uint32_t e0, uint32_t e1,
-                                                    uint32_t ia, int lane) {
+                                                    uint32_t ia, int lane, double scale) {
   for (uint32_t base = e0; base < e1; base += 64) {
     const uint32_t e = base + lane;
     if (e < e1) {
@@ -317,7 +338,7 @@ __device__ __forceinline__ void value_resid_entries(WaveSmem<RB, G, true>& ws, u
       for (int g = 0; g < G; ++g) pv[g] = ws.p[t][g];
       const float s = ws.rsv[t] * code;
 #pragma unroll
-      for (int g = 0; g < G; ++g) atomicAdd(&ws.racc[g][c], pv[g] * s);
+      for (int g = 0; g < G; ++g) resid_add(&ws.racc[g][c], pv[g] * s, scale);
     }
   }
 }
@@ -326,7 +347,7 @@ __device__ __forceinline__ void value_resid_entries(WaveSmem<RB, G, true>& ws, u
 // entries read from HBM.
 template <int RB, int G>
 __device__ __forceinline__ void value_resid_tokens_global(WaveSmem<RB, G, true>& ws, const Ctx& x,
-                                                          const Meta& m, int lane) {
+                                                          const Meta& m, int lane, double scale) {
   if (lane >= Cfg<RB>::TT) return;
   float pv[G];
 #pragma unroll
@@ -336,7 +357,7 @@ __device__ __forceinline__ void value_resid_tokens_global(WaveSmem<RB, G, true>&
     const uint32_t c = x.idx[1][e] & (D - 1);
     const float s = rs * (float)entry_code(x.val[1][e >> 1], e);
 #pragma unroll
-    for (int g = 0; g < G; ++g) atomicAdd(&ws.racc[g][c], pv[g] * s);
+    for (int g = 0; g < G; ++g) resid_add(&ws.racc[g][c], pv[g] * s, scale);
   }
 }
 
@@ -446,7 +467,9 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
       for (int it = 0; it < (G * D) / 64; ++it) {
         const int g = (it * 64) / D;
         const float ag = __shfl(alpha, g);
-        (&ws.racc[0][0])[it * 64 + lane] *= ag;
+        auto& r = (&ws.racc[0][0])[it * 64 + lane];
+        if constexpr (kFixedResid<RB, G>) r = __double2ll_rn((double)r * (double)ag);
+        else r *= ag;
       }
     }
     // 7. probabilities to LDS for the value entries
@@ -479,10 +502,28 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
 
   // 9. value residual entries scatter p*code*scale into their channel
   if constexpr (RESID) {
+    double scale = 0.0;
+    if constexpr (kFixedResid<RB, G>) {
+      // a value scale beyond the wave's bound shifts the accumulators down first
+      const uint32_t eb = (mc.sv >> 10) & 31u;
+      const int el = lane < TT ? (int)max(eb, 1u) - 14 : st.ex;
+      if (__ballot(el > st.ex) != 0) {
+        int emax = el;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) emax = max(emax, __shfl_xor(emax, o));
+        const double f = ldexp(1.0, st.ex - emax);
+        for (int i = lane; i < G * D; i += 64) {
+          auto& r = (&ws.racc[0][0])[i];
+          r = __double2ll_rn((double)r * f);
+        }
+        st.ex = emax;
+      }
+      scale = ldexp(1.0, kFxTopG - st.ex);
+    }
     wave_lds_fence();
     if (e1 > e0) {
-      if (staged) value_resid_entries<RB, G>(ws, e0, e1, ia, lane);
-      else value_resid_tokens_global<RB, G>(ws, x, mc, lane);
+      if (staged) value_resid_entries<RB, G>(ws, e0, e1, ia, lane, scale);
+      else value_resid_tokens_global<RB, G>(ws, x, mc, lane, scale);
     }
     wave_lds_fence();
     mc = mn;
@@ -644,9 +685,10 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   }
   st.m = -INFINITY;
   st.l = 0.f;
+  st.ex = -14;
   auto& ws = sm.w[wv];
   if constexpr (RESID) {
-    for (int i = lane; i < G * D; i += 64) (&ws.racc[0][0])[i] = 0.f;
+    for (int i = lane; i < G * D; i += 64) (&ws.racc[0][0])[i] = 0;
   }
 
   // Every prologue load completes before the loop (the first iteration needs
@@ -656,6 +698,9 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
 
   // stream the wave's tiles
   for (int j = wv; j < x.ntile; j += kWaves) step<RB, G, RESID, !IDENT>(st, fr, mc, mn, mnn, ec, en, j, x, sm, ws, lane);
+  if constexpr (RESID) {
+    if (lane == 0) ws.ex = st.ex;      // read by every thread after the epilogue's barrier
+  }
 
   // epilogue: the 4 waves merge (B^V rows, needed only for the projection,
   // are requested while they do), project a~ through B^V, write the partial
@@ -715,7 +760,12 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
       for (int k = 0; k < RB; ++k) o += sm.acomb[g][k] * half_bits_to_float(sm.bvs[k][c_out]);
     }
     if constexpr (RESID) {
-      for (int v = 0; v < kWaves; ++v) o += sm.sw[v][g] * sm.w[v].racc[g][c_out];
+      for (int v = 0; v < kWaves; ++v) {
+        if constexpr (kFixedResid<RB, G>)
+          o += sm.sw[v][g] * (fixed_to_float(sm.w[v].racc[g][c_out]) * ldexpf(1.0f, sm.w[v].ex - kFxTopG));
+        else
+          o += sm.sw[v][g] * sm.w[v].racc[g][c_out];
+      }
     }
     float* dst = part_ws + (((int64_t)w * a.n_slots + slot) * G + g) * kPartStride;
     dst[c_out] = o;

@@ -301,24 +301,6 @@ __device__ __forceinline__ void load_entries(TEnt& e, const TCtx& x, const TMeta
   }
 }
 
-// Fixed point: round(v * scale) as a two's complement int64 for
-// |v * scale| < 2^51 (adding 1.5 * 2^52 leaves the rounded integer in the low
-// mantissa bits).
-__device__ __forceinline__ unsigned long long to_fixed(float v, double scale) {
-  const double magic = 6755399441055744.0;
-  const double t = __builtin_fma((double)v, scale, magic);
-  return (unsigned long long)(__double_as_longlong(t) - __double_as_longlong(magic));
-}
-
-// A fixed-point accumulator as float.  Below 2^53 in magnitude the two
-// halves combine exactly in double and the result is rounded once (terms stay
-// below 2^45, so this holds while a wave adds at most 256 tokens to a
-// channel); above it a second rounding can move the result by one float ulp.
-__device__ __forceinline__ float fixed_to_float(long long v) {
-  const double hi = (double)(int32_t)(v >> 32), lo = (double)(uint32_t)(v & 0xFFFFFFFFll);
-  return (float)__builtin_fma(hi, 4294967296.0, lo);
-}
-
 // Order LDS traffic between lanes of one wave.
 __device__ __forceinline__ void wave_lds_fence() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

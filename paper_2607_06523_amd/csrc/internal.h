@@ -32,6 +32,27 @@ struct WorkTable {
   int32_t tok[kKernargSeqs + 1];
 };
 
+// Value-residual sums in LDS are int64 fixed point: integer LDS atomics cost a
+// few cycles per instruction whatever the active lanes (float ones a few per
+// lane), and their sums do not depend on the order of the additions.
+// Fixed point: round(v * scale) as a two's complement int64 for
+// |v * scale| < 2^51 (adding 1.5 * 2^52 leaves the rounded integer in the low
+// mantissa bits).
+__device__ __forceinline__ unsigned long long to_fixed(float v, double scale) {
+  const double magic = 6755399441055744.0;
+  const double t = __builtin_fma((double)v, scale, magic);
+  return (unsigned long long)(__double_as_longlong(t) - __double_as_longlong(magic));
+}
+
+// A fixed-point accumulator as float.  Below 2^53 in magnitude the two
+// halves combine exactly in double and the result is rounded once (with terms
+// below 2^45 this holds while a wave adds at most 256 of them to one
+// accumulator); above it a second rounding can move the result by one ulp.
+__device__ __forceinline__ float fixed_to_float(long long v) {
+  const double hi = (double)(int32_t)(v >> 32), lo = (double)(uint32_t)(v & 0xFFFFFFFFll);
+  return (float)__builtin_fma(hi, 4294967296.0, lo);
+}
+
 // fp16 coefficient layouts, element index inside one (layer, KV head) slab of
 // T16 = T rounded up to 16 tokens (padding zero).  Keys: tiles of 16 tokens x
 // 8 coefficients, [T16/16][rb/8][16][8]; values: 8-token blocks, [T16/8][rb][8].
