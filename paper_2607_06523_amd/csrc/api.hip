@@ -69,6 +69,8 @@ bool uses_token_lane(const dwkv_dims* d) {
          chunks * g * kPartStrideTL * (int64_t)sizeof(float) < ((int64_t)1 << 31);
 }
 
+int64_t count_work(const dwkv_dims* d, int split);
+
 int plan_split(const dwkv_dims* d) {
   if (d->split_tokens > 0) return d->split_tokens;
   const int64_t work = d->total_tokens * d->n_kv_heads;
@@ -77,6 +79,9 @@ int plan_split(const dwkv_dims* d) {
   int64_t c = (work + target - 1) / target;
   c = (c + kSplitQuantum - 1) / kSplitQuantum * kSplitQuantum;
   if (c < kSplitQuantum) c = kSplitQuantum;
+  // every sequence rounds its chunks up: grow the chunk until the workgroups
+  // of all sequences fit one round of the target
+  while (c < kSplitMax && count_work(d, (int)c) * d->n_kv_heads > target) c += kSplitQuantum;
   if (c > kSplitMax) c = kSplitMax;
   return (int)c;
 }
