@@ -677,22 +677,33 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
           atomicAdd(reinterpret_cast<unsigned long long*>(&sm.racc[wv][i][c]), to_fixed(wv4[bb][i] * code, scale));
       }
     }
-    // entries past the preloaded batches (tiles with more than 64 kVB)
-    for (uint32_t b0 = 64u * kVB; b0 < n; b0 += 64) {
-      const uint32_t e = b0 + lane;
-      int t = e < n ? sm.emap[wv][e] : 0;
-      t = max(wave_incl_max(t), carry);
-      carry = __builtin_amdgcn_readlane(t, 63);
-      if (e < n) {
-        const uint32_t ea = e0 + e;
-        const uint32_t ch = __builtin_amdgcn_raw_buffer_load_b8(x.idx[1], ea, 0, 0);
-        const uint32_t cb = __builtin_amdgcn_raw_buffer_load_b8(x.val[1], ea >> 1, 0, 0);
-        const f4 w = *reinterpret_cast<const f4*>(&sm.pw[wv][t - 1][0]);
-        const float code = (float)int4_value(cb >> ((ea & 1u) * 4u));
-        const uint32_t c = ch & (D - 1);
+    // entries past the preloaded batches (tiles with more than 64 kVB): their
+    // bytes are requested kXB batches at a time, one round trip per group
+    constexpr int kXB = 4;
+    for (uint32_t g0 = 64u * kVB; g0 < n; g0 += 64u * kXB) {
+      uint32_t chv[kXB], cbv[kXB];
 #pragma unroll
-        for (int i = 0; i < G; ++i)
-          atomicAdd(reinterpret_cast<unsigned long long*>(&sm.racc[wv][i][c]), to_fixed(w[i] * code, scale));
+      for (int u = 0; u < kXB; ++u) {   // past the slab a buffer load reads zero
+        const uint32_t ea = e0 + g0 + 64u * u + lane;
+        chv[u] = __builtin_amdgcn_raw_buffer_load_b8(x.idx[1], ea, 0, 0);
+        cbv[u] = __builtin_amdgcn_raw_buffer_load_b8(x.val[1], ea >> 1, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < kXB; ++u) {
+        const uint32_t e = g0 + 64u * u + lane;
+        if (g0 + 64u * u >= n) break;   // uniform
+        int t = e < n ? sm.emap[wv][e] : 0;
+        t = max(wave_incl_max(t), carry);
+        carry = __builtin_amdgcn_readlane(t, 63);
+        if (e < n) {
+          const uint32_t ea = e0 + e;
+          const f4 w = *reinterpret_cast<const f4*>(&sm.pw[wv][t - 1][0]);
+          const float code = (float)int4_value(cbv[u] >> ((ea & 1u) * 4u));
+          const uint32_t c = chv[u] & (D - 1);
+#pragma unroll
+          for (int i = 0; i < G; ++i)
+            atomicAdd(reinterpret_cast<unsigned long long*>(&sm.racc[wv][i][c]), to_fixed(w[i] * code, scale));
+        }
       }
     }
     mc = mn;
