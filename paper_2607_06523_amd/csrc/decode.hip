@@ -178,21 +178,39 @@ __device__ __forceinline__ int64_t tile_start(const Ctx& x, int j) {
   return x.tb + (int64_t)j * Cfg<RB>::TT;
 }
 
-// Key rows (tile row = token, 4 consecutive coefficients per k-step): from the
-// coefficient tiles (key_index) or, for a dense cache (TILED false), rows [T][RB].
+// Key fragments (row = token, 4 coefficients per k-step).  From the coefficient
+// tiles in the key_k order: lane group g reads a 16-byte piece of coefficient
+// group 4 m + g for k-steps 2 m, 2 m + 1 (an odd last k-step: 8-byte halves),
+// so every instruction reads whole tile rows, nontemporal.  For a dense cache
+// (TILED false) rows [T][RB], coefficients KH g + 4 s + i.
 template <int RB, bool TILED>
 __device__ __forceinline__ void load_k(Frags<RB>& f, const Ctx& x, int j, int lane) {
   using C = Cfg<RB>;
+  typedef uint32_t u4n __attribute__((ext_vector_type(4)));
+  typedef uint32_t u2n __attribute__((ext_vector_type(2)));
   const int64_t t0 = tile_start<RB>(x, j);
   const int grp = lane >> 4, col = lane & 15;
 #pragma unroll
   for (int bk = 0; bk < C::NBK; ++bk) {
-    const int64_t row = min(t0 + 16 * bk + col, x.T - 1);
+    if constexpr (TILED) {
+      const int64_t blk = min((t0 >> 4) + bk, x.nblk - 1);
+      const uint16_t* tile = x.ck + blk * 16 * RB + col * 8;
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s) {
-      const int k0 = C::KH * grp + 4 * s;
-      const int64_t e = TILED ? key_index(row, k0, RB) : row * RB + k0;
-      f.k[bk][s] = *reinterpret_cast<const uint2*>(x.ck + e);
+      for (int s = 0; s + 1 < C::NS; s += 2) {
+        const u4n w = __builtin_nontemporal_load(reinterpret_cast<const u4n*>(tile + (2 * s + grp) * 128));
+        f.k[bk][s] = make_uint2(w.x, w.y);
+        f.k[bk][s + 1] = make_uint2(w.z, w.w);
+      }
+      if constexpr (C::NS % 2 == 1) {
+        const u2n w = __builtin_nontemporal_load(
+            reinterpret_cast<const u2n*>(tile + (2 * (C::NS - 1) + (grp >> 1)) * 128 + 4 * (grp & 1)));
+        f.k[bk][C::NS - 1] = make_uint2(w.x, w.y);
+      }
+    } else {
+      const int64_t row = min(t0 + 16 * bk + col, x.T - 1);
+#pragma unroll
+      for (int s = 0; s < C::NS; ++s)
+        f.k[bk][s] = *reinterpret_cast<const uint2*>(x.ck + row * RB + C::KH * grp + 4 * s);
     }
   }
 }
@@ -210,8 +228,14 @@ __device__ __forceinline__ void load_v(Frags<RB>& f, const Ctx& x, int j, int la
 #pragma unroll
     for (int s = 0; s < C::NS; ++s) {
       const int c = col + 16 * s;
-      const int64_t e = TILED ? value_index(16 * blk + 4 * grp, c, RB) : (blk * RB + c) * 16 + 4 * grp;
-      f.v[bk][s] = *reinterpret_cast<const uint2*>(x.cv + e);
+      if constexpr (TILED) {             // 16 channels x 16 bytes of two 8-token blocks: whole lines
+        typedef uint32_t u2n __attribute__((ext_vector_type(2)));
+        const u2n w = __builtin_nontemporal_load(
+            reinterpret_cast<const u2n*>(x.cv + value_index(16 * blk + 4 * grp, c, RB)));
+        f.v[bk][s] = make_uint2(w.x, w.y);
+      } else {
+        f.v[bk][s] = *reinterpret_cast<const uint2*>(x.cv + (blk * RB + c) * 16 + 4 * grp);
+      }
     }
   }
 }
@@ -674,7 +698,7 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
     for (int s = 0; s < NS; ++s) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int k = C::KH * grp + 4 * s + i;
+        const int k = IDENT ? C::KH * grp + 4 * s + i : key_k<NS>(s, grp, i);
         const float v = col < G ? (IDENT ? sm.qs[k][col] : sm.qt[col][k]) * up : 0.f;
         const _Float16 hh = (_Float16)v;
         st.qhi[s][i] = hh;

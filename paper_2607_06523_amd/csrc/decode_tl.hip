@@ -191,13 +191,6 @@ __device__ __forceinline__ void load_k(TFrags<RB, false>& f, const TCtx& x, int 
   }
 }
 
-// Coefficient k held in element i of k-step s by lane group g (the same
-// order on both operands of the score product).
-template <int NS>
-__device__ __forceinline__ int key_k(int s, int g, int i) {
-  return s < NS - (NS & 1) ? 32 * (s >> 1) + 8 * g + 4 * (s & 1) + i : 32 * (NS >> 1) + 4 * g + i;
-}
-
 // Value blocks (8 tokens, value_index): lane c reads channel c's 8 tokens of
 // each block, quads 2 u and 2 u + 1; one instruction reads a whole block.
 // Lanes past r_b read nothing (their products are never used).

@@ -65,6 +65,15 @@ __host__ __device__ __forceinline__ int64_t value_index(int64_t t, int c, int rb
   return ((t >> 3) * rb + c) * 8 + (t & 7);
 }
 
+// Score-product k order over the key tiles: coefficient k held in element i
+// of 16-deep k-step s by lane group g (of NS k-steps), so that a pair of
+// k-steps reads one 16-byte tile row piece per lane and an odd last k-step
+// two 8-byte halves; both operands of the product use it.
+template <int NS>
+__device__ __forceinline__ int key_k(int s, int g, int i) {
+  return s < NS - (NS & 1) ? 32 * (s >> 1) + 8 * g + 4 * (s & 1) + i : 32 * (NS >> 1) + 4 * g + i;
+}
+
 // One split-K pass over a layer: grid = (work items, head slots).
 struct SplitArgs {
   const uint16_t* coef_k;      // slot 0 key tiles (key_index; int8: rows [T][RB]); slot s adds s*T16*RB (int8 s*T*RB)
