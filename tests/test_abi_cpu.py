@@ -340,3 +340,27 @@ def test_hbm_read_rejects_bad_arguments(lib):
     assert lib.dwkv_hbm_read(FAKE, 1024, FAKE, blocks - 1, None) == 4          # sink too small
     assert lib.dwkv_hbm_read(FAKE + 8, 1024, FAKE, blocks, None) == 7          # buffer alignment
     assert lib.dwkv_hbm_read(FAKE, 1024, FAKE + 2, blocks, None) == 7          # sink alignment
+
+
+@pytest.mark.parametrize("lens,hk", [([65536], 8), ([32768], 8), ([131072], 8),
+                                     ([8192 + 917 * i for i in range(16)], 8),     # ragged batch
+                                     ([100, 20000, 3, 45000, 7777], 4), ([1] * 40, 8)])
+def test_split_plan_fits_one_round(lib, lens, hk):
+    """The automatic chunk is a multiple of 256 tokens and, on the token-lane
+    path, the work items of every sequence (each rounded up) times the KV
+    heads fit 256 workgroups whenever a chunk of at most 8192 tokens allows."""
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64).tolist()
+    d, keep = dims(batch=len(lens), n_kv_heads=hk, n_q_heads=4 * hk, basis_rank=48, levels=(0, 4, 8, 16),
+                   cu_seqlens_host=cu, total_tokens=cu[-1], res_stride=1 << 26)
+    split = lib.dwkv_split_tokens(C.byref(d))
+    assert split % 256 == 0 and 256 <= split <= 8192
+    items = sum(-(-n // split) for n in lens)
+    fits_at_max = sum(-(-n // 8192) for n in lens) * hk <= 256
+    if fits_at_max:
+        assert items * hk <= 256, f"split {split}: {items * hk} workgroups"
+        if split > 256:                  # and the next smaller chunk would not fit
+            assert sum(-(-n // (split - 256)) for n in lens) * hk > 256
+    # an explicit split is taken as given
+    d2, keep2 = dims(batch=len(lens), n_kv_heads=hk, n_q_heads=4 * hk, basis_rank=48, levels=(0, 4, 8, 16),
+                     cu_seqlens_host=cu, total_tokens=cu[-1], res_stride=1 << 26, split_tokens=1024)
+    assert lib.dwkv_split_tokens(C.byref(d2)) == 1024
