@@ -317,7 +317,7 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
 // Merge pass: output rows (and Eq. 3 for probed heads); also writes the zero
 // outputs of empty sequences.
 dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, float* out,
-                        const dwkv_probe* probe, void* workspace, hipStream_t s) {
+                        const dwkv_probe* probe, void* workspace, hipStream_t s, float* mstats = nullptr) {
   if (!out || !c || !c->basis) return DWKV_E_NULL;
   if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
   if (!aligned16(out) || !aligned16(c->basis)) return DWKV_E_ALIGN;
@@ -340,6 +340,7 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
     a.n_work = (int32_t)count_work(d, a.split);
     for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
     a.wt = work_table(d, a.split);
+    a.mstats = mstats;
     return hip_status(launch_merge_tl(d->basis_rank, d->n_q_heads / d->n_kv_heads, a, s));
   }
   MergeArgs mg;
@@ -712,7 +713,8 @@ dwkv_status dwkv_dense_decode(const dwkv_dims* d, const void* k, const void* v, 
 size_t dwkv_features_workspace_bytes(const dwkv_dims* d) {
   if (check_dims(d) != DWKV_OK || !uses_token_lane(d)) return 0;
   const size_t sc = align_up((size_t)d->n_q_heads * (size_t)d->total_tokens * sizeof(float), 256);
-  return ws_layout(d, nullptr).total + sc;
+  const size_t ms = align_up((size_t)d->batch * d->n_q_heads * 2 * sizeof(float), 256);
+  return ws_layout(d, nullptr).total + sc + ms;
 }
 
 dwkv_status dwkv_decode_features(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
@@ -729,21 +731,20 @@ dwkv_status dwkv_decode_features(const dwkv_dims* d, const dwkv_cache* c, int32_
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
   float* scores = reinterpret_cast<float*>(ws + ws_layout(d, nullptr).total);
+  float* mstats = reinterpret_cast<float*>(
+      ws + ws_layout(d, nullptr).total + align_up((size_t)d->n_q_heads * (size_t)d->total_tokens * sizeof(float), 256));
   if ((st = partials_phase(d, c, layer, q, q_type, sm_scale, nullptr, workspace, s, scores)) != DWKV_OK) return st;
-  if ((st = merge_phase(d, c, layer, out, nullptr, workspace, s)) != DWKV_OK) return st;
-  const int split = plan_split(d);
+  if ((st = merge_phase(d, c, layer, out, nullptr, workspace, s, mstats)) != DWKV_OK) return st;
   FeatArgs f;
   std::memset(&f, 0, sizeof(f));
-  f.part = reinterpret_cast<const float*>(ws);
+  f.mstats = mstats;
   f.scores = scores;
   f.phi = phi + (int64_t)(layer / d->window) * d->n_kv_heads * d->total_tokens * 4;
   f.cu = d->cu_seqlens;
-  f.wt = work_table(d, split);
   f.T = d->total_tokens;
   f.batch = d->batch;
   f.n_kv_heads = d->n_kv_heads;
-  f.split = split;
-  f.n_work = (int32_t)count_work(d, split);
+  f.n_q_heads = d->n_q_heads;
   return hip_status(launch_features(d->n_q_heads / d->n_kv_heads, f, s));
 }
 

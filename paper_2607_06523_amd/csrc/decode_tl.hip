@@ -734,7 +734,7 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const SplitArgs a
   const int kvh = a.kv_of_slot[slot];
   // every kernel argument the merge needs, loaded in one batch at entry
   asm volatile("" ::"s"(a.part), "s"(a.basis), "s"(a.basis_b_stride), "s"(a.out), "s"(a.n_q_heads), "s"(a.n_work),
-               "s"(a.split), "s"(kvh));
+               "s"(a.split), "s"(kvh), "s"(a.mstats));
   int base, ns;
   seq_work_entry(a.wt, a.cu, a.split, b, base, ns);
   // B^V rows [kg KPG, kg KPG + KPG) of channel c0 + tid % 16
@@ -801,6 +801,11 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const SplitArgs a
     }
     o *= l > 0.f ? 1.0f / l : 0.f;
     *reinterpret_cast<f4*>(&fin[4 * tid]) = o;
+    if (a.mstats && ch == 0 && tid == 0) {   // the merged statistics, for the attention features
+      float* ms = a.mstats + ((int64_t)b * a.n_q_heads + kvh * G + g) * 2;
+      ms[0] = mx;
+      ms[1] = l;
+    }
   }
   __syncthreads();
   {

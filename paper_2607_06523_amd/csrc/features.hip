@@ -7,8 +7,8 @@
 //   phi[t][0] += sum over the KV head's query heads of p
 //   phi[t][1]  = max(phi[t][1], max over those heads of p)
 // One workgroup per 256 packed tokens of one KV head; m* and l* of each
-// sequence come from the split partials (m, l of every chunk), reduced by the
-// whole workgroup.
+// sequence and query head are the merge's own (it merged the split partials
+// just before and stored them).
 #include "internal.h"
 
 namespace dwkv {
@@ -28,7 +28,6 @@ __device__ __forceinline__ int seq_at(const int32_t* cu, int batch, int64_t t) {
 template <int G>
 __global__ __launch_bounds__(kFT) void features_kernel(const FeatArgs a) {
   __shared__ float mstar[G], linv[G];
-  __shared__ float red[kFT / 64][G];
   const int h = blockIdx.y, tid = threadIdx.x;
   const int64_t g0 = (int64_t)blockIdx.x * kFT;
   const int64_t gend = min(g0 + (int64_t)kFT, a.T);
@@ -42,50 +41,10 @@ __global__ __launch_bounds__(kFT) void features_kernel(const FeatArgs a) {
     const int64_t s0 = max(g0, (int64_t)a.cu[b]), s1 = min(gend, (int64_t)a.cu[b + 1]);
     if (s1 <= s0) continue;              // empty sequence (uniform)
     __syncthreads();                     // the previous sequence's statistics are read
-    {                                    // merged softmax statistics of (b, h, g), all threads
-      int base, ns;
-      seq_work(a.wt, a.cu, a.split, b, base, ns);
-      const float* pr = a.part + ((int64_t)h * a.n_work + base) * G * kPartStrideTL;
-      float mg[G], lg[G];
-#pragma unroll
-      for (int g = 0; g < G; ++g) { mg[g] = -INFINITY; lg[g] = 0.f; }
-      for (int i = tid; i < ns; i += kFT)
-#pragma unroll
-        for (int g = 0; g < G; ++g) mg[g] = fmaxf(mg[g], pr[((int64_t)i * G + g) * kPartStrideTL + kPartTLM]);
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        for (int o = 32; o >= 1; o >>= 1) mg[g] = fmaxf(mg[g], __shfl_xor(mg[g], o));
-        if ((tid & 63) == 0) red[tid >> 6][g] = mg[g];
-      }
-      __syncthreads();
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        float m = red[0][g];
-        for (int wv = 1; wv < kFT / 64; ++wv) m = fmaxf(m, red[wv][g]);
-        mg[g] = m;
-      }
-      for (int i = tid; i < ns; i += kFT)
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const float* r = pr + ((int64_t)i * G + g) * kPartStrideTL;
-          lg[g] += exp2f(r[kPartTLM] - mg[g]) * r[kPartTLM + 1];
-        }
-      __syncthreads();                   // red[] is reused for the sums
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        for (int o = 32; o >= 1; o >>= 1) lg[g] += __shfl_xor(lg[g], o);
-        if ((tid & 63) == 0) red[tid >> 6][g] = lg[g];
-      }
-      __syncthreads();
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        if (tid == g) {
-          float l = 0.f;
-          for (int wv = 0; wv < kFT / 64; ++wv) l += red[wv][g];
-          mstar[g] = mg[g];
-          linv[g] = 1.0f / l;
-        }
-      }
+    if (tid < G) {                       // the merge's statistics of (b, h, g)
+      const float* ms = a.mstats + ((int64_t)b * a.n_q_heads + h * G + tid) * 2;
+      mstar[tid] = ms[0];
+      linv[tid] = 1.0f / ms[1];
     }
     __syncthreads();
     if (t >= s0 && t < s1) {

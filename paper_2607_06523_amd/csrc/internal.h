@@ -106,6 +106,7 @@ struct SplitArgs {
   float qscale;                // sm_scale * log2(e)
   int32_t kv_of_slot[DWKV_MAX_PROBE_HEADS];
   WorkTable wt;
+  float* mstats;               // token-lane merge: merged (m*, l*) per [B][Hq] when not null
 };
 
 // Split merge (and Eq. 3 for probed heads): grid = (Hq, B).
@@ -294,13 +295,12 @@ hipError_t launch_stream_read(const void* buf, uint64_t n16, uint32_t* sink, hip
 
 // Attention-mass features of one decode (token-lane partials and stored scores).
 struct FeatArgs {
-  const float* part;           // token-lane partials [Hkv][n_work][G][kPartStrideTL]
+  const float* mstats;         // merged softmax statistics (m*, l*) per [B][Hq], from the merge
   const float* scores;         // [Hkv][T][G] raw scores (exp2 units)
   float* phi;                  // the window's features [Hkv][T][4] (columns 0, 1 updated)
   const int32_t* cu;           // device cu_seqlens
-  WorkTable wt;
   int64_t T;
-  int32_t batch, n_kv_heads, split, n_work;
+  int32_t batch, n_kv_heads, n_q_heads;
 };
 hipError_t launch_features(int g, const FeatArgs& a, hipStream_t s);
 

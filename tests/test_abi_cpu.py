@@ -253,7 +253,7 @@ def test_features_argument_checks(lib):
     d, keep = dims()                          # groups of 4, r_b 32, ranks <= 16: token-lane path
     base = lib.dwkv_workspace_bytes(C.byref(d), None)
     need = lib.dwkv_features_workspace_bytes(C.byref(d))
-    assert need == base + up256(8 * 3000 * 4)
+    assert need == base + up256(8 * 3000 * 4) + up256(2 * 8 * 2 * 4)   # scores, then (m*, l*) per (b, hq)
     d8, keep8 = dims(n_q_heads=16)            # groups of 8: general kernel, no features
     assert lib.dwkv_features_workspace_bytes(C.byref(d8)) == 0
     c = binding.Cache(*([FAKE] * 8))
