@@ -5,7 +5,12 @@ calls on one stream (the whole hot path: query projection, coefficient and
 residual streaming, softmax, value product, split merge).  Inputs are synthetic
 and already resident in HBM when the timed region starts.
 
-Prints ONE JSON line on stdout; progress goes to stderr.
+Prints ONE JSON line on stdout; progress goes to stderr.  Beside the metric
+it carries `roofline` (the split-K kernel's achieved bandwidth against the
+published peak and against the device's measured read ceiling, with counter
+traffic from the committed profile), `hbm_read_ceiling`, `cpu_baseline` (the
+float64 oracle on the host cores) and, unless skipped, the int8-coefficient,
+features, probe, append, comparison and control-loop measurements.
 """
 from __future__ import annotations
 
