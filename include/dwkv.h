@@ -249,9 +249,11 @@ dwkv_status dwkv_route_budget(const dwkv_dims* dims, const float* phi, const flo
  *   res_scale = fp16(g * S) (0 for a rank-0 token); entries stored at
  *           [res_off[t], res_off[t+1]) ordered by descending |code|, then
  *           ascending channel.
- * Arithmetic: float32, every product and sum rounded on its own, sums left to
- * right over the contracted index; the integer results are therefore exact
- * functions of the inputs.
+ * Arithmetic: float32, every product and sum rounded on its own; each sum runs
+ * left to right over its contracted index (j = 0..d-1 for A_i, i = 0..r_b-1
+ * for the basis term), starting from its first product; A is rounded to fp16
+ * before the residual; S and r_c / S are correctly rounded divisions.  The
+ * integer results are therefore exact functions of the inputs.
  *   x_k, x_v: fp16 [t1-t0][Hkv][d] dense keys / values of the tokens
  *             (keys post positional encoding, as the decode expects)
  *   gate:     NULL (g = 1) or fp32 [2][Hkv][t1-t0], g in [0, 1]

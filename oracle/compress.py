@@ -26,17 +26,15 @@ Readings where the paper is silent (each listed in the design notes):
   order the layout validator checks).
 
 Precision.  The kept channels and the codes are integers decided by floating
-point, so this module takes those decisions in the float32 arithmetic the GPU
-path uses, in a fixed order that both follow: every product and every sum is
-rounded to float32 on its own (no fused multiply-add); a sum over the
-contracted index (the d channels for A, the r_b basis rows for the basis term
-of r) is split into four contiguous quarters, each summed left to right from
-its first product, and the quarters are combined as (q0 + q1) + (q2 + q3); A
-is rounded to fp16 (round-half-even) before the residual, and r_c = x_c - p_c
-with p_c the basis term of channel c.  S = |r|_max / 7 and r_c / S are
-correctly rounded float32 divisions.  Every fp16 conversion rounds half to
-even.  (The paper fixes no order; four independent partial sums let the GPU
-overlap their latencies.)
+point, and the paper fixes no arithmetic for them.  Reading used here: single
+precision written out in the plainest order, the one a scalar loop takes.
+Every product and every sum is rounded to float32 on its own (no fused
+multiply-add).  A sum over the contracted index (the d channels for A, the
+r_b basis rows for the basis term of r) runs left to right, starting from its
+first product.  A is rounded to fp16 (round-half-even) before the residual,
+and r_c = x_c - p_c with p_c the basis term of channel c.  S = |r|_max / 7 and
+r_c / S are correctly rounded float32 divisions.  Every fp16 conversion
+rounds half to even.
 """
 from __future__ import annotations
 
@@ -46,46 +44,33 @@ from .factorized import window_of
 
 
 # ------------------------------------------------------------ one vector
-def quarters(n: int):
-    """The four contiguous chunks [floor(q n/4), floor((q+1) n/4)) of a length-n sum."""
-    b = [q * n // 4 for q in range(5)]
-    return [(b[q], b[q + 1]) for q in range(4)]
-
-
-def _sum_quarters(terms):
-    """A sum of float32 terms (a list, summed along the list) in the fixed
-    order: each quarter left to right from its first term, then
-    (q0 + q1) + (q2 + q3).  An empty quarter is +0."""
-    part = []
-    for a, b in quarters(len(terms)):
-        if b == a:
-            part.append(np.zeros_like(terms[0]))
-            continue
-        acc = terms[a]
-        for j in range(a + 1, b):
-            acc = acc + terms[j]
-        part.append(acc)
-    return (part[0] + part[1]) + (part[2] + part[3])
+def _sum_in_order(terms):
+    """A sum of float32 terms (a list, summed along the list) left to right:
+    the first term, then each next term added with one rounding."""
+    acc = terms[0]
+    for t in terms[1:]:
+        acc = acc + t
+    return acc
 
 
 def project(x: np.ndarray, B: np.ndarray) -> np.ndarray:
     """Coefficient rows A = x B^T for vectors x [n, d] against basis rows
-    B [r_b, d] (fp16 values), float32 products summed over the d channels in
-    the quarter order, rounded to fp16.  Returns float16 [n, r_b]."""
+    B [r_b, d] (fp16 values): float32 products summed over the d channels left
+    to right, rounded to fp16.  Returns float16 [n, r_b]."""
     x = np.asarray(x, dtype=np.float16).astype(np.float32)
     B = np.asarray(B, dtype=np.float16).astype(np.float32)
     terms = [x[:, j:j + 1] * B[None, :, j] for j in range(x.shape[1])]
-    return _sum_quarters(terms).astype(np.float16)
+    return _sum_in_order(terms).astype(np.float16)
 
 
 def residual(x: np.ndarray, B: np.ndarray, a16: np.ndarray) -> np.ndarray:
     """r = x - A B in float32: the basis term of each channel summed over the
-    basis rows in the quarter order, then subtracted from x.  Returns float32 [n, d]."""
+    basis rows left to right, then subtracted from x.  Returns float32 [n, d]."""
     x = np.asarray(x, dtype=np.float16).astype(np.float32)
     B = np.asarray(B, dtype=np.float16).astype(np.float32)
     a = np.asarray(a16, dtype=np.float16).astype(np.float32)
     terms = [a[:, i:i + 1] * B[None, i, :] for i in range(B.shape[0])]
-    return x - _sum_quarters(terms)
+    return x - _sum_in_order(terms)
 
 
 def select_channels(r: np.ndarray, rho: int) -> np.ndarray:

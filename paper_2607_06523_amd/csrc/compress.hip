@@ -7,13 +7,12 @@
 // token at a time:
 //   A_i   = fp16( sum_j x_j B_ij )                    lane i
 //   r_c   = x_c - sum_i A_i B_ic                      lanes own channels 2l, 2l+1
-//   (each sum in four contiguous quarters of its index, each left to right,
-//   combined as (q0 + q1) + (q2 + q3): four independent chains per lane)
+//   (each sum left to right over its index, one chain per lane and sum)
 //   kept  = rho largest |r_c|, ties to the lower channel (threshold search on
 //           64-bit keys, one ballot pair per key bit)
 //   S     = max |r| / 7,  code = rne(r_c / S) in [-7, 7],  scale = fp16(g S)
 //   entries in storage order (|code| descending, then channel) via ballots.
-// Every sum is rounded to float32 term by term in that fixed order; products of
+// Every sum is rounded to float32 term by term, left to right; products of
 // two fp16 values are exact in float32, so they are accumulated with fused
 // multiply-adds (the same numbers as separately rounded products and sums) and
 // nothing else is contracted, so the integer results are exact functions of
@@ -118,31 +117,25 @@ __device__ __forceinline__ void compress_token(const CompressArgs& a, const Slab
   *reinterpret_cast<float2*>(&sm.xs[wv][2 * lane]) = make_float2(x0, x1);
   wave_lds_sync();
 
-  // ---- coefficients: lane i sums x_j B_ij over the four channel quarters
-  // (32 channels each, left to right) as four independent chains
-  constexpr int QD = D / 4;
+  // ---- coefficients: lane i sums x_j B_ij over the channels, left to right
   for (int i = lane; i < rb; i += 64) {
     const uint16_t* row = sm.bas + i * kBRow;
-    float s[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
-    for (int j0 = 0; j0 < QD; j0 += 8) {
+    float s = -0.0f;
+#pragma unroll 4
+    for (int j0 = 0; j0 < D; j0 += 8) {
+      const uint4 bw = *reinterpret_cast<const uint4*>(row + j0);
+      const float4 xa = *reinterpret_cast<const float4*>(&sm.xs[wv][j0]);
+      const float4 xb = *reinterpret_cast<const float4*>(&sm.xs[wv][j0 + 4]);
+      const float xv8[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+      const uint32_t bw4[4] = {bw.x, bw.y, bw.z, bw.w};
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint4 bw = *reinterpret_cast<const uint4*>(row + q * QD + j0);
-        const float4 xa = *reinterpret_cast<const float4*>(&sm.xs[wv][q * QD + j0]);
-        const float4 xb = *reinterpret_cast<const float4*>(&sm.xs[wv][q * QD + j0 + 4]);
-        const float xv8[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
-        const uint32_t bw4[4] = {bw.x, bw.y, bw.z, bw.w};
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const uint32_t w = bw4[j >> 1];
-          const uint16_t bij = (uint16_t)((j & 1) ? (w >> 16) : (w & 0xffffu));
-          s[q] = fma_exact(xv8[j], bij, (j0 == 0 && j == 0) ? -0.0f : s[q]);
-        }
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t w = bw4[j >> 1];
+        const uint16_t bij = (uint16_t)((j & 1) ? (w >> 16) : (w & 0xffffu));
+        s = fma_exact(xv8[j], bij, s);
       }
     }
-    const float acc = (s[0] + s[1]) + (s[2] + s[3]);
-    const uint16_t ab = float_to_half_bits(acc);
+    const uint16_t ab = float_to_half_bits(s);
     sm.as[wv][i] = half_bits_to_float(ab);
     if (z == 0)
       sl.coef[key_index(t, i, rb)] = ab;
@@ -152,25 +145,19 @@ __device__ __forceinline__ void compress_token(const CompressArgs& a, const Slab
   wave_lds_sync();
 
   // ---- residual of channels c0 = 2 lane, c1 = 2 lane + 1: the basis term
-  // summed over the four quarters of the basis rows (rb/4 rows each, in order)
-  const int qr = rb >> 2;                // a multiple of 4
-  float u0[4] = {0.f, 0.f, 0.f, 0.f}, u1[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int i0 = 0; i0 < qr; i0 += 4) {
+  // summed over the basis rows, left to right
+  float p0 = -0.0f, p1 = -0.0f;
+#pragma unroll 2
+  for (int i0 = 0; i0 < rb; i0 += 4) {
+    const float4 a4 = *reinterpret_cast<const float4*>(&sm.as[wv][i0]);
+    const float av[4] = {a4.x, a4.y, a4.z, a4.w};
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float4 a4 = *reinterpret_cast<const float4*>(&sm.as[wv][q * qr + i0]);
-      const float av[4] = {a4.x, a4.y, a4.z, a4.w};
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const uint32_t bw = *reinterpret_cast<const uint32_t*>(sm.bas + (q * qr + i0 + v) * kBRow + 2 * lane);
-        const bool first = i0 == 0 && v == 0;
-        u0[q] = fma_exact(av[v], (uint16_t)(bw & 0xffffu), first ? -0.0f : u0[q]);
-        u1[q] = fma_exact(av[v], (uint16_t)(bw >> 16), first ? -0.0f : u1[q]);
-      }
+    for (int v = 0; v < 4; ++v) {
+      const uint32_t bw = *reinterpret_cast<const uint32_t*>(sm.bas + (i0 + v) * kBRow + 2 * lane);
+      p0 = fma_exact(av[v], (uint16_t)(bw & 0xffffu), p0);
+      p1 = fma_exact(av[v], (uint16_t)(bw >> 16), p1);
     }
   }
-  const float p0 = (u0[0] + u0[1]) + (u0[2] + u0[3]);
-  const float p1 = (u1[0] + u1[1]) + (u1[2] + u1[3]);
   const float r0 = x0 - p0, r1 = x1 - p1;
 
   // ---- routed rank of the token (shared by the window's layers and K/V)

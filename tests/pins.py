@@ -25,8 +25,10 @@ says what disagreed.  The pins are:
   running loop;
 * the router's attention features: per-sequence masses summing to G, spike
   below mass below G spike, uniform and ln-3 closed forms, the table fold;
-* threshold control: a hand-worked feedback trace with clamps, and the
-  budget-driven selection against enumeration of the promoted sets;
+* threshold control: a hand-worked feedback trace with clamps, the
+  budget-driven selection against enumeration of the promoted sets, and
+  budget routing of a token range against a running loop (exact scores,
+  planted ties, offsets continued from a non-zero start);
 * sketch basis: Gram-Schmidt against numpy's QR, the exact row space of a
   rank-r_b prefill, zero rows of a rank-deficient sketch;
 * 8-bit blockwise coefficients: a scalar loop over code * block scale, and an
@@ -740,28 +742,21 @@ def pin_compress_rne_table(o):
     return None
 
 
-def _exact_quarter_sum(terms):
-    """Exact-arithmetic model of the fixed float32 order: four contiguous
-    chunks [floor(q n/4), floor((q+1) n/4)), each summed left to right with
-    every addition rounded to float32, then (q0 + q1) + (q2 + q3)."""
-    n = len(terms)
-    b = [q * n // 4 for q in range(5)]
-    part = []
-    for q in range(4):
-        chunk = terms[b[q]:b[q + 1]]
-        acc = chunk[0] if chunk else Fraction(0)
-        for t in chunk[1:]:
-            acc = fp32_round(acc + t)
-        part.append(acc)
-    return fp32_round(fp32_round(part[0] + part[1]) + fp32_round(part[2] + part[3]))
+def _exact_ordered_sum(terms):
+    """Exact-arithmetic model of a float32 sum left to right: the first term,
+    then every next term added with one rounding to float32."""
+    acc = terms[0] if terms else Fraction(0)
+    for t in terms[1:]:
+        acc = fp32_round(acc + t)
+    return acc
 
 
 def _exact_project(x, B):
-    """A_i = fp16 of the fixed-order float32 sum of the rounded products x_j B_ij."""
+    """A_i = fp16 of the left-to-right float32 sum of the rounded products x_j B_ij."""
     out = []
     for i in range(B.shape[0]):
         terms = [fp32_round(Fraction(float(x[j])) * Fraction(float(B[i, j]))) for j in range(len(x))]
-        out.append(fp16_round(_exact_quarter_sum(terms)))
+        out.append(fp16_round(_exact_ordered_sum(terms)))
     return out
 
 
@@ -769,7 +764,7 @@ def _exact_residual(x, B, a):
     out = []
     for c in range(len(x)):
         terms = [fp32_round(a[i] * Fraction(float(B[i, c]))) for i in range(B.shape[0])]
-        out.append(fp32_round(Fraction(float(x[c])) - _exact_quarter_sum(terms)))
+        out.append(fp32_round(Fraction(float(x[c])) - _exact_ordered_sum(terms)))
     return out
 
 
@@ -789,10 +784,10 @@ def pin_compress_arithmetic(o):
     for k in range(4):
         ea = _exact_project(x[k], B)
         if [Fraction(float(v)) for v in a16[k]] != ea:
-            return f"projection is not the per-op rounded fixed-order float32 sum (vector {k})"
+            return f"projection is not the per-op rounded left-to-right float32 sum (vector {k})"
         er = _exact_residual(x[k], B, ea)
         if [Fraction(float(v)) for v in r[k]] != er:
-            return f"residual is not x - (fixed-order float32 basis term) (vector {k})"
+            return f"residual is not x - (left-to-right float32 basis term) (vector {k})"
         for rho in (2, 8):
             S = fp32_round(max(abs(v) for v in er) / 7)
             want = _expected_entries(er, rho, S)
@@ -814,9 +809,9 @@ def pin_compress_arithmetic(o):
     for k in range(3):
         ea = _exact_project(x2[k], B2)
         if [Fraction(float(v)) for v in a2[k]] != ea:
-            return f"projection of cancelling terms is not the fixed-order float32 sum (vector {k})"
+            return f"projection of cancelling terms is not the left-to-right float32 sum (vector {k})"
         if [Fraction(float(v)) for v in r2[k]] != _exact_residual(x2[k], B2, ea):
-            return f"residual of cancelling terms is not the fixed-order float32 sum (vector {k})"
+            return f"residual of cancelling terms is not the left-to-right float32 sum (vector {k})"
     # enumeration: on 6 channels with repeated magnitudes, the kept set is the
     # lexicographically first subset (by channel) among those with the largest
     # sorted |r| profile
@@ -1044,6 +1039,69 @@ def pin_control(o):
     return None
 
 
+def pin_route_budget(o):
+    """Budget routing of a token range against a running loop written here:
+    router scores in exact rational arithmetic rounded per operation, the n
+    tokens of largest score promoted (ties to the lower token, n from the
+    budget and clamped to [0, N]), codes as level indices 0 / 1, and offsets
+    continued from a non-zero off[t0] by the routed levels.  Budgets run from
+    infeasible to generous; the promotion boundary falls inside a group of
+    exactly tied scores; rho_min is positive in one level pair; codes and
+    offsets outside the range stay untouched."""
+    OC = o.control
+    w = small_workload(levels=(0, 16), probs=(0.5, 0.5))
+    M, Hk, T = 2, 2, 120
+    phi, u, _ = router_inputs(w, n_windows=M, T=T)
+    t0, t1 = 30, 100
+    N = t1 - t0
+    # a tie group: tokens 50..59 share one feature row, so their scores tie
+    # exactly; budgets below put the promotion boundary inside it
+    for m in range(M):
+        for h in range(Hk):
+            phi[m, h, 50:60] = phi[m, h, 41]
+    for lo, hi in ((0, 16), (2, 8)):
+        lev = (lo, hi)
+        for which in range(5):
+            entries = np.zeros((M, Hk), np.int64)
+            for m in range(M):
+                for h in range(Hk):
+                    zs = [exact_score(u[m], phi[m, h, t]) for t in range(t0, t1)]
+                    order = sorted(range(N), key=lambda k: (-zs[k], k))
+                    tie = [k for k in order if zs[k] == zs[50 - t0]]
+                    cut = order.index(tie[len(tie) // 2])       # a boundary inside the tie group
+                    n_want = (0, cut, N, N // 3, N)[which]
+                    extra = (-(N * lo) - 5 if lo else -3, 0, 7, hi - lo - 1, 10 * N * hi)[which]
+                    entries[m, h] = N * lo + n_want * (hi - lo) + extra
+            codes = np.full((M, Hk, T), 9, np.uint8)
+            off = np.full((M, Hk, T + 1), 7, np.uint32)
+            off[:, :, t0] = 1234
+            OC.route_budget(phi, u, entries, lev, t0, t1, codes, off)
+            for m in range(M):
+                for h in range(Hk):
+                    zs = [exact_score(u[m], phi[m, h, t]) for t in range(t0, t1)]
+                    E = int(entries[m, h])
+                    n = max(0, min(N, (E - N * lo) // (hi - lo)))
+                    order = sorted(range(N), key=lambda k: (-zs[k], k))
+                    promoted = set(order[:n])
+                    run = 1234
+                    for k in range(N):
+                        t = t0 + k
+                        want = 1 if k in promoted else 0
+                        if int(codes[m, h, t]) != want:
+                            return (f"levels {lev}, budget {E}: code of token {t} (m={m}, h={h}) is "
+                                    f"{int(codes[m, h, t])}, the loop gives {want}")
+                        if int(off[m, h, t]) != run:
+                            return f"levels {lev}, budget {E}: offset of token {t} is {int(off[m, h, t])}, want {run}"
+                        run += lev[want]
+                    if int(off[m, h, t1]) != run:
+                        return f"levels {lev}, budget {E}: final offset {int(off[m, h, t1])}, want {run}"
+                    if np.any(codes[m, h, :t0] != 9) or np.any(codes[m, h, t1:] != 9):
+                        return "budget routing wrote codes outside the range"
+                    if np.any(off[m, h, :t0] != 7) or np.any(off[m, h, t1 + 1:] != 7):
+                        return "budget routing wrote offsets outside the range"
+    return None
+
+
 def pin_sketch(o):
     """Sketch basis: Gram-Schmidt rows against numpy's QR (same signs after
     fixing R's diagonal positive), orthonormality, the exact row space of a
@@ -1117,7 +1175,7 @@ def pin_int8_coefficients(o):
 ALL_PINS = [pin_query_formats, pin_nibbles, pin_residual_map, pin_brute_force, pin_closed_forms,
             pin_reductions, pin_invariants, pin_probe, pin_router, pin_compress_closed_forms,
             pin_compress_rne_table, pin_compress_arithmetic, pin_compress_bounds,
-            pin_compress_into_cache, pin_route_range, pin_attention_features, pin_control, pin_sketch,
+            pin_compress_into_cache, pin_route_range, pin_attention_features, pin_control, pin_route_budget, pin_sketch,
             pin_int8_coefficients]
 
 

@@ -114,23 +114,30 @@ def _project_reversed(x, B):
     return acc.astype(np.float16)
 
 
-def _project_left_to_right(x, B):
+def _blocked_sum(terms):
+    """Four contiguous quarters, each left to right, combined (q0 + q1) + (q2 + q3)."""
+    n = len(terms)
+    b = [q * n // 4 for q in range(5)]
+    part = []
+    for q in range(4):
+        acc = terms[b[q]]
+        for j in range(b[q] + 1, b[q + 1]):
+            acc = acc + terms[j]
+        part.append(acc)
+    return (part[0] + part[1]) + (part[2] + part[3])
+
+
+def _project_quarters(x, B):
     x = np.asarray(x, dtype=np.float16).astype(np.float32)
     B = np.asarray(B, dtype=np.float16).astype(np.float32)
-    acc = x[:, 0:1] * B[None, :, 0]
-    for j in range(1, x.shape[1]):
-        acc = acc + x[:, j:j + 1] * B[None, :, j]
-    return acc.astype(np.float16)
+    return _blocked_sum([x[:, j:j + 1] * B[None, :, j] for j in range(x.shape[1])]).astype(np.float16)
 
 
-def _residual_left_to_right(x, B, a16):
+def _residual_quarters(x, B, a16):
     xx = np.asarray(x, dtype=np.float16).astype(np.float32)
     BB = np.asarray(B, dtype=np.float16).astype(np.float32)
     a = np.asarray(a16, dtype=np.float16).astype(np.float32)
-    p = a[:, 0:1] * BB[None, 0, :]
-    for i in range(1, BB.shape[0]):
-        p = p + a[:, i:i + 1] * BB[None, i, :]
-    return xx - p
+    return xx - _blocked_sum([a[:, i:i + 1] * BB[None, i, :] for i in range(BB.shape[0])])
 
 
 def _project_f64(x, B):
@@ -263,6 +270,17 @@ def _budget_ceil(z, entries, rho_min, rho_max):
     return codes
 
 
+def _budget_offsets_from_zero(phi, u, entries, levels, t0, t1, codes, off):
+    off[:, :, t0] = 0
+    return CT.__dict__["_orig_route_budget"](phi, u, entries, levels, t0, t1, codes, off)
+
+
+def _budget_code_as_level(phi, u, entries, levels, t0, t1, codes, off):
+    CT.__dict__["_orig_route_budget"](phi, u, entries, levels, t0, t1, codes, off)
+    codes[:, :, t0:t1] = np.asarray(levels, np.uint8)[codes[:, :, t0:t1]]
+    return codes, off
+
+
 def _gs_no_normalize(Y):
     Y = np.array(Y, dtype=np.float64)
     Q = np.zeros_like(Y)
@@ -331,8 +349,8 @@ MUTANTS = {
         cache.coef_v[layer, h].reshape(-1, cache.coef_v.shape[3])[t0:t1].astype(np.float64))],
     "projection summed right to left": [(CP, "project", _project_reversed)],
     "projection in float64": [(CP, "project", _project_f64)],
-    "projection summed left to right without quarters": [(CP, "project", _project_left_to_right)],
-    "basis term summed left to right without quarters": [(CP, "residual", _residual_left_to_right)],
+    "projection summed in four blocked quarters": [(CP, "project", _project_quarters)],
+    "basis term summed in four blocked quarters": [(CP, "residual", _residual_quarters)],
     "residual from the unrounded coefficients": [(CP, "residual", _residual_unrounded_a)],
     "residual basis term summed right to left": [(CP, "residual", _residual_reversed)],
     "residual sign flipped in compress": [(CP, "residual", lambda x, B, a16:
@@ -356,6 +374,8 @@ MUTANTS = {
     "step up one interval late": [(CT, "controller_update", _ctl_variant("patience_late"))],
     "budget ties go to the higher token": [(CT, "budget_select", _budget_ties_up)],
     "budget count rounded up": [(CT, "budget_select", _budget_ceil)],
+    "budget routing restarts the offsets at zero": [(CT, "route_budget", _budget_offsets_from_zero)],
+    "budget routing writes the level as the code": [(CT, "route_budget", _budget_code_as_level)],
     "Gram-Schmidt rows scaled by max instead of norm": [(SK, "orthonormal_rows", _gs_no_normalize)],
     "sketch with the token order reversed": [(SK, "sketch", _sketch_transposed)],
     "int8 block scale indexed by i mod blocks": [(F, "coefficient_rows", _coef_rows_variant("block_mod"))],
@@ -371,6 +391,7 @@ def test_mutant_is_caught(name, monkeypatch):
     R.__dict__.setdefault("_orig_route", R.route)
     R.__dict__.setdefault("_orig_route_range", R.route_range)
     CP.__dict__.setdefault("_orig_residual", CP.residual)
+    CT.__dict__.setdefault("_orig_route_budget", CT.route_budget)
     for mod, attr, fn in MUTANTS[name]:
         monkeypatch.setattr(mod, attr, fn)
         if hasattr(oracle, attr):
