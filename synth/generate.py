@@ -14,6 +14,13 @@ generation.  The draws follow the workload's stated distributions:
 * residual entries: the routed number of distinct channels drawn uniformly,
   int4 codes uniform on [-7, 7], stored largest |code| first, then by channel;
 * per-token residual scale (gate folded in, gate = 1): U(0.01, 0.1) in fp16;
+  or, in the "wide" scale mode, scales spanning fp16's range: within every
+  run of `scale_period` tokens of a sequence the binary exponent ramps up
+  from the subnormals (2^-24) to 2^15 for values and to 2^1 for keys, times
+  U(1, 2), with 4% of the scales zero and the last token of every run at the
+  ramp's top (so that the largest scale of a chunk comes late);
+* int8 block scales in the "wide" coefficient-scale mode: 2^U(-12, 7) for
+  values and 2^U(-5, -2) for keys (several binades within one token);
 * queries: N(0,1)/sqrt(d) rounded to the workload's query dtype.
 
 Packing variable-length residual entries needs the running position of each
@@ -43,6 +50,20 @@ RES_ALIGN = 256         # res_stride is a multiple of this
 
 def rng_for(*key) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64DXSM(np.random.SeedSequence(list(key))))
+
+
+def _residual_scales(w: Workload, g: np.random.Generator, z: int, n: int) -> np.ndarray:
+    """fp16 residual scales of one sequence's n tokens of a (layer, Z, head) slab."""
+    if getattr(w, "scale_mode", "uniform") != "wide":
+        return g.uniform(0.01, 0.1, size=n).astype(np.float16)
+    P = max(int(w.scale_period), 2)
+    top = 15.0 if z == 1 else 1.0
+    pos = np.arange(n) % P
+    e = np.floor(-24.0 + (top + 24.0) * pos / (P - 1))
+    s = np.exp2(e) * g.uniform(1.0, 2.0, size=n)
+    s[pos == P - 1] = np.exp2(top) * 1.99
+    s[g.random(n) < 0.04] = 0.0
+    return np.minimum(s, 65504.0).astype(np.float16)
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -252,7 +273,12 @@ def generate(w: Workload, layers: tuple | None = None, threads: int | None = Non
                 continue
             if c8:
                 rows = (rng_for(w.seed, _COEF8, b, l, z, h).binomial(254, 0.5, size=(n, rb)) - 127).astype(np.int8)
-                sc = rng_for(w.seed, _COEF8_SCALE, b, l, z, h).uniform(0.11, 0.14, size=(rb // 16, n))
+                gs = rng_for(w.seed, _COEF8_SCALE, b, l, z, h)
+                if getattr(w, "coef_scale_mode", "narrow") == "wide":
+                    lo, hi = (-12.0, 7.0) if z == 1 else (-5.0, -2.0)
+                    sc = np.exp2(gs.uniform(lo, hi, size=(rb // 16, n)))
+                else:
+                    sc = gs.uniform(0.11, 0.14, size=(rb // 16, n))
                 (cs_k if z == 0 else cs_v)[li, h, :, t0:t1] = sc.astype(np.float16)
             else:
                 g = rng_for(w.seed, _COEF, b, l, z, h)
@@ -262,8 +288,7 @@ def generate(w: Workload, layers: tuple | None = None, threads: int | None = Non
             else:   # scatter into the token-fastest blocks
                 tt = np.arange(t0, t1)
                 coef_v[li, h, tt // BLOCK, :, tt % BLOCK] = rows
-            s = rng_for(w.seed, _RES_SCALE, b, l, z, h).uniform(0.01, 0.1, size=n)
-            res_scale[li, z, h, t0:t1] = s.astype(np.float16)
+            res_scale[li, z, h, t0:t1] = _residual_scales(w, rng_for(w.seed, _RES_SCALE, b, l, z, h), z, n)
         # entries of every sequence, packed in token order
         all_ch, all_k = [], []
         for b in range(B):

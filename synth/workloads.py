@@ -35,6 +35,9 @@ class Workload:
     salient_level: int = 0           # level index forced inside spans
     probe: bool = False              # attention-output probe on every layer
     coef_format: str = "f16"         # "f16" coefficient rows, or "int8" (8-bit blockwise)
+    scale_mode: str = "uniform"      # residual scales: "uniform" U(0.01, 0.1), or "wide" (see generate)
+    scale_period: int = 1024         # "wide": tokens per ramp of the scale exponent
+    coef_scale_mode: str = "narrow"  # int8 block scales: "narrow" U(0.11, 0.14), or "wide"
     description: str = field(default="", compare=False)
 
     @property
