@@ -20,6 +20,8 @@
  *  - All buffers are owned by the caller; the library allocates nothing and
  *    keeps no global mutable state, so calls on different streams do not
  *    interfere (calls sharing one workspace must be ordered by the caller).
+ *    The one exception is dwkv_decode_noalloc, whose static scratch array is
+ *    shared by its calls on one GPU.
  *  - Argument errors are detected on the host before anything is enqueued and
  *    returned synchronously; DWKV_E_HIP reports a failed HIP call or launch.
  *  - Kernels run asynchronously on `stream` (a hipStream_t; NULL = the null
@@ -54,7 +56,9 @@ typedef enum dwkv_status {
   DWKV_E_WORKSPACE = 4,   /* workspace smaller than the *_workspace_bytes value    */
   DWKV_E_LAYOUT = 5,      /* dwkv_validate found a malformed cache                 */
   DWKV_E_HIP = 6,         /* a HIP runtime call or kernel launch failed            */
-  DWKV_E_ALIGN = 7        /* a decode device pointer is not 16-byte aligned         */
+  DWKV_E_ALIGN = 7,       /* a decode device pointer is not 16-byte aligned         */
+  DWKV_E_SCRATCH = 8      /* dwkv_decode_noalloc: the call needs more scratch than
+                             dwkv_static_scratch_bytes()                           */
 } dwkv_status;
 
 typedef enum dwkv_qtype { DWKV_F16 = 0, DWKV_BF16 = 1 } dwkv_qtype;
@@ -180,6 +184,29 @@ dwkv_status dwkv_decode_partials(const dwkv_dims* dims, const dwkv_cache* cache,
 dwkv_status dwkv_decode_merge(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
                               float* out, const dwkv_probe* probe, void* workspace,
                               size_t ws_bytes, void* stream);
+
+/* For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): dwkv_decode with the same
+ * arguments and results, minus the workspace.  Its split partials live in a
+ * library-owned static device array of dwkv_static_scratch_bytes() bytes
+ * (DWKV_STATIC_SCRATCH_BYTES, 16 MiB), one copy per GPU the library runs on,
+ * held until the process ends; its address on a device is looked up (without
+ * allocating) on the first call made with that device current.  The call
+ * itself allocates nothing and calls no allocating routine; the caller still
+ * passes q, out and the cache.  It returns DWKV_E_SCRATCH, enqueuing nothing,
+ * when the dims (and probe) need more than the array holds, i.e. when
+ * dwkv_workspace_bytes(dims, probe) > dwkv_static_scratch_bytes().  Every call
+ * on one GPU shares that GPU's array and leaves its partials there: calls that
+ * overlap on one GPU (different streams, or threads without ordering) race and
+ * must be serialised by the caller.  The decode needs no initial contents in
+ * the array, so nothing is cleared between calls.  This is the one piece of
+ * global state in the library (the per-device address table is guarded by a
+ * mutex). */
+#define DWKV_STATIC_SCRATCH_BYTES (16u << 20)
+size_t dwkv_static_scratch_bytes(void);
+dwkv_status dwkv_decode_noalloc(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
+                                const void* q, int32_t q_type, float sm_scale, float* out,
+                                const dwkv_probe* probe, void* stream);
 
 /* Bytes of device workspace dwkv_route needs (0 when dims are invalid). */
 size_t dwkv_route_workspace_bytes(const dwkv_dims* dims);

@@ -203,6 +203,22 @@ class DeviceCache:
         binding.check(st, "dwkv_decode")
         return out if probe is None else (out, err, out_ref)
 
+    def decode_noalloc(self, layer: int, q=None, sm_scale: float | None = None, out=None):
+        """dwkv_decode_noalloc: decode with the library's static scratch (no
+        workspace); out [B,Hq,d] fp32 must be given or is allocated here by torch."""
+        torch = self.torch
+        if q is None:
+            q = self.q[layer]
+        if q.dtype not in (torch.float16, torch.bfloat16):
+            raise TypeError("q must be float16 or bfloat16")
+        qt = F16 if q.dtype == torch.float16 else BF16
+        if out is None:
+            out = torch.empty((self.batch, self.n_q_heads, self.head_dim), dtype=torch.float32, device=self.device)
+        st = self.lib.dwkv_decode_noalloc(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(q), qt,
+                                          float(sm_scale or 0.0), _ptr(out), None, _stream(torch, self.device))
+        binding.check(st, "dwkv_decode_noalloc")
+        return out
+
     def decode_partials(self, layer: int, q=None, sm_scale: float | None = None, workspace=None):
         """First half of decode: the split-K pass (no probe); dwkv_decode_merge finishes it."""
         torch = self.torch

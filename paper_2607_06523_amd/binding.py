@@ -20,7 +20,8 @@ F16, BF16 = 0, 1
 COEF_F16, COEF_I8 = 0, 1
 
 STATUS = {0: "ok", 1: "null pointer", 2: "inconsistent dimensions", 3: "unsupported shape",
-          4: "workspace too small", 5: "malformed cache layout", 6: "HIP runtime error"}
+          4: "workspace too small", 5: "malformed cache layout", 6: "HIP runtime error",
+          7: "device pointer not 16-byte aligned", 8: "needs more than the static scratch"}
 
 
 class DwkvError(RuntimeError):
@@ -58,7 +59,8 @@ class Probe(C.Structure):
 
 
 EXPORTS = ["dwkv_abi_version", "dwkv_status_str", "dwkv_split_tokens", "dwkv_workspace_bytes",
-           "dwkv_decode_launches", "dwkv_decode", "dwkv_decode_partials", "dwkv_decode_merge", "dwkv_route_workspace_bytes", "dwkv_route",
+           "dwkv_decode_launches", "dwkv_decode", "dwkv_decode_partials", "dwkv_decode_merge",
+           "dwkv_static_scratch_bytes", "dwkv_decode_noalloc", "dwkv_route_workspace_bytes", "dwkv_route",
            "dwkv_route_range", "dwkv_route_budget_workspace_bytes", "dwkv_route_budget", "dwkv_compress", "dwkv_features_workspace_bytes", "dwkv_decode_features",
            "dwkv_controller_update", "dwkv_sketch_workspace_bytes", "dwkv_sketch_basis", "dwkv_materialize", "dwkv_dense_workspace_bytes",
            "dwkv_dense_decode", "dwkv_residual_map",
@@ -94,6 +96,11 @@ def load(path: str = LIB_PATH):
     lib.dwkv_decode_merge.restype = C.c_int
     lib.dwkv_decode_merge.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_void_p, P(Probe), C.c_void_p,
                                       C.c_size_t, C.c_void_p]
+    lib.dwkv_static_scratch_bytes.restype = C.c_size_t
+    lib.dwkv_static_scratch_bytes.argtypes = []
+    lib.dwkv_decode_noalloc.restype = C.c_int
+    lib.dwkv_decode_noalloc.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_void_p, C.c_int32, C.c_float,
+                                        C.c_void_p, P(Probe), C.c_void_p]
     lib.dwkv_route_workspace_bytes.restype = C.c_size_t
     lib.dwkv_route_workspace_bytes.argtypes = [P(Dims)]
     lib.dwkv_route.restype = C.c_int

@@ -2,6 +2,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "internal.h"
 
@@ -186,6 +187,7 @@ const char* dwkv_status_str(dwkv_status s) {
     case DWKV_E_LAYOUT: return "malformed cache layout";
     case DWKV_E_HIP: return "HIP runtime error";
     case DWKV_E_ALIGN: return "device pointer not 16-byte aligned";
+    case DWKV_E_SCRATCH: return "needs more than the library's static scratch";
   }
   return "unknown status";
 }
@@ -404,6 +406,58 @@ dwkv_status dwkv_decode_merge(const dwkv_dims* d, const dwkv_cache* c, int32_t l
   dwkv_status st = check_decode_common(d, probe, workspace, ws_bytes);
   if (st != DWKV_OK) return st;
   return merge_phase(d, c, layer, out, probe, workspace, reinterpret_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"
+
+// The allocation-free decode keeps its split partials in this file-scope
+// array: one copy per GPU the library runs on, held until the process ends.
+// Host code never uses the array's name as an address (on the host it is a
+// stand-in, not device memory): each device's address is looked up once with
+// hipGetSymbolAddress, with that device current, and kept below.
+namespace {
+constexpr size_t kStaticScratchBytes = (size_t)DWKV_STATIC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+void* g_scratch_ptr[kMaxDevices] = {};
+std::mutex g_scratch_mu;
+}  // namespace
+
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+// Address of the current device's copy of `scratch`, looked up on the first
+// call on that device; null when the lookup fails.
+void* static_scratch_ptr() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+}  // namespace
+
+extern "C" {
+
+size_t dwkv_static_scratch_bytes(void) { return kStaticScratchBytes; }
+
+dwkv_status dwkv_decode_noalloc(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
+                                int32_t q_type, float sm_scale, float* out, const dwkv_probe* probe,
+                                void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if ((st = check_probe(d, probe)) != DWKV_OK) return st;
+  if (!out) return DWKV_E_NULL;
+  if (!aligned16(out)) return DWKV_E_ALIGN;
+  if (ws_layout(d, probe).total > kStaticScratchBytes) return DWKV_E_SCRATCH;
+  void* ws = static_scratch_ptr();
+  if (!ws) return DWKV_E_HIP;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if ((st = partials_phase(d, c, layer, q, q_type, sm_scale, probe, ws, s)) != DWKV_OK) return st;
+  return merge_phase(d, c, layer, out, probe, ws, s);
 }
 
 size_t dwkv_route_workspace_bytes(const dwkv_dims* d) {

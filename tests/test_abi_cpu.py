@@ -364,3 +364,23 @@ def test_split_plan_fits_one_round(lib, lens, hk):
     d2, keep2 = dims(batch=len(lens), n_kv_heads=hk, n_q_heads=4 * hk, basis_rank=48, levels=(0, 4, 8, 16),
                      cu_seqlens_host=cu, total_tokens=cu[-1], res_stride=1 << 26, split_tokens=1024)
     assert lib.dwkv_split_tokens(C.byref(d2)) == 1024
+
+
+def test_noalloc_refuses_beyond_static_scratch(lib):
+    """dwkv_decode_noalloc checks its scratch need on the host before anything
+    touches the GPU: dims whose workspace exceeds the static array get
+    DWKV_E_SCRATCH."""
+    from paper_2607_06523_amd import binding
+    limit = int(lib.dwkv_static_scratch_bytes())
+    assert limit == 16 << 20
+    n = 40000
+    cu = np.arange(n + 1, dtype=np.int32) * 64
+    d, keep = binding.make_dims(batch=n, n_layers=1, window=1, n_kv_heads=8, n_q_heads=32, head_dim=128,
+                                basis_rank=48, levels=(0,), cu_seqlens_host=cu, cu_seqlens_dev_ptr=16,
+                                total_tokens=int(cu[-1]), res_stride=1024, split_tokens=64)
+    assert lib.dwkv_workspace_bytes(C.byref(d), None) > limit
+    cache = binding.Cache()
+    st = lib.dwkv_decode_noalloc(C.byref(d), C.byref(cache), 0, C.c_void_p(16), 0,
+                                 C.c_float(0.0), C.c_void_p(16), None, None)
+    assert st == 8
+    assert lib.dwkv_status_str(8) == b"needs more than the library's static scratch"
