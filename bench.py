@@ -6,9 +6,10 @@ residual streaming, softmax, value product, split merge).  Inputs are synthetic
 and already resident in HBM when the timed region starts.
 
 Prints ONE JSON line on stdout; progress goes to stderr.  Beside the metric
-it carries `roofline` (the split-K kernel's achieved bandwidth against the
-published peak and against the device's measured read ceiling, with counter
-traffic from the committed profile), `hbm_read_ceiling`, `cpu_baseline` (the
+(mean step time, with the median and p10/p90 of the timed steps) it carries
+`roofline` (the split-K kernel's achieved bandwidth against the published
+peak and against the device's measured read ceiling, with counter traffic
+from the committed profile, and the whole step's fraction beside it), `hbm_read_ceiling`, `cpu_baseline` (the
 float64 oracle on the host cores) and, unless skipped, the int8-coefficient,
 features, probe, append, comparison and control-loop measurements.
 """
@@ -62,7 +63,9 @@ def dense_fp16_bytes_per_layer(host) -> float:
 def cpu_baseline(host, n_pairs: int, budget_s: float):
     """The float64 oracle, as it stands, on a bounded sample of the same step:
     up to n_pairs (layer, KV head) slabs within budget_s seconds, extrapolated
-    to the whole step when the sample is not all of it."""
+    to the whole step when the sample is not all of it.  `cores` is the thread
+    count of the BLAS pool the oracle's numpy runs on (the threads it used),
+    `host_cores` the host's logical CPU count."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -83,7 +86,8 @@ def cpu_baseline(host, n_pairs: int, budget_s: float):
             break
     dt = time.perf_counter() - t0
     step_s = dt / done * len(pairs)
-    return {"value": B / step_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+    return {"value": B / step_s, "unit": "tokens/s", "cores": int(threads), "host_cores": os.cpu_count(),
+            "kind": "oracle",
             "sample": (f"all {len(pairs)} (layer, KV head) slabs of one decode step, {dt:.1f} s"
                        if done == len(pairs) else
                        f"{done} of {len(pairs)} (layer, KV head) slabs of one decode step, "
@@ -504,7 +508,7 @@ def main():
     # into its own workspace), then the L merges, with one event pair around
     # each run on the kernels' stream.  That times the split-K kernel (the
     # dominant one) on its own without an event between every pair of launches.
-    ev_step = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev_step = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     ev_calls = [torch.cuda.Event(enable_timing=True) for _ in range(3)] if graph is None else None
     ws_layer = [dc.new_workspace() for _ in range(L)] if graph is None else None
     torch.cuda.synchronize()
@@ -523,11 +527,12 @@ def main():
             ev_calls[2].record(stream)
         else:
             step()
-    ev_step[1].record(stream)
+        ev_step[k + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    total_ms = ev_step[0].elapsed_time(ev_step[1])
+    total_ms = ev_step[0].elapsed_time(ev_step[args.steps])
     ms_per_step = total_ms / args.steps
+    per_step = np.array([ev_step[k].elapsed_time(ev_step[k + 1]) for k in range(args.steps)])
     split_ms = merge_ms = None
     if ev_calls is not None:
         split_ms = ev_calls[0].elapsed_time(ev_calls[1]) / L
@@ -553,6 +558,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step_median": round(float(np.median(per_step)), 4),
+        "ms_per_step_p10": round(float(np.percentile(per_step, 10)), 4),
+        "ms_per_step_p90": round(float(np.percentile(per_step, 90)), 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -565,8 +573,11 @@ def main():
                    "graph": bool(graph is not None)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "kernel": "split-K partials pass (tl_kernel at this workload)",
-                     "measured_ceiling": ceiling["gbps"], "frac_of_measured_ceiling": round(achieved / ceiling["gbps"], 4)},
+                     "kernel": "split-K partials pass (the dominant kernel: tl_kernel at this workload)",
+                     "measured_ceiling": ceiling["gbps"], "frac_of_measured_ceiling": round(achieved / ceiling["gbps"], 4),
+                     "whole_step": {"achieved": round(step_gbps, 1), "frac": round(step_gbps / HBM_PEAK_GBPS, 4),
+                                    "note": "algorithmic bytes of all L per-layer calls / the whole step's time "
+                                            "(split-K pass, merge and launch gaps)"}},
         "hbm_read_ceiling": ceiling,
         "step_gbps": round(step_gbps, 1),
         "bytes_per_step": int(bytes_step),

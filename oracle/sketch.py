@@ -2,9 +2,9 @@
 
 TEST INFRASTRUCTURE ONLY.  Nothing in the library imports or calls this module.
 
-Sec. 3 initializes each depth window's shared bases from a small randomized
-low-rank sketch of the cached keys and values after prefill, per head and
-separately for keys and values.  Reading used here: for sequence b, window m,
+In Sec. 3 the shared bases of a depth window start out, once the prompt has
+been prefilled, as a low-rank random projection of that window's keys and of
+its values (each head on its own, keys apart from values).  Reading used here: for sequence b, window m,
 KV head h and Z, stack the window's prefill vectors of that head (every layer
 of the window, every token) as the rows of X ((w T_b) x d); with a random
 sketch matrix Omega (r_b x (w T_b), an input, shared by the heads and by K and
