@@ -76,7 +76,7 @@ struct alignas(16) TSmem {
   float ep_m[kTW][HG];
   float ep_l[kTW][HG];
   float ep_a[kTW][HG][RB];
-  int qmax[HG];
+  float qmaxw[4][HG];                   // per q~ wave: largest |q~| of each head
   // Value residual, per wave.  Accumulators are fixed point in units of
   // 2^(ex - kFxTop) (ex: the wave's bound on the value scales): integer LDS
   // atomics run at one instruction per few cycles whatever the active lanes,
@@ -257,6 +257,43 @@ __device__ __forceinline__ void load_v8(TFrags<RB, true>& f, const TCtx& x, int 
 #pragma unroll
   for (int s = 0; s < C::NS; ++s)
     f.vs[s] = __builtin_amdgcn_raw_buffer_load_b16(x.cvs, ((uint32_t)s * (uint32_t)x.T + t) * 2, 0, 0);
+}
+
+template <int RB, bool C8>
+__device__ __forceinline__ void load_coef(TFrags<RB, C8>& f, const TCtx& x, int j, int lane) {
+  if constexpr (C8) {
+    load_k8<RB>(f, x, j, lane);
+    load_v8<RB>(f, x, j, lane);
+  } else {
+    load_k<RB>(f, x, j, lane);
+    load_v<RB>(f, x, j, lane);
+  }
+}
+
+// Tiles of wave w in a chunk of `ntile` 64-token tiles.  Waves w and w + 4
+// share a SIMD, and the older one (w < 4) issues first, so the pair's tiles
+// j = p + 4 i (p = w % 4, i = 0 .. m - 1) are split unevenly: the older wave
+// takes every even i and, when the pair has an even count of at least four,
+// also the last one; the younger wave takes the other odd i.  At 32 tiles per
+// chunk that is 5 and 3 tiles.  The assignment is fixed, so each wave's
+// summation order does not depend on timing.
+static_assert(kTW == 8, "the tile schedule pairs waves w and w + 4");
+struct TileSeq {
+  int p, m, older, n;
+  __device__ __forceinline__ int at(int k) const {
+    if (!older) return p + 4 * (2 * k + 1);
+    return k < (m + 1) / 2 ? p + 8 * k : p + 4 * (m - 1);
+  }
+};
+
+__device__ __forceinline__ TileSeq tile_seq(int w, int ntile) {
+  TileSeq t;
+  t.p = w & 3;
+  t.m = ntile > t.p ? (ntile - t.p + 3) / 4 : 0;
+  t.older = w < 4;
+  const int extra = (t.m >= 4 && (t.m & 1) == 0) ? 1 : 0;
+  t.n = t.older ? (t.m + 1) / 2 + extra : t.m / 2 - extra;
+  return t;
 }
 
 // Entry range of the lane's token, clipped to the chunk (tokens outside it own
@@ -877,15 +914,20 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   }
   const uint16_t* bk_rows = a.basis + (int64_t)b * a.basis_b_stride + (int64_t)kvh * 2 * RB * D;
 
-  // Requests in issue order (vector loads complete in order): the fragments
-  // of the q~ product (B^K rows, q); the query for the LDS table; the first
-  // tile's offsets and scales; its coefficient fragments; last its residual
-  // entries, whose addresses need the offsets.  Every tile load is
-  // unconditional (a wave with no tile reads the chunk's last one and never
-  // uses it); only the waves that own basis rows request q~ fragments.
+  // Requests in issue order (vector loads complete in order): the first
+  // tile's offsets, alone, so that its residual entries can be requested as
+  // soon as they return; the fragments of the q~ product (B^K rows, q); the
+  // query for the LDS table; the first tile's scales and the second tile's
+  // offsets; the residual entries.  Then the coefficient burst of the first
+  // tile, which stalls a wave's instruction issue for a while: the waves that
+  // do not compute q~ issue it at once, the others once q~ is written, so that
+  // q~ is ready before the burst has landed.  One barrier publishes q~ and the
+  // query table.  Every tile load is unconditional (a wave with no tile reads
+  // the chunk's last one and never uses it).
   constexpr int QPT = (G * D + kTThreads - 1) / kTThreads;     // query elements per thread
-  const int j0 = min(wv, x.ntile - 1);
-  const int j1 = min(wv + kTW, x.ntile - 1);
+  const TileSeq ts = tile_seq(wv, x.ntile);
+  const int j0 = ts.n > 0 ? ts.at(0) : x.ntile - 1;
+  const int j1 = ts.n > 1 ? ts.at(1) : j0;
   TFrags<RB, C8> fr{};                  // lanes past r_b never load values: keep them zero
   TMeta mc{}, mn{}, mnn{};
   TEnt ec{}, en{};
@@ -893,6 +935,8 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   // on 16x16x32 MFMA, A = B^K rows (row = lane % 16, channels 32s + 8(lane/16)
   // + i), B = q (column = head lane % 16)
   u4v bkf[4], qf[4];
+  if constexpr (RESID) load_offsets(mc, x, j0, lane);
+  __builtin_amdgcn_sched_barrier(0);
   if (wv < NS) {
     const uint16_t* brow = bk_rows + (int64_t)(16 * wv + col) * D + 8 * grp;
     const uint16_t* qrow = a.q + ((int64_t)b * a.n_q_heads + kvh * G + min(col, G - 1)) * D + 8 * grp;
@@ -907,33 +951,28 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
     const int i = min(tid + n * kTThreads, G * D - 1);
     qraw[n] = a.q[((int64_t)b * a.n_q_heads + kvh * G + i / D) * D + i % D];
   }
-  __builtin_amdgcn_sched_barrier(0);
   if constexpr (RESID) {
-    load_offsets(mc, x, j0, lane);
     load_scales(mc, x, j0, lane);
     load_offsets(mn, x, j1, lane);
   }
   __builtin_amdgcn_sched_barrier(0);
-  if constexpr (C8) {
-    load_k8<RB>(fr, x, j0, lane);
-    load_v8<RB>(fr, x, j0, lane);
-  } else {
-    load_k<RB>(fr, x, j0, lane);
-    load_v<RB>(fr, x, j0, lane);
-  }
-  __builtin_amdgcn_sched_barrier(0);
   if constexpr (RESID) load_entries(ec, x, mc, lane);
-
-  if (tid < HG) sm.qmax[tid] = 0;
-  for (int i = tid; i < D * HG; i += kTThreads) (&sm.qs[0][0])[i] = 0.f;
-  __syncthreads();
+  __builtin_amdgcn_sched_barrier(0);
+  // every entry of the query table once: the group's heads, zeros past G
 #pragma unroll
-  for (int n = 0; n < QPT; ++n) {
+  for (int n = 0; n < (D * HG + kTThreads - 1) / kTThreads; ++n) {
     const int i = tid + n * kTThreads;
-    if (i < G * D)
-      sm.qs[i % D][i / D] = (a.q_bf16 ? bf16_bits_to_float(qraw[n]) : half_bits_to_float(qraw[n])) * a.qscale;
+    if (i >= D * HG) break;
+    const int hh = i / D, c = i % D;
+    float v = 0.f;
+    if (hh < G && n < QPT) {
+      const uint16_t bits = qraw[n < QPT ? n : 0];
+      v = (a.q_bf16 ? bf16_bits_to_float(bits) : half_bits_to_float(bits)) * a.qscale;
+    }
+    sm.qs[c][hh] = v;
   }
-  __syncthreads();
+  // the waves that do not compute q~ request their first tile now
+  if (wv >= NS) load_coef<RB, C8>(fr, x, j0, lane);
   if (wv < NS) {
     // q * qscale for head col, scaled by a power of two so the head's largest
     // entry sits just under 2^14 and split into fp16 hi + lo
@@ -982,8 +1021,11 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
         sm.qt[col][16 * wv + 4 * grp + i] = v;
         am = fmaxf(am, fabsf(v));
       }
-      atomicMax(&sm.qmax[col], __float_as_int(am));
+      am = fmaxf(am, __shfl_xor(am, 16));
+      am = fmaxf(am, __shfl_xor(am, 32));
+      if (grp == 0) sm.qmaxw[wv][col] = am;
     }
+    load_coef<RB, C8>(fr, x, j0, lane);
   }
   __syncthreads();
 
@@ -998,7 +1040,9 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
     for (int i = 0; i < HG; ++i) {
       int kexp = 0;
       if (i < G) {
-        const float mx = __int_as_float(sm.qmax[i]);
+        float mx = 0.f;
+#pragma unroll
+        for (int w2 = 0; w2 < NS; ++w2) mx = fmaxf(mx, sm.qmaxw[w2][i]);
         if (mx > 0.f) {
           int e;
           frexpf(mx, &e);
@@ -1040,14 +1084,15 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   }
 
 
-  // tiles wv, wv + 8, wv + 16, ...: a fixed assignment keeps the summation
+  // the wave's tiles (tile_seq): a fixed assignment keeps the summation
   // order, and so the result, independent of timing.  The last tile of the
   // wave runs without the next tiles' loads.
-  int j = wv;
-  for (; j + kTW < x.ntile; j += kTW)
-    tstep<RB, G, RESID, SCORES, C8, false>(st, fr, mc, mn, mnn, ec, en, j, j + kTW, j + 2 * kTW, x, sm, wv, lane);
-  if (j < x.ntile)
-    tstep<RB, G, RESID, SCORES, C8, true>(st, fr, mc, mn, mnn, ec, en, j, j + kTW, j + 2 * kTW, x, sm, wv, lane);
+  for (int k = 0; k + 1 < ts.n; ++k)
+    tstep<RB, G, RESID, SCORES, C8, false>(st, fr, mc, mn, mnn, ec, en, ts.at(k), ts.at(k + 1),
+                                           k + 2 < ts.n ? ts.at(k + 2) : x.ntile, x, sm, wv, lane);
+  if (ts.n > 0)
+    tstep<RB, G, RESID, SCORES, C8, true>(st, fr, mc, mn, mnn, ec, en, ts.at(ts.n - 1), x.ntile, x.ntile, x, sm,
+                                          wv, lane);
 
   // epilogue: the waves combine; the partial keeps a~ in basis space (the
   // merge projects it through B^V once per sequence and head).  Each wave
