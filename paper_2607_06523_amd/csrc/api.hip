@@ -234,7 +234,7 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   if (q_type != DWKV_F16 && q_type != DWKV_BF16) return DWKV_E_DIMS;
   const bool c8 = d->coef_format == DWKV_COEF_I8;
   if (c8) {
-    if (!uses_token_lane(d) || probe || scores) return DWKV_E_UNSUPPORTED;
+    if (!uses_token_lane(d) || d->n_q_heads / d->n_kv_heads > 4 || probe || scores) return DWKV_E_UNSUPPORTED;
     if (!c->coef_k_scale || !c->coef_v_scale) return DWKV_E_NULL;
     if ((reinterpret_cast<uintptr_t>(c->coef_k_scale) | reinterpret_cast<uintptr_t>(c->coef_v_scale)) & 1u)
       return DWKV_E_ALIGN;

@@ -1,5 +1,6 @@
 // Token-lane split-K decode attention over the cross-depth factorized KV cache,
-// gfx950, for query groups of at most 4 heads and basis ranks up to 64.
+// gfx950, for query groups of 1, 2, 4 (ranks up to 16) or 8 heads (ranks up
+// to 32) and basis ranks up to 64.
 //
 // Same arithmetic as the general kernel (Sec. 3, Eq. 1 used through its
 // linearity: scores A^K_t (B^K q) plus the routed residual channels, values
@@ -51,11 +52,24 @@ typedef uint32_t u2v __attribute__((ext_vector_type(2)));
 
 constexpr int D = kHeadDim;
 constexpr int TT = 64;                  // tokens per tile = lanes per wave
-constexpr int HG = 4;                   // head rows of the score and value products
 constexpr float kLazy = 8.0f;           // log2 headroom of the running reference
-constexpr int kMaxRank = 16;            // residual entries per token this kernel reads
 constexpr int kVB = 3;                  // value-entry batches of 64 loaded ahead per tile
-constexpr int kEmap = TT * kMaxRank;    // entries a tile can hold
+
+// Sizes that follow the query-group size G: groups of up to 4 heads use 4
+// head rows in the score product and read ranks up to 16; groups of 8 use 8
+// head rows (two groups of 4 in the value product) and read ranks up to 32.
+template <int G>
+struct TGrp {
+  static constexpr int HG = G > 4 ? 8 : 4;     // head rows (heads past G are zero)
+  static constexpr int NHG = HG / 4;           // groups of 4 heads
+  static constexpr int MR = G > 4 ? 32 : 16;   // residual entries per token the kernel reads
+  static constexpr int KR = G > 4 ? 4 : 8;     // key-residual entries per LDS lookup round
+  static constexpr int NR = MR / KR;           // lookup rounds for the largest rank
+  static constexpr int EMAP = TT * MR;         // residual entries a tile can hold
+  static constexpr int CW = MR / 4 + 1;        // channel-byte dwords of a lane's entry window
+  static constexpr int VW = MR / 8 + 1;        // code dwords of the window
+  static_assert(G == 1 || G == 2 || G == 4 || G == 8, "query group");
+};
 constexpr int kFxTop = 34;              // fixed-point fraction bits = kFxTop - scale exponent bound
 constexpr int kWaitVmcnt0 = 0x0F70;     // s_waitcnt immediate: vmcnt(0) only
 constexpr int kNT = 2;                  // buffer cache policy: nontemporal (whole lines read once)
@@ -69,21 +83,25 @@ struct TCfg {
   static_assert(RB % 16 == 0 && RB >= 16 && RB <= 64, "basis rank");
 };
 
-template <int RB, bool RESID>
+template <int RB, int G, bool RESID>
 struct alignas(16) TSmem {
+  static constexpr int HG = TGrp<G>::HG;
   alignas(16) float qs[D][HG];          // q * sm_scale * log2(e), heads past G zero
   float qt[HG][RB];                     // q~ = B^K q (scaled)
   float ep_m[kTW][HG];
   float ep_l[kTW][HG];
   float ep_a[kTW][HG][RB];
   float qmaxw[4][HG];                   // per q~ wave: largest |q~| of each head
+  // groups of 8: the score product's q~ operands (hi, lo per k-step, the
+  // lane's fragment), re-read each tile instead of held in registers
+  alignas(16) h4 qa[HG == 8 ? 2 : 1][HG == 8 ? TCfg<RB>::NS : 1][64];
   // Value residual, per wave.  Accumulators are fixed point in units of
   // 2^(ex - kFxTop) (ex: the wave's bound on the value scales): integer LDS
   // atomics run at one instruction per few cycles whatever the active lanes,
   // float LDS atomics at a few cycles per lane.  After its loop a wave
   // rewrites its accumulators as floats [HG][D] in the same storage.
   long long racc[kTW][RESID ? HG : 1][RESID ? D : 1];
-  alignas(4) uint8_t emap[kTW][RESID ? kEmap : 4];  // token lane + 1 at each token's first entry
+  alignas(4) uint8_t emap[kTW][RESID ? TGrp<G>::EMAP : 4];  // token lane + 1 at each token's first entry
   alignas(16) float pw[kTW][RESID ? TT : 1][HG];  // p * value scale per token lane
 };
 
@@ -108,17 +126,20 @@ struct TMeta {
   uint32_t sk, sv;                      // residual scale bits
 };
 
+template <int G>
 struct TEnt {
-  uint32_t ck[5], vk[3];                // key channel bytes / codes around this lane's oa
+  uint32_t ck[TGrp<G>::CW], vk[TGrp<G>::VW];  // key channel bytes / codes around this lane's oa
   uint32_t vc[kVB], vv[kVB];            // value entries e0 + 64b + lane: channel byte, code byte
 };
 
-template <int RB, bool C8>
+template <int RB, int G, bool C8>
 struct TState {
-  static constexpr int NACC = C8 ? TCfg<RB>::NS : 1;
+  static constexpr int HG = TGrp<G>::HG;
+  static constexpr int NACC = C8 ? TCfg<RB>::NS : TGrp<G>::NHG;
   h4 qhi[TCfg<RB>::NS], qlo[TCfg<RB>::NS];
-  f4 acc_h[NACC], acc_l[NACC];          // a~[head][channel lane] from p hi / p lo (int8: one pair
-                                        // per coefficient block, each valid in its block's lanes)
+  f4 acc_h[NACC], acc_l[NACC];          // a~[head][channel lane] from p hi / p lo: one pair per group
+                                        // of 4 heads (int8: one pair per coefficient block, each
+                                        // valid in its block's lanes)
   float m[HG], l[HG], down[HG];
   int ex;                               // bound on the value scales seen: |s_v| < 2^ex
 };
@@ -311,17 +332,34 @@ __device__ __forceinline__ void load_scales(TMeta& m, const TCtx& x, int j, int 
   m.sv = __builtin_amdgcn_raw_buffer_load_b16(x.sv, t * 2, 0, 0);
 }
 
-// Key entries: the window around the lane's own entries, 20 channel bytes
-// from oa rounded down to 4 and 12 code bytes from oa/2 rounded down to 4
-// (kMaxRank entries; oa is even).  Value entries: the tile's first 64*kVB,
-// one per lane and batch.  Bytes past the entries in use are never used.
-__device__ __forceinline__ void load_entries(TEnt& e, const TCtx& x, const TMeta& m, int lane) {
+// Key entries: the window around the lane's own entries, 4 CW channel bytes
+// from oa rounded down to 4 and 4 VW code bytes from oa/2 rounded down to 4
+// (MR entries; oa is even).  Value entries: the tile's first 64*kVB, one per
+// lane and batch.  Bytes past the entries in use are never used.
+template <int N>
+__device__ __forceinline__ void load_words(uint32_t (&w)[N], rsrc_t r, uint32_t off) {
+#pragma unroll
+  for (int i = 0; i + 4 <= N; i += 4) {
+    const u4v v = __builtin_amdgcn_raw_buffer_load_b128(r, off + 4 * i, 0, 0);
+    w[i] = v.x; w[i + 1] = v.y; w[i + 2] = v.z; w[i + 3] = v.w;
+  }
+  constexpr int R = N % 4, B = N - R;
+  if constexpr (R == 3) {
+    const u3v v = __builtin_amdgcn_raw_buffer_load_b96(r, off + 4 * B, 0, 0);
+    w[B] = v.x; w[B + 1] = v.y; w[B + 2] = v.z;
+  } else if constexpr (R == 2) {
+    const u2v v = __builtin_amdgcn_raw_buffer_load_b64(r, off + 4 * B, 0, 0);
+    w[B] = v.x; w[B + 1] = v.y;
+  } else if constexpr (R == 1) {
+    w[B] = __builtin_amdgcn_raw_buffer_load_b32(r, off + 4 * B, 0, 0);
+  }
+}
+
+template <int G>
+__device__ __forceinline__ void load_entries(TEnt<G>& e, const TCtx& x, const TMeta& m, int lane) {
   const uint32_t a = m.oa & ~3u, ca = (m.oa >> 1) & ~3u;
-  const u4v c4 = __builtin_amdgcn_raw_buffer_load_b128(x.idx[0], a, 0, 0);
-  e.ck[0] = c4.x; e.ck[1] = c4.y; e.ck[2] = c4.z; e.ck[3] = c4.w;
-  e.ck[4] = __builtin_amdgcn_raw_buffer_load_b32(x.idx[0], a + 16, 0, 0);
-  const u3v v3 = __builtin_amdgcn_raw_buffer_load_b96(x.val[0], ca, 0, 0);
-  e.vk[0] = v3.x; e.vk[1] = v3.y; e.vk[2] = v3.z;
+  load_words(e.ck, x.idx[0], a);
+  load_words(e.vk, x.val[0], ca);
   const uint32_t e0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)m.oa);
 #pragma unroll
   for (int b = 0; b < kVB; ++b) {
@@ -338,19 +376,21 @@ __device__ __forceinline__ void wave_lds_fence() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Channel bytes of entries [4w, 4w+4) of the token and its 16 codes, aligned.
+// Channel bytes of entries [4w, 4w+4) of the token and its MR codes, aligned.
+template <int G>
 struct Window {
-  uint32_t ch[4];
-  uint32_t cd[2];
+  uint32_t ch[TGrp<G>::MR / 4];
+  uint32_t cd[TGrp<G>::MR / 8];
 };
 
-__device__ __forceinline__ Window align_window(const uint32_t* c5, const uint32_t* v3, uint32_t oa) {
-  Window w;
+template <int G>
+__device__ __forceinline__ Window<G> align_window(const uint32_t* cw, const uint32_t* vw, uint32_t oa) {
+  Window<G> w;
   const uint32_t sc = oa & 3u, sv = (oa >> 1) & 3u;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) w.ch[i] = __builtin_amdgcn_alignbyte(c5[i + 1], c5[i], sc);
-  w.cd[0] = __builtin_amdgcn_alignbyte(v3[1], v3[0], sv);
-  w.cd[1] = __builtin_amdgcn_alignbyte(v3[2], v3[1], sv);
+  for (int i = 0; i < TGrp<G>::MR / 4; ++i) w.ch[i] = __builtin_amdgcn_alignbyte(cw[i + 1], cw[i], sc);
+#pragma unroll
+  for (int i = 0; i < TGrp<G>::MR / 8; ++i) w.cd[i] = __builtin_amdgcn_alignbyte(vw[i + 1], vw[i], sv);
   return w;
 }
 
@@ -444,11 +484,13 @@ __device__ __forceinline__ void pv_tile_h(f4& acc_h, f4& acc_l, h4 ph, h4 pl, co
 }
 
 template <int RB, int G, bool RESID, bool SCORES, bool C8, bool LAST>
-__device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TMeta& mc, TMeta& mn, TMeta& mnn,
-                                      TEnt& ec, TEnt& en, int j, int jn, int jnn, const TCtx& x,
-                                      TSmem<RB, RESID>& sm, int wv, int lane) {
+__device__ __forceinline__ void tstep(TState<RB, G, C8>& st, TFrags<RB, C8>& fr, TMeta& mc, TMeta& mn, TMeta& mnn,
+                                      TEnt<G>& ec, TEnt<G>& en, int j, int jn, int jnn, const TCtx& x,
+                                      TSmem<RB, G, RESID>& sm, int wv, int lane) {
   using C = TCfg<RB>;
+  using Q = TGrp<G>;
   constexpr int NS = C::NS;
+  constexpr int HG = Q::HG, NHG = Q::NHG, MR = Q::MR, KR = Q::KR, NR = Q::NR;
   const int grp = lane >> 4;
   const int32_t t0 = tstart(x, j);
   // two tiles ahead of the wave's second-to-last tile the offset prefetch
@@ -471,26 +513,45 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
   // query-table lookups, and the entry->token map of the value residual
   // (token lanes mark their first entry; a running maximum over the entry
   // lanes resolves it after the scores)
-  uint32_t rank = 0, e0 = 0, n = 0, cd0 = 0, cd1 = 0;
-  Window wk{};
-  f4 qv0[8];
+  uint32_t rank = 0, e0 = 0, n = 0;
+  uint32_t cd[MR / 8] = {};
+  Window<G> wk{};
+  f4 qv0[KR][NHG];
   if constexpr (RESID) {
-    rank = min(mc.ob - mc.oa, (uint32_t)kMaxRank);
+    rank = min(mc.ob - mc.oa, (uint32_t)MR);
     if (mc.ob < mc.oa) rank = 0;
-    wk = align_window(ec.ck, ec.vk, mc.oa);
+    wk = align_window<G>(ec.ck, ec.vk, mc.oa);
     // codes past the token's rank read as zero: mask the packed code words
-    // once (rank <= 16, 4 bits per entry)
+    // once (rank <= MR, 4 bits per entry)
     const uint32_t nb = 4u * rank;
-    cd0 = nb >= 32u ? wk.cd[0] : wk.cd[0] & ((1u << nb) - 1u);
-    cd1 = nb <= 32u ? 0u : (nb >= 64u ? wk.cd[1] : wk.cd[1] & ((1u << (nb - 32u)) - 1u));
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-      qv0[u] = *reinterpret_cast<const f4*>(&sm.qs[(wk.ch[u >> 2] >> (8 * (u & 3))) & (D - 1)][0]);
+    for (int k = 0; k < MR / 8; ++k) {
+      const uint32_t lo = 32u * k;
+      cd[k] = nb >= lo + 32u ? wk.cd[k] : (nb <= lo ? 0u : wk.cd[k] & ((1u << (nb - lo)) - 1u));
+    }
+#pragma unroll
+    for (int u = 0; u < KR; ++u)
+#pragma unroll
+      for (int h = 0; h < NHG; ++h)
+        qv0[u][h] = *reinterpret_cast<const f4*>(&sm.qs[(wk.ch[u >> 2] >> (8 * (u & 3))) & (D - 1)][4 * h]);
     e0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)mc.oa);
     const uint32_t e1 = (uint32_t)__builtin_amdgcn_readlane((int)mc.ob, 63);
-    n = e1 > e0 ? min(e1 - e0, (uint32_t)kEmap) : 0u;
+    n = e1 > e0 ? min(e1 - e0, (uint32_t)Q::EMAP) : 0u;
     for (uint32_t i = 4 * lane; i < n; i += 256) *reinterpret_cast<uint32_t*>(&sm.emap[wv][i]) = 0u;
     if (rank > 0 && mc.oa - e0 < n) sm.emap[wv][mc.oa - e0] = (uint8_t)(lane + 1);
+  }
+
+  // the q~ operands: from registers, or for groups of 8 from the LDS table
+  h4 qh[NS], ql[NS];
+#pragma unroll
+  for (int k = 0; k < NS; ++k) {
+    if constexpr (HG == 8) {
+      qh[k] = sm.qa[0][k][lane];
+      ql[k] = sm.qa[1][k][lane];
+    } else {
+      qh[k] = st.qhi[k];
+      ql[k] = st.qlo[k];
+    }
   }
 
   // 2. scores: block bk lands in every lane group; lane group g keeps block g
@@ -506,8 +567,8 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
 #pragma unroll
       for (int bk = 0; bk < 4; ++bk) {
         const h4 kf = i8x4_to_h4(fr.k[bk][s]);
-        f4 o = mfma16(st.qhi[s], kf, f4{0.f, 0.f, 0.f, 0.f});
-        o = mfma16(st.qlo[s], kf, o);
+        f4 o = mfma16(qh[s], kf, f4{0.f, 0.f, 0.f, 0.f});
+        o = mfma16(ql[s], kf, o);
 #pragma unroll
         for (int i = 0; i < 4; ++i) sacc[bk][i] += o[i] * ksc;
       }
@@ -519,49 +580,78 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
 #pragma unroll
       for (int bk = 0; bk < 4; ++bk) {
         const h4 k0 = __builtin_bit_cast(h4, fr.k[bk][s]), k1 = __builtin_bit_cast(h4, fr.k[bk][s + 1]);
-        sacc[bk] = mfma32(st.qhi[s], st.qhi[s + 1], k0, k1, sacc[bk]);
-        sacc[bk] = mfma32(st.qlo[s], st.qlo[s + 1], k0, k1, sacc[bk]);
+        sacc[bk] = mfma32(qh[s], qh[s + 1], k0, k1, sacc[bk]);
+        sacc[bk] = mfma32(ql[s], ql[s + 1], k0, k1, sacc[bk]);
       }
     if constexpr (NS % 2 == 1) {
 #pragma unroll
       for (int bk = 0; bk < 4; ++bk) {
         const h4 kf = __builtin_bit_cast(h4, fr.k[bk][NS - 1]);
-        sacc[bk] = mfma16(st.qhi[NS - 1], kf, sacc[bk]);
-        sacc[bk] = mfma16(st.qlo[NS - 1], kf, sacc[bk]);
+        sacc[bk] = mfma16(qh[NS - 1], kf, sacc[bk]);
+        sacc[bk] = mfma16(ql[NS - 1], kf, sacc[bk]);
       }
     }
     if constexpr (!LAST) load_k<RB>(fr, x, jn_l, lane);
   }
   float sc[HG];
+  if constexpr (HG == 4) {
 #pragma unroll
-  for (int i = 0; i < HG; ++i) {
-    const float a01 = grp == 0 ? sacc[0][i] : sacc[1][i];
-    const float a23 = grp == 2 ? sacc[2][i] : sacc[3][i];
-    sc[i] = (grp < 2 ? a01 : a23) * st.down[i];
+    for (int i = 0; i < HG; ++i) {
+      const float a01 = grp == 0 ? sacc[0][i] : sacc[1][i];
+      const float a23 = grp == 2 ? sacc[2][i] : sacc[3][i];
+      sc[i] = (grp < 2 ? a01 : a23) * st.down[i];
+    }
+  } else {
+    // 8 head rows: lane group g holds heads 4 (g & 1) .. + 3 of every block;
+    // its own token's other four heads are in the partner group g ^ 1's copy
+    // of block g, fetched with one row swap (v_permlane16_swap)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float a01 = grp == 0 ? sacc[0][i] : sacc[1][i];
+      const float a23 = grp == 2 ? sacc[2][i] : sacc[3][i];
+      const float own = grp < 2 ? a01 : a23;
+      const float b01 = grp == 0 ? sacc[1][i] : sacc[0][i];
+      const float b23 = grp == 2 ? sacc[3][i] : sacc[2][i];
+      const uint32_t y = __builtin_bit_cast(uint32_t, grp < 2 ? b01 : b23);
+      const auto r = __builtin_amdgcn_permlane16_swap(y, y, false, false);
+      const float oth = __builtin_bit_cast(float, (grp & 1) ? r[0] : r[1]);
+      sc[i] = ((grp & 1) ? oth : own) * st.down[i];
+      sc[4 + i] = ((grp & 1) ? own : oth) * st.down[4 + i];
+    }
   }
 
   // 3. key residual: this lane's entries add code * q[c] * scale
   int tk[kVB];                          // value residual: token lane + 1 of each preloaded entry
   int carry = 0;
   if constexpr (RESID) {
-    float rk[HG] = {0.f, 0.f, 0.f, 0.f};
-    // entries 0..7 from the lookups of step 1b, 8..15 in one more round
+    float rk[HG];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const float code = code_at(cd0, u);
+    for (int i = 0; i < HG; ++i) rk[i] = 0.f;
+    // entries 0 .. KR-1 from the lookups of step 1b, then further rounds of
+    // KR while some token of the wave has more entries
 #pragma unroll
-      for (int i = 0; i < G; ++i) rk[i] += code * qv0[u][i];
+    for (int u = 0; u < KR; ++u) {
+      const float code = code_at(cd[u >> 3], u & 7);
+#pragma unroll
+      for (int i = 0; i < G; ++i) rk[i] += code * qv0[u][i >> 2][i & 3];
     }
-    if (__ballot(rank > 8u) != 0) {
-      f4 qv[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        qv[u] = *reinterpret_cast<const f4*>(&sm.qs[(wk.ch[2 + (u >> 2)] >> (8 * (u & 3))) & (D - 1)][0]);
+    for (int r = 1; r < NR; ++r) {
+      if (__ballot(rank > (uint32_t)(KR * r)) == 0) break;
+      f4 qv[KR][NHG];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float code = code_at(cd1, u);
+      for (int u = 0; u < KR; ++u) {
+        const int e = KR * r + u;
 #pragma unroll
-        for (int i = 0; i < G; ++i) rk[i] += code * qv[u][i];
+        for (int h = 0; h < NHG; ++h)
+          qv[u][h] = *reinterpret_cast<const f4*>(&sm.qs[(wk.ch[e >> 2] >> (8 * (e & 3))) & (D - 1)][4 * h]);
+      }
+#pragma unroll
+      for (int u = 0; u < KR; ++u) {
+        const int e = KR * r + u;
+        const float code = code_at(cd[e >> 3], e & 7);
+#pragma unroll
+        for (int i = 0; i < G; ++i) rk[i] += code * qv[u][i >> 2][i & 3];
       }
     }
     const float rs = half_bits_to_float((uint16_t)mc.sk);
@@ -587,7 +677,10 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
     if constexpr (SCORES) {             // the token's scores, for the attention-mass features
       if (valid) {
         float* dst = x.sco + (int64_t)t * G;
-        if constexpr (G == 4) *reinterpret_cast<f4*>(dst) = f4{sc[0], sc[1], sc[2], sc[3]};
+        if constexpr (G == 8) {
+          *reinterpret_cast<f4*>(dst) = f4{sc[0], sc[1], sc[2], sc[3]};
+          *reinterpret_cast<f4*>(dst + 4) = f4{sc[4], sc[5], sc[6], sc[7]};
+        } else if constexpr (G == 4) *reinterpret_cast<f4*>(dst) = f4{sc[0], sc[1], sc[2], sc[3]};
         else if constexpr (G == 2) *reinterpret_cast<float2*>(dst) = make_float2(sc[0], sc[1]);
         else dst[0] = sc[0];
       }
@@ -607,12 +700,17 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
         alpha[i] = mnew == -INFINITY ? 1.0f : exp2f(st.m[i] - mnew);
         st.m[i] = mnew;
         st.l[i] *= alpha[i];
-#pragma unroll
-        for (int b = 0; b < TState<RB, C8>::NACC; ++b) {
-          st.acc_h[b][i] *= alpha[i];
-          st.acc_l[b][i] *= alpha[i];
-        }
       }
+      // accumulator pair b, element i holds head i (int8: one pair per
+      // coefficient block) or head 4 b + i (one pair per group of 4 heads)
+#pragma unroll
+      for (int b = 0; b < TState<RB, G, C8>::NACC; ++b)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float al = alpha[C8 ? i : 4 * b + i];
+          st.acc_h[b][i] *= al;
+          st.acc_l[b][i] *= al;
+        }
       if constexpr (RESID) {
 #pragma unroll
         for (int i = 0; i < G; ++i) {
@@ -654,16 +752,19 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
     }
     if constexpr (!LAST) load_v8<RB>(fr, x, jn_l, lane);
   } else {
-    float pt[4] = {p[0], p[1], p[2], p[3]};
-    quad_transpose(pt, lane);
-    h4 ph, pl;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const _Float16 hh = (_Float16)pt[i];
-      ph[i] = hh;
-      pl[i] = (_Float16)(pt[i] - (float)hh);
+    for (int hg = 0; hg < NHG; ++hg) {      // one pass per group of 4 heads
+      float pt[4] = {p[4 * hg], p[4 * hg + 1], p[4 * hg + 2], p[4 * hg + 3]};
+      quad_transpose(pt, lane);
+      h4 ph, pl;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const _Float16 hh = (_Float16)pt[i];
+        ph[i] = hh;
+        pl[i] = (_Float16)(pt[i] - (float)hh);
+      }
+      pv_tile(st.acc_h[hg], st.acc_l[hg], ph, pl, fr.v, std::make_integer_sequence<int, 16>{});
     }
-    pv_tile(st.acc_h[0], st.acc_l[0], ph, pl, fr.v, std::make_integer_sequence<int, 16>{});
     if constexpr (!LAST) load_v<RB>(fr, x, jn_l, lane);
   }
 
@@ -690,11 +791,17 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
     }
     const double scale = ldexp(1.0, kFxTop - st.ex);
     const float rs = half_bits_to_float((uint16_t)mc.sv);
-    *reinterpret_cast<f4*>(&sm.pw[wv][lane][0]) = f4{p[0] * rs, p[1] * rs, p[2] * rs, p[3] * rs};
-    wave_lds_fence();
-    f4 wv4[kVB];
 #pragma unroll
-    for (int bb = 0; bb < kVB; ++bb) wv4[bb] = *reinterpret_cast<const f4*>(&sm.pw[wv][max(tk[bb] - 1, 0)][0]);
+    for (int hg = 0; hg < NHG; ++hg)
+      *reinterpret_cast<f4*>(&sm.pw[wv][lane][4 * hg]) =
+          f4{p[4 * hg] * rs, p[4 * hg + 1] * rs, p[4 * hg + 2] * rs, p[4 * hg + 3] * rs};
+    wave_lds_fence();
+    f4 wv4[kVB][NHG];
+#pragma unroll
+    for (int bb = 0; bb < kVB; ++bb)
+#pragma unroll
+      for (int hg = 0; hg < NHG; ++hg)
+        wv4[bb][hg] = *reinterpret_cast<const f4*>(&sm.pw[wv][max(tk[bb] - 1, 0)][4 * hg]);
 #pragma unroll
     for (int bb = 0; bb < kVB; ++bb) {
       const uint32_t e = 64u * bb + lane;
@@ -704,7 +811,8 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
         const uint32_t c = ec.vc[bb] & (D - 1);
 #pragma unroll
         for (int i = 0; i < G; ++i)
-          atomicAdd(reinterpret_cast<unsigned long long*>(&sm.racc[wv][i][c]), to_fixed(wv4[bb][i] * code, scale));
+          atomicAdd(reinterpret_cast<unsigned long long*>(&sm.racc[wv][i][c]),
+                    to_fixed(wv4[bb][i >> 2][i & 3] * code, scale));
       }
     }
     // entries past the preloaded batches (tiles with more than 64 kVB): their
@@ -727,12 +835,15 @@ __device__ __forceinline__ void tstep(TState<RB, C8>& st, TFrags<RB, C8>& fr, TM
         carry = __builtin_amdgcn_readlane(t, 63);
         if (e < n) {
           const uint32_t ea = e0 + e;
-          const f4 w = *reinterpret_cast<const f4*>(&sm.pw[wv][t - 1][0]);
+          f4 w[NHG];
+#pragma unroll
+          for (int hg = 0; hg < NHG; ++hg) w[hg] = *reinterpret_cast<const f4*>(&sm.pw[wv][t - 1][4 * hg]);
           const float code = (float)int4_value(cbv[u] >> ((ea & 1u) * 4u));
           const uint32_t c = chv[u] & (D - 1);
 #pragma unroll
           for (int i = 0; i < G; ++i)
-            atomicAdd(reinterpret_cast<unsigned long long*>(&sm.racc[wv][i][c]), to_fixed(w[i] * code, scale));
+            atomicAdd(reinterpret_cast<unsigned long long*>(&sm.racc[wv][i][c]),
+                      to_fixed(w[i >> 2][i & 3] * code, scale));
         }
       }
     }
@@ -866,7 +977,9 @@ template <int RB, int G, bool RESID, bool SCORES, bool C8>
 __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   using C = TCfg<RB>;
   constexpr int NS = C::NS;
-  __shared__ TSmem<RB, RESID> sm;
+  constexpr int HG = TGrp<G>::HG;
+  static_assert(!C8 || HG == 4, "int8 coefficients: query groups of up to 4 heads");
+  __shared__ TSmem<RB, G, RESID> sm;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int grp = lane >> 4, col = lane & 15;
   const int slot = blockIdx.y;
@@ -930,7 +1043,7 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   const int j1 = ts.n > 1 ? ts.at(1) : j0;
   TFrags<RB, C8> fr{};                  // lanes past r_b never load values: keep them zero
   TMeta mc{}, mn{}, mnn{};
-  TEnt ec{}, en{};
+  TEnt<G> ec{}, en{};
   // q~ fragments, waves below NS only: wave w takes basis rows [16w, 16w+16)
   // on 16x16x32 MFMA, A = B^K rows (row = lane % 16, channels 32s + 8(lane/16)
   // + i), B = q (column = head lane % 16)
@@ -1032,9 +1145,9 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   // q~ as the A operand (row = head, repeated per 4 rows), scaled per head by
   // a power of two so its largest entry sits just under 2^14, split into fp16
   // hi + lo; the score of head i is scaled back by down[i]
-  TState<RB, C8> st;
+  TState<RB, G, C8> st;
   {
-    const int h = col & 3;
+    const int h = col & (HG - 1);
     float up = 1.0f;
 #pragma unroll
     for (int i = 0; i < HG; ++i) {
@@ -1067,8 +1180,16 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
         st.qlo[s][i] = (_Float16)(v - (float)hh);
       }
     }
+    if constexpr (HG == 8) {            // every wave writes the same bytes
 #pragma unroll
-    for (int b = 0; b < TState<RB, C8>::NACC; ++b) {
+      for (int s = 0; s < NS; ++s) {
+        sm.qa[0][s][lane] = st.qhi[s];
+        sm.qa[1][s][lane] = st.qlo[s];
+      }
+      wave_lds_fence();
+    }
+#pragma unroll
+    for (int b = 0; b < TState<RB, G, C8>::NACC; ++b) {
       st.acc_h[b] = f4{0.f, 0.f, 0.f, 0.f};
       st.acc_l[b] = f4{0.f, 0.f, 0.f, 0.f};
     }
@@ -1124,14 +1245,19 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
     }
   }
   if (lane < RB) {
-    f4 ah = st.acc_h[0], al = st.acc_l[0];
     if constexpr (C8) {                 // lane c keeps the pass of its coefficient block c / 16
+      f4 ah = st.acc_h[0], al = st.acc_l[0];
 #pragma unroll
-      for (int b = 1; b < TState<RB, C8>::NACC; ++b)
+      for (int b = 1; b < TState<RB, G, C8>::NACC; ++b)
         if ((lane >> 4) == b) { ah = st.acc_h[b]; al = st.acc_l[b]; }
-    }
 #pragma unroll
-    for (int i = 0; i < HG; ++i) sm.ep_a[wv][i][lane] = ah[i] + al[i];
+      for (int i = 0; i < 4; ++i) sm.ep_a[wv][i][lane] = ah[i] + al[i];
+    } else {                            // pair hg holds heads 4 hg .. 4 hg + 3
+#pragma unroll
+      for (int hg = 0; hg < TGrp<G>::NHG; ++hg)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sm.ep_a[wv][4 * hg + i][lane] = st.acc_h[hg][i] + st.acc_l[hg][i];
+    }
   }
   __syncthreads();
   constexpr int ROW = D + RB;                 // r[d] then a~[r_b]
@@ -1180,6 +1306,9 @@ hipError_t launch_tl_g(int g, const SplitArgs& a, int n_work, hipStream_t s) {
     case 1: return launch_tl_t<RB, 1, R, S, C8>(a, n_work, s);
     case 2: return launch_tl_t<RB, 2, R, S, C8>(a, n_work, s);
     case 4: return launch_tl_t<RB, 4, R, S, C8>(a, n_work, s);
+    case 8:
+      if constexpr (!C8) return launch_tl_t<RB, 8, R, S, C8>(a, n_work, s);
+      break;
   }
   return hipErrorInvalidValue;
 }
@@ -1204,6 +1333,7 @@ hipError_t launch_merge_tl_rb(int g, const SplitArgs& a, hipStream_t s) {
     case 1: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 1>), grid, dim3(kWmThreads), 0, s, a); break;
     case 2: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 2>), grid, dim3(kWmThreads), 0, s, a); break;
     case 4: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 4>), grid, dim3(kWmThreads), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 8>), grid, dim3(kWmThreads), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -1212,8 +1342,10 @@ hipError_t launch_merge_tl_rb(int g, const SplitArgs& a, hipStream_t s) {
 bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t res_stride) {
   // every slab must stay below 2^31 bytes for the 32-bit buffer offsets
   const int64_t lim = (int64_t)1 << 31;
-  return (g == 1 || g == 2 || g == 4) && rb % 16 == 0 && rb >= 16 && rb <= 64 && max_level <= kMaxRank &&
-         (tokens + 64) * rb * 2 < lim && (tokens + 64) * 4 < lim && res_stride < lim;
+  const bool group = ((g == 1 || g == 2 || g == 4) && max_level <= TGrp<4>::MR) ||
+                     (g == 8 && max_level <= TGrp<8>::MR);
+  return group && rb % 16 == 0 && rb >= 16 && rb <= 64 && (tokens + 64) * rb * 2 < lim && (tokens + 64) * 4 < lim &&
+         res_stride < lim;
 }
 
 hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {

@@ -71,6 +71,7 @@ hipError_t launch_features(int g, const FeatArgs& a, hipStream_t s) {
     case 1: hipLaunchKernelGGL(features_kernel<1>, grid, dim3(kFT), 0, s, a); break;
     case 2: hipLaunchKernelGGL(features_kernel<2>, grid, dim3(kFT), 0, s, a); break;
     case 4: hipLaunchKernelGGL(features_kernel<4>, grid, dim3(kFT), 0, s, a); break;
+    case 8: hipLaunchKernelGGL(features_kernel<8>, grid, dim3(kFT), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

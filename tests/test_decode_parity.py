@@ -45,6 +45,14 @@ SMALL = [
     # token-lane merge over more chunks than one load round covers (79 and 47 partials)
     ("rb48-g4-many-chunks", 48, 4, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), [5000, 37], 64, "bf16"),
     ("rb64-g2-many-chunks", 64, 2, (0, 8, 16), (0.8, 0.15, 0.05), [3000], 64, "f16"),
+    # token-lane kernel, groups of 8 heads (ranks to 32): ragged tails, empty
+    # sequences, every basis rank, rank-32-heavy tiles (past the preloaded
+    # value-entry batches and up to the 2048-entry map), and many chunks
+    ("rb32-g8-tails", 32, 8, (0, 2, 4, 8, 16, 32), (0.4, 0.2, 0.15, 0.1, 0.1, 0.05), [1, 63, 65, 300, 0], 64, "f16"),
+    ("rb16-g8", 16, 8, (0, 8), (0.5, 0.5), [777], 128, "bf16"),
+    ("rb48-g8-five-levels", 48, 8, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), [2000, 33], 0, "bf16"),
+    ("rb64-g8-rank32-heavy", 64, 8, (0, 32), (0.1, 0.9), [1500, 64], 256, "bf16"),
+    ("rb64-g8-many-chunks", 64, 8, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), [5000, 37], 64, "bf16"),
 ]
 
 
@@ -101,28 +109,29 @@ def _needles(host, layer, n_needles, seed, scale_q=1.0):
                 host.coef_k[layer, h, t] = (lam * dirn).astype(np.float16)
 
 
-def test_needles_and_peaked_queries():
+@pytest.mark.parametrize("G", [4, 8])
+def test_needles_and_peaked_queries(G):
     torch = torch_gpu()
-    w = _Fixed(Workload(name="needles", batch=2, n_layers=2, window=2, n_kv_heads=2, n_q_heads=8,
+    w = _Fixed(Workload(name="needles", batch=2, n_layers=2, window=2, n_kv_heads=2, n_q_heads=2 * G,
                         head_dim=128, context=9000, basis_rank=48, levels=(0, 4, 8, 16),
                         probs=(0.75, 0.12, 0.08, 0.05), q_dtype="bf16", seed=77), [9000, 5000])
     host = generate(w, threads=4)
     _needles(host, 0, 4, seed=5)
     dc = device_cache(host, split_tokens=512)
     pairs = [(b, h) for b in range(2) for h in range(2)]
-    announce("decode needles layer 0")
+    announce(f"decode needles G={G} layer 0")
     out = dc.decode(0).cpu().numpy()
     ref, probs = oracle.decode(host, 0, with_probs=True)
     top = max(p.max() for p in probs.values())
     assert top > 0.1, f"needle setup did not concentrate the softmax (max p {top:.3f})"
-    compare(out, ref, pairs, 4, "needles")
+    compare(out, ref, pairs, G, f"needles G={G}")
     # peaked: query scaled by 32 (bf16 scaling by a power of two is exact)
     q = dc.q[1].float() * 32
     q = q.to(torch.bfloat16)
-    announce("decode peaked layer 1")
+    announce(f"decode peaked G={G} layer 1")
     out = dc.decode(1, q=q).cpu().numpy()
     ref = oracle.decode(host, 1, q=oracle.q_to_f64(host.q_bits[1], "bf16") * 32)
-    compare(out, ref, pairs, 4, "peaked q x32")
+    compare(out, ref, pairs, G, f"peaked q x32 G={G}")
 
 
 def test_softmax_scale_argument():

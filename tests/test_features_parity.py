@@ -33,6 +33,7 @@ CASES = [
     ("rb48-g2-one-seq", 48, 2, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), [3000], 0),
     ("rb16-g1-short", 16, 1, (0, 2), (0.6, 0.4), [1, 63, 65], 64),
     ("rb64-g4-no-residual", 64, 4, (0,), (1.0,), [1500, 37], 128),
+    ("rb64-g8-ranks-to-32", 64, 8, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), [0, 900, 2100], 256),
 ]
 
 

@@ -65,7 +65,7 @@ def test_int8_refused_where_unsupported():
                  context=300, basis_rank=32, levels=(0, 8), probs=(0.5, 0.5), q_dtype="bf16", seed=3,
                  coef_format="int8")
     host = generate(w, threads=4)
-    dc = device_cache(host)                    # groups of 8: off the token-lane path
+    dc = device_cache(host)                    # int8 is built for groups of up to 4 heads
     with pytest.raises(DwkvError) as e:
         dc.decode(0)
     assert e.value.status == 3
