@@ -146,8 +146,11 @@ int32_t dwkv_split_tokens(const dwkv_dims* dims);
 size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe);
 
 /* Kernel launches one dwkv_decode call enqueues for these dims (2: the
- * split-K pass and the merge; 3 with a probe pass), or -1 when the dims or
- * probe are invalid.  probe may be NULL. */
+ * split-K pass and the merge; with a probe, 3 on the general kernel -- the
+ * reference pass is added and one merge covers both -- and 4 on the
+ * token-lane kernel, whose merge is followed by a small merge of the probed
+ * heads' reference partials), or -1 when the dims or probe are invalid.
+ * probe may be NULL. */
 int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe);
 
 /* Per-layer decode attention over the factorized cache (Eq. 1 folded into the
@@ -163,7 +166,8 @@ int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe);
  *   workspace:>= dwkv_workspace_bytes(dims, probe) bytes of device memory;
  *             contents need no initialisation and are clobbered; calls
  *             sharing it must be ordered (same stream).
- * Launches the split-K kernel(s) (two with a probe) and one merge kernel.
+ * Launches the split-K kernel(s) (two with a probe) and the merge kernel(s)
+ * (dwkv_decode_launches gives the count).
  * Returns DWKV_OK once enqueued. */
 dwkv_status dwkv_decode(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
                         const void* q, int32_t q_type, float sm_scale, float* out,

@@ -204,7 +204,8 @@ size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe) {
 
 int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe) {
   if (check_dims(dims) != DWKV_OK || check_probe(dims, probe) != DWKV_OK) return -1;
-  return probe ? 3 : 2;
+  if (!probe) return 2;
+  return uses_token_lane(dims) ? 4 : 3;
 }
 
 }  // extern "C"
@@ -325,7 +326,8 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   if (!aligned16(out) || !aligned16(c->basis)) return DWKV_E_ALIGN;
   const WsLayout wl = ws_layout(d, probe);
   char* ws = static_cast<char*>(workspace);
-  if (!probe && uses_token_lane(d)) {
+  const bool tl = uses_token_lane(d);
+  if (tl) {
     SplitArgs a;
     std::memset(&a, 0, sizeof(a));
     const int64_t Hk = d->n_kv_heads, M = d->n_layers / d->window, m = layer / d->window;
@@ -343,7 +345,10 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
     for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
     a.wt = work_table(d, a.split);
     a.mstats = mstats;
-    return hip_status(launch_merge_tl(d->basis_rank, d->n_q_heads / d->n_kv_heads, a, s));
+    const hipError_t e = launch_merge_tl(d->basis_rank, d->n_q_heads / d->n_kv_heads, a, s);
+    // with a probe, a second small launch merges the reference partials of
+    // the probed heads and evaluates Eq. 3 against the rows just written
+    if (e != hipSuccess || !probe) return hip_status(e);
   }
   MergeArgs mg;
   std::memset(&mg, 0, sizeof(mg));
@@ -372,7 +377,11 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   mg.ref_wt = work_table(d, mg.ref_split);
   for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) mg.probe_slot_of_kv[h] = -1;
   if (probe)
-    for (int i = 0; i < probe->n_heads; ++i) mg.probe_slot_of_kv[probe->kv_heads_host[i]] = i;
+    for (int i = 0; i < probe->n_heads; ++i) {
+      mg.probe_slot_of_kv[probe->kv_heads_host[i]] = i;
+      mg.kv_of_probe[i] = probe->kv_heads_host[i];
+    }
+  mg.probe_only = tl ? 1 : 0;
   return hip_status(launch_merge(mg, s));
 }
 

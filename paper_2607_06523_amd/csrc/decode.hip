@@ -818,9 +818,11 @@ struct Merged {
   f4 x, y;
 };
 
+template <int NT = kMergeThreads>
 __device__ __forceinline__ Merged merge_rows(const float* part, int64_t row0, int64_t row_step, int ns,
                                              int stride, int m_off, int ncols, float* red_m, float* red_l,
                                              f4* red_o) {
+  constexpr int kMergeGroups = NT / (D / 4);
   const int tid = threadIdx.x, c4 = tid % (D / 4), sg = tid / (D / 4);
   const bool two = D + 4 * c4 < ncols;
   const f4 z4 = f4{0.f, 0.f, 0.f, 0.f};
@@ -1005,6 +1007,52 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   }
 }
 
+// Probe merge after the token-lane merge: one 1024-thread workgroup per
+// (probed query head, sequence) merges the reference partials (32 split
+// groups of 8, so that one round of loads covers up to 256 partials) in a
+// fixed order, reads the output row the token-lane merge wrote, and evaluates
+// Eq. 3.
+constexpr int kProbeThreads = 1024;
+
+__global__ __launch_bounds__(kProbeThreads) void probe_merge_kernel(const MergeArgs a) {
+  constexpr int NG = kProbeThreads / (D / 4);
+  __shared__ float red_m[NG], red_l[NG];
+  __shared__ f4 red_o[kProbeThreads];
+  __shared__ float red2[2][kProbeThreads / 64];
+  const int b = blockIdx.y, tid = threadIdx.x;
+  const int G = a.n_q_heads / a.n_kv_heads;
+  const int sl = blockIdx.x / G, g = blockIdx.x % G;
+  const int hq = a.kv_of_probe[sl] * G + g;
+  const int c4 = tid % (D / 4), sg = tid / (D / 4);
+  const f4 o = reinterpret_cast<const f4*>(a.out + ((int64_t)b * a.n_q_heads + hq) * D)[c4];
+  int base_r, ns_r;
+  seq_work(a.ref_wt, a.cu, a.ref_split, b, base_r, ns_r);
+  const f4 r = merge_rows<kProbeThreads>(a.part_ref, (int64_t)base_r * a.n_probe * G + sl * G + g,
+                                         (int64_t)a.n_probe * G, ns_r, kPartStride, D, D, red_m, red_l, red_o).x;
+  const int64_t col = (int64_t)b * a.n_probe * G + sl * G + g;
+  float d2 = 0.f, r2 = 0.f;
+  if (sg == 0) {
+    if (a.out_ref) reinterpret_cast<f4*>(a.out_ref + col * D)[c4] = r;
+    const float dx = r.x - o.x, dy = r.y - o.y, dz = r.z - o.z, dw = r.w - o.w;
+    d2 = dx * dx + dy * dy + dz * dz + dw * dw;
+    r2 = r.x * r.x + r.y * r.y + r.z * r.z + r.w * r.w;
+  }
+  for (int o2 = 32; o2 > 0; o2 >>= 1) {
+    d2 += __shfl_xor(d2, o2);
+    r2 += __shfl_xor(r2, o2);
+  }
+  if ((tid & 63) == 0) {
+    red2[0][tid >> 6] = d2;
+    red2[1][tid >> 6] = r2;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float sd = 0.f, sr = 0.f;
+    for (int i = 0; i < kProbeThreads / 64; ++i) { sd += red2[0][i]; sr += red2[1][i]; }
+    a.err[col] = sqrtf(sd) / (sqrtf(sr) + a.eps);
+  }
+}
+
 template <int RB, int G, bool R, bool I>
 hipError_t launch_t(const SplitArgs& a, int n_work, hipStream_t s) {
   hipLaunchKernelGGL((split_kernel<RB, G, R, I>), dim3(n_work, a.n_slots), dim3(kThreads), 0, s, a);
@@ -1047,6 +1095,11 @@ hipError_t launch_split(int rb, int g, bool resid, bool ident, const SplitArgs& 
 }
 
 hipError_t launch_merge(const MergeArgs& a, hipStream_t s) {
+  if (a.probe_only) {
+    const int g = a.n_q_heads / a.n_kv_heads;
+    hipLaunchKernelGGL(probe_merge_kernel, dim3(a.n_probe * g, a.batch), dim3(kProbeThreads), 0, s, a);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(merge_kernel, dim3(a.n_q_heads, a.batch), dim3(kMergeThreads), 0, s, a);
   return hipGetLastError();
 }

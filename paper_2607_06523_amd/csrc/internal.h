@@ -132,6 +132,11 @@ struct MergeArgs {
   int64_t basis_b_stride;
   int32_t ref_split;           // the probe pass's chunk size and work split
   WorkTable ref_wt;
+  // probe_only: grid (n_probe * G, B), one workgroup per probed query head;
+  // the output rows are already in `out` (written by the token-lane merge),
+  // only the reference partials are merged and Eq. 3 evaluated against them
+  int32_t probe_only;
+  int32_t kv_of_probe[DWKV_MAX_PROBE_HEADS];
 };
 
 // Makes the kernel-argument values the whole split kernel needs live in scalar

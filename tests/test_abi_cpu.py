@@ -138,7 +138,8 @@ def up256(n):
 
 def test_workspace_and_split_plan(lib):
     # automatic chunk: ceil(T*Hkv/n) rounded up to 256, clamped to [256, 8192], with n = 256
-    # workgroups for the token-lane kernel (groups of 4, r_b 32, ranks <= 16) and 512 otherwise
+    # workgroups for the token-lane kernel (groups of up to 4 with ranks <= 16, groups of 8 with
+    # ranks <= 32; r_b <= 64) and 512 otherwise
     for T, Hk, want in [(4096, 2, 256), (32768, 8, 1024), (65536, 8, 2048), (262144, 8, 8192),
                         (10**6, 8, 8192)]:
         d, keep = dims(cu_seqlens_host=[0, T], batch=1, total_tokens=T, n_kv_heads=Hk, n_q_heads=4 * Hk,
@@ -148,17 +149,20 @@ def test_workspace_and_split_plan(lib):
         # token-lane partials (group of 4, r_b 32, ranks <= 16): d + 64 + 4 floats
         assert lib.dwkv_workspace_bytes(C.byref(d), None) == up256(n_work * Hk * 4 * 196 * 4)
     d, keep = dims(cu_seqlens_host=[0, 65536], batch=1, total_tokens=65536, n_kv_heads=8, n_q_heads=64,
+                   res_stride=65536 * 16 + 512, levels=(0, 8, 32))
+    assert lib.dwkv_split_tokens(C.byref(d)) == 2048      # group of 8, ranks <= 32: token-lane kernel
+    d, keep = dims(cu_seqlens_host=[0, 65536], batch=1, total_tokens=65536, n_kv_heads=8, n_q_heads=128,
                    res_stride=65536 * 16 + 512)
-    assert lib.dwkv_split_tokens(C.byref(d)) == 1024      # group of 8: general kernel
+    assert lib.dwkv_split_tokens(C.byref(d)) == 1024      # group of 16: general kernel
     d, keep = dims(split_tokens=640)
     assert lib.dwkv_split_tokens(C.byref(d)) == 640
     # ragged: per-sequence chunk counts, empty sequences contribute none
     d, keep = dims(batch=3, cu_seqlens_host=[0, 700, 700, 1300], total_tokens=1300, split_tokens=256)
     assert lib.dwkv_workspace_bytes(C.byref(d), None) == up256((3 + 3) * 2 * 4 * 196 * 4)
-    # general kernel partials (group of 8): d + 4 floats
+    # general kernel partials (group of 16): d + 4 floats
     d, keep = dims(batch=3, cu_seqlens_host=[0, 700, 700, 1300], total_tokens=1300, split_tokens=256,
-                   n_q_heads=16)
-    assert lib.dwkv_workspace_bytes(C.byref(d), None) == up256((3 + 3) * 2 * 8 * 132 * 4)
+                   n_q_heads=32)
+    assert lib.dwkv_workspace_bytes(C.byref(d), None) == up256((3 + 3) * 2 * 16 * 132 * 4)
 
 
 def test_route_and_map_argument_checks(lib):
@@ -178,14 +182,17 @@ def test_route_and_map_argument_checks(lib):
 
 
 def test_decode_launch_count(lib):
-    """The split-K pass and the merge; a probe adds its reference pass."""
+    """The split-K pass and the merge; a probe adds its reference pass, and on
+    the token-lane kernel a small merge of the probed heads after the wide one."""
     from paper_2607_06523_amd import binding
     for kw in (dict(), dict(n_q_heads=16), dict(batch=3, cu_seqlens_host=[0, 700, 700, 1300], total_tokens=1300)):
         d, keep = dims(**kw)
         assert lib.dwkv_decode_launches(C.byref(d), None) == 2
-    d, keep = dims()
     heads = np.array([1], dtype=np.int32)
     p = binding.Probe(1, heads.ctypes.data_as(C.POINTER(C.c_int32)), FAKE, FAKE, 1e-6, FAKE, 0)
+    d, keep = dims()                                  # G = 4, r_b 32: token-lane kernel
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 4
+    d, keep = dims(n_q_heads=32)                      # G = 16: general kernel
     assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3
     d, keep = dims(n_q_heads=7)
     assert lib.dwkv_decode_launches(C.byref(d), None) == -1
@@ -254,7 +261,7 @@ def test_features_argument_checks(lib):
     base = lib.dwkv_workspace_bytes(C.byref(d), None)
     need = lib.dwkv_features_workspace_bytes(C.byref(d))
     assert need == base + up256(8 * 3000 * 4) + up256(2 * 8 * 2 * 4)   # scores, then (m*, l*) per (b, hq)
-    d8, keep8 = dims(n_q_heads=16)            # groups of 8: general kernel, no features
+    d8, keep8 = dims(n_q_heads=32)            # groups of 16: general kernel, no features
     assert lib.dwkv_features_workspace_bytes(C.byref(d8)) == 0
     c = binding.Cache(*([FAKE] * 8))
     f = lambda dd=d, **kw: lib.dwkv_decode_features(C.byref(dd), C.byref(c), kw.get("layer", 0), FAKE, 0, 0.0,

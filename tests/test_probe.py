@@ -34,26 +34,54 @@ def _run_probe(dc, layer, heads, K, V, eps=1e-6):
     return out.cpu().numpy(), err.cpu().numpy(), out_ref.cpu().numpy()
 
 
-def test_probe_matches_oracle():
+class _Fixed:
+    def __init__(self, w, lengths):
+        self._w, self._lengths = w, list(lengths)
+
+    def __getattr__(self, k):
+        if k.startswith("_"):
+            raise AttributeError(k)
+        return getattr(self._w, k)
+
+    def seqlens(self):
+        return list(self._lengths)
+
+
+PROBE_CASES = [
+    # name, G, r_b, levels, probs, lengths (None: ragged draw), split
+    # general kernel (ranks to 32 at G = 4): one merge covers outputs and probe
+    ("general-g4-ranks32", 4, 64, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), None, 512),
+    # token-lane kernels: the wide merge, then the probe merge of the probed heads
+    ("tl-g4", 4, 48, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), None, 512),
+    ("tl-g8-empty-seq", 8, 64, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), [0, 2100, 1700], 256),
+]
+
+
+@pytest.mark.parametrize("case", PROBE_CASES, ids=[c[0] for c in PROBE_CASES])
+def test_probe_matches_oracle(case):
     torch_gpu()
-    w = Workload(name="probe", batch=2, n_layers=2, window=2, n_kv_heads=4, n_q_heads=16,
-                 head_dim=128, context=3000, basis_rank=64, levels=(0, 4, 8, 16, 32),
-                 probs=(0.7, 0.12, 0.1, 0.06, 0.02), q_dtype="bf16", seed=55, ragged=(1500, 3000))
+    name, G, rb, levels, probs, lengths, split = case
+    w = Workload(name="probe-" + name, batch=2 if lengths is None else len(lengths), n_layers=2, window=2,
+                 n_kv_heads=4, n_q_heads=4 * G, head_dim=128, context=3000, basis_rank=rb, levels=levels,
+                 probs=probs, q_dtype="bf16", seed=55, ragged=(1500, 3000))
+    if lengths is not None:
+        w = _Fixed(w, lengths)
     host = generate(w, threads=4)
-    dc = device_cache(host, split_tokens=512)
+    dc = device_cache(host, split_tokens=split)
     heads = [3, 0, 2]
     K, V = _refs(host, 1, heads, 0.05, seed=3)
-    announce("probe layer 1, heads 3,0,2")
+    announce(f"probe {name} layer 1, heads 3,0,2")
     out, err, out_ref = _run_probe(dc, 1, heads, K, V)
     e_ref = oracle.probe(host, 1, heads, K, V)
     assert np.abs(err - e_ref).max() <= 1e-4 + 1e-3 * np.abs(e_ref).max(), (err, e_ref)
-    assert e_ref.min() > 0.01, "noise should give a visible probe error"
+    nonempty = [b for b in range(host.batch) if host.cu_seqlens[b + 1] > host.cu_seqlens[b]]
+    assert e_ref[nonempty].min() > 0.01, "noise should give a visible probe error"
     # the compressed output is unchanged by probing
-    compare(out, oracle.decode(host, 1), [(b, h) for b in range(2) for h in range(4)], 4, "probe out")
+    compare(out, oracle.decode(host, 1), [(b, h) for b in range(host.batch) for h in range(4)], G,
+            f"probe {name} out")
     # the reference output is plain attention over the dense reference cache
-    G = 4
     for i, h in enumerate(heads):
-        for b in range(2):
+        for b in nonempty:
             t0, t1 = int(host.cu_seqlens[b]), int(host.cu_seqlens[b + 1])
             q = oracle.q_to_f64(host.q_bits[1], "bf16")[b, h * G:(h + 1) * G]
             o, _ = oracle.attention(q, K[i, t0:t1].astype(np.float64), V[i, t0:t1].astype(np.float64),
