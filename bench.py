@@ -431,6 +431,9 @@ def main():
     ap.add_argument("--variant", default="full", choices=["full", "bases-only"],
                     help="bases-only: every routed residual rank 0 (shared bases only)")
     ap.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
+    ap.add_argument("--probe-heads", type=int, default=-1,
+                    help="KV heads probed (Eq. 3) in every layer of the timed step, each layer with its own "
+                         "fp16 reference; -1 = the workload's setting (one head when it probes every layer)")
     ap.add_argument("--cpu-pairs", type=int, default=0, help="slabs to time on the CPU (0 = all)")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -471,13 +474,29 @@ def main():
     dc = DeviceCache(host, split_tokens=args.split)
     L = host.n_layers
     stream = torch.cuda.current_stream()
-    ws = dc.workspace()
     outs = [torch.empty((host.batch, host.n_q_heads, host.head_dim), dtype=torch.float32, device="cuda")
             for _ in range(L)]
+    n_probe = args.probe_heads if args.probe_heads >= 0 else (1 if getattr(wl, "probe", False) else 0)
+    probes = errs = None
+    if n_probe > 0:
+        # one synthetic fp16 reference per layer for the first n_probe KV heads
+        from paper_2607_06523_amd import ProbeRef
+        T, d = host.total_tokens, host.head_dim
+        T16 = -(-T // 16) * 16
+        gen = torch.Generator(device="cuda").manual_seed(7)
+        probes = [ProbeRef(list(range(n_probe)), torch.randn((n_probe, T, d), device="cuda", generator=gen).half(),
+                           torch.randn((n_probe, T16 // 16, d, 16), device="cuda", generator=gen).half())
+                  for _ in range(L)]
+        errs = [torch.empty((host.batch, n_probe * wl.group), dtype=torch.float32, device="cuda") for _ in range(L)]
+        log(f"[bench] probe: {n_probe} KV head(s) in every layer, {len(probes)} references")
+    ws = dc.workspace(probes[0] if probes else None)
 
     def step():
         for l in range(L):
-            dc.decode(l, out=outs[l], workspace=ws)
+            if probes:
+                dc.decode(l, out=outs[l], workspace=ws, probe=probes[l], err=errs[l], with_ref=False)
+            else:
+                dc.decode(l, out=outs[l], workspace=ws)
 
     if args.copy_calib_mib > 0:
         n = args.copy_calib_mib * (1 << 20) // 4
@@ -510,7 +529,8 @@ def main():
     # dominant one) on its own without an event between every pair of launches.
     ev_step = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     ev_calls = [torch.cuda.Event(enable_timing=True) for _ in range(3)] if graph is None else None
-    ws_layer = [dc.new_workspace() for _ in range(L)] if graph is None else None
+    ws_layer = ([dc.new_workspace(probes[0] if probes else None) for _ in range(L)]
+                if graph is None else None)
     torch.cuda.synchronize()
     ev_step[0].record(stream)
     wall0 = time.perf_counter()
@@ -520,10 +540,12 @@ def main():
         elif k == args.steps - 1:
             ev_calls[0].record(stream)
             for l in range(L):
-                dc.decode_partials(l, workspace=ws_layer[l])
+                dc.decode_partials(l, workspace=ws_layer[l], probe=probes[l] if probes else None,
+                                   err=errs[l] if probes else None)
             ev_calls[1].record(stream)
             for l in range(L):
-                dc.decode_merge(l, out=outs[l], workspace=ws_layer[l])
+                dc.decode_merge(l, out=outs[l], workspace=ws_layer[l], probe=probes[l] if probes else None,
+                                err=errs[l] if probes else None)
             ev_calls[2].record(stream)
         else:
             step()
@@ -539,6 +561,10 @@ def main():
         merge_ms = ev_calls[1].elapsed_time(ev_calls[2]) / L
 
     bytes_layer = algorithmic_bytes_per_layer(host)
+    probe_bytes_layer = 0.0
+    if probes:       # the dense fp16 reference keys and values of the probed heads, read once per layer
+        probe_bytes_layer = float(n_probe * host.total_tokens * host.head_dim * 2 * 2)
+        bytes_layer = [b + probe_bytes_layer for b in bytes_layer]
     bytes_step = float(sum(bytes_layer))
     tok_s = host.batch / (ms_per_step / 1e3)
     step_gbps = bytes_step / (ms_per_step / 1e3) / 1e9
@@ -573,7 +599,11 @@ def main():
                    "graph": bool(graph is not None)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "kernel": "split-K partials pass (the dominant kernel: tl_kernel at this workload)",
+                     "kernel": ("split-K partials pass (the dominant kernel: "
+                                + ("tl_kernel" if dc.uses_token_lane else "split_kernel") + " at this workload)"
+                                if not probes else
+                                "split-K phase of the probed step: the factorized pass and the probe's dense "
+                                "reference pass, over both passes' bytes"),
                      "measured_ceiling": ceiling["gbps"], "frac_of_measured_ceiling": round(achieved / ceiling["gbps"], 4),
                      "whole_step": {"achieved": round(step_gbps, 1), "frac": round(step_gbps / HBM_PEAK_GBPS, 4),
                                     "note": "algorithmic bytes of all L per-layer calls / the whole step's time "
@@ -585,7 +615,11 @@ def main():
         "launches_per_layer": dc.decode_launches,
         "split_kernel_ms": round(avg_split_ms, 5),
         "merge_kernel_ms": round(float(merge_ms), 5) if merge_ms is not None else None,
-        "compression_vs_fp16": round(dense_fp16_bytes_per_layer(host) / np.mean(bytes_layer), 3),
+        "compression_vs_fp16": round(dense_fp16_bytes_per_layer(host) / (np.mean(bytes_layer) - probe_bytes_layer), 3),
+        "probe": ({"kv_heads_per_layer": n_probe, "reference_bytes_per_layer": int(probe_bytes_layer),
+                   "note": "Eq. 3 probe in every layer: dense fp16 reference pass of the probed heads plus the "
+                           "probe merge; its bytes are included in bytes_per_layer_call and the roofline"}
+                  if probes else None),
         "kv_token_layers_per_s": round(host.total_tokens * L / (ms_per_step / 1e3), 1),
         "wall_s_timed": round(wall, 3),
     }

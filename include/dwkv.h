@@ -141,6 +141,11 @@ const char* dwkv_status_str(dwkv_status s);
  * choice when dims->split_tokens is 0), or -1 when the dims are invalid. */
 int32_t dwkv_split_tokens(const dwkv_dims* dims);
 
+/* Which split-K kernel dwkv_decode runs for these dims: 1 the token-lane
+ * kernel (query groups of 1, 2 or 4 heads with ranks up to 16, or 8 heads with
+ * ranks up to 32; r_b up to 64), 0 the general kernel, -1 invalid dims. */
+int32_t dwkv_decode_kernel(const dwkv_dims* dims);
+
 /* Bytes of device workspace dwkv_decode needs (0 when dims are invalid).
  * probe may be NULL. */
 size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe);

@@ -134,6 +134,11 @@ class DeviceCache:
         return int(self.lib.dwkv_split_tokens(C.byref(self.dims)))
 
     @property
+    def uses_token_lane(self) -> bool:
+        """True when dwkv_decode runs the token-lane split kernel for this cache."""
+        return int(self.lib.dwkv_decode_kernel(C.byref(self.dims))) == 1
+
+    @property
     def decode_launches(self) -> int:
         """Kernel launches of one decode call without a probe (the split-K pass and the merge)."""
         return int(self.lib.dwkv_decode_launches(C.byref(self.dims), None))
@@ -177,9 +182,9 @@ class DeviceCache:
 
     # -- calls -----------------------------------------------------------------------
     def decode(self, layer: int, q=None, sm_scale: float | None = None, probe: ProbeRef | None = None,
-               out=None, workspace=None, with_ref: bool = True):
+               out=None, workspace=None, with_ref: bool = True, err=None):
         """Per-layer decode attention; returns out [B,Hq,d] fp32, or
-        (out, err [B, n*G], out_ref [B, n*G, d]) with a probe."""
+        (out, err [B, n*G], out_ref [B, n*G, d]) with a probe (err may be given)."""
         torch = self.torch
         if q is None:
             q = self.q[layer]
@@ -190,10 +195,11 @@ class DeviceCache:
         if out is None:
             out = torch.empty((B, Hq, d), dtype=torch.float32, device=self.device)
         G = Hq // self.n_kv_heads
-        err = out_ref = None
+        out_ref = None
         if probe is not None:
             n = len(probe.kv_heads)
-            err = torch.empty((B, n * G), dtype=torch.float32, device=self.device)
+            if err is None:
+                err = torch.empty((B, n * G), dtype=torch.float32, device=self.device)
             out_ref = torch.empty((B, n * G, d), dtype=torch.float32, device=self.device) if with_ref else None
         p, keep = self._probe_struct(probe, err, out_ref)
         ws = workspace if workspace is not None else self.workspace(probe)
@@ -219,26 +225,32 @@ class DeviceCache:
         binding.check(st, "dwkv_decode_noalloc")
         return out
 
-    def decode_partials(self, layer: int, q=None, sm_scale: float | None = None, workspace=None):
-        """First half of decode: the split-K pass (no probe); dwkv_decode_merge finishes it."""
+    def decode_partials(self, layer: int, q=None, sm_scale: float | None = None, workspace=None,
+                        probe: ProbeRef | None = None, err=None):
+        """First half of decode: the split-K pass(es); dwkv_decode_merge finishes it
+        (with the same probe and err)."""
         torch = self.torch
         if q is None:
             q = self.q[layer]
         qt = F16 if q.dtype == torch.float16 else BF16
-        ws = workspace if workspace is not None else self.workspace(None)
+        p, keep = self._probe_struct(probe, err, None)
+        ws = workspace if workspace is not None else self.workspace(probe)
         st = self.lib.dwkv_decode_partials(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(q), qt,
-                                           float(sm_scale or 0.0), None, _ptr(ws), ws.numel(),
-                                           _stream(torch, self.device))
+                                           float(sm_scale or 0.0), C.byref(p) if p is not None else None,
+                                           _ptr(ws), ws.numel(), _stream(torch, self.device))
         binding.check(st, "dwkv_decode_partials")
 
-    def decode_merge(self, layer: int, out=None, workspace=None):
-        """Second half of decode: merges the split partials of `layer` into out [B,Hq,d]."""
+    def decode_merge(self, layer: int, out=None, workspace=None, probe: ProbeRef | None = None, err=None):
+        """Second half of decode: merges the split partials of `layer` into out [B,Hq,d]
+        (and, with a probe, writes err [B, n*G])."""
         torch = self.torch
         if out is None:
             out = torch.empty((self.batch, self.n_q_heads, self.head_dim), dtype=torch.float32, device=self.device)
-        ws = workspace if workspace is not None else self.workspace(None)
-        st = self.lib.dwkv_decode_merge(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(out), None,
-                                        _ptr(ws), ws.numel(), _stream(torch, self.device))
+        p, keep = self._probe_struct(probe, err, None)
+        ws = workspace if workspace is not None else self.workspace(probe)
+        st = self.lib.dwkv_decode_merge(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(out),
+                                        C.byref(p) if p is not None else None, _ptr(ws), ws.numel(),
+                                        _stream(torch, self.device))
         binding.check(st, "dwkv_decode_merge")
         return out
 

@@ -58,7 +58,7 @@ class Probe(C.Structure):
                 ("err", C.c_void_p), ("out_ref", C.c_void_p)]
 
 
-EXPORTS = ["dwkv_abi_version", "dwkv_status_str", "dwkv_split_tokens", "dwkv_workspace_bytes",
+EXPORTS = ["dwkv_abi_version", "dwkv_status_str", "dwkv_split_tokens", "dwkv_decode_kernel", "dwkv_workspace_bytes",
            "dwkv_decode_launches", "dwkv_decode", "dwkv_decode_partials", "dwkv_decode_merge",
            "dwkv_static_scratch_bytes", "dwkv_decode_noalloc", "dwkv_route_workspace_bytes", "dwkv_route",
            "dwkv_route_range", "dwkv_route_budget_workspace_bytes", "dwkv_route_budget", "dwkv_compress", "dwkv_features_workspace_bytes", "dwkv_decode_features",
@@ -83,6 +83,8 @@ def load(path: str = LIB_PATH):
     lib.dwkv_status_str.argtypes = [C.c_int]
     lib.dwkv_split_tokens.restype = C.c_int32
     lib.dwkv_split_tokens.argtypes = [P(Dims)]
+    lib.dwkv_decode_kernel.restype = C.c_int32
+    lib.dwkv_decode_kernel.argtypes = [P(Dims)]
     lib.dwkv_workspace_bytes.restype = C.c_size_t
     lib.dwkv_workspace_bytes.argtypes = [P(Dims), P(Probe)]
     lib.dwkv_decode_launches.restype = C.c_int32

@@ -197,6 +197,11 @@ int32_t dwkv_split_tokens(const dwkv_dims* dims) {
   return plan_split(dims);
 }
 
+int32_t dwkv_decode_kernel(const dwkv_dims* dims) {
+  if (check_dims(dims) != DWKV_OK) return -1;
+  return uses_token_lane(dims) ? 1 : 0;
+}
+
 size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe) {
   if (check_dims(dims) != DWKV_OK || check_probe(dims, probe) != DWKV_OK) return 0;
   return ws_layout(dims, probe).total;

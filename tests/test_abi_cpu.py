@@ -391,3 +391,12 @@ def test_noalloc_refuses_beyond_static_scratch(lib):
                                  C.c_float(0.0), C.c_void_p(16), None, None)
     assert st == 8
     assert lib.dwkv_status_str(8) == b"needs more than the library's static scratch"
+
+
+def test_decode_kernel_query(lib):
+    """Which split kernel the plan picks: token-lane for groups of up to 4 with
+    ranks up to 16 and groups of 8 with ranks up to 32 (r_b up to 64)."""
+    for kw, want in [(dict(), 1), (dict(n_q_heads=16, levels=(0, 8, 32)), 1), (dict(levels=(0, 8, 32)), 0),
+                     (dict(n_q_heads=32), 0), (dict(basis_rank=80), 0), (dict(n_q_heads=7), -1)]:
+        d, keep = dims(**kw)
+        assert lib.dwkv_decode_kernel(C.byref(d)) == want, kw
