@@ -49,10 +49,10 @@ typedef enum dwkv_status {
   DWKV_E_UNSUPPORTED = 3, /* consistent but not built: head_dim != 128,
                              G = Hq/Hkv not in {1,2,4,8,16}, r_b not a multiple of
                              16 in [16,128], more than 8 levels, 32-bit offset
-                             overflow possible; int8 coefficients off the
-                             token-lane path (G <= 4, r_b <= 64, levels <= 16),
-                             with a probe, or in the calls that write or
-                             rebuild fp16 coefficients                            */
+                             overflow possible; int8 coefficients in a decode
+                             off the token-lane path for groups of up to 4
+                             (r_b <= 64, levels <= 16), with a probe, or in
+                             dwkv_materialize                                     */
   DWKV_E_WORKSPACE = 4,   /* workspace smaller than the *_workspace_bytes value    */
   DWKV_E_LAYOUT = 5,      /* dwkv_validate found a malformed cache                 */
   DWKV_E_HIP = 6,         /* a HIP runtime call or kernel launch failed            */
@@ -285,6 +285,16 @@ dwkv_status dwkv_route_budget(const dwkv_dims* dims, const float* phi, const flo
  *   res_scale = fp16(g * S) (0 for a rank-0 token); entries stored at
  *           [res_off[t], res_off[t+1]) ordered by descending |code|, then
  *           ascending channel.
+ * With dims->coef_format == DWKV_COEF_I8 the coefficient rows are written in
+ * the 8-bit blockwise form instead (Sec. 3): per token and block of 16
+ * coefficients [16 s, 16 s + 16), from the float32 projection A (not rounded
+ * to fp16),
+ *   S_s   = fp16(max_i |A_i| / 127),  code_i = round-half-even(A_i / S_s)
+ *           clamped to [-127, 127] (0 when S_s == 0)
+ * into coef_k / coef_v (int8 tiles) and coef_k_scale / coef_v_scale (the
+ * layouts dwkv_cache states), and the residual is taken against the rebuilt
+ * rows code_i * S_s; in the basis term of the residual each product is then
+ * rounded to float32 before it is added.
  * Arithmetic: float32, every product and sum rounded on its own; each sum runs
  * left to right over its contracted index (j = 0..d-1 for A_i, i = 0..r_b-1
  * for the basis term), starting from its first product; A is rounded to fp16
@@ -315,8 +325,8 @@ dwkv_status dwkv_residual_map(const dwkv_dims* dims, const dwkv_cache* cache, in
                               float* dense, void* stream);
 
 /* Bytes of device workspace dwkv_decode_features needs (0 when the dims are
- * invalid or the shape is not on the token-lane path: G = Hq/Hkv in {1, 2, 4},
- * r_b <= 64, levels <= 16). */
+ * invalid or the shape is not on the token-lane path: dwkv_decode_kernel
+ * returns 0). */
 size_t dwkv_features_workspace_bytes(const dwkv_dims* dims);
 
 /* dwkv_decode (no probe), plus the attention features the router reads
@@ -335,6 +345,25 @@ size_t dwkv_features_workspace_bytes(const dwkv_dims* dims);
 dwkv_status dwkv_decode_features(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
                                  const void* q, int32_t q_type, float sm_scale, float* out, float* phi,
                                  void* workspace, size_t ws_bytes, void* stream);
+
+/* The fourth router feature (Sec. 3: the attention-output reconstruction
+ * error from the previous probe interval, Eq. 3).  Eq. 3 yields one error per
+ * sequence and query head; the router scores tokens.  For every probed KV
+ * head h = kv_heads_host[i] and sequence b, with e the largest of
+ * err[b][i*G .. i*G + G-1] (over h's query heads):
+ *   phi[m][h][t][3] = fresh ? e : max(phi[m][h][t][3], e)
+ * for every packed token t of b, m = layer / window.  Call it once per probed
+ * layer of an interval, the first time with fresh = 1, so that the column
+ * holds the largest error over the window's probed layers; heads not probed
+ * keep their value, and columns 0-2 are untouched.
+ *   err:  device fp32 [B][n_heads * G], as dwkv_decode writes it for a probe
+ *         with the same kv_heads_host
+ *   phi:  device fp32 [M][Hkv][T][4], read and written
+ * One launch.  Argument errors (n_heads outside 1..min(Hkv, 64), repeated or
+ * out-of-range heads, layer out of range) return before anything is enqueued. */
+dwkv_status dwkv_probe_feature(const dwkv_dims* dims, int32_t layer, int32_t n_heads,
+                               const int32_t* kv_heads_host, const float* err, int32_t fresh,
+                               float* phi, void* stream);
 
 /* Bytes of device workspace dwkv_sketch_basis needs for a prefill of
  * n_tokens tokens (0 when invalid). */

@@ -24,6 +24,12 @@ Readings where the paper is silent (each listed in the design notes):
   stores scale 0.
 * Entry order inside a token: descending |code|, then ascending channel (the
   order the layout validator checks).
+* 8-bit blockwise coefficients (Sec. 3 stores A in that form; reading C7):
+  per token and block of 16 coefficients [16 s, 16 s + 16), the scale is
+  S_s = fp16(max_i |A_i| / 127) from the float32 projection (not the fp16
+  one), and code_i = round-half-even(A_i / S_s) clamped to [-127, 127] (0 when
+  S_s == 0).  The residual is then taken against the coefficients the decode
+  rebuilds, code_i * S_s (exact in float32).
 
 Precision.  The kept channels and the codes are integers decided by floating
 point, and the paper fixes no arithmetic for them.  Reading used here: single
@@ -53,22 +59,50 @@ def _sum_in_order(terms):
     return acc
 
 
-def project(x: np.ndarray, B: np.ndarray) -> np.ndarray:
+def project32(x: np.ndarray, B: np.ndarray) -> np.ndarray:
     """Coefficient rows A = x B^T for vectors x [n, d] against basis rows
     B [r_b, d] (fp16 values): float32 products summed over the d channels left
-    to right, rounded to fp16.  Returns float16 [n, r_b]."""
+    to right.  Returns float32 [n, r_b]."""
     x = np.asarray(x, dtype=np.float16).astype(np.float32)
     B = np.asarray(B, dtype=np.float16).astype(np.float32)
     terms = [x[:, j:j + 1] * B[None, :, j] for j in range(x.shape[1])]
-    return _sum_in_order(terms).astype(np.float16)
+    return _sum_in_order(terms)
 
 
-def residual(x: np.ndarray, B: np.ndarray, a16: np.ndarray) -> np.ndarray:
-    """r = x - A B in float32: the basis term of each channel summed over the
-    basis rows left to right, then subtracted from x.  Returns float32 [n, d]."""
+def project(x: np.ndarray, B: np.ndarray) -> np.ndarray:
+    """project32 rounded to fp16 (the fp16 coefficient form).  Returns float16 [n, r_b]."""
+    return project32(x, B).astype(np.float16)
+
+
+def quantize_coefficients(a32: np.ndarray):
+    """8-bit blockwise form of float32 coefficient rows a32 [n, r_b] (r_b a
+    multiple of 16).  Returns (codes int8 [n, r_b], scales float16 [n, r_b/16],
+    the rebuilt rows code * scale as float32 [n, r_b])."""
+    a = np.asarray(a32, dtype=np.float32)
+    n, rb = a.shape
+    codes = np.zeros((n, rb), dtype=np.int8)
+    scales = np.zeros((n, rb // 16), dtype=np.float16)
+    for k in range(n):
+        for s in range(rb // 16):
+            blk = a[k, 16 * s:16 * s + 16]
+            S = np.float16(np.float32(np.abs(blk).max()) / np.float32(127.0))
+            scales[k, s] = S
+            if S == 0:
+                continue
+            q = np.rint(blk / np.float32(S))
+            codes[k, 16 * s:16 * s + 16] = np.clip(q, -127, 127).astype(np.int8)
+    rebuilt = codes.astype(np.float32) * np.repeat(scales.astype(np.float32), 16, axis=1)
+    return codes, scales, rebuilt
+
+
+def residual(x: np.ndarray, B: np.ndarray, a: np.ndarray) -> np.ndarray:
+    """r = x - A B in float32 for coefficient rows a [n, r_b] (the values the
+    decode rebuilds: fp16 rows, or the dequantized 8-bit form): the basis term
+    of each channel summed over the basis rows left to right, then subtracted
+    from x.  Returns float32 [n, d]."""
     x = np.asarray(x, dtype=np.float16).astype(np.float32)
     B = np.asarray(B, dtype=np.float16).astype(np.float32)
-    a = np.asarray(a16, dtype=np.float16).astype(np.float32)
+    a = np.asarray(a, dtype=np.float32)
     terms = [a[:, i:i + 1] * B[None, i, :] for i in range(B.shape[0])]
     return x - _sum_in_order(terms)
 
@@ -105,15 +139,21 @@ def fold_gate(S: np.float32, g: float) -> np.float16:
     return np.float16(np.float32(g) * np.float32(S))
 
 
-def compress_vectors(x: np.ndarray, B: np.ndarray, rhos, gates=None):
+def compress_vectors(x: np.ndarray, B: np.ndarray, rhos, gates=None, coef_format: str = "f16"):
     """Compress n vectors x [n, d] sharing basis B [r_b, d].
 
-    Returns (a16 [n, r_b] float16, entries, scale16 [n] float16) where
-    entries[k] = (channels, codes) of vector k in storage order."""
+    Returns (coef, entries, scale16 [n] float16) where entries[k] = (channels,
+    codes) of vector k in storage order, and coef is the float16 rows [n, r_b]
+    or, for coef_format "int8", the pair (codes int8 [n, r_b], block scales
+    float16 [n, r_b/16])."""
     x = np.asarray(x, dtype=np.float16)
     n = x.shape[0]
-    a16 = project(x, B)
-    r = residual(x, B, a16)
+    if coef_format == "int8":
+        codes8, cscales, rows = quantize_coefficients(project32(x, B))
+        a16 = (codes8, cscales)
+    else:
+        a16 = rows = project(x, B)
+    r = residual(x, B, rows)
     entries, scales = [], np.zeros(n, dtype=np.float16)
     for k in range(n):
         rho = int(rhos[k])
@@ -148,8 +188,10 @@ def compress(cache, layer: int, x_k: np.ndarray, x_v: np.ndarray, t0: int, t1: i
     gate: None (g = 1) or float32 [2][Hkv][t1-t0].
     The routed ranks and offsets of the tokens (rank_code, res_off of the
     layer's window) must already be in the cache.  Coefficients go to coef_k
-    (row-major) and coef_v (16-token blocks, token fastest); entries to
-    res_idx / res_val at the token's offsets; the folded scale to res_scale."""
+    (row-major) and coef_v (16-token blocks, token fastest), fp16 rows or, for
+    an int8 cache, codes with their block scales in coef_scale_k / _v
+    ([L][Hkv][r_b/16][T]); entries to res_idx / res_val at the token's
+    offsets; the folded scale to res_scale."""
     m = window_of(layer, cache.window)
     levels = np.asarray(cache.levels, dtype=np.int64)
     Hk = cache.n_kv_heads
@@ -166,9 +208,14 @@ def compress(cache, layer: int, x_k: np.ndarray, x_v: np.ndarray, t0: int, t1: i
                 B = cache.basis[b, m, h, z]
                 rhos = levels[cache.rank_code[m, h, toks]]
                 g = None if gate is None else np.asarray(gate, np.float32)[z, h, ks]
-                a16, entries, scales = compress_vectors(X[ks, h], B, rhos, g)
+                c8 = getattr(cache, "coef_format", "f16") == "int8"
+                coef, entries, scales = compress_vectors(X[ks, h], B, rhos, g, "int8" if c8 else "f16")
                 for j, t in enumerate(toks):
-                    store_coefficients(cache, layer, z, h, int(t), a16[j])
+                    if c8:
+                        store_coefficients(cache, layer, z, h, int(t), coef[0][j])
+                        (cache.coef_scale_k if z == 0 else cache.coef_scale_v)[layer, h, :, t] = coef[1][j]
+                    else:
+                        store_coefficients(cache, layer, z, h, int(t), coef[j])
                     cache.res_scale[layer, z, h, t] = scales[j]
                     store_entries(cache, layer, z, h, int(t), *entries[j])
     return cache

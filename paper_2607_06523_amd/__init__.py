@@ -254,6 +254,16 @@ class DeviceCache:
         binding.check(st, "dwkv_decode_merge")
         return out
 
+    def probe_feature(self, layer: int, kv_heads, err, phi, fresh: bool):
+        """dwkv_probe_feature: fold one probed layer's Eq. 3 errors err [B, n*G]
+        into column 3 of the layer's window of phi [M, Hkv, T, 4] (in place)."""
+        heads = np.ascontiguousarray(kv_heads, dtype=np.int32)
+        st = self.lib.dwkv_probe_feature(C.byref(self.dims), int(layer), len(heads),
+                                         heads.ctypes.data_as(C.POINTER(C.c_int32)), _ptr(err), int(bool(fresh)),
+                                         _ptr(phi), _stream(self.torch, self.device))
+        binding.check(st, "dwkv_probe_feature")
+        return phi
+
     def route(self, phi, u, theta, rank_code=None, res_off=None):
         """Eq. 2 routing on the GPU; returns (rank_code uint8 [M,Hkv,T], res_off int32-view [M,Hkv,T+1])."""
         torch = self.torch

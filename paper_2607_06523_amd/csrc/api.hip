@@ -567,10 +567,13 @@ dwkv_status dwkv_compress(const dwkv_dims* d, const dwkv_cache* c, int32_t layer
                           const void* x_v, const float* gate, int64_t t0, int64_t t1, void* stream) {
   dwkv_status st = check_dims(d);
   if (st != DWKV_OK) return st;
-  if (d->coef_format != DWKV_COEF_F16) return DWKV_E_UNSUPPORTED;
+  const bool c8 = d->coef_format == DWKV_COEF_I8;
   if (!c || !c->basis || !c->coef_k || !c->coef_v || !c->rank_code || !c->res_off || !c->res_idx ||
       !c->res_val || !c->res_scale)
     return DWKV_E_NULL;
+  if (c8 && (!c->coef_k_scale || !c->coef_v_scale)) return DWKV_E_NULL;
+  if (c8 && ((reinterpret_cast<uintptr_t>(c->coef_k_scale) | reinterpret_cast<uintptr_t>(c->coef_v_scale)) & 1u))
+    return DWKV_E_ALIGN;
   if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
   if (t0 < 0 || t1 < t0 || t1 > d->total_tokens) return DWKV_E_DIMS;
   if (t1 == t0) return DWKV_OK;
@@ -595,8 +598,18 @@ dwkv_status dwkv_compress(const dwkv_dims* d, const dwkv_cache* c, int32_t layer
   a.xv = static_cast<const uint16_t*>(x_v);
   a.gate = gate;
   // the cache's arrays are written in place (the pointers are const only for decode)
-  a.coef_k = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->coef_k)) + (int64_t)layer * Hk * T16 * rb;
-  a.coef_v = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->coef_v)) + (int64_t)layer * Hk * T16 * rb;
+  if (c8) {                     // int8 codes: one byte per coefficient; fp16 block scales
+    a.coef_k = reinterpret_cast<uint16_t*>(const_cast<uint8_t*>(static_cast<const uint8_t*>(c->coef_k)) +
+                                           (int64_t)layer * Hk * T16 * rb);
+    a.coef_v = reinterpret_cast<uint16_t*>(const_cast<uint8_t*>(static_cast<const uint8_t*>(c->coef_v)) +
+                                           (int64_t)layer * Hk * T16 * rb);
+    a.cscale_k = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->coef_k_scale)) + (int64_t)layer * Hk * (rb / 16) * T;
+    a.cscale_v = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->coef_v_scale)) + (int64_t)layer * Hk * (rb / 16) * T;
+    a.c8 = 1;
+  } else {
+    a.coef_k = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->coef_k)) + (int64_t)layer * Hk * T16 * rb;
+    a.coef_v = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->coef_v)) + (int64_t)layer * Hk * T16 * rb;
+  }
   a.res_idx = const_cast<uint8_t*>(c->res_idx) + (int64_t)layer * 2 * Hk * d->res_stride;
   a.res_val = const_cast<uint8_t*>(c->res_val) + (int64_t)layer * 2 * Hk * (d->res_stride / 2);
   a.res_scale = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->res_scale)) + (int64_t)layer * 2 * Hk * T;
@@ -776,6 +789,34 @@ dwkv_status dwkv_dense_decode(const dwkv_dims* d, const void* k, const void* v, 
   mg.rb = kHeadDim;
   for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) mg.probe_slot_of_kv[h] = -1;
   return hip_status(launch_merge(mg, s));
+}
+
+dwkv_status dwkv_probe_feature(const dwkv_dims* d, int32_t layer, int32_t n_heads, const int32_t* kv_heads_host,
+                               const float* err, int32_t fresh, float* phi, void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
+  if (n_heads < 1 || n_heads > d->n_kv_heads || n_heads > DWKV_MAX_PROBE_HEADS) return DWKV_E_DIMS;
+  if (!kv_heads_host || !err || !phi) return DWKV_E_NULL;
+  if (!aligned16(phi) || (reinterpret_cast<uintptr_t>(err) & 3u)) return DWKV_E_ALIGN;
+  ProbeFeatArgs a;
+  std::memset(&a, 0, sizeof(a));
+  bool seen[DWKV_MAX_PROBE_HEADS] = {};
+  for (int i = 0; i < n_heads; ++i) {
+    const int h = kv_heads_host[i];
+    if (h < 0 || h >= d->n_kv_heads || seen[h]) return DWKV_E_DIMS;
+    seen[h] = true;
+    a.kv_heads[i] = h;
+  }
+  a.err = err;
+  a.phi = phi + (int64_t)(layer / d->window) * d->n_kv_heads * d->total_tokens * 4;
+  a.cu = d->cu_seqlens;
+  a.T = d->total_tokens;
+  a.batch = d->batch;
+  a.n_heads = n_heads;
+  a.G = d->n_q_heads / d->n_kv_heads;
+  a.fresh = fresh ? 1 : 0;
+  return hip_status(launch_probe_feature(a, reinterpret_cast<hipStream_t>(stream)));
 }
 
 size_t dwkv_features_workspace_bytes(const dwkv_dims* d) {

@@ -5,7 +5,9 @@
 // One workgroup (4 waves) takes up to 64 tokens of one (KV head, Z) and holds
 // the window basis of the tokens' sequence in LDS; each wave compresses one
 // token at a time:
-//   A_i   = fp16( sum_j x_j B_ij )                    lane i
+//   A_i   = fp16( sum_j x_j B_ij )                    lane i (or the 8-bit
+//           blockwise form: per block of 16, S = fp16(max |A| / 127),
+//           code = rne(A / S), A_i = code * S from here on)
 //   r_c   = x_c - sum_i A_i B_ic                      lanes own channels 2l, 2l+1
 //   (each sum left to right over its index, one chain per lane and sum)
 //   kept  = rho largest |r_c|, ties to the lower channel (threshold search on
@@ -77,7 +79,9 @@ __device__ __forceinline__ int sequence_of(const int32_t* cu, int batch, int64_t
 struct Slab {
   const uint8_t* code;         // [T]
   const uint32_t* off;         // [T+1]
-  uint16_t* coef;              // keys [T][rb]; values [T16/16][rb][16]
+  uint16_t* coef;              // fp16: key tiles (key_index) or value blocks (value_index)
+  uint8_t* coef8;              // int8: key tiles [T16/16][rb/16][16][16] or value blocks [T16/16][rb][16]
+  uint16_t* cscale;            // int8: block scales [rb/16][T]
   uint8_t* res_idx;            // [res_stride]
   uint8_t* res_val;            // [res_stride/2]
   uint16_t* res_scale;         // [T]
@@ -135,12 +139,30 @@ __device__ __forceinline__ void compress_token(const CompressArgs& a, const Slab
         s = fma_exact(xv8[j], bij, s);
       }
     }
-    const uint16_t ab = float_to_half_bits(s);
-    sm.as[wv][i] = half_bits_to_float(ab);
-    if (z == 0)
-      sl.coef[key_index(t, i, rb)] = ab;
-    else
-      sl.coef[value_index(t, i, rb)] = ab;
+    if (a.c8) {
+      // 8-bit blockwise: the 16 lanes of coefficient block i / 16 share
+      // S = fp16(max |A| / 127); code = rne(A / S) in [-127, 127] (0 when S
+      // is 0); the residual below uses the rebuilt code * S (exact)
+      float mx = fabsf(s);
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      const uint16_t sb = float_to_half_bits(mx / 127.0f);
+      const float S = half_bits_to_float(sb);
+      int q = 0;
+      if (S > 0.f) q = (int)fminf(fmaxf(__builtin_rintf(s / S), -127.f), 127.f);
+      sm.as[wv][i] = (float)q * S;
+      const int64_t pos = z == 0 ? (((t >> 4) * (rb >> 4) + (i >> 4)) << 8) + ((t & 15) << 4) + (i & 15)
+                                 : (((t >> 4) * rb + i) << 4) + (t & 15);
+      sl.coef8[pos] = (uint8_t)(int8_t)q;
+      if ((i & 15) == 0) sl.cscale[(int64_t)(i >> 4) * a.T + t] = sb;
+    } else {
+      const uint16_t ab = float_to_half_bits(s);
+      sm.as[wv][i] = half_bits_to_float(ab);
+      if (z == 0)
+        sl.coef[key_index(t, i, rb)] = ab;
+      else
+        sl.coef[value_index(t, i, rb)] = ab;
+    }
   }
   wave_lds_sync();
 
@@ -154,8 +176,16 @@ __device__ __forceinline__ void compress_token(const CompressArgs& a, const Slab
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const uint32_t bw = *reinterpret_cast<const uint32_t*>(sm.bas + (i0 + v) * kBRow + 2 * lane);
-      p0 = fma_exact(av[v], (uint16_t)(bw & 0xffffu), p0);
-      p1 = fma_exact(av[v], (uint16_t)(bw >> 16), p1);
+      if (a.c8) {
+        // int8 rows code * S carry up to 18 significant bits: their products
+        // with the fp16 basis are not exact in float32, so each product is
+        // rounded on its own before the sum (no contraction in this function)
+        p0 = p0 + av[v] * half_bits_to_float((uint16_t)(bw & 0xffffu));
+        p1 = p1 + av[v] * half_bits_to_float((uint16_t)(bw >> 16));
+      } else {
+        p0 = fma_exact(av[v], (uint16_t)(bw & 0xffffu), p0);
+        p1 = fma_exact(av[v], (uint16_t)(bw >> 16), p1);
+      }
     }
   }
   const float r0 = x0 - p0, r1 = x1 - p1;
@@ -238,6 +268,8 @@ __global__ __launch_bounds__(kCW * 64) void compress_kernel(const CompressArgs a
   sl.code = a.code + (int64_t)h * a.T;
   sl.off = a.off + (int64_t)h * (a.T + 1);
   sl.coef = (z == 0 ? a.coef_k : a.coef_v) + (int64_t)h * a.T16 * a.rb;
+  sl.coef8 = reinterpret_cast<uint8_t*>(z == 0 ? a.coef_k : a.coef_v) + (int64_t)h * a.T16 * a.rb;
+  sl.cscale = a.c8 ? (z == 0 ? a.cscale_k : a.cscale_v) + (int64_t)h * (a.rb / 16) * a.T : nullptr;
   sl.res_idx = a.res_idx + slab * a.res_stride;
   sl.res_val = a.res_val + slab * (a.res_stride / 2);
   sl.res_scale = a.res_scale + slab * a.T;

@@ -62,6 +62,21 @@ __global__ __launch_bounds__(kFT) void features_kernel(const FeatArgs a) {
   }
 }
 
+// The probe-error feature: one thread per token of one probed KV head.  The
+// error of (sequence, head) is the largest over the head's group members;
+// `fresh` overwrites column 3, otherwise it keeps the maximum.
+__global__ __launch_bounds__(kFT) void probe_feature_kernel(const ProbeFeatArgs a) {
+  const int i = blockIdx.y;
+  const int64_t t = (int64_t)blockIdx.x * kFT + threadIdx.x;
+  if (t >= a.T) return;
+  const int b = seq_at(a.cu, a.batch, t);
+  const float* e = a.err + ((int64_t)b * a.n_heads + i) * a.G;
+  float mx = e[0];
+  for (int g = 1; g < a.G; ++g) mx = fmaxf(mx, e[g]);
+  float* f = a.phi + ((int64_t)a.kv_heads[i] * a.T + t) * 4 + 3;
+  *f = a.fresh ? mx : fmaxf(*f, mx);
+}
+
 }  // namespace
 
 hipError_t launch_features(int g, const FeatArgs& a, hipStream_t s) {
@@ -74,6 +89,13 @@ hipError_t launch_features(int g, const FeatArgs& a, hipStream_t s) {
     case 8: hipLaunchKernelGGL(features_kernel<8>, grid, dim3(kFT), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_probe_feature(const ProbeFeatArgs& a, hipStream_t s) {
+  if (a.T <= 0 || a.n_heads <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((a.T + kFT - 1) / kFT), a.n_heads);
+  hipLaunchKernelGGL(probe_feature_kernel, grid, dim3(kFT), 0, s, a);
   return hipGetLastError();
 }
 

@@ -244,13 +244,16 @@ struct CompressArgs {
   const uint16_t* xk;          // [n][Hkv][d] fp16
   const uint16_t* xv;
   const float* gate;           // [2][Hkv][n] or null (g = 1)
-  uint16_t* coef_k;            // layer's [Hkv] slabs of T16*rb (key_index)
-  uint16_t* coef_v;            // layer's [Hkv] slabs of T16*rb (value_index)
+  uint16_t* coef_k;            // layer's [Hkv] slabs of T16*rb (key_index); int8: bytes, 16x16 key tiles
+  uint16_t* coef_v;            // layer's [Hkv] slabs of T16*rb (value_index); int8: bytes, [T16/16][rb][16]
+  uint16_t* cscale_k;          // int8 coefficients: layer's [Hkv] slabs of (rb/16)*T block scales, else null
+  uint16_t* cscale_v;
   uint8_t* res_idx;            // layer's [2][Hkv][res_stride]
   uint8_t* res_val;            // layer's [2][Hkv][res_stride/2]
   uint16_t* res_scale;         // layer's [2][Hkv][T]
   int64_t T, T16, t0, n, res_stride;
   int32_t batch, n_kv_heads, rb, n_levels;
+  int32_t c8;                  // write the 8-bit blockwise coefficient form
   int32_t levels[DWKV_MAX_LEVELS];
 };
 
@@ -308,6 +311,18 @@ struct FeatArgs {
   int32_t batch, n_kv_heads, n_q_heads;
 };
 hipError_t launch_features(int g, const FeatArgs& a, hipStream_t s);
+
+// The probe-error router feature (column 3 of a window's phi) from one
+// probed layer's Eq. 3 errors.
+struct ProbeFeatArgs {
+  const float* err;            // [B][n_heads * G]
+  float* phi;                  // the window's features [Hkv][T][4]
+  const int32_t* cu;           // device cu_seqlens
+  int64_t T;
+  int32_t batch, n_heads, G, fresh;
+  int32_t kv_heads[DWKV_MAX_PROBE_HEADS];
+};
+hipError_t launch_probe_feature(const ProbeFeatArgs& a, hipStream_t s);
 
 // Randomized-sketch basis initialization of one (sequence, window).
 struct SketchArgs {

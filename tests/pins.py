@@ -20,11 +20,14 @@ says what disagreed.  The pins are:
 * the append/compress step: signed-permutation bases (exact projection and
   residual), the round-half-even tie table in ``tests/golden/int4_rne_ties.txt``,
   the float32 decision path in exact rational arithmetic, enumeration of the
-  kept channels, float64 error bounds with an orthonormal basis, the rebuilt
+  kept channels, the 8-bit blockwise encode (exact model, round-half-even
+  ties, zero block, half-step bound, rows rebuilt from the cache), float64 error bounds with an orthonormal basis, the rebuilt
   Eq. 1 vectors after writing into the layout, and range routing against a
   running loop;
 * the router's attention features: per-sequence masses summing to G, spike
   below mass below G spike, uniform and ln-3 closed forms, the table fold;
+  the probe-error feature on a hand-worked case (fresh fold, maximum fold,
+  unprobed heads, an empty sequence);
 * threshold control: a hand-worked feedback trace with clamps, the
   budget-driven selection against enumeration of the promoted sets, and
   budget routing of a token range against a running loop (exact scores,
@@ -829,6 +832,113 @@ def pin_compress_arithmetic(o):
     return None
 
 
+def _rne_int(q: Fraction) -> int:
+    """Round a rational to the nearest integer, ties to even."""
+    fl = q.numerator // q.denominator
+    rem = q - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    return int(fl)
+
+
+def pin_compress_int8(o):
+    """The 8-bit blockwise encode (reading C7): the whole decision path in
+    exact rational arithmetic rounded per operation (float32 projection left
+    to right, S = fp16(fp32(max|A| / 127)), code = rne(fp32(A / S)) clamped,
+    the residual against code * S); round-half-even ties at an exact scale of
+    2^-4; a zero block; the half-step bound; and the rows rebuilt from the
+    cache after writing."""
+    C = o.compress
+    rng = np.random.default_rng(59)
+    d, r_b = 32, 32
+    B = _f16(rng.standard_normal((r_b, d)) * 2.0 ** rng.integers(-4, 2, size=(r_b, d)))
+    x = _f16(rng.standard_normal((3, d)) * 2.0 ** rng.integers(-6, 4, size=(3, d)))
+    codes, scales, rows = C.quantize_coefficients(C.project32(x, B))
+    for k in range(3):
+        a32 = []
+        for i in range(r_b):
+            terms = [fp32_round(Fraction(float(x[k, j])) * Fraction(float(B[i, j]))) for j in range(d)]
+            a32.append(_exact_ordered_sum(terms))
+        want_rows = []
+        for sblk in range(r_b // 16):
+            blk = a32[16 * sblk:16 * sblk + 16]
+            S = fp16_round(fp32_round(max(abs(v) for v in blk) / 127))
+            if Fraction(float(scales[k, sblk])) != S:
+                return f"vector {k} block {sblk}: scale {float(scales[k, sblk])} is not fp16(max|A| / 127)"
+            for i, v in enumerate(blk):
+                q = 0 if S == 0 else max(-127, min(127, _rne_int(fp32_round(v / S))))
+                if int(codes[k, 16 * sblk + i]) != q:
+                    return f"vector {k} coefficient {16 * sblk + i}: code {int(codes[k, 16 * sblk + i])}, want {q}"
+                want_rows.append(q * S)
+        if [Fraction(float(v)) for v in rows[k]] != want_rows:
+            return f"vector {k}: rebuilt rows are not code * scale"
+        er = _exact_residual(x[k], B, want_rows)
+        _, entries, _ = C.compress_vectors(x[k:k + 1], B, [8], coef_format="int8")
+        Sr = fp32_round(max(abs(v) for v in er) / 7)
+        if [(int(c), int(q)) for c, q in zip(*entries[0])] != _expected_entries(er, 8, Sr):
+            return f"vector {k}: residual entries are not taken against code * scale"
+    # a vector in the span of an orthonormal basis: its residual is the
+    # coefficients' quantization error, so only residuals taken against
+    # code * scale give these entries
+    qb, _ = np.linalg.qr(rng.standard_normal((32, 16)))
+    Bo = _f16(qb.T)
+    xo = _f16(rng.standard_normal((2, 16)) @ Bo.astype(np.float64))
+    _, _, rows_o = C.quantize_coefficients(C.project32(xo, Bo))
+    for k in range(2):
+        er = _exact_residual(xo[k], Bo, [Fraction(float(v)) for v in rows_o[k]])
+        _, entries, _ = C.compress_vectors(xo[k:k + 1], Bo, [6], coef_format="int8")
+        Sr = fp32_round(max(abs(v) for v in er) / 7)
+        if [(int(c), int(q)) for c, q in zip(*entries[0])] != _expected_entries(er, 6, Sr):
+            return f"in-span vector {k}: residual entries are not taken against code * scale"
+    # ties: a signed-permutation basis makes A exact; block 0's largest entry is
+    # 127 * 2^-4, so S = 2^-4 and the others sit on half steps
+    d2, rb2 = 32, 16
+    perm = rng.permutation(d2)
+    B2 = np.zeros((rb2, d2))
+    for i in range(rb2):
+        B2[i, perm[i]] = 1.0 if i % 3 else -1.0
+    B2 = _f16(B2)
+    vals = [127, 2.5, 3.5, -2.5, -0.5, 126.5, 0.5, 1.5, -1.5, 7.25, -127, 64.5, 0, 3, -3.5, 5.5]
+    want = [127, 2, 4, -2, 0, 126, 0, 2, -2, 7, -127, 64, 0, 3, -4, 6]
+    x2 = np.zeros((1, d2))
+    for i in range(rb2):
+        x2[0, perm[i]] = (1.0 if i % 3 else -1.0) * vals[i] * 2.0 ** -4
+    c2, s2, _ = C.quantize_coefficients(C.project32(_f16(x2), B2))
+    if float(s2[0, 0]) != 2.0 ** -4 or [int(v) for v in c2[0]] != want:
+        return f"int8 ties: scale {float(s2[0, 0])}, codes {[int(v) for v in c2[0]]}, want 2^-4 and {want}"
+    # a zero block stores scale 0 and codes 0
+    c3, s3, r3 = C.quantize_coefficients(np.zeros((2, 32), np.float32))
+    if np.any(c3 != 0) or np.any(s3 != 0) or np.any(r3 != 0):
+        return "a zero block must store scale 0 and codes 0"
+    # the half-step bound on a realistic orthonormal basis
+    q, _ = np.linalg.qr(rng.standard_normal((128, 48)))
+    B4 = _f16(q.T)
+    x4 = _f16(rng.standard_normal((20, 128)))
+    a4 = x4.astype(np.float64) @ B4.astype(np.float64).T
+    c4, s4, r4 = C.quantize_coefficients(C.project32(x4, B4))
+    S4 = np.repeat(s4.astype(np.float64), 16, axis=1)
+    if np.any(np.abs(r4 - a4) > S4 * 0.5 * (1 + 2.0 ** -9) + 1e-6):
+        return "int8 coefficients off by more than half a step"
+    # written into an int8 cache, the rows rebuilt from it are code * scale
+    c = small_cache(levels=(0, 2, 4), probs=(0.4, 0.3, 0.3), context=20, ragged=(13, 30), basis_rank=32,
+                    head_dim=32, coef_format="int8")
+    layer, t0, t1 = 1, 3, 17
+    Hk = c.n_kv_heads
+    xk = _f16(rng.standard_normal((t1 - t0, Hk, 32)))
+    xv = _f16(rng.standard_normal((t1 - t0, Hk, 32)))
+    c2c = copy.deepcopy(c)
+    C.compress(c2c, layer, xk, xv, t0, t1)
+    for z, X in ((0, xk), (1, xv)):
+        for h in range(Hk):
+            b = C.sequence_of(c.cu_seqlens, t0)
+            _, _, want_rows = C.quantize_coefficients(C.project32(X[:int(c.cu_seqlens[b + 1]) - t0, h],
+                                                                   c.basis[b, 0, h, z]))
+            got = o.factorized.coefficient_rows(c2c, layer, z, h, t0, min(t1, int(c.cu_seqlens[b + 1])))
+            if not np.array_equal(got, want_rows.astype(np.float64)):
+                return f"int8 rows rebuilt from the cache differ (z={z}, h={h})"
+    return None
+
+
 def pin_compress_bounds(o):
     """With a realistic orthonormal basis (d = 128): A matches the float64
     projection to fp16 rounding, every kept channel is reproduced within
@@ -995,6 +1105,36 @@ def pin_attention_features(o):
     OF.update_features(phi, 0, np.array([[0.1, 0.1]]), np.array([[0.1, 0.6]]))
     if not np.allclose(phi[0, 0], [[0.3, 0.5, 7, 7], [0.4, 0.6, 7, 7]]):
         return f"feature table must add masses and keep maxima, got {phi[0, 0]}"
+    return None
+
+
+def pin_probe_feature(o):
+    """The probe-error feature on a hand-worked case: two sequences (one empty),
+    three KV heads of which two are probed in a different order, G = 2; a fresh
+    fold writes each probed head's largest group error on every token of the
+    sequence, a second fold keeps the maximum, the unprobed head and columns
+    0-2 stay as they were."""
+    OF = o.features
+    cu = [0, 3, 3, 5]                                  # sequence 1 is empty
+    phi = np.full((2, 3, 5, 4), 9.0, np.float32)
+    phi[1, :, :, 3] = 0.5
+    err = np.array([[0.1, 0.3, 0.2, 0.05],             # b = 0: head 2 -> 0.3, head 0 -> 0.2
+                    [0.7, 0.7, 0.7, 0.7],              # b = 1 (empty): nothing to write
+                    [0.0, 0.25, 0.6, 0.4]], np.float32)  # b = 2: head 2 -> 0.25, head 0 -> 0.6
+    OF.probe_feature(phi, cu, 1, [2, 0], err, 2, True)
+    want = np.full((3, 5), 0.5, np.float32)
+    want[2, 0:3], want[0, 0:3] = 0.3, 0.2
+    want[2, 3:5], want[0, 3:5] = 0.25, 0.6
+    if not np.array_equal(phi[1, :, :, 3], want):
+        return f"fresh probe feature: got {phi[1, :, :, 3]}, want {want}"
+    if not (np.all(phi[:, :, :, :3] == 9.0) and np.all(phi[0, :, :, 3] == 9.0)):
+        return "probe feature touched other columns or another window"
+    err2 = np.array([[0.35, 0.0, 0.1, 0.1], [0, 0, 0, 0], [0.1, 0.2, 0.9, 0.0]], np.float32)
+    OF.probe_feature(phi, cu, 1, [2, 0], err2, 2, False)
+    want[2, 0:3] = 0.35                               # max(0.3, 0.35)
+    want[0, 3:5] = 0.9                                # max(0.6, 0.9); the rest keep the larger earlier value
+    if not np.array_equal(phi[1, :, :, 3], want):
+        return f"accumulated probe feature must keep the maximum: got {phi[1, :, :, 3]}, want {want}"
     return None
 
 
@@ -1174,8 +1314,8 @@ def pin_int8_coefficients(o):
 
 ALL_PINS = [pin_query_formats, pin_nibbles, pin_residual_map, pin_brute_force, pin_closed_forms,
             pin_reductions, pin_invariants, pin_probe, pin_router, pin_compress_closed_forms,
-            pin_compress_rne_table, pin_compress_arithmetic, pin_compress_bounds,
-            pin_compress_into_cache, pin_route_range, pin_attention_features, pin_control, pin_route_budget, pin_sketch,
+            pin_compress_rne_table, pin_compress_arithmetic, pin_compress_int8, pin_compress_bounds,
+            pin_compress_into_cache, pin_route_range, pin_attention_features, pin_probe_feature, pin_control, pin_route_budget, pin_sketch,
             pin_int8_coefficients]
 
 

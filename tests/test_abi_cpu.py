@@ -231,6 +231,12 @@ def test_route_range_and_compress_argument_checks(lib):
     assert cp(cache=c3) == 1
     d2, keep2 = dims(head_dim=64)
     assert lib.dwkv_compress(C.byref(d2), C.byref(c), 0, FAKE, FAKE, None, 0, 1, None) == 3
+    # the 8-bit blockwise form needs its block-scale arrays, 2-byte aligned
+    d8, keep8 = dims(coef_format=1)
+    assert lib.dwkv_compress(C.byref(d8), C.byref(c), 0, FAKE, FAKE, None, 0, 1, None) == 1
+    c8 = binding.Cache(*([FAKE] * 8))
+    c8.coef_k_scale, c8.coef_v_scale = FAKE, FAKE + 1
+    assert lib.dwkv_compress(C.byref(d8), C.byref(c8), 0, FAKE, FAKE, None, 0, 1, None) == 7
 
 
 def test_materialize_and_dense_argument_checks(lib):
@@ -400,3 +406,16 @@ def test_decode_kernel_query(lib):
                      (dict(n_q_heads=32), 0), (dict(basis_rank=80), 0), (dict(n_q_heads=7), -1)]:
         d, keep = dims(**kw)
         assert lib.dwkv_decode_kernel(C.byref(d)) == want, kw
+
+
+def test_probe_feature_argument_checks(lib):
+    d, keep = dims()
+    heads = np.array([1, 0], dtype=np.int32)
+    hp = heads.ctypes.data_as(C.POINTER(C.c_int32))
+    f = lambda layer=0, n=2, h=hp, err=FAKE, phi=FAKE: lib.dwkv_probe_feature(C.byref(d), layer, n, h, err, 1,
+                                                                               phi, None)
+    assert f(n=0) == 2 and f(n=3) == 2 and f(layer=4) == 2
+    assert f(h=None) == 1 and f(err=0) == 1 and f(phi=0) == 1
+    assert f(phi=FAKE + 4) == 7 and f(err=FAKE + 2) == 7
+    dup = np.array([1, 1], dtype=np.int32)
+    assert f(h=dup.ctypes.data_as(C.POINTER(C.c_int32))) == 2

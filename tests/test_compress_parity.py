@@ -42,11 +42,19 @@ class _Fixed:
 WRITTEN = ("coef_k", "coef_v", "res_idx", "res_val", "res_scale")
 
 
+WRITTEN_I8 = ("coef_k", "coef_v", "coef_scale_k", "coef_scale_v", "res_idx", "res_val", "res_scale")
+
+
 def _host_arrays(dc):
     keys, values = dc.coef_host()       # back from the ABI's tiled layouts
+    if dc.coef_format == "int8":
+        extra = {"coef_k": keys.view(np.int8), "coef_v": values.view(np.int8),
+                 "coef_scale_k": dc.coef_scale_k.cpu().numpy().view(np.float16),
+                 "coef_scale_v": dc.coef_scale_v.cpu().numpy().view(np.float16)}
+    else:
+        extra = {"coef_k": keys.view(np.float16), "coef_v": values.view(np.float16)}
     return {
-        "coef_k": keys.view(np.float16),
-        "coef_v": values.view(np.float16),
+        **extra,
         "res_idx": dc.res_idx.cpu().numpy(),
         "res_val": dc.res_val.cpu().numpy(),
         "res_scale": dc.res_scale.cpu().numpy().view(np.float16),
@@ -128,7 +136,8 @@ def _run_case(host, dc, layers, t0, t1, xs, gates, routing=None, label=""):
         dc.compress(layer, dev(xk), dev(xv), t0, t1, gate=None if gate is None else dev(gate))
         torch.cuda.synchronize()
         OC.compress(ref, layer, xk, xv, t0, t1, gate)
-    _assert_same(_host_arrays(dc), ref, WRITTEN + ("rank_code", "res_off"), label)
+    written = WRITTEN_I8 if getattr(host, "coef_format", "f16") == "int8" else WRITTEN
+    _assert_same(_host_arrays(dc), ref, written + ("rank_code", "res_off"), label)
     announce(f"validate {label}")
     ok, bad = dc.validate()
     assert ok, f"{label}: the validator rejects the compressed cache at {bad}"
@@ -181,6 +190,55 @@ def test_compress_bit_exact(case):
         out = dc.decode(l).cpu().numpy()
         torch.cuda.synchronize()
         compare(out, oracle.decode(ref, l), pairs, host.n_q_heads // host.n_kv_heads, f"{name} decode l={l}")
+
+
+I8_CASES = [
+    # name, r_b, levels, probs, lengths, layer, range, gate, x, route, decode afterwards
+    ("i8-rb48-decode-token-append", 48, (0, 4, 8, 16), (0.25, 0.25, 0.25, 0.25), [2048], 1, "last", False,
+     "near-cache", True, True),
+    ("i8-rb32-across-seqs-gated", 32, (0, 8, 16), (0.3, 0.4, 0.3), [0, 129, 700, 0, 300], 2, (100, 1100), True,
+     "normal", False, True),
+    ("i8-rb64-prefill", 64, (0, 4, 8, 16), (0.4, 0.3, 0.2, 0.1), [1000], 3, "all", False, "near-cache", True,
+     True),
+    ("i8-rb16-tail", 16, (0, 2), (0.5, 0.5), [63, 65], 0, "tail100", False, "normal", True, True),
+    ("i8-rb128-compress-only", 128, (0, 16, 32), (0.4, 0.3, 0.3), [500], 1, "all", True, "normal", False, False),
+]
+
+
+@pytest.mark.parametrize("case", I8_CASES, ids=[c[0] for c in I8_CASES])
+def test_compress_int8_bit_exact(case):
+    """dwkv_compress writing the 8-bit blockwise coefficient form (reading C7):
+    codes, block scales, residual channels, codes and scales equal the
+    oracle's byte for byte; then the int8 decode over the written cache matches
+    the float64 decode of the oracle's cache (r_b above 64 is encoded only: the
+    int8 decode serves r_b up to 64)."""
+    torch = torch_gpu()
+    name, rb, levels, probs, lengths, layer, rng_spec, use_gate, xkind, route, decode = case
+    w = _Fixed(Workload(name=name, batch=len(lengths), n_layers=4, window=2, n_kv_heads=2, n_q_heads=8,
+                        head_dim=128, context=max(lengths), basis_rank=rb, levels=levels, probs=probs,
+                        q_dtype="bf16", seed=500 + len(name), coef_format="int8"), lengths)
+    host = generate(w, threads=4)
+    T = host.total_tokens
+    t0, t1 = {"last": (T - 1, T), "tail100": (T - 100, T), "all": (0, T)}.get(rng_spec, rng_spec)
+    rng = np.random.default_rng(9 + len(name))
+    routing = None
+    layers = [layer]
+    if route:
+        routing = router_inputs(w, host.n_windows, T)
+        _room_for_routing(host, routing, t0, t1)
+        layers = list(range(host.n_layers))
+    xs = [_inputs(host, l, t0, t1, xkind, rng) for l in layers]
+    gates = [rng.uniform(0.0, 1.0, size=(2, host.n_kv_heads, t1 - t0)).astype(np.float32) if use_gate else None
+             for _ in layers]
+    dc = device_cache(host)
+    ref = _run_case(host, dc, layers, t0, t1, xs, gates, routing, name)
+    if decode:
+        pairs = [(b, h) for b in range(host.batch) for h in range(host.n_kv_heads)]
+        for l in layers:
+            announce(f"int8 decode after compress {name} layer={l}")
+            out = dc.decode(l).cpu().numpy()
+            torch.cuda.synchronize()
+            compare(out, oracle.decode(ref, l), pairs, host.n_q_heads // host.n_kv_heads, f"{name} decode l={l}")
 
 
 def test_compress_zero_residual_and_ties():

@@ -92,3 +92,40 @@ def test_features_full_size_sampled():
         ref[0, 0, :, 0] = p.sum(axis=0)
         ref[0, 0, :, 1] = p.max(axis=0)
         _check(got[0:1, h:h + 1], ref, f"64k head {h}")
+
+
+def test_probe_feature_matches_oracle():
+    """The probe-error feature (column 3 of phi) from the Eq. 3 errors of two
+    probed layers of one window: a fresh fold then a maximum fold, on the GPU
+    through dwkv_probe_feature, against the oracle's fold of the same errors,
+    bit for bit (a maximum and a copy, no arithmetic)."""
+    torch = torch_gpu()
+    import oracle.features as OFE
+    from paper_2607_06523_amd import ProbeRef
+    from synth.layout import block_values
+    w = _Fixed(Workload(name="probe-feature", batch=3, n_layers=4, window=2, n_kv_heads=4, n_q_heads=16,
+                        head_dim=128, context=900, basis_rank=32, levels=(0, 8, 16), probs=(0.8, 0.15, 0.05),
+                        q_dtype="bf16", seed=91), [500, 0, 900])
+    host = generate(w, threads=4)
+    dc = device_cache(host, split_tokens=256)
+    M, Hk, T = host.n_windows, host.n_kv_heads, host.total_tokens
+    rng = np.random.default_rng(4)
+    phi0 = rng.uniform(0.0, 0.5, size=(M, Hk, T, 4)).astype(np.float32)
+    phi = torch.from_numpy(phi0.copy()).cuda()
+    ref = phi0.copy()
+    heads = [3, 1]
+    for k, layer in enumerate((2, 3)):              # window 1, fresh then folded
+        K = rng.standard_normal((len(heads), T, 128)).astype(np.float16)
+        V = rng.standard_normal((len(heads), T, 128)).astype(np.float16)
+        pr = ProbeRef(heads, torch.from_numpy(K.view(np.uint16)).view(torch.float16).cuda(),
+                      torch.from_numpy(block_values(V).view(np.uint16)).view(torch.float16).cuda())
+        announce(f"probe feature layer {layer}")
+        _, err, _ = dc.decode(layer, probe=pr)
+        dc.probe_feature(layer, heads, err, phi, fresh=(k == 0))
+        torch.cuda.synchronize()
+        OFE.probe_feature(ref, host.cu_seqlens, layer // host.window, heads, err.cpu().numpy(), 4, k == 0)
+    got = phi.cpu().numpy()
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32)), "probe feature differs from the oracle"
+    assert np.array_equal(got[:, :, :, :3], phi0[:, :, :, :3]) and np.array_equal(got[0], phi0[0])
+    print(f"[parity] probe feature: column 3 of window 1 bit-equal; range {got[1, heads, :, 3].min():.3f}"
+          f"..{got[1, heads, :, 3].max():.3f}", flush=True)

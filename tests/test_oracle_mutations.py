@@ -281,6 +281,67 @@ def _budget_code_as_level(phi, u, entries, levels, t0, t1, codes, off):
     return codes, off
 
 
+def _pf_mean(phi, cu, window, kv_heads, err, G, fresh):
+    err = np.asarray(err, np.float32)
+    e2 = np.repeat(err.reshape(err.shape[0], -1, G).mean(axis=2), G, axis=1)
+    return FE.__dict__["_orig_probe_feature"](phi, cu, window, kv_heads, e2, G, fresh)
+
+
+def _pf_overwrite(phi, cu, window, kv_heads, err, G, fresh):
+    return FE.__dict__["_orig_probe_feature"](phi, cu, window, kv_heads, err, G, True)
+
+
+def _pf_all_heads(phi, cu, window, kv_heads, err, G, fresh):
+    FE.__dict__["_orig_probe_feature"](phi, cu, window, kv_heads, err, G, fresh)
+    h0 = kv_heads[0]
+    for h in range(phi.shape[1]):
+        phi[window, h, :, 3] = phi[window, h0, :, 3]
+    return phi
+
+
+def _q8_variant(kind):
+    def q8(a32):
+        a = np.asarray(a32, dtype=np.float32)
+        n, rb = a.shape
+        bw = 8 if kind == "block8" else 16
+        codes = np.zeros((n, rb), dtype=np.int8)
+        scales = np.zeros((n, rb // 16), dtype=np.float16)
+        rows = np.zeros((n, rb), dtype=np.float32)
+        for k in range(n):
+            for s in range(rb // bw):
+                blk = a[k, bw * s:bw * s + bw]
+                S = np.float16(np.float32(np.abs(blk).max()) / np.float32(128.0 if kind == "div128" else 127.0))
+                if bw == 16:
+                    scales[k, s] = S
+                if S == 0:
+                    continue
+                q = blk / np.float32(S)
+                q = np.sign(q) * np.floor(np.abs(q) + 0.5) if kind == "half_away" else np.rint(q)
+                codes[k, bw * s:bw * s + bw] = np.clip(q, -127, 127).astype(np.int8)
+                rows[k, bw * s:bw * s + bw] = codes[k, bw * s:bw * s + bw].astype(np.float32) * np.float32(S)
+        return codes, scales, rows
+    return q8
+
+
+def _cv_residual_fp16(x, B, rhos, gates=None, coef_format="f16"):
+    if coef_format != "int8":
+        return CP.__dict__["_orig_compress_vectors"](x, B, rhos, gates, coef_format)
+    x = np.asarray(x, dtype=np.float16)
+    codes8, cscales, _ = CP.quantize_coefficients(CP.project32(x, B))
+    r = CP.residual(x, B, CP.project(x, B))
+    entries, scales = [], np.zeros(x.shape[0], dtype=np.float16)
+    for k in range(x.shape[0]):
+        rho = int(rhos[k])
+        if rho == 0:
+            entries.append((np.zeros(0, np.int64), np.zeros(0, np.int64)))
+            continue
+        S = CP.quant_scale(r[k])
+        ch = CP.select_channels(r[k], rho)
+        entries.append(CP.entry_order(ch, CP.quantize(r[k][ch], S)))
+        scales[k] = CP.fold_gate(S, 1.0 if gates is None else float(gates[k]))
+    return (codes8, cscales), entries, scales
+
+
 def _gs_no_normalize(Y):
     Y = np.array(Y, dtype=np.float64)
     Q = np.zeros_like(Y)
@@ -362,6 +423,10 @@ MUTANTS = {
     "entries stored in channel order": [(CP, "entry_order", lambda ch, k: (np.asarray(ch)[np.argsort(ch)],
                                                                         np.asarray(k)[np.argsort(ch)]))],
     "gate not folded into the scale": [(CP, "fold_gate", lambda S, g: np.float16(S))],
+    "int8 block scale max|A| / 128": [(CP, "quantize_coefficients", _q8_variant("div128"))],
+    "int8 codes round half away from zero": [(CP, "quantize_coefficients", _q8_variant("half_away"))],
+    "int8 blocks of 8 coefficients": [(CP, "quantize_coefficients", _q8_variant("block8"))],
+    "int8 residual against the fp16 projection": [(CP, "compress_vectors", _cv_residual_fp16)],
     "value coefficients written row-major": [(CP, "store_coefficients", _store_values_row_major)],
     "entries written at the next token's offset": [(CP, "store_entries", _store_entries_at_next)],
     "range routing restarts the offsets at zero": [(R, "route_range", _route_range_from_zero)],
@@ -369,6 +434,9 @@ MUTANTS = {
     "attention spike summed over heads": [(FE, "attention_features", _features_variant("spike_sum"))],
     "feature mass overwritten instead of accumulated": [(FE, "update_features", _update_overwrite)],
     "feature spike keeps the last value": [(FE, "update_features", _update_spike_last)],
+    "probe feature averages the group's errors": [(FE, "probe_feature", _pf_mean)],
+    "probe feature overwrites when folding": [(FE, "probe_feature", _pf_overwrite)],
+    "probe feature written to every head": [(FE, "probe_feature", _pf_all_heads)],
     "threshold steps not clamped": [(CT, "controller_update", _ctl_variant("no_clamp"))],
     "NaN probe error counted as quiet": [(CT, "controller_update", _ctl_variant("nan_quiet"))],
     "step up one interval late": [(CT, "controller_update", _ctl_variant("patience_late"))],
@@ -392,6 +460,8 @@ def test_mutant_is_caught(name, monkeypatch):
     R.__dict__.setdefault("_orig_route_range", R.route_range)
     CP.__dict__.setdefault("_orig_residual", CP.residual)
     CT.__dict__.setdefault("_orig_route_budget", CT.route_budget)
+    FE.__dict__.setdefault("_orig_probe_feature", FE.probe_feature)
+    CP.__dict__.setdefault("_orig_compress_vectors", CP.compress_vectors)
     for mod, attr, fn in MUTANTS[name]:
         monkeypatch.setattr(mod, attr, fn)
         if hasattr(oracle, attr):
