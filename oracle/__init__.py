@@ -22,7 +22,7 @@ closed forms, reductions to library attention, invariants); none is marked
 "parity unpinned".
 """
 from . import factorized, router, compress, features, control, sketch
-from .factorized import (attention, decode, probe, probe_error, reconstruct,
+from .factorized import (attention, decode, probe, probe_error, probe_positions, reconstruct,
                          residual_map, int4_from_nibble, entry_codes, q_to_f64,
                          default_scale)
 from .router import route, route_range, router_score, level_index, theta_from_tau

@@ -19,6 +19,10 @@ What it computes, following the paper's Method section (Sec. 3):
   materialises them instead).
 * Eq. 3: the probe error e = ||Attn(Q,K,V) - Attn(Q,K_hat,V_hat)||_2 /
   (||Attn(Q,K,V)||_2 + eps), with (K,V) the higher-fidelity reference cache.
+  The probe may evaluate several recent query positions; then the norms run
+  over those positions and d together, and the query j steps back attends to
+  the first T_b - j tokens of its sequence (the prefix its position saw), in
+  the current cache.
 
 Readings where the paper is silent (each listed in the design notes):
 depth windows are contiguous non-overlapping groups (m = l // w); the routed
@@ -181,6 +185,41 @@ def probe(cache, layer: int, kv_heads, k_ref: np.ndarray, v_ref: np.ndarray,
             o, _ = attention(qq, reconstruct(cache, layer, 0, h, b),
                              reconstruct(cache, layer, 1, h, b), scale)
             err[b, i * G:(i + 1) * G] = probe_error(o_ref, o, eps)
+    return err
+
+
+def probe_positions(cache, layer: int, kv_heads, k_ref: np.ndarray, v_ref: np.ndarray, qs: np.ndarray,
+                    sm_scale: float | None = None, eps: float = 1e-6):
+    """Eq. 3 over several recent query positions.  qs [P][B][Hq][d]: the
+    queries of the last P decode positions of every sequence, j = 0 the
+    current one.  The query j steps back attends to the tokens its position
+    could see, the first T_b - j of the sequence (none when T_b <= j).  Per
+    sequence and probed query head, with O_j and O_ref_j the outputs over the
+    rebuilt and the reference cache,
+        e = sqrt(sum_j ||O_ref_j - O_j||^2) / (sqrt(sum_j ||O_ref_j||^2) + eps),
+    the 2-norm taken over the positions and d together.
+    Returns err [B, n_probe * G]."""
+    B, Hq, Hk, d = cache.batch, cache.n_q_heads, cache.n_kv_heads, cache.head_dim
+    G = Hq // Hk
+    scale = default_scale(d) if sm_scale is None or sm_scale <= 0 else sm_scale
+    qs = np.asarray(qs, dtype=np.float64)
+    err = np.zeros((B, len(kv_heads) * G))
+    for i, h in enumerate(kv_heads):
+        for b in range(B):
+            t0, t1 = int(cache.cu_seqlens[b]), int(cache.cu_seqlens[b + 1])
+            K = reconstruct(cache, layer, 0, h, b)
+            V = reconstruct(cache, layer, 1, h, b)
+            d2 = np.zeros(G)
+            r2 = np.zeros(G)
+            for j in range(qs.shape[0]):
+                n = max(t1 - t0 - j, 0)
+                qq = qs[j, b, h * G:(h + 1) * G]
+                o_ref, _ = attention(qq, k_ref[i, t0:t0 + n].astype(np.float64),
+                                     v_ref[i, t0:t0 + n].astype(np.float64), scale)
+                o, _ = attention(qq, K[:n], V[:n], scale)
+                d2 += ((o_ref - o) ** 2).sum(axis=-1)
+                r2 += (o_ref ** 2).sum(axis=-1)
+            err[b, i * G:(i + 1) * G] = np.sqrt(d2) / (np.sqrt(r2) + eps)
     return err
 
 

@@ -12,7 +12,9 @@ says what disagreed.  The pins are:
 * invariants: probabilities sum to one, token-permutation invariance, sequence
   independence, the query-head to KV-head grouping;
 * Eq. 3 closed forms (e = 0 for an exact reference, e = |1-c|/(|c| + eps/||O||)
-  for a value reference scaled by c);
+  for a value reference scaled by c); over several recent positions, the same
+  scaled-reference form with the norm over positions, a last-token change
+  seen by the current position only, and the one-position reduction;
 * the router score in exact rational arithmetic rounded per operation, Eq. 2 in
   float64 for two levels, infinite thresholds, monotonicity, and offsets by a
   running loop;
@@ -492,6 +494,79 @@ def pin_probe(o):
                 exp = abs(1 - cval) * n / (abs(cval) * n + eps)
                 if np.abs(e[:, i * G + g] - exp).max() > 1e-12:
                     return f"Eq. 3 scaled-reference closed form wrong (c={cval})"
+    return None
+
+
+def _probe_pos_setup(o):
+    c = small_cache(head_dim=16, basis_rank=4, batch=4, ragged=(0, 7), context=7, seed=28,
+                    levels=(0, 2), probs=(0.5, 0.5))
+    _perm_basis(c, 29)
+    rng = np.random.default_rng(30)
+    c.coef_k[:] = rng.integers(-3, 4, size=c.coef_k.shape).astype(np.float16)
+    c.coef_v[:] = rng.integers(-3, 4, size=c.coef_v.shape).astype(np.float16)
+    c.res_scale[:] = np.float16(0.5)
+    layer, heads = 1, [1, 0]
+    K = np.stack([np.concatenate([o.reconstruct(c, layer, 0, h, b) for b in range(c.batch)]) for h in heads])
+    V = np.stack([np.concatenate([o.reconstruct(c, layer, 1, h, b) for b in range(c.batch)]) for h in heads])
+    P = 3
+    qs = rng.standard_normal((P, c.batch, c.n_q_heads, c.head_dim)).astype(np.float16).astype(np.float64)
+    return c, layer, heads, K, V, qs
+
+
+def pin_probe_positions(o):
+    """Eq. 3 over several recent positions (norm over the positions and d).
+    Lengths 0, 6, 1 and 4 with three positions: the query j steps back sees
+    the first T_b - j tokens, none when T_b <= j.  Expected values come from
+    torch's attention over prefixes of the rebuilt rows."""
+    c, layer, heads, K, V, qs = _probe_pos_setup(o)
+    if not np.array_equal(V.astype(np.float16).astype(np.float64), V):
+        return "probe positions setup: reference not fp16-exact"
+    G = c.n_q_heads // c.n_kv_heads
+    P = qs.shape[0]
+    scale = 1.0 / np.sqrt(c.head_dim)
+    cu = c.cu_seqlens
+    # one position is the single-position probe
+    e1 = o.probe_positions(c, layer, heads, K.astype(np.float16), V.astype(np.float16), qs[:1])
+    e0 = o.probe(c, layer, heads, K.astype(np.float16), V.astype(np.float16), q=qs[0])
+    if not np.array_equal(e1, e0):
+        return "probe over one position differs from the single-position probe"
+
+    def rows(i, b, j, Vm):
+        h = heads[i]
+        n = max(int(cu[b + 1] - cu[b]) - j, 0)
+        t0 = int(cu[b])
+        if n == 0:
+            return np.zeros((G, c.head_dim))
+        return _sdpa(qs[j, b, h * G:(h + 1) * G], K[i, t0:t0 + n], Vm[i, t0:t0 + n], scale)
+
+    # scaled reference values: every position's reference output is cval times
+    # the rebuilt one, e = |1 - c| N / (|c| N + eps) with N^2 summed over positions
+    eps = 0.5
+    for cval in (2.0, -0.5):
+        e = o.probe_positions(c, layer, heads, K.astype(np.float16), (cval * V).astype(np.float16), qs, eps=eps)
+        for i in range(len(heads)):
+            for b in range(c.batch):
+                N = np.sqrt(sum((rows(i, b, j, V) ** 2).sum(axis=-1) for j in range(P)))
+                want = abs(1 - cval) * N / (abs(cval) * N + eps)
+                if np.abs(e[b, i * G:(i + 1) * G] - want).max() > 1e-12:
+                    return f"probe positions scaled-reference closed form wrong (c={cval}, b={b}, head {i})"
+    # a change to the last token of every sequence is seen by the current
+    # position only
+    Vr = V.copy()
+    last = cu[1:][cu[1:] > cu[:-1]] - 1
+    Vr[:, last, :] += 1.0
+    e = o.probe_positions(c, layer, heads, K.astype(np.float16), Vr.astype(np.float16), qs, eps=1e-6)
+    for i in range(len(heads)):
+        for b in range(c.batch):
+            d2 = ((rows(i, b, 0, Vr) - rows(i, b, 0, V)) ** 2).sum(axis=-1)
+            r2 = (rows(i, b, 0, Vr) ** 2).sum(axis=-1) + sum((rows(i, b, j, V) ** 2).sum(axis=-1) for j in range(1, P))
+            want = np.sqrt(d2) / (np.sqrt(r2) + 1e-6)
+            if np.abs(e[b, i * G:(i + 1) * G] - want).max() > 1e-12:
+                return f"probe positions last-token case wrong (b={b}, head {i}): {e[b, i * G:(i + 1) * G]} vs {want}"
+            if cu[b + 1] == cu[b] and np.any(e[b, i * G:(i + 1) * G] != 0):
+                return "probe positions: an empty sequence has a non-zero error"
+    if not np.any(e > 0):
+        return "probe positions last-token case: no error seen"
     return None
 
 
@@ -1313,7 +1388,7 @@ def pin_int8_coefficients(o):
 
 
 ALL_PINS = [pin_query_formats, pin_nibbles, pin_residual_map, pin_brute_force, pin_closed_forms,
-            pin_reductions, pin_invariants, pin_probe, pin_router, pin_compress_closed_forms,
+            pin_reductions, pin_invariants, pin_probe, pin_probe_positions, pin_router, pin_compress_closed_forms,
             pin_compress_rne_table, pin_compress_arithmetic, pin_compress_int8, pin_compress_bounds,
             pin_compress_into_cache, pin_route_range, pin_attention_features, pin_probe_feature, pin_control, pin_route_budget, pin_sketch,
             pin_int8_coefficients]

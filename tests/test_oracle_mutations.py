@@ -380,6 +380,39 @@ def _coef_rows_variant(kind):
     return rows
 
 
+
+def _pp_variant(kind):
+    def pp(cache, layer, kv_heads, k_ref, v_ref, qs, sm_scale=None, eps=1e-6):
+        G = cache.n_q_heads // cache.n_kv_heads
+        scale = F.default_scale(cache.head_dim) if not sm_scale or sm_scale <= 0 else sm_scale
+        qs = np.asarray(qs, np.float64)
+        P = qs.shape[0]
+        err = np.zeros((cache.batch, len(kv_heads) * G))
+        for i, h in enumerate(kv_heads):
+            for b in range(cache.batch):
+                t0, t1 = int(cache.cu_seqlens[b]), int(cache.cu_seqlens[b + 1])
+                K, V = F.reconstruct(cache, layer, 0, h, b), F.reconstruct(cache, layer, 1, h, b)
+                d2, r2, per = np.zeros(G), np.zeros(G), []
+                for j in range(P):
+                    n = max(t1 - t0 - j, 0)
+                    lo, hi = (j, t1 - t0) if kind == "front" else (0, n)
+                    if kind == "plus_one" and j > 0:
+                        hi = min(n + 1, t1 - t0)
+                    lo = min(lo, hi)
+                    qq = qs[P - 1 - j if kind == "reverse" else j, b, h * G:(h + 1) * G]
+                    o_ref, _ = F.attention(qq, np.asarray(k_ref[i, t0 + lo:t0 + hi], np.float64),
+                                           np.asarray(v_ref[i, t0 + lo:t0 + hi], np.float64), scale)
+                    o, _ = F.attention(qq, K[lo:hi], V[lo:hi], scale)
+                    dd, rr = ((o_ref - o) ** 2).sum(-1), (o_ref ** 2).sum(-1)
+                    if kind == "first_only" and j > 0:
+                        dd = rr = 0 * dd
+                    d2, r2 = d2 + dd, r2 + rr
+                    per.append(np.sqrt(dd) / (np.sqrt(rr) + eps))
+                err[b, i * G:(i + 1) * G] = (np.mean(per, axis=0) if kind == "mean"
+                                             else np.sqrt(d2) / (np.sqrt(r2) + eps))
+        return err
+    return pp
+
 MUTANTS = {
     "residual dropped": [(F, "reconstruct", _reconstruct_variant("no_residual"))],
     "residual sign flipped": [(F, "reconstruct", _reconstruct_variant("residual_sign"))],
@@ -401,6 +434,11 @@ MUTANTS = {
     "probe eps dropped": [
         (F, "probe_error", lambda o_ref, o, eps=1e-6: np.linalg.norm(np.asarray(o_ref) - o, axis=-1)
          / np.maximum(np.linalg.norm(o_ref, axis=-1), 1e-300))],
+    "probe positions average the per-position errors": [(F, "probe_positions", _pp_variant("mean"))],
+    "probe positions trimmed from the front": [(F, "probe_positions", _pp_variant("front"))],
+    "probe positions see one token too many": [(F, "probe_positions", _pp_variant("plus_one"))],
+    "probe positions pair the queries in reverse": [(F, "probe_positions", _pp_variant("reverse"))],
+    "probe positions keep only the current one": [(F, "probe_positions", _pp_variant("first_only"))],
     "router score in float64": [(R, "router_score", _router_fused)],
     "router score summed in reverse": [(R, "router_score", _router_reordered)],
     "router ties go up": [(R, "level_index", _level_ge)],
