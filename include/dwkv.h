@@ -38,9 +38,10 @@
 extern "C" {
 #endif
 
-#define DWKV_ABI_VERSION 3
+#define DWKV_ABI_VERSION 4
 #define DWKV_MAX_LEVELS 8
 #define DWKV_MAX_PROBE_HEADS 64
+#define DWKV_MAX_PROBE_POS 8      /* recent query positions one probe evaluates */
 
 typedef enum dwkv_status {
   DWKV_OK = 0,
@@ -131,7 +132,18 @@ typedef struct dwkv_probe {
   float* err;                  /* out fp32 [B][n_heads*G]: probed head i, group member g
                                   at column i*G+g                                      */
   float* out_ref;              /* optional out fp32 [B][n_heads*G][d]: attention over the
-                                  reference cache; may be NULL                         */
+                                  reference cache of the current position's query; may
+                                  be NULL                                              */
+  /* Several recent query positions (Sec. 3 evaluates a subset of heads and
+   * recent positions twice).  The query j steps back (j = 1..n_pos-1) attends
+   * to the first T_b - j tokens of its sequence in this cache and in the
+   * reference (nothing when T_b <= j), and err becomes, per column,
+   *   sqrt(sum_j ||O_ref_j - O_j||^2) / (sqrt(sum_j ||O_ref_j||^2) + eps)
+   * with the norms over the positions j = 0..n_pos-1 and d together. */
+  int32_t n_pos;               /* positions, 1..DWKV_MAX_PROBE_POS; 0 reads as 1       */
+  const void* q_prev;          /* n_pos > 1: [n_pos-1][B][Hq][d] in the decode's q_type,
+                                  slice j-1 the query of the position j steps back
+                                  (16-byte aligned); ignored when n_pos <= 1           */
 } dwkv_probe;
 
 int32_t dwkv_abi_version(void);
@@ -154,8 +166,10 @@ size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe);
  * split-K pass and the merge; with a probe, 3 on the general kernel -- the
  * reference pass is added and one merge covers both -- and 4 on the
  * token-lane kernel, whose merge is followed by a small merge of the probed
- * heads' reference partials), or -1 when the dims or probe are invalid.
- * probe may be NULL. */
+ * heads' reference partials; a probe over n_pos > 1 positions adds two split
+ * passes -- factorized and reference, on the probed heads -- for every
+ * earlier position that still sees a token of some sequence, and one merge),
+ * or -1 when the dims or probe are invalid.  probe may be NULL. */
 int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe);
 
 /* Per-layer decode attention over the factorized cache (Eq. 1 folded into the

@@ -56,11 +56,19 @@ def hbm_read(buf, sink):
 
 @dataclass
 class ProbeRef:
-    """Dense higher-fidelity reference cache for Eq. 3 (fp16 [n][T][d] device tensors)."""
+    """Dense higher-fidelity reference cache for Eq. 3 (fp16 [n][T][d] device
+    tensors).  q_prev, optional, holds the queries of earlier decode positions
+    ([P-1][B][Hq][d], the decode query's dtype, slice j-1 from j steps back):
+    the probe then evaluates P positions, the norms over positions and d."""
     kv_heads: list
     k_ref: object
     v_ref: object
     eps: float = 1e-6
+    q_prev: object = None
+
+    @property
+    def n_pos(self) -> int:
+        return 1 if self.q_prev is None else 1 + int(self.q_prev.shape[0])
 
 
 class DeviceCache:
@@ -154,6 +162,12 @@ class DeviceCache:
         p.eps = probe.eps
         p.err = err.data_ptr()
         p.out_ref = out_ref.data_ptr() if out_ref is not None else None
+        p.n_pos = probe.n_pos
+        if probe.q_prev is not None:
+            qp = probe.q_prev
+            if tuple(qp.shape[1:]) != (self.batch, self.n_q_heads, self.head_dim) or not qp.is_contiguous():
+                raise ValueError("q_prev must be a contiguous [P-1, B, Hq, d] tensor")
+            p.q_prev = qp.data_ptr()
         return p, heads
 
     def workspace_bytes(self, probe: ProbeRef | None = None) -> int:
@@ -173,7 +187,7 @@ class DeviceCache:
     def workspace(self, probe: ProbeRef | None = None):
         """A decode workspace, allocated once per probe shape and reused."""
         need = self.workspace_bytes(probe)
-        key = None if probe is None else len(probe.kv_heads)
+        key = None if probe is None else (len(probe.kv_heads), probe.n_pos)
         ws = self._ws.get(key)
         if ws is None or ws.numel() < need:
             ws = self.new_workspace(probe)
@@ -197,6 +211,8 @@ class DeviceCache:
         G = Hq // self.n_kv_heads
         out_ref = None
         if probe is not None:
+            if probe.q_prev is not None and probe.q_prev.dtype != q.dtype:
+                raise TypeError("q_prev must have the decode query's dtype")
             n = len(probe.kv_heads)
             if err is None:
                 err = torch.empty((B, n * G), dtype=torch.float32, device=self.device)

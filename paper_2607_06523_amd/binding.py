@@ -55,7 +55,7 @@ class Controller(C.Structure):
 class Probe(C.Structure):
     _fields_ = [("n_heads", C.c_int32), ("kv_heads_host", C.POINTER(C.c_int32)),
                 ("k_ref", C.c_void_p), ("v_ref", C.c_void_p), ("eps", C.c_float),
-                ("err", C.c_void_p), ("out_ref", C.c_void_p)]
+                ("err", C.c_void_p), ("out_ref", C.c_void_p), ("n_pos", C.c_int32), ("q_prev", C.c_void_p)]
 
 
 EXPORTS = ["dwkv_abi_version", "dwkv_status_str", "dwkv_split_tokens", "dwkv_decode_kernel", "dwkv_workspace_bytes",
@@ -69,6 +69,9 @@ EXPORTS = ["dwkv_abi_version", "dwkv_status_str", "dwkv_split_tokens", "dwkv_dec
 _lib = None
 
 
+ABI_VERSION = 4      # DWKV_ABI_VERSION of the structures above
+
+
 def load(path: str = LIB_PATH):
     """Load libdwkv.so (raises when it has not been built)."""
     global _lib
@@ -79,6 +82,9 @@ def load(path: str = LIB_PATH):
     lib = C.CDLL(path)
     P = C.POINTER
     lib.dwkv_abi_version.restype = C.c_int32
+    if lib.dwkv_abi_version() != ABI_VERSION:
+        raise ImportError(f"{path} has ABI version {lib.dwkv_abi_version()}, the binding expects "
+                          f"{ABI_VERSION}: rebuild it with paper_2607_06523_amd.build.build()")
     lib.dwkv_status_str.restype = C.c_char_p
     lib.dwkv_status_str.argtypes = [C.c_int]
     lib.dwkv_split_tokens.restype = C.c_int32

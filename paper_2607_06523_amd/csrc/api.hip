@@ -70,7 +70,7 @@ bool uses_token_lane(const dwkv_dims* d) {
          chunks * g * kPartStrideTL * (int64_t)sizeof(float) < ((int64_t)1 << 31);
 }
 
-int64_t count_work(const dwkv_dims* d, int split);
+int64_t count_work(const dwkv_dims* d, int split, int trim = 0);
 
 int plan_split(const dwkv_dims* d) {
   if (d->split_tokens > 0) return d->split_tokens;
@@ -113,14 +113,18 @@ int plan_split_ref(const dwkv_dims* d, int n_heads) {
   return (int)c;
 }
 
-int64_t count_work(const dwkv_dims* d, int split) {
+// Work items of a pass over chunks of `split` tokens, every sequence cut
+// `trim` tokens short.
+int64_t count_work(const dwkv_dims* d, int split, int trim) {
   int64_t n = 0;
   for (int b = 0; b < d->batch; ++b) {
-    const int64_t tb = d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b];
+    const int64_t tb = std::max<int64_t>(d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b] - trim, 0);
     n += (tb + split - 1) / split;
   }
   return n;
 }
+
+int probe_positions(const dwkv_probe* p) { return p && p->n_pos > 1 ? p->n_pos : 1; }
 
 dwkv_status check_probe(const dwkv_dims* d, const dwkv_probe* p) {
   if (!p) return DWKV_OK;
@@ -134,12 +138,19 @@ dwkv_status check_probe(const dwkv_dims* d, const dwkv_probe* p) {
     seen[h] = true;
   }
   if (!(p->eps >= 0.f)) return DWKV_E_DIMS;
+  if (p->n_pos < 0 || p->n_pos > DWKV_MAX_PROBE_POS) return DWKV_E_DIMS;
+  if (p->n_pos > 1) {
+    if (!p->q_prev) return DWKV_E_NULL;
+    if (!aligned16(p->q_prev)) return DWKV_E_ALIGN;
+  }
   return DWKV_OK;
 }
 
-// Workspace: the partials of the decode pass, then those of the probe pass.
+// Workspace: the partials of the decode pass, then those of the probe pass;
+// with several probe positions, for each earlier position its rebuilt and
+// reference partials (pos_bytes each), then the Eq. 3 sums of the current one.
 struct WsLayout {
-  size_t main_bytes, ref_bytes, total;
+  size_t main_bytes, ref_bytes, pos_bytes, acc_off, total;
 };
 
 WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
@@ -151,21 +162,25 @@ WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
   w.main_bytes = align_up((size_t)nw * d->n_kv_heads * g * stride * sizeof(float), 256);
   const int64_t nw_ref = p ? count_work(d, plan_split_ref(d, p->n_heads)) : 0;
   w.ref_bytes = p ? align_up((size_t)nw_ref * p->n_heads * g * kPartStride * sizeof(float), 256) : 0;
-  w.total = w.main_bytes + w.ref_bytes;
+  const int np = probe_positions(p);
+  w.pos_bytes = np > 1 ? w.ref_bytes : 0;
+  w.acc_off = w.main_bytes + w.ref_bytes + (size_t)(np - 1) * 2 * w.pos_bytes;
+  const size_t acc_bytes = np > 1 ? align_up((size_t)d->batch * p->n_heads * g * 2 * sizeof(float), 256) : 0;
+  w.total = w.acc_off + acc_bytes;
   if (w.total == 0) w.total = 256;
   return w;
 }
 
 dwkv_status hip_status(hipError_t e) { return e == hipSuccess ? DWKV_OK : DWKV_E_HIP; }
 
-WorkTable work_table(const dwkv_dims* d, int split) {
+WorkTable work_table(const dwkv_dims* d, int split, int trim = 0) {
   WorkTable t;
   std::memset(&t, 0, sizeof(t));
   if (d->batch > kKernargSeqs) return t;
   t.n_seq = d->batch;
   for (int b = 0; b <= d->batch; ++b) t.tok[b] = d->cu_seqlens_host[b];
   for (int b = 0; b < d->batch; ++b) {
-    const int64_t len = d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b];
+    const int64_t len = std::max<int64_t>(d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b] - trim, 0);
     t.work[b + 1] = t.work[b] + (int32_t)((len + split - 1) / split);
   }
   return t;
@@ -210,7 +225,11 @@ size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe) {
 int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe) {
   if (check_dims(dims) != DWKV_OK || check_probe(dims, probe) != DWKV_OK) return -1;
   if (!probe) return 2;
-  return uses_token_lane(dims) ? 4 : 3;
+  int32_t n = uses_token_lane(dims) ? 4 : 3;
+  const int np = probe_positions(probe), split = plan_split_ref(dims, probe->n_heads);
+  for (int j = 1; j < np; ++j)
+    if (count_work(dims, split, j) > 0) n += 2;
+  return np > 1 ? n + 1 : n;
 }
 
 }  // extern "C"
@@ -318,6 +337,31 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
     r.n_work = (int32_t)nw_ref;
     r.wt = work_table(d, r.split);
     if (launch_split(kHeadDim, G, false, true, r, (int)nw_ref, s) != hipSuccess) return DWKV_E_HIP;
+    // earlier positions: the query j steps back over the sequences cut j
+    // tokens short, on the factorized cache (general kernel, probed heads
+    // only) and on the reference
+    for (int j = 1; j < probe_positions(probe); ++j) {
+      const int64_t nwj = count_work(d, r.split, j);
+      if (nwj == 0) continue;
+      char* pos = ws + wl.main_bytes + wl.ref_bytes + (size_t)(j - 1) * 2 * wl.pos_bytes;
+      SplitArgs f = a;
+      f.q = static_cast<const uint16_t*>(probe->q_prev) + (int64_t)(j - 1) * d->batch * d->n_q_heads * kHeadDim;
+      f.n_slots = probe->n_heads;
+      for (int i = 0; i < probe->n_heads; ++i) f.kv_of_slot[i] = probe->kv_heads_host[i];
+      f.split = r.split;
+      f.n_work = (int32_t)nwj;
+      f.wt = work_table(d, r.split, j);
+      f.trim = j;
+      f.part = reinterpret_cast<float*>(pos);
+      if (launch_split(RB, G, max_level(d) > 0, false, f, (int)nwj, s) != hipSuccess) return DWKV_E_HIP;
+      SplitArgs fr = r;
+      fr.q = f.q;
+      fr.n_work = f.n_work;
+      fr.wt = f.wt;
+      fr.trim = j;
+      fr.part = reinterpret_cast<float*>(pos + wl.pos_bytes);
+      if (launch_split(kHeadDim, G, false, true, fr, (int)nwj, s) != hipSuccess) return DWKV_E_HIP;
+    }
   }
   return DWKV_OK;
 }
@@ -387,6 +431,14 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
       mg.kv_of_probe[i] = probe->kv_heads_host[i];
     }
   mg.probe_only = tl ? 1 : 0;
+  const int np = probe_positions(probe);
+  if (np > 1) mg.acc = reinterpret_cast<float*>(ws + wl.acc_off);
+  hipError_t e = launch_merge(mg, s);
+  if (e != hipSuccess || np == 1) return hip_status(e);
+  // the earlier positions' sums, then err
+  mg.part_pos = reinterpret_cast<const float*>(ws + wl.main_bytes + wl.ref_bytes);
+  mg.pos_stride = (int64_t)(wl.pos_bytes / sizeof(float));
+  mg.n_pos = np;
   return hip_status(launch_merge(mg, s));
 }
 

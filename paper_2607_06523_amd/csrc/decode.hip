@@ -571,7 +571,7 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   const int w = blockIdx.x;
   int b;
   Ctx x;
-  work_item(a.wt, a.cu, a.batch, a.split, w, b, x.c0, x.c1);
+  work_item(a.wt, a.cu, a.batch, a.split, w, b, x.c0, x.c1, a.trim);
   x.c1 = min(x.c1, a.T);
   x.c0 = min(x.c0, x.c1);
   x.tb = x.c0 & ~(int64_t)15;
@@ -579,8 +579,10 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   x.T = a.T;
   x.nblk = (a.T + 15) / 16;
   x.res_stride = a.res_stride;
-  x.ck = a.coef_k + (int64_t)slot * (IDENT ? a.T : x.nblk * 16) * RB;
-  x.cv = a.coef_v + (int64_t)slot * x.nblk * 16 * RB;
+  // the reference rows are stored per probed slot, the factorized cache per KV head
+  const int64_t ch = IDENT ? slot : kvh;
+  x.ck = a.coef_k + ch * (IDENT ? a.T : x.nblk * 16) * RB;
+  x.cv = a.coef_v + ch * x.nblk * 16 * RB;
   if constexpr (RESID) {
     x.off = a.off + (int64_t)kvh * (a.T + 1);
     x.idx[0] = a.idx_k + (int64_t)kvh * a.res_stride;
@@ -1001,7 +1003,12 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
       if (tid == 0) {
         float sd = 0.f, sr = 0.f;
         for (int i = 0; i < kMergeThreads / 64; ++i) { sd += red2[0][i]; sr += red2[1][i]; }
-        a.err[col] = sqrtf(sd) / (sqrtf(sr) + a.eps);
+        if (a.acc) {
+          a.acc[2 * col] = sd;
+          a.acc[2 * col + 1] = sr;
+        } else {
+          a.err[col] = sqrtf(sd) / (sqrtf(sr) + a.eps);
+        }
       }
     }
   }
@@ -1049,6 +1056,59 @@ __global__ __launch_bounds__(kProbeThreads) void probe_merge_kernel(const MergeA
   if (tid == 0) {
     float sd = 0.f, sr = 0.f;
     for (int i = 0; i < kProbeThreads / 64; ++i) { sd += red2[0][i]; sr += red2[1][i]; }
+    if (a.acc) {
+      a.acc[2 * col] = sd;
+      a.acc[2 * col + 1] = sr;
+    } else {
+      a.err[col] = sqrtf(sd) / (sqrtf(sr) + a.eps);
+    }
+  }
+}
+
+// Eq. 3 over the earlier query positions: one workgroup per (probed query
+// head, sequence).  For every position j = 1..n_pos-1 it merges the rebuilt
+// and the reference partials of the sequence cut j tokens short (none when
+// T_b <= j: the position adds nothing), adds their squared distance and the
+// reference's squared norm to the current position's sums, and writes
+// sqrt(sum d^2) / (sqrt(sum r^2) + eps).
+__global__ __launch_bounds__(kMergeThreads) void probe_pos_merge_kernel(const MergeArgs a) {
+  __shared__ float red_m[kMergeGroups], red_l[kMergeGroups];
+  __shared__ f4 red_o[kMergeThreads];
+  __shared__ float red2[2][kMergeThreads / 64];
+  const int b = blockIdx.y, tid = threadIdx.x;
+  const int G = a.n_q_heads / a.n_kv_heads;
+  const int sl = blockIdx.x / G, g = blockIdx.x % G;
+  const int sg = tid / (D / 4);
+  const int64_t col = (int64_t)b * a.n_probe * G + sl * G + g;
+  const int len = a.cu[b + 1] - a.cu[b];
+  float d2 = 0.f, r2 = 0.f;
+  for (int j = 1; j < a.n_pos; ++j) {
+    // work items of sequence b in the pass over sequences cut j tokens short
+    int base = 0;
+    for (int i = 0; i < b; ++i) base += (max(a.cu[i + 1] - a.cu[i] - j, 0) + a.ref_split - 1) / a.ref_split;
+    const int ns = (max(len - j, 0) + a.ref_split - 1) / a.ref_split;
+    const float* pm = a.part_pos + (int64_t)(j - 1) * 2 * a.pos_stride;
+    const int64_t row0 = (int64_t)base * a.n_probe * G + sl * G + g, step = (int64_t)a.n_probe * G;
+    const f4 o = merge_rows(pm, row0, step, ns, kPartStride, D, D, red_m, red_l, red_o).x;
+    const f4 r = merge_rows(pm + a.pos_stride, row0, step, ns, kPartStride, D, D, red_m, red_l, red_o).x;
+    if (sg == 0) {
+      const float dx = r.x - o.x, dy = r.y - o.y, dz = r.z - o.z, dw = r.w - o.w;
+      d2 += dx * dx + dy * dy + dz * dz + dw * dw;
+      r2 += r.x * r.x + r.y * r.y + r.z * r.z + r.w * r.w;
+    }
+  }
+  for (int o2 = 32; o2 > 0; o2 >>= 1) {
+    d2 += __shfl_xor(d2, o2);
+    r2 += __shfl_xor(r2, o2);
+  }
+  if ((tid & 63) == 0) {
+    red2[0][tid >> 6] = d2;
+    red2[1][tid >> 6] = r2;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float sd = a.acc[2 * col], sr = a.acc[2 * col + 1];
+    for (int i = 0; i < kMergeThreads / 64; ++i) { sd += red2[0][i]; sr += red2[1][i]; }
     a.err[col] = sqrtf(sd) / (sqrtf(sr) + a.eps);
   }
 }
@@ -1095,6 +1155,11 @@ hipError_t launch_split(int rb, int g, bool resid, bool ident, const SplitArgs& 
 }
 
 hipError_t launch_merge(const MergeArgs& a, hipStream_t s) {
+  if (a.part_pos) {
+    const int g = a.n_q_heads / a.n_kv_heads;
+    hipLaunchKernelGGL(probe_pos_merge_kernel, dim3(a.n_probe * g, a.batch), dim3(kMergeThreads), 0, s, a);
+    return hipGetLastError();
+  }
   if (a.probe_only) {
     const int g = a.n_q_heads / a.n_kv_heads;
     hipLaunchKernelGGL(probe_merge_kernel, dim3(a.n_probe * g, a.batch), dim3(kProbeThreads), 0, s, a);

@@ -107,6 +107,7 @@ struct SplitArgs {
   int32_t kv_of_slot[DWKV_MAX_PROBE_HEADS];
   WorkTable wt;
   float* mstats;               // token-lane merge: merged (m*, l*) per [B][Hq] when not null
+  int32_t trim;                // tokens dropped from the end of every sequence (earlier probe positions)
 };
 
 // Split merge (and Eq. 3 for probed heads): grid = (Hq, B).
@@ -137,6 +138,17 @@ struct MergeArgs {
   // only the reference partials are merged and Eq. 3 evaluated against them
   int32_t probe_only;
   int32_t kv_of_probe[DWKV_MAX_PROBE_HEADS];
+  // probe over several query positions: the current position's merge writes
+  // (sum d^2, sum r^2) per probed column to acc [B][n_probe*G][2] instead of
+  // err; the position merge (grid (n_probe * G, B)) adds the earlier
+  // positions' sums and writes err.  Position j (1..n_pos-1) keeps its
+  // rebuilt partials at part_pos + (j-1) * 2 * pos_stride and its reference
+  // partials pos_stride floats further, both [work][n_probe][G][kPartStride]
+  // over chunks of ref_split tokens of the sequences cut j tokens short.
+  float* acc;
+  const float* part_pos;
+  int64_t pos_stride;
+  int32_t n_pos;
 };
 
 // Makes the kernel-argument values the whole split kernel needs live in scalar
@@ -149,9 +161,11 @@ __device__ __forceinline__ void pin_split_args(const SplitArgs& a, int kvh) {
                "s"(a.n_q_heads), "s"(a.q_bf16), "s"(a.qscale), "s"(a.part), "s"(a.n_work));
 }
 
-// Sequence b and token chunk [c0, c1) of work item w.
+// Sequence b and token chunk [c0, c1) of work item w.  With trim > 0 every
+// sequence ends trim tokens early (a query of an earlier decode position sees
+// that prefix); the work table then counts the trimmed lengths.
 __device__ __forceinline__ void work_item(const WorkTable& wt, const int32_t* cu, int batch, int split,
-                                          int w, int& b, int64_t& c0, int64_t& c1) {
+                                          int w, int& b, int64_t& c0, int64_t& c1, int trim = 0) {
   if (__builtin_expect(wt.n_seq > 0, 1)) {
     // branch-free scan of the whole table: every read is at a fixed argument
     // offset, so they are all issued at once
@@ -168,16 +182,16 @@ __device__ __forceinline__ void work_item(const WorkTable& wt, const int32_t* cu
     }
     b = bw;
     c0 = (int64_t)t0 + (int64_t)(w - w0) * split;
-    c1 = t1;
+    c1 = t1 - trim;
   } else {
     int base = 0;
     for (b = 0; b < batch - 1; ++b) {
-      const int ns = (cu[b + 1] - cu[b] + split - 1) / split;
+      const int ns = (max(cu[b + 1] - cu[b] - trim, 0) + split - 1) / split;
       if (w < base + ns) break;
       base += ns;
     }
     c0 = (int64_t)cu[b] + (int64_t)(w - base) * split;
-    c1 = cu[b + 1];
+    c1 = cu[b + 1] - trim;
   }
   c1 = c1 < c0 + split ? c1 : c0 + split;
   c0 = c0 < c1 ? c0 : c1;

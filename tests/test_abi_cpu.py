@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.dwkv_abi_version() == 3
+    assert lib.dwkv_abi_version() == 4
     for s, text in [(0, b"ok"), (3, b"unsupported shape"), (5, b"malformed cache layout"),
                     (7, b"device pointer not 16-byte aligned")]:
         assert lib.dwkv_status_str(s) == text
@@ -130,6 +130,24 @@ def test_probe_argument_checks(lib):
     need = lib.dwkv_workspace_bytes(C.byref(d), C.byref(p))
     assert need > lib.dwkv_workspace_bytes(C.byref(d), None)
     assert decode_status(lib, d, probe=p, ws=need - 1) == 4
+    # several positions: q_prev required and aligned, at most 8 positions,
+    # per earlier position two more reference-sized regions and the sums
+    p.n_pos = 3
+    assert decode_status(lib, d, probe=p) == 1           # q_prev missing
+    p.q_prev = FAKE + 2
+    assert decode_status(lib, d, probe=p) == 7           # misaligned
+    p.q_prev = FAKE
+    for bad in (-1, 9):
+        p.n_pos = bad
+        assert decode_status(lib, d, probe=p) == 2
+    p.n_pos = 3
+    need3 = lib.dwkv_workspace_bytes(C.byref(d), C.byref(p))
+    ref = need - lib.dwkv_workspace_bytes(C.byref(d), None)
+    G = d.n_q_heads // d.n_kv_heads
+    assert need3 == need + 2 * 2 * ref + up256(d.batch * 2 * G * 2 * 4)
+    assert decode_status(lib, d, probe=p, ws=need3 - 1) == 4
+    p.n_pos = 0
+    assert lib.dwkv_workspace_bytes(C.byref(d), C.byref(p)) == need
 
 
 def up256(n):
@@ -196,6 +214,16 @@ def test_decode_launch_count(lib):
     assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3
     d, keep = dims(n_q_heads=7)
     assert lib.dwkv_decode_launches(C.byref(d), None) == -1
+    # several positions: two passes per earlier position that still sees a
+    # token, then one merge; lengths 700, 0 and 2 with 4 positions and 256-token
+    # chunks: positions 1 and 2 see tokens (of the first sequences), 3 only of the first
+    d, keep = dims(batch=3, cu_seqlens_host=[0, 700, 700, 702], total_tokens=702, split_tokens=256)
+    p.n_pos, p.q_prev = 4, FAKE
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 4 + 2 * 3 + 1
+    d, keep = dims(batch=2, cu_seqlens_host=[0, 2, 3], total_tokens=3, split_tokens=256)
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 4 + 2 * 1 + 1
+    p.n_pos = 1
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 4
 
 
 def test_route_range_and_compress_argument_checks(lib):

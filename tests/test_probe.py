@@ -130,3 +130,56 @@ def test_probe_full_size_70b_shape():
     out, err, out_ref = _run_probe(dc, 3, heads, K, V)
     e_ref = oracle.probe(host, 3, heads, K, V)
     assert np.abs(err - e_ref).max() <= 1e-4 + 1e-3 * np.abs(e_ref).max(), (err, e_ref)
+
+
+POS_CASES = [
+    # name, G, r_b, levels, probs, lengths, split, positions
+    # general kernel: a 1025-token sequence loses its last 256-token chunk
+    # one position back; a 2-token one sees positions 0 and 1 only
+    ("general-g4-p4", 4, 64, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), [1025, 2, 1700], 256, 4),
+    ("tl-g4-p3", 4, 48, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), [2049, 0, 1500], 512, 3),
+    ("tl-g8-p8", 8, 64, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), [3, 1800, 7], 256, 8),
+]
+
+
+@pytest.mark.parametrize("case", POS_CASES, ids=[c[0] for c in POS_CASES])
+def test_probe_positions_match_oracle(case):
+    """Eq. 3 over several recent positions: the query j steps back attends to
+    the first T_b - j tokens; the norms run over positions and d together."""
+    torch = torch_gpu()
+    from paper_2607_06523_amd import ProbeRef
+    from synth.layout import block_values
+    name, G, rb, levels, probs, lengths, split, P = case
+    w = _Fixed(Workload(name="probepos-" + name, batch=len(lengths), n_layers=2, window=2, n_kv_heads=4,
+                        n_q_heads=4 * G, head_dim=128, context=max(lengths), basis_rank=rb, levels=levels,
+                        probs=probs, q_dtype="bf16", seed=61), lengths)
+    host = generate(w, threads=4)
+    dc = device_cache(host, split_tokens=split)
+    heads, layer = [2, 0], 1
+    K, V = _refs(host, layer, heads, 0.05, seed=5)
+    rng = np.random.default_rng(7)
+    q_prev = torch.from_numpy(rng.standard_normal((P - 1, host.batch, host.n_q_heads, 128)).astype(np.float32)
+                              ).to(torch.bfloat16)
+    qs = np.concatenate([oracle.q_to_f64(host.q_bits[layer], "bf16")[None],
+                         q_prev.float().numpy().astype(np.float64)])
+    pr = ProbeRef(heads, torch.from_numpy(K.view(np.uint16)).view(torch.float16).cuda(),
+                  torch.from_numpy(block_values(V).view(np.uint16)).view(torch.float16).cuda(), 1e-6,
+                  q_prev=q_prev.cuda())
+    announce(f"probe positions {name} P={P} layer {layer} heads 2,0 lengths {lengths} split {split}")
+    out, err, _ = dc.decode(layer, probe=pr)
+    err = err.cpu().numpy()
+    e_ref = oracle.probe_positions(host, layer, heads, K, V, qs)
+    assert np.abs(err - e_ref).max() <= 1e-4 + 1e-3 * np.abs(e_ref).max(), (err, e_ref)
+    # the earlier positions change the error (they are not ignored)
+    e_cur = oracle.probe(host, layer, heads, K, V)
+    nonempty = [b for b in range(host.batch) if host.cu_seqlens[b + 1] - host.cu_seqlens[b] > 1]
+    assert np.abs(e_cur - e_ref)[nonempty].max() > 10 * (1e-4 + 1e-3 * np.abs(e_ref).max())
+    for b, L in enumerate(lengths):
+        if L == 0:
+            assert np.all(err[b] == 0)
+    # the decode output is unchanged by probing
+    compare(out.cpu().numpy(), oracle.decode(host, layer), [(b, h) for b in range(host.batch) for h in range(4)],
+            G, f"probe positions {name} out")
+    # two calls in a row agree bit for bit
+    _, err2, _ = dc.decode(layer, probe=pr)
+    assert np.array_equal(err, err2.cpu().numpy())
