@@ -429,6 +429,22 @@ typedef struct dwkv_controller {
 dwkv_status dwkv_controller_update(const dwkv_controller* ctl, int32_t n_windows, int32_t n_thresholds,
                                    const float* err_host, float* theta_host, int32_t* below_host);
 
+/* Probe schedule (Sec. 3: every p decode steps a small subset of heads and
+ * recent query positions is evaluated twice).  The paper fixes neither the
+ * subset nor p; the schedule here rotates it: decode step `step` (0-based,
+ * counted from the first decode step after prefill) probes when
+ * step % period == 0, and the k-th probe (k = step / period) takes the KV
+ * heads (k * n_heads + i) % n_kv_heads, i < n_heads, so every head is probed
+ * in every ceil(n_kv_heads / n_heads) consecutive probes, over
+ * min(n_pos, step + 1) recent positions (the decode steps so far).
+ *   heads_host: [n_heads] written on a probe step (for dwkv_probe.kv_heads_host)
+ *   n_pos_host: written, the positions to probe (0 on other steps)
+ * Returns n_heads on a probe step, 0 on other steps, -1 for bad arguments
+ * (period < 1, n_heads outside 1..min(n_kv_heads, 64), n_pos outside 1..8,
+ * step < 0, null pointers).  Host code. */
+int32_t dwkv_probe_schedule(int64_t step, int32_t period, int32_t n_heads, int32_t n_kv_heads, int32_t n_pos,
+                            int32_t* heads_host, int32_t* n_pos_host);
+
 /* Comparison paths (the fused decode's alternatives: the paper's "full KV"
  * baseline and its "w/o fused kernel" ablation, Table 1 and Table 2).
  *

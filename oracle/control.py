@@ -19,6 +19,14 @@ the two-level form of Eq. 2 (rho_min, rho_max): with E residual entries
 allowed for the window and head, and N tokens, the n = floor((E - N rho_min) /
 (rho_max - rho_min)) tokens of largest router score z (ties to the lower token
 index; clamped to [0, N]) get rho_max and the rest rho_min.
+
+Probe schedule: the probe runs every p decode steps on a small subset of heads
+and recent query positions.  Reading used here: decode step s (0-based, counted
+from the first decode step after prefill) probes when s mod p == 0; the k-th
+probe (k = s / p) takes the n KV heads (k n + i) mod Hkv, i = 0..n-1, so the
+subset rotates and every head is probed in every ceil(Hkv / n) consecutive
+probes; it evaluates min(P, s + 1) recent positions (the decode steps so far,
+the current one included).
 """
 from __future__ import annotations
 
@@ -73,3 +81,12 @@ def route_budget(phi, u, entries, levels, t0: int, t1: int, codes, off):
             codes[m, h, t0:t1] = k
             off[m, h, t0 + 1:t1 + 1] = int(off[m, h, t0]) + np.cumsum(lev[k.astype(np.int64)])
     return codes, off
+
+
+def probe_schedule(step: int, period: int, n_heads: int, n_kv_heads: int, n_pos: int):
+    """(probed KV heads, positions) at decode step `step`; ([], 0) when the
+    step does not probe."""
+    if step % period != 0:
+        return [], 0
+    k = step // period
+    return [(k * n_heads + i) % n_kv_heads for i in range(n_heads)], min(n_pos, step + 1)

@@ -21,7 +21,8 @@ import numpy as np
 from . import binding, layout
 from .binding import DwkvError, F16, BF16
 
-__all__ = ["DeviceCache", "ProbeRef", "DwkvError", "load", "F16", "BF16", "hbm_read", "hbm_read_blocks"]
+__all__ = ["DeviceCache", "ProbeRef", "DwkvError", "load", "F16", "BF16", "hbm_read", "hbm_read_blocks",
+           "probe_schedule"]
 
 
 def load():
@@ -34,6 +35,19 @@ def _ptr(t):
 
 def _stream(torch, device):
     return C.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def probe_schedule(step: int, period: int, n_heads: int, n_kv_heads: int, n_pos: int = 1):
+    """dwkv_probe_schedule: (probed KV heads, positions) at decode step
+    `step`, ([], 0) on a step that does not probe."""
+    lib = load()
+    heads = (C.c_int32 * max(1, n_heads))()
+    npos = C.c_int32(0)
+    n = lib.dwkv_probe_schedule(int(step), int(period), int(n_heads), int(n_kv_heads), int(n_pos), heads,
+                                C.byref(npos))
+    if n < 0:
+        raise DwkvError(2, "dwkv_probe_schedule")
+    return list(heads[:n]), int(npos.value)
 
 
 def hbm_read_blocks() -> int:

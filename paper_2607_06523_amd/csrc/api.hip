@@ -934,6 +934,19 @@ dwkv_status dwkv_controller_update(const dwkv_controller* ctl, int32_t n_windows
   return DWKV_OK;
 }
 
+int32_t dwkv_probe_schedule(int64_t step, int32_t period, int32_t n_heads, int32_t n_kv_heads, int32_t n_pos,
+                            int32_t* heads_host, int32_t* n_pos_host) {
+  if (step < 0 || period < 1 || n_kv_heads < 1 || n_heads < 1 || n_heads > n_kv_heads ||
+      n_heads > DWKV_MAX_PROBE_HEADS || n_pos < 1 || n_pos > DWKV_MAX_PROBE_POS || !heads_host || !n_pos_host)
+    return -1;
+  *n_pos_host = 0;
+  if (step % period != 0) return 0;
+  const int64_t k = step / period;
+  for (int32_t i = 0; i < n_heads; ++i) heads_host[i] = (int32_t)((k % n_kv_heads * n_heads + i) % n_kv_heads);
+  *n_pos_host = (int32_t)std::min<int64_t>(n_pos, step + 1);
+  return n_heads;
+}
+
 size_t dwkv_validate_workspace_bytes(void) { return 256; }
 
 dwkv_status dwkv_validate(const dwkv_dims* d, const dwkv_cache* c, int64_t* bad_index, void* workspace,

@@ -30,6 +30,8 @@ says what disagreed.  The pins are:
   below mass below G spike, uniform and ln-3 closed forms, the table fold;
   the probe-error feature on a hand-worked case (fresh fold, maximum fold,
   unprobed heads, an empty sequence);
+* the probe schedule: a hand-worked rotation table and its period, coverage
+  and distinctness invariants;
 * threshold control: a hand-worked feedback trace with clamps, the
   budget-driven selection against enumeration of the promoted sets, and
   budget routing of a token range against a running loop (exact scores,
@@ -1254,6 +1256,43 @@ def pin_control(o):
     return None
 
 
+def pin_probe_schedule(o):
+    """The probe schedule on a hand-worked table (Hkv 8, 3 heads, every 4
+    steps), and its invariants over many steps: probes only every p steps,
+    distinct heads, every head within each ceil(Hkv / n) consecutive probes
+    (exactly once per Hkv / n probes when n divides Hkv), positions limited by
+    the decode steps so far."""
+    OC = o.control
+    table = {0: [0, 1, 2], 4: [3, 4, 5], 8: [6, 7, 0], 12: [1, 2, 3], 16: [4, 5, 6]}
+    for s in range(20):
+        heads, npos = OC.probe_schedule(s, 4, 3, 8, 5)
+        if s in table:
+            if heads != table[s] or npos != min(5, s + 1):
+                return f"probe schedule step {s}: got {heads}, {npos}"
+        elif heads or npos:
+            return f"probe schedule probes at step {s}"
+    for hk, n, p in ((8, 1, 1), (8, 2, 3), (8, 3, 2), (5, 4, 1), (64, 8, 16), (8, 8, 2)):
+        probes = []
+        for s in range(0, 60 * p):
+            heads, npos = OC.probe_schedule(s, p, n, hk, 4)
+            if (s % p == 0) != bool(heads):
+                return f"probe schedule (Hkv {hk}, n {n}, p {p}) wrong at step {s}"
+            if heads:
+                if len(heads) != n or len(set(heads)) != n or not all(0 <= h < hk for h in heads):
+                    return f"probe schedule heads {heads} invalid"
+                if npos != min(4, s + 1):
+                    return "probe schedule positions wrong"
+                probes.append(heads)
+        span = -(-hk // n)
+        for k in range(len(probes) - span + 1):
+            seen = set(h for hs in probes[k:k + span] for h in hs)
+            if len(seen) != hk:
+                return f"probe schedule (Hkv {hk}, n {n}): probes {k}..{k + span - 1} miss a head"
+            if hk % n == 0 and sum(len(hs) for hs in probes[k:k + span]) != hk:
+                return "probe schedule repeats a head within a rotation"
+    return None
+
+
 def pin_route_budget(o):
     """Budget routing of a token range against a running loop written here:
     router scores in exact rational arithmetic rounded per operation, the n
@@ -1390,7 +1429,7 @@ def pin_int8_coefficients(o):
 ALL_PINS = [pin_query_formats, pin_nibbles, pin_residual_map, pin_brute_force, pin_closed_forms,
             pin_reductions, pin_invariants, pin_probe, pin_probe_positions, pin_router, pin_compress_closed_forms,
             pin_compress_rne_table, pin_compress_arithmetic, pin_compress_int8, pin_compress_bounds,
-            pin_compress_into_cache, pin_route_range, pin_attention_features, pin_probe_feature, pin_control, pin_route_budget, pin_sketch,
+            pin_compress_into_cache, pin_route_range, pin_attention_features, pin_probe_feature, pin_control, pin_probe_schedule, pin_route_budget, pin_sketch,
             pin_int8_coefficients]
 
 

@@ -447,3 +447,18 @@ def test_probe_feature_argument_checks(lib):
     assert f(phi=FAKE + 4) == 7 and f(err=FAKE + 2) == 7
     dup = np.array([1, 1], dtype=np.int32)
     assert f(h=dup.ctypes.data_as(C.POINTER(C.c_int32))) == 2
+
+
+def test_probe_schedule_matches_oracle(lib):
+    """The host probe schedule against the oracle's rotation, and its argument checks."""
+    import oracle.control as OC
+    from paper_2607_06523_amd import probe_schedule
+    for hk, n, p, P in ((8, 1, 1, 1), (8, 3, 4, 5), (5, 4, 2, 8), (64, 8, 16, 3), (8, 8, 1, 2)):
+        for s in list(range(0, 70)) + [10**12, 10**12 + p * 7]:
+            assert probe_schedule(s, p, n, hk, P) == OC.probe_schedule(s, p, n, hk, P), (hk, n, p, s)
+    h = (C.c_int32 * 8)()
+    npos = C.c_int32(0)
+    for args in ((-1, 1, 1, 8, 1), (0, 0, 1, 8, 1), (0, 1, 0, 8, 1), (0, 1, 9, 8, 1), (0, 1, 1, 8, 0),
+                 (0, 1, 1, 8, 9)):
+        assert lib.dwkv_probe_schedule(*args, h, C.byref(npos)) == -1, args
+    assert lib.dwkv_probe_schedule(0, 1, 1, 8, 1, None, C.byref(npos)) == -1

@@ -439,6 +439,12 @@ MUTANTS = {
     "probe positions see one token too many": [(F, "probe_positions", _pp_variant("plus_one"))],
     "probe positions pair the queries in reverse": [(F, "probe_positions", _pp_variant("reverse"))],
     "probe positions keep only the current one": [(F, "probe_positions", _pp_variant("first_only"))],
+    "probe schedule rotates by one head": [(CT, "probe_schedule", lambda s, p, n, hk, P: (
+        ([((s // p) + i) % hk for i in range(n)], min(P, s + 1)) if s % p == 0 else ([], 0)))],
+    "probe schedule probes one step late": [(CT, "probe_schedule", lambda s, p, n, hk, P: (
+        ([(((s - 1) // p) * n + i) % hk for i in range(n)], min(P, s)) if s % p == 1 % p else ([], 0)))],
+    "probe schedule ignores the step count for positions": [(CT, "probe_schedule", lambda s, p, n, hk, P: (
+        ([((s // p) * n + i) % hk for i in range(n)], P) if s % p == 0 else ([], 0)))],
     "router score in float64": [(R, "router_score", _router_fused)],
     "router score summed in reverse": [(R, "router_score", _router_reordered)],
     "router ties go up": [(R, "level_index", _level_ge)],
