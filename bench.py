@@ -114,23 +114,48 @@ def measure_append(dc, host, wl, torch, reps: int = 20):
         for l in range(L):
             dc.compress(l, x1[l][0], x1[l][1], T - 1, T)
 
-    append_step()
-    torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        append_step()
-    torch.cuda.synchronize()
+    out = torch.empty((host.batch, host.n_q_heads, d), dtype=torch.float32, device="cuda")
+
+    def decode_step():
+        for l in range(L):
+            dc.decode(l, out=out)
+
+    def two_step():                       # append, then decode, layer by layer
+        dc.route_range(phi_d, u_d, th_d, T - 1, T)
+        for l in range(L):
+            dc.compress(l, x1[l][0], x1[l][1], T - 1, T)
+            dc.decode(l, out=out)
+
+    def fused_step():                     # the decode that appends, layer by layer
+        dc.route_range(phi_d, u_d, th_d, T - 1, T)
+        for l in range(L):
+            dc.decode_append(l, x1[l][0].view(1, Hk, d), x1[l][1].view(1, Hk, d), out=out)
+
     stream = torch.cuda.current_stream()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    graph.replay()
-    torch.cuda.synchronize()
-    ev[0].record(stream)
-    for _ in range(reps):
+
+    def graph_us(fn):
+        fn()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            fn()
+        torch.cuda.synchronize()
         graph.replay()
-    ev[1].record(stream)
-    torch.cuda.synchronize()
-    step_us = ev[0].elapsed_time(ev[1]) / reps * 1e3
-    del graph
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for _ in range(reps):
+            graph.replay()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        t = ev[0].elapsed_time(ev[1]) / reps * 1e3
+        del graph
+        return t
+
+    step_us = graph_us(append_step)
+    dec_us = graph_us(decode_step)
+    two_us = graph_us(two_step)
+    fused_us = graph_us(fused_step)
     # prefill side: every token of one layer
     xk = torch.randn((T, Hk, d), generator=g, device="cuda").half()
     xv = torch.randn((T, Hk, d), generator=g, device="cuda").half()
@@ -145,10 +170,18 @@ def measure_append(dc, host, wl, torch, reps: int = 20):
     layer_ms = ev[0].elapsed_time(ev[1]) / n_rep
     return {"decode_token_append_us_per_step": round(step_us, 2),
             "append_launches_per_step": 3 + L,
+            "decode_step_us": round(dec_us, 2),
+            "append_then_decode_step_us": round(two_us, 2),
+            "decode_append_step_us": round(fused_us, 2),
+            "decode_append_overhead_us_per_step": round(fused_us - dec_us, 2),
+            "decode_append_launches_per_layer": dc.decode_append_launches,
             "prefill_compress_ms_per_layer": round(layer_ms, 4),
             "prefill_compress_vectors_per_s": round(2 * Hk * T / (layer_ms / 1e3), 1),
-            "note": "route_range of the new token in every window plus one dwkv_compress per layer "
-                    "(graph replay); prefill = dwkv_compress of all T tokens of one layer, K and V"}
+            "note": "graph replays: route_range of the new token in every window plus one dwkv_compress per "
+                    "layer (append alone); the 32-layer decode alone; route_range then per layer "
+                    "dwkv_compress + dwkv_decode; route_range then per layer dwkv_decode_append (the new "
+                    "token compressed inside the decode launch); overhead = that minus the decode alone. "
+                    "prefill = dwkv_compress of all T tokens of one layer, K and V"}
 
 
 def measure_int8(wl, torch, steps: int = 20, warmup: int = 5):

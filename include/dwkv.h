@@ -329,6 +329,38 @@ dwkv_status dwkv_compress(const dwkv_dims* dims, const dwkv_cache* cache, int32_
                           const void* x_k, const void* x_v, const float* gate, int64_t t0,
                           int64_t t1, void* stream);
 
+/* One decode step of layer `layer` that appends first: the new token of
+ * every non-empty sequence b is its last packed token t_b = cu[b+1] - 1 (its
+ * slot and routing already in the cache, as dwkv_compress requires);
+ *   dwkv_compress of t_b from x_k[b], x_v[b] (and gate), then
+ *   dwkv_decode of the layer (no probe),
+ * with the same stored factors (bit for bit those of dwkv_compress) and the
+ * same output semantics (the new token attended in its compressed form, Eq. 1).
+ * For query groups and ranks the token-lane kernel serves, fp16 coefficients
+ * and at most 16 sequences, it is one split-K launch plus the merge: the
+ * split items cover each sequence's tokens but its last, and one more
+ * workgroup per sequence and KV head compresses the new token, writes it to
+ * the cache and contributes its own term to the merge (its score against the
+ * key rebuilt from the stored factors, its value in basis space), so no
+ * workgroup reads what another writes.  Otherwise the append/compress kernel
+ * runs once per sequence, then the decode.  The output then differs from
+ * dwkv_compress + dwkv_decode only in float32 rounding order.
+ *   q, q_type, sm_scale, out: as in dwkv_decode
+ *   x_k, x_v: fp16 [B][Hkv][d] the new token's key / value of each sequence
+ *             (rows of empty sequences unused), 16-byte aligned
+ *   gate:     NULL (g = 1) or fp32 [2][Hkv][B], 4-byte aligned
+ *   workspace:>= dwkv_decode_append_workspace_bytes(dims) bytes of device
+ *             memory, no initial contents, clobbered
+ * WRITES the cache as dwkv_compress does.  Returns DWKV_OK once enqueued. */
+size_t dwkv_decode_append_workspace_bytes(const dwkv_dims* dims);
+/* Kernel launches of one dwkv_decode_append call: 2 on the one-launch path,
+ * else the number of non-empty sequences plus 2; -1 for invalid dims. */
+int32_t dwkv_decode_append_launches(const dwkv_dims* dims);
+dwkv_status dwkv_decode_append(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
+                               const void* q, int32_t q_type, float sm_scale, float* out,
+                               const void* x_k, const void* x_v, const float* gate,
+                               void* workspace, size_t ws_bytes, void* stream);
+
 /* Dense residual term g*R of Eq. 1 for packed tokens [t0, t1) of slab
  * (layer, z, kv_head): dense[t-t0][c] = res_scale * code for every stored entry
  * of token t at channel c, zero elsewhere; fp32 [t1-t0][d] (may be NULL when

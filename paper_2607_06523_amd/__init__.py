@@ -350,6 +350,43 @@ class DeviceCache:
                                     _ptr(gate), int(t0), int(t1), _stream(torch, self.device))
         binding.check(st, "dwkv_compress")
 
+    @property
+    def decode_append_launches(self) -> int:
+        return int(self.lib.dwkv_decode_append_launches(C.byref(self.dims)))
+
+    def decode_append(self, layer: int, x_k, x_v, gate=None, q=None, sm_scale: float | None = None, out=None,
+                      workspace=None):
+        """dwkv_decode_append: append the new token of every sequence (its
+        last) from x_k, x_v [B, Hkv, d] fp16 (gate None or fp32 [2, Hkv, B]),
+        then decode the layer; returns out [B, Hq, d] fp32."""
+        torch = self.torch
+        for x in (x_k, x_v):
+            if x.dtype != torch.float16 or not x.is_contiguous():
+                raise TypeError("x_k / x_v must be contiguous float16")
+        if gate is not None and (gate.dtype != torch.float32 or not gate.is_contiguous()):
+            raise TypeError("gate must be contiguous float32")
+        if q is None:
+            q = self.q[layer]
+        if q.dtype not in (torch.float16, torch.bfloat16):
+            raise TypeError("q must be float16 or bfloat16")
+        qt = F16 if q.dtype == torch.float16 else BF16
+        if out is None:
+            out = torch.empty((self.batch, self.n_q_heads, self.head_dim), dtype=torch.float32, device=self.device)
+        need = int(self.lib.dwkv_decode_append_workspace_bytes(C.byref(self.dims)))
+        if need == 0:
+            raise DwkvError(2, "dwkv_decode_append_workspace_bytes")
+        if workspace is None:
+            ws = self._ws.get("append")
+            if ws is None or ws.numel() < need:
+                ws = torch.zeros(need, dtype=torch.uint8, device=self.device)
+                self._ws["append"] = ws
+            workspace = ws
+        st = self.lib.dwkv_decode_append(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(q), qt,
+                                         float(sm_scale or 0.0), _ptr(out), _ptr(x_k), _ptr(x_v), _ptr(gate),
+                                         _ptr(workspace), workspace.numel(), _stream(torch, self.device))
+        binding.check(st, "dwkv_decode_append")
+        return out
+
     def decode_features(self, layer: int, phi, q=None, sm_scale: float | None = None, out=None, workspace=None):
         """dwkv_decode plus the router's attention features: phi fp32 [M, Hkv, T, 4]
         (columns 0 mass, 1 spike) is updated in place; returns out [B, Hq, d]."""

@@ -62,6 +62,7 @@ EXPORTS = ["dwkv_abi_version", "dwkv_status_str", "dwkv_split_tokens", "dwkv_dec
            "dwkv_decode_launches", "dwkv_decode", "dwkv_decode_partials", "dwkv_decode_merge",
            "dwkv_static_scratch_bytes", "dwkv_decode_noalloc", "dwkv_route_workspace_bytes", "dwkv_route",
            "dwkv_route_range", "dwkv_route_budget_workspace_bytes", "dwkv_route_budget", "dwkv_compress", "dwkv_features_workspace_bytes", "dwkv_decode_features", "dwkv_probe_feature", "dwkv_probe_schedule",
+           "dwkv_decode_append_workspace_bytes", "dwkv_decode_append_launches", "dwkv_decode_append",
            "dwkv_controller_update", "dwkv_sketch_workspace_bytes", "dwkv_sketch_basis", "dwkv_materialize", "dwkv_dense_workspace_bytes",
            "dwkv_dense_decode", "dwkv_residual_map",
            "dwkv_validate_workspace_bytes", "dwkv_validate", "dwkv_hbm_read_blocks", "dwkv_hbm_read"]
@@ -130,6 +131,13 @@ def load(path: str = LIB_PATH):
     lib.dwkv_decode_features.restype = C.c_int
     lib.dwkv_decode_features.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_void_p, C.c_int32, C.c_float,
                                          C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
+    lib.dwkv_decode_append_workspace_bytes.restype = C.c_size_t
+    lib.dwkv_decode_append_workspace_bytes.argtypes = [P(Dims)]
+    lib.dwkv_decode_append_launches.restype = C.c_int32
+    lib.dwkv_decode_append_launches.argtypes = [P(Dims)]
+    lib.dwkv_decode_append.restype = C.c_int
+    lib.dwkv_decode_append.argtypes = [P(Dims), P(Cache), C.c_int32, C.c_void_p, C.c_int32, C.c_float, C.c_void_p,
+                                       C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
     lib.dwkv_probe_schedule.restype = C.c_int32
     lib.dwkv_probe_schedule.argtypes = [C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32, P(C.c_int32),
                                         P(C.c_int32)]

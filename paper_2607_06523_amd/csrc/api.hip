@@ -247,10 +247,10 @@ dwkv_status check_decode_common(const dwkv_dims* d, const dwkv_probe* probe, voi
   return DWKV_OK;
 }
 
-// Split-K pass(es): partial (o, m, l) per (work item, head slot, group member).
-dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
-                           int32_t q_type, float sm_scale, const dwkv_probe* probe, void* workspace,
-                           hipStream_t s, float* scores = nullptr) {
+// Arguments of the layer's split-K pass over the whole cache (work split and
+// partial layout left to the caller); checks the cache pointers.
+dwkv_status split_args(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q, int32_t q_type,
+                       float sm_scale, void* workspace, SplitArgs& a) {
   if (!c || !q) return DWKV_E_NULL;
   if (!c->basis || !c->coef_k || !c->coef_v || !c->res_off || !c->res_idx || !c->res_val ||
       !c->res_scale)
@@ -259,7 +259,6 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   if (q_type != DWKV_F16 && q_type != DWKV_BF16) return DWKV_E_DIMS;
   const bool c8 = d->coef_format == DWKV_COEF_I8;
   if (c8) {
-    if (!uses_token_lane(d) || d->n_q_heads / d->n_kv_heads > 4 || probe || scores) return DWKV_E_UNSUPPORTED;
     if (!c->coef_k_scale || !c->coef_v_scale) return DWKV_E_NULL;
     if ((reinterpret_cast<uintptr_t>(c->coef_k_scale) | reinterpret_cast<uintptr_t>(c->coef_v_scale)) & 1u)
       return DWKV_E_ALIGN;
@@ -267,23 +266,14 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   const void* const ptrs[] = {q, c->basis, c->coef_k, c->coef_v, c->res_off, c->res_idx, c->res_val, c->res_scale};
   for (const void* p : ptrs)
     if (!aligned16(p)) return DWKV_E_ALIGN;
-  const WsLayout wl = ws_layout(d, probe);
-  const int G = d->n_q_heads / d->n_kv_heads;
   const int RB = d->basis_rank;
   const int64_t T = d->total_tokens;
   const int64_t T16 = (T + 15) / 16 * 16;
   const int64_t Hk = d->n_kv_heads;
   const int M = d->n_layers / d->window;
   const int m = layer / d->window;
-  const int split = plan_split(d);
-  const int64_t nw = count_work(d, split);
-  if (nw > 0x7fffffff) return DWKV_E_UNSUPPORTED;
-  if (nw == 0) return DWKV_OK;
   if (!(sm_scale > 0.f)) sm_scale = 1.0f / std::sqrt((float)kHeadDim);
-  char* ws = static_cast<char*>(workspace);
   const uint16_t* scale = static_cast<const uint16_t*>(c->res_scale);
-
-  SplitArgs a;
   std::memset(&a, 0, sizeof(a));
   if (c8) {                     // int8 codes: one byte per coefficient
     a.coef_k = reinterpret_cast<const uint16_t*>(static_cast<const uint8_t*>(c->coef_k) + (int64_t)layer * Hk * T16 * RB);
@@ -305,18 +295,39 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   a.scale_v = scale + ((int64_t)layer * 2 + 1) * Hk * T;
   a.q = static_cast<const uint16_t*>(q);
   a.cu = d->cu_seqlens;
-  a.part = reinterpret_cast<float*>(ws);
+  a.part = static_cast<float*>(workspace);
   a.T = T;
   a.res_stride = d->res_stride;
   a.batch = d->batch;
   a.n_q_heads = d->n_q_heads;
   a.n_kv_heads = d->n_kv_heads;
   a.n_slots = d->n_kv_heads;
-  a.split = split;
-  a.n_work = (int32_t)nw;
   a.q_bf16 = q_type == DWKV_BF16;
   a.qscale = sm_scale * 1.4426950408889634f;
   for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
+  return DWKV_OK;
+}
+
+// Split-K pass(es): partial (o, m, l) per (work item, head slot, group member).
+dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
+                           int32_t q_type, float sm_scale, const dwkv_probe* probe, void* workspace,
+                           hipStream_t s, float* scores = nullptr) {
+  if (!c || !q) return DWKV_E_NULL;
+  const bool c8 = d->coef_format == DWKV_COEF_I8;
+  if (c8 && (!uses_token_lane(d) || d->n_q_heads / d->n_kv_heads > 4 || probe || scores)) return DWKV_E_UNSUPPORTED;
+  SplitArgs a;
+  dwkv_status st = split_args(d, c, layer, q, q_type, sm_scale, workspace, a);
+  if (st != DWKV_OK) return st;
+  const WsLayout wl = ws_layout(d, probe);
+  const int G = d->n_q_heads / d->n_kv_heads;
+  const int RB = d->basis_rank;
+  const int split = plan_split(d);
+  const int64_t nw = count_work(d, split);
+  if (nw > 0x7fffffff) return DWKV_E_UNSUPPORTED;
+  if (nw == 0) return DWKV_OK;
+  char* ws = static_cast<char*>(workspace);
+  a.split = split;
+  a.n_work = (int32_t)nw;
   a.wt = work_table(d, split);
   a.scores = scores;
   const hipError_t e = c8 ? launch_split_tl_c8(RB, G, max_level(d) > 0, a, (int)nw, s)
@@ -615,10 +626,14 @@ dwkv_status dwkv_route_budget(const dwkv_dims* d, const float* phi, const float*
   return hip_status(launch_route_budget(a, n_mh, reinterpret_cast<hipStream_t>(stream)));
 }
 
-dwkv_status dwkv_compress(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* x_k,
-                          const void* x_v, const float* gate, int64_t t0, int64_t t1, void* stream) {
-  dwkv_status st = check_dims(d);
-  if (st != DWKV_OK) return st;
+}  // extern "C"
+
+namespace {
+
+// Arguments of the append/compress kernel for layer `layer`, every field but
+// the token range (t0, n, gate_ld, gate_k0); checks the cache and inputs.
+dwkv_status compress_args(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* x_k,
+                          const void* x_v, const float* gate, CompressArgs& a) {
   const bool c8 = d->coef_format == DWKV_COEF_I8;
   if (!c || !c->basis || !c->coef_k || !c->coef_v || !c->rank_code || !c->res_off || !c->res_idx ||
       !c->res_val || !c->res_scale)
@@ -627,8 +642,6 @@ dwkv_status dwkv_compress(const dwkv_dims* d, const dwkv_cache* c, int32_t layer
   if (c8 && ((reinterpret_cast<uintptr_t>(c->coef_k_scale) | reinterpret_cast<uintptr_t>(c->coef_v_scale)) & 1u))
     return DWKV_E_ALIGN;
   if (layer < 0 || layer >= d->n_layers) return DWKV_E_DIMS;
-  if (t0 < 0 || t1 < t0 || t1 > d->total_tokens) return DWKV_E_DIMS;
-  if (t1 == t0) return DWKV_OK;
   if (!x_k || !x_v) return DWKV_E_NULL;
   const void* const ptrs[] = {c->basis, c->coef_k, c->coef_v, x_k, x_v};
   for (const void* p : ptrs)
@@ -639,7 +652,6 @@ dwkv_status dwkv_compress(const dwkv_dims* d, const dwkv_cache* c, int32_t layer
   const int64_t T = d->total_tokens, Hk = d->n_kv_heads, rb = d->basis_rank;
   const int64_t T16 = (T + 15) / 16 * 16;
   const int M = d->n_layers / d->window, m = layer / d->window;
-  CompressArgs a;
   std::memset(&a, 0, sizeof(a));
   a.basis = static_cast<const uint16_t*>(c->basis) + (int64_t)m * Hk * 2 * rb * kHeadDim;
   a.basis_b_stride = (int64_t)M * Hk * 2 * rb * kHeadDim;
@@ -667,15 +679,151 @@ dwkv_status dwkv_compress(const dwkv_dims* d, const dwkv_cache* c, int32_t layer
   a.res_scale = const_cast<uint16_t*>(static_cast<const uint16_t*>(c->res_scale)) + (int64_t)layer * 2 * Hk * T;
   a.T = T;
   a.T16 = T16;
-  a.t0 = t0;
-  a.n = t1 - t0;
   a.res_stride = d->res_stride;
   a.batch = d->batch;
   a.n_kv_heads = d->n_kv_heads;
   a.rb = d->basis_rank;
   a.n_levels = d->n_levels;
   for (int i = 0; i < DWKV_MAX_LEVELS; ++i) a.levels[i] = i < d->n_levels ? d->levels[i] : 0;
+  return DWKV_OK;
+}
+
+// The decode that appends runs in one split launch when the token-lane kernel
+// serves the dims with fp16 coefficients and the batch's work split travels
+// in the kernel arguments; otherwise it is the append/compress kernel, once
+// per sequence, then the plain decode.
+bool append_fused(const dwkv_dims* d) {
+  return uses_token_lane(d) && d->coef_format != DWKV_COEF_I8 && d->batch <= kKernargSeqs;
+}
+
+int64_t nonempty_seqs(const dwkv_dims* d) {
+  int64_t n = 0;
+  for (int b = 0; b < d->batch; ++b) n += d->cu_seqlens_host[b + 1] > d->cu_seqlens_host[b];
+  return n;
+}
+
+// Work items of the fused decode: each sequence's tokens but the last in
+// chunks of `split`, then its append item.
+int64_t count_work_append(const dwkv_dims* d, int split) {
+  return count_work(d, split, 1) + nonempty_seqs(d);
+}
+
+// Chunk size of the fused decode: the token-lane kernel's one workgroup per
+// CU, with room for the append items beside the split items when they are
+// few (at most 32; more of them run once workgroups finish, as a separate
+// launch would); chunks in multiples of 64 tokens.
+int plan_split_append(const dwkv_dims* d) {
+  if (d->split_tokens > 0) return d->split_tokens;
+  const int64_t Hk = d->n_kv_heads, napp = nonempty_seqs(d) * Hk, target = kTargetWorkgroups / 2;
+  const int64_t budget = napp <= 32 ? target - napp : target;
+  const int64_t work = std::max<int64_t>(d->total_tokens - nonempty_seqs(d), 1) * Hk;
+  int64_t c = (work + budget - 1) / budget;
+  c = std::max<int64_t>((c + 63) / 64 * 64, 64);
+  while (c < kSplitMax && count_work(d, (int)c, 1) * Hk > budget) c += 64;
+  return (int)std::min<int64_t>(c, kSplitMax);
+}
+
+WorkTable work_table_append(const dwkv_dims* d, int split) {
+  WorkTable t = work_table(d, split, 1);
+  int acc = 0;                            // plus one append item per non-empty sequence
+  for (int b = 0; b < t.n_seq; ++b) {
+    const int64_t len = d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b];
+    acc += len > 0 ? (int32_t)((len - 1 + split - 1) / split) + 1 : 0;
+    t.work[b + 1] = acc;
+  }
+  return t;
+}
+
+size_t append_ws_bytes(const dwkv_dims* d) {
+  if (!append_fused(d)) return ws_layout(d, nullptr).total;
+  const int g = d->n_q_heads / d->n_kv_heads;
+  const int64_t nw = count_work_append(d, plan_split_append(d));
+  return std::max<size_t>(align_up((size_t)nw * d->n_kv_heads * g * kPartStrideTL * sizeof(float), 256), 256);
+}
+
+}  // namespace
+
+extern "C" {
+
+dwkv_status dwkv_compress(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* x_k,
+                          const void* x_v, const float* gate, int64_t t0, int64_t t1, void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (t0 < 0 || t1 < t0 || t1 > d->total_tokens) return DWKV_E_DIMS;
+  CompressArgs a;
+  if ((st = compress_args(d, c, layer, x_k, x_v, gate, a)) != DWKV_OK) {
+    // an empty range needs no inputs
+    if (t1 == t0 && st == DWKV_E_NULL && c && c->basis && c->coef_k && c->coef_v && c->rank_code &&
+        c->res_off && c->res_idx && c->res_val && c->res_scale && layer >= 0 && layer < d->n_layers)
+      return DWKV_OK;
+    return st;
+  }
+  if (t1 == t0) return DWKV_OK;
+  a.t0 = t0;
+  a.n = t1 - t0;
+  a.gate_ld = a.n;
   return hip_status(launch_compress(a, reinterpret_cast<hipStream_t>(stream)));
+}
+
+size_t dwkv_decode_append_workspace_bytes(const dwkv_dims* dims) {
+  if (check_dims(dims) != DWKV_OK) return 0;
+  return append_ws_bytes(dims);
+}
+
+int32_t dwkv_decode_append_launches(const dwkv_dims* dims) {
+  if (check_dims(dims) != DWKV_OK) return -1;
+  return append_fused(dims) ? 2 : (int32_t)nonempty_seqs(dims) + 2;
+}
+
+dwkv_status dwkv_decode_append(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
+                               int32_t q_type, float sm_scale, float* out, const void* x_k, const void* x_v,
+                               const float* gate, void* workspace, size_t ws_bytes, void* stream) {
+  dwkv_status st = check_dims(d);
+  if (st != DWKV_OK) return st;
+  if (!workspace || !q || !out) return DWKV_E_NULL;
+  if (!aligned16(workspace) || !aligned16(q) || !aligned16(out)) return DWKV_E_ALIGN;
+  if (q_type != DWKV_F16 && q_type != DWKV_BF16) return DWKV_E_DIMS;
+  if (ws_bytes < append_ws_bytes(d)) return DWKV_E_WORKSPACE;
+  CompressArgs ca;
+  if ((st = compress_args(d, c, layer, x_k, x_v, gate, ca)) != DWKV_OK) return st;
+  ca.gate_ld = d->batch;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (!append_fused(d)) {
+    // the append/compress kernel on each sequence's last token, then the decode
+    for (int b = 0; b < d->batch; ++b) {
+      const int64_t t1 = d->cu_seqlens_host[b + 1];
+      if (t1 == d->cu_seqlens_host[b]) continue;
+      CompressArgs one = ca;
+      one.t0 = t1 - 1;
+      one.n = 1;
+      one.xk = ca.xk + (int64_t)b * d->n_kv_heads * kHeadDim;
+      one.xv = ca.xv + (int64_t)b * d->n_kv_heads * kHeadDim;
+      one.gate_k0 = b;
+      if (launch_compress(one, s) != hipSuccess) return DWKV_E_HIP;
+    }
+    if ((st = partials_phase(d, c, layer, q, q_type, sm_scale, nullptr, workspace, s)) != DWKV_OK) return st;
+    return merge_phase(d, c, layer, out, nullptr, workspace, s);
+  }
+  // one split launch: the split items over every sequence but its last token,
+  // and per sequence and KV head the append item; then the wide merge
+  const int split = plan_split_append(d);
+  const int64_t nw = count_work_append(d, split);
+  if (nw == 0) return merge_phase(d, c, layer, out, nullptr, workspace, s);   // zero outputs only
+  TLAppendArgs A;
+  std::memset(&A, 0, sizeof(A));
+  A.c = ca;
+  const WorkTable wt = work_table_append(d, split);
+  if ((st = split_args(d, c, layer, q, q_type, sm_scale, workspace, A.s)) != DWKV_OK) return st;
+  A.s.split = split;
+  A.s.n_work = (int32_t)nw;
+  A.s.wt = wt;
+  A.s.trim = 1;
+  const int G = d->n_q_heads / d->n_kv_heads;
+  if (launch_split_tl_append(d->basis_rank, G, max_level(d) > 0, A, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
+  SplitArgs m = A.s;
+  m.out = out;
+  m.mstats = nullptr;
+  return hip_status(launch_merge_tl(d->basis_rank, G, m, s));
 }
 
 dwkv_status dwkv_residual_map(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, int32_t z,

@@ -37,6 +37,7 @@
 //    16 output channels), so that every CU reads a small share.
 #include <utility>
 
+#include "compress_dev.h"
 #include "entry.h"
 #include "internal.h"
 
@@ -974,12 +975,11 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const SplitArgs a
 }
 
 template <int RB, int G, bool RESID, bool SCORES, bool C8>
-__global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
+__device__ __forceinline__ void tl_body(const SplitArgs& a, TSmem<RB, G, RESID>& sm) {
   using C = TCfg<RB>;
   constexpr int NS = C::NS;
   constexpr int HG = TGrp<G>::HG;
   static_assert(!C8 || HG == 4, "int8 coefficients: query groups of up to 4 heads");
-  __shared__ TSmem<RB, G, RESID> sm;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int grp = lane >> 4, col = lane & 15;
   const int slot = blockIdx.y;
@@ -992,7 +992,7 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   TCtx x;
   {
     int64_t c0, c1;
-    work_item(a.wt, a.cu, a.batch, a.split, w, b, c0, c1);
+    work_item(a.wt, a.cu, a.batch, a.split, w, b, c0, c1, a.trim);
     c1 = min(c1, a.T);
     c0 = min(c0, c1);
     x.c0 = (int32_t)c0;
@@ -1294,6 +1294,161 @@ __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   }
 }
 
+template <int RB, int G, bool RESID, bool SCORES, bool C8>
+__global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
+  __shared__ TSmem<RB, G, RESID> sm;
+  tl_body<RB, G, RESID, SCORES, C8>(a, sm);
+}
+
+// LDS of the append item, in the decode workgroup's storage: both bases of
+// the sequence's window and head (K rows, then V rows), per Z the compress
+// arrays, the rebuilt key, the value's residual g R and the heads' scores.
+template <int RB>
+struct alignas(16) ASmem {
+  alignas(16) uint16_t bas[2][RB * cdev::kBRow];
+  alignas(16) float xs[2][D];
+  alignas(16) float as[2][RB];
+  uint8_t ech[2][D];
+  uint8_t ecode[2][D];
+  float kh[D];
+  float vr[D];
+  float sc[8];
+  int rho;
+  uint16_t scale[2];
+};
+
+// The append item of sequence b and KV head `slot`: wave 0 compresses the new
+// token t's key and wave 1 its value (the append/compress arithmetic, written
+// to the cache), then the workgroup writes the token's own partial for every
+// head of the group: score m = q . K_hat (log2 units, K_hat = A^K B^K + g R^K
+// rebuilt from what was stored), l = 1, and the value in basis space:
+// r = g R^V, a~ = A^V.  The merge takes it like any other partial.
+template <int RB, int G>
+__device__ __forceinline__ void tl_append(const TLAppendArgs& A, unsigned char* lds, int b, int64_t t, int slot,
+                                          int w) {
+  ASmem<RB>& sm = *reinterpret_cast<ASmem<RB>*>(lds);
+  const SplitArgs& a = A.s;
+  const CompressArgs& c = A.c;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int kvh = a.kv_of_slot[slot];
+  const int Hk = c.n_kv_heads;
+  const uint16_t* src = c.basis + (int64_t)b * c.basis_b_stride + (int64_t)kvh * 2 * RB * D;
+  for (int e = tid; e < 2 * RB * (D / 8); e += kTThreads) {
+    const int z = e / (RB * (D / 8)), r = e % (RB * (D / 8));
+    const int i = r / (D / 8), q = r % (D / 8);
+    *reinterpret_cast<uint4*>(&sm.bas[z][i * cdev::kBRow + 8 * q]) =
+        *reinterpret_cast<const uint4*>(src + ((int64_t)z * RB + i) * D + 8 * q);
+  }
+  cdev::TokenIn in{};
+  cdev::Slab sl{};
+  if (wv < 2) {
+    const int z = wv;
+    const int64_t slab = (int64_t)z * Hk + kvh;
+    sl.code = c.code + (int64_t)kvh * c.T;
+    sl.off = c.off + (int64_t)kvh * (c.T + 1);
+    sl.coef = (z == 0 ? c.coef_k : c.coef_v) + (int64_t)kvh * c.T16 * c.rb;
+    sl.res_idx = c.res_idx + slab * c.res_stride;
+    sl.res_val = c.res_val + slab * (c.res_stride / 2);
+    sl.res_scale = c.res_scale + slab * c.T;
+    const uint16_t* X = (z ? c.xv : c.xk) + ((int64_t)b * Hk + kvh) * D;
+    in.xw = reinterpret_cast<const uint32_t*>(X)[lane];
+    in.lvl = sl.code[t];
+    in.e0 = sl.off[t];
+    in.e1 = sl.off[t + 1];
+    in.g = c.gate ? c.gate[(int64_t)(z * Hk + kvh) * c.gate_ld + b] : 1.0f;
+  }
+  __syncthreads();
+  if (wv < 2) {
+    const cdev::TokOut o =
+        cdev::compress_token(c, sl, cdev::CWave{sm.bas[wv], sm.xs[wv], sm.as[wv], sm.ech[wv], sm.ecode[wv]}, lane,
+                             wv, t, in);
+    if (lane == 0) {
+      sm.scale[wv] = o.scale;
+      if (wv == 0) sm.rho = o.rho;
+    }
+  }
+  __syncthreads();
+  // the rebuilt key's basis term and a zero value residual, channel tid
+  if (tid < D) {
+    float k = 0.f;
+    for (int i = 0; i < RB; ++i) k = __builtin_fmaf(sm.as[0][i], half_bits_to_float(sm.bas[0][i * cdev::kBRow + tid]), k);
+    sm.kh[tid] = k;
+    sm.vr[tid] = 0.f;
+  }
+  __syncthreads();
+  // the residual entries (distinct channels within each of K and V)
+  const int rho = sm.rho;
+  if (tid < rho) {
+    sm.kh[sm.ech[0][tid]] += half_bits_to_float(sm.scale[0]) * (float)int4_value(sm.ecode[0][tid]);
+    sm.vr[sm.ech[1][tid]] = half_bits_to_float(sm.scale[1]) * (float)int4_value(sm.ecode[1][tid]);
+  }
+  __syncthreads();
+  if (wv < G) {                          // wave g: the score of head g
+    const uint16_t* qrow = a.q + ((int64_t)b * a.n_q_heads + kvh * G + wv) * D;
+    const float q0 = a.q_bf16 ? bf16_bits_to_float(qrow[lane]) : half_bits_to_float(qrow[lane]);
+    const float q1 = a.q_bf16 ? bf16_bits_to_float(qrow[lane + 64]) : half_bits_to_float(qrow[lane + 64]);
+    const float sv = wave_sum(q0 * sm.kh[lane] + q1 * sm.kh[lane + 64]);
+    if (lane == 0) sm.sc[wv] = sv * a.qscale;
+  }
+  __syncthreads();
+  constexpr int ROW = D + RB;
+  for (int e = tid; e < G * ROW; e += kTThreads) {
+    const int g = e / ROW, cc = e % ROW;
+    float* dst = a.part + (((int64_t)slot * a.n_work + w) * G + g) * kPartStrideTL;
+    __hip_atomic_store(dst + cc, cc < D ? sm.vr[cc] : sm.as[1][cc - D], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  if (tid < G) {
+    float* dst = a.part + (((int64_t)slot * a.n_work + w) * G + tid) * kPartStrideTL;
+    __hip_atomic_store(dst + kPartTLM, sm.sc[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(dst + kPartTLM + 1, 1.0f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// The decode that appends: the append item of a sequence is the last of its
+// work items (its chunk is empty once the new token is trimmed off).
+template <int RB, int G, bool RESID>
+__global__ __launch_bounds__(kTThreads) void tl_append_kernel(const TLAppendArgs A) {
+  constexpr size_t kT = sizeof(TSmem<RB, G, RESID>), kA = sizeof(ASmem<RB>);
+  __shared__ alignas(16) unsigned char lds[kT > kA ? kT : kA];
+  const SplitArgs& a = A.s;
+  int b;
+  int64_t c0, c1;
+  work_item(a.wt, a.cu, a.batch, a.split, blockIdx.x, b, c0, c1, a.trim);
+  if (c0 >= c1) {
+    tl_append<RB, G>(A, lds, b, c1, blockIdx.y, blockIdx.x);
+    return;
+  }
+  tl_body<RB, G, RESID, false, false>(a, *reinterpret_cast<TSmem<RB, G, RESID>*>(lds));
+}
+
+template <int RB, int G, bool R>
+hipError_t launch_tla_t(const TLAppendArgs& a, int n_work, hipStream_t s) {
+  hipLaunchKernelGGL((tl_append_kernel<RB, G, R>), dim3(n_work, a.s.n_slots), dim3(kTThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int RB, bool R>
+hipError_t launch_tla_g(int g, const TLAppendArgs& a, int n_work, hipStream_t s) {
+  switch (g) {
+    case 1: return launch_tla_t<RB, 1, R>(a, n_work, s);
+    case 2: return launch_tla_t<RB, 2, R>(a, n_work, s);
+    case 4: return launch_tla_t<RB, 4, R>(a, n_work, s);
+    case 8: return launch_tla_t<RB, 8, R>(a, n_work, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <bool R>
+hipError_t launch_tla_rb(int rb, int g, const TLAppendArgs& a, int n_work, hipStream_t s) {
+  switch (rb) {
+    case 16: return launch_tla_g<16, R>(g, a, n_work, s);
+    case 32: return launch_tla_g<32, R>(g, a, n_work, s);
+    case 48: return launch_tla_g<48, R>(g, a, n_work, s);
+    case 64: return launch_tla_g<64, R>(g, a, n_work, s);
+  }
+  return hipErrorInvalidValue;
+}
+
 template <int RB, int G, bool R, bool S, bool C8>
 hipError_t launch_tl_t(const SplitArgs& a, int n_work, hipStream_t s) {
   hipLaunchKernelGGL((tl_kernel<RB, G, R, S, C8>), dim3(n_work, a.n_slots), dim3(kTThreads), 0, s, a);
@@ -1351,6 +1506,10 @@ bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t 
 hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {
   return resid ? launch_tl_rb<true, false, false>(rb, g, a, n_work, s)
                : launch_tl_rb<false, false, false>(rb, g, a, n_work, s);
+}
+
+hipError_t launch_split_tl_append(int rb, int g, bool resid, const TLAppendArgs& a, int n_work, hipStream_t s) {
+  return resid ? launch_tla_rb<true>(rb, g, a, n_work, s) : launch_tla_rb<false>(rb, g, a, n_work, s);
 }
 
 hipError_t launch_split_tl_scores(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {

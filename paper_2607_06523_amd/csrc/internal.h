@@ -257,7 +257,8 @@ struct CompressArgs {
   const int32_t* cu;           // device cu_seqlens [batch+1]
   const uint16_t* xk;          // [n][Hkv][d] fp16
   const uint16_t* xv;
-  const float* gate;           // [2][Hkv][n] or null (g = 1)
+  const float* gate;           // null (g = 1), or gate of token k of (z, h) at
+                               // [(z*Hkv + h)*gate_ld + gate_k0 + k] ([2][Hkv][n] by default)
   uint16_t* coef_k;            // layer's [Hkv] slabs of T16*rb (key_index); int8: bytes, 16x16 key tiles
   uint16_t* coef_v;            // layer's [Hkv] slabs of T16*rb (value_index); int8: bytes, [T16/16][rb][16]
   uint16_t* cscale_k;          // int8 coefficients: layer's [Hkv] slabs of (rb/16)*T block scales, else null
@@ -268,6 +269,7 @@ struct CompressArgs {
   int64_t T, T16, t0, n, res_stride;
   int32_t batch, n_kv_heads, rb, n_levels;
   int32_t c8;                  // write the 8-bit blockwise coefficient form
+  int64_t gate_ld, gate_k0;
   int32_t levels[DWKV_MAX_LEVELS];
 };
 
@@ -292,6 +294,20 @@ hipError_t launch_route(const RouteArgs& a, int n_mh, hipStream_t s);
 // a.keys [M*Hkv][T]; one workgroup per (window, head).
 hipError_t launch_route_budget(const RouteArgs& a, int n_mh, hipStream_t s);
 hipError_t launch_compress(const CompressArgs& a, hipStream_t s);
+
+// Decode of one layer that first appends the new token of every sequence (its
+// last): the split pass covers each sequence's tokens but the last (trim 1),
+// and one more work item per non-empty sequence -- the last of its range --
+// compresses the new token's key and value (as the append/compress kernel
+// does, written to the cache) and writes the token's own partial (score
+// against the rebuilt key; the rebuilt value in basis space).  c carries the
+// compress arguments; x rows are [B][Hkv][d] and gate [2][Hkv][B]
+// (gate_ld = B).
+struct TLAppendArgs {
+  SplitArgs s;
+  CompressArgs c;
+};
+hipError_t launch_split_tl_append(int rb, int g, bool resid, const TLAppendArgs& a, int n_work, hipStream_t s);
 
 // Materialization of one layer's rebuilt keys and values (Eq. 1) as fp16.
 struct MatArgs {

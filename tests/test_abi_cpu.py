@@ -462,3 +462,39 @@ def test_probe_schedule_matches_oracle(lib):
                  (0, 1, 1, 8, 9)):
         assert lib.dwkv_probe_schedule(*args, h, C.byref(npos)) == -1, args
     assert lib.dwkv_probe_schedule(0, 1, 1, 8, 1, None, C.byref(npos)) == -1
+
+
+def test_decode_append_plan_and_argument_checks(lib):
+    """The decode that appends: one launch plus the merge on token-lane dims
+    (chunks sized so the split items and one append item per sequence and KV
+    head fill one round of 256 workgroups), else one compress launch per
+    non-empty sequence plus the decode; bad arguments refused on the host."""
+    from paper_2607_06523_amd import binding
+    T = 65536
+    d, keep = dims(cu_seqlens_host=[0, T], batch=1, total_tokens=T, n_kv_heads=8, n_q_heads=32,
+                   res_stride=T * 16 + 512, basis_rank=48, levels=(0, 4, 8, 16))
+    assert lib.dwkv_decode_append_launches(C.byref(d)) == 2
+    # chunks of 2176 tokens: 31 split items per head over 65535 tokens, + 1 append item
+    assert lib.dwkv_decode_append_workspace_bytes(C.byref(d)) == up256((31 + 1) * 8 * 4 * 196 * 4)
+    d, keep = dims(batch=3, cu_seqlens_host=[0, 700, 700, 1301], total_tokens=1301, split_tokens=256)
+    # per head: ceil(699/256) + 1 and ceil(600/256) + 1 items; the empty sequence none
+    assert lib.dwkv_decode_append_workspace_bytes(C.byref(d)) == up256((3 + 1 + 3 + 1) * 2 * 4 * 196 * 4)
+    assert lib.dwkv_decode_append_launches(C.byref(d)) == 2
+    d16, keep16 = dims(batch=3, cu_seqlens_host=[0, 700, 700, 1301], total_tokens=1301, n_q_heads=32)
+    assert lib.dwkv_decode_append_launches(C.byref(d16)) == 2 + 2          # general kernel: per-sequence compress
+    assert lib.dwkv_decode_append_workspace_bytes(C.byref(d16)) == lib.dwkv_workspace_bytes(C.byref(d16), None)
+    bad, keepb = dims(n_q_heads=7)
+    assert lib.dwkv_decode_append_launches(C.byref(bad)) == -1
+    assert lib.dwkv_decode_append_workspace_bytes(C.byref(bad)) == 0
+    c = binding.Cache(*([FAKE] * 8))
+    need = lib.dwkv_decode_append_workspace_bytes(C.byref(d))
+
+    def call(x_k=FAKE, x_v=FAKE, gate=None, ws=FAKE, ws_bytes=need, q=FAKE, out=FAKE, layer=0):
+        return lib.dwkv_decode_append(C.byref(d), C.byref(c), layer, q, 0, 0.0, out, x_k, x_v, gate, ws, ws_bytes,
+                                      None)
+    assert call(x_k=None) == 1
+    assert call(q=None) == 1
+    assert call(x_v=FAKE + 8) == 7
+    assert call(gate=FAKE + 2) == 7
+    assert call(ws_bytes=need - 1) == 4
+    assert call(layer=4) == 2
