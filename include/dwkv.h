@@ -163,13 +163,11 @@ int32_t dwkv_decode_kernel(const dwkv_dims* dims);
 size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe);
 
 /* Kernel launches one dwkv_decode call enqueues for these dims (2: the
- * split-K pass and the merge; with a probe, 3 on the general kernel -- the
- * reference pass is added and one merge covers both -- and 4 on the
- * token-lane kernel, whose merge is followed by a small merge of the probed
- * heads' reference partials; a probe over n_pos > 1 positions adds two split
- * passes -- factorized and reference, on the probed heads -- for every
- * earlier position that still sees a token of some sequence, and one merge),
- * or -1 when the dims or probe are invalid.  probe may be NULL. */
+ * split-K pass and the merge; with a probe, 3: the reference pass is added
+ * and the merge also evaluates Eq. 3; a probe over n_pos > 1 positions adds
+ * two split passes -- factorized and reference, on the probed heads -- for
+ * every earlier position that still sees a token of some sequence, and one
+ * merge), or -1 when the dims or probe are invalid.  probe may be NULL. */
 int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe);
 
 /* Per-layer decode attention over the factorized cache (Eq. 1 folded into the

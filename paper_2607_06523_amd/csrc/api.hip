@@ -150,8 +150,10 @@ dwkv_status check_probe(const dwkv_dims* d, const dwkv_probe* p) {
 // with several probe positions, for each earlier position its rebuilt and
 // reference partials (pos_bytes each), then the Eq. 3 sums of the current one.
 struct WsLayout {
-  size_t main_bytes, ref_bytes, pos_bytes, acc_off, total;
+  size_t main_bytes, ref_bytes, pos_bytes, acc_off, chunk_off, count_off, total;
 };
+
+constexpr int kProbeChunks = kHeadDim / 16;   // output-channel chunks of the token-lane wide merge
 
 WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
   const int split = plan_split(d);
@@ -166,7 +168,11 @@ WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
   w.pos_bytes = np > 1 ? w.ref_bytes : 0;
   w.acc_off = w.main_bytes + w.ref_bytes + (size_t)(np - 1) * 2 * w.pos_bytes;
   const size_t acc_bytes = np > 1 ? align_up((size_t)d->batch * p->n_heads * g * 2 * sizeof(float), 256) : 0;
-  w.total = w.acc_off + acc_bytes;
+  // the wide merge's Eq. 3 sums per output-channel chunk, and its counters
+  const size_t cols = p ? (size_t)d->batch * p->n_heads * g : 0;
+  w.chunk_off = w.acc_off + acc_bytes;
+  w.count_off = w.chunk_off + align_up(cols * kProbeChunks * 2 * sizeof(float), 256);
+  w.total = w.count_off + align_up(cols * sizeof(uint32_t), 256);
   if (w.total == 0) w.total = 256;
   return w;
 }
@@ -225,7 +231,7 @@ size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe) {
 int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe) {
   if (check_dims(dims) != DWKV_OK || check_probe(dims, probe) != DWKV_OK) return -1;
   if (!probe) return 2;
-  int32_t n = uses_token_lane(dims) ? 4 : 3;
+  int32_t n = 3;
   const int np = probe_positions(probe), split = plan_split_ref(dims, probe->n_heads);
   for (int j = 1; j < np; ++j)
     if (count_work(dims, split, j) > 0) n += 2;
@@ -347,7 +353,11 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
     const int64_t nw_ref = count_work(d, r.split);
     r.n_work = (int32_t)nw_ref;
     r.wt = work_table(d, r.split);
+    r.zero = reinterpret_cast<uint32_t*>(ws + wl.count_off);
+    r.n_zero = d->batch * probe->n_heads * G;
     if (launch_split(kHeadDim, G, false, true, r, (int)nw_ref, s) != hipSuccess) return DWKV_E_HIP;
+    r.zero = nullptr;
+    r.n_zero = 0;
     // earlier positions: the query j steps back over the sequences cut j
     // tokens short, on the factorized cache (general kernel, probed heads
     // only) and on the reference
@@ -405,10 +415,26 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
     for (int h = 0; h < d->n_kv_heads; ++h) a.kv_of_slot[h] = h;
     a.wt = work_table(d, a.split);
     a.mstats = mstats;
-    const hipError_t e = launch_merge_tl(d->basis_rank, d->n_q_heads / d->n_kv_heads, a, s);
-    // with a probe, a second small launch merges the reference partials of
-    // the probed heads and evaluates Eq. 3 against the rows just written
-    if (e != hipSuccess || !probe) return hip_status(e);
+    WMergeArgs wm;
+    std::memset(&wm, 0, sizeof(wm));
+    wm.s = a;
+    for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) wm.p.slot_of_kv[h] = -1;
+    if (probe) {                       // Eq. 3 in the same launch
+      WideProbe& P = wm.p;
+      P.part_ref = reinterpret_cast<const float*>(ws + wl.main_bytes);
+      P.err = probe->err;
+      P.out_ref = probe->out_ref;
+      P.acc = probe_positions(probe) > 1 ? reinterpret_cast<float*>(ws + wl.acc_off) : nullptr;
+      P.chunk = reinterpret_cast<float*>(ws + wl.chunk_off);
+      P.count = reinterpret_cast<uint32_t*>(ws + wl.count_off);
+      P.n_probe = probe->n_heads;
+      P.eps = probe->eps;
+      P.ref_split = plan_split_ref(d, probe->n_heads);
+      P.ref_wt = work_table(d, P.ref_split);
+      for (int i = 0; i < probe->n_heads; ++i) P.slot_of_kv[probe->kv_heads_host[i]] = i;
+    }
+    const hipError_t e = launch_merge_tl(d->basis_rank, d->n_q_heads / d->n_kv_heads, wm, s);
+    if (e != hipSuccess || probe_positions(probe) == 1) return hip_status(e);
   }
   MergeArgs mg;
   std::memset(&mg, 0, sizeof(mg));
@@ -439,13 +465,13 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
   if (probe)
     for (int i = 0; i < probe->n_heads; ++i) {
       mg.probe_slot_of_kv[probe->kv_heads_host[i]] = i;
-      mg.kv_of_probe[i] = probe->kv_heads_host[i];
     }
-  mg.probe_only = tl ? 1 : 0;
   const int np = probe_positions(probe);
   if (np > 1) mg.acc = reinterpret_cast<float*>(ws + wl.acc_off);
-  hipError_t e = launch_merge(mg, s);
-  if (e != hipSuccess || np == 1) return hip_status(e);
+  if (!tl) {                           // outputs and the current position's Eq. 3
+    const hipError_t e = launch_merge(mg, s);
+    if (e != hipSuccess || np == 1) return hip_status(e);
+  }
   // the earlier positions' sums, then err
   mg.part_pos = reinterpret_cast<const float*>(ws + wl.main_bytes + wl.ref_bytes);
   mg.pos_stride = (int64_t)(wl.pos_bytes / sizeof(float));
@@ -820,9 +846,12 @@ dwkv_status dwkv_decode_append(const dwkv_dims* d, const dwkv_cache* c, int32_t 
   A.s.trim = 1;
   const int G = d->n_q_heads / d->n_kv_heads;
   if (launch_split_tl_append(d->basis_rank, G, max_level(d) > 0, A, (int)nw, s) != hipSuccess) return DWKV_E_HIP;
-  SplitArgs m = A.s;
-  m.out = out;
-  m.mstats = nullptr;
+  WMergeArgs m;
+  std::memset(&m, 0, sizeof(m));
+  m.s = A.s;
+  m.s.out = out;
+  m.s.mstats = nullptr;
+  for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) m.p.slot_of_kv[h] = -1;
   return hip_status(launch_merge_tl(d->basis_rank, G, m, s));
 }
 

@@ -566,6 +566,10 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   const int slot = blockIdx.y;
   const int kvh = a.kv_of_slot[slot];
   pin_split_args(a, kvh);
+  if constexpr (IDENT) {
+    if (a.zero && blockIdx.x == 0 && blockIdx.y == 0)
+      for (int i = threadIdx.x; i < a.n_zero; i += kThreads) a.zero[i] = 0;
+  }
 
   // work item -> (sequence, chunk)
   const int w = blockIdx.x;
@@ -1014,57 +1018,6 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   }
 }
 
-// Probe merge after the token-lane merge: one 1024-thread workgroup per
-// (probed query head, sequence) merges the reference partials (32 split
-// groups of 8, so that one round of loads covers up to 256 partials) in a
-// fixed order, reads the output row the token-lane merge wrote, and evaluates
-// Eq. 3.
-constexpr int kProbeThreads = 1024;
-
-__global__ __launch_bounds__(kProbeThreads) void probe_merge_kernel(const MergeArgs a) {
-  constexpr int NG = kProbeThreads / (D / 4);
-  __shared__ float red_m[NG], red_l[NG];
-  __shared__ f4 red_o[kProbeThreads];
-  __shared__ float red2[2][kProbeThreads / 64];
-  const int b = blockIdx.y, tid = threadIdx.x;
-  const int G = a.n_q_heads / a.n_kv_heads;
-  const int sl = blockIdx.x / G, g = blockIdx.x % G;
-  const int hq = a.kv_of_probe[sl] * G + g;
-  const int c4 = tid % (D / 4), sg = tid / (D / 4);
-  const f4 o = reinterpret_cast<const f4*>(a.out + ((int64_t)b * a.n_q_heads + hq) * D)[c4];
-  int base_r, ns_r;
-  seq_work(a.ref_wt, a.cu, a.ref_split, b, base_r, ns_r);
-  const f4 r = merge_rows<kProbeThreads>(a.part_ref, (int64_t)base_r * a.n_probe * G + sl * G + g,
-                                         (int64_t)a.n_probe * G, ns_r, kPartStride, D, D, red_m, red_l, red_o).x;
-  const int64_t col = (int64_t)b * a.n_probe * G + sl * G + g;
-  float d2 = 0.f, r2 = 0.f;
-  if (sg == 0) {
-    if (a.out_ref) reinterpret_cast<f4*>(a.out_ref + col * D)[c4] = r;
-    const float dx = r.x - o.x, dy = r.y - o.y, dz = r.z - o.z, dw = r.w - o.w;
-    d2 = dx * dx + dy * dy + dz * dz + dw * dw;
-    r2 = r.x * r.x + r.y * r.y + r.z * r.z + r.w * r.w;
-  }
-  for (int o2 = 32; o2 > 0; o2 >>= 1) {
-    d2 += __shfl_xor(d2, o2);
-    r2 += __shfl_xor(r2, o2);
-  }
-  if ((tid & 63) == 0) {
-    red2[0][tid >> 6] = d2;
-    red2[1][tid >> 6] = r2;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    float sd = 0.f, sr = 0.f;
-    for (int i = 0; i < kProbeThreads / 64; ++i) { sd += red2[0][i]; sr += red2[1][i]; }
-    if (a.acc) {
-      a.acc[2 * col] = sd;
-      a.acc[2 * col + 1] = sr;
-    } else {
-      a.err[col] = sqrtf(sd) / (sqrtf(sr) + a.eps);
-    }
-  }
-}
-
 // Eq. 3 over the earlier query positions: one workgroup per (probed query
 // head, sequence).  For every position j = 1..n_pos-1 it merges the rebuilt
 // and the reference partials of the sequence cut j tokens short (none when
@@ -1158,11 +1111,6 @@ hipError_t launch_merge(const MergeArgs& a, hipStream_t s) {
   if (a.part_pos) {
     const int g = a.n_q_heads / a.n_kv_heads;
     hipLaunchKernelGGL(probe_pos_merge_kernel, dim3(a.n_probe * g, a.batch), dim3(kMergeThreads), 0, s, a);
-    return hipGetLastError();
-  }
-  if (a.probe_only) {
-    const int g = a.n_q_heads / a.n_kv_heads;
-    hipLaunchKernelGGL(probe_merge_kernel, dim3(a.n_probe * g, a.batch), dim3(kProbeThreads), 0, s, a);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(merge_kernel, dim3(a.n_q_heads, a.batch), dim3(kMergeThreads), 0, s, a);

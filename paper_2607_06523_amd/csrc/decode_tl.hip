@@ -865,8 +865,12 @@ constexpr int kSc1 = 16;                // buffer cache policy: device-coherent 
 constexpr int kWmThreads = 256;
 constexpr int kWmCh = 16;                       // output channels per workgroup
 
+constexpr int kPrG = kWmThreads / (kWmCh / 4);  // reference row groups of the probe tail (64)
+constexpr int kPrRPT = 4;                         // reference partials per thread per round
+
 template <int RB, int G>
-__global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const SplitArgs a) {
+__global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs A) {
+  const SplitArgs& a = A.s;
   constexpr int QW = kWmCh / 4 + RB / 4;        // quads per row: the r chunk, then a~
   constexpr int RG = kWmThreads / QW;           // row groups
   constexpr int RPT = 2;                        // partials per thread per round (32 per round at r_b 48)
@@ -877,6 +881,10 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const SplitArgs a
   __shared__ float wm[RG], wl[RG];
   __shared__ alignas(16) float fin[4 * QW];
   __shared__ float red2[KG][kWmCh];
+  __shared__ f4 pred[kPrG][kWmCh / 4];
+  __shared__ float pm[kPrG], pl[kPrG];
+  __shared__ float pfin[2][kWmCh];
+  __shared__ uint32_t plast;
   const int tid = threadIdx.x;
   const int ch = blockIdx.x % NCH, g = (blockIdx.x / NCH) % G, slot = blockIdx.x / (NCH * G), b = blockIdx.y;
   const int c0 = ch * kWmCh;
@@ -966,12 +974,101 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const SplitArgs a
     red2[kg][pc] = o;
   }
   __syncthreads();
+  const int sl = A.p.n_probe > 0 ? A.p.slot_of_kv[kvh] : -1;
   if (tid < kWmCh) {
     float o = fin[tid];
 #pragma unroll
     for (int j = 0; j < KG; ++j) o += red2[j][tid];
     a.out[((int64_t)b * a.n_q_heads + kvh * G + g) * D + c0 + tid] = o;
+    pfin[0][tid] = o;
   }
+  if (sl < 0) return;
+
+  // Eq. 3 for a probed head: merge the reference partials' channels
+  // [c0, c0 + 16) (row group tid / 4 takes every 64th partial, quad tid % 4)
+  const WideProbe& P = A.p;
+  int base_r, ns_r;
+  seq_work(P.ref_wt, a.cu, P.ref_split, b, base_r, ns_r);
+  const int pq = tid % (kWmCh / 4), prg = tid / (kWmCh / 4);
+  const int64_t prs = (int64_t)P.n_probe * G * kPartStride;
+  const float* pr0 = P.part_ref + (((int64_t)base_r * P.n_probe + sl) * G + g) * kPartStride;
+  f4 racc = f4{0.f, 0.f, 0.f, 0.f};
+  float rm = -INFINITY, rl = 0.f;
+  for (int s0 = 0; s0 < ns_r; s0 += kPrG * kPrRPT) {
+    f4 xv[kPrRPT];
+    float mv[kPrRPT], lv[kPrRPT];
+#pragma unroll
+    for (int i = 0; i < kPrRPT; ++i) {
+      const float* row = pr0 + (int64_t)min(s0 + prg + kPrG * i, ns_r - 1) * prs;
+      xv[i] = *reinterpret_cast<const f4*>(row + c0 + 4 * pq);
+      mv[i] = row[D];
+      lv[i] = row[D + 1];
+    }
+    float mr = rm;
+#pragma unroll
+    for (int i = 0; i < kPrRPT; ++i) {
+      if (s0 + prg + kPrG * i >= ns_r) mv[i] = -INFINITY;
+      mr = fmaxf(mr, mv[i]);
+    }
+    const float resc = rm == -INFINITY ? 0.f : exp2f(rm - mr);
+    racc *= resc;
+    rl *= resc;
+#pragma unroll
+    for (int i = 0; i < kPrRPT; ++i) {
+      const float w = mv[i] == -INFINITY ? 0.f : exp2f(mv[i] - mr);
+      racc += w * xv[i];
+      rl += w * lv[i];
+    }
+    rm = mr;
+  }
+  pred[prg][pq] = racc;
+  if (pq == 0) {
+    pm[prg] = rm;
+    pl[prg] = rl;
+  }
+  __syncthreads();
+  const int64_t col = (int64_t)b * P.n_probe * G + sl * G + g;
+  if (tid < kWmCh / 4) {
+    float mx = -INFINITY;
+    for (int j = 0; j < kPrG; ++j) mx = fmaxf(mx, pm[j]);
+    f4 r = f4{0.f, 0.f, 0.f, 0.f};
+    float l = 0.f;
+    for (int j = 0; j < kPrG; ++j) {
+      const float e = pm[j] == -INFINITY ? 0.f : exp2f(pm[j] - mx);
+      r += e * pred[j][tid];
+      l += e * pl[j];
+    }
+    r *= l > 0.f ? 1.0f / l : 0.f;
+    *reinterpret_cast<f4*>(&pfin[1][4 * tid]) = r;
+    if (P.out_ref) *reinterpret_cast<f4*>(P.out_ref + col * D + c0 + 4 * tid) = r;
+  }
+  __syncthreads();
+  if (tid < 64) {                       // wave 0: this chunk's sums, then the column's count
+    const float r = tid < kWmCh ? pfin[1][tid] : 0.f, o = tid < kWmCh ? pfin[0][tid] : 0.f;
+    const float d2 = wave_sum((r - o) * (r - o)), r2 = wave_sum(r * r);
+    if (tid == 0) {
+      P.chunk[(col * NCH + ch) * 2] = d2;
+      P.chunk[(col * NCH + ch) * 2 + 1] = r2;
+      __threadfence();
+      plast = atomicAdd(&P.count[col], 1u);
+    }
+  }
+  __syncthreads();
+  if (plast != (uint32_t)(NCH - 1) || tid != 0) return;
+  // the column's last chunk: every chunk's sums are visible after the fence
+  __threadfence();
+  float sd = 0.f, sr = 0.f;
+  for (int k = 0; k < NCH; ++k) {
+    sd += __hip_atomic_load(&P.chunk[(col * NCH + k) * 2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    sr += __hip_atomic_load(&P.chunk[(col * NCH + k) * 2 + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  if (P.acc) {
+    P.acc[2 * col] = sd;
+    P.acc[2 * col + 1] = sr;
+  } else {
+    P.err[col] = sqrtf(sd) / (sqrtf(sr) + P.eps);
+  }
+  P.count[col] = 0;                     // ready for the next call
 }
 
 template <int RB, int G, bool RESID, bool SCORES, bool C8>
@@ -1482,8 +1579,8 @@ hipError_t launch_tl_rb(int rb, int g, const SplitArgs& a, int n_work, hipStream
 }  // namespace
 
 template <int RB>
-hipError_t launch_merge_tl_rb(int g, const SplitArgs& a, hipStream_t s) {
-  const dim3 grid(a.n_slots * g * (D / kWmCh), a.batch);
+hipError_t launch_merge_tl_rb(int g, const WMergeArgs& a, hipStream_t s) {
+  const dim3 grid(a.s.n_slots * g * (D / kWmCh), a.s.batch);
   switch (g) {
     case 1: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 1>), grid, dim3(kWmThreads), 0, s, a); break;
     case 2: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 2>), grid, dim3(kWmThreads), 0, s, a); break;
@@ -1522,7 +1619,7 @@ hipError_t launch_split_tl_c8(int rb, int g, bool resid, const SplitArgs& a, int
                : launch_tl_rb<false, false, true>(rb, g, a, n_work, s);
 }
 
-hipError_t launch_merge_tl(int rb, int g, const SplitArgs& a, hipStream_t s) {
+hipError_t launch_merge_tl(int rb, int g, const WMergeArgs& a, hipStream_t s) {
   switch (rb) {
     case 16: return launch_merge_tl_rb<16>(g, a, s);
     case 32: return launch_merge_tl_rb<32>(g, a, s);

@@ -108,6 +108,32 @@ struct SplitArgs {
   WorkTable wt;
   float* mstats;               // token-lane merge: merged (m*, l*) per [B][Hq] when not null
   int32_t trim;                // tokens dropped from the end of every sequence (earlier probe positions)
+  uint32_t* zero;              // reference pass: n_zero words its first workgroup clears (the wide
+  int32_t n_zero;              // merge's probe counters), or null
+};
+
+// Eq. 3 in the token-lane wide merge: the workgroups of a probed KV head also
+// merge the reference partials of their 16 output channels, leave the
+// chunk's sums of (O_ref - O)^2 and O_ref^2, and the last of the d/16 chunk
+// workgroups of a column (a counter) adds them in chunk order and writes err
+// (or, with several positions, the sums to acc).
+struct WideProbe {
+  const float* part_ref;       // reference partials [work][n_probe][G][kPartStride]
+  float* err;                  // [B][n_probe*G]
+  float* out_ref;              // [B][n_probe*G][d] or null
+  float* acc;                  // [B][n_probe*G][2] (several positions) or null
+  float* chunk;                // [B][n_probe*G][d/16][2] per-chunk sums
+  uint32_t* count;             // [B][n_probe*G] chunks done: zero before the merge, reset by the last
+  int32_t n_probe;             // 0: no probe
+  float eps;
+  int32_t ref_split;
+  WorkTable ref_wt;
+  int32_t slot_of_kv[DWKV_MAX_PROBE_HEADS];   // probed slot of each KV head, -1 when not probed
+};
+
+struct WMergeArgs {
+  SplitArgs s;
+  WideProbe p;
 };
 
 // Split merge (and Eq. 3 for probed heads): grid = (Hq, B).
@@ -133,11 +159,6 @@ struct MergeArgs {
   int64_t basis_b_stride;
   int32_t ref_split;           // the probe pass's chunk size and work split
   WorkTable ref_wt;
-  // probe_only: grid (n_probe * G, B), one workgroup per probed query head;
-  // the output rows are already in `out` (written by the token-lane merge),
-  // only the reference partials are merged and Eq. 3 evaluated against them
-  int32_t probe_only;
-  int32_t kv_of_probe[DWKV_MAX_PROBE_HEADS];
   // probe over several query positions: the current position's merge writes
   // (sum d^2, sum r^2) per probed column to acc [B][n_probe*G][2] instead of
   // err; the position merge (grid (n_probe * G, B)) adds the earlier
@@ -287,7 +308,7 @@ hipError_t launch_split_tl_scores(int rb, int g, bool resid, const SplitArgs& a,
 hipError_t launch_split_tl_c8(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s);
 // Token-lane merge: reads a.part, writes a.out (one workgroup per slot, head
 // and 16 output channels).
-hipError_t launch_merge_tl(int rb, int g, const SplitArgs& a, hipStream_t s);
+hipError_t launch_merge_tl(int rb, int g, const WMergeArgs& a, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, int n_mh, hipStream_t s);
 // Two-level routing under a budget: a.entries [M*Hkv] (device), keys scratch

@@ -142,8 +142,13 @@ def test_probe_argument_checks(lib):
         assert decode_status(lib, d, probe=p) == 2
     p.n_pos = 3
     need3 = lib.dwkv_workspace_bytes(C.byref(d), C.byref(p))
-    ref = need - lib.dwkv_workspace_bytes(C.byref(d), None)
     G = d.n_q_heads // d.n_kv_heads
+    # reference partials: 256-token chunks (3000 tokens x 2 heads over 256
+    # workgroups), 4 + 8 work items of the 1000- and 2000-token sequences
+    ref = up256(12 * 2 * G * 132 * 4)
+    # the wide merge's per-chunk Eq. 3 sums (8 chunks of 16 channels) and counters
+    assert need == lib.dwkv_workspace_bytes(C.byref(d), None) + ref + up256(d.batch * 2 * G * 8 * 2 * 4) \
+        + up256(d.batch * 2 * G * 4)
     assert need3 == need + 2 * 2 * ref + up256(d.batch * 2 * G * 2 * 4)
     assert decode_status(lib, d, probe=p, ws=need3 - 1) == 4
     p.n_pos = 0
@@ -200,8 +205,8 @@ def test_route_and_map_argument_checks(lib):
 
 
 def test_decode_launch_count(lib):
-    """The split-K pass and the merge; a probe adds its reference pass, and on
-    the token-lane kernel a small merge of the probed heads after the wide one."""
+    """The split-K pass and the merge; a probe adds its reference pass (the
+    merge evaluates Eq. 3 on either kernel)."""
     from paper_2607_06523_amd import binding
     for kw in (dict(), dict(n_q_heads=16), dict(batch=3, cu_seqlens_host=[0, 700, 700, 1300], total_tokens=1300)):
         d, keep = dims(**kw)
@@ -209,7 +214,7 @@ def test_decode_launch_count(lib):
     heads = np.array([1], dtype=np.int32)
     p = binding.Probe(1, heads.ctypes.data_as(C.POINTER(C.c_int32)), FAKE, FAKE, 1e-6, FAKE, 0)
     d, keep = dims()                                  # G = 4, r_b 32: token-lane kernel
-    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 4
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3
     d, keep = dims(n_q_heads=32)                      # G = 16: general kernel
     assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3
     d, keep = dims(n_q_heads=7)
@@ -219,11 +224,11 @@ def test_decode_launch_count(lib):
     # chunks: positions 1 and 2 see tokens (of the first sequences), 3 only of the first
     d, keep = dims(batch=3, cu_seqlens_host=[0, 700, 700, 702], total_tokens=702, split_tokens=256)
     p.n_pos, p.q_prev = 4, FAKE
-    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 4 + 2 * 3 + 1
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3 + 2 * 3 + 1
     d, keep = dims(batch=2, cu_seqlens_host=[0, 2, 3], total_tokens=3, split_tokens=256)
-    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 4 + 2 * 1 + 1
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3 + 2 * 1 + 1
     p.n_pos = 1
-    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 4
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3
 
 
 def test_route_range_and_compress_argument_checks(lib):

@@ -51,7 +51,8 @@ PROBE_CASES = [
     # name, G, r_b, levels, probs, lengths (None: ragged draw), split
     # general kernel (ranks to 32 at G = 4): one merge covers outputs and probe
     ("general-g4-ranks32", 4, 64, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), None, 512),
-    # token-lane kernels: the wide merge, then the probe merge of the probed heads
+    # token-lane kernels: the wide merge's probed-head workgroups evaluate Eq. 3 per
+    # channel chunk; the last chunk of a column adds the chunks' sums
     ("tl-g4", 4, 48, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), None, 512),
     ("tl-g8-empty-seq", 8, 64, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), [0, 2100, 1700], 256),
 ]
