@@ -153,7 +153,6 @@ struct WsLayout {
   size_t main_bytes, ref_bytes, pos_bytes, acc_off, chunk_off, count_off, total;
 };
 
-constexpr int kProbeChunks = kHeadDim / 16;   // output-channel chunks of the token-lane wide merge
 
 WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
   const int split = plan_split(d);
@@ -168,10 +167,10 @@ WsLayout ws_layout(const dwkv_dims* d, const dwkv_probe* p) {
   w.pos_bytes = np > 1 ? w.ref_bytes : 0;
   w.acc_off = w.main_bytes + w.ref_bytes + (size_t)(np - 1) * 2 * w.pos_bytes;
   const size_t acc_bytes = np > 1 ? align_up((size_t)d->batch * p->n_heads * g * 2 * sizeof(float), 256) : 0;
-  // the wide merge's Eq. 3 sums per output-channel chunk, and its counters
+  // the wide merge's reference rows of the probed columns, and its counters
   const size_t cols = p ? (size_t)d->batch * p->n_heads * g : 0;
   w.chunk_off = w.acc_off + acc_bytes;
-  w.count_off = w.chunk_off + align_up(cols * kProbeChunks * 2 * sizeof(float), 256);
+  w.count_off = w.chunk_off + align_up(cols * kHeadDim * sizeof(float), 256);
   w.total = w.count_off + align_up(cols * sizeof(uint32_t), 256);
   if (w.total == 0) w.total = 256;
   return w;
@@ -425,13 +424,16 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
       P.err = probe->err;
       P.out_ref = probe->out_ref;
       P.acc = probe_positions(probe) > 1 ? reinterpret_cast<float*>(ws + wl.acc_off) : nullptr;
-      P.chunk = reinterpret_cast<float*>(ws + wl.chunk_off);
+      P.oref = reinterpret_cast<float*>(ws + wl.chunk_off);
       P.count = reinterpret_cast<uint32_t*>(ws + wl.count_off);
       P.n_probe = probe->n_heads;
       P.eps = probe->eps;
       P.ref_split = plan_split_ref(d, probe->n_heads);
       P.ref_wt = work_table(d, P.ref_split);
-      for (int i = 0; i < probe->n_heads; ++i) P.slot_of_kv[probe->kv_heads_host[i]] = i;
+      for (int i = 0; i < probe->n_heads; ++i) {
+        P.slot_of_kv[probe->kv_heads_host[i]] = i;
+        P.kv_of_slot[i] = probe->kv_heads_host[i];
+      }
     }
     const hipError_t e = launch_merge_tl(d->basis_rank, d->n_q_heads / d->n_kv_heads, wm, s);
     if (e != hipSuccess || probe_positions(probe) == 1) return hip_status(e);

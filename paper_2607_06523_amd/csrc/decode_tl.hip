@@ -865,8 +865,131 @@ constexpr int kSc1 = 16;                // buffer cache policy: device-coherent 
 constexpr int kWmThreads = 256;
 constexpr int kWmCh = 16;                       // output channels per workgroup
 
-constexpr int kPrG = kWmThreads / (kWmCh / 4);  // reference row groups of the probe tail (64)
+constexpr int kPrG = kWmThreads / (kWmCh / 4);  // reference row groups of a probe chunk (64)
 constexpr int kPrRPT = 4;                         // reference partials per thread per round
+constexpr int kWmNCH = D / kWmCh;                 // output-channel chunks of a row
+
+// Eq. 3 for a probed column (b, probed slot, group member) in the wide merge:
+// its 8 output chunks (the merge's own workgroups) and its 8 reference chunks
+// (extra workgroups) each publish their 16 channels and count themselves in;
+// the 16th to arrive reads both rows and writes err (or, with several
+// positions, the sums to acc), then resets the counter.  Nothing waits.
+__device__ __forceinline__ void wm_probe_arrive(const WideProbe& P, int64_t col, int64_t orow, const float* out) {
+  __shared__ uint32_t arrived;
+  __syncthreads();                      // this chunk's stores are fenced by their writers
+  if (threadIdx.x == 0) arrived = atomicAdd(&P.count[col], 1u);
+  __syncthreads();
+  if (arrived != 2u * kWmNCH - 1u) return;
+  __threadfence();                      // every chunk of the column is visible
+  if (threadIdx.x >= 64) return;
+  const int lane = threadIdx.x;
+  float d2 = 0.f, r2 = 0.f;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int c = lane + 64 * h;
+    const float o = __hip_atomic_load(out + orow + c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const float r = __hip_atomic_load(P.oref + col * D + c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    d2 += (r - o) * (r - o);
+    r2 += r * r;
+  }
+  d2 = wave_sum(d2);
+  r2 = wave_sum(r2);
+  if (lane == 0) {
+    if (P.acc) {
+      P.acc[2 * col] = d2;
+      P.acc[2 * col + 1] = r2;
+    } else {
+      P.err[col] = sqrtf(d2) / (sqrtf(r2) + P.eps);
+    }
+    P.count[col] = 0;                   // ready for the next call
+  }
+}
+
+// Reference chunk `idx` (probed slot, group member, channel chunk) of
+// sequence b: the reference partials' channels [c0, c0 + 16) merged in a
+// fixed order (64 row groups of 4 quads, each taking every 64th partial; then
+// a butterfly over the wave's row groups and the 4 waves through LDS).
+template <int G>
+__device__ __forceinline__ void wm_probe_ref(const WMergeArgs& A, int idx, int b) {
+  __shared__ f4 wr[kWmThreads / 64][kWmCh / 4];
+  __shared__ float wmx[kWmThreads / 64][kWmCh / 4], wlx[kWmThreads / 64][kWmCh / 4];
+  const SplitArgs& a = A.s;
+  const WideProbe& P = A.p;
+  const int ch = idx % kWmNCH, g = (idx / kWmNCH) % G, sl = idx / (kWmNCH * G);
+  const int c0 = ch * kWmCh;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  int base_r, ns_r;
+  seq_work_entry(P.ref_wt, a.cu, P.ref_split, b, base_r, ns_r);
+  const int pq = tid % (kWmCh / 4), prg = tid / (kWmCh / 4);
+  const int64_t prs = (int64_t)P.n_probe * G * kPartStride;
+  const float* pr0 = P.part_ref + (((int64_t)base_r * P.n_probe + sl) * G + g) * kPartStride;
+  f4 racc = f4{0.f, 0.f, 0.f, 0.f};
+  float rm = -INFINITY, rl = 0.f;
+  for (int s0 = 0; s0 < ns_r; s0 += kPrG * kPrRPT) {
+    f4 xv[kPrRPT];
+    float2 ml[kPrRPT];
+#pragma unroll
+    for (int i = 0; i < kPrRPT; ++i) {
+      const float* row = pr0 + (int64_t)min(s0 + prg + kPrG * i, ns_r - 1) * prs;
+      xv[i] = *reinterpret_cast<const f4*>(row + c0 + 4 * pq);
+      ml[i] = *reinterpret_cast<const float2*>(row + D);
+    }
+    float mv[kPrRPT];
+    float mr = rm;
+#pragma unroll
+    for (int i = 0; i < kPrRPT; ++i) {
+      mv[i] = s0 + prg + kPrG * i < ns_r ? ml[i].x : -INFINITY;
+      mr = fmaxf(mr, mv[i]);
+    }
+    const float resc = rm == -INFINITY ? 0.f : exp2f(rm - mr);
+    racc *= resc;
+    rl *= resc;
+#pragma unroll
+    for (int i = 0; i < kPrRPT; ++i) {
+      const float w = mv[i] == -INFINITY ? 0.f : exp2f(mv[i] - mr);
+      racc += w * xv[i];
+      rl += w * ml[i].y;
+    }
+    rm = mr;
+  }
+  // the wave's 16 row groups of each quad (lanes pq, pq + 4, ...)
+#pragma unroll
+  for (int o = 4; o < 64; o <<= 1) {
+    const float m2 = __shfl_xor(rm, o), l2 = __shfl_xor(rl, o);
+    const f4 a2 = f4{__shfl_xor(racc.x, o), __shfl_xor(racc.y, o), __shfl_xor(racc.z, o), __shfl_xor(racc.w, o)};
+    const float mx = fmaxf(rm, m2);
+    const float e1 = rm == -INFINITY ? 0.f : exp2f(rm - mx), e2 = m2 == -INFINITY ? 0.f : exp2f(m2 - mx);
+    racc = e1 * racc + e2 * a2;
+    rl = e1 * rl + e2 * l2;
+    rm = mx;
+  }
+  if (lane < kWmCh / 4) {
+    wr[wv][lane] = racc;
+    wmx[wv][lane] = rm;
+    wlx[wv][lane] = rl;
+  }
+  __syncthreads();
+  const int64_t col = (int64_t)b * P.n_probe * G + sl * G + g;
+  if (tid < kWmCh / 4) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < kWmThreads / 64; ++v) mx = fmaxf(mx, wmx[v][tid]);
+    f4 r = f4{0.f, 0.f, 0.f, 0.f};
+    float l = 0.f;
+#pragma unroll
+    for (int v = 0; v < kWmThreads / 64; ++v) {
+      const float e = wmx[v][tid] == -INFINITY ? 0.f : exp2f(wmx[v][tid] - mx);
+      r += e * wr[v][tid];
+      l += e * wlx[v][tid];
+    }
+    r *= l > 0.f ? 1.0f / l : 0.f;
+    *reinterpret_cast<f4*>(P.oref + col * D + c0 + 4 * tid) = r;
+    if (P.out_ref) *reinterpret_cast<f4*>(P.out_ref + col * D + c0 + 4 * tid) = r;
+    __threadfence();
+  }
+  const int64_t orow = ((int64_t)b * a.n_q_heads + P.kv_of_slot[sl] * G + g) * D;
+  wm_probe_arrive(P, col, orow, a.out);
+}
 
 template <int RB, int G>
 __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs A) {
@@ -881,11 +1004,11 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
   __shared__ float wm[RG], wl[RG];
   __shared__ alignas(16) float fin[4 * QW];
   __shared__ float red2[KG][kWmCh];
-  __shared__ f4 pred[kPrG][kWmCh / 4];
-  __shared__ float pm[kPrG], pl[kPrG];
-  __shared__ float pfin[2][kWmCh];
-  __shared__ uint32_t plast;
   const int tid = threadIdx.x;
+  if ((int)blockIdx.x >= a.n_slots * G * NCH) {   // a probed column's reference chunk
+    wm_probe_ref<G>(A, blockIdx.x - a.n_slots * G * NCH, blockIdx.y);
+    return;
+  }
   const int ch = blockIdx.x % NCH, g = (blockIdx.x / NCH) % G, slot = blockIdx.x / (NCH * G), b = blockIdx.y;
   const int c0 = ch * kWmCh;
   const int kvh = a.kv_of_slot[slot];
@@ -975,100 +1098,15 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
   }
   __syncthreads();
   const int sl = A.p.n_probe > 0 ? A.p.slot_of_kv[kvh] : -1;
+  const int64_t orow = ((int64_t)b * a.n_q_heads + kvh * G + g) * D;
   if (tid < kWmCh) {
     float o = fin[tid];
 #pragma unroll
     for (int j = 0; j < KG; ++j) o += red2[j][tid];
-    a.out[((int64_t)b * a.n_q_heads + kvh * G + g) * D + c0 + tid] = o;
-    pfin[0][tid] = o;
+    a.out[orow + c0 + tid] = o;
+    if (sl >= 0) __threadfence();       // published for the column's Eq. 3
   }
-  if (sl < 0) return;
-
-  // Eq. 3 for a probed head: merge the reference partials' channels
-  // [c0, c0 + 16) (row group tid / 4 takes every 64th partial, quad tid % 4)
-  const WideProbe& P = A.p;
-  int base_r, ns_r;
-  seq_work(P.ref_wt, a.cu, P.ref_split, b, base_r, ns_r);
-  const int pq = tid % (kWmCh / 4), prg = tid / (kWmCh / 4);
-  const int64_t prs = (int64_t)P.n_probe * G * kPartStride;
-  const float* pr0 = P.part_ref + (((int64_t)base_r * P.n_probe + sl) * G + g) * kPartStride;
-  f4 racc = f4{0.f, 0.f, 0.f, 0.f};
-  float rm = -INFINITY, rl = 0.f;
-  for (int s0 = 0; s0 < ns_r; s0 += kPrG * kPrRPT) {
-    f4 xv[kPrRPT];
-    float mv[kPrRPT], lv[kPrRPT];
-#pragma unroll
-    for (int i = 0; i < kPrRPT; ++i) {
-      const float* row = pr0 + (int64_t)min(s0 + prg + kPrG * i, ns_r - 1) * prs;
-      xv[i] = *reinterpret_cast<const f4*>(row + c0 + 4 * pq);
-      mv[i] = row[D];
-      lv[i] = row[D + 1];
-    }
-    float mr = rm;
-#pragma unroll
-    for (int i = 0; i < kPrRPT; ++i) {
-      if (s0 + prg + kPrG * i >= ns_r) mv[i] = -INFINITY;
-      mr = fmaxf(mr, mv[i]);
-    }
-    const float resc = rm == -INFINITY ? 0.f : exp2f(rm - mr);
-    racc *= resc;
-    rl *= resc;
-#pragma unroll
-    for (int i = 0; i < kPrRPT; ++i) {
-      const float w = mv[i] == -INFINITY ? 0.f : exp2f(mv[i] - mr);
-      racc += w * xv[i];
-      rl += w * lv[i];
-    }
-    rm = mr;
-  }
-  pred[prg][pq] = racc;
-  if (pq == 0) {
-    pm[prg] = rm;
-    pl[prg] = rl;
-  }
-  __syncthreads();
-  const int64_t col = (int64_t)b * P.n_probe * G + sl * G + g;
-  if (tid < kWmCh / 4) {
-    float mx = -INFINITY;
-    for (int j = 0; j < kPrG; ++j) mx = fmaxf(mx, pm[j]);
-    f4 r = f4{0.f, 0.f, 0.f, 0.f};
-    float l = 0.f;
-    for (int j = 0; j < kPrG; ++j) {
-      const float e = pm[j] == -INFINITY ? 0.f : exp2f(pm[j] - mx);
-      r += e * pred[j][tid];
-      l += e * pl[j];
-    }
-    r *= l > 0.f ? 1.0f / l : 0.f;
-    *reinterpret_cast<f4*>(&pfin[1][4 * tid]) = r;
-    if (P.out_ref) *reinterpret_cast<f4*>(P.out_ref + col * D + c0 + 4 * tid) = r;
-  }
-  __syncthreads();
-  if (tid < 64) {                       // wave 0: this chunk's sums, then the column's count
-    const float r = tid < kWmCh ? pfin[1][tid] : 0.f, o = tid < kWmCh ? pfin[0][tid] : 0.f;
-    const float d2 = wave_sum((r - o) * (r - o)), r2 = wave_sum(r * r);
-    if (tid == 0) {
-      P.chunk[(col * NCH + ch) * 2] = d2;
-      P.chunk[(col * NCH + ch) * 2 + 1] = r2;
-      __threadfence();
-      plast = atomicAdd(&P.count[col], 1u);
-    }
-  }
-  __syncthreads();
-  if (plast != (uint32_t)(NCH - 1) || tid != 0) return;
-  // the column's last chunk: every chunk's sums are visible after the fence
-  __threadfence();
-  float sd = 0.f, sr = 0.f;
-  for (int k = 0; k < NCH; ++k) {
-    sd += __hip_atomic_load(&P.chunk[(col * NCH + k) * 2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    sr += __hip_atomic_load(&P.chunk[(col * NCH + k) * 2 + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  if (P.acc) {
-    P.acc[2 * col] = sd;
-    P.acc[2 * col + 1] = sr;
-  } else {
-    P.err[col] = sqrtf(sd) / (sqrtf(sr) + P.eps);
-  }
-  P.count[col] = 0;                     // ready for the next call
+  if (sl >= 0) wm_probe_arrive(A.p, (int64_t)b * A.p.n_probe * G + sl * G + g, orow, a.out);
 }
 
 template <int RB, int G, bool RESID, bool SCORES, bool C8>
@@ -1580,7 +1618,7 @@ hipError_t launch_tl_rb(int rb, int g, const SplitArgs& a, int n_work, hipStream
 
 template <int RB>
 hipError_t launch_merge_tl_rb(int g, const WMergeArgs& a, hipStream_t s) {
-  const dim3 grid(a.s.n_slots * g * (D / kWmCh), a.s.batch);
+  const dim3 grid((a.s.n_slots + a.p.n_probe) * g * kWmNCH, a.s.batch);
   switch (g) {
     case 1: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 1>), grid, dim3(kWmThreads), 0, s, a); break;
     case 2: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 2>), grid, dim3(kWmThreads), 0, s, a); break;

@@ -112,23 +112,23 @@ struct SplitArgs {
   int32_t n_zero;              // merge's probe counters), or null
 };
 
-// Eq. 3 in the token-lane wide merge: the workgroups of a probed KV head also
-// merge the reference partials of their 16 output channels, leave the
-// chunk's sums of (O_ref - O)^2 and O_ref^2, and the last of the d/16 chunk
-// workgroups of a column (a counter) adds them in chunk order and writes err
-// (or, with several positions, the sums to acc).
+// Eq. 3 in the token-lane wide merge: extra workgroups merge the reference
+// partials of a probed column 16 channels at a time into oref; the last of
+// the column's output and reference chunk workgroups (a counter) reads both
+// rows and writes err (or, with several positions, the sums to acc).
 struct WideProbe {
   const float* part_ref;       // reference partials [work][n_probe][G][kPartStride]
   float* err;                  // [B][n_probe*G]
   float* out_ref;              // [B][n_probe*G][d] or null
   float* acc;                  // [B][n_probe*G][2] (several positions) or null
-  float* chunk;                // [B][n_probe*G][d/16][2] per-chunk sums
+  float* oref;                 // [B][n_probe*G][d] the reference rows (workspace)
   uint32_t* count;             // [B][n_probe*G] chunks done: zero before the merge, reset by the last
   int32_t n_probe;             // 0: no probe
   float eps;
   int32_t ref_split;
   WorkTable ref_wt;
   int32_t slot_of_kv[DWKV_MAX_PROBE_HEADS];   // probed slot of each KV head, -1 when not probed
+  int32_t kv_of_slot[DWKV_MAX_PROBE_HEADS];   // KV head of each probed slot
 };
 
 struct WMergeArgs {

@@ -146,8 +146,8 @@ def test_probe_argument_checks(lib):
     # reference partials: 256-token chunks (3000 tokens x 2 heads over 256
     # workgroups), 4 + 8 work items of the 1000- and 2000-token sequences
     ref = up256(12 * 2 * G * 132 * 4)
-    # the wide merge's per-chunk Eq. 3 sums (8 chunks of 16 channels) and counters
-    assert need == lib.dwkv_workspace_bytes(C.byref(d), None) + ref + up256(d.batch * 2 * G * 8 * 2 * 4) \
+    # the wide merge's reference rows of the probed columns, and its counters
+    assert need == lib.dwkv_workspace_bytes(C.byref(d), None) + ref + up256(d.batch * 2 * G * 128 * 4) \
         + up256(d.batch * 2 * G * 4)
     assert need3 == need + 2 * 2 * ref + up256(d.batch * 2 * G * 2 * 4)
     assert decode_status(lib, d, probe=p, ws=need3 - 1) == 4
