@@ -876,11 +876,14 @@ constexpr int kWmNCH = D / kWmCh;                 // output-channel chunks of a 
 // positions, the sums to acc), then resets the counter.  Nothing waits.
 __device__ __forceinline__ void wm_probe_arrive(const WideProbe& P, int64_t col, int64_t orow, const float* out) {
   __shared__ uint32_t arrived;
-  __syncthreads();                      // this chunk's stores are fenced by their writers
+  // the chunk's rows went out as device-coherent (agent-scope atomic) stores;
+  // each wave waits for its own to complete before the count, so a reader
+  // that sees the count reaches them with device-coherent loads
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  __syncthreads();
   if (threadIdx.x == 0) arrived = atomicAdd(&P.count[col], 1u);
   __syncthreads();
   if (arrived != 2u * kWmNCH - 1u) return;
-  __threadfence();                      // every chunk of the column is visible
   if (threadIdx.x >= 64) return;
   const int lane = threadIdx.x;
   float d2 = 0.f, r2 = 0.f;
@@ -983,9 +986,12 @@ __device__ __forceinline__ void wm_probe_ref(const WMergeArgs& A, int idx, int b
       l += e * wlx[v][tid];
     }
     r *= l > 0.f ? 1.0f / l : 0.f;
-    *reinterpret_cast<f4*>(P.oref + col * D + c0 + 4 * tid) = r;
+    float* dst = P.oref + col * D + c0 + 4 * tid;
+    __hip_atomic_store(dst, r.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(dst + 1, r.y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(dst + 2, r.z, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(dst + 3, r.w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (P.out_ref) *reinterpret_cast<f4*>(P.out_ref + col * D + c0 + 4 * tid) = r;
-    __threadfence();
   }
   const int64_t orow = ((int64_t)b * a.n_q_heads + P.kv_of_slot[sl] * G + g) * D;
   wm_probe_arrive(P, col, orow, a.out);
@@ -1103,8 +1109,10 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
     float o = fin[tid];
 #pragma unroll
     for (int j = 0; j < KG; ++j) o += red2[j][tid];
-    a.out[orow + c0 + tid] = o;
-    if (sl >= 0) __threadfence();       // published for the column's Eq. 3
+    if (sl >= 0)                        // device-coherent: read back by the column's Eq. 3
+      __hip_atomic_store(a.out + orow + c0 + tid, o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+      a.out[orow + c0 + tid] = o;
   }
   if (sl >= 0) wm_probe_arrive(A.p, (int64_t)b * A.p.n_probe * G + sl * G + g, orow, a.out);
 }
