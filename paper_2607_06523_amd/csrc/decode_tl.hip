@@ -93,9 +93,11 @@ struct alignas(16) TSmem {
   float ep_l[kTW][HG];
   float ep_a[kTW][HG][RB];
   float qmaxw[4][HG];                   // per q~ wave: largest |q~| of each head
-  // groups of 8: the score product's q~ operands (hi, lo per k-step, the
-  // lane's fragment), re-read each tile instead of held in registers
-  alignas(16) h4 qa[HG == 8 ? 2 : 1][HG == 8 ? TCfg<RB>::NS : 1][64];
+  // groups of 8 (and r_b 64 with int8 codes): the score product's q~
+  // operands (hi, lo per k-step, the lane's fragment), re-read each tile
+  // instead of held in registers
+  static constexpr bool QLDS = HG == 8 || RB == 64;
+  alignas(16) h4 qa[QLDS ? 2 : 1][QLDS ? TCfg<RB>::NS : 1][64];
   // Value residual, per wave.  Accumulators are fixed point in units of
   // 2^(ex - kFxTop) (ex: the wave's bound on the value scales): integer LDS
   // atomics run at one instruction per few cycles whatever the active lanes,
@@ -546,7 +548,7 @@ __device__ __forceinline__ void tstep(TState<RB, G, C8>& st, TFrags<RB, C8>& fr,
   h4 qh[NS], ql[NS];
 #pragma unroll
   for (int k = 0; k < NS; ++k) {
-    if constexpr (HG == 8) {
+    if constexpr (HG == 8 || (C8 && RB == 64)) {
       qh[k] = sm.qa[0][k][lane];
       ql[k] = sm.qa[1][k][lane];
     } else {
@@ -1323,7 +1325,7 @@ __device__ __forceinline__ void tl_body(const SplitArgs& a, TSmem<RB, G, RESID>&
         st.qlo[s][i] = (_Float16)(v - (float)hh);
       }
     }
-    if constexpr (HG == 8) {            // every wave writes the same bytes
+    if constexpr (HG == 8 || (C8 && RB == 64)) {   // every wave writes the same bytes
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
         sm.qa[0][s][lane] = st.qhi[s];
