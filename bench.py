@@ -329,8 +329,9 @@ class DeviceCache2:
 def measure_probe(dc, host, torch, steps: int = 5, warmup: int = 2):
     """The decode step with the Eq. 3 probe on one KV head and on all of them:
     each layer runs the factorized decode plus the dense reference pass over
-    the probed heads' fp16 reference cache and the probe error.  One synthetic
-    reference (random fp16, all T tokens) serves every layer."""
+    the probed heads' fp16 reference cache and the probe error.  Every layer
+    has its own synthetic reference (random fp16, all T tokens), so no layer
+    finds another's reference in a cache."""
     from paper_2607_06523_amd import ProbeRef
     L, T, d, Hk = host.n_layers, host.total_tokens, host.head_dim, host.n_kv_heads
     T16 = -(-T // 16) * 16
@@ -339,14 +340,14 @@ def measure_probe(dc, host, torch, steps: int = 5, warmup: int = 2):
     for heads in ((0,), tuple(range(Hk))):
         n = len(heads)
         gen = torch.Generator(device="cuda").manual_seed(7)
-        k_ref = torch.randn((n, T, d), device="cuda", generator=gen).half()
-        v_ref = torch.randn((n, T16 // 16, d, 16), device="cuda", generator=gen).half()
-        probe = ProbeRef(list(heads), k_ref, v_ref)
-        ws = dc.new_workspace(probe)
+        probes = [ProbeRef(list(heads), torch.randn((n, T, d), device="cuda", generator=gen).half(),
+                           torch.randn((n, T16 // 16, d, 16), device="cuda", generator=gen).half())
+                  for _ in range(L)]
+        ws = dc.new_workspace(probes[0])
 
         def step():
             for l in range(L):
-                dc.decode(l, probe=probe, workspace=ws)
+                dc.decode(l, probe=probes[l], workspace=ws)
         for _ in range(warmup):
             step()
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -359,9 +360,10 @@ def measure_probe(dc, host, torch, steps: int = 5, warmup: int = 2):
         ms = ev[0].elapsed_time(ev[1]) / steps
         res[f"probe_{n}_heads"] = {"tokens_per_s": round(host.batch / (ms / 1e3), 2), "ms_per_step": round(ms, 4),
                                    "reference_bytes_per_layer": int(n * T * d * 2 * 2)}
-        del k_ref, v_ref, ws
-    res["note"] = ("dwkv_decode with a probe on every layer: the factorized decode plus a dense split pass over "
-                   "the probed heads' fp16 reference and the Eq. 3 error in the merge")
+        del probes, ws
+    res["note"] = ("dwkv_decode with a probe on every layer (each layer its own fp16 reference): the factorized "
+                   "decode plus a dense split pass over the probed heads' reference and the Eq. 3 error in the "
+                   "merge")
     return res
 
 
