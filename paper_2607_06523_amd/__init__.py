@@ -239,9 +239,11 @@ class DeviceCache:
         binding.check(st, "dwkv_decode")
         return out if probe is None else (out, err, out_ref)
 
-    def decode_noalloc(self, layer: int, q=None, sm_scale: float | None = None, out=None):
+    def decode_noalloc(self, layer: int, q=None, sm_scale: float | None = None, out=None,
+                       probe: ProbeRef | None = None, err=None):
         """dwkv_decode_noalloc: decode with the library's static scratch (no
-        workspace); out [B,Hq,d] fp32 must be given or is allocated here by torch."""
+        workspace); out [B,Hq,d] fp32 (and err [B, n*G] with a probe) must be
+        given or are allocated here by torch.  Returns out, or (out, err)."""
         torch = self.torch
         if q is None:
             q = self.q[layer]
@@ -250,10 +252,15 @@ class DeviceCache:
         qt = F16 if q.dtype == torch.float16 else BF16
         if out is None:
             out = torch.empty((self.batch, self.n_q_heads, self.head_dim), dtype=torch.float32, device=self.device)
+        if probe is not None and err is None:
+            G = self.n_q_heads // self.n_kv_heads
+            err = torch.empty((self.batch, len(probe.kv_heads) * G), dtype=torch.float32, device=self.device)
+        p, keep = self._probe_struct(probe, err, None)
         st = self.lib.dwkv_decode_noalloc(C.byref(self.dims), C.byref(self.cstruct), int(layer), _ptr(q), qt,
-                                          float(sm_scale or 0.0), _ptr(out), None, _stream(torch, self.device))
+                                          float(sm_scale or 0.0), _ptr(out), C.byref(p) if p is not None else None,
+                                          _stream(torch, self.device))
         binding.check(st, "dwkv_decode_noalloc")
-        return out
+        return out if probe is None else (out, err)
 
     def decode_partials(self, layer: int, q=None, sm_scale: float | None = None, workspace=None,
                         probe: ProbeRef | None = None, err=None):

@@ -184,3 +184,33 @@ def test_probe_positions_match_oracle(case):
     # two calls in a row agree bit for bit
     _, err2, _ = dc.decode(layer, probe=pr)
     assert np.array_equal(err, err2.cpu().numpy())
+
+
+@pytest.mark.parametrize("positions", [1, 3])
+def test_probe_two_phase_matches_one_phase(positions):
+    """dwkv_decode_partials + dwkv_decode_merge with a probe (the reference
+    passes in the first half, Eq. 3 in the second) equal dwkv_decode bit for
+    bit, outputs and errors, on the token-lane kernel."""
+    torch = torch_gpu()
+    from paper_2607_06523_amd import ProbeRef
+    from synth.layout import block_values
+    host = generate(Workload(name="probe-two-phase", batch=2, n_layers=2, window=2, n_kv_heads=2, n_q_heads=8,
+                             head_dim=128, context=2000, basis_rank=32, levels=(0, 8, 16), probs=(0.7, 0.2, 0.1),
+                             q_dtype="bf16", seed=43, ragged=(1, 2000)), threads=4)
+    dc = device_cache(host, split_tokens=256)
+    heads = [1]
+    K, V = _refs(host, 0, heads, 0.05, seed=9)
+    q_prev = None
+    if positions > 1:
+        q_prev = torch.randn((positions - 1, host.batch, host.n_q_heads, 128)).to(torch.bfloat16).cuda()
+    pr = ProbeRef(heads, torch.from_numpy(K.view(np.uint16)).view(torch.float16).cuda(),
+                  torch.from_numpy(block_values(V).view(np.uint16)).view(torch.float16).cuda(), 1e-6, q_prev=q_prev)
+    announce(f"probe two-phase, {positions} position(s)")
+    out1, err1, _ = dc.decode(0, probe=pr)
+    ws = dc.new_workspace(pr)
+    err2 = torch.empty_like(err1)
+    dc.decode_partials(0, workspace=ws, probe=pr, err=err2)
+    out2 = dc.decode_merge(0, workspace=ws, probe=pr, err=err2)
+    torch.cuda.synchronize()
+    assert np.array_equal(out1.cpu().numpy(), out2.cpu().numpy())
+    assert np.array_equal(err1.cpu().numpy(), err2.cpu().numpy())

@@ -32,3 +32,34 @@ def test_noalloc_matches_decode_two_calls():
         assert np.array_equal(got, want), f"{host.workload.name}: noalloc output differs from dwkv_decode"
         compare(got, oracle.decode(host, layer, heads=pairs), pairs, G, f"noalloc {host.workload.name}")
         del dc
+
+
+def test_noalloc_with_probe_matches_decode():
+    """With an Eq. 3 probe (the wide merge's counters live in the static array
+    and are cleared by the reference pass of each call), at one and at three
+    positions: outputs and errors equal dwkv_decode's bit for bit, twice in a
+    row."""
+    torch = torch_gpu()
+    from paper_2607_06523_amd import ProbeRef
+    from synth.layout import block_values
+    host = generate(Workload(name="noalloc-probe", batch=2, n_layers=2, window=2, n_kv_heads=4, n_q_heads=16,
+                             head_dim=128, context=1500, basis_rank=48, levels=(0, 4, 8, 16),
+                             probs=(0.7, 0.1, 0.1, 0.1), q_dtype="bf16", seed=37, ragged=(2, 1500)), threads=4)
+    dc = device_cache(host)
+    rng = np.random.default_rng(5)
+    T = host.total_tokens
+    heads = [3, 1]
+    K = rng.standard_normal((2, T, 128)).astype(np.float16)
+    V = rng.standard_normal((2, T, 128)).astype(np.float16)
+    kd = torch.from_numpy(K.view(np.uint16)).view(torch.float16).cuda()
+    vd = torch.from_numpy(block_values(V).view(np.uint16)).view(torch.float16).cuda()
+    q_prev = torch.randn((2, host.batch, host.n_q_heads, 128), dtype=torch.float32).to(torch.bfloat16).cuda()
+    for name, pr in (("one position", ProbeRef(heads, kd, vd)),
+                     ("three positions", ProbeRef(heads, kd, vd, q_prev=q_prev))):
+        for rep in range(2):
+            announce(f"decode_noalloc with probe, {name}, call {rep}")
+            out_n, err_n = dc.decode_noalloc(1, probe=pr)
+            out_d, err_d, _ = dc.decode(1, probe=pr)
+            torch.cuda.synchronize()
+            assert np.array_equal(out_n.cpu().numpy(), out_d.cpu().numpy()), name
+            assert np.array_equal(err_n.cpu().numpy(), err_d.cpu().numpy()), name
