@@ -63,3 +63,37 @@ def test_noalloc_with_probe_matches_decode():
             torch.cuda.synchronize()
             assert np.array_equal(out_n.cpu().numpy(), out_d.cpu().numpy()), name
             assert np.array_equal(err_n.cpu().numpy(), err_d.cpu().numpy()), name
+
+
+def test_noalloc_replayed_from_a_graph():
+    """The allocation-free decode captured in a HIP graph (it enqueues no
+    allocation and no memset) and replayed three times, with eager work and
+    synchronizations between the replays: every replay's output equals the
+    eager call's bit for bit."""
+    torch = torch_gpu()
+    host = generate(Workload(name="noalloc-graph", batch=2, n_layers=2, window=2, n_kv_heads=2, n_q_heads=8,
+                             head_dim=128, context=3000, basis_rank=48, levels=(0, 4, 8, 16),
+                             probs=(0.7, 0.1, 0.1, 0.1), q_dtype="bf16", seed=41, ragged=(1, 3000)), threads=4)
+    dc = device_cache(host)
+    out = torch.empty((host.batch, host.n_q_heads, 128), dtype=torch.float32, device="cuda")
+    announce("decode_noalloc eager")
+    want = dc.decode_noalloc(1, out=torch.empty_like(out)).cpu().numpy()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        dc.decode_noalloc(1, out=out)                 # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    announce("decode_noalloc graph capture")
+    with torch.cuda.graph(graph):
+        dc.decode_noalloc(1, out=out)
+    for rep in range(3):
+        out.fill_(float("nan"))
+        announce(f"decode_noalloc graph replay {rep}")
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy(), want), f"replay {rep} differs from the eager call"
+        dc.decode(0)                                   # eager work between the replays
+        torch.cuda.synchronize()
+    del graph
