@@ -84,6 +84,8 @@ CASES = [
     ("g1-rank0", 1, 16, (0,), (1.0,), [900, 64], 0, False, "f16", 2),
     ("g16-general", 16, 64, (0, 8, 32), (0.5, 0.3, 0.2), [1200, 1], 0, True, "f16", 4),
     ("int8", 4, 48, (0, 4, 8, 16), (0.55, 0.2, 0.15, 0.1), [2000], 0, False, "int8", 3),
+    # more than 16 sequences: one compress launch per non-empty sequence, then the decode
+    ("20-seqs", 4, 32, (0, 8), (0.7, 0.3), [0, 1] + [37 + 23 * i for i in range(18)], 64, True, "f16", 21),
 ]
 
 

@@ -140,6 +140,9 @@ POS_CASES = [
     ("general-g4-p4", 4, 64, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), [1025, 2, 1700], 256, 4),
     ("tl-g4-p3", 4, 48, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), [2049, 0, 1500], 512, 3),
     ("tl-g8-p8", 8, 64, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), [3, 1800, 7], 256, 8),
+    # more sequences than the kernel-argument work table holds: the trimmed
+    # passes walk the device sequence table
+    ("tl-g4-20-seqs-p3", 4, 32, (0, 8), (0.7, 0.3), [1, 2, 0] + [37 + 23 * i for i in range(17)], 64, 3),
 ]
 
 
