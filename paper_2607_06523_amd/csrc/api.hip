@@ -126,6 +126,18 @@ int64_t count_work(const dwkv_dims* d, int split, int trim) {
 
 int probe_positions(const dwkv_probe* p) { return p && p->n_pos > 1 ? p->n_pos : 1; }
 
+// Most work items of any one sequence (chunks of `split`, cut `trim` tokens
+// short, plus `extra` items per non-empty sequence).
+int32_t max_items(const dwkv_dims* d, int split, int trim = 0, int extra = 0) {
+  int64_t n = 0;
+  for (int b = 0; b < d->batch; ++b) {
+    const int64_t len = d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b];
+    const int64_t tb = std::max<int64_t>(len - trim, 0);
+    n = std::max<int64_t>(n, (tb + split - 1) / split + (len > 0 ? extra : 0));
+  }
+  return (int32_t)std::min<int64_t>(n, 0x7fffffff);
+}
+
 dwkv_status check_probe(const dwkv_dims* d, const dwkv_probe* p) {
   if (!p) return DWKV_OK;
   if (p->n_heads < 1 || p->n_heads > d->n_kv_heads || p->n_heads > DWKV_MAX_PROBE_HEADS) return DWKV_E_DIMS;
@@ -417,6 +429,7 @@ dwkv_status merge_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, 
     WMergeArgs wm;
     std::memset(&wm, 0, sizeof(wm));
     wm.s = a;
+    wm.max_ns = max_items(d, a.split);
     for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) wm.p.slot_of_kv[h] = -1;
     if (probe) {                       // Eq. 3 in the same launch
       WideProbe& P = wm.p;
@@ -851,6 +864,7 @@ dwkv_status dwkv_decode_append(const dwkv_dims* d, const dwkv_cache* c, int32_t 
   WMergeArgs m;
   std::memset(&m, 0, sizeof(m));
   m.s = A.s;
+  m.max_ns = max_items(d, split, 1, 1);
   m.s.out = out;
   m.s.mstats = nullptr;
   for (int h = 0; h < DWKV_MAX_PROBE_HEADS; ++h) m.p.slot_of_kv[h] = -1;

@@ -999,34 +999,38 @@ __device__ __forceinline__ void wm_probe_ref(const WMergeArgs& A, int idx, int b
   wm_probe_arrive(P, col, orow, a.out);
 }
 
-template <int RB, int G>
+// CH output channels per workgroup: 16 (and Eq. 3 for probed heads), or 64
+// for merges of a few partials per sequence (fewer, wider workgroups).
+template <int RB, int G, int CH>
 __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs A) {
   const SplitArgs& a = A.s;
-  constexpr int QW = kWmCh / 4 + RB / 4;        // quads per row: the r chunk, then a~
+  constexpr int QW = CH / 4 + RB / 4;        // quads per row: the r chunk, then a~
   constexpr int RG = kWmThreads / QW;           // row groups
   constexpr int RPT = 2;                        // partials per thread per round (32 per round at r_b 48)
-  constexpr int KG = kWmThreads / kWmCh;        // k groups of the projection
+  constexpr int KG = kWmThreads / CH;        // k groups of the projection
   constexpr int KPG = (RB + KG - 1) / KG;       // basis rows per k group
-  constexpr int NCH = D / kWmCh;
+  constexpr int NCH = D / CH;
   __shared__ f4 red[RG][QW];
   __shared__ float wm[RG], wl[RG];
   __shared__ alignas(16) float fin[4 * QW];
-  __shared__ float red2[KG][kWmCh];
+  __shared__ float red2[KG][CH];
   const int tid = threadIdx.x;
-  if ((int)blockIdx.x >= a.n_slots * G * NCH) {   // a probed column's reference chunk
-    wm_probe_ref<G>(A, blockIdx.x - a.n_slots * G * NCH, blockIdx.y);
-    return;
+  if constexpr (CH == kWmCh) {
+    if ((int)blockIdx.x >= a.n_slots * G * NCH) {   // a probed column's reference chunk
+      wm_probe_ref<G>(A, blockIdx.x - a.n_slots * G * NCH, blockIdx.y);
+      return;
+    }
   }
   const int ch = blockIdx.x % NCH, g = (blockIdx.x / NCH) % G, slot = blockIdx.x / (NCH * G), b = blockIdx.y;
-  const int c0 = ch * kWmCh;
+  const int c0 = ch * CH;
   const int kvh = a.kv_of_slot[slot];
   // every kernel argument the merge needs, loaded in one batch at entry
   asm volatile("" ::"s"(a.part), "s"(a.basis), "s"(a.basis_b_stride), "s"(a.out), "s"(a.n_q_heads), "s"(a.n_work),
                "s"(a.split), "s"(kvh), "s"(a.mstats));
   int base, ns;
   seq_work_entry(a.wt, a.cu, a.split, b, base, ns);
-  // B^V rows [kg KPG, kg KPG + KPG) of channel c0 + tid % 16
-  const int pc = tid % kWmCh, kg = tid / kWmCh;
+  // B^V rows [kg KPG, kg KPG + KPG) of channel c0 + tid % CH
+  const int pc = tid % CH, kg = tid / CH;
   const uint16_t* bv = a.basis + (int64_t)b * a.basis_b_stride + ((int64_t)kvh * 2 + 1) * RB * D + c0 + pc;
   uint16_t bvr[KPG];
 #pragma unroll
@@ -1037,7 +1041,7 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
   const int64_t rs = (int64_t)G * kPartStrideTL;
   const float* p0 = a.part + (((int64_t)slot * a.n_work + base) * G + g) * kPartStrideTL;
   const rsrc_t pr = make_rsrc(p0, (uint32_t)(max(ns, 1) * rs * 4));
-  const uint32_t qoff = qi < kWmCh / 4 ? (uint32_t)(c0 + 4 * qi) : (uint32_t)(D + 4 * (qi - kWmCh / 4));
+  const uint32_t qoff = qi < CH / 4 ? (uint32_t)(c0 + 4 * qi) : (uint32_t)(D + 4 * (qi - CH / 4));
   f4 acc = f4{0.f, 0.f, 0.f, 0.f};
   float mstar = -INFINITY, lsum = 0.f;
   for (int s0 = 0; s0 < ns; s0 += RG * RPT) {
@@ -1097,17 +1101,17 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
   }
   __syncthreads();
   {
-    // fin: [r chunk (16) | a~ (RB)]
+    // fin: [r chunk (CH) | a~ (RB)]
     float o = 0.f;
 #pragma unroll
     for (int k = 0; k < KPG; ++k)
-      if (kg * KPG + k < RB) o += fin[kWmCh + kg * KPG + k] * half_bits_to_float(bvr[k]);
+      if (kg * KPG + k < RB) o += fin[CH + kg * KPG + k] * half_bits_to_float(bvr[k]);
     red2[kg][pc] = o;
   }
   __syncthreads();
-  const int sl = A.p.n_probe > 0 ? A.p.slot_of_kv[kvh] : -1;
+  const int sl = CH == kWmCh && A.p.n_probe > 0 ? A.p.slot_of_kv[kvh] : -1;
   const int64_t orow = ((int64_t)b * a.n_q_heads + kvh * G + g) * D;
-  if (tid < kWmCh) {
+  if (tid < CH) {
     float o = fin[tid];
 #pragma unroll
     for (int j = 0; j < KG; ++j) o += red2[j][tid];
@@ -1116,7 +1120,9 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
     else
       a.out[orow + c0 + tid] = o;
   }
-  if (sl >= 0) wm_probe_arrive(A.p, (int64_t)b * A.p.n_probe * G + sl * G + g, orow, a.out);
+  if constexpr (CH == kWmCh) {
+    if (sl >= 0) wm_probe_arrive(A.p, (int64_t)b * A.p.n_probe * G + sl * G + g, orow, a.out);
+  }
 }
 
 template <int RB, int G, bool RESID, bool SCORES, bool C8>
@@ -1626,17 +1632,28 @@ hipError_t launch_tl_rb(int rb, int g, const SplitArgs& a, int n_work, hipStream
 
 }  // namespace
 
-template <int RB>
-hipError_t launch_merge_tl_rb(int g, const WMergeArgs& a, hipStream_t s) {
-  const dim3 grid((a.s.n_slots + a.p.n_probe) * g * kWmNCH, a.s.batch);
+template <int RB, int CH>
+hipError_t launch_merge_tl_ch(int g, const WMergeArgs& a, hipStream_t s) {
+  const dim3 grid((a.s.n_slots + (CH == kWmCh ? a.p.n_probe : 0)) * g * (D / CH), a.s.batch);
   switch (g) {
-    case 1: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 1>), grid, dim3(kWmThreads), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 2>), grid, dim3(kWmThreads), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 4>), grid, dim3(kWmThreads), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 8>), grid, dim3(kWmThreads), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 1, CH>), grid, dim3(kWmThreads), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 2, CH>), grid, dim3(kWmThreads), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 4, CH>), grid, dim3(kWmThreads), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 8, CH>), grid, dim3(kWmThreads), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+// 64-channel workgroups when every sequence has at most kWideFew partials and
+// nothing is probed: the merge is then a few loads per workgroup, and four
+// times fewer workgroups start sooner.
+constexpr int kWideFew = 4;
+
+template <int RB>
+hipError_t launch_merge_tl_rb(int g, const WMergeArgs& a, hipStream_t s) {
+  if (a.p.n_probe == 0 && a.max_ns <= kWideFew) return launch_merge_tl_ch<RB, 64>(g, a, s);
+  return launch_merge_tl_ch<RB, kWmCh>(g, a, s);
 }
 
 bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t res_stride) {

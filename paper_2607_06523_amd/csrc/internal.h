@@ -134,6 +134,7 @@ struct WideProbe {
 struct WMergeArgs {
   SplitArgs s;
   WideProbe p;
+  int32_t max_ns;              // most work items of any sequence (picks the workgroup width)
 };
 
 // Split merge (and Eq. 3 for probed heads): grid = (Hq, B).
