@@ -52,7 +52,8 @@ typedef enum dwkv_status {
                              16 in [16,128], more than 8 levels, 32-bit offset
                              overflow possible; int8 coefficients in a decode
                              off the token-lane path for groups of up to 4
-                             (r_b <= 64, levels <= 16), with a probe, or in
+                             (r_b <= 64, levels <= 16), with a probe over
+                             several positions, with features, or in
                              dwkv_materialize                                     */
   DWKV_E_WORKSPACE = 4,   /* workspace smaller than the *_workspace_bytes value    */
   DWKV_E_LAYOUT = 5,      /* dwkv_validate found a malformed cache                 */

@@ -331,7 +331,10 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
                            hipStream_t s, float* scores = nullptr) {
   if (!c || !q) return DWKV_E_NULL;
   const bool c8 = d->coef_format == DWKV_COEF_I8;
-  if (c8 && (!uses_token_lane(d) || d->n_q_heads / d->n_kv_heads > 4 || probe || scores)) return DWKV_E_UNSUPPORTED;
+  // int8 coefficients: the token-lane kernel for groups of up to 4; a probe of
+  // the current position only (the earlier positions run the general kernel)
+  if (c8 && (!uses_token_lane(d) || d->n_q_heads / d->n_kv_heads > 4 || probe_positions(probe) > 1 || scores))
+    return DWKV_E_UNSUPPORTED;
   SplitArgs a;
   dwkv_status st = split_args(d, c, layer, q, q_type, sm_scale, workspace, a);
   if (st != DWKV_OK) return st;

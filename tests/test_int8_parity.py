@@ -88,3 +88,40 @@ def test_int8_full_size_sampled():
         torch.cuda.synchronize()
         pairs = [(0, 2), (0, 7)]
         compare(out, oracle.decode(host, layer, heads=pairs), pairs, G, f"int8 64k layer {layer}")
+
+
+def test_int8_with_probe():
+    """Eq. 3 on an int8 cache (the current position): the int8 token-lane pass,
+    the dense reference pass and Eq. 3 in the wide merge, against the oracle;
+    a probe over several positions is refused (its earlier positions run the
+    general kernel, which reads fp16 coefficients)."""
+    torch = torch_gpu()
+    from paper_2607_06523_amd import DwkvError, ProbeRef
+    from synth.layout import block_values
+    w = _Fixed(Workload(name="i8-probe", batch=3, n_layers=2, window=2, n_kv_heads=4, n_q_heads=16, head_dim=128,
+                        context=1500, basis_rank=48, levels=(0, 4, 8, 16), probs=(0.7, 0.1, 0.1, 0.1),
+                        q_dtype="bf16", seed=77, coef_format="int8"), [1500, 0, 700])
+    host = generate(w, threads=4)
+    dc = device_cache(host, split_tokens=256)
+    heads, layer = [2, 0], 1
+    rng = np.random.default_rng(3)
+    K = np.stack([np.concatenate([oracle.reconstruct(host, layer, 0, h, b) for b in range(host.batch)])
+                  for h in heads])
+    V = np.stack([np.concatenate([oracle.reconstruct(host, layer, 1, h, b) for b in range(host.batch)])
+                  for h in heads])
+    K = (K + rng.normal(0, 0.05, K.shape)).astype(np.float16)
+    V = (V + rng.normal(0, 0.05, V.shape)).astype(np.float16)
+    pr = ProbeRef(heads, torch.from_numpy(K.view(np.uint16)).view(torch.float16).cuda(),
+                  torch.from_numpy(block_values(V).view(np.uint16)).view(torch.float16).cuda(), 1e-6)
+    announce("int8 decode with a probe")
+    out, err, _ = dc.decode(layer, probe=pr)
+    err = err.cpu().numpy()
+    e_ref = oracle.probe(host, layer, heads, K, V)
+    assert np.abs(err - e_ref).max() <= 1e-4 + 1e-3 * np.abs(e_ref).max(), (err, e_ref)
+    assert np.all(err[1] == 0)
+    compare(out.cpu().numpy(), oracle.decode(host, layer), [(b, h) for b in range(3) for h in range(4)], 4,
+            "int8 with probe")
+    q_prev = torch.zeros((1, host.batch, host.n_q_heads, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(DwkvError) as e:
+        dc.decode(layer, probe=ProbeRef(heads, pr.k_ref, pr.v_ref, 1e-6, q_prev=q_prev))
+    assert e.value.status == 3
