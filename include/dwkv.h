@@ -53,8 +53,7 @@ typedef enum dwkv_status {
                              overflow possible; int8 coefficients in a decode
                              off the token-lane path for groups of up to 4
                              (r_b <= 64, levels <= 16), with a probe over
-                             several positions, with features, or in
-                             dwkv_materialize                                     */
+                             several positions, or in dwkv_materialize            */
   DWKV_E_WORKSPACE = 4,   /* workspace smaller than the *_workspace_bytes value    */
   DWKV_E_LAYOUT = 5,      /* dwkv_validate found a malformed cache                 */
   DWKV_E_HIP = 6,         /* a HIP runtime call or kernel launch failed            */
@@ -386,7 +385,7 @@ size_t dwkv_features_workspace_bytes(const dwkv_dims* dims);
  *   workspace: >= dwkv_features_workspace_bytes(dims) bytes, no initial contents
  * `out` equals dwkv_decode's bit for bit.  Three launches (split-K pass that
  * also stores the scores, merge, features).  DWKV_E_UNSUPPORTED off the
- * token-lane path. */
+ * token-lane path (fp16 coefficients, or int8 for groups of up to 4). */
 dwkv_status dwkv_decode_features(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
                                  const void* q, int32_t q_type, float sm_scale, float* out, float* phi,
                                  void* workspace, size_t ws_bytes, void* stream);

@@ -333,7 +333,7 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   const bool c8 = d->coef_format == DWKV_COEF_I8;
   // int8 coefficients: the token-lane kernel for groups of up to 4; a probe of
   // the current position only (the earlier positions run the general kernel)
-  if (c8 && (!uses_token_lane(d) || d->n_q_heads / d->n_kv_heads > 4 || probe_positions(probe) > 1 || scores))
+  if (c8 && (!uses_token_lane(d) || d->n_q_heads / d->n_kv_heads > 4 || probe_positions(probe) > 1))
     return DWKV_E_UNSUPPORTED;
   SplitArgs a;
   dwkv_status st = split_args(d, c, layer, q, q_type, sm_scale, workspace, a);
@@ -350,7 +350,8 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   a.n_work = (int32_t)nw;
   a.wt = work_table(d, split);
   a.scores = scores;
-  const hipError_t e = c8 ? launch_split_tl_c8(RB, G, max_level(d) > 0, a, (int)nw, s)
+  const hipError_t e = c8 ? (scores ? launch_split_tl_scores_c8(RB, G, max_level(d) > 0, a, (int)nw, s)
+                                   : launch_split_tl_c8(RB, G, max_level(d) > 0, a, (int)nw, s))
                        : uses_token_lane(d)
                            ? (scores ? launch_split_tl_scores(RB, G, max_level(d) > 0, a, (int)nw, s)
                                      : launch_split_tl(RB, G, max_level(d) > 0, a, (int)nw, s))
@@ -1079,7 +1080,6 @@ dwkv_status dwkv_decode_features(const dwkv_dims* d, const dwkv_cache* c, int32_
                                  size_t ws_bytes, void* stream) {
   dwkv_status st = check_decode_common(d, nullptr, workspace, ws_bytes);
   if (st != DWKV_OK) return st;
-  if (d->coef_format != DWKV_COEF_F16) return DWKV_E_UNSUPPORTED;
   if (!uses_token_lane(d)) return DWKV_E_UNSUPPORTED;
   if (!out || !phi) return DWKV_E_NULL;
   if (!aligned16(out) || !aligned16(phi)) return DWKV_E_ALIGN;

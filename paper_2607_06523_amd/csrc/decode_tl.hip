@@ -1679,6 +1679,11 @@ hipError_t launch_split_tl_scores(int rb, int g, bool resid, const SplitArgs& a,
                : launch_tl_rb<false, true, false>(rb, g, a, n_work, s);
 }
 
+hipError_t launch_split_tl_scores_c8(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {
+  return resid ? launch_tl_rb<true, true, true>(rb, g, a, n_work, s)
+               : launch_tl_rb<false, true, true>(rb, g, a, n_work, s);
+}
+
 hipError_t launch_split_tl_c8(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {
   return resid ? launch_tl_rb<true, false, true>(rb, g, a, n_work, s)
                : launch_tl_rb<false, false, true>(rb, g, a, n_work, s);

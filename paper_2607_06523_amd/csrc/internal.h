@@ -307,6 +307,7 @@ hipError_t launch_split_tl_scores(int rb, int g, bool resid, const SplitArgs& a,
 // The pass over int8-blockwise coefficients (coef_k / coef_v point at int8
 // codes, cscale_k / cscale_v at their fp16 block scales).
 hipError_t launch_split_tl_c8(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s);
+hipError_t launch_split_tl_scores_c8(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s);
 // Token-lane merge: reads a.part, writes a.out (one workgroup per slot, head
 // and 16 output channels).
 hipError_t launch_merge_tl(int rb, int g, const WMergeArgs& a, hipStream_t s);

@@ -34,6 +34,9 @@ CASES = [
     ("rb16-g1-short", 16, 1, (0, 2), (0.6, 0.4), [1, 63, 65], 64),
     ("rb64-g4-no-residual", 64, 4, (0,), (1.0,), [1500, 37], 128),
     ("rb64-g8-ranks-to-32", 64, 8, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), [0, 900, 2100], 256),
+    # 8-bit blockwise coefficients
+    ("i8-rb48-g4-ragged", 48, 4, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), [0, 700, 129, 2100], 256),
+    ("i8-rb64-g2-one-seq", 64, 2, (0, 8, 16), (0.7, 0.2, 0.1), [1800], 0),
 ]
 
 
@@ -55,7 +58,8 @@ def test_features_small(case):
     name, rb, G, levels, probs, lengths, split = case
     w = _Fixed(Workload(name=name, batch=len(lengths), n_layers=4, window=2, n_kv_heads=2, n_q_heads=2 * G,
                         head_dim=128, context=max(lengths), basis_rank=rb, levels=levels, probs=probs,
-                        q_dtype="bf16", seed=700 + len(name)), lengths)
+                        q_dtype="bf16", seed=700 + len(name),
+                        coef_format="int8" if name.startswith("i8") else "f16"), lengths)
     host = generate(w, threads=4)
     dc = device_cache(host, split_tokens=split)
     M, Hk, T = host.n_windows, host.n_kv_heads, host.total_tokens
