@@ -1220,6 +1220,10 @@ __device__ __forceinline__ void tl_body(const SplitArgs& a, TSmem<RB, G, RESID>&
     load_offsets(mn, x, j1, lane);
   }
   __builtin_amdgcn_sched_barrier(0);
+  // the waves that do not compute q~ request their first tile now, ahead of
+  // the entries (which wait for the offsets)
+  if (wv >= NS) load_coef<RB, C8>(fr, x, j0, lane);
+  __builtin_amdgcn_sched_barrier(0);
   if constexpr (RESID) load_entries(ec, x, mc, lane);
   __builtin_amdgcn_sched_barrier(0);
   // every entry of the query table once: the group's heads, zeros past G
@@ -1235,8 +1239,6 @@ __device__ __forceinline__ void tl_body(const SplitArgs& a, TSmem<RB, G, RESID>&
     }
     sm.qs[c][hh] = v;
   }
-  // the waves that do not compute q~ request their first tile now
-  if (wv >= NS) load_coef<RB, C8>(fr, x, j0, lane);
   if (wv < NS) {
     // q * qscale for head col, scaled by a power of two so the head's largest
     // entry sits just under 2^14 and split into fp16 hi + lo
