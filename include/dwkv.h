@@ -163,8 +163,10 @@ int32_t dwkv_decode_kernel(const dwkv_dims* dims);
 size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe);
 
 /* Kernel launches one dwkv_decode call enqueues for these dims (2: the
- * split-K pass and the merge; with a probe, 3: the reference pass is added
- * and the merge also evaluates Eq. 3; a probe over n_pos > 1 positions adds
+ * split-K pass and the merge; with a probe the merge also evaluates Eq. 3 and
+ * the reference pass is added -- inside the split-K launch on the token-lane
+ * kernel (still 2), as a launch of its own on the general kernel (3) -- and a
+ * probe over n_pos > 1 positions adds
  * two split passes -- factorized and reference, on the probed heads -- for
  * every earlier position that still sees a token of some sequence, and one
  * merge), or -1 when the dims or probe are invalid.  probe may be NULL. */
@@ -183,8 +185,8 @@ int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe);
  *   workspace:>= dwkv_workspace_bytes(dims, probe) bytes of device memory;
  *             contents need no initialisation and are clobbered; calls
  *             sharing it must be ordered (same stream).
- * Launches the split-K kernel(s) (two with a probe) and the merge kernel(s)
- * (dwkv_decode_launches gives the count).
+ * Launches the split-K kernel(s) (with a probe, the reference pass too) and
+ * the merge kernel(s) (dwkv_decode_launches gives the count).
  * Returns DWKV_OK once enqueued. */
 dwkv_status dwkv_decode(const dwkv_dims* dims, const dwkv_cache* cache, int32_t layer,
                         const void* q, int32_t q_type, float sm_scale, float* out,

@@ -126,6 +126,16 @@ int64_t count_work(const dwkv_dims* d, int split, int trim) {
 
 int probe_positions(const dwkv_probe* p) { return p && p->n_pos > 1 ? p->n_pos : 1; }
 
+// The probe's reference pass runs inside the split-K launch on the token-lane
+// path (one grid of n_work * n_kv_heads split-K workgroups plus one workgroup
+// per reference item).
+bool fused_probe(const dwkv_dims* d, const dwkv_probe* p) {
+  if (!p || !uses_token_lane(d)) return false;
+  const int64_t nt = count_work(d, plan_split(d)) * d->n_kv_heads;
+  const int64_t nr = count_work(d, plan_split_ref(d, p->n_heads)) * p->n_heads;
+  return nr > 0 && nt + nr <= 0x7fffffff;
+}
+
 // Most work items of any one sequence (chunks of `split`, cut `trim` tokens
 // short, plus `extra` items per non-empty sequence).
 int32_t max_items(const dwkv_dims* d, int split, int trim = 0, int extra = 0) {
@@ -242,7 +252,7 @@ size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe) {
 int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe) {
   if (check_dims(dims) != DWKV_OK || check_probe(dims, probe) != DWKV_OK) return -1;
   if (!probe) return 2;
-  int32_t n = 3;
+  int32_t n = fused_probe(dims, probe) ? 2 : 3;
   const int np = probe_positions(probe), split = plan_split_ref(dims, probe->n_heads);
   for (int j = 1; j < np; ++j)
     if (count_work(dims, split, j) > 0) n += 2;
@@ -326,6 +336,8 @@ dwkv_status split_args(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, c
 }
 
 // Split-K pass(es): partial (o, m, l) per (work item, head slot, group member).
+// On the token-lane path the probe's reference pass of the current position
+// shares the split-K launch (launch_split_tl_probe).
 dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t layer, const void* q,
                            int32_t q_type, float sm_scale, const dwkv_probe* probe, void* workspace,
                            hipStream_t s, float* scores = nullptr) {
@@ -350,27 +362,37 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
   a.n_work = (int32_t)nw;
   a.wt = work_table(d, split);
   a.scores = scores;
-  const hipError_t e = c8 ? (scores ? launch_split_tl_scores_c8(RB, G, max_level(d) > 0, a, (int)nw, s)
-                                   : launch_split_tl_c8(RB, G, max_level(d) > 0, a, (int)nw, s))
-                       : uses_token_lane(d)
-                           ? (scores ? launch_split_tl_scores(RB, G, max_level(d) > 0, a, (int)nw, s)
-                                     : launch_split_tl(RB, G, max_level(d) > 0, a, (int)nw, s))
-                           : launch_split(RB, G, max_level(d) > 0, false, a, (int)nw, s);
-  if (e != hipSuccess) return DWKV_E_HIP;
+  // the probe's reference pass (identity basis over the dense rows); its
+  // first workgroup clears the wide merge's probe counters
+  SplitArgs r;
   if (probe) {
-    SplitArgs r = a;
+    r = a;
+    r.scores = nullptr;
     r.coef_k = static_cast<const uint16_t*>(probe->k_ref);
     r.coef_v = static_cast<const uint16_t*>(probe->v_ref);
     r.part = reinterpret_cast<float*>(ws + wl.main_bytes);
     r.n_slots = probe->n_heads;
     for (int i = 0; i < probe->n_heads; ++i) r.kv_of_slot[i] = probe->kv_heads_host[i];
     r.split = plan_split_ref(d, probe->n_heads);
-    const int64_t nw_ref = count_work(d, r.split);
-    r.n_work = (int32_t)nw_ref;
+    r.n_work = (int32_t)count_work(d, r.split);
     r.wt = work_table(d, r.split);
     r.zero = reinterpret_cast<uint32_t*>(ws + wl.count_off);
     r.n_zero = d->batch * probe->n_heads * G;
-    if (launch_split(kHeadDim, G, false, true, r, (int)nw_ref, s) != hipSuccess) return DWKV_E_HIP;
+  }
+  hipError_t e;
+  if (probe && !scores && fused_probe(d, probe)) {
+    e = launch_split_tl_probe(RB, G, max_level(d) > 0, c8, TLProbeArgs{a, r}, s);
+  } else {
+    e = c8 ? (scores ? launch_split_tl_scores_c8(RB, G, max_level(d) > 0, a, (int)nw, s)
+                     : launch_split_tl_c8(RB, G, max_level(d) > 0, a, (int)nw, s))
+           : uses_token_lane(d)
+               ? (scores ? launch_split_tl_scores(RB, G, max_level(d) > 0, a, (int)nw, s)
+                         : launch_split_tl(RB, G, max_level(d) > 0, a, (int)nw, s))
+               : launch_split(RB, G, max_level(d) > 0, false, a, (int)nw, s);
+    if (e == hipSuccess && probe) e = launch_split(kHeadDim, G, false, true, r, r.n_work, s);
+  }
+  if (e != hipSuccess) return DWKV_E_HIP;
+  if (probe) {
     r.zero = nullptr;
     r.n_zero = 0;
     // earlier positions: the query j steps back over the sequences cut j

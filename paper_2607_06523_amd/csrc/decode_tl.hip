@@ -40,6 +40,7 @@
 #include "compress_dev.h"
 #include "entry.h"
 #include "internal.h"
+#include "split_dev.h"
 
 namespace dwkv {
 namespace {
@@ -1126,19 +1127,17 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
 }
 
 template <int RB, int G, bool RESID, bool SCORES, bool C8>
-__device__ __forceinline__ void tl_body(const SplitArgs& a, TSmem<RB, G, RESID>& sm) {
+__device__ __forceinline__ void tl_body(const SplitArgs& a, TSmem<RB, G, RESID>& sm, int w, int slot) {
   using C = TCfg<RB>;
   constexpr int NS = C::NS;
   constexpr int HG = TGrp<G>::HG;
   static_assert(!C8 || HG == 4, "int8 coefficients: query groups of up to 4 heads");
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int grp = lane >> 4, col = lane & 15;
-  const int slot = blockIdx.y;
   const int kvh = a.kv_of_slot[slot];
   pin_split_args(a, kvh);
 
   // work item -> (sequence, chunk)
-  const int w = blockIdx.x;
   int b;
   TCtx x;
   {
@@ -1450,7 +1449,7 @@ __device__ __forceinline__ void tl_body(const SplitArgs& a, TSmem<RB, G, RESID>&
 template <int RB, int G, bool RESID, bool SCORES, bool C8>
 __global__ __launch_bounds__(kTThreads) void tl_kernel(const SplitArgs a) {
   __shared__ TSmem<RB, G, RESID> sm;
-  tl_body<RB, G, RESID, SCORES, C8>(a, sm);
+  tl_body<RB, G, RESID, SCORES, C8>(a, sm, blockIdx.x, blockIdx.y);
 }
 
 // LDS of the append item, in the decode workgroup's storage: both bases of
@@ -1571,7 +1570,61 @@ __global__ __launch_bounds__(kTThreads) void tl_append_kernel(const TLAppendArgs
     tl_append<RB, G>(A, lds, b, c1, blockIdx.y, blockIdx.x);
     return;
   }
-  tl_body<RB, G, RESID, false, false>(a, *reinterpret_cast<TSmem<RB, G, RESID>*>(lds));
+  tl_body<RB, G, RESID, false, false>(a, *reinterpret_cast<TSmem<RB, G, RESID>*>(lds), blockIdx.x, blockIdx.y);
+}
+
+// The split-K pass with a probe's reference pass in the same grid: workgroups
+// [0, n_work * n_slots) take the token-lane items in tl_kernel's order, the
+// rest one reference item each (the general kernel's identity-basis body on
+// this launch's kTW waves).  The dispatcher hands out workgroups in index
+// order, so the reference items start on the compute units as their split-K
+// items finish, with no second launch.
+template <int RB, int G, bool RESID, bool C8>
+__global__ __launch_bounds__(kTThreads) void tl_probe_kernel(const TLProbeArgs A) {
+  using RS = gsplit::Smem<D, G, false, kTW>;
+  constexpr size_t kT = sizeof(TSmem<RB, G, RESID>), kR = sizeof(RS);
+  __shared__ alignas(16) unsigned char lds[kT > kR ? kT : kR];
+  const int nt = A.s.n_work * A.s.n_slots;
+  const int i = blockIdx.x;
+  if (i < nt) {
+    tl_body<RB, G, RESID, false, C8>(A.s, *reinterpret_cast<TSmem<RB, G, RESID>*>(lds), i % A.s.n_work,
+                                     i / A.s.n_work);
+    return;
+  }
+  const int k = i - nt;
+  gsplit::split_body<D, G, false, true, kTW>(A.r, k % A.r.n_work, k / A.r.n_work, threadIdx.x,
+                                             *reinterpret_cast<RS*>(lds));
+}
+
+template <int RB, int G, bool R, bool C8>
+hipError_t launch_tlp_t(const TLProbeArgs& a, hipStream_t s) {
+  const int nt = a.s.n_work * a.s.n_slots, nr = a.r.n_work * a.r.n_slots;
+  hipLaunchKernelGGL((tl_probe_kernel<RB, G, R, C8>), dim3(nt + nr), dim3(kTThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int RB, bool R, bool C8>
+hipError_t launch_tlp_g(int g, const TLProbeArgs& a, hipStream_t s) {
+  switch (g) {
+    case 1: return launch_tlp_t<RB, 1, R, C8>(a, s);
+    case 2: return launch_tlp_t<RB, 2, R, C8>(a, s);
+    case 4: return launch_tlp_t<RB, 4, R, C8>(a, s);
+    case 8:
+      if constexpr (!C8) return launch_tlp_t<RB, 8, R, C8>(a, s);
+      break;
+  }
+  return hipErrorInvalidValue;
+}
+
+template <bool R, bool C8>
+hipError_t launch_tlp_rb(int rb, int g, const TLProbeArgs& a, hipStream_t s) {
+  switch (rb) {
+    case 16: return launch_tlp_g<16, R, C8>(g, a, s);
+    case 32: return launch_tlp_g<32, R, C8>(g, a, s);
+    case 48: return launch_tlp_g<48, R, C8>(g, a, s);
+    case 64: return launch_tlp_g<64, R, C8>(g, a, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 template <int RB, int G, bool R>
@@ -1674,6 +1727,11 @@ hipError_t launch_split_tl(int rb, int g, bool resid, const SplitArgs& a, int n_
 
 hipError_t launch_split_tl_append(int rb, int g, bool resid, const TLAppendArgs& a, int n_work, hipStream_t s) {
   return resid ? launch_tla_rb<true>(rb, g, a, n_work, s) : launch_tla_rb<false>(rb, g, a, n_work, s);
+}
+
+hipError_t launch_split_tl_probe(int rb, int g, bool resid, bool c8, const TLProbeArgs& a, hipStream_t s) {
+  if (c8) return resid ? launch_tlp_rb<true, true>(rb, g, a, s) : launch_tlp_rb<false, true>(rb, g, a, s);
+  return resid ? launch_tlp_rb<true, false>(rb, g, a, s) : launch_tlp_rb<false, false>(rb, g, a, s);
 }
 
 hipError_t launch_split_tl_scores(int rb, int g, bool resid, const SplitArgs& a, int n_work, hipStream_t s) {

@@ -332,6 +332,15 @@ struct TLAppendArgs {
 };
 hipError_t launch_split_tl_append(int rb, int g, bool resid, const TLAppendArgs& a, int n_work, hipStream_t s);
 
+// The token-lane split-K pass and a probe's reference pass (the general
+// kernel's identity-basis path over the dense rows, kHeadDim ranks) in one
+// launch: s as for launch_split_tl, r as for the reference launch_split call.
+struct TLProbeArgs {
+  SplitArgs s;
+  SplitArgs r;
+};
+hipError_t launch_split_tl_probe(int rb, int g, bool resid, bool c8, const TLProbeArgs& a, hipStream_t s);
+
 // Materialization of one layer's rebuilt keys and values (Eq. 1) as fp16.
 struct MatArgs {
   const uint16_t* basis;       // window m, sequence 0; sequence b adds b*basis_b_stride, (h, z) add (h*2+z)*rb*d

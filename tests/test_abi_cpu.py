@@ -205,8 +205,9 @@ def test_route_and_map_argument_checks(lib):
 
 
 def test_decode_launch_count(lib):
-    """The split-K pass and the merge; a probe adds its reference pass (the
-    merge evaluates Eq. 3 on either kernel)."""
+    """The split-K pass and the merge; a probe adds its reference pass, inside
+    the split-K launch on the token-lane kernel and as a launch of its own on
+    the general kernel (the merge evaluates Eq. 3 on either)."""
     from paper_2607_06523_amd import binding
     for kw in (dict(), dict(n_q_heads=16), dict(batch=3, cu_seqlens_host=[0, 700, 700, 1300], total_tokens=1300)):
         d, keep = dims(**kw)
@@ -214,7 +215,7 @@ def test_decode_launch_count(lib):
     heads = np.array([1], dtype=np.int32)
     p = binding.Probe(1, heads.ctypes.data_as(C.POINTER(C.c_int32)), FAKE, FAKE, 1e-6, FAKE, 0)
     d, keep = dims()                                  # G = 4, r_b 32: token-lane kernel
-    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 2
     d, keep = dims(n_q_heads=32)                      # G = 16: general kernel
     assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3
     d, keep = dims(n_q_heads=7)
@@ -224,11 +225,11 @@ def test_decode_launch_count(lib):
     # chunks: positions 1 and 2 see tokens (of the first sequences), 3 only of the first
     d, keep = dims(batch=3, cu_seqlens_host=[0, 700, 700, 702], total_tokens=702, split_tokens=256)
     p.n_pos, p.q_prev = 4, FAKE
-    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3 + 2 * 3 + 1
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 2 + 2 * 3 + 1
     d, keep = dims(batch=2, cu_seqlens_host=[0, 2, 3], total_tokens=3, split_tokens=256)
-    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3 + 2 * 1 + 1
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 2 + 2 * 1 + 1
     p.n_pos = 1
-    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 2
 
 
 def test_route_range_and_compress_argument_checks(lib):
