@@ -859,14 +859,14 @@ __device__ __forceinline__ void tstep(TState<RB, G, C8>& st, TFrags<RB, C8>& fr,
 
 constexpr int kSc1 = 16;                // buffer cache policy: device-coherent access
 
-// Wide merge: one workgroup per (slot, head, 16 output channels).  Each
-// reads, from every partial of its (sequence, slot, head), its 16 residual
+// Wide merge: one workgroup per (slot, head, CH output channels).  Each
+// reads, from every partial of its (sequence, slot, head), its CH residual
 // channels and all of a~ (plus m, l), merges them in a fixed order and writes
 // o = r + a~ B^V for its channels.  Spreading one slot's merge over G * d/16
 // workgroups keeps every CU's share of the partials small: the loads of one
 // CU, not the bytes, bound a merge that a single workgroup does.
 constexpr int kWmThreads = 256;
-constexpr int kWmCh = 16;                       // output channels per workgroup
+constexpr int kWmCh = 16;                       // output channels per workgroup with a probe
 
 constexpr int kPrG = kWmThreads / (kWmCh / 4);  // reference row groups of a probe chunk (64)
 constexpr int kPrRPT = 4;                         // reference partials per thread per round
@@ -1700,15 +1700,18 @@ hipError_t launch_merge_tl_ch(int g, const WMergeArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// 64-channel workgroups when every sequence has at most kWideFew partials and
-// nothing is probed: the merge is then a few loads per workgroup, and four
-// times fewer workgroups start sooner.
+// Channels per merge workgroup: 16 with a probe (Eq. 3's chunk counters);
+// otherwise 64 when every sequence has at most kWideFew partials (a few loads
+// per workgroup, and four times fewer workgroups start sooner), else 32 (at
+// 32 partials per sequence, 4.0 us per launch against 4.2 with 16 channels
+// and 4.1 with 64).
 constexpr int kWideFew = 4;
 
 template <int RB>
 hipError_t launch_merge_tl_rb(int g, const WMergeArgs& a, hipStream_t s) {
-  if (a.p.n_probe == 0 && a.max_ns <= kWideFew) return launch_merge_tl_ch<RB, 64>(g, a, s);
-  return launch_merge_tl_ch<RB, kWmCh>(g, a, s);
+  if (a.p.n_probe > 0) return launch_merge_tl_ch<RB, kWmCh>(g, a, s);
+  if (a.max_ns <= kWideFew) return launch_merge_tl_ch<RB, 64>(g, a, s);
+  return launch_merge_tl_ch<RB, 32>(g, a, s);
 }
 
 bool token_lane_supported(int rb, int g, int max_level, int64_t tokens, int64_t res_stride) {
