@@ -392,7 +392,9 @@ __device__ __forceinline__ void value_resid_tokens_global(WaveSmem<RB, G, true>&
   }
 }
 
-template <int RB, int G, bool RESID, bool TILED, int NW>
+// One tile of the wave; LAST: the wave's last tile, which requests nothing
+// for later tiles (a request there would hold the epilogue until it lands).
+template <int RB, int G, bool RESID, bool TILED, int NW, bool LAST>
 __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Meta& mn, Meta& mnn,
                                      Ent& ec, Ent& en, int j, const Ctx& x, Smem<RB, G, RESID, NW>& sm,
                                      WaveSmem<RB, G, RESID>& ws, int lane) {
@@ -401,10 +403,9 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
   const int grp = lane >> 4, col = lane & 15;
   const int64_t t0 = tile_start<RB>(x, j);
   const int jn = j + NW, jnn = j + 2 * NW;
-  const bool has_next = jn < x.ntile;
-  // past the wave's last tile the prefetches re-read a tile of this chunk
-  // (cache resident, results unused) so the load sequence stays the same
-  const int jn_l = has_next ? jn : j;
+  // two tiles ahead of the wave's second-to-last tile the offset prefetch
+  // re-reads a tile of this chunk (cache resident, results unused)
+  const int jn_l = jn < x.ntile ? jn : j;
   const int jnn_l = jnn < x.ntile ? jnn : jn_l;
 
   // 1. stage this tile's residual entries; request the next tiles' metadata
@@ -421,9 +422,11 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
     reinterpret_cast<uint32_t*>(ws.eidx[1])[lane + 64] = ec.iv[1];
     reinterpret_cast<uint32_t*>(ws.eval[0])[lane] = ec.vk;
     reinterpret_cast<uint32_t*>(ws.eval[1])[lane] = ec.vv;
-    load_offsets<RB>(mnn, x, jnn_l, lane);
-    load_entries<TT>(en, x, mn, lane);
-    load_scales<RB>(mn, x, jn_l, lane);
+    if constexpr (!LAST) {
+      load_offsets<RB>(mnn, x, jnn_l, lane);
+      load_entries<TT>(en, x, mn, lane);
+      load_scales<RB>(mn, x, jn_l, lane);
+    }
     wave_lds_fence();
   }
 
@@ -439,7 +442,7 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
       sacc[bk] = mfma16(av, st.qlo[s], sacc[bk]);
     }
   }
-  load_k<RB, TILED>(fr, x, jn_l, lane);
+  if constexpr (!LAST) load_k<RB, TILED>(fr, x, jn_l, lane);
 
   // 3. key residual entries add q[c]*code*scale to their token's score
   if constexpr (RESID) {
@@ -529,7 +532,7 @@ __device__ __forceinline__ void step(State<RB>& st, Frags<RB>& fr, Meta& mc, Met
       st.acc[cb] = mfma16(pl, vf, st.acc[cb]);
     }
   }
-  load_v<RB, TILED>(fr, x, jn_l, lane);
+  if constexpr (!LAST) load_v<RB, TILED>(fr, x, jn_l, lane);
 
   // 9. value residual entries scatter p*code*scale into their channel
   if constexpr (RESID) {
@@ -735,7 +738,9 @@ __device__ __forceinline__ void split_body(const SplitArgs& a, int w, int slot, 
   __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 
   // stream the wave's tiles
-  for (int j = wv; j < x.ntile; j += NW) step<RB, G, RESID, !IDENT, NW>(st, fr, mc, mn, mnn, ec, en, j, x, sm, ws, lane);
+  int j = wv;
+  for (; j + NW < x.ntile; j += NW) step<RB, G, RESID, !IDENT, NW, false>(st, fr, mc, mn, mnn, ec, en, j, x, sm, ws, lane);
+  if (j < x.ntile) step<RB, G, RESID, !IDENT, NW, true>(st, fr, mc, mn, mnn, ec, en, j, x, sm, ws, lane);
   if constexpr (RESID) {
     if (lane == 0) ws.ex = st.ex;      // read by every thread after the epilogue's barrier
   }
