@@ -55,6 +55,9 @@ PROBE_CASES = [
     # channel chunk; the last chunk of a column adds the chunks' sums
     ("tl-g4", 4, 48, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), None, 512),
     ("tl-g8-empty-seq", 8, 64, (0, 4, 8, 16, 32), (0.7, 0.12, 0.1, 0.06, 0.02), [0, 2100, 1700], 256),
+    # groups of 1 and 2: the reference pass inside the split-K launch at those widths
+    ("tl-g1", 1, 32, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), None, 256),
+    ("tl-g2-tiny-seqs", 2, 16, (0, 8, 16), (0.8, 0.15, 0.05), [5, 1, 2300], 512),
 ]
 
 
