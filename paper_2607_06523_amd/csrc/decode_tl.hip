@@ -866,18 +866,20 @@ constexpr int kSc1 = 16;                // buffer cache policy: device-coherent 
 // workgroups keeps every CU's share of the partials small: the loads of one
 // CU, not the bytes, bound a merge that a single workgroup does.
 constexpr int kWmThreads = 256;
-constexpr int kWmCh = 16;                       // output channels per workgroup with a probe
+constexpr int kWmCh = 16;                       // channels of a probe reference chunk
 
 constexpr int kPrG = kWmThreads / (kWmCh / 4);  // reference row groups of a probe chunk (64)
 constexpr int kPrRPT = 4;                         // reference partials per thread per round
 constexpr int kWmNCH = D / kWmCh;                 // output-channel chunks of a row
 
 // Eq. 3 for a probed column (b, probed slot, group member) in the wide merge:
-// its 8 output chunks (the merge's own workgroups) and its 8 reference chunks
-// (extra workgroups) each publish their 16 channels and count themselves in;
-// the 16th to arrive reads both rows and writes err (or, with several
-// positions, the sums to acc), then resets the counter.  Nothing waits.
-__device__ __forceinline__ void wm_probe_arrive(const WideProbe& P, int64_t col, int64_t orow, const float* out) {
+// its d/CH output chunks (the merge's own workgroups) and its 8 reference
+// chunks of 16 channels (extra workgroups) each publish their channels and
+// count themselves in; the last of the n_arrive to arrive reads both rows and
+// writes err (or, with several positions, the sums to acc), then resets the
+// counter.  Nothing waits.
+__device__ __forceinline__ void wm_probe_arrive(const WideProbe& P, int64_t col, int64_t orow, const float* out,
+                                                uint32_t n_arrive) {
   __shared__ uint32_t arrived;
   // the chunk's rows went out as device-coherent (agent-scope atomic) stores;
   // each wave waits for its own to complete before the count, so a reader
@@ -886,7 +888,7 @@ __device__ __forceinline__ void wm_probe_arrive(const WideProbe& P, int64_t col,
   __syncthreads();
   if (threadIdx.x == 0) arrived = atomicAdd(&P.count[col], 1u);
   __syncthreads();
-  if (arrived != 2u * kWmNCH - 1u) return;
+  if (arrived != n_arrive - 1u) return;
   if (threadIdx.x >= 64) return;
   const int lane = threadIdx.x;
   float d2 = 0.f, r2 = 0.f;
@@ -916,7 +918,7 @@ __device__ __forceinline__ void wm_probe_arrive(const WideProbe& P, int64_t col,
 // fixed order (64 row groups of 4 quads, each taking every 64th partial; then
 // a butterfly over the wave's row groups and the 4 waves through LDS).
 template <int G>
-__device__ __forceinline__ void wm_probe_ref(const WMergeArgs& A, int idx, int b) {
+__device__ __forceinline__ void wm_probe_ref(const WMergeArgs& A, int idx, int b, uint32_t n_arrive) {
   __shared__ f4 wr[kWmThreads / 64][kWmCh / 4];
   __shared__ float wmx[kWmThreads / 64][kWmCh / 4], wlx[kWmThreads / 64][kWmCh / 4];
   const SplitArgs& a = A.s;
@@ -997,7 +999,7 @@ __device__ __forceinline__ void wm_probe_ref(const WMergeArgs& A, int idx, int b
     if (P.out_ref) *reinterpret_cast<f4*>(P.out_ref + col * D + c0 + 4 * tid) = r;
   }
   const int64_t orow = ((int64_t)b * a.n_q_heads + P.kv_of_slot[sl] * G + g) * D;
-  wm_probe_arrive(P, col, orow, a.out);
+  wm_probe_arrive(P, col, orow, a.out, n_arrive);
 }
 
 // CH output channels per workgroup: 16 (and Eq. 3 for probed heads), or 64
@@ -1016,11 +1018,9 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
   __shared__ alignas(16) float fin[4 * QW];
   __shared__ float red2[KG][CH];
   const int tid = threadIdx.x;
-  if constexpr (CH == kWmCh) {
-    if ((int)blockIdx.x >= a.n_slots * G * NCH) {   // a probed column's reference chunk
-      wm_probe_ref<G>(A, blockIdx.x - a.n_slots * G * NCH, blockIdx.y);
-      return;
-    }
+  if ((int)blockIdx.x >= a.n_slots * G * NCH) {     // a probed column's reference chunk
+    wm_probe_ref<G>(A, blockIdx.x - a.n_slots * G * NCH, blockIdx.y, NCH + kWmNCH);
+    return;
   }
   const int ch = blockIdx.x % NCH, g = (blockIdx.x / NCH) % G, slot = blockIdx.x / (NCH * G), b = blockIdx.y;
   const int c0 = ch * CH;
@@ -1110,7 +1110,7 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
     red2[kg][pc] = o;
   }
   __syncthreads();
-  const int sl = CH == kWmCh && A.p.n_probe > 0 ? A.p.slot_of_kv[kvh] : -1;
+  const int sl = A.p.n_probe > 0 ? A.p.slot_of_kv[kvh] : -1;
   const int64_t orow = ((int64_t)b * a.n_q_heads + kvh * G + g) * D;
   if (tid < CH) {
     float o = fin[tid];
@@ -1121,9 +1121,7 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
     else
       a.out[orow + c0 + tid] = o;
   }
-  if constexpr (CH == kWmCh) {
-    if (sl >= 0) wm_probe_arrive(A.p, (int64_t)b * A.p.n_probe * G + sl * G + g, orow, a.out);
-  }
+  if (sl >= 0) wm_probe_arrive(A.p, (int64_t)b * A.p.n_probe * G + sl * G + g, orow, a.out, NCH + kWmNCH);
 }
 
 template <int RB, int G, bool RESID, bool SCORES, bool C8>
@@ -1689,7 +1687,7 @@ hipError_t launch_tl_rb(int rb, int g, const SplitArgs& a, int n_work, hipStream
 
 template <int RB, int CH>
 hipError_t launch_merge_tl_ch(int g, const WMergeArgs& a, hipStream_t s) {
-  const dim3 grid((a.s.n_slots + (CH == kWmCh ? a.p.n_probe : 0)) * g * (D / CH), a.s.batch);
+  const dim3 grid((a.s.n_slots * (D / CH) + a.p.n_probe * kWmNCH) * g, a.s.batch);
   switch (g) {
     case 1: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 1, CH>), grid, dim3(kWmThreads), 0, s, a); break;
     case 2: hipLaunchKernelGGL((tl_wmerge_kernel<RB, 2, CH>), grid, dim3(kWmThreads), 0, s, a); break;
@@ -1700,16 +1698,15 @@ hipError_t launch_merge_tl_ch(int g, const WMergeArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Channels per merge workgroup: 16 with a probe (Eq. 3's chunk counters);
-// otherwise 64 when every sequence has at most kWideFew partials (a few loads
-// per workgroup, and four times fewer workgroups start sooner), else 32 (at
-// 32 partials per sequence, 4.0 us per launch against 4.2 with 16 channels
-// and 4.1 with 64).
+// Channels per merge workgroup: 64 when every sequence has at most kWideFew
+// partials (a few loads per workgroup, and four times fewer workgroups start
+// sooner), else 32 (at 32 partials per sequence, 4.0 us per launch against
+// 4.2 with 16 channels and 4.1 with 64).  A probe's reference chunks keep 16
+// channels.
 constexpr int kWideFew = 4;
 
 template <int RB>
 hipError_t launch_merge_tl_rb(int g, const WMergeArgs& a, hipStream_t s) {
-  if (a.p.n_probe > 0) return launch_merge_tl_ch<RB, kWmCh>(g, a, s);
   if (a.max_ns <= kWideFew) return launch_merge_tl_ch<RB, 64>(g, a, s);
   return launch_merge_tl_ch<RB, 32>(g, a, s);
 }
