@@ -1009,7 +1009,10 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
   const SplitArgs& a = A.s;
   constexpr int QW = CH / 4 + RB / 4;        // quads per row: the r chunk, then a~
   constexpr int RG = kWmThreads / QW;           // row groups
-  constexpr int RPT = 2;                        // partials per thread per round (32 per round at r_b 48)
+  // partials per thread per round: at 32 channels one round covers 32
+  // partials (a 64K sequence's chunks) at every r_b (4.0 us per launch
+  // against 4.3 in two rounds); 64-channel columns merge at most kWideFew
+  constexpr int RPT = CH >= 64 ? 2 : ((32 + RG - 1) / RG > 2 ? (32 + RG - 1) / RG : 2);
   constexpr int KG = kWmThreads / CH;        // k groups of the projection
   constexpr int KPG = (RB + KG - 1) / KG;       // basis rows per k group
   constexpr int NCH = D / CH;
