@@ -12,8 +12,9 @@
 // routed residual entries touch only the score of their token (keys) or one
 // channel of a d-vector accumulator (values).
 //
-// Mapping (one workgroup = 4 waves = one chunk of `split` tokens of one
-// sequence and one KV head; each wave streams every 4th tile of 16*NBK tokens):
+// Mapping (one workgroup = NW waves, 4 in the general launch, = one chunk of
+// `split` tokens of one sequence and one KV head; each wave streams every
+// NW-th tile of 16*NBK tokens):
 //  * scores S[tok][g] = A^K[tok][:] . q~[:][g] on v_mfma_f32_16x16x16_f16: key
 //    coefficients are the A operand, loaded straight into registers (lane =
 //    token % 16, 4 consecutive coefficients by lane / 16: one 8-byte load from
@@ -29,7 +30,7 @@
 //  * fragments are single-buffered with early release: the next tile's key
 //    fragments are requested right after this tile's score MFMAs, its value
 //    fragments right after the value MFMAs; offsets run two tiles ahead and
-//    residual entries one tile ahead.
+//    residual entries one tile ahead; a wave's last tile requests nothing.
 //  * online softmax in exp2 units; running max via lane shuffles.
 //  * residual entries: one lane per entry; token of an entry from an LDS map
 //    written by the token lanes; key entries add into an LDS score buffer,
