@@ -466,6 +466,8 @@ def main():
     ap.add_argument("--variant", default="full", choices=["full", "bases-only"],
                     help="bases-only: every routed residual rank 0 (shared bases only)")
     ap.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
+    ap.add_argument("--coef", default="fp16", choices=["fp16", "int8"],
+                    help="coefficient format of the timed workload (int8: the 8-bit blockwise form)")
     ap.add_argument("--probe-heads", type=int, default=-1,
                     help="KV heads probed (Eq. 3) in every layer of the timed step, each layer with its own "
                          "fp16 reference; -1 = the workload's setting (one head when it probes every layer)")
@@ -502,6 +504,8 @@ def main():
         wl = wl.with_(context=args.context, name=f"{wl.name.rsplit('-', 1)[0]}-{args.context // 1024}k")
     if args.variant == "bases-only":
         wl = wl.with_(levels=(0,), probs=(1.0,), salient_frac=0.0, name=wl.name + "-bases-only")
+    if args.coef == "int8":
+        wl = wl.with_(coef_format="int8", name=wl.name + "-int8")
     log(f"[bench] generating {wl.name} ({wl.description})")
     t = time.time()
     host = generate(wl)
