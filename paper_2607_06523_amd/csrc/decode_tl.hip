@@ -999,7 +999,7 @@ __device__ __forceinline__ void wm_probe_ref(const WMergeArgs& A, int idx, int b
     if (P.out_ref) *reinterpret_cast<f4*>(P.out_ref + col * D + c0 + 4 * tid) = r;
   }
   const int64_t orow = ((int64_t)b * a.n_q_heads + P.kv_of_slot[sl] * G + g) * D;
-  wm_probe_arrive(P, col, orow, a.out, n_arrive);
+  if (ns_r > 0) wm_probe_arrive(P, col, orow, a.out, n_arrive);   // an empty sequence: see wm_body
 }
 
 // CH output channels per workgroup: 16 (and Eq. 3 for probed heads), or 64
@@ -1124,7 +1124,19 @@ __global__ __launch_bounds__(kWmThreads) void tl_wmerge_kernel(const WMergeArgs 
     else
       a.out[orow + c0 + tid] = o;
   }
-  if (sl >= 0) wm_probe_arrive(A.p, (int64_t)b * A.p.n_probe * G + sl * G + g, orow, a.out, NCH + kWmNCH);
+  if (sl >= 0) {
+    const int64_t col = (int64_t)b * A.p.n_probe * G + sl * G + g;
+    if (ns > 0) {
+      wm_probe_arrive(A.p, col, orow, a.out, NCH + kWmNCH);
+    } else if (ch == 0 && tid == 0) {   // an empty sequence: e = 0 with no count (its counter may be stale)
+      if (A.p.acc) {
+        A.p.acc[2 * col] = 0.f;
+        A.p.acc[2 * col + 1] = 0.f;
+      } else {
+        A.p.err[col] = 0.f;
+      }
+    }
+  }
 }
 
 template <int RB, int G, bool RESID, bool SCORES, bool C8>

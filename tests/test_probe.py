@@ -220,3 +220,36 @@ def test_probe_two_phase_matches_one_phase(positions):
     torch.cuda.synchronize()
     assert np.array_equal(out1.cpu().numpy(), out2.cpu().numpy())
     assert np.array_equal(err1.cpu().numpy(), err2.cpu().numpy())
+
+
+def test_probe_with_uninitialised_workspace():
+    """The decode needs no initial workspace contents: a workspace whose bytes
+    are all 0xFF (stale counters and partials) gives the clean workspace's
+    outputs and probe errors bit for bit, on the token-lane path (the wide
+    merge's counters) and the general one, with an empty sequence in the batch
+    (its columns take e = 0 without counting in)."""
+    torch = torch_gpu()
+    from paper_2607_06523_amd import ProbeRef
+    from synth.layout import block_values
+    for G, rb in ((4, 32), (16, 32)):
+        w = _Fixed(Workload(name=f"probe-stale-g{G}", batch=3, n_layers=2, window=2, n_kv_heads=2, n_q_heads=2 * G,
+                            head_dim=128, context=1300, basis_rank=rb, levels=(0, 8), probs=(0.7, 0.3),
+                            q_dtype="bf16", seed=19), [700, 0, 1300])
+        host = generate(w, threads=4)
+        dc = device_cache(host, split_tokens=256)
+        heads = [1]
+        K, V = _refs(host, 1, heads, 0.05, seed=5)
+        pr = ProbeRef(heads, torch.from_numpy(K.view(np.uint16)).view(torch.float16).cuda(),
+                      torch.from_numpy(block_values(V).view(np.uint16)).view(torch.float16).cuda())
+        res = []
+        for fill in (0, 0xFF, 0xFF):
+            ws = dc.new_workspace(pr)
+            ws.fill_(fill)
+            announce(f"probe G {G} workspace filled with {fill:#x}")
+            out, err, _ = dc.decode(1, probe=pr, workspace=ws)
+            res.append((out.cpu().numpy(), err.cpu().numpy()))
+        for out, err in res[1:]:
+            assert np.array_equal(out, res[0][0]) and np.array_equal(err, res[0][1])
+        assert np.all(res[0][1][1] == 0.0), "an empty sequence's probe error is 0"
+        e_ref = oracle.probe(host, 1, heads, K, V)
+        assert np.abs(res[0][1] - e_ref).max() <= 1e-4 + 1e-3 * np.abs(e_ref).max()
