@@ -167,9 +167,9 @@ size_t dwkv_workspace_bytes(const dwkv_dims* dims, const dwkv_probe* probe);
  * the reference pass is added -- inside the split-K launch on the token-lane
  * kernel (still 2), as a launch of its own on the general kernel (3) -- and a
  * probe over n_pos > 1 positions adds
- * two split passes -- factorized and reference, on the probed heads -- for
- * every earlier position that still sees a token of some sequence, and one
- * merge), or -1 when the dims or probe are invalid.  probe may be NULL. */
+ * one launch -- the factorized and the reference pass on the probed heads --
+ * for every earlier position that still sees a token of some sequence, and
+ * one merge), or -1 when the dims or probe are invalid.  probe may be NULL. */
 int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe);
 
 /* Per-layer decode attention over the factorized cache (Eq. 1 folded into the

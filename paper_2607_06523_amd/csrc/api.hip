@@ -255,7 +255,7 @@ int32_t dwkv_decode_launches(const dwkv_dims* dims, const dwkv_probe* probe) {
   int32_t n = fused_probe(dims, probe) ? 2 : 3;
   const int np = probe_positions(probe), split = plan_split_ref(dims, probe->n_heads);
   for (int j = 1; j < np; ++j)
-    if (count_work(dims, split, j) > 0) n += 2;
+    if (count_work(dims, split, j) > 0) n += 1;
   return np > 1 ? n + 1 : n;
 }
 
@@ -397,7 +397,7 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
     r.n_zero = 0;
     // earlier positions: the query j steps back over the sequences cut j
     // tokens short, on the factorized cache (general kernel, probed heads
-    // only) and on the reference
+    // only) and on the reference, both passes in one launch
     for (int j = 1; j < probe_positions(probe); ++j) {
       const int64_t nwj = count_work(d, r.split, j);
       if (nwj == 0) continue;
@@ -411,14 +411,13 @@ dwkv_status partials_phase(const dwkv_dims* d, const dwkv_cache* c, int32_t laye
       f.wt = work_table(d, r.split, j);
       f.trim = j;
       f.part = reinterpret_cast<float*>(pos);
-      if (launch_split(RB, G, max_level(d) > 0, false, f, (int)nwj, s) != hipSuccess) return DWKV_E_HIP;
       SplitArgs fr = r;
       fr.q = f.q;
       fr.n_work = f.n_work;
       fr.wt = f.wt;
       fr.trim = j;
       fr.part = reinterpret_cast<float*>(pos + wl.pos_bytes);
-      if (launch_split(kHeadDim, G, false, true, fr, (int)nwj, s) != hipSuccess) return DWKV_E_HIP;
+      if (launch_probe_pos(RB, G, max_level(d) > 0, TLProbeArgs{f, fr}, s) != hipSuccess) return DWKV_E_HIP;
     }
   }
   return DWKV_OK;

@@ -13,6 +13,24 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const SplitArgs a) {
   split_body<RB, G, RESID, IDENT>(a, blockIdx.x, blockIdx.y, threadIdx.x, sm);
 }
 
+// An earlier probe position's two passes in one launch: workgroups
+// [0, n_work * n_slots) of A.s run the factorized pass over the probed heads
+// (in split_kernel's order), the rest the reference pass A.r (identity basis).
+template <int RB, int G, bool RESID>
+__global__ __launch_bounds__(kThreads) void pos_pair_kernel(const TLProbeArgs A) {
+  using FS = Smem<RB, G, RESID>;
+  using RS = Smem<D, G, false>;
+  __shared__ alignas(16) unsigned char lds[sizeof(FS) > sizeof(RS) ? sizeof(FS) : sizeof(RS)];
+  const int nf = A.s.n_work * A.s.n_slots;
+  const int i = blockIdx.x;
+  if (i < nf) {
+    split_body<RB, G, RESID, false>(A.s, i % A.s.n_work, i / A.s.n_work, threadIdx.x, *reinterpret_cast<FS*>(lds));
+    return;
+  }
+  const int k = i - nf;
+  split_body<D, G, false, true>(A.r, k % A.r.n_work, k / A.r.n_work, threadIdx.x, *reinterpret_cast<RS*>(lds));
+}
+
 // One workgroup per (query head, sequence) merges that head's split partials
 // in a fixed order: every partial's (m, l) and output slice are requested in
 // one round of loads.  For a probed KV head it also merges the reference
@@ -304,7 +322,45 @@ hipError_t launch_rb(int rb, int g, const SplitArgs& a, int n_work, hipStream_t 
   return hipErrorInvalidValue;
 }
 
+template <int RB, int G, bool R>
+hipError_t launch_pp_t(const TLProbeArgs& a, hipStream_t s) {
+  const int n = a.s.n_work * a.s.n_slots + a.r.n_work * a.r.n_slots;
+  hipLaunchKernelGGL((pos_pair_kernel<RB, G, R>), dim3(n), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int RB, bool R>
+hipError_t launch_pp_g(int g, const TLProbeArgs& a, hipStream_t s) {
+  switch (g) {
+    case 1: return launch_pp_t<RB, 1, R>(a, s);
+    case 2: return launch_pp_t<RB, 2, R>(a, s);
+    case 4: return launch_pp_t<RB, 4, R>(a, s);
+    case 8: return launch_pp_t<RB, 8, R>(a, s);
+    case 16: return launch_pp_t<RB, 16, R>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <bool R>
+hipError_t launch_pp_rb(int rb, int g, const TLProbeArgs& a, hipStream_t s) {
+  switch (rb) {
+    case 16: return launch_pp_g<16, R>(g, a, s);
+    case 32: return launch_pp_g<32, R>(g, a, s);
+    case 48: return launch_pp_g<48, R>(g, a, s);
+    case 64: return launch_pp_g<64, R>(g, a, s);
+    case 80: return launch_pp_g<80, R>(g, a, s);
+    case 96: return launch_pp_g<96, R>(g, a, s);
+    case 112: return launch_pp_g<112, R>(g, a, s);
+    case 128: return launch_pp_g<128, R>(g, a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
 }  // namespace
+
+hipError_t launch_probe_pos(int rb, int g, bool resid, const TLProbeArgs& a, hipStream_t s) {
+  return resid ? launch_pp_rb<true>(rb, g, a, s) : launch_pp_rb<false>(rb, g, a, s);
+}
 
 hipError_t launch_split(int rb, int g, bool resid, bool ident, const SplitArgs& a, int n_work,
                         hipStream_t s) {

@@ -340,6 +340,9 @@ struct TLProbeArgs {
   SplitArgs r;
 };
 hipError_t launch_split_tl_probe(int rb, int g, bool resid, bool c8, const TLProbeArgs& a, hipStream_t s);
+// An earlier probe position: the general kernel's factorized pass over the
+// probed heads (s, r_b rb) and its reference pass (r) in one launch.
+hipError_t launch_probe_pos(int rb, int g, bool resid, const TLProbeArgs& a, hipStream_t s);
 
 // Materialization of one layer's rebuilt keys and values (Eq. 1) as fp16.
 struct MatArgs {

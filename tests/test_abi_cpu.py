@@ -220,14 +220,14 @@ def test_decode_launch_count(lib):
     assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 3
     d, keep = dims(n_q_heads=7)
     assert lib.dwkv_decode_launches(C.byref(d), None) == -1
-    # several positions: two passes per earlier position that still sees a
+    # several positions: one launch per earlier position that still sees a
     # token, then one merge; lengths 700, 0 and 2 with 4 positions and 256-token
     # chunks: positions 1 and 2 see tokens (of the first sequences), 3 only of the first
     d, keep = dims(batch=3, cu_seqlens_host=[0, 700, 700, 702], total_tokens=702, split_tokens=256)
     p.n_pos, p.q_prev = 4, FAKE
-    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 2 + 2 * 3 + 1
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 2 + 3 + 1
     d, keep = dims(batch=2, cu_seqlens_host=[0, 2, 3], total_tokens=3, split_tokens=256)
-    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 2 + 2 * 1 + 1
+    assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 2 + 1 + 1
     p.n_pos = 1
     assert lib.dwkv_decode_launches(C.byref(d), C.byref(p)) == 2
 
