@@ -90,17 +90,18 @@ def test_int8_full_size_sampled():
         compare(out, oracle.decode(host, layer, heads=pairs), pairs, G, f"int8 64k layer {layer}")
 
 
-def test_int8_with_probe():
-    """Eq. 3 on an int8 cache (the current position): the int8 token-lane pass,
-    the dense reference pass and Eq. 3 in the wide merge, against the oracle;
-    a probe over several positions is refused (its earlier positions run the
-    general kernel, which reads fp16 coefficients)."""
+@pytest.mark.parametrize("G,rb", [(4, 48), (1, 16), (2, 64)])
+def test_int8_with_probe(G, rb):
+    """Eq. 3 on an int8 cache (the current position): the int8 token-lane pass
+    and the dense reference pass in one launch, Eq. 3 in the wide merge,
+    against the oracle; a probe over several positions is refused (its earlier
+    positions run the general kernel, which reads fp16 coefficients)."""
     torch = torch_gpu()
     from paper_2607_06523_amd import DwkvError, ProbeRef
     from synth.layout import block_values
-    w = _Fixed(Workload(name="i8-probe", batch=3, n_layers=2, window=2, n_kv_heads=4, n_q_heads=16, head_dim=128,
-                        context=1500, basis_rank=48, levels=(0, 4, 8, 16), probs=(0.7, 0.1, 0.1, 0.1),
-                        q_dtype="bf16", seed=77, coef_format="int8"), [1500, 0, 700])
+    w = _Fixed(Workload(name=f"i8-probe-g{G}-rb{rb}", batch=3, n_layers=2, window=2, n_kv_heads=4, n_q_heads=4 * G,
+                        head_dim=128, context=1500, basis_rank=rb, levels=(0, 4, 8, 16), probs=(0.7, 0.1, 0.1, 0.1),
+                        q_dtype="bf16", seed=77 + G, coef_format="int8"), [1500, 0, 700])
     host = generate(w, threads=4)
     dc = device_cache(host, split_tokens=256)
     heads, layer = [2, 0], 1
@@ -113,13 +114,13 @@ def test_int8_with_probe():
     V = (V + rng.normal(0, 0.05, V.shape)).astype(np.float16)
     pr = ProbeRef(heads, torch.from_numpy(K.view(np.uint16)).view(torch.float16).cuda(),
                   torch.from_numpy(block_values(V).view(np.uint16)).view(torch.float16).cuda(), 1e-6)
-    announce("int8 decode with a probe")
+    announce(f"int8 decode with a probe, G {G}, r_b {rb}")
     out, err, _ = dc.decode(layer, probe=pr)
     err = err.cpu().numpy()
     e_ref = oracle.probe(host, layer, heads, K, V)
     assert np.abs(err - e_ref).max() <= 1e-4 + 1e-3 * np.abs(e_ref).max(), (err, e_ref)
     assert np.all(err[1] == 0)
-    compare(out.cpu().numpy(), oracle.decode(host, layer), [(b, h) for b in range(3) for h in range(4)], 4,
+    compare(out.cpu().numpy(), oracle.decode(host, layer), [(b, h) for b in range(3) for h in range(4)], G,
             "int8 with probe")
     q_prev = torch.zeros((1, host.batch, host.n_q_heads, 128), dtype=torch.bfloat16, device="cuda")
     with pytest.raises(DwkvError) as e:
