@@ -58,6 +58,10 @@ PROBE_CASES = [
     # groups of 1 and 2: the reference pass inside the split-K launch at those widths
     ("tl-g1", 1, 32, (0, 4, 8, 16), (0.75, 0.12, 0.08, 0.05), None, 256),
     ("tl-g2-tiny-seqs", 2, 16, (0, 8, 16), (0.8, 0.15, 0.05), [5, 1, 2300], 512),
+    ("tl-g8-rb32", 8, 32, (0, 8, 32), (0.8, 0.15, 0.05), None, 256),
+    # bases only (every rank 0): the kernels without the residual path
+    ("tl-g4-bases-only", 4, 48, (0,), (1.0,), None, 512),
+    ("general-g16-bases-only", 16, 32, (0,), (1.0,), None, 512),
 ]
 
 
